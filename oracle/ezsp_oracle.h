@@ -1,0 +1,161 @@
+/*
+ * ezsp_oracle.h -- plain sequential CPU oracle for the EZ-SP partition step.
+ *
+ * TEST INFRASTRUCTURE ONLY.  This library exists to check the GPU path; it is
+ * never called by the product library.  Only the test-suite, the smoke check
+ * and the CPU-baseline leg of the benchmark may load it.  It shares no code,
+ * header, table or helper with the HIP path.
+ *
+ * What it computes (arXiv 2512.00385):
+ *   - the undirected k-nearest-neighbour adjacency, weights w = 1
+ *     (Sec. 3.1 "Semantic Transition Prediction", Sec. 4.1 "Implementation
+ *     Details");
+ *   - the contour-regularised energy  Omega = sum_p |f_p - y_p|^2
+ *       + lambda * sum_(p,q) w_pq [y_p != y_q]          (Sec. 3.2, Eq. gmpp);
+ *   - the merge gain  Delta(P,Q) = -|P||Q|/(|P|+|Q|) |f_P - f_Q|^2
+ *       + lambda * w_PQ                                  (Prop. 1, Eq. delta);
+ *   - the round-synchronous parallel merge: candidate merges, conflict
+ *     removal, weakly-connected-component merging, recalibration
+ *     (Sec. 3.2 "Parallel Implementation", Steps 0-4; App. Alg. A-1, A-2),
+ *     applied recursively over a ladder of regularisation strengths
+ *     (Sec. 3.2 "Hierarchical Partition").
+ *
+ * Readings taken where the paper is silent (each one is listed, with the
+ * reason, in the design notes of the repository):
+ *   R1  kNN excludes the point itself by index; d2 is IEEE fp32,
+ *       d2 = ((dx*dx) + (dy*dy)) + (dz*dz) with dx = x_q - x_p, no FMA;
+ *       neighbours ordered by (d2, index); -1 padding when n-1 < k.
+ *   R2  the graph is the union of the kNN relations, one edge per unordered
+ *       pair, w = 1.
+ *   R3  component sums are exact int64 fixed point, S = rint(e * 2^F); means
+ *       and gains are fp64 in a fixed operation order.
+ *   R4  component ids are ordered by their smallest member index.
+ *   R5  conflict removal keeps, per node, the incident candidate edge that is
+ *       largest under (Delta desc, lo asc, hi asc).
+ *   R6  |P| < s_min is strict; s_min <= 1 disables it.
+ *   R7  "connect isolated nodes" is not applied.
+ *   R8  the cut term counts edges whose end points lie in different
+ *       components.
+ *   R9  level l+1 starts from level l's contracted graph and statistics.
+ *   R10 Delta > 0 is strict.
+ *
+ * Conventions: all pointers are host pointers owned by the caller.
+ * Functions return 0 on success and a negative code on error:
+ *   -1 invalid argument, -2 non-finite input, -3 fixed-point range,
+ *   -4 out of memory, -6 round cap reached.
+ */
+#ifndef EZSP_ORACLE_H
+#define EZSP_ORACLE_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---- kNN (Sec. 3.1, Sec. 4.1; reading R1) -------------------------------- */
+
+/* Brute force over all pairs.  nbr: n*k int32 (out), d2: n*k fp32 (out,
+ * nullable). */
+int or_knn_brute(const float *xyz, int64_t n, int32_t k, int32_t *nbr,
+                 float *d2);
+
+/* Brute force for the single query point p (k entries). */
+int or_knn_one(const float *xyz, int64_t n, int32_t k, int64_t p,
+               int32_t *nbr, float *d2);
+
+/* Exact kNN through a k-d tree; same output as or_knn_brute. */
+int or_knn_kdtree(const float *xyz, int64_t n, int32_t k, int32_t *nbr,
+                  float *d2);
+
+/* ---- graph (reading R2) -------------------------------------------------- */
+
+/* Unique undirected edges of the kNN relation, sorted by (lo, hi), w = 1.
+ * lo, hi, w: capacity n*k.  Returns the edge count or a negative code. */
+int64_t or_graph(const int32_t *nbr, int64_t n, int32_t k, int32_t *lo,
+                 int32_t *hi, int64_t *w);
+
+/* ---- fixed point (reading R3) -------------------------------------------- */
+
+/* F = min(40, 61 - ceil(log2 n) - max(0, ceil(log2 A))), A = max |e|.
+ * Returns F, or -2 on a non-finite value, -3 when F < 16. */
+int or_fixed_shift(const float *emb, int64_t n, int32_t d);
+
+/* S[p*d+i] = rint(e[p*d+i] * 2^F), round half to even. */
+void or_quantize(const float *emb, int64_t n, int32_t d, int32_t F,
+                 int64_t *S);
+
+/* ---- one merge round, exposed step by step ------------------------------- */
+
+/* Eq. delta for every edge.  size: nn, S: nn*d (fixed point). */
+void or_gains(int64_t ne, const int32_t *lo, const int32_t *hi,
+              const int64_t *w, const int64_t *size, const int64_t *S,
+              int32_t d, int32_t F, double lambda, double *delta);
+
+/* Steps 1-2: target[v] = other end of v's retained edge, or -1. */
+void or_select(int64_t nn, int64_t ne, const int32_t *lo, const int32_t *hi,
+               const double *delta, const int64_t *size, int64_t min_size,
+               int32_t *target);
+
+/* Step 3: weakly connected components of {v -> target[v]}, numbered by
+ * smallest member (reading R4).  Returns the component count. */
+int64_t or_components(int64_t nn, const int32_t *target, int32_t *label);
+
+/* Step 4: component sizes and sums, and the contracted edge list (sorted by
+ * (lo, hi), self loops dropped, weights of parallel edges added).
+ * out arrays: size_out nc, S_out nc*d, lo/hi/w_out capacity ne.
+ * Returns the contracted edge count. */
+int64_t or_contract(int64_t nn, int64_t ne, const int32_t *lo,
+                    const int32_t *hi, const int64_t *w, const int64_t *size,
+                    const int64_t *S, int32_t d, const int32_t *label,
+                    int64_t nc, int64_t *size_out, int64_t *S_out,
+                    int32_t *lo_out, int32_t *hi_out, int64_t *w_out);
+
+/* ---- the ladder (Steps 0-4 per level; hierarchical partition) ------------ */
+
+typedef struct {
+  int32_t level;
+  int32_t round;
+  int64_t n_nodes;     /* nodes entering the round                       */
+  int64_t n_edges;     /* undirected edges entering the round            */
+  int64_t n_choosing;  /* nodes that kept an outgoing merge edge         */
+  int64_t n_comp;      /* components after the round                     */
+  double min_gap;      /* smallest relative gap between a node's best and
+                          second-best candidate gain (1 when < 2 cands)  */
+  double min_sign;     /* smallest |Delta_best| / (f*ss + lambda*w)      */
+} or_round_log;
+
+/* Full ladder on a given graph.
+ *   emb      n*d fp32 embeddings
+ *   lo,hi,w  ne undirected edges (any order, no self loops, no duplicates)
+ *   lambdas  L regularisation strengths; min_size L values or NULL
+ *   labels   L*n int32 (out), canonical per level
+ *   n_comp   L (out); energy L (out, nullable)
+ *   log      capacity log_cap (nullable); *log_len receives the count
+ * Returns 0, or a negative code (-6 when max_rounds is reached). */
+int or_partition(const float *emb, int64_t n, int32_t d, int64_t ne,
+                 const int32_t *lo, const int32_t *hi, const int64_t *w,
+                 int32_t L, const double *lambdas, const int64_t *min_size,
+                 int32_t max_rounds, int32_t *labels, int64_t *n_comp,
+                 double *energy, or_round_log *log, int64_t log_cap,
+                 int64_t *log_len);
+
+/* Eq. gmpp evaluated for a labelling (direct form, fp64).  Means are the
+ * fixed-point means ((double)S_C / |C|) * 2^-F.  The cut term runs over the
+ * given edges. */
+double or_energy(const float *emb, int64_t n, int32_t d, int32_t F,
+                 const int32_t *label, int64_t nc, int64_t ne,
+                 const int32_t *lo, const int32_t *hi, const int64_t *w,
+                 double lambda);
+
+/* Per-component size, mean embedding and centroid for a labelling.
+ * Means: ((double)sum_fixed / size) * 2^-F rounded to fp32, F from
+ * or_fixed_shift on emb; centroids the same with their own F from xyz. */
+int or_component_stats(const int32_t *label, int64_t n, int64_t nc,
+                       const float *emb, int32_t d, const float *xyz,
+                       int64_t *size, float *mean, float *centroid);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* EZSP_ORACLE_H */

@@ -1,0 +1,408 @@
+"""Seeded synthetic point clouds and embeddings for the partition workloads.
+
+This module holds input generation only -- none of the partition method's
+arithmetic -- and is the one piece both the GPU path's tests and the oracle's
+tests consume.  Scenes stand in for the paper's datasets (S3DIS, KITTI-360,
+DALES; Sec. 4.1), which are not available: each scene is built from planar,
+box, cylinder, heightfield and blob primitives, and every point's embedding is
+its primitive's constant vector drawn N(0, I_D) plus N(0, sigma^2) noise, the
+structure the learned embeddings of Sec. 3.1 are trained to have
+(homogeneous inside objects, contrasted across them).
+
+Every draw uses ``numpy.random.default_rng(seed)`` (PCG64) in a fixed order,
+so a scene is a pure function of its name and seed.
+"""
+from __future__ import annotations
+
+import hashlib
+import os
+from dataclasses import dataclass, field
+
+import numpy as np
+
+NOISE_XYZ = 0.005  # 5 mm position noise in every scene
+
+
+@dataclass
+class Scene:
+    name: str
+    xyz: np.ndarray          # [n, 3] float32
+    emb: np.ndarray          # [n, d] float32
+    obj: np.ndarray          # [n] int32 primitive id (diagnostics only)
+    k: int
+    lambdas: list = field(default_factory=list)
+
+    @property
+    def n(self) -> int:
+        return self.xyz.shape[0]
+
+    @property
+    def d(self) -> int:
+        return self.emb.shape[1]
+
+    def digest(self) -> str:
+        h = hashlib.sha256()
+        h.update(self.xyz.tobytes())
+        h.update(self.emb.tobytes())
+        return h.hexdigest()[:16]
+
+
+# --------------------------------------------------------------------------
+# primitive samplers (area-uniform)
+# --------------------------------------------------------------------------
+
+def _rect(rng, m, origin, u, v):
+    """m points uniform on the parallelogram origin + a*u + b*v, a,b in [0,1)."""
+    a = rng.random(m)[:, None]
+    b = rng.random(m)[:, None]
+    return origin[None, :] + a * u[None, :] + b * v[None, :]
+
+
+def _box_faces(lo, hi):
+    """The 5 faces of an axis-aligned box resting on its bottom face
+    (bottom excluded): list of (origin, u, v, area)."""
+    dx, dy, dz = hi - lo
+    ex, ey, ez = np.array([dx, 0, 0.]), np.array([0, dy, 0.]), \
+        np.array([0, 0, dz])
+    faces = [
+        (np.array([lo[0], lo[1], hi[2]]), ex, ey, dx * dy),   # top
+        (lo.copy(), ex, ez, dx * dz),                          # y = lo
+        (np.array([lo[0], hi[1], lo[2]]), ex, ez, dx * dz),   # y = hi
+        (lo.copy(), ey, ez, dy * dz),                          # x = lo
+        (np.array([hi[0], lo[1], lo[2]]), ey, ez, dy * dz),   # x = hi
+    ]
+    return faces
+
+
+def _sample_faces(rng, faces, m):
+    areas = np.array([f[3] for f in faces])
+    cnt = rng.multinomial(m, areas / areas.sum())
+    parts = [_rect(rng, c, f[0], f[1], f[2]) for f, c in zip(faces, cnt)]
+    return np.concatenate(parts, 0) if parts else np.zeros((0, 3))
+
+
+def _embed(rng, obj, n_obj, d, sigma):
+    centers = rng.standard_normal((n_obj, d))
+    noise = rng.standard_normal((obj.shape[0], d)) * sigma
+    return (centers[obj] + noise).astype(np.float32)
+
+
+def _finish(rng, name, pts, obj, d, sigma, k, lambdas, shuffle=True):
+    pts = pts + rng.standard_normal(pts.shape) * NOISE_XYZ
+    n_obj = int(obj.max()) + 1
+    emb = _embed(rng, obj, n_obj, d, sigma)
+    if shuffle:
+        perm = rng.permutation(pts.shape[0])
+        pts, obj, emb = pts[perm], obj[perm], emb[perm]
+    return Scene(name, np.ascontiguousarray(pts, dtype=np.float32),
+                 np.ascontiguousarray(emb), obj.astype(np.int32), k,
+                 list(lambdas))
+
+
+# --------------------------------------------------------------------------
+# indoor rooms
+# --------------------------------------------------------------------------
+
+def _room_primitives(rng, size, n_boxes):
+    """Room shell (6 planes) and n_boxes boxes standing on the floor."""
+    X, Y, Z = size
+    prims = [
+        [(np.zeros(3), np.array([X, 0, 0.]), np.array([0, Y, 0.]), X * Y)],
+        [(np.array([0, 0, Z]), np.array([X, 0, 0.]), np.array([0, Y, 0.]),
+          X * Y)],
+        [(np.zeros(3), np.array([X, 0, 0.]), np.array([0, 0, Z]), X * Z)],
+        [(np.array([0, Y, 0.]), np.array([X, 0, 0.]), np.array([0, 0, Z]),
+          X * Z)],
+        [(np.zeros(3), np.array([0, Y, 0.]), np.array([0, 0, Z]), Y * Z)],
+        [(np.array([X, 0, 0.]), np.array([0, Y, 0.]), np.array([0, 0, Z]),
+          Y * Z)],
+    ]
+    for _ in range(n_boxes):
+        s = rng.uniform(0.3, 1.5, 3)
+        s[2] = min(s[2], Z - 0.05)
+        x0 = rng.uniform(0.0, X - s[0])
+        y0 = rng.uniform(0.0, Y - s[1])
+        lo = np.array([x0, y0, 0.0])
+        prims.append(_box_faces(lo, lo + s))
+    return prims
+
+
+def _sample_room(rng, prims, m):
+    areas = np.array([sum(f[3] for f in p) for p in prims])
+    cnt = rng.multinomial(m, areas / areas.sum())
+    pts, obj = [], []
+    for i, (p, c) in enumerate(zip(prims, cnt)):
+        pts.append(_sample_faces(rng, p, c))
+        obj.append(np.full(c, i, np.int32))
+    return np.concatenate(pts, 0), np.concatenate(obj, 0)
+
+
+def room_small(seed: int = 0) -> Scene:
+    """Indoor room, 20,000 points: 6 planes of a 5x5x3 m box plus 10 boxes;
+    D = 8, embedding noise 0.05; k = 10; lambda = 0.1."""
+    rng = np.random.default_rng(seed)
+    prims = _room_primitives(rng, (5.0, 5.0, 3.0), 10)
+    pts, obj = _sample_room(rng, prims, 20_000)
+    return _finish(rng, "room-20k", pts, obj, 8, 0.05, 10, [0.1])
+
+
+def room_1m(seed: int = 0) -> Scene:
+    """Indoor room, 1,000,000 points after 2 cm voxel subsampling: 40
+    primitives (6 planes + 34 boxes) in a 10x8x3 m volume; D = 16, embedding
+    noise 0.05; k = 10; lambda ladder {0.05, 0.2, 0.8}."""
+    rng = np.random.default_rng(seed)
+    prims = _room_primitives(rng, (10.0, 8.0, 3.0), 34)
+    m = 6_000_000
+    while True:
+        pts, obj = _sample_room(rng, prims, m)
+        pts = pts + rng.standard_normal(pts.shape) * NOISE_XYZ
+        # 2 cm grid subsampling: keep the lowest-index point of each voxel
+        vox = np.floor(pts / 0.02).astype(np.int64)
+        vox -= vox.min(0)
+        key = (vox[:, 0] * (vox[:, 1].max() + 1) + vox[:, 1]) * \
+            (vox[:, 2].max() + 1) + vox[:, 2]
+        _, first = np.unique(key, return_index=True)
+        if first.shape[0] >= 1_000_000:
+            break
+        m *= 2
+    keep = np.sort(rng.choice(first, 1_000_000, replace=False))
+    pts, obj = pts[keep], obj[keep]
+    n_obj = int(obj.max()) + 1
+    emb = _embed(rng, obj, n_obj, 16, 0.05)
+    perm = rng.permutation(pts.shape[0])
+    return Scene("room-1m", np.ascontiguousarray(pts[perm], np.float32),
+                 np.ascontiguousarray(emb[perm]), obj[perm].astype(np.int32),
+                 10, [0.05, 0.2, 0.8])
+
+
+# --------------------------------------------------------------------------
+# driving tile (mobile LiDAR stand-in)
+# --------------------------------------------------------------------------
+
+def _heightfield(rng, n_waves, wl_lo, wl_hi, amp):
+    th = rng.uniform(0, 2 * np.pi, n_waves)
+    wl = rng.uniform(wl_lo, wl_hi, n_waves)
+    ph = rng.uniform(0, 2 * np.pi, n_waves)
+    a = amp / n_waves
+
+    def h(x, y):
+        z = np.zeros(np.broadcast(x, y).shape)
+        for j in range(n_waves):
+            z += a * np.sin(2 * np.pi * (x * np.cos(th[j]) + y * np.sin(th[j]))
+                            / wl[j] + ph[j])
+        return z
+    return h
+
+
+def _density(x, y):
+    """Relative point density of a sensor at the origin: 1/max(r, 2 m)^2,
+    scaled to 1 inside the 2 m disk."""
+    r = np.hypot(x, y)
+    return (2.0 / np.maximum(r, 2.0)) ** 2
+
+
+def _rect_min_range(x0, x1, y0, y1):
+    dx = max(x0, 0.0, -x1)
+    dy = max(y0, 0.0, -y1)
+    return np.hypot(dx, dy)
+
+
+def driving_tile(seed: int = 0, n_points: int = 3_000_000) -> Scene:
+    """Driving tile, 3,000,000 points: ground heightfield (8 sinusoids,
+    wavelengths 10-50 m, 1 m peak) over 100x100 m, 200 car boxes, 300 poles
+    (r = 0.15 m), 40 facade planes; density 1/max(r, 2 m)^2 around a sensor at
+    the origin; D = 16, embedding noise 0.05; k = 10; ladder {0.05, 0.2,
+    0.8}."""
+    rng = np.random.default_rng(seed)
+    half = 50.0
+    h = _heightfield(rng, 8, 10.0, 50.0, 1.0)
+    objs = []  # (kind, params) ; ground is object 0
+
+    for _ in range(200):  # cars: ~4.5 x 1.8 x 1.5 m, +-10 %, axis-aligned
+        s = np.array([4.5, 1.8, 1.5]) * rng.uniform(0.9, 1.1, 3)
+        if rng.random() < 0.5:
+            s[0], s[1] = s[1], s[0]
+        c = rng.uniform(-half + 3, half - 3, 2)
+        lo = np.array([c[0] - s[0] / 2, c[1] - s[1] / 2, float(h(c[0], c[1]))])
+        objs.append(("box", lo, lo + s))
+    for _ in range(300):  # poles
+        c = rng.uniform(-half + 1, half - 1, 2)
+        ht = rng.uniform(3.0, 8.0)
+        objs.append(("pole", np.array([c[0], c[1], float(h(c[0], c[1]))]), ht))
+    for _ in range(40):  # facades: vertical rectangles
+        wdt = rng.uniform(10.0, 40.0)
+        ht = rng.uniform(5.0, 15.0)
+        c = rng.uniform(-half + 5, half - 5, 2)
+        along_x = rng.random() < 0.5
+        z0 = float(h(c[0], c[1]))
+        if along_x:
+            o = np.array([c[0] - wdt / 2, c[1], z0])
+            u = np.array([wdt, 0, 0.])
+        else:
+            o = np.array([c[0], c[1] - wdt / 2, z0])
+            u = np.array([0, wdt, 0.])
+        objs.append(("facade", o, u, np.array([0, 0, ht])))
+
+    def obj_surface(ob, m):
+        if ob[0] == "box":
+            return _sample_faces(rng, _box_faces(ob[1], ob[2]), m)
+        if ob[0] == "pole":
+            base, ht = ob[1], ob[2]
+            t = rng.uniform(0, 2 * np.pi, m)
+            z = rng.uniform(0, ht, m)
+            return np.stack([base[0] + 0.15 * np.cos(t),
+                             base[1] + 0.15 * np.sin(t), base[2] + z], 1)
+        return _rect(rng, m, ob[1], ob[2], ob[3])
+
+    def obj_area_pmax(ob):
+        if ob[0] == "box":
+            lo, hi = ob[1], ob[2]
+            area = sum(f[3] for f in _box_faces(lo, hi))
+            r = _rect_min_range(lo[0], hi[0], lo[1], hi[1])
+        elif ob[0] == "pole":
+            area = 2 * np.pi * 0.15 * ob[2]
+            r = max(np.hypot(ob[1][0], ob[1][1]) - 0.15, 0.0)
+        else:
+            p0, p1 = ob[1][:2], ob[1][:2] + ob[2][:2]
+            area = np.linalg.norm(ob[2]) * ob[3][2]
+            r = _rect_min_range(min(p0[0], p1[0]), max(p0[0], p1[0]),
+                                min(p0[1], p1[1]), max(p0[1], p1[1]))
+        return area, (2.0 / max(r, 2.0)) ** 2
+
+    # density integrals: ground over the tile by the radial law; objects by
+    # a pilot Monte-Carlo pass
+    R = half * np.sqrt(2.0)
+    disk_int = 4 * np.pi + 8 * np.pi * np.log(R / 2.0)  # density over the disk
+    pilot = rng.uniform(-half, half, (200_000, 2))
+    ground_int = (2 * half) ** 2 * _density(pilot[:, 0], pilot[:, 1]).mean()
+    obj_int = []
+    for ob in objs:
+        q = obj_surface(ob, 512)
+        area, _ = obj_area_pmax(ob)
+        obj_int.append(area * _density(q[:, 0], q[:, 1]).mean())
+    K = 1.04 * n_points / (ground_int + sum(obj_int))  # points per unit
+
+    # ground: radial inverse-CDF sampling, rejected outside the square
+    m_g = int(round(K * disk_int))
+    u = rng.random(m_g) * (0.5 + np.log(R / 2.0))
+    r = np.where(u < 0.5, np.sqrt(8.0 * u), 2.0 * np.exp(u - 0.5))
+    t = rng.uniform(0, 2 * np.pi, m_g)
+    gx, gy = r * np.cos(t), r * np.sin(t)
+    inside = (np.abs(gx) < half) & (np.abs(gy) < half)
+    gx, gy = gx[inside], gy[inside]
+    pts = [np.stack([gx, gy, h(gx, gy)], 1)]
+    obj = [np.zeros(gx.shape[0], np.int32)]
+    for i, ob in enumerate(objs):
+        area, pmax = obj_area_pmax(ob)
+        m = int(np.ceil(K * area * pmax))
+        q = obj_surface(ob, m)
+        acc = rng.random(m) < _density(q[:, 0], q[:, 1]) / pmax
+        pts.append(q[acc])
+        obj.append(np.full(int(acc.sum()), i + 1, np.int32))
+    pts = np.concatenate(pts, 0)
+    obj = np.concatenate(obj, 0)
+    if pts.shape[0] < n_points:
+        raise RuntimeError("driving tile generator undershot: %d" % pts.shape[0])
+    keep = np.sort(rng.choice(pts.shape[0], n_points, replace=False))
+    return _finish(rng, "driving-3m", pts[keep], obj[keep], 16, 0.05, 10,
+                   [0.05, 0.2, 0.8])
+
+
+# --------------------------------------------------------------------------
+# aerial tile (airborne LiDAR stand-in)
+# --------------------------------------------------------------------------
+
+def aerial_tile(seed: int = 0, n_points: int = 10_000_000) -> Scene:
+    """Aerial tile, 10,000,000 points: 500x500 m terrain (5 m amplitude,
+    wavelengths 50-200 m), 400 non-overlapping buildings (footprint 10-40 m,
+    height 5-30 m), 2000 Gaussian vegetation blobs; 90 % of points top-down
+    uniform (roof or terrain), 10 % in blobs (about 40 pts/m^2); D = 16,
+    embedding noise 0.1; k = 10; ladder {0.05, 0.2, 0.8, 3.2}."""
+    rng = np.random.default_rng(seed)
+    S = 500.0
+    h = _heightfield(rng, 8, 50.0, 200.0, 5.0)
+    grid = -np.ones((500, 500), np.int32)  # 1 m raster of building ids
+    bld = []
+    tries = 0
+    while len(bld) < 400 and tries < 100_000:
+        tries += 1
+        w, l = rng.uniform(10, 40, 2)
+        x0, y0 = rng.uniform(0, S - w), rng.uniform(0, S - l)
+        i0, i1 = int(np.floor(x0)), int(np.ceil(x0 + w))
+        j0, j1 = int(np.floor(y0)), int(np.ceil(y0 + l))
+        if (grid[i0:i1, j0:j1] >= 0).any():
+            continue
+        ht = rng.uniform(5, 30)
+        roof = float(h(x0 + w / 2, y0 + l / 2)) + ht
+        grid[i0:i1, j0:j1] = len(bld)
+        bld.append((x0, y0, w, l, roof))
+    roof_z = np.array([b[4] for b in bld])
+    n_top = int(round(0.9 * n_points))
+    x = rng.uniform(0, S, n_top)
+    y = rng.uniform(0, S, n_top)
+    b = grid[np.minimum(x.astype(np.int64), 499), np.minimum(y.astype(np.int64), 499)]
+    # exact footprint test inside the raster cells that carry a building id
+    bx0 = np.array([q[0] for q in bld]); by0 = np.array([q[1] for q in bld])
+    bw = np.array([q[2] for q in bld]); bl = np.array([q[3] for q in bld])
+    on = b >= 0
+    bb = np.where(on, b, 0)
+    on &= (x >= bx0[bb]) & (x < bx0[bb] + bw[bb]) & (y >= by0[bb]) & \
+        (y < by0[bb] + bl[bb])
+    z = np.where(on, roof_z[bb], h(x, y))
+    obj_top = np.where(on, 1 + bb, 0).astype(np.int32)
+    n_blob = n_points - n_top
+    bc = np.stack([rng.uniform(0, S, 2000), rng.uniform(0, S, 2000)], 1)
+    bz = h(bc[:, 0], bc[:, 1]) + rng.uniform(3, 10, 2000)
+    bs = rng.uniform(1, 3, 2000)
+    which = rng.integers(0, 2000, n_blob)
+    off = rng.standard_normal((n_blob, 3)) * bs[which][:, None]
+    blob = np.stack([bc[which, 0], bc[which, 1], bz[which]], 1) + off
+    pts = np.concatenate([np.stack([x, y, z], 1), blob], 0)
+    obj = np.concatenate([obj_top, (1 + len(bld) + which).astype(np.int32)])
+    return _finish(rng, "aerial-10m", pts, obj, 16, 0.1, 10,
+                   [0.05, 0.2, 0.8, 3.2])
+
+
+# --------------------------------------------------------------------------
+# registry and cache
+# --------------------------------------------------------------------------
+
+SCENES = {
+    "room-20k": room_small,
+    "room-1m": room_1m,
+    "driving-3m": driving_tile,
+    "aerial-10m": aerial_tile,
+}
+
+
+def _cache_dir():
+    return os.environ.get("EZSP_SCENE_CACHE", "/tmp/ezsp_scenes")
+
+
+def load(name: str, seed: int = 0, cache: bool = True) -> Scene:
+    """Generate (or read back from the on-disk cache) a named scene."""
+    path = os.path.join(_cache_dir(), f"{name}-s{seed}.npz")
+    if cache and os.path.exists(path):
+        z = np.load(path, allow_pickle=False)
+        return Scene(name, z["xyz"], z["emb"], z["obj"], int(z["k"]),
+                     list(z["lambdas"]))
+    sc = SCENES[name](seed)
+    if cache:
+        os.makedirs(_cache_dir(), exist_ok=True)
+        tmp = path + ".tmp%d.npz" % os.getpid()
+        np.savez(tmp, xyz=sc.xyz, emb=sc.emb, obj=sc.obj, k=sc.k,
+                 lambdas=np.array(sc.lambdas))
+        os.replace(tmp, path)
+    return sc
+
+
+def random_cloud(n: int, d: int, seed: int = 0, n_obj: int = 8,
+                 sigma: float = 0.05, extent: float = 1.0) -> Scene:
+    """Small unstructured cloud: n_obj Gaussian clusters with constant
+    embeddings plus noise (test inputs of any size)."""
+    rng = np.random.default_rng(seed)
+    c = rng.uniform(0, extent, (n_obj, 3))
+    obj = rng.integers(0, n_obj, n).astype(np.int32)
+    xyz = c[obj] + rng.standard_normal((n, 3)) * (0.1 * extent)
+    emb = _embed(rng, obj, n_obj, d, sigma)
+    return Scene(f"random-{n}", xyz.astype(np.float32), emb, obj, 10, [0.1])
