@@ -1,0 +1,177 @@
+/*
+ * ezsp.h -- C ABI of the MI355X (gfx950) EZ-SP partition library.
+ *
+ * The library computes the partition step of EZ-SP (arXiv 2512.00385):
+ * the exact k-nearest-neighbour adjacency of a point cloud, then the
+ * round-synchronous parallel merge of adjacent components that greedily
+ * lowers the contour-regularised energy
+ *
+ *   Omega = sum_p |f_p - y_p|^2 + lambda * sum_(p,q) w_pq [y_p != y_q]
+ *                                                   (Sec. 3.2, Eq. gmpp)
+ *
+ * with the merge gain of Prop. 1 (Eq. delta), Steps 0-4 of Sec. 3.2
+ * ("Parallel Implementation"; App. Alg. A-1 and A-2), repeated over a ladder
+ * of regularisation strengths (Sec. 3.2, "Hierarchical Partition").
+ *
+ * Conventions shared by every entry point
+ *   - Every array pointer is a DEVICE pointer unless marked (host).  The
+ *     caller owns every buffer.  The library allocates nothing on the device:
+ *     all scratch memory comes from the caller's workspace `ws` of
+ *     `ws_bytes` bytes (size from the matching *_workspace_size query;
+ *     any alignment, the library aligns internally).
+ *   - `stream` is a hipStream_t passed as void* (NULL = the null stream).
+ *     All device work is enqueued on it.  Every entry point synchronises
+ *     `stream` before it returns, so that it can report errors the device
+ *     detected; outputs are complete when it returns EZSP_OK.
+ *   - Arguments are validated on the host before anything is launched; an
+ *     invalid argument returns EZSP_ERR_INVALID_ARG and touches no memory.
+ *   - On any status other than EZSP_OK the outputs are unspecified.
+ *   - Calls on different streams with different workspaces may run
+ *     concurrently; the only global state is the thread-local message of
+ *     ezsp_last_error().
+ *   - Arrays are row-major and contiguous: xyz is n*3 fp32, emb is n*d fp32.
+ */
+#ifndef EZSP_H
+#define EZSP_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  EZSP_OK = 0,
+  EZSP_ERR_INVALID_ARG = -1,   /* bad size, pointer, parameter            */
+  EZSP_ERR_NONFINITE = -2,     /* NaN or Inf in xyz or emb                */
+  EZSP_ERR_RANGE = -3,         /* embeddings too large for the exact
+                                  fixed-point sums (shift F < 16)         */
+  EZSP_ERR_WORKSPACE = -4,     /* ws_bytes below the queried size         */
+  EZSP_ERR_DEVICE = -5,        /* a HIP call failed, or an internal
+                                  consistency check on the device tripped */
+  EZSP_ERR_NOT_CONVERGED = -6  /* a level reached max_rounds merge rounds */
+} ezsp_status;
+
+/* Flags of ezsp_params.flags. */
+#define EZSP_F_ENERGY 1u /* fill energy[] (Eq. gmpp per level) */
+
+typedef struct {
+  int32_t k;                /* neighbours per point, 1..64                   */
+  int32_t n_levels;         /* L >= 1 (at most 16)                           */
+  const double *lambdas;    /* (host) L regularisation strengths, finite,
+                               >= 0; level l merges with lambdas[l]          */
+  const int64_t *min_size;  /* (host) L minimum superpoint sizes s_min, or
+                               NULL.  A component smaller than s_min may
+                               merge along its best edge even when the gain
+                               is not positive (Step 1); values <= 1 disable */
+  int32_t max_rounds;       /* merge rounds allowed per level; 0 = 256       */
+  uint32_t flags;           /* EZSP_F_* bits                                 */
+} ezsp_params;
+
+/* ---- kNN adjacency (Sec. 3.1: a graph linking every point to its k
+ * nearest neighbours; Sec. 4.1: unit edge weights) ----------------------- */
+
+size_t ezsp_knn_workspace_size(int64_t n, int32_t k);
+
+/* Exact k nearest neighbours of every point.
+ *   xyz  n*3 fp32 (in)
+ *   nbr  n*k int32 (out): row p lists the k points q != p with the smallest
+ *        (d2(p,q), q), in increasing order, where
+ *        d2 = ((dx*dx) + (dy*dy)) + (dz*dz), dx = x_q - x_p, each operation
+ *        one IEEE fp32 rounding (no fused multiply-add).  Ties in d2 go to
+ *        the smaller index.  When n-1 < k the row ends in -1 entries.
+ *   d2   n*k fp32 (out, nullable): the matching squared distances, +inf
+ *        where nbr is -1.
+ * Errors: INVALID_ARG (n < 1, n >= 2^31, k outside 1..64, NULL pointer),
+ *         NONFINITE, WORKSPACE, DEVICE. */
+int ezsp_knn(const float *xyz, int64_t n, int32_t k, int32_t *nbr, float *d2,
+             void *ws, size_t ws_bytes, void *stream);
+
+/* ---- partition (Sec. 3.2: Eq. gmpp, Prop. 1, Steps 0-4, hierarchical
+ * partition; App. Alg. A-1, A-2) ----------------------------------------- */
+
+size_t ezsp_partition_workspace_size(int64_t n, int32_t d,
+                                     const ezsp_params *p);
+
+/* kNN graph of xyz (as ezsp_knn, one undirected edge of weight 1 per
+ * neighbouring pair), then the merge ladder on the embeddings.
+ *   xyz     n*3 fp32 (in)
+ *   emb     n*d fp32 (in), 1 <= d <= 64
+ *   labels  L*n int32 (out): row l holds every point's superpoint at level
+ *           l, numbered 0..n_comp[l]-1 in increasing order of each
+ *           superpoint's smallest point index
+ *   n_comp  (host) L int64 (out): superpoints per level
+ *   energy  (host) L double (out, nullable; written when EZSP_F_ENERGY is
+ *           set): Omega of Eq. gmpp for level l with lambdas[l], each
+ *           superpoint's value being its mean embedding
+ * Component means and sums are exact: embeddings enter as int64 fixed point
+ * S = rint(e * 2^F), F = min(40, 61 - ceil(log2 n) - max(0, ceil(log2 A))),
+ * A = max |e|; gains are fp64 in a fixed operation order, so decisions do not
+ * depend on summation order.  Conflict removal keeps, per component, the
+ * candidate edge with the largest gain, ties to the smaller neighbour (in the
+ * order of smallest point index).
+ * Errors: INVALID_ARG, NONFINITE, RANGE (F < 16), WORKSPACE, DEVICE,
+ *         NOT_CONVERGED. */
+int ezsp_partition(const float *xyz, const float *emb, int64_t n, int32_t d,
+                   const ezsp_params *p, int32_t *labels, int64_t *n_comp,
+                   double *energy, void *ws, size_t ws_bytes, void *stream);
+
+/* The merge ladder on a given neighbour table instead of xyz.
+ *   nbr  n*k int32 (in): entries in [-1, n); -1 and q == p are ignored,
+ *        repeated entries count once.  The graph is the set of unordered
+ *        pairs {p, q} with q in row p or p in row q, each of weight 1.
+ * Other arguments and errors as ezsp_partition (p->k is the row length). */
+int ezsp_partition_from_knn(const int32_t *nbr, const float *emb, int64_t n,
+                            int32_t d, const ezsp_params *p, int32_t *labels,
+                            int64_t *n_comp, double *energy, void *ws,
+                            size_t ws_bytes, void *stream);
+
+/* ---- per-superpoint attributes (Sec. 3.2: mean embedding Y_P of each
+ * superpoint; App. Alg. A-2, component_attributes) ----------------------- */
+
+size_t ezsp_component_stats_workspace_size(int64_t n, int64_t n_comp,
+                                           int32_t d);
+
+/* Size, mean embedding and centroid of every superpoint of a labelling.
+ *   labels    n int32 (in), each in [0, n_comp)
+ *   emb       n*d fp32 (in); xyz n*3 fp32 (in, nullable)
+ *   size      n_comp int64 (out)
+ *   emb_mean  n_comp*d fp32 (out): ((double)sum S / size) * 2^-F rounded to
+ *             fp32, S the fixed point of emb with F by the rule above
+ *             (0 for an empty superpoint)
+ *   centroid  n_comp*3 fp32 (out, NULL when xyz is NULL): the same for xyz
+ *             with its own F
+ * Errors: INVALID_ARG (also for a label outside [0, n_comp), detected on
+ *         the device), NONFINITE, RANGE, WORKSPACE, DEVICE. */
+int ezsp_component_stats(const int32_t *labels, int64_t n, int64_t n_comp,
+                         const float *emb, int32_t d, const float *xyz,
+                         int64_t *size, float *emb_mean, float *centroid,
+                         void *ws, size_t ws_bytes, void *stream);
+
+/* ---- diagnostics --------------------------------------------------------- */
+
+/* Static text for a status code. */
+const char *ezsp_status_string(int status);
+
+/* Detail of the last error on the calling thread ("" if none). */
+const char *ezsp_last_error(void);
+
+/* Per-stage timing with HIP events recorded on the caller's stream around
+ * the launches of each stage ("knn_query", "morton_sort", "graph_build",
+ * "select", "union", "stats", "contract", "compose").  Off by default; a
+ * diagnostic for benchmarks.  ezsp_profile_enable(1) clears the totals and
+ * starts recording, ezsp_profile_enable(0) stops.  ezsp_profile_read gives
+ * the number of recorded launches of `stage`, their summed duration in
+ * milliseconds and the summed algorithmic bytes the stage has to move (its
+ * input and output arrays, each counted once; host pointers, each
+ * nullable); it returns -1, with zeros, for a stage never recorded.
+ * Process-wide state: not for concurrent callers. */
+int ezsp_profile_enable(int on);
+int ezsp_profile_read(const char *stage, int64_t *launches, double *ms,
+                      double *alg_bytes);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* EZSP_H */

@@ -604,33 +604,47 @@ int or_partition(const float *emb, int64_t n, int32_t d, int64_t ne,
       for (int64_t v = 0; v < nn; ++v) choosing += (target[v] >= 0);
 
       if (log && log_len && *log_len < log_cap) {
-        /* decision margins: best vs second-best, and |Delta| relative to
-         * the magnitude of its two terms, over every choosing node */
-        double min_gap = 1.0, min_sign = 1.0;
-        for (int64_t v = 0; v < nn; ++v) {
-          int64_t b1 = -1, b2 = -1;
-          for (int64_t e = 0; e < me; ++e) {
-            if (elo[e] != v && ehi[e] != v) continue;
+        /* decision margins over every choosing node: best vs second-best
+         * candidate, and |Delta_best| relative to the magnitude of its two
+         * terms.  One pass over the edges keeps each node's two best. */
+        int64_t *b1 = (int64_t *)malloc(sizeof(int64_t) * (size_t)nn);
+        int64_t *b2 = (int64_t *)malloc(sizeof(int64_t) * (size_t)nn);
+        if (!b1 || !b2) {
+          free(b1);
+          free(b2);
+          rc = OR_ENOMEM;
+          goto done;
+        }
+        for (int64_t v = 0; v < nn; ++v) b1[v] = b2[v] = -1;
+        for (int64_t e = 0; e < me; ++e) {
+          int32_t ends[2] = {elo[e], ehi[e]};
+          for (int s2 = 0; s2 < 2; ++s2) {
+            int32_t v = ends[s2];
             if (!is_candidate(delta[e], size[v], smin)) continue;
-            if (b1 < 0 || edge_better(e, b1, elo, ehi, delta)) {
-              b2 = b1;
-              b1 = e;
-            } else if (b2 < 0 || edge_better(e, b2, elo, ehi, delta)) {
-              b2 = e;
+            if (b1[v] < 0 || edge_better(e, b1[v], elo, ehi, delta)) {
+              b2[v] = b1[v];
+              b1[v] = e;
+            } else if (b2[v] < 0 || edge_better(e, b2[v], elo, ehi, delta)) {
+              b2[v] = e;
             }
           }
-          if (b1 < 0) continue;
+        }
+        double min_gap = 1.0, min_sign = 1.0;
+        for (int64_t v = 0; v < nn; ++v) {
+          if (b1[v] < 0) continue;
           double f, ss;
-          double g = edge_gain(elo[b1], ehi[b1], ew[b1], size, S, d, scale,
-                               lambda, &f, &ss);
-          double mag = f * ss + lambda * (double)ew[b1];
+          double g = edge_gain(elo[b1[v]], ehi[b1[v]], ew[b1[v]], size, S, d,
+                               scale, lambda, &f, &ss);
+          double mag = f * ss + lambda * (double)ew[b1[v]];
           if (mag > 0.0 && fabs(g) / mag < min_sign) min_sign = fabs(g) / mag;
-          if (b2 >= 0) {
-            double g2 = delta[b2];
+          if (b2[v] >= 0) {
+            double g2 = delta[b2[v]];
             double den = fmax(fabs(g), fabs(g2));
             if (den > 0.0 && (g - g2) / den < min_gap) min_gap = (g - g2) / den;
           }
         }
+        free(b1);
+        free(b2);
         or_round_log *r = &log[(*log_len)++];
         r->level = l;
         r->round = round;

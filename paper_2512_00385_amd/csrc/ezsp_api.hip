@@ -1,0 +1,256 @@
+// ezsp_api.hip -- the extern "C" entry points declared in include/ezsp.h:
+// argument validation on the host, workspace carving, and dispatch to the
+// kernel launchers.
+#include <math.h>
+#include <string.h>
+
+#include "../../include/ezsp.h"
+#include "ezsp_internal.h"
+
+namespace ezsp {
+const char *last_error_text();
+int prof_enable(int on);
+int prof_read(const char *name, int64_t *launches, double *ms,
+              double *bytes);
+}
+
+using namespace ezsp;
+
+namespace {
+
+constexpr int64_t kMaxN = (int64_t)1 << 31;
+
+// Aligns the caller's workspace; Ctl first, then the rest.
+Arena open_ws(void *ws, size_t bytes) {
+  Arena a;
+  uintptr_t p = reinterpret_cast<uintptr_t>(ws);
+  uintptr_t q = (p + 255) & ~uintptr_t(255);
+  a.base = reinterpret_cast<char *>(q);
+  a.cap = (bytes > (q - p)) ? bytes - (q - p) : 0;
+  return a;
+}
+
+int fail(int code, const char *msg) {
+  set_error("%s", msg);
+  return code;
+}
+
+bool n_ok(int64_t n) { return n >= 1 && n < kMaxN; }
+
+// Graph arrays are indexed with int32: 2*k*n directed entries must fit.
+bool edges_ok(int64_t n, int32_t k) {
+  return 2 * n * (int64_t)k < kMaxN - 1;
+}
+
+int check_params(int64_t n, int32_t d, const ezsp_params *p) {
+  if (!p) return fail(EZSP_ERR_INVALID_ARG, "params is NULL");
+  if (!n_ok(n)) return fail(EZSP_ERR_INVALID_ARG, "n must be in [1, 2^31)");
+  if (d < 1 || d > 64) return fail(EZSP_ERR_INVALID_ARG, "d must be in 1..64");
+  if (p->k < 1 || p->k > 64)
+    return fail(EZSP_ERR_INVALID_ARG, "k must be in 1..64");
+  if (!edges_ok(n, p->k))
+    return fail(EZSP_ERR_INVALID_ARG, "2*k*n must stay below 2^31");
+  if ((int64_t)n * d >= kMaxN)
+    return fail(EZSP_ERR_INVALID_ARG, "n*d must stay below 2^31");
+  if (p->n_levels < 1 || p->n_levels > 16)
+    return fail(EZSP_ERR_INVALID_ARG, "n_levels must be in 1..16");
+  if (!p->lambdas) return fail(EZSP_ERR_INVALID_ARG, "lambdas is NULL");
+  for (int32_t l = 0; l < p->n_levels; ++l)
+    if (!isfinite(p->lambdas[l]) || p->lambdas[l] < 0.0)
+      return fail(EZSP_ERR_INVALID_ARG, "every lambda must be finite and >= 0");
+  if (p->max_rounds < 0)
+    return fail(EZSP_ERR_INVALID_ARG, "max_rounds must be >= 0");
+  if (p->flags & ~EZSP_F_ENERGY)
+    return fail(EZSP_ERR_INVALID_ARG, "unknown flag bits");
+  return EZSP_OK;
+}
+
+size_t partition_bytes(int64_t n, int32_t d, int32_t k, bool with_knn) {
+  Arena a;
+  a.take<Ctl>(1);
+  if (with_knn) {
+    KnnWork w;
+    knn_reserve(a, (int32_t)n, k, &w);
+  }
+  ladder_reserve(a, (int32_t)n, d, k);
+  return a.off + 512;
+}
+
+int run_partition(const float *xyz, const int32_t *nbr_in, const float *emb,
+                  int64_t n, int32_t d, const ezsp_params *p, int32_t *labels,
+                  int64_t *n_comp, double *energy, void *ws, size_t ws_bytes,
+                  void *stream) {
+  const bool with_knn = xyz != nullptr;
+  if (ws_bytes < partition_bytes(n, d, p->k, with_knn))
+    return fail(EZSP_ERR_WORKSPACE, "workspace smaller than the queried size");
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  Arena a = open_ws(ws, ws_bytes);
+  Ctl *ctl = a.take<Ctl>(1);
+  hipLaunchKernelGGL(k_ctl_init, dim3(1), dim3(64), 0, st, ctl);
+  LadderArgs g;
+  memset(&g, 0, sizeof(g));
+  if (with_knn) {
+    KnnWork w;
+    knn_reserve(a, (int32_t)n, p->k, &w);
+    int rc = check_hip(
+        knn_launch(xyz, (int32_t)n, p->k, ctl, w, nullptr, nullptr, st),
+        "knn launch");
+    if (rc) return rc;
+    g.nbr = w.nbr_int;
+    g.perm = w.perm;
+    g.inv = w.inv;
+    g.check_nbr = false;
+  } else {
+    g.nbr = nbr_in;
+    g.check_nbr = true;
+  }
+  g.emb = emb;
+  g.n = (int32_t)n;
+  g.d = d;
+  g.k = p->k;
+  g.n_levels = p->n_levels;
+  g.lambdas = p->lambdas;
+  g.min_size = p->min_size;
+  g.max_rounds = p->max_rounds;
+  g.want_energy = (p->flags & EZSP_F_ENERGY) != 0;
+  g.labels = labels;
+  g.n_comp = n_comp;
+  g.energy = energy;
+  return ladder_run(g, ctl, a, st);
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *ezsp_status_string(int status) {
+  switch (status) {
+    case EZSP_OK: return "ok";
+    case EZSP_ERR_INVALID_ARG: return "invalid argument";
+    case EZSP_ERR_NONFINITE: return "non-finite input";
+    case EZSP_ERR_RANGE: return "embeddings out of fixed-point range";
+    case EZSP_ERR_WORKSPACE: return "workspace too small";
+    case EZSP_ERR_DEVICE: return "device error";
+    case EZSP_ERR_NOT_CONVERGED: return "max_rounds reached";
+    default: return "unknown status";
+  }
+}
+
+const char *ezsp_last_error(void) { return last_error_text(); }
+
+int ezsp_profile_enable(int on) { return prof_enable(on); }
+
+int ezsp_profile_read(const char *stage, int64_t *launches, double *ms,
+                      double *alg_bytes) {
+  return prof_read(stage, launches, ms, alg_bytes);
+}
+
+size_t ezsp_knn_workspace_size(int64_t n, int32_t k) {
+  if (!n_ok(n) || k < 1 || k > 64 || (int64_t)n * k >= kMaxN) return 0;
+  Arena a;
+  a.take<Ctl>(1);
+  KnnWork w;
+  knn_reserve(a, (int32_t)n, k, &w);
+  return a.off + 512;
+}
+
+int ezsp_knn(const float *xyz, int64_t n, int32_t k, int32_t *nbr, float *d2,
+             void *ws, size_t ws_bytes, void *stream) {
+  set_error("%s", "");
+  if (!xyz || !nbr || !ws)
+    return fail(EZSP_ERR_INVALID_ARG, "xyz, nbr and ws must not be NULL");
+  if (!n_ok(n)) return fail(EZSP_ERR_INVALID_ARG, "n must be in [1, 2^31)");
+  if (k < 1 || k > 64) return fail(EZSP_ERR_INVALID_ARG, "k must be in 1..64");
+  if ((int64_t)n * k >= kMaxN)
+    return fail(EZSP_ERR_INVALID_ARG, "n*k must stay below 2^31");
+  if (ws_bytes < ezsp_knn_workspace_size(n, k))
+    return fail(EZSP_ERR_WORKSPACE, "workspace smaller than the queried size");
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  Arena a = open_ws(ws, ws_bytes);
+  Ctl *ctl = a.take<Ctl>(1);
+  KnnWork w;
+  knn_reserve(a, (int32_t)n, k, &w);
+  hipLaunchKernelGGL(k_ctl_init, dim3(1), dim3(64), 0, st, ctl);
+  int rc = check_hip(knn_launch(xyz, (int32_t)n, k, ctl, w, nbr, d2, st),
+                     "knn launch");
+  if (rc) return rc;
+  Ctl *h = pinned_ctl();
+  if (!h) return fail(EZSP_ERR_DEVICE, "hipHostMalloc of the control block");
+  if ((rc = read_ctl(ctl, h, st))) return rc;
+  if (h->err & kErrNonFinite)
+    return fail(EZSP_ERR_NONFINITE, "non-finite coordinate in xyz");
+  if (h->err) return fail(EZSP_ERR_DEVICE, "internal check failed in kNN");
+  return EZSP_OK;
+}
+
+size_t ezsp_partition_workspace_size(int64_t n, int32_t d,
+                                     const ezsp_params *p) {
+  if (!p || !n_ok(n) || d < 1 || d > 64 || p->k < 1 || p->k > 64 ||
+      !edges_ok(n, p->k))
+    return 0;
+  return partition_bytes(n, d, p->k, true);
+}
+
+int ezsp_partition(const float *xyz, const float *emb, int64_t n, int32_t d,
+                   const ezsp_params *p, int32_t *labels, int64_t *n_comp,
+                   double *energy, void *ws, size_t ws_bytes, void *stream) {
+  set_error("%s", "");
+  if (!xyz || !emb || !labels || !n_comp || !ws)
+    return fail(EZSP_ERR_INVALID_ARG,
+                "xyz, emb, labels, n_comp and ws must not be NULL");
+  int rc = check_params(n, d, p);
+  if (rc) return rc;
+  return run_partition(xyz, nullptr, emb, n, d, p, labels, n_comp, energy, ws,
+                       ws_bytes, stream);
+}
+
+int ezsp_partition_from_knn(const int32_t *nbr, const float *emb, int64_t n,
+                            int32_t d, const ezsp_params *p, int32_t *labels,
+                            int64_t *n_comp, double *energy, void *ws,
+                            size_t ws_bytes, void *stream) {
+  set_error("%s", "");
+  if (!nbr || !emb || !labels || !n_comp || !ws)
+    return fail(EZSP_ERR_INVALID_ARG,
+                "nbr, emb, labels, n_comp and ws must not be NULL");
+  int rc = check_params(n, d, p);
+  if (rc) return rc;
+  return run_partition(nullptr, nbr, emb, n, d, p, labels, n_comp, energy, ws,
+                       ws_bytes, stream);
+}
+
+size_t ezsp_component_stats_workspace_size(int64_t n, int64_t n_comp,
+                                           int32_t d) {
+  if (!n_ok(n) || n_comp < 1 || n_comp >= kMaxN || d < 1 || d > 64 ||
+      n_comp * d >= kMaxN)
+    return 0;
+  Arena a;
+  a.take<Ctl>(1);
+  stats_reserve(a, (int32_t)n, n_comp, d);
+  return a.off + 512;
+}
+
+int ezsp_component_stats(const int32_t *labels, int64_t n, int64_t n_comp,
+                         const float *emb, int32_t d, const float *xyz,
+                         int64_t *size, float *emb_mean, float *centroid,
+                         void *ws, size_t ws_bytes, void *stream) {
+  set_error("%s", "");
+  if (!labels || !emb || !size || !emb_mean || !ws)
+    return fail(EZSP_ERR_INVALID_ARG,
+                "labels, emb, size, emb_mean and ws must not be NULL");
+  if (xyz && !centroid)
+    return fail(EZSP_ERR_INVALID_ARG, "centroid must be given with xyz");
+  if (!n_ok(n)) return fail(EZSP_ERR_INVALID_ARG, "n must be in [1, 2^31)");
+  if (d < 1 || d > 64) return fail(EZSP_ERR_INVALID_ARG, "d must be in 1..64");
+  if (n_comp < 1 || n_comp >= kMaxN || n_comp * d >= kMaxN || n * d >= kMaxN)
+    return fail(EZSP_ERR_INVALID_ARG, "n_comp out of range");
+  if (ws_bytes < ezsp_component_stats_workspace_size(n, n_comp, d))
+    return fail(EZSP_ERR_WORKSPACE, "workspace smaller than the queried size");
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  Arena a = open_ws(ws, ws_bytes);
+  Ctl *ctl = a.take<Ctl>(1);
+  hipLaunchKernelGGL(k_ctl_init, dim3(1), dim3(64), 0, st, ctl);
+  return stats_run(labels, (int32_t)n, (int32_t)n_comp, emb, d, xyz, size,
+                   emb_mean, centroid, ctl, a, st);
+}
+
+}  // extern "C"

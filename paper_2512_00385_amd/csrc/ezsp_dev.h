@@ -1,0 +1,198 @@
+// ezsp_dev.h -- device-side building blocks shared by the HIP kernels of the
+// EZ-SP partition library (gfx950, wave64): the device control block, wave
+// and block scans, a device-wide scan driven by functors, and an LSD radix
+// sort of 64-bit keys with 32-bit payloads.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace ezsp {
+
+constexpr int kWave = 64;
+
+// Error bits raised on the device and read back by the host.
+enum : uint32_t {
+  kErrNonFinite = 1u,  // NaN / Inf in xyz or emb
+  kErrRange = 2u,      // fixed-point shift below 16
+  kErrInternal = 4u,   // an index or capacity check failed
+  kErrBadIndex = 8u,   // caller data out of range (neighbour id, label)
+  kErrJump = 16u,      // pointer jumping hit its iteration cap
+};
+
+// Small block of device scalars, one per call, at the start of the
+// workspace.  The host reads it back once per merge round.
+struct Ctl {
+  uint32_t err;
+  int32_t F;            // fixed-point shift of the embeddings
+  int32_t any_choice;   // some node kept a merge edge this round
+  int32_t n_next;       // components after this round
+  int32_t e_next;       // directed edges after this round
+  int32_t slots;        // hash-table slots this round
+  uint32_t maxabs_bits; // max |e| as fp32 bits (monotone for >= 0)
+  int32_t pad0;
+  int32_t bbox_enc[6];  // min xyz, max xyz in order-preserving int form
+  int32_t pad1[2];
+  int64_t cut_w2;       // 2 * cut weight (directed sum) of the current graph
+  double fid_total;     // fidelity term of the energy
+};
+
+// --- order-preserving float <-> int (for atomic min/max on floats) --------
+__device__ __forceinline__ int32_t f2ord(float f) {
+  int32_t i = __float_as_int(f);
+  return i >= 0 ? i : (i ^ 0x7fffffff);
+}
+__host__ __device__ __forceinline__ float ord2f(int32_t i) {
+  int32_t b = i >= 0 ? i : (i ^ 0x7fffffff);
+  union { int32_t i; float f; } u;
+  u.i = b;
+  return u.f;
+}
+
+__device__ __forceinline__ void raise_err(Ctl *ctl, uint32_t bits) {
+  atomicOr(&ctl->err, bits);
+}
+
+// --- wave / block scans (wave64) ------------------------------------------
+template <class T>
+__device__ __forceinline__ T wave_incl_scan(T v) {
+  const int lane = threadIdx.x & (kWave - 1);
+#pragma unroll
+  for (int off = 1; off < kWave; off <<= 1) {
+    T t = __shfl_up(v, off, kWave);
+    if (lane >= off) v += t;
+  }
+  return v;
+}
+
+template <class T>
+__device__ __forceinline__ T wave_sum(T v) {
+#pragma unroll
+  for (int off = kWave / 2; off > 0; off >>= 1) v += __shfl_xor(v, off, kWave);
+  return v;
+}
+
+// Exclusive scan over a block of NT threads; *total gets the block sum.
+// `wsum` is LDS scratch of NT/64 elements.  Contains barriers.
+template <int NT, class T>
+__device__ __forceinline__ T block_excl_scan(T v, T *wsum, T *total) {
+  const int lane = threadIdx.x & (kWave - 1);
+  const int wid = threadIdx.x / kWave;
+  T inc = wave_incl_scan(v);
+  if (lane == kWave - 1) wsum[wid] = inc;
+  __syncthreads();
+  T off = 0, tot = 0;
+#pragma unroll
+  for (int w = 0; w < NT / kWave; ++w) {
+    T s = wsum[w];
+    off += (w < wid) ? s : T(0);
+    tot += s;
+  }
+  __syncthreads();
+  *total = tot;
+  return off + inc - v;
+}
+
+// --- device-wide exclusive scan of int32 values produced by a functor -----
+// Op provides:  __device__ int32_t value(int32_t i) const;
+//               __device__ void emit(int32_t i, int32_t excl, int32_t v) const;
+// The scan runs over [0, n_bound); op.value must return 0 past the real end.
+constexpr int kScanNT = 256;
+constexpr int kScanItems = 8;
+constexpr int kScanTile = kScanNT * kScanItems;
+
+template <class Op>
+__global__ __launch_bounds__(kScanNT) void k_scan_reduce(Op op, int32_t n,
+                                                         int32_t *bsum) {
+  __shared__ int32_t wsum[kScanNT / kWave];
+  const int32_t base = blockIdx.x * kScanTile + threadIdx.x * kScanItems;
+  int32_t s = 0;
+#pragma unroll
+  for (int j = 0; j < kScanItems; ++j) {
+    int32_t i = base + j;
+    if (i < n) s += op.value(i);
+  }
+  int32_t tot;
+  block_excl_scan<kScanNT>(s, wsum, &tot);
+  if (threadIdx.x == 0) bsum[blockIdx.x] = tot;
+}
+
+// One block: exclusive scan of bsum[0, nb) in place, total to *total.
+__global__ __launch_bounds__(1024) void k_scan_bsums(int32_t *bsum, int32_t nb,
+                                                     int32_t *total);
+
+template <class Op>
+__global__ __launch_bounds__(kScanNT) void k_scan_apply(Op op, int32_t n,
+                                                        const int32_t *bsum) {
+  __shared__ int32_t wsum[kScanNT / kWave];
+  const int32_t base = blockIdx.x * kScanTile + threadIdx.x * kScanItems;
+  int32_t v[kScanItems];
+  int32_t s = 0;
+#pragma unroll
+  for (int j = 0; j < kScanItems; ++j) {
+    int32_t i = base + j;
+    v[j] = (i < n) ? op.value(i) : 0;
+    s += v[j];
+  }
+  int32_t tot;
+  int32_t run = block_excl_scan<kScanNT>(s, wsum, &tot) + bsum[blockIdx.x];
+#pragma unroll
+  for (int j = 0; j < kScanItems; ++j) {
+    int32_t i = base + j;
+    if (i < n) op.emit(i, run, v[j]);
+    run += v[j];
+  }
+}
+
+inline int32_t scan_blocks(int64_t n) {
+  return (int32_t)((n + kScanTile - 1) / kScanTile);
+}
+
+// Exclusive scan; `bsum` needs scan_blocks(n) ints; `total` (device) gets the
+// sum.  n may be 0.
+template <class Op>
+inline void device_scan(const Op &op, int32_t n, int32_t *bsum, int32_t *total,
+                        hipStream_t st) {
+  int32_t nb = scan_blocks(n);
+  if (nb == 0) {
+    hipLaunchKernelGGL(k_scan_bsums, dim3(1), dim3(1024), 0, st, bsum, 0,
+                       total);
+    return;
+  }
+  hipLaunchKernelGGL(k_scan_reduce<Op>, dim3(nb), dim3(kScanNT), 0, st, op, n,
+                     bsum);
+  hipLaunchKernelGGL(k_scan_bsums, dim3(1), dim3(1024), 0, st, bsum, nb,
+                     total);
+  hipLaunchKernelGGL(k_scan_apply<Op>, dim3(nb), dim3(kScanNT), 0, st, op, n,
+                     bsum);
+}
+
+// Common functor: exclusive scan of an int32 array into another.  The real
+// length is `n` or, when `n_dev` is set, the device value *n_dev; items past
+// it count as 0, and out[len] receives the total, so a scan over len+1
+// items produces a CSR offset array.
+struct ScanArray {
+  const int32_t *in;
+  int32_t *out;
+  int32_t n;
+  const int32_t *n_dev;
+  __device__ int32_t len() const { return n_dev ? *n_dev : n; }
+  __device__ int32_t value(int32_t i) const {
+    return (i < len()) ? in[i] : 0;
+  }
+  __device__ void emit(int32_t i, int32_t excl, int32_t) const {
+    if (i <= len()) out[i] = excl;
+  }
+};
+
+// --- LSD radix sort of (uint64 key, uint32 value) -------------------------
+constexpr int kSortNT = 256;
+constexpr int kSortItems = 16;
+constexpr int kSortTile = kSortNT * kSortItems;
+constexpr int kSortBins = 256;
+
+inline int32_t sort_blocks(int64_t n) {
+  return (int32_t)((n + kSortTile - 1) / kSortTile);
+}
+
+}  // namespace ezsp

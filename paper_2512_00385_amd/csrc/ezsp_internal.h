@@ -1,0 +1,119 @@
+// ezsp_internal.h -- host-side internal interface between the C ABI layer
+// and the kernel launchers of the EZ-SP partition library.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "ezsp_dev.h"
+
+namespace ezsp {
+
+// Bump allocator over the caller's workspace.  With base == nullptr it only
+// measures: every take() returns nullptr and `off` ends at the bytes needed.
+struct Arena {
+  char *base = nullptr;
+  size_t cap = 0;
+  size_t off = 0;
+  template <class T>
+  T *take(size_t count) {
+    off = (off + 255) & ~size_t(255);
+    T *p = base ? reinterpret_cast<T *>(base + off) : nullptr;
+    off += count * sizeof(T);
+    return p;
+  }
+};
+
+// Implicit 8-ary tree of boxes over the Morton-ordered points: level 0 holds
+// one box per bucket of kBucket consecutive points, level l+1 one box per 8
+// boxes of level l, up to a single root at level `top`.
+constexpr int kBucket = 32;
+constexpr int kFan = 8;
+constexpr int kMaxTreeLevels = 16;
+struct Tree {
+  int32_t off[kMaxTreeLevels];
+  int32_t cnt[kMaxTreeLevels];
+  int32_t top;
+  int32_t total;
+};
+Tree make_tree(int32_t n);
+
+// Radix sort of (key, value) pairs on bits [0, nbits).  Returns true when
+// the sorted result ended in the *_alt buffers.
+bool radix_sort_pairs(uint64_t *keys, uint32_t *vals, uint64_t *keys_alt,
+                      uint32_t *vals_alt, int32_t n, int nbits,
+                      int32_t *hist, int32_t *bsum, int32_t *total, Ctl *ctl,
+                      hipStream_t st);
+size_t radix_hist_ints(int32_t n);
+
+// kNN: Morton sort, box tree, exact query.  Produces the internal
+// (Morton-order) neighbour table nbr_int (n*k, -1 padded) and the maps
+// perm (internal -> original) and inv (original -> internal); optionally the
+// caller-facing tables in original order.
+struct KnnWork {
+  int32_t *perm = nullptr;     // n
+  int32_t *inv = nullptr;      // n
+  int32_t *nbr_int = nullptr;  // n*k
+  uint64_t *keys = nullptr, *keys2 = nullptr;
+  uint32_t *vals = nullptr, *vals2 = nullptr;
+  float4 *pts = nullptr, *blo = nullptr, *bhi = nullptr;
+  int32_t *hist = nullptr, *bsum = nullptr, *total = nullptr;
+};
+void knn_reserve(Arena &a, int32_t n, int32_t k, KnnWork *w);
+hipError_t knn_launch(const float *xyz, int32_t n, int32_t k, Ctl *ctl,
+                      const KnnWork &w, int32_t *nbr_out, float *d2_out,
+                      hipStream_t st);
+
+// Merge ladder on a neighbour table (internal ids; perm/inv may be null
+// when internal == original order).
+struct LadderArgs {
+  const int32_t *nbr;   // n*k
+  const int32_t *perm;  // nullable
+  const int32_t *inv;   // nullable
+  const float *emb;     // n*d, caller order
+  int32_t n, d, k;
+  int32_t n_levels;
+  const double *lambdas;
+  const int64_t *min_size;
+  int32_t max_rounds;
+  bool want_energy;
+  bool check_nbr;       // validate caller-supplied neighbour ids
+  int32_t *labels;      // L*n, caller order
+  int64_t *n_comp;      // host
+  double *energy;       // host, nullable
+};
+void ladder_reserve(Arena &a, int32_t n, int32_t d, int32_t k);
+// Returns an ezsp_status code; detail text goes through set_error().
+int ladder_run(const LadderArgs &args, Ctl *ctl, Arena &a, hipStream_t st);
+
+// Component statistics of a labelling.
+void stats_reserve(Arena &a, int32_t n, int64_t n_comp, int32_t d);
+int stats_run(const int32_t *labels, int32_t n, int32_t n_comp,
+              const float *emb, int32_t d, const float *xyz, int64_t *size,
+              float *emb_mean, float *centroid, Ctl *ctl, Arena &a,
+              hipStream_t st);
+
+// Shared host helpers.
+void set_error(const char *fmt, ...);
+int read_ctl(Ctl *ctl, Ctl *host, hipStream_t st);  // sync + copy back
+int check_hip(hipError_t e, const char *what);
+Ctl *pinned_ctl();
+__global__ void k_ctl_init(Ctl *ctl);
+__global__ void k_maxabs(const float *v, int64_t count, Ctl *ctl);
+__global__ void k_fixshift(Ctl *ctl, int32_t n);
+
+}  // namespace ezsp
+
+namespace ezsp {
+// Optional per-kernel timing with HIP events on the launch stream (off by
+// default; a diagnostic for the benchmark).  prof_begin/prof_end bracket one
+// launch; prof_flush, called after the stream has synchronised, adds the
+// elapsed times to per-name totals.
+bool prof_on();
+void prof_begin(const char *name, hipStream_t st);
+void prof_end(hipStream_t st);
+void prof_flush();
+// Adds the algorithmic bytes of one launch of a stage to its total.
+void prof_bytes(const char *name, double bytes);
+}  // namespace ezsp

@@ -1,0 +1,364 @@
+// ezsp_knn.hip -- exact k-nearest-neighbour adjacency (Sec. 3.1: every point
+// linked to its k nearest neighbours; Sec. 4.1: k and unit weights).
+//
+// Grid build: each point gets a 48-bit Morton key of its 16-bit-per-axis
+// voxel in the bounding box; a radix sort lays the points out in Morton
+// order.  Consecutive runs of 32 sorted points form buckets, and an implicit
+// 8-ary tree of axis-aligned boxes sits over the buckets, so the voxel
+// hierarchy adapts to any density.
+//
+// Query: one wavefront per 64 consecutive sorted points.  Each lane keeps its
+// own sorted top-k of (d2, original index) in registers.  The wave scans its
+// own two buckets first, then walks the tree without a stack in Morton order
+// and enters a box whenever some lane's box distance does not exceed that
+// lane's current k-th distance; bucket points are broadcast lane to lane
+// with readlane.  The box distance is built from the same IEEE operations as
+// d2 and rounding is monotone, so it never exceeds the d2 of a point inside
+// the box: no neighbour, and no tie with a smaller index, can be skipped.
+#include "ezsp_internal.h"
+
+namespace ezsp {
+
+__global__ __launch_bounds__(256) void k_bbox(const float *xyz, int32_t n,
+                                              Ctl *ctl) {
+  float mn[3] = {INFINITY, INFINITY, INFINITY};
+  float mx[3] = {-INFINITY, -INFINITY, -INFINITY};
+  bool bad = false;
+  for (int32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < n;
+       i += gridDim.x * blockDim.x) {
+#pragma unroll
+    for (int a = 0; a < 3; ++a) {
+      float v = xyz[3 * (int64_t)i + a];
+      if (!isfinite(v)) {
+        bad = true;
+      } else {
+        mn[a] = fminf(mn[a], v);
+        mx[a] = fmaxf(mx[a], v);
+      }
+    }
+  }
+#pragma unroll
+  for (int a = 0; a < 3; ++a) {
+#pragma unroll
+    for (int off = kWave / 2; off > 0; off >>= 1) {
+      mn[a] = fminf(mn[a], __shfl_xor(mn[a], off, kWave));
+      mx[a] = fmaxf(mx[a], __shfl_xor(mx[a], off, kWave));
+    }
+  }
+  const bool lead = (threadIdx.x & (kWave - 1)) == 0;
+  if (lead) {
+#pragma unroll
+    for (int a = 0; a < 3; ++a) {
+      atomicMin(&ctl->bbox_enc[a], f2ord(mn[a]));
+      atomicMax(&ctl->bbox_enc[3 + a], f2ord(mx[a]));
+    }
+  }
+  if (__ballot(bad) && lead) raise_err(ctl, kErrNonFinite);
+}
+
+// 16 bits -> every third bit of 48.
+__device__ __forceinline__ uint64_t spread3(uint32_t v) {
+  uint64_t x = v & 0xffffu;
+  x = (x | (x << 16)) & 0x0000ff0000ffull;
+  x = (x | (x << 8)) & 0x00f00f00f00full;
+  x = (x | (x << 4)) & 0x0c30c30c30c3ull;
+  x = (x | (x << 2)) & 0x249249249249ull;
+  return x;
+}
+
+__global__ __launch_bounds__(256) void k_morton(const float *xyz, int32_t n,
+                                                const Ctl *ctl, uint64_t *keys,
+                                                uint32_t *vals) {
+  const int32_t i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  float lo[3], ext = 0.0f;
+#pragma unroll
+  for (int a = 0; a < 3; ++a) {
+    lo[a] = ord2f(ctl->bbox_enc[a]);
+    ext = fmaxf(ext, ord2f(ctl->bbox_enc[3 + a]) - lo[a]);
+  }
+  const float scale = (ext > 0.0f) ? 65535.0f / ext : 0.0f;
+  uint32_t q[3];
+#pragma unroll
+  for (int a = 0; a < 3; ++a) {
+    float t = (xyz[3 * (int64_t)i + a] - lo[a]) * scale;
+    t = fminf(fmaxf(t, 0.0f), 65535.0f);  // NaN maps to 0
+    q[a] = (uint32_t)t;
+  }
+  keys[i] = spread3(q[0]) | (spread3(q[1]) << 1) | (spread3(q[2]) << 2);
+  vals[i] = (uint32_t)i;
+}
+
+// Sorted points as float4 (x, y, z, original index bits) plus both maps.
+__global__ __launch_bounds__(256) void k_gather_points(
+    const float *xyz, int32_t n, const uint32_t *order, float4 *pts,
+    int32_t *perm, int32_t *inv, Ctl *ctl) {
+  const int32_t i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  const uint32_t o = order[i];
+  if (o >= (uint32_t)n) {
+    raise_err(ctl, kErrInternal);
+    return;
+  }
+  const float *p = xyz + 3 * (int64_t)o;
+  pts[i] = make_float4(p[0], p[1], p[2], __int_as_float((int32_t)o));
+  perm[i] = (int32_t)o;
+  inv[o] = i;
+}
+
+__global__ __launch_bounds__(256) void k_leaf_boxes(const float4 *pts,
+                                                    int32_t n, int32_t nb,
+                                                    float4 *blo, float4 *bhi) {
+  const int32_t b = blockIdx.x * blockDim.x + threadIdx.x;
+  if (b >= nb) return;
+  const int32_t s = b * kBucket;
+  const int32_t e = min(n, s + kBucket);
+  float4 lo = make_float4(INFINITY, INFINITY, INFINITY, 0.f);
+  float4 hi = make_float4(-INFINITY, -INFINITY, -INFINITY, 0.f);
+  for (int32_t i = s; i < e; ++i) {
+    float4 p = pts[i];
+    lo.x = fminf(lo.x, p.x);
+    lo.y = fminf(lo.y, p.y);
+    lo.z = fminf(lo.z, p.z);
+    hi.x = fmaxf(hi.x, p.x);
+    hi.y = fmaxf(hi.y, p.y);
+    hi.z = fmaxf(hi.z, p.z);
+  }
+  blo[b] = lo;
+  bhi[b] = hi;
+}
+
+__global__ __launch_bounds__(256) void k_up_boxes(float4 *blo, float4 *bhi,
+                                                  int32_t child_off,
+                                                  int32_t child_cnt,
+                                                  int32_t off, int32_t cnt) {
+  const int32_t j = blockIdx.x * blockDim.x + threadIdx.x;
+  if (j >= cnt) return;
+  const int32_t s = j * kFan;
+  const int32_t e = min(child_cnt, s + kFan);
+  float4 lo = make_float4(INFINITY, INFINITY, INFINITY, 0.f);
+  float4 hi = make_float4(-INFINITY, -INFINITY, -INFINITY, 0.f);
+  for (int32_t c = s; c < e; ++c) {
+    float4 a = blo[child_off + c], b = bhi[child_off + c];
+    lo.x = fminf(lo.x, a.x);
+    lo.y = fminf(lo.y, a.y);
+    lo.z = fminf(lo.z, a.z);
+    hi.x = fmaxf(hi.x, b.x);
+    hi.y = fmaxf(hi.y, b.y);
+    hi.z = fmaxf(hi.z, b.z);
+  }
+  blo[off + j] = lo;
+  bhi[off + j] = hi;
+}
+
+// (d, o) strictly before (bd, bo): smaller distance, ties to smaller index.
+__device__ __forceinline__ bool pair_lt(float d, int32_t o, float bd,
+                                        int32_t bo) {
+  return d < bd || (d == bd && o < bo);
+}
+
+// Insert into a sorted top-K whose last entry is known to lose to (d, o).
+template <int K>
+__device__ __forceinline__ void topk_insert(float (&bd)[K], int32_t (&bo)[K],
+                                            int32_t (&bp)[K], float d,
+                                            int32_t o, int32_t pos) {
+#pragma unroll
+  for (int t = K - 1; t > 0; --t) {
+    const bool before_prev = pair_lt(d, o, bd[t - 1], bo[t - 1]);
+    const bool before_cur = pair_lt(d, o, bd[t], bo[t]);
+    const float nd = before_prev ? bd[t - 1] : (before_cur ? d : bd[t]);
+    const int32_t no = before_prev ? bo[t - 1] : (before_cur ? o : bo[t]);
+    const int32_t np = before_prev ? bp[t - 1] : (before_cur ? pos : bp[t]);
+    bd[t] = nd;
+    bo[t] = no;
+    bp[t] = np;
+  }
+  if (pair_lt(d, o, bd[0], bo[0])) {
+    bd[0] = d;
+    bo[0] = o;
+    bp[0] = pos;
+  }
+}
+
+__device__ __forceinline__ float rl(float v, int j) {
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), j));
+}
+
+template <int K>
+__device__ __forceinline__ void scan_bucket(const float4 *__restrict__ pts,
+                                            int32_t n, int32_t b, int lane,
+                                            bool act, float px, float py,
+                                            float pz, int32_t me,
+                                            float (&bd)[K], int32_t (&bo)[K],
+                                            int32_t (&bp)[K]) {
+  const int32_t base = b * kBucket;
+  const int32_t cnt = min(kBucket, n - base);
+  float4 q = make_float4(0.f, 0.f, 0.f, 0.f);
+  if (lane < cnt) q = pts[base + lane];
+  for (int j = 0; j < cnt; ++j) {
+    const float qx = rl(q.x, j), qy = rl(q.y, j), qz = rl(q.z, j);
+    const int32_t qo = __builtin_amdgcn_readlane(__float_as_int(q.w), j);
+    // d2 = ((dx*dx) + (dy*dy)) + (dz*dz), dx = x_q - x_p, no contraction
+    const float dx = qx - px, dy = qy - py, dz = qz - pz;
+    const float xx = dx * dx, yy = dy * dy, zz = dz * dz;
+    const float d2 = (xx + yy) + zz;
+    if (act && qo != me && pair_lt(d2, qo, bd[K - 1], bo[K - 1]))
+      topk_insert<K>(bd, bo, bp, d2, qo, base + j);
+  }
+}
+
+template <int K>
+__global__ __launch_bounds__(256) void k_knn_query(
+    const float4 *__restrict__ pts, int32_t n, const float4 *__restrict__ blo,
+    const float4 *__restrict__ bhi, Tree tree, int32_t k,
+    int32_t *__restrict__ nbr_int, int32_t *__restrict__ nbr_out,
+    float *__restrict__ d2_out) {
+  const int lane = threadIdx.x & (kWave - 1);
+  const int32_t w = (int32_t)((blockIdx.x * blockDim.x + threadIdx.x) / kWave);
+  if ((int64_t)w * kWave >= n) return;  // whole wave past the end
+  const int32_t i = w * kWave + lane;
+  const bool act = i < n;
+  float4 p = act ? pts[i] : make_float4(0.f, 0.f, 0.f, 0.f);
+  const int32_t me = act ? __float_as_int(p.w) : -1;
+  float bd[K];
+  int32_t bo[K], bp[K];
+#pragma unroll
+  for (int t = 0; t < K; ++t) {
+    bd[t] = INFINITY;
+    bo[t] = INT32_MAX;
+    bp[t] = -1;
+  }
+  const int32_t nb0 = tree.cnt[0];
+  const int32_t own0 = w * (kWave / kBucket);
+  const int32_t own1 = own0 + 1;
+  scan_bucket<K>(pts, n, own0, lane, act, p.x, p.y, p.z, me, bd, bo, bp);
+  if (own1 < nb0)
+    scan_bucket<K>(pts, n, own1, lane, act, p.x, p.y, p.z, me, bd, bo, bp);
+
+  int level = tree.top;
+  int32_t idx = 0;
+  for (;;) {
+    const int32_t j = tree.off[level] + idx;
+    const float4 lo = blo[j], hi = bhi[j];
+    const float ex = p.x < lo.x ? lo.x - p.x : (p.x > hi.x ? p.x - hi.x : 0.f);
+    const float ey = p.y < lo.y ? lo.y - p.y : (p.y > hi.y ? p.y - hi.y : 0.f);
+    const float ez = p.z < lo.z ? lo.z - p.z : (p.z > hi.z ? p.z - hi.z : 0.f);
+    const float bx = ex * ex, by = ey * ey, bz = ez * ez;
+    const float d2b = (bx + by) + bz;
+    const bool need = act && d2b <= bd[K - 1];
+    if (__ballot(need)) {
+      if (level > 0) {
+        --level;
+        idx *= kFan;
+        continue;
+      }
+      if (idx != own0 && idx != own1)
+        scan_bucket<K>(pts, n, idx, lane, act, p.x, p.y, p.z, me, bd, bo, bp);
+    }
+    // next box in Morton order: a later sibling, else climb
+    bool done = false;
+    for (;;) {
+      if (level == tree.top) {
+        done = true;
+        break;
+      }
+      if ((idx % kFan) != kFan - 1 && idx + 1 < tree.cnt[level]) {
+        ++idx;
+        break;
+      }
+      ++level;
+      idx /= kFan;
+    }
+    if (done) break;
+  }
+
+  if (!act) return;
+#pragma unroll
+  for (int t = 0; t < K; ++t) {
+    if (t < k) {
+      nbr_int[(int64_t)i * k + t] = bp[t];
+      if (nbr_out)
+        nbr_out[(int64_t)me * k + t] = (bp[t] < 0) ? -1 : bo[t];
+      if (d2_out) d2_out[(int64_t)me * k + t] = bd[t];
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// host side
+// ---------------------------------------------------------------------------
+static int knn_template_k(int32_t k) {
+  static const int ks[] = {4, 8, 10, 16, 32, 64};
+  for (int v : ks)
+    if (k <= v) return v;
+  return -1;
+}
+
+void knn_reserve(Arena &a, int32_t n, int32_t k, KnnWork *w) {
+  const Tree t = make_tree(n);
+  w->perm = a.take<int32_t>(n);
+  w->inv = a.take<int32_t>(n);
+  w->nbr_int = a.take<int32_t>((size_t)n * k);
+  w->keys = a.take<uint64_t>(n);
+  w->keys2 = a.take<uint64_t>(n);
+  w->vals = a.take<uint32_t>(n);
+  w->vals2 = a.take<uint32_t>(n);
+  w->pts = a.take<float4>(n);
+  w->blo = a.take<float4>(t.total);
+  w->bhi = a.take<float4>(t.total);
+  w->hist = a.take<int32_t>(radix_hist_ints(n));
+  w->bsum = a.take<int32_t>(scan_blocks(radix_hist_ints(n)) + 1);
+  w->total = a.take<int32_t>(4);
+}
+
+hipError_t knn_launch(const float *xyz, int32_t n, int32_t k, Ctl *ctl,
+                      const KnnWork &s, int32_t *nbr_out, float *d2_out,
+                      hipStream_t st) {
+  const KnnWork &w = s;
+  const Tree tree = make_tree(n);
+  const int nt = 256;
+  const int gb = (n + nt - 1) / nt;
+  hipLaunchKernelGGL(k_bbox, dim3(min(gb, 1024)), dim3(nt), 0, st, xyz, n,
+                     ctl);
+  hipLaunchKernelGGL(k_morton, dim3(gb), dim3(nt), 0, st, xyz, n, ctl, s.keys,
+                     s.vals);
+  prof_begin("morton_sort", st);
+  const bool alt = radix_sort_pairs(s.keys, s.vals, s.keys2, s.vals2, n, 48,
+                                    s.hist, s.bsum, s.total, ctl, st);
+  prof_end(st);
+  const uint32_t *order = alt ? s.vals2 : s.vals;
+  hipLaunchKernelGGL(k_gather_points, dim3(gb), dim3(nt), 0, st, xyz, n, order,
+                     s.pts, w.perm, w.inv, ctl);
+  hipLaunchKernelGGL(k_leaf_boxes, dim3((tree.cnt[0] + nt - 1) / nt), dim3(nt),
+                     0, st, s.pts, n, tree.cnt[0], s.blo, s.bhi);
+  for (int l = 1; l <= tree.top; ++l)
+    hipLaunchKernelGGL(k_up_boxes, dim3((tree.cnt[l] + nt - 1) / nt), dim3(nt),
+                       0, st, s.blo, s.bhi, tree.off[l - 1], tree.cnt[l - 1],
+                       tree.off[l], tree.cnt[l]);
+  const int64_t waves = ((int64_t)n + kWave - 1) / kWave;
+  const dim3 grid((unsigned)((waves * kWave + nt - 1) / nt));
+  prof_begin("knn_query", st);
+  switch (knn_template_k(k)) {
+#define EZSP_KNN_CASE(KK)                                                    \
+  case KK:                                                                   \
+    hipLaunchKernelGGL(k_knn_query<KK>, grid, dim3(nt), 0, st, s.pts, n,     \
+                       s.blo, s.bhi, tree, k, w.nbr_int, nbr_out, d2_out);   \
+    break;
+    EZSP_KNN_CASE(4)
+    EZSP_KNN_CASE(8)
+    EZSP_KNN_CASE(10)
+    EZSP_KNN_CASE(16)
+    EZSP_KNN_CASE(32)
+    EZSP_KNN_CASE(64)
+#undef EZSP_KNN_CASE
+    default:
+      prof_end(st);
+      return hipErrorInvalidValue;
+  }
+  prof_end(st);
+  // algorithmic bytes: read xyz, write the n*k neighbour table
+  prof_bytes("knn_query", (12.0 + 4.0 * k) * n);
+  return hipGetLastError();
+}
+
+}  // namespace ezsp

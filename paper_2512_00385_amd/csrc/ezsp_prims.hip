@@ -1,0 +1,373 @@
+// ezsp_prims.hip -- device-wide scan tail, LSD radix sort, control block and
+// fixed-point shift kernels, and the host helpers shared by the launchers.
+#include <stdarg.h>
+#include <mutex>
+#include <string>
+#include <unordered_map>
+#include <vector>
+#include <stdio.h>
+#include <string.h>
+
+#include "ezsp_internal.h"
+
+namespace ezsp {
+
+// ---------------------------------------------------------------------------
+// scan of the per-block sums: one block of 1024 threads walks the array in
+// chunks of 4096 with a running carry.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(1024) void k_scan_bsums(int32_t *bsum, int32_t nb,
+                                                     int32_t *total) {
+  __shared__ int32_t wsum[1024 / kWave];
+  constexpr int kPer = 4;
+  int32_t carry = 0;
+  for (int32_t c0 = 0; c0 < nb; c0 += 1024 * kPer) {
+    int32_t v[kPer];
+    int32_t s = 0;
+    const int32_t base = c0 + threadIdx.x * kPer;
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) {
+      int32_t i = base + j;
+      v[j] = (i < nb) ? bsum[i] : 0;
+      s += v[j];
+    }
+    int32_t tot;
+    int32_t run = carry + block_excl_scan<1024>(s, wsum, &tot);
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) {
+      int32_t i = base + j;
+      if (i < nb) bsum[i] = run;
+      run += v[j];
+    }
+    carry += tot;
+  }
+  if (threadIdx.x == 0) *total = carry;
+}
+
+// ---------------------------------------------------------------------------
+// LSD radix sort, 8-bit digits.  Tile of kSortTile keys per block; inside a
+// tile, key j*256 + t is handled by thread t at step j, so (step, thread)
+// order is the input order and the per-step ranking keeps the sort stable.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(kSortNT) void k_rs_hist(const uint64_t *keys,
+                                                     int32_t n, int shift,
+                                                     int32_t *hist, int32_t nb) {
+  __shared__ int32_t h[kSortBins];
+  for (int d = threadIdx.x; d < kSortBins; d += kSortNT) h[d] = 0;
+  __syncthreads();
+  const int32_t base = blockIdx.x * kSortTile;
+#pragma unroll 4
+  for (int j = 0; j < kSortItems; ++j) {
+    int32_t i = base + j * kSortNT + threadIdx.x;
+    if (i < n) atomicAdd(&h[(keys[i] >> shift) & (kSortBins - 1)], 1);
+  }
+  __syncthreads();
+  for (int d = threadIdx.x; d < kSortBins; d += kSortNT)
+    hist[d * nb + blockIdx.x] = h[d];
+}
+
+__global__ __launch_bounds__(kSortNT) void k_rs_scatter(
+    const uint64_t *__restrict__ kin, const uint32_t *__restrict__ vin,
+    uint64_t *__restrict__ kout, uint32_t *__restrict__ vout, int32_t n,
+    int shift, const int32_t *__restrict__ offs, int32_t nb, Ctl *ctl) {
+  constexpr int kW = kSortNT / kWave;
+  __shared__ int32_t run[kSortBins];
+  __shared__ int32_t wc[kW][kSortBins];
+  const int lane = threadIdx.x & (kWave - 1);
+  const int wid = threadIdx.x / kWave;
+  for (int d = threadIdx.x; d < kSortBins; d += kSortNT)
+    run[d] = offs[d * nb + blockIdx.x];
+  const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (kWave - lane));
+  const int32_t base = blockIdx.x * kSortTile;
+  for (int j = 0; j < kSortItems; ++j) {
+    for (int t = threadIdx.x; t < kW * kSortBins; t += kSortNT)
+      (&wc[0][0])[t] = 0;
+    __syncthreads();
+    const int32_t i = base + j * kSortNT + threadIdx.x;
+    const bool valid = i < n;
+    const uint64_t key = valid ? kin[i] : 0ull;
+    const uint32_t val = valid ? vin[i] : 0u;
+    const int dig = (int)((key >> shift) & (kSortBins - 1));
+    uint64_t peers = __ballot(valid);
+#pragma unroll
+    for (int b = 0; b < 8; ++b) {
+      const int bit = (dig >> b) & 1;
+      const uint64_t bal = __ballot(bit);
+      peers &= bit ? bal : ~bal;
+    }
+    const int rank = __popcll(peers & lt_mask);
+    if (valid && rank == 0) wc[wid][dig] = __popcll(peers);
+    __syncthreads();
+    for (int d = threadIdx.x; d < kSortBins; d += kSortNT) {
+      int32_t p = run[d];
+#pragma unroll
+      for (int w = 0; w < kW; ++w) {
+        int32_t c = wc[w][d];
+        wc[w][d] = p;
+        p += c;
+      }
+      run[d] = p;
+    }
+    __syncthreads();
+    if (valid) {
+      const int32_t pos = wc[wid][dig] + rank;
+      if ((uint32_t)pos < (uint32_t)n) {
+        kout[pos] = key;
+        vout[pos] = val;
+      } else {
+        raise_err(ctl, kErrInternal);
+      }
+    }
+    __syncthreads();
+  }
+}
+
+size_t radix_hist_ints(int32_t n) {
+  return (size_t)kSortBins * (size_t)sort_blocks(n);
+}
+
+bool radix_sort_pairs(uint64_t *keys, uint32_t *vals, uint64_t *keys_alt,
+                      uint32_t *vals_alt, int32_t n, int nbits,
+                      int32_t *hist, int32_t *bsum, int32_t *total, Ctl *ctl,
+                      hipStream_t st) {
+  if (n <= 1) return false;
+  const int32_t nb = sort_blocks(n);
+  uint64_t *kin = keys, *kout = keys_alt;
+  uint32_t *vin = vals, *vout = vals_alt;
+  bool flip = false;
+  for (int shift = 0; shift < nbits; shift += 8) {
+    hipLaunchKernelGGL(k_rs_hist, dim3(nb), dim3(kSortNT), 0, st, kin, n,
+                       shift, hist, nb);
+    const int32_t nh = kSortBins * nb;
+    device_scan(ScanArray{hist, hist, nh, nullptr}, nh, bsum, total, st);
+    hipLaunchKernelGGL(k_rs_scatter, dim3(nb), dim3(kSortNT), 0, st, kin, vin,
+                       kout, vout, n, shift, hist, nb, ctl);
+    uint64_t *tk = kin;
+    kin = kout;
+    kout = tk;
+    uint32_t *tv = vin;
+    vin = vout;
+    vout = tv;
+    flip = !flip;
+  }
+  return flip;
+}
+
+// ---------------------------------------------------------------------------
+// control block, max |v| and the fixed-point shift
+// ---------------------------------------------------------------------------
+__global__ void k_ctl_init(Ctl *ctl) {
+  if (threadIdx.x == 0 && blockIdx.x == 0) {
+    ctl->err = 0;
+    ctl->F = 0;
+    ctl->any_choice = 0;
+    ctl->n_next = 0;
+    ctl->e_next = 0;
+    ctl->slots = 0;
+    ctl->maxabs_bits = 0;
+    ctl->pad0 = 0;
+    for (int a = 0; a < 3; ++a) {
+      ctl->bbox_enc[a] = f2ord(INFINITY);
+      ctl->bbox_enc[3 + a] = f2ord(-INFINITY);
+    }
+    ctl->pad1[0] = ctl->pad1[1] = 0;
+    ctl->cut_w2 = 0;
+    ctl->fid_total = 0.0;
+  }
+}
+
+__global__ __launch_bounds__(256) void k_maxabs(const float *v, int64_t count,
+                                                Ctl *ctl) {
+  uint32_t m = 0;
+  bool bad = false;
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < count;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    float x = v[i];
+    if (!isfinite(x)) bad = true;
+    else m = max(m, __float_as_uint(fabsf(x)));
+  }
+#pragma unroll
+  for (int off = kWave / 2; off > 0; off >>= 1)
+    m = max(m, (uint32_t)__shfl_xor((int)m, off, kWave));
+  if ((threadIdx.x & (kWave - 1)) == 0) atomicMax(&ctl->maxabs_bits, m);
+  if (__ballot(bad) && (threadIdx.x & (kWave - 1)) == 0)
+    raise_err(ctl, kErrNonFinite);
+}
+
+// F = min(40, 61 - ceil(log2 n) - max(0, ceil(log2 A))), A = max |e|.
+__global__ void k_fixshift(Ctl *ctl, int32_t n) {
+  if (threadIdx.x != 0 || blockIdx.x != 0) return;
+  const float A = __uint_as_float(ctl->maxabs_bits);
+  int cn = 0;
+  while (((int64_t)1 << cn) < (int64_t)n) ++cn;
+  int ca = 0;
+  if (A > 0.0f) {
+    int e;
+    float m = frexpf(A, &e);  // A = m * 2^e, m in [0.5, 1)
+    ca = (m == 0.5f) ? e - 1 : e;
+    if (ca < 0) ca = 0;
+  }
+  int F = 61 - cn - ca;
+  if (F > 40) F = 40;
+  ctl->F = F;
+  if (F < 16) raise_err(ctl, kErrRange);
+}
+
+// ---------------------------------------------------------------------------
+// host helpers
+// ---------------------------------------------------------------------------
+static thread_local char g_msg[512];
+
+void set_error(const char *fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_msg, sizeof(g_msg), fmt, ap);
+  va_end(ap);
+}
+
+const char *last_error_text() { return g_msg; }
+
+int check_hip(hipError_t e, const char *what) {
+  if (e == hipSuccess) return 0;
+  set_error("%s: %s", what, hipGetErrorString(e));
+  return -5;  // EZSP_ERR_DEVICE
+}
+
+Ctl *pinned_ctl() {
+  static thread_local Ctl *p = nullptr;
+  if (!p) {
+    void *q = nullptr;
+    if (hipHostMalloc(&q, sizeof(Ctl), hipHostMallocDefault) != hipSuccess)
+      return nullptr;
+    p = static_cast<Ctl *>(q);
+  }
+  return p;
+}
+
+// ---------------------------------------------------------------------------
+// per-kernel event timing (diagnostic)
+// ---------------------------------------------------------------------------
+namespace {
+struct ProfRec {
+  const char *name;
+  hipEvent_t a, b;
+};
+struct ProfTotal {
+  int64_t launches = 0;
+  double ms = 0.0;
+  double bytes = 0.0;
+};
+std::mutex g_prof_mu;
+bool g_prof = false;
+std::vector<hipEvent_t> g_pool;
+std::vector<ProfRec> g_pending;
+std::unordered_map<std::string, ProfTotal> g_totals;
+
+hipEvent_t pool_get() {
+  if (!g_pool.empty()) {
+    hipEvent_t e = g_pool.back();
+    g_pool.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+}  // namespace
+
+bool prof_on() { return g_prof; }
+
+void prof_begin(const char *name, hipStream_t st) {
+  if (!g_prof) return;
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  ProfRec r{name, pool_get(), pool_get()};
+  if (!r.a || !r.b) return;
+  hipEventRecord(r.a, st);
+  g_pending.push_back(r);
+}
+
+void prof_end(hipStream_t st) {
+  if (!g_prof) return;
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  if (!g_pending.empty()) hipEventRecord(g_pending.back().b, st);
+}
+
+void prof_flush() {
+  if (!g_prof) return;
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  for (const ProfRec &r : g_pending) {
+    float ms = 0.0f;
+    if (hipEventSynchronize(r.b) == hipSuccess &&
+        hipEventElapsedTime(&ms, r.a, r.b) == hipSuccess) {
+      ProfTotal &t = g_totals[r.name];
+      t.launches += 1;
+      t.ms += ms;
+    }
+    g_pool.push_back(r.a);
+    g_pool.push_back(r.b);
+  }
+  g_pending.clear();
+}
+
+void prof_bytes(const char *name, double bytes) {
+  if (!g_prof) return;
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  g_totals[name].bytes += bytes;
+}
+
+int prof_enable(int on) {
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  g_prof = on != 0;
+  g_totals.clear();
+  g_pending.clear();
+  return 0;
+}
+
+int prof_read(const char *name, int64_t *launches, double *ms,
+              double *bytes) {
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  auto it = g_totals.find(name ? name : "");
+  if (it == g_totals.end()) {
+    if (launches) *launches = 0;
+    if (ms) *ms = 0.0;
+    if (bytes) *bytes = 0.0;
+    return -1;
+  }
+  if (launches) *launches = it->second.launches;
+  if (ms) *ms = it->second.ms;
+  if (bytes) *bytes = it->second.bytes;
+  return 0;
+}
+
+int read_ctl(Ctl *ctl, Ctl *host, hipStream_t st) {
+  int rc = check_hip(hipGetLastError(), "kernel launch");
+  if (rc) return rc;
+  rc = check_hip(hipMemcpyAsync(host, ctl, sizeof(Ctl), hipMemcpyDeviceToHost,
+                                st),
+                 "hipMemcpyAsync(ctl)");
+  if (rc) return rc;
+  rc = check_hip(hipStreamSynchronize(st), "hipStreamSynchronize");
+  prof_flush();
+  return rc;
+}
+
+Tree make_tree(int32_t n) {
+  Tree t;
+  memset(&t, 0, sizeof(t));
+  int32_t cnt = (n + kBucket - 1) / kBucket;
+  int32_t off = 0;
+  int l = 0;
+  for (;;) {
+    t.off[l] = off;
+    t.cnt[l] = cnt;
+    off += cnt;
+    if (cnt <= 1 || l + 1 >= kMaxTreeLevels) break;
+    cnt = (cnt + kFan - 1) / kFan;
+    ++l;
+  }
+  t.top = l;
+  t.total = off;
+  return t;
+}
+
+}  // namespace ezsp
