@@ -10,6 +10,21 @@
 
 namespace ezsp {
 
+// XCD-aware block order.  Workgroups are dispatched round-robin over the 8
+// XCDs (each with its own L2), so physical block b runs on XCD b % 8.  The
+// grid is rounded up to a multiple of 8 and block b takes logical block
+// (b % 8) * (grid / 8) + b / 8: each XCD works on one contiguous range of
+// logical blocks, and neighbouring data stays in one L2.
+constexpr int kXcd = 8;
+inline unsigned xcd_grid(int64_t logical_blocks) {
+  int64_t g = (logical_blocks + kXcd - 1) / kXcd * kXcd;
+  return (unsigned)(g < kXcd ? kXcd : g);
+}
+__device__ __forceinline__ int32_t xcd_block() {
+  const int32_t per = (int32_t)(gridDim.x / kXcd);
+  return (int32_t)(blockIdx.x % kXcd) * per + (int32_t)(blockIdx.x / kXcd);
+}
+
 // Bump allocator over the caller's workspace.  With base == nullptr it only
 // measures: every take() returns nullptr and `off` ends at the bytes needed.
 struct Arena {
@@ -27,8 +42,9 @@ struct Arena {
 
 // Implicit 8-ary tree of boxes over the Morton-ordered points: level 0 holds
 // one box per bucket of kBucket consecutive points, level l+1 one box per 8
-// boxes of level l, up to a single root at level `top`.
-constexpr int kBucket = 32;
+// boxes of level l, up to a single root at level `top`.  A bucket is also
+// the query group of the kNN kernel: 16 lanes, one DPP row.
+constexpr int kBucket = 16;
 constexpr int kFan = 8;
 constexpr int kMaxTreeLevels = 16;
 struct Tree {

@@ -180,13 +180,52 @@ __device__ __forceinline__ void topk_insert(float (&bd)[K], int32_t (&bo)[K],
   }
 }
 
-__device__ __forceinline__ float rl(float v, int j) {
-  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), j));
+// Broadcast lane J of every 16-lane row (one DPP row = one query group).
+template <int J>
+__device__ __forceinline__ float row_bcast(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(
+      0, __float_as_int(v), 0x150 + J, 0xF, 0xF, false));
+}
+template <int J>
+__device__ __forceinline__ int32_t row_bcast_i(int32_t v) {
+  return __builtin_amdgcn_update_dpp(0, v, 0x150 + J, 0xF, 0xF, false);
 }
 
+// Candidate J of the bucket held one point per lane in (q, qo): d2 in the
+// fixed order ((dx*dx) + (dy*dy)) + (dz*dz), dx = x_q - x_p.
+template <int K, int J>
+struct BucketStep {
+  __device__ __forceinline__ static void run(const float4 &q, int32_t base,
+                                             int32_t cnt, bool act,
+                                             float px, float py, float pz,
+                                             int32_t me, float (&bd)[K],
+                                             int32_t (&bo)[K],
+                                             int32_t (&bp)[K]) {
+    if (J < cnt) {
+      const float dx = row_bcast<J>(q.x) - px;
+      const float dy = row_bcast<J>(q.y) - py;
+      const float dz = row_bcast<J>(q.z) - pz;
+      const int32_t qo = row_bcast_i<J>(__float_as_int(q.w));
+      const float xx = dx * dx, yy = dy * dy, zz = dz * dz;
+      const float d2 = (xx + yy) + zz;
+      if (act && qo != me && pair_lt(d2, qo, bd[K - 1], bo[K - 1]))
+        topk_insert<K>(bd, bo, bp, d2, qo, base + J);
+      BucketStep<K, J + 1>::run(q, base, cnt, act, px, py, pz, me, bd, bo, bp);
+    }
+  }
+};
+template <int K>
+struct BucketStep<K, kBucket> {
+  __device__ __forceinline__ static void run(const float4 &, int32_t, int32_t,
+                                             bool, float, float, float,
+                                             int32_t, float (&)[K],
+                                             int32_t (&)[K], int32_t (&)[K]) {}
+};
+
+// All 16 lanes of a group scan bucket b together (group-uniform call).
 template <int K>
 __device__ __forceinline__ void scan_bucket(const float4 *__restrict__ pts,
-                                            int32_t n, int32_t b, int lane,
+                                            int32_t n, int32_t b, int lane16,
                                             bool act, float px, float py,
                                             float pz, int32_t me,
                                             float (&bd)[K], int32_t (&bo)[K],
@@ -194,31 +233,30 @@ __device__ __forceinline__ void scan_bucket(const float4 *__restrict__ pts,
   const int32_t base = b * kBucket;
   const int32_t cnt = min(kBucket, n - base);
   float4 q = make_float4(0.f, 0.f, 0.f, 0.f);
-  if (lane < cnt) q = pts[base + lane];
-  for (int j = 0; j < cnt; ++j) {
-    const float qx = rl(q.x, j), qy = rl(q.y, j), qz = rl(q.z, j);
-    const int32_t qo = __builtin_amdgcn_readlane(__float_as_int(q.w), j);
-    // d2 = ((dx*dx) + (dy*dy)) + (dz*dz), dx = x_q - x_p, no contraction
-    const float dx = qx - px, dy = qy - py, dz = qz - pz;
-    const float xx = dx * dx, yy = dy * dy, zz = dz * dz;
-    const float d2 = (xx + yy) + zz;
-    if (act && qo != me && pair_lt(d2, qo, bd[K - 1], bo[K - 1]))
-      topk_insert<K>(bd, bo, bp, d2, qo, base + j);
-  }
+  if (lane16 < cnt) q = pts[base + lane16];
+  BucketStep<K, 0>::run(q, base, cnt, act, px, py, pz, me, bd, bo, bp);
 }
 
+// One query group = 16 lanes = the 16 points of one bucket.  Every group
+// walks the tree on its own (group-uniform decisions from a 16-lane vote);
+// the four groups of a wave alternate between finding their next bucket and
+// scanning it together.
 template <int K>
 __global__ __launch_bounds__(256) void k_knn_query(
     const float4 *__restrict__ pts, int32_t n, const float4 *__restrict__ blo,
     const float4 *__restrict__ bhi, Tree tree, int32_t k,
     int32_t *__restrict__ nbr_int, int32_t *__restrict__ nbr_out,
-    float *__restrict__ d2_out) {
-  const int lane = threadIdx.x & (kWave - 1);
-  const int32_t w = (int32_t)((blockIdx.x * blockDim.x + threadIdx.x) / kWave);
-  if ((int64_t)w * kWave >= n) return;  // whole wave past the end
-  const int32_t i = w * kWave + lane;
+    float *__restrict__ d2_out, int32_t n_blocks) {
+  const int32_t lb = xcd_block();
+  if (lb >= n_blocks) return;
+  const int lane16 = threadIdx.x & (kBucket - 1);
+  const int gshift = threadIdx.x & (kWave - kBucket);  // 0, 16, 32, 48
+  const int32_t nb0 = tree.cnt[0];
+  const int32_t grp = lb * (256 / kBucket) + (int32_t)(threadIdx.x / kBucket);
+  if (grp >= nb0) return;  // whole group past the end
+  const int32_t i = grp * kBucket + lane16;
   const bool act = i < n;
-  float4 p = act ? pts[i] : make_float4(0.f, 0.f, 0.f, 0.f);
+  const float4 p = act ? pts[i] : make_float4(0.f, 0.f, 0.f, 0.f);
   const int32_t me = act ? __float_as_int(p.w) : -1;
   float bd[K];
   int32_t bo[K], bp[K];
@@ -228,48 +266,58 @@ __global__ __launch_bounds__(256) void k_knn_query(
     bo[t] = INT32_MAX;
     bp[t] = -1;
   }
-  const int32_t nb0 = tree.cnt[0];
-  const int32_t own0 = w * (kWave / kBucket);
-  const int32_t own1 = own0 + 1;
-  scan_bucket<K>(pts, n, own0, lane, act, p.x, p.y, p.z, me, bd, bo, bp);
-  if (own1 < nb0)
-    scan_bucket<K>(pts, n, own1, lane, act, p.x, p.y, p.z, me, bd, bo, bp);
+  // own bucket and its Morton neighbours first: a tight k-th distance early
+  scan_bucket<K>(pts, n, grp, lane16, act, p.x, p.y, p.z, me, bd, bo, bp);
+  if (grp > 0)
+    scan_bucket<K>(pts, n, grp - 1, lane16, act, p.x, p.y, p.z, me, bd, bo,
+                   bp);
+  if (grp + 1 < nb0)
+    scan_bucket<K>(pts, n, grp + 1, lane16, act, p.x, p.y, p.z, me, bd, bo,
+                   bp);
 
   int level = tree.top;
   int32_t idx = 0;
+  bool done = false;
   for (;;) {
-    const int32_t j = tree.off[level] + idx;
-    const float4 lo = blo[j], hi = bhi[j];
-    const float ex = p.x < lo.x ? lo.x - p.x : (p.x > hi.x ? p.x - hi.x : 0.f);
-    const float ey = p.y < lo.y ? lo.y - p.y : (p.y > hi.y ? p.y - hi.y : 0.f);
-    const float ez = p.z < lo.z ? lo.z - p.z : (p.z > hi.z ? p.z - hi.z : 0.f);
-    const float bx = ex * ex, by = ey * ey, bz = ez * ez;
-    const float d2b = (bx + by) + bz;
-    const bool need = act && d2b <= bd[K - 1];
-    if (__ballot(need)) {
-      if (level > 0) {
+    int32_t leaf = -1;
+    while (!done) {
+      const int32_t j = tree.off[level] + idx;
+      const float4 lo = blo[j], hi = bhi[j];
+      const float ex =
+          p.x < lo.x ? lo.x - p.x : (p.x > hi.x ? p.x - hi.x : 0.f);
+      const float ey =
+          p.y < lo.y ? lo.y - p.y : (p.y > hi.y ? p.y - hi.y : 0.f);
+      const float ez =
+          p.z < lo.z ? lo.z - p.z : (p.z > hi.z ? p.z - hi.z : 0.f);
+      const float bx = ex * ex, by = ey * ey, bz = ez * ez;
+      const float d2b = (bx + by) + bz;
+      const bool need = act && d2b <= bd[K - 1];
+      const bool any = ((__ballot(need) >> gshift) & 0xffffull) != 0;
+      if (any && level > 0) {
         --level;
         idx *= kFan;
         continue;
       }
-      if (idx != own0 && idx != own1)
-        scan_bucket<K>(pts, n, idx, lane, act, p.x, p.y, p.z, me, bd, bo, bp);
-    }
-    // next box in Morton order: a later sibling, else climb
-    bool done = false;
-    for (;;) {
-      if (level == tree.top) {
-        done = true;
-        break;
+      if (any && (idx < grp - 1 || idx > grp + 1)) leaf = idx;
+      // next box in Morton order: a later sibling, else climb
+      for (;;) {
+        if (level == tree.top) {
+          done = true;
+          break;
+        }
+        if ((idx % kFan) != kFan - 1 && idx + 1 < tree.cnt[level]) {
+          ++idx;
+          break;
+        }
+        ++level;
+        idx /= kFan;
       }
-      if ((idx % kFan) != kFan - 1 && idx + 1 < tree.cnt[level]) {
-        ++idx;
-        break;
-      }
-      ++level;
-      idx /= kFan;
+      if (leaf >= 0) break;
     }
-    if (done) break;
+    if (__ballot(leaf >= 0) == 0) break;
+    if (leaf >= 0)
+      scan_bucket<K>(pts, n, leaf, lane16, act, p.x, p.y, p.z, me, bd, bo,
+                     bp);
   }
 
   if (!act) return;
@@ -335,14 +383,15 @@ hipError_t knn_launch(const float *xyz, int32_t n, int32_t k, Ctl *ctl,
     hipLaunchKernelGGL(k_up_boxes, dim3((tree.cnt[l] + nt - 1) / nt), dim3(nt),
                        0, st, s.blo, s.bhi, tree.off[l - 1], tree.cnt[l - 1],
                        tree.off[l], tree.cnt[l]);
-  const int64_t waves = ((int64_t)n + kWave - 1) / kWave;
-  const dim3 grid((unsigned)((waves * kWave + nt - 1) / nt));
+  const int32_t qblocks = (tree.cnt[0] + (nt / kBucket) - 1) / (nt / kBucket);
+  const dim3 grid(xcd_grid(qblocks));
   prof_begin("knn_query", st);
   switch (knn_template_k(k)) {
 #define EZSP_KNN_CASE(KK)                                                    \
   case KK:                                                                   \
     hipLaunchKernelGGL(k_knn_query<KK>, grid, dim3(nt), 0, st, s.pts, n,     \
-                       s.blo, s.bhi, tree, k, w.nbr_int, nbr_out, d2_out);   \
+                       s.blo, s.bhi, tree, k, w.nbr_int, nbr_out, d2_out,    \
+                       qblocks);                                             \
     break;
     EZSP_KNN_CASE(4)
     EZSP_KNN_CASE(8)
