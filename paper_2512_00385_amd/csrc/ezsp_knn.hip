@@ -151,33 +151,25 @@ __global__ __launch_bounds__(256) void k_up_boxes(float4 *blo, float4 *bhi,
   bhi[off + j] = hi;
 }
 
-// (d, o) strictly before (bd, bo): smaller distance, ties to smaller index.
-__device__ __forceinline__ bool pair_lt(float d, int32_t o, float bd,
-                                        int32_t bo) {
-  return d < bd || (d == bd && o < bo);
+// A candidate is the 64-bit key (fp32 bits of d2) << 32 | original index.
+// d2 >= 0, so the bits of d2 are ordered like d2 and the key order is the
+// order (d2, index).  An empty slot holds ~0.
+constexpr uint64_t kNoKey = ~0ull;
+
+__device__ __forceinline__ uint64_t cand_key(float d2, int32_t o) {
+  return ((uint64_t)__float_as_uint(d2) << 32) | (uint32_t)o;
 }
 
-// Insert into a sorted top-K whose last entry is known to lose to (d, o).
+// Insert nk into the sorted top-K; nk is known to beat the last entry.
 template <int K>
-__device__ __forceinline__ void topk_insert(float (&bd)[K], int32_t (&bo)[K],
-                                            int32_t (&bp)[K], float d,
-                                            int32_t o, int32_t pos) {
+__device__ __forceinline__ void topk_insert(uint64_t (&key)[K], uint64_t nk) {
 #pragma unroll
   for (int t = K - 1; t > 0; --t) {
-    const bool before_prev = pair_lt(d, o, bd[t - 1], bo[t - 1]);
-    const bool before_cur = pair_lt(d, o, bd[t], bo[t]);
-    const float nd = before_prev ? bd[t - 1] : (before_cur ? d : bd[t]);
-    const int32_t no = before_prev ? bo[t - 1] : (before_cur ? o : bo[t]);
-    const int32_t np = before_prev ? bp[t - 1] : (before_cur ? pos : bp[t]);
-    bd[t] = nd;
-    bo[t] = no;
-    bp[t] = np;
+    const bool before_prev = nk < key[t - 1];
+    const uint64_t cur = (nk < key[t]) ? nk : key[t];
+    key[t] = before_prev ? key[t - 1] : cur;
   }
-  if (pair_lt(d, o, bd[0], bo[0])) {
-    bd[0] = d;
-    bo[0] = o;
-    bp[0] = pos;
-  }
+  key[0] = (nk < key[0]) ? nk : key[0];
 }
 
 // Broadcast lane J of every 16-lane row (one DPP row = one query group).
@@ -191,62 +183,66 @@ __device__ __forceinline__ int32_t row_bcast_i(int32_t v) {
   return __builtin_amdgcn_update_dpp(0, v, 0x150 + J, 0xF, 0xF, false);
 }
 
-// Candidate J of the bucket held one point per lane in (q, qo): d2 in the
-// fixed order ((dx*dx) + (dy*dy)) + (dz*dz), dx = x_q - x_p.
+// Key of candidate J of the bucket held one point per lane in q: d2 in the
+// fixed order ((dx*dx) + (dy*dy)) + (dz*dz), dx = x_q - x_p; the query
+// itself and lanes past the bucket's end give kNoKey.
+template <int J>
+__device__ __forceinline__ uint64_t bucket_key(const float4 &q, float px,
+                                               float py, float pz, int32_t me,
+                                               int32_t cnt) {
+  const float dx = row_bcast<J>(q.x) - px;
+  const float dy = row_bcast<J>(q.y) - py;
+  const float dz = row_bcast<J>(q.z) - pz;
+  const int32_t qo = row_bcast_i<J>(__float_as_int(q.w));
+  const float xx = dx * dx, yy = dy * dy, zz = dz * dz;
+  const float d2 = (xx + yy) + zz;
+  return (J < cnt && qo != me) ? cand_key(d2, qo) : kNoKey;
+}
+
 template <int K, int J>
 struct BucketStep {
-  __device__ __forceinline__ static void run(const float4 &q, int32_t base,
-                                             int32_t cnt, bool act,
-                                             float px, float py, float pz,
-                                             int32_t me, float (&bd)[K],
-                                             int32_t (&bo)[K],
-                                             int32_t (&bp)[K]) {
-    if (J < cnt) {
-      const float dx = row_bcast<J>(q.x) - px;
-      const float dy = row_bcast<J>(q.y) - py;
-      const float dz = row_bcast<J>(q.z) - pz;
-      const int32_t qo = row_bcast_i<J>(__float_as_int(q.w));
-      const float xx = dx * dx, yy = dy * dy, zz = dz * dz;
-      const float d2 = (xx + yy) + zz;
-      if (act && qo != me && pair_lt(d2, qo, bd[K - 1], bo[K - 1]))
-        topk_insert<K>(bd, bo, bp, d2, qo, base + J);
-      BucketStep<K, J + 1>::run(q, base, cnt, act, px, py, pz, me, bd, bo, bp);
-    }
+  __device__ __forceinline__ static void run(const float4 &q, float px,
+                                             float py, float pz, int32_t me,
+                                             int32_t cnt, uint64_t (&key)[K]) {
+    const uint64_t nk = bucket_key<J>(q, px, py, pz, me, cnt);
+    if (nk < key[K - 1]) topk_insert<K>(key, nk);
+    BucketStep<K, J + 1>::run(q, px, py, pz, me, cnt, key);
   }
 };
 template <int K>
 struct BucketStep<K, kBucket> {
-  __device__ __forceinline__ static void run(const float4 &, int32_t, int32_t,
-                                             bool, float, float, float,
-                                             int32_t, float (&)[K],
-                                             int32_t (&)[K], int32_t (&)[K]) {}
+  __device__ __forceinline__ static void run(const float4 &, float, float,
+                                             float, int32_t, int32_t,
+                                             uint64_t (&)[K]) {}
 };
 
 // All 16 lanes of a group scan bucket b together (group-uniform call).
+// Lanes of an inactive query (me = -1) carry keys too, they are not written.
 template <int K>
 __device__ __forceinline__ void scan_bucket(const float4 *__restrict__ pts,
                                             int32_t n, int32_t b, int lane16,
-                                            bool act, float px, float py,
-                                            float pz, int32_t me,
-                                            float (&bd)[K], int32_t (&bo)[K],
-                                            int32_t (&bp)[K]) {
+                                            float px, float py, float pz,
+                                            int32_t me, uint64_t (&key)[K]) {
   const int32_t base = b * kBucket;
   const int32_t cnt = min(kBucket, n - base);
   float4 q = make_float4(0.f, 0.f, 0.f, 0.f);
   if (lane16 < cnt) q = pts[base + lane16];
-  BucketStep<K, 0>::run(q, base, cnt, act, px, py, pz, me, bd, bo, bp);
+  BucketStep<K, 0>::run(q, px, py, pz, me, cnt, key);
 }
 
 // One query group = 16 lanes = the 16 points of one bucket.  Every group
 // walks the tree on its own (group-uniform decisions from a 16-lane vote);
 // the four groups of a wave alternate between finding their next bucket and
-// scanning it together.
+// scanning it together.  A box is entered when its fp32 distance (same
+// operations as d2, so never above the d2 of a point inside) does not
+// exceed some lane's current k-th distance.
 template <int K>
 __global__ __launch_bounds__(256) void k_knn_query(
-    const float4 *__restrict__ pts, int32_t n, const float4 *__restrict__ blo,
-    const float4 *__restrict__ bhi, Tree tree, int32_t k,
-    int32_t *__restrict__ nbr_int, int32_t *__restrict__ nbr_out,
-    float *__restrict__ d2_out, int32_t n_blocks) {
+    const float4 *__restrict__ pts, const int32_t *__restrict__ inv,
+    int32_t n, const float4 *__restrict__ blo, const float4 *__restrict__ bhi,
+    Tree tree, int32_t k, int32_t *__restrict__ nbr_int,
+    int32_t *__restrict__ nbr_out, float *__restrict__ d2_out,
+    int32_t n_blocks) {
   const int32_t lb = xcd_block();
   if (lb >= n_blocks) return;
   const int lane16 = threadIdx.x & (kBucket - 1);
@@ -258,22 +254,15 @@ __global__ __launch_bounds__(256) void k_knn_query(
   const bool act = i < n;
   const float4 p = act ? pts[i] : make_float4(0.f, 0.f, 0.f, 0.f);
   const int32_t me = act ? __float_as_int(p.w) : -1;
-  float bd[K];
-  int32_t bo[K], bp[K];
+  uint64_t key[K];
 #pragma unroll
-  for (int t = 0; t < K; ++t) {
-    bd[t] = INFINITY;
-    bo[t] = INT32_MAX;
-    bp[t] = -1;
-  }
+  for (int t = 0; t < K; ++t) key[t] = kNoKey;
   // own bucket and its Morton neighbours first: a tight k-th distance early
-  scan_bucket<K>(pts, n, grp, lane16, act, p.x, p.y, p.z, me, bd, bo, bp);
+  scan_bucket<K>(pts, n, grp, lane16, p.x, p.y, p.z, me, key);
   if (grp > 0)
-    scan_bucket<K>(pts, n, grp - 1, lane16, act, p.x, p.y, p.z, me, bd, bo,
-                   bp);
+    scan_bucket<K>(pts, n, grp - 1, lane16, p.x, p.y, p.z, me, key);
   if (grp + 1 < nb0)
-    scan_bucket<K>(pts, n, grp + 1, lane16, act, p.x, p.y, p.z, me, bd, bo,
-                   bp);
+    scan_bucket<K>(pts, n, grp + 1, lane16, p.x, p.y, p.z, me, key);
 
   int level = tree.top;
   int32_t idx = 0;
@@ -283,15 +272,14 @@ __global__ __launch_bounds__(256) void k_knn_query(
     while (!done) {
       const int32_t j = tree.off[level] + idx;
       const float4 lo = blo[j], hi = bhi[j];
-      const float ex =
-          p.x < lo.x ? lo.x - p.x : (p.x > hi.x ? p.x - hi.x : 0.f);
-      const float ey =
-          p.y < lo.y ? lo.y - p.y : (p.y > hi.y ? p.y - hi.y : 0.f);
-      const float ez =
-          p.z < lo.z ? lo.z - p.z : (p.z > hi.z ? p.z - hi.z : 0.f);
+      const float ex = fmaxf(fmaxf(lo.x - p.x, p.x - hi.x), 0.f);
+      const float ey = fmaxf(fmaxf(lo.y - p.y, p.y - hi.y), 0.f);
+      const float ez = fmaxf(fmaxf(lo.z - p.z, p.z - hi.z), 0.f);
       const float bx = ex * ex, by = ey * ey, bz = ez * ez;
       const float d2b = (bx + by) + bz;
-      const bool need = act && d2b <= bd[K - 1];
+      // d2b <= k-th d2 (an empty list, kNoKey, admits everything)
+      const bool need =
+          act && __float_as_uint(d2b) <= (uint32_t)(key[K - 1] >> 32);
       const bool any = ((__ballot(need) >> gshift) & 0xffffull) != 0;
       if (any && level > 0) {
         --level;
@@ -316,18 +304,20 @@ __global__ __launch_bounds__(256) void k_knn_query(
     }
     if (__ballot(leaf >= 0) == 0) break;
     if (leaf >= 0)
-      scan_bucket<K>(pts, n, leaf, lane16, act, p.x, p.y, p.z, me, bd, bo,
-                     bp);
+      scan_bucket<K>(pts, n, leaf, lane16, p.x, p.y, p.z, me, key);
   }
 
   if (!act) return;
 #pragma unroll
   for (int t = 0; t < K; ++t) {
     if (t < k) {
-      nbr_int[(int64_t)i * k + t] = bp[t];
-      if (nbr_out)
-        nbr_out[(int64_t)me * k + t] = (bp[t] < 0) ? -1 : bo[t];
-      if (d2_out) d2_out[(int64_t)me * k + t] = bd[t];
+      const bool has = key[t] != kNoKey;
+      const int32_t o = (int32_t)(uint32_t)key[t];
+      nbr_int[(int64_t)i * k + t] = has ? inv[o] : -1;
+      if (nbr_out) nbr_out[(int64_t)me * k + t] = has ? o : -1;
+      if (d2_out)
+        d2_out[(int64_t)me * k + t] =
+            has ? __uint_as_float((uint32_t)(key[t] >> 32)) : INFINITY;
     }
   }
 }
@@ -389,7 +379,8 @@ hipError_t knn_launch(const float *xyz, int32_t n, int32_t k, Ctl *ctl,
   switch (knn_template_k(k)) {
 #define EZSP_KNN_CASE(KK)                                                    \
   case KK:                                                                   \
-    hipLaunchKernelGGL(k_knn_query<KK>, grid, dim3(nt), 0, st, s.pts, n,     \
+    hipLaunchKernelGGL(k_knn_query<KK>, grid, dim3(nt), 0, st, s.pts, w.inv, \
+                       n,                                                    \
                        s.blo, s.bhi, tree, k, w.nbr_int, nbr_out, d2_out,    \
                        qblocks);                                             \
     break;
