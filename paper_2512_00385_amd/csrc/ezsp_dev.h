@@ -30,7 +30,7 @@ struct Ctl {
   int32_t e_next;       // directed edges after this round
   int32_t slots;        // hash-table slots this round
   uint32_t maxabs_bits; // max |e| as fp32 bits (monotone for >= 0)
-  int32_t pad0;
+  int32_t n_long;       // nodes whose row goes to the long-row select
   int32_t bbox_enc[6];  // min xyz, max xyz in order-preserving int form
   int32_t pad1[2];
   int64_t cut_w2;       // 2 * cut weight (directed sum) of the current graph

@@ -24,6 +24,10 @@ __device__ __forceinline__ int32_t xcd_block() {
   const int32_t per = (int32_t)(gridDim.x / kXcd);
   return (int32_t)(blockIdx.x % kXcd) * per + (int32_t)(blockIdx.x / kXcd);
 }
+// Global thread index under the XCD-aware block order.
+__device__ __forceinline__ int32_t xcd_tid() {
+  return xcd_block() * (int32_t)blockDim.x + (int32_t)threadIdx.x;
+}
 
 // Bump allocator over the caller's workspace.  With base == nullptr it only
 // measures: every take() returns nullptr and `off` ends at the bytes needed.

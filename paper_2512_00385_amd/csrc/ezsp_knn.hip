@@ -45,15 +45,33 @@ __global__ __launch_bounds__(256) void k_bbox(const float *xyz, int32_t n,
       mx[a] = fmaxf(mx[a], __shfl_xor(mx[a], off, kWave));
     }
   }
-  const bool lead = (threadIdx.x & (kWave - 1)) == 0;
-  if (lead) {
+  __shared__ float smn[3][256 / kWave], smx[3][256 / kWave];
+  __shared__ int sbad;
+  const int wid = threadIdx.x / kWave;
+  if (threadIdx.x == 0) sbad = 0;
+  __syncthreads();
+  if ((threadIdx.x & (kWave - 1)) == 0) {
 #pragma unroll
     for (int a = 0; a < 3; ++a) {
-      atomicMin(&ctl->bbox_enc[a], f2ord(mn[a]));
-      atomicMax(&ctl->bbox_enc[3 + a], f2ord(mx[a]));
+      smn[a][wid] = mn[a];
+      smx[a][wid] = mx[a];
     }
   }
-  if (__ballot(bad) && lead) raise_err(ctl, kErrNonFinite);
+  if (__ballot(bad) && (threadIdx.x & (kWave - 1)) == 0) sbad = 1;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+#pragma unroll
+    for (int a = 0; a < 3; ++a) {
+      float lo = smn[a][0], hi = smx[a][0];
+      for (int q = 1; q < 256 / kWave; ++q) {
+        lo = fminf(lo, smn[a][q]);
+        hi = fmaxf(hi, smx[a][q]);
+      }
+      atomicMin(&ctl->bbox_enc[a], f2ord(lo));
+      atomicMax(&ctl->bbox_enc[3 + a], f2ord(hi));
+    }
+    if (sbad) raise_err(ctl, kErrNonFinite);
+  }
 }
 
 // 16 bits -> every third bit of 48.
@@ -356,7 +374,7 @@ hipError_t knn_launch(const float *xyz, int32_t n, int32_t k, Ctl *ctl,
   const Tree tree = make_tree(n);
   const int nt = 256;
   const int gb = (n + nt - 1) / nt;
-  hipLaunchKernelGGL(k_bbox, dim3(min(gb, 1024)), dim3(nt), 0, st, xyz, n,
+  hipLaunchKernelGGL(k_bbox, dim3(min(gb, 256)), dim3(nt), 0, st, xyz, n,
                      ctl);
   hipLaunchKernelGGL(k_morton, dim3(gb), dim3(nt), 0, st, xyz, n, ctl, s.keys,
                      s.vals);

@@ -34,6 +34,8 @@ namespace ezsp {
 
 constexpr uint64_t kEmpty = ~0ull;
 constexpr int kJumpCap = 1 << 16;
+constexpr int kLongRow = 64;  // rows longer than this go to k_select_long
+constexpr int kLongGrid = 1024;
 
 // ---------------------------------------------------------------------------
 // small kernels
@@ -87,7 +89,7 @@ __global__ __launch_bounds__(256) void k_graph_count(const int32_t *nbr,
                                                      int32_t n, int32_t k,
                                                      int32_t *fwd, int32_t *rev,
                                                      Ctl *ctl) {
-  const int32_t i = blockIdx.x * blockDim.x + threadIdx.x;
+  const int32_t i = xcd_tid();
   if (i >= n) return;
   const int32_t *row = nbr + (int64_t)i * k;
   int32_t c = 0;
@@ -116,7 +118,7 @@ __global__ __launch_bounds__(256) void k_graph_fill(
     const int32_t *nbr, int32_t n, int32_t k, const int32_t *fwd,
     const int32_t *rp, int32_t *cursor, int32_t *col, int32_t *w, int32_t *src,
     Ctl *ctl) {
-  const int32_t i = blockIdx.x * blockDim.x + threadIdx.x;
+  const int32_t i = xcd_tid();
   if (i >= n) return;
   const int32_t *row = nbr + (int64_t)i * k;
   const int32_t base = rp[i];
@@ -184,6 +186,7 @@ __global__ void k_round_init(Ctl *ctl) {
     ctl->n_next = 0;
     ctl->e_next = 0;
     ctl->slots = 0;
+    ctl->n_long = 0;
   }
 }
 
@@ -197,9 +200,16 @@ template <bool FIRST>
 __global__ __launch_bounds__(256) void k_select(
     int32_t nn, const int32_t *__restrict__ rp, const int32_t *__restrict__ col,
     const int32_t *__restrict__ w, NodeIn s, int32_t d, double lambda,
-    int64_t smin, int32_t *__restrict__ target, Ctl *ctl) {
-  const int32_t v = blockIdx.x * blockDim.x + threadIdx.x;
+    int64_t smin, int32_t *__restrict__ target, int32_t *__restrict__ long_rows,
+    Ctl *ctl) {
+  const int32_t v = xcd_tid();
   if (v >= nn) return;
+  const int32_t e0 = rp[v], e1 = rp[v + 1];
+  if (e1 - e0 > kLongRow) {  // a whole block takes this row later
+    const int32_t slot = atomicAdd(&ctl->n_long, 1);
+    long_rows[slot] = v;
+    return;
+  }
   const int F = ctl->F;
   const double sF = ldexp(1.0, F), sIF = ldexp(1.0, -F);
   const int32_t sv = node_size<FIRST>(s, v);
@@ -208,8 +218,7 @@ __global__ __launch_bounds__(256) void k_select(
   bool has = false;
   double bD = 0.0;
   int32_t bMP = 0, bU = -1;
-  const int32_t e1 = rp[v + 1];
-  for (int32_t e = rp[v]; e < e1; ++e) {
+  for (int32_t e = e0; e < e1; ++e) {
     const int32_t u = col[e];
     if ((uint32_t)u >= (uint32_t)nn) {
       raise_err(ctl, kErrInternal);
@@ -241,6 +250,94 @@ __global__ __launch_bounds__(256) void k_select(
   }
   target[v] = has ? bU : -1;
   if (__ballot(has) && (threadIdx.x & (kWave - 1)) == 0) ctl->any_choice = 1;
+}
+
+// Steps 1-2 for rows longer than kLongRow: one block per row, threads stride
+// over the row and the best candidate is found by a block reduction under
+// the same order (larger gain, then smaller minpt).
+struct Best {
+  double g;
+  int32_t mp, u;  // u < 0: no candidate
+};
+
+__device__ __forceinline__ bool best_before(const Best &a, const Best &b) {
+  if (a.u < 0) return false;
+  if (b.u < 0) return true;
+  return a.g > b.g || (a.g == b.g && a.mp < b.mp);
+}
+
+template <bool FIRST>
+__global__ __launch_bounds__(256) void k_select_long(
+    const int32_t *__restrict__ rp, const int32_t *__restrict__ col,
+    const int32_t *__restrict__ w, NodeIn s, int32_t d, double lambda,
+    int64_t smin, int32_t nn, int32_t *__restrict__ target,
+    const int32_t *__restrict__ long_rows, Ctl *ctl) {
+  __shared__ double sg[256 / kWave];
+  __shared__ int32_t smp[256 / kWave], su[256 / kWave];
+  const int32_t n_long = ctl->n_long;
+  const int F = ctl->F;
+  const double sF = ldexp(1.0, F), sIF = ldexp(1.0, -F);
+  for (int32_t li = blockIdx.x; li < n_long; li += gridDim.x) {
+    const int32_t v = long_rows[li];
+    if ((uint32_t)v >= (uint32_t)nn) {
+      raise_err(ctl, kErrInternal);
+      continue;
+    }
+    const int32_t sv = node_size<FIRST>(s, v);
+    const double dsv = (double)sv;
+    const bool small = (int64_t)sv < smin;
+    Best b{0.0, 0, -1};
+    for (int32_t e = rp[v] + threadIdx.x; e < rp[v + 1]; e += blockDim.x) {
+      const int32_t u = col[e];
+      if ((uint32_t)u >= (uint32_t)nn) {
+        raise_err(ctl, kErrInternal);
+        continue;
+      }
+      const double dsu = (double)node_size<FIRST>(s, u);
+      const double num = dsv * dsu;
+      const double den = dsv + dsu;
+      const double f = num / den;
+      double ss = 0.0;
+      for (int32_t i = 0; i < d; ++i) {
+        const double diff = node_mu<FIRST>(s, v, i, d, sF, sIF) -
+                            node_mu<FIRST>(s, u, i, d, sF, sIF);
+        const double sq = diff * diff;
+        ss = ss + sq;
+      }
+      const double cut = lambda * (double)w[e];
+      const double fit = f * ss;
+      const double g = cut - fit;
+      if (g > 0.0 || small) {
+        const Best c{g, node_minpt<FIRST>(s, u), u};
+        if (best_before(c, b)) b = c;
+      }
+    }
+#pragma unroll
+    for (int off = kWave / 2; off > 0; off >>= 1) {
+      Best o;
+      o.g = __shfl_xor(b.g, off, kWave);
+      o.mp = __shfl_xor(b.mp, off, kWave);
+      o.u = __shfl_xor(b.u, off, kWave);
+      if (best_before(o, b)) b = o;
+    }
+    const int wid = threadIdx.x / kWave;
+    if ((threadIdx.x & (kWave - 1)) == 0) {
+      sg[wid] = b.g;
+      smp[wid] = b.mp;
+      su[wid] = b.u;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      Best r{sg[0], smp[0], su[0]};
+      for (int q = 1; q < 256 / kWave; ++q) {
+        const Best o{sg[q], smp[q], su[q]};
+        if (best_before(o, r)) r = o;
+      }
+      target[v] = r.u;
+      if (r.u >= 0) ctl->any_choice = 1;
+    }
+    __syncthreads();
+  }
 }
 
 // Merge graph -> forest: a node points to its choice, except the lower end
@@ -333,7 +430,7 @@ __global__ __launch_bounds__(256) void k_stats_add(
     NodeIn s, int32_t d, Ctl *ctl, int32_t *size, int64_t *S, int32_t *minpt,
     int32_t *cap) {
   if (!ctl->any_choice) return;
-  const int32_t v = blockIdx.x * blockDim.x + threadIdx.x;
+  const int32_t v = xcd_tid();
   if (v >= nn) return;
   const int32_t c = L[v];
   if ((uint32_t)c >= (uint32_t)ctl->n_next) {
@@ -390,7 +487,7 @@ __global__ __launch_bounds__(256) void k_insert(
     uint64_t *keys, int32_t *tw, int32_t *ndeg, int32_t nn, int32_t table_cap,
     Ctl *ctl) {
   if (!ctl->any_choice) return;
-  const int32_t e = blockIdx.x * blockDim.x + threadIdx.x;
+  const int32_t e = xcd_tid();
   if (e >= ed) return;
   const int32_t a = src[e], b = col[e];
   if ((uint32_t)a >= (uint32_t)nn || (uint32_t)b >= (uint32_t)nn) {
@@ -455,7 +552,7 @@ __global__ __launch_bounds__(256) void k_compose(int32_t n, int32_t nn,
                                                  int32_t *M, const int32_t *L,
                                                  Ctl *ctl) {
   if (!ctl->any_choice) return;
-  const int32_t i = blockIdx.x * blockDim.x + threadIdx.x;
+  const int32_t i = xcd_tid();
   if (i >= n) return;
   const int32_t c = FIRST ? i : M[i];
   if ((uint32_t)c >= (uint32_t)nn) {
@@ -594,7 +691,7 @@ struct Bufs {
   int32_t *size[2], *minpt[2];
   int64_t *S[2];
   double *mu;
-  int32_t *target, *parent, *newid, *L, *cap, *toff, *ndeg;
+  int32_t *target, *parent, *newid, *L, *cap, *toff, *ndeg, *long_rows;
   uint64_t *keys;
   int32_t *tw;
   int32_t *M, *mark, *rank;
@@ -629,6 +726,7 @@ void carve(Arena &a, int32_t n, int32_t d, int32_t k, bool need_emb,
   b->cap = a.take<int32_t>(n1);
   b->toff = a.take<int32_t>(n1);
   b->ndeg = a.take<int32_t>(n1);
+  b->long_rows = a.take<int32_t>(n1);
   b->keys = a.take<uint64_t>(ed);
   b->tw = a.take<int32_t>(ed);
   b->M = a.take<int32_t>(n1);
@@ -674,9 +772,12 @@ void launch_round(const Bufs &b, int cur, int32_t n, int32_t k, int32_t nn,
   const int32_t tcap = (int32_t)edge_bound(n, k);
   hipLaunchKernelGGL(k_round_init, dim3(1), dim3(64), 0, st, ctl);
   prof_begin("select", st);
-  hipLaunchKernelGGL(k_select<FIRST>, blocks_for(nn), dim3(256), 0, st, nn,
-                     b.rp[cur], b.col[cur], b.w[cur], s, d, lambda, smin,
-                     b.target, ctl);
+  hipLaunchKernelGGL(k_select<FIRST>, xcd_grid(blocks_for(nn).x), dim3(256), 0,
+                     st, nn, b.rp[cur], b.col[cur], b.w[cur], s, d, lambda,
+                     smin, b.target, b.long_rows, ctl);
+  hipLaunchKernelGGL(k_select_long<FIRST>, dim3(kLongGrid), dim3(256), 0, st,
+                     b.rp[cur], b.col[cur], b.w[cur], s, d, lambda, smin, nn,
+                     b.target, b.long_rows, ctl);
   prof_end(st);
   prof_begin("union", st);
   hipLaunchKernelGGL(k_hook, blocks_for(nn), dim3(256), 0, st, nn, b.target,
@@ -690,7 +791,8 @@ void launch_round(const Bufs &b, int cur, int32_t n, int32_t k, int32_t nn,
   prof_begin("stats", st);
   hipLaunchKernelGGL(k_zero_acc, blocks_for(nn), dim3(256), 0, st, nn, d, ctl,
                      b.size[nxt], b.S[nxt], b.minpt[nxt], b.cap, b.ndeg);
-  hipLaunchKernelGGL(k_stats_add<FIRST>, blocks_for(nn), dim3(256), 0, st, nn,
+  hipLaunchKernelGGL(k_stats_add<FIRST>, xcd_grid(blocks_for(nn).x), dim3(256),
+                     0, st, nn,
                      b.L, b.rp[cur], s, d, ctl, b.size[nxt], b.S[nxt],
                      b.minpt[nxt], b.cap);
   hipLaunchKernelGGL(k_stats_final, blocks_for((int64_t)nn * d), dim3(256), 0,
@@ -701,7 +803,8 @@ void launch_round(const Bufs &b, int cur, int32_t n, int32_t k, int32_t nn,
               &ctl->slots, st);
   hipLaunchKernelGGL(k_table_clear, blocks_for(ed), dim3(256), 0, st, ed, ctl,
                      b.keys, b.tw);
-  hipLaunchKernelGGL(k_insert, blocks_for(ed), dim3(256), 0, st, ed,
+  hipLaunchKernelGGL(k_insert, xcd_grid(blocks_for(ed).x), dim3(256), 0, st,
+                     ed,
                      b.src[cur], b.col[cur], b.w[cur], b.L, b.toff, b.cap,
                      b.keys, b.tw, b.ndeg, nn, tcap, ctl);
   device_scan(ScanArray{b.ndeg, b.rp[nxt], nn, &ctl->n_next}, nn + 1, b.bsum,
@@ -711,7 +814,8 @@ void launch_round(const Bufs &b, int cur, int32_t n, int32_t k, int32_t nn,
               ed, b.bsum, b.tmp, st);
   prof_end(st);
   prof_begin("compose", st);
-  hipLaunchKernelGGL(k_compose<FIRST>, blocks_for(n), dim3(256), 0, st, n, nn,
+  hipLaunchKernelGGL(k_compose<FIRST>, xcd_grid(blocks_for(n).x), dim3(256), 0,
+                     st, n, nn,
                      b.M, b.L, ctl);
   prof_end(st);
 }
@@ -741,7 +845,7 @@ int ladder_run(const LadderArgs &g, Ctl *ctl, Arena &a, hipStream_t st) {
                        0, st, g.emb, g.perm, n, d, b.emb_int);
     emb = b.emb_int;
   }
-  hipLaunchKernelGGL(k_maxabs, dim3(1024), dim3(256), 0, st, emb,
+  hipLaunchKernelGGL(k_maxabs, dim3(256), dim3(256), 0, st, emb,
                      (int64_t)n * d, ctl);
   hipLaunchKernelGGL(k_fixshift, dim3(1), dim3(64), 0, st, ctl, n);
 
@@ -751,11 +855,13 @@ int ladder_run(const LadderArgs &g, Ctl *ctl, Arena &a, hipStream_t st) {
   hipLaunchKernelGGL(k_fill_i32, blocks_for(n), dim3(256), 0, st, b.cursor,
                      (int64_t)n, 0);
   prof_begin("graph_build", st);
-  hipLaunchKernelGGL(k_graph_count, blocks_for(n), dim3(256), 0, st, g.nbr, n,
+  hipLaunchKernelGGL(k_graph_count, xcd_grid(blocks_for(n).x), dim3(256), 0,
+                     st, g.nbr, n,
                      k, b.fwd, b.rev, ctl);
   device_scan(ScanDeg{b.fwd, b.rev, b.rp[0], n}, n + 1, b.bsum, &ctl->e_next,
               st);
-  hipLaunchKernelGGL(k_graph_fill, blocks_for(n), dim3(256), 0, st, g.nbr, n,
+  hipLaunchKernelGGL(k_graph_fill, xcd_grid(blocks_for(n).x), dim3(256), 0,
+                     st, g.nbr, n,
                      k, b.fwd, b.rp[0], b.cursor, b.col[0], b.w[0], b.src[0],
                      ctl);
   prof_end(st);

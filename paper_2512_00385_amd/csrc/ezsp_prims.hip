@@ -165,7 +165,7 @@ __global__ void k_ctl_init(Ctl *ctl) {
     ctl->e_next = 0;
     ctl->slots = 0;
     ctl->maxabs_bits = 0;
-    ctl->pad0 = 0;
+    ctl->n_long = 0;
     for (int a = 0; a < 3; ++a) {
       ctl->bbox_enc[a] = f2ord(INFINITY);
       ctl->bbox_enc[3 + a] = f2ord(-INFINITY);
@@ -189,9 +189,19 @@ __global__ __launch_bounds__(256) void k_maxabs(const float *v, int64_t count,
 #pragma unroll
   for (int off = kWave / 2; off > 0; off >>= 1)
     m = max(m, (uint32_t)__shfl_xor((int)m, off, kWave));
-  if ((threadIdx.x & (kWave - 1)) == 0) atomicMax(&ctl->maxabs_bits, m);
-  if (__ballot(bad) && (threadIdx.x & (kWave - 1)) == 0)
-    raise_err(ctl, kErrNonFinite);
+  __shared__ uint32_t sm[256 / kWave];
+  __shared__ int sbad;
+  if (threadIdx.x == 0) sbad = 0;
+  __syncthreads();
+  if ((threadIdx.x & (kWave - 1)) == 0) sm[threadIdx.x / kWave] = m;
+  if (__ballot(bad) && (threadIdx.x & (kWave - 1)) == 0) sbad = 1;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint32_t r = sm[0];
+    for (int q = 1; q < 256 / kWave; ++q) r = max(r, sm[q]);
+    atomicMax(&ctl->maxabs_bits, r);
+    if (sbad) raise_err(ctl, kErrNonFinite);
+  }
 }
 
 // F = min(40, 61 - ceil(log2 n) - max(0, ceil(log2 A))), A = max |e|.
