@@ -28,11 +28,14 @@ struct Ctl {
   int32_t any_choice;   // some node kept a merge edge this round
   int32_t n_next;       // components after this round
   int32_t e_next;       // directed edges after this round
-  int32_t slots;        // hash-table slots this round
+  int32_t slots;        // adjacency-table slots of the next round
   uint32_t maxabs_bits; // max |e| as fp32 bits (monotone for >= 0)
-  int32_t n_long;       // nodes whose row goes to the long-row select
+  int32_t n_long;       // nodes whose row goes to the block-per-row kernels
   int32_t bbox_enc[6];  // min xyz, max xyz in order-preserving int form
-  int32_t pad1[2];
+  int32_t n_big;        // components that go to the block-per-component path
+  int32_t e_rev;        // reverse-only entries of the first-round graph
+  int32_t e_fwd;        // valid forward entries of the first-round graph
+  int32_t n_cbig;       // components whose table window exceeds one chunk
   int64_t cut_w2;       // 2 * cut weight (directed sum) of the current graph
   double fid_total;     // fidelity term of the energy
 };

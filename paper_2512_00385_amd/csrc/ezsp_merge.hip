@@ -1,31 +1,41 @@
 // ezsp_merge.hip -- the merge ladder of EZ-SP (arXiv 2512.00385, Sec. 3.2):
-// kNN graph build, then rounds of Steps 1-4 on the superpoint adjacency
-// until no candidate merge is left, for every regularisation strength of the
-// ladder (hierarchical partition).
+// kNN graph, then rounds of Steps 1-4 on the superpoint adjacency until no
+// candidate merge is left, for every regularisation strength of the ladder
+// (hierarchical partition).
 //
-// Representation.  Nodes of round r are the superpoints of round r, stored
-// in an internal order (Morton order of their first point when the graph came
-// from xyz) that keeps neighbours close in memory.  The adjacency is a CSR
-// holding every undirected edge in both directions: row v lists (u, w_vu).
-// Each node keeps its size |P|, the exact int64 fixed-point sum of its
-// embeddings, its mean in fp64 and `minpt`, the smallest original point
-// index of its points; ordering nodes by minpt is the same as ordering them
-// by their canonical number, so ties and output labels use minpt and the
-// internal order never shows in the results.
+// Representation.  Nodes of a round are its superpoints, stored in an
+// internal order (Morton order of the points when the graph came from xyz)
+// that keeps neighbours close in memory.  Each node keeps its size |P|, the
+// exact int64 fixed-point sum of its embeddings, its fp64 mean and `minpt`,
+// the smallest original point index of its points.  Ordering nodes by minpt
+// is ordering them by their canonical number, so the tie rule and the output
+// labels use minpt and the internal order never shows in the results.
 //
-// One round (all on the device, one host readback at the end):
-//   select   Steps 1-2: every node scans its row, evaluates Prop. 1's gain,
-//            keeps the best candidate (largest gain, ties to smaller minpt)
-//   hook     merge graph of chosen edges; every cycle of it is a mutual pair
-//            (each choice is at least as good as the choice it follows), the
-//            lower id becomes the root
-//   jump     pointer jumping to the roots = weakly connected components
-//            (Step 3, what App. Alg. A-1 computes)
-//   relabel  roots numbered by a scan
-//   stats    Step 4: sizes, int64 sums, minpt, row capacity per component
-//   contract Step 4: per-component open-addressing tables collect the
-//            relabelled edges and add up the weights of parallel edges; a
-//            scan compacts them into the next CSR
+// Adjacency, both directions of every undirected edge:
+//   first round  row v = the valid entries of the kNN row v (weight 1) plus
+//                a short reverse list of the u that have v in their kNN row
+//                while v does not have u;
+//   later rounds row v = a window [ws[v], ws[v] + wl[v]) of a table of
+//                packed (neighbour << 32 | weight) slots, empty slots = ~0.
+//
+// One round (host reads the control block back once at the end):
+//   select    Steps 1-2: each node scans its row, evaluates Prop. 1's gain
+//             and keeps the best candidate (largest gain, ties to the
+//             smaller minpt); rows longer than kLongRow take a whole wave
+//   hook      merge graph -> forest: every cycle of the merge graph is a
+//             mutual pair (each choice is at least as good as the choice it
+//             follows), the lower id of a pair becomes a root
+//   jump      pointer jumping to the roots: weakly connected components
+//             (Step 3, the partition App. Alg. A-1 computes)
+//   relabel   roots numbered by a scan
+//   members   counting sort of the nodes by component (one atomic per node)
+//   stats     Step 4: size, int64 sums, fp64 mean, minpt, summed degree per
+//             component, gathered from its members (no atomics)
+//   contract  Step 4: one thread per directed entry relabels it into its
+//             component's window of the next table (capacity = summed
+//             degree); parallel edges add their weights in the same slot,
+//             edges inside a component are dropped; the window is the next
+//             round's row and every occupied slot records its owner
 #include <math.h>
 
 #include "ezsp_internal.h"
@@ -34,8 +44,13 @@ namespace ezsp {
 
 constexpr uint64_t kEmpty = ~0ull;
 constexpr int kJumpCap = 1 << 16;
-constexpr int kLongRow = 64;  // rows longer than this go to k_select_long
-constexpr int kLongGrid = 1024;
+constexpr int kLongRow = 128;   // rows longer than this: one wave per row
+constexpr int kLongGrid = 2048; // blocks of 4 waves for the long rows
+constexpr int kBigComp = 128;   // components with more members: one block
+constexpr int kBigGrid = 512;
+constexpr int kChunk = 2048;    // table slots contracted by one block in LDS
+constexpr int kBatch = 256;     // members taken at a time by a block
+constexpr int kPreSlots = 4096; // LDS pre-aggregation table of a big tile
 
 // ---------------------------------------------------------------------------
 // small kernels
@@ -58,10 +73,33 @@ __global__ __launch_bounds__(256) void k_gather_rows(const float *emb,
 }
 
 // ---------------------------------------------------------------------------
-// graph build: the union of the kNN relations, one undirected edge of weight
-// 1 per pair (Sec. 3.1, Sec. 4.1; duplicates and self loops removed as in
-// App. Alg. A-2, prepare_graph), stored in both directions
+// first-round graph: the union of the kNN relations, one undirected edge of
+// weight 1 per pair (Sec. 3.1, Sec. 4.1; self loops and repeats removed as
+// App. Alg. A-2's prepare_graph does)
 // ---------------------------------------------------------------------------
+
+// A caller's neighbour table: entries outside [-1, n) are an error; -1, the
+// point itself and repeats of an earlier entry become -1.
+__global__ __launch_bounds__(256) void k_sanitize(const int32_t *nbr,
+                                                  int32_t n, int32_t k,
+                                                  int32_t *out, Ctl *ctl) {
+  const int32_t i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  const int32_t *r = nbr + (int64_t)i * k;
+  int32_t *o = out + (int64_t)i * k;
+  for (int32_t t = 0; t < k; ++t) {
+    int32_t j = r[t];
+    if (j < -1 || j >= n) {
+      raise_err(ctl, kErrBadIndex);
+      j = -1;
+    }
+    if (j == i) j = -1;
+    for (int32_t s = 0; s < t && j >= 0; ++s)
+      if (r[s] == j) j = -1;
+    o[t] = j;
+  }
+}
+
 __device__ __forceinline__ bool row_has(const int32_t *nbr, int32_t k,
                                         int32_t j, int32_t x) {
   const int32_t *r = nbr + (int64_t)j * k;
@@ -70,89 +108,68 @@ __device__ __forceinline__ bool row_has(const int32_t *nbr, int32_t k,
   return false;
 }
 
-// Entry t of row i is a forward edge when it is a valid id, not i itself and
-// not a repeat of an earlier entry of the row.
-__device__ __forceinline__ bool fwd_entry(const int32_t *row, int32_t t,
-                                          int32_t i, int32_t n, Ctl *ctl) {
-  const int32_t j = row[t];
-  if (j == -1 || j == i) return false;
-  if (j < -1 || j >= n) {
-    raise_err(ctl, kErrBadIndex);
-    return false;
+// Reverse entries: i lists u, u does not list i -> u's row gets i.
+__global__ __launch_bounds__(256) void k_rev_count(const int32_t *nbr,
+                                                   int32_t n, int32_t k,
+                                                   int32_t *rev, Ctl *ctl) {
+  const int32_t i = xcd_tid();
+  int32_t fwd = 0;
+  if (i < n) {
+    const int32_t *r = nbr + (int64_t)i * k;
+    for (int32_t t = 0; t < k; ++t) {
+      const int32_t u = r[t];
+      if (u < 0) continue;
+      ++fwd;
+      if (!row_has(nbr, k, u, i)) atomicAdd(&rev[u], 1);
+    }
   }
-  for (int32_t s = 0; s < t; ++s)
-    if (row[s] == j) return false;
-  return true;
+  fwd = wave_sum(fwd);
+  if ((threadIdx.x & (kWave - 1)) == 0 && fwd) atomicAdd(&ctl->e_fwd, fwd);
 }
 
-__global__ __launch_bounds__(256) void k_graph_count(const int32_t *nbr,
-                                                     int32_t n, int32_t k,
-                                                     int32_t *fwd, int32_t *rev,
-                                                     Ctl *ctl) {
+__global__ __launch_bounds__(256) void k_rev_fill(const int32_t *nbr,
+                                                  int32_t n, int32_t k,
+                                                  const int32_t *rrp,
+                                                  int32_t *cursor,
+                                                  int32_t *rcol,
+                                                  int32_t *rown, Ctl *ctl) {
   const int32_t i = xcd_tid();
   if (i >= n) return;
-  const int32_t *row = nbr + (int64_t)i * k;
-  int32_t c = 0;
+  const int32_t *r = nbr + (int64_t)i * k;
   for (int32_t t = 0; t < k; ++t) {
-    if (!fwd_entry(row, t, i, n, ctl)) continue;
-    const int32_t j = row[t];
-    ++c;
-    if (!row_has(nbr, k, j, i)) atomicAdd(&rev[j], 1);
-  }
-  fwd[i] = c;
-}
-
-struct ScanDeg {
-  const int32_t *fwd, *rev;
-  int32_t *out;
-  int32_t n;
-  __device__ int32_t value(int32_t i) const {
-    return i < n ? fwd[i] + rev[i] : 0;
-  }
-  __device__ void emit(int32_t i, int32_t excl, int32_t) const {
-    if (i <= n) out[i] = excl;
-  }
-};
-
-__global__ __launch_bounds__(256) void k_graph_fill(
-    const int32_t *nbr, int32_t n, int32_t k, const int32_t *fwd,
-    const int32_t *rp, int32_t *cursor, int32_t *col, int32_t *w, int32_t *src,
-    Ctl *ctl) {
-  const int32_t i = xcd_tid();
-  if (i >= n) return;
-  const int32_t *row = nbr + (int64_t)i * k;
-  const int32_t base = rp[i];
-  int32_t c = 0;
-  for (int32_t t = 0; t < k; ++t) {
-    if (!fwd_entry(row, t, i, n, ctl)) continue;
-    const int32_t j = row[t];
-    col[base + c] = j;
-    w[base + c] = 1;
-    src[base + c] = i;
-    ++c;
-    if (!row_has(nbr, k, j, i)) {
-      const int32_t pos = rp[j] + fwd[j] + atomicAdd(&cursor[j], 1);
-      if (pos < rp[j + 1]) {
-        col[pos] = i;
-        w[pos] = 1;
-        src[pos] = j;
-      } else {
-        raise_err(ctl, kErrInternal);
-      }
+    const int32_t u = r[t];
+    if (u < 0 || row_has(nbr, k, u, i)) continue;
+    const int32_t pos = rrp[u] + atomicAdd(&cursor[u], 1);
+    if (pos < rrp[u + 1]) {
+      rcol[pos] = i;
+      rown[pos] = u;
+    } else {
+      raise_err(ctl, kErrInternal);
     }
   }
 }
 
 // ---------------------------------------------------------------------------
-// node state of a round
+// node state and adjacency of a round
 // ---------------------------------------------------------------------------
 struct NodeIn {
-  const int32_t *size;   // |P|            (null in the first round)
+  const int32_t *size;   // |P|              (null in the first round)
   const int64_t *S;      // fixed-point sums (null in the first round)
-  const double *mu;      // fp64 means      (null in the first round)
-  const int32_t *minpt;  // smallest point  (null in the first round)
+  const double *mu;      // fp64 means       (null in the first round)
+  const int32_t *minpt;  // smallest point   (null in the first round)
   const float *emb;      // point embeddings, internal order (first round)
   const int32_t *perm;   // internal -> original point, nullable (identity)
+};
+
+struct Adj {
+  // first round
+  const int32_t *nbr;  // n*k, -1 = no entry
+  int32_t k;
+  const int32_t *rrp, *rcol, *rown;  // reverse list and the row it is in
+  int32_t n_rev;
+  // later rounds
+  const int32_t *ws, *wl;
+  const uint64_t *tbl;
 };
 
 // Mean of node v along dimension i: ((double)S / |P|) * 2^-F.  In the first
@@ -170,6 +187,13 @@ __device__ __forceinline__ double node_mu(const NodeIn &s, int32_t v,
 }
 
 template <bool FIRST>
+__device__ __forceinline__ int64_t node_S(const NodeIn &s, int32_t v,
+                                          int32_t i, int32_t d, double sF) {
+  if (FIRST) return (int64_t)rint((double)s.emb[(int64_t)v * d + i] * sF);
+  return s.S[(int64_t)v * d + i];
+}
+
+template <bool FIRST>
 __device__ __forceinline__ int32_t node_size(const NodeIn &s, int32_t v) {
   return FIRST ? 1 : s.size[v];
 }
@@ -180,6 +204,50 @@ __device__ __forceinline__ int32_t node_minpt(const NodeIn &s, int32_t v) {
   return s.minpt[v];
 }
 
+// Slots of v's row (including empty ones).
+template <bool FIRST>
+__device__ __forceinline__ int32_t row_span(const Adj &a, int32_t v) {
+  if (FIRST) return a.k + (a.rrp[v + 1] - a.rrp[v]);
+  return a.wl[v];
+}
+
+// Calls f(u, w) for the entries j = begin, begin + stride, ... of v's row.
+template <bool FIRST, class Fn>
+__device__ __forceinline__ void for_row(const Adj &a, int32_t v, int32_t begin,
+                                        int32_t stride, Fn &&f) {
+  if (FIRST) {
+    const int32_t *r = a.nbr + (int64_t)v * a.k;
+    const int32_t r0 = a.rrp[v];
+    const int32_t len = a.k + (a.rrp[v + 1] - r0);
+    for (int32_t j = begin; j < len; j += stride) {
+      const int32_t u = (j < a.k) ? r[j] : a.rcol[r0 + (j - a.k)];
+      if (u >= 0) f(u, 1);
+    }
+  } else {
+    const uint64_t *t = a.tbl + a.ws[v];
+    const int32_t len = a.wl[v];
+    for (int32_t j = begin; j < len; j += stride) {
+      const uint64_t e = t[j];
+      if (e != kEmpty) f((int32_t)(e >> 32), (int32_t)(uint32_t)e);
+    }
+  }
+}
+
+// Entry j of v's row (0 <= j < row_span); false for an empty entry.
+template <bool FIRST>
+__device__ __forceinline__ bool row_entry(const Adj &a, int32_t v, int32_t j,
+                                          int32_t &u, int32_t &w) {
+  if (FIRST) {
+    u = (j < a.k) ? a.nbr[(int64_t)v * a.k + j] : a.rcol[a.rrp[v] + (j - a.k)];
+    w = 1;
+    return u >= 0;
+  }
+  const uint64_t e = a.tbl[a.ws[v] + j];
+  u = (int32_t)(e >> 32);
+  w = (int32_t)(uint32_t)e;
+  return e != kEmpty;
+}
+
 __global__ void k_round_init(Ctl *ctl) {
   if (threadIdx.x == 0 && blockIdx.x == 0) {
     ctl->any_choice = 0;
@@ -187,74 +255,20 @@ __global__ void k_round_init(Ctl *ctl) {
     ctl->e_next = 0;
     ctl->slots = 0;
     ctl->n_long = 0;
+    ctl->n_big = 0;
+    ctl->n_cbig = 0;
   }
 }
 
+// ---------------------------------------------------------------------------
 // Steps 1-2.  Prop. 1 (Eq. delta):
 //   Delta(P,Q) = lambda * w_PQ - |P||Q| / (|P|+|Q|) * |Y_P - Y_Q|^2,
 // evaluated in fp64 in a fixed order (no contraction): f = (sP*sQ)/(sP+sQ),
 // ss = sum_i (mu_P,i - mu_Q,i)^2 left to right, Delta = lambda*w - f*ss.
+// The formula is symmetric bit for bit, so P and Q see the same value.
 // A directed edge P -> Q is a candidate when Delta > 0 or |P| < s_min; P
 // keeps its largest candidate, ties to the neighbour with smaller minpt.
-template <bool FIRST>
-__global__ __launch_bounds__(256) void k_select(
-    int32_t nn, const int32_t *__restrict__ rp, const int32_t *__restrict__ col,
-    const int32_t *__restrict__ w, NodeIn s, int32_t d, double lambda,
-    int64_t smin, int32_t *__restrict__ target, int32_t *__restrict__ long_rows,
-    Ctl *ctl) {
-  const int32_t v = xcd_tid();
-  if (v >= nn) return;
-  const int32_t e0 = rp[v], e1 = rp[v + 1];
-  if (e1 - e0 > kLongRow) {  // a whole block takes this row later
-    const int32_t slot = atomicAdd(&ctl->n_long, 1);
-    long_rows[slot] = v;
-    return;
-  }
-  const int F = ctl->F;
-  const double sF = ldexp(1.0, F), sIF = ldexp(1.0, -F);
-  const int32_t sv = node_size<FIRST>(s, v);
-  const double dsv = (double)sv;
-  const bool small = (int64_t)sv < smin;
-  bool has = false;
-  double bD = 0.0;
-  int32_t bMP = 0, bU = -1;
-  for (int32_t e = e0; e < e1; ++e) {
-    const int32_t u = col[e];
-    if ((uint32_t)u >= (uint32_t)nn) {
-      raise_err(ctl, kErrInternal);
-      continue;
-    }
-    const double dsu = (double)node_size<FIRST>(s, u);
-    const double num = dsv * dsu;
-    const double den = dsv + dsu;
-    const double f = num / den;
-    double ss = 0.0;
-    for (int32_t i = 0; i < d; ++i) {
-      const double diff = node_mu<FIRST>(s, v, i, d, sF, sIF) -
-                          node_mu<FIRST>(s, u, i, d, sF, sIF);
-      const double sq = diff * diff;
-      ss = ss + sq;
-    }
-    const double cut = lambda * (double)w[e];
-    const double fit = f * ss;
-    const double g = cut - fit;
-    if (g > 0.0 || small) {
-      const int32_t mp = node_minpt<FIRST>(s, u);
-      if (!has || g > bD || (g == bD && mp < bMP)) {
-        has = true;
-        bD = g;
-        bMP = mp;
-        bU = u;
-      }
-    }
-  }
-  target[v] = has ? bU : -1;
-  if (__ballot(has) && (threadIdx.x & (kWave - 1)) == 0) ctl->any_choice = 1;
-}
-
-// Steps 1-2 for rows longer than kLongRow: one block per row, threads stride
-// over the row and the best candidate is found by a block reduction under
-// the same order (larger gain, then smaller minpt).
+// ---------------------------------------------------------------------------
 struct Best {
   double g;
   int32_t mp, u;  // u < 0: no candidate
@@ -267,17 +281,76 @@ __device__ __forceinline__ bool best_before(const Best &a, const Best &b) {
 }
 
 template <bool FIRST>
+__device__ __forceinline__ double edge_gain(const NodeIn &s, int32_t v,
+                                            double dsv, int32_t u, int32_t w,
+                                            int32_t d, double lambda,
+                                            double sF, double sIF) {
+  const double dsu = (double)node_size<FIRST>(s, u);
+  const double num = dsv * dsu;
+  const double den = dsv + dsu;
+  const double f = num / den;
+  double ss = 0.0;
+  for (int32_t i = 0; i < d; ++i) {
+    const double diff = node_mu<FIRST>(s, v, i, d, sF, sIF) -
+                        node_mu<FIRST>(s, u, i, d, sF, sIF);
+    const double sq = diff * diff;
+    ss = ss + sq;
+  }
+  const double cut = lambda * (double)w;
+  const double fit = f * ss;
+  return cut - fit;
+}
+
+template <bool FIRST>
+__global__ __launch_bounds__(256) void k_select(
+    int32_t nn, Adj a, NodeIn s, int32_t d, double lambda, int64_t smin,
+    int32_t *__restrict__ target, int32_t *__restrict__ deg,
+    int32_t *__restrict__ long_rows, Ctl *ctl) {
+  const int32_t v = xcd_tid();
+  if (v >= nn) return;
+  if (row_span<FIRST>(a, v) > kLongRow) {  // a whole block takes this row
+    const int32_t slot = atomicAdd(&ctl->n_long, 1);
+    long_rows[slot] = v;
+    return;
+  }
+  const int F = ctl->F;
+  const double sF = ldexp(1.0, F), sIF = ldexp(1.0, -F);
+  const int32_t sv = node_size<FIRST>(s, v);
+  const double dsv = (double)sv;
+  const bool small = (int64_t)sv < smin;
+  Best b{0.0, 0, -1};
+  int32_t cnt = 0;
+  for_row<FIRST>(a, v, 0, 1, [&](int32_t u, int32_t w) {
+    ++cnt;
+    if ((uint32_t)u >= (uint32_t)nn) {
+      raise_err(ctl, kErrInternal);
+      return;
+    }
+    const double g = edge_gain<FIRST>(s, v, dsv, u, w, d, lambda, sF, sIF);
+    if (g > 0.0 || small) {
+      const Best c{g, node_minpt<FIRST>(s, u), u};
+      if (best_before(c, b)) b = c;
+    }
+  });
+  target[v] = b.u;
+  deg[v] = cnt;
+  if (__ballot(b.u >= 0) && (threadIdx.x & (kWave - 1)) == 0)
+    ctl->any_choice = 1;
+}
+
+template <bool FIRST>
 __global__ __launch_bounds__(256) void k_select_long(
-    const int32_t *__restrict__ rp, const int32_t *__restrict__ col,
-    const int32_t *__restrict__ w, NodeIn s, int32_t d, double lambda,
-    int64_t smin, int32_t nn, int32_t *__restrict__ target,
+    int32_t nn, Adj a, NodeIn s, int32_t d, double lambda, int64_t smin,
+    int32_t *__restrict__ target, int32_t *__restrict__ deg,
     const int32_t *__restrict__ long_rows, Ctl *ctl) {
-  __shared__ double sg[256 / kWave];
-  __shared__ int32_t smp[256 / kWave], su[256 / kWave];
   const int32_t n_long = ctl->n_long;
   const int F = ctl->F;
   const double sF = ldexp(1.0, F), sIF = ldexp(1.0, -F);
-  for (int32_t li = blockIdx.x; li < n_long; li += gridDim.x) {
+  const int lane = threadIdx.x & (kWave - 1);
+  const int32_t wave0 = (int32_t)(blockIdx.x * (blockDim.x / kWave) +
+                                  threadIdx.x / kWave);
+  const int32_t nwaves = (int32_t)(gridDim.x * (blockDim.x / kWave));
+  for (int32_t li = wave0; li < n_long; li += nwaves) {
     const int32_t v = long_rows[li];
     if ((uint32_t)v >= (uint32_t)nn) {
       raise_err(ctl, kErrInternal);
@@ -287,31 +360,20 @@ __global__ __launch_bounds__(256) void k_select_long(
     const double dsv = (double)sv;
     const bool small = (int64_t)sv < smin;
     Best b{0.0, 0, -1};
-    for (int32_t e = rp[v] + threadIdx.x; e < rp[v + 1]; e += blockDim.x) {
-      const int32_t u = col[e];
+    int32_t cnt = 0;
+    for_row<FIRST>(a, v, lane, kWave, [&](int32_t u, int32_t w) {
+      ++cnt;
       if ((uint32_t)u >= (uint32_t)nn) {
         raise_err(ctl, kErrInternal);
-        continue;
+        return;
       }
-      const double dsu = (double)node_size<FIRST>(s, u);
-      const double num = dsv * dsu;
-      const double den = dsv + dsu;
-      const double f = num / den;
-      double ss = 0.0;
-      for (int32_t i = 0; i < d; ++i) {
-        const double diff = node_mu<FIRST>(s, v, i, d, sF, sIF) -
-                            node_mu<FIRST>(s, u, i, d, sF, sIF);
-        const double sq = diff * diff;
-        ss = ss + sq;
-      }
-      const double cut = lambda * (double)w[e];
-      const double fit = f * ss;
-      const double g = cut - fit;
+      const double g = edge_gain<FIRST>(s, v, dsv, u, w, d, lambda, sF, sIF);
       if (g > 0.0 || small) {
         const Best c{g, node_minpt<FIRST>(s, u), u};
         if (best_before(c, b)) b = c;
       }
-    }
+    });
+    cnt = wave_sum(cnt);
 #pragma unroll
     for (int off = kWave / 2; off > 0; off >>= 1) {
       Best o;
@@ -320,28 +382,20 @@ __global__ __launch_bounds__(256) void k_select_long(
       o.u = __shfl_xor(b.u, off, kWave);
       if (best_before(o, b)) b = o;
     }
-    const int wid = threadIdx.x / kWave;
-    if ((threadIdx.x & (kWave - 1)) == 0) {
-      sg[wid] = b.g;
-      smp[wid] = b.mp;
-      su[wid] = b.u;
+    if (lane == 0) {
+      target[v] = b.u;
+      deg[v] = cnt;
+      if (b.u >= 0) ctl->any_choice = 1;
     }
-    __syncthreads();
-    if (threadIdx.x == 0) {
-      Best r{sg[0], smp[0], su[0]};
-      for (int q = 1; q < 256 / kWave; ++q) {
-        const Best o{sg[q], smp[q], su[q]};
-        if (best_before(o, r)) r = o;
-      }
-      target[v] = r.u;
-      if (r.u >= 0) ctl->any_choice = 1;
-    }
-    __syncthreads();
   }
 }
 
-// Merge graph -> forest: a node points to its choice, except the lower end
-// of a mutual pair, which becomes a root.  Always writes every parent.
+// ---------------------------------------------------------------------------
+// Step 3: merge graph -> forest -> components
+// ---------------------------------------------------------------------------
+
+// A node points to its choice, except the lower end of a mutual pair, which
+// becomes a root.  Always writes every parent.
 __global__ __launch_bounds__(256) void k_hook(int32_t nn, const int32_t *target,
                                               int32_t *parent, Ctl *ctl) {
   const int32_t v = blockIdx.x * blockDim.x + threadIdx.x;
@@ -393,11 +447,15 @@ struct ScanRoots {
   }
 };
 
+// Component of every node; also counts members (the rank is the node's
+// place among its component's members).
 __global__ __launch_bounds__(256) void k_assign(int32_t nn,
                                                 const int32_t *parent,
                                                 const int32_t *newid,
-                                                int32_t *L, Ctl *ctl) {
-  const int32_t v = blockIdx.x * blockDim.x + threadIdx.x;
+                                                int32_t *L, int32_t *cnt,
+                                                int32_t *rank, Ctl *ctl) {
+  if (!ctl->any_choice) return;
+  const int32_t v = xcd_tid();
   if (v >= nn) return;
   const int32_t r = parent[v];
   int32_t c = 0;
@@ -406,145 +464,452 @@ __global__ __launch_bounds__(256) void k_assign(int32_t nn,
   } else {
     raise_err(ctl, kErrInternal);
   }
+  if ((uint32_t)c >= (uint32_t)ctl->n_next) {
+    raise_err(ctl, kErrInternal);
+    c = 0;
+  }
   L[v] = c;
+  rank[v] = atomicAdd(&cnt[c], 1);
 }
 
-// Step 4 statistics.  acc arrays are the next round's node state.
-__global__ __launch_bounds__(256) void k_zero_acc(int32_t bound, int32_t d,
-                                                  const Ctl *ctl, int32_t *size,
-                                                  int64_t *S, int32_t *minpt,
-                                                  int32_t *cap, int32_t *ndeg) {
+__global__ __launch_bounds__(256) void k_zero_cnt(int32_t bound, const Ctl *ctl,
+                                                  int32_t *cnt) {
   if (!ctl->any_choice) return;
   const int32_t c = blockIdx.x * blockDim.x + threadIdx.x;
-  if (c >= bound || c >= ctl->n_next) return;
-  size[c] = 0;
-  minpt[c] = INT32_MAX;
-  cap[c] = 0;
-  ndeg[c] = 0;
-  for (int32_t i = 0; i < d; ++i) S[(int64_t)c * d + i] = 0;
+  if (c < bound && c < ctl->n_next) cnt[c] = 0;
 }
 
-template <bool FIRST>
-__global__ __launch_bounds__(256) void k_stats_add(
-    int32_t nn, const int32_t *__restrict__ L, const int32_t *__restrict__ rp,
-    NodeIn s, int32_t d, Ctl *ctl, int32_t *size, int64_t *S, int32_t *minpt,
-    int32_t *cap) {
+__global__ __launch_bounds__(256) void k_place(int32_t nn, const int32_t *L,
+                                               const int32_t *moff,
+                                               const int32_t *rank,
+                                               int32_t *mem, Ctl *ctl) {
   if (!ctl->any_choice) return;
   const int32_t v = xcd_tid();
   if (v >= nn) return;
-  const int32_t c = L[v];
-  if ((uint32_t)c >= (uint32_t)ctl->n_next) {
+  const int32_t pos = moff[L[v]] + rank[v];
+  if ((uint32_t)pos < (uint32_t)nn) {
+    mem[pos] = v;
+  } else {
     raise_err(ctl, kErrInternal);
-    return;
-  }
-  atomicAdd(&size[c], node_size<FIRST>(s, v));
-  atomicMin(&minpt[c], node_minpt<FIRST>(s, v));
-  atomicAdd(&cap[c], rp[v + 1] - rp[v]);
-  const double sF = ldexp(1.0, ctl->F);
-  for (int32_t i = 0; i < d; ++i) {
-    int64_t q;
-    if (FIRST)
-      q = (int64_t)rint((double)s.emb[(int64_t)v * d + i] * sF);
-    else
-      q = s.S[(int64_t)v * d + i];
-    atomicAdd(reinterpret_cast<unsigned long long *>(&S[(int64_t)c * d + i]),
-              (unsigned long long)q);
   }
 }
 
-__global__ __launch_bounds__(256) void k_stats_final(int32_t bound, int32_t d,
-                                                     const Ctl *ctl,
-                                                     const int32_t *size,
-                                                     const int64_t *S,
-                                                     double *mu) {
+// ---------------------------------------------------------------------------
+// Step 4 statistics, gathered from the members of each component
+// ---------------------------------------------------------------------------
+struct NodeOut {
+  int32_t *size;
+  int64_t *S;
+  double *mu;
+  int32_t *minpt;
+  int32_t *cap;   // summed member degree = window of the next table
+  int32_t *wl;    // row length (the window until a chunk compacts it)
+  int32_t *cbig;  // components whose window exceeds one chunk
+};
+
+__device__ __forceinline__ void note_window(const NodeOut &o, int32_t c,
+                                            int32_t cap, Ctl *ctl) {
+  o.cap[c] = cap;
+  o.wl[c] = cap;
+  if (cap > kChunk) o.cbig[atomicAdd(&ctl->n_cbig, 1)] = c;
+}
+
+constexpr int kDimChunk = 8;
+
+template <bool FIRST>
+__global__ __launch_bounds__(256) void k_stats(
+    int32_t bound, const int32_t *__restrict__ mem,
+    const int32_t *__restrict__ moff, NodeIn s,
+    const int32_t *__restrict__ deg, int32_t d, NodeOut o,
+    int32_t *__restrict__ big, Ctl *ctl) {
   if (!ctl->any_choice) return;
-  const int64_t t = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
-  const int64_t c = t / d;
+  const int32_t c = xcd_tid();
   if (c >= bound || c >= ctl->n_next) return;
-  const double sIF = ldexp(1.0, -ctl->F);
-  const double q = (double)S[t] / (double)size[c];
-  mu[t] = q * sIF;
+  const int32_t m0 = moff[c], m1 = moff[c + 1];
+  if (m1 - m0 > kBigComp) {
+    big[atomicAdd(&ctl->n_big, 1)] = c;
+    return;
+  }
+  const double sF = ldexp(1.0, ctl->F), sIF = ldexp(1.0, -ctl->F);
+  int32_t size = 0, mp = INT32_MAX, cap = 0;
+  for (int32_t j = m0; j < m1; ++j) {
+    const int32_t m = mem[j];
+    size += node_size<FIRST>(s, m);
+    mp = min(mp, node_minpt<FIRST>(s, m));
+    cap += deg[m];
+  }
+  o.size[c] = size;
+  o.minpt[c] = mp;
+  note_window(o, c, cap, ctl);
+  const double dsz = (double)size;
+  for (int32_t i0 = 0; i0 < d; i0 += kDimChunk) {
+    int64_t acc[kDimChunk];
+#pragma unroll
+    for (int q = 0; q < kDimChunk; ++q) acc[q] = 0;
+    for (int32_t j = m0; j < m1; ++j) {
+      const int32_t m = mem[j];
+#pragma unroll
+      for (int q = 0; q < kDimChunk; ++q)
+        if (i0 + q < d) acc[q] += node_S<FIRST>(s, m, i0 + q, d, sF);
+    }
+#pragma unroll
+    for (int q = 0; q < kDimChunk; ++q) {
+      if (i0 + q < d) {
+        const int64_t t = (int64_t)c * d + i0 + q;
+        o.S[t] = acc[q];
+        const double qv = (double)acc[q] / dsz;
+        o.mu[t] = qv * sIF;
+      }
+    }
+  }
 }
 
-// Contraction into per-component open-addressing tables.  Component A owns
-// slots [toff[A], toff[A] + cap[A]) where cap[A] is the summed degree of its
-// members, an upper bound on its distinct neighbours.
-__global__ __launch_bounds__(256) void k_table_clear(int32_t bound,
-                                                     const Ctl *ctl,
-                                                     uint64_t *keys,
-                                                     int32_t *tw) {
+// Components with many members: one block each, threads stride over the
+// members and the sums are combined in shared memory (integer, so the
+// order does not matter).
+template <bool FIRST>
+__global__ __launch_bounds__(256) void k_stats_big(
+    const int32_t *__restrict__ mem, const int32_t *__restrict__ moff,
+    NodeIn s, const int32_t *__restrict__ deg, int32_t d, NodeOut o,
+    const int32_t *__restrict__ big, Ctl *ctl) {
+  __shared__ unsigned long long sS[64];
+  __shared__ int32_t ssize, smp, scap;
   if (!ctl->any_choice) return;
-  const int32_t s = blockIdx.x * blockDim.x + threadIdx.x;
-  if (s >= bound || s >= ctl->slots) return;
-  keys[s] = kEmpty;
-  tw[s] = 0;
+  const double sF = ldexp(1.0, ctl->F), sIF = ldexp(1.0, -ctl->F);
+  const int32_t n_big = ctl->n_big;
+  for (int32_t bi = blockIdx.x; bi < n_big; bi += gridDim.x) {
+    const int32_t c = big[bi];
+    const int32_t m0 = moff[c], m1 = moff[c + 1];
+    for (int t = threadIdx.x; t < 64; t += blockDim.x) sS[t] = 0ull;
+    if (threadIdx.x == 0) {
+      ssize = 0;
+      smp = INT32_MAX;
+      scap = 0;
+    }
+    __syncthreads();
+    int32_t size = 0, mp = INT32_MAX, cap = 0;
+    for (int32_t j = m0 + threadIdx.x; j < m1; j += blockDim.x) {
+      const int32_t m = mem[j];
+      size += node_size<FIRST>(s, m);
+      mp = min(mp, node_minpt<FIRST>(s, m));
+      cap += deg[m];
+    }
+    atomicAdd(&ssize, size);
+    atomicMin(&smp, mp);
+    atomicAdd(&scap, cap);
+    for (int32_t i0 = 0; i0 < d; i0 += kDimChunk) {
+      int64_t acc[kDimChunk];
+#pragma unroll
+      for (int q = 0; q < kDimChunk; ++q) acc[q] = 0;
+      for (int32_t j = m0 + threadIdx.x; j < m1; j += blockDim.x) {
+        const int32_t m = mem[j];
+#pragma unroll
+        for (int q = 0; q < kDimChunk; ++q)
+          if (i0 + q < d) acc[q] += node_S<FIRST>(s, m, i0 + q, d, sF);
+      }
+#pragma unroll
+      for (int q = 0; q < kDimChunk; ++q) {
+        if (i0 + q < d) {
+          const long long r = wave_sum((long long)acc[q]);
+          if ((threadIdx.x & (kWave - 1)) == 0)
+            atomicAdd(&sS[i0 + q], (unsigned long long)r);
+        }
+      }
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      o.size[c] = ssize;
+      o.minpt[c] = smp;
+      note_window(o, c, scap, ctl);
+    }
+    for (int32_t i = threadIdx.x; i < d; i += blockDim.x) {
+      const int64_t t = (int64_t)c * d + i;
+      const int64_t v = (int64_t)sS[i];
+      o.S[t] = v;
+      const double qv = (double)v / (double)ssize;
+      o.mu[t] = qv * sIF;
+    }
+    __syncthreads();
+  }
 }
 
-__global__ __launch_bounds__(256) void k_insert(
-    int32_t ed, const int32_t *__restrict__ src, const int32_t *__restrict__ col,
-    const int32_t *__restrict__ w, const int32_t *__restrict__ L,
+// ---------------------------------------------------------------------------
+// Step 4 contraction into the next table.  Component A owns the slots
+// [toff[A], toff[A] + cap[A]); cap[A], the summed degree of its members,
+// bounds its distinct neighbours, so open addressing always finds a slot.
+//
+// Chunks: block j takes the components whose window starts in
+// [j*kChunk, (j+1)*kChunk) and whose window is at most kChunk slots; their
+// windows lie inside 2*kChunk slots from j*kChunk, which the block keeps in
+// LDS.  It walks their members' rows in batches of 256 members (the entries
+// of a batch are spread over all threads), adds every relabelled edge to
+// the LDS window of its component (parallel edges add their weights,
+// edges inside a component are dropped), then writes each row compacted to
+// the start of its window.  Larger windows go through the global path.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ int32_t lower_bound_i32(const int32_t *a,
+                                                   int32_t n, int32_t x) {
+  int32_t lo = 0, hi = n;
+  while (lo < hi) {
+    const int32_t mid = (lo + hi) >> 1;
+    if (a[mid] < x) lo = mid + 1;
+    else hi = mid;
+  }
+  return lo;
+}
+
+// Loads a batch of members into LDS with the exclusive prefix of their row
+// spans (members of skipped components count 0); returns the entry total.
+template <bool FIRST, class Keep>
+__device__ __forceinline__ int32_t load_batch(const Adj &a,
+                                              const int32_t *__restrict__ mem,
+                                              int32_t idx0, int32_t idx1,
+                                              int32_t *pre, int32_t *bm,
+                                              int32_t *wsum, Keep &&keep) {
+  const int32_t idx = idx0 + (int32_t)threadIdx.x;
+  int32_t m = -1, span = 0;
+  if (idx < idx1) {
+    m = mem[idx];
+    if (keep(m)) span = row_span<FIRST>(a, m);
+  }
+  int32_t total;
+  const int32_t excl = block_excl_scan<256>(span, wsum, &total);
+  pre[threadIdx.x] = excl;
+  bm[threadIdx.x] = m;
+  if (threadIdx.x == 0) pre[kBatch] = total;
+  __syncthreads();
+  return total;
+}
+
+// Member and entry of flat index f of the batch.
+__device__ __forceinline__ void batch_find(const int32_t *pre, int32_t f,
+                                           int32_t &slot, int32_t &j) {
+  int32_t lo = 0, hi = kBatch;
+  while (hi - lo > 1) {
+    const int32_t mid = (lo + hi) >> 1;
+    if (pre[mid] <= f) lo = mid;
+    else hi = mid;
+  }
+  slot = lo;
+  j = f - pre[lo];
+}
+
+template <bool FIRST>
+__global__ __launch_bounds__(256) void k_contract_chunk(
+    int32_t nn, Adj a, const int32_t *__restrict__ L,
+    const int32_t *__restrict__ mem, const int32_t *__restrict__ moff,
     const int32_t *__restrict__ toff, const int32_t *__restrict__ cap,
-    uint64_t *keys, int32_t *tw, int32_t *ndeg, int32_t nn, int32_t table_cap,
-    Ctl *ctl) {
+    uint64_t *__restrict__ tbl, int32_t *__restrict__ wl, Ctl *ctl) {
+  __shared__ int32_t kb[2 * kChunk];
+  __shared__ int32_t kw[2 * kChunk];
+  __shared__ int32_t pre[kBatch + 1];
+  __shared__ int32_t bm[kBatch];
+  __shared__ int32_t wsum[256 / kWave];
+  __shared__ int32_t crange[2];
   if (!ctl->any_choice) return;
-  const int32_t e = xcd_tid();
-  if (e >= ed) return;
-  const int32_t a = src[e], b = col[e];
-  if ((uint32_t)a >= (uint32_t)nn || (uint32_t)b >= (uint32_t)nn) {
-    raise_err(ctl, kErrInternal);
-    return;
-  }
-  const int32_t A = L[a];
-  const int32_t B = L[b];
-  if (A == B) return;  // edge inside a merged component
   const int32_t nc = ctl->n_next;
-  if ((uint32_t)A >= (uint32_t)nc || (uint32_t)B >= (uint32_t)nc) {
-    raise_err(ctl, kErrInternal);
-    return;
+  const int32_t j0 = xcd_block() * kChunk;
+  if (j0 >= ctl->slots) return;
+  if (threadIdx.x == 0) {
+    crange[0] = lower_bound_i32(toff, nc, j0);
+    crange[1] = lower_bound_i32(toff, nc, j0 + kChunk);
   }
-  const int32_t c = cap[A];
-  const int32_t base = toff[A];
-  if (c <= 0 || base < 0 || base + c > ctl->slots || base + c > table_cap) {
-    raise_err(ctl, kErrInternal);
-    return;
+  for (int t = threadIdx.x; t < 2 * kChunk; t += blockDim.x) {
+    kb[t] = -1;
+    kw[t] = 0;
   }
-  const uint64_t key = ((uint64_t)(uint32_t)A << 32) | (uint32_t)B;
-  uint32_t h = ((uint32_t)B * 2654435761u) % (uint32_t)c;
-  for (int32_t probe = 0; probe < c; ++probe) {
+  __syncthreads();
+  const int32_t c_lo = crange[0], c_hi = crange[1];
+  const int32_t m_lo = moff[c_lo];
+  // a window larger than a chunk can only be the last one starting here
+  // (the next window starts past the chunk); its members are not walked
+  const int32_t m_hi =
+      (c_hi > c_lo && cap[c_hi - 1] > kChunk) ? moff[c_hi - 1] : moff[c_hi];
+  auto keep = [&](int32_t m) {
+    const int32_t c = cap[L[m]];
+    return c > 0 && c <= kChunk;
+  };
+  for (int32_t b0 = m_lo; b0 < m_hi; b0 += kBatch) {
+    const int32_t total = load_batch<FIRST>(a, mem, b0, m_hi, pre, bm, wsum,
+                                            keep);
+    for (int32_t f = threadIdx.x; f < total; f += blockDim.x) {
+      int32_t slot, j, u, w;
+      batch_find(pre, f, slot, j);
+      const int32_t m = bm[slot];
+      if (!row_entry<FIRST>(a, m, j, u, w)) continue;
+      if ((uint32_t)u >= (uint32_t)nn) {
+        raise_err(ctl, kErrInternal);
+        continue;
+      }
+      const int32_t A = L[m], B = L[u];
+      if (A == B) continue;  // edge inside a merged component
+      const int32_t lb = toff[A] - j0, cp = cap[A];
+      if (lb < 0 || cp <= 0 || lb + cp > 2 * kChunk) {
+        raise_err(ctl, kErrInternal);
+        continue;
+      }
+      uint32_t h = ((uint32_t)B * 2654435761u) % (uint32_t)cp;
+      int32_t probe = 0;
+      for (; probe < cp; ++probe) {
+        const int32_t old = atomicCAS(&kb[lb + h], -1, B);
+        if (old == -1 || old == B) {
+          atomicAdd(&kw[lb + h], w);
+          break;
+        }
+        h = (h + 1 == (uint32_t)cp) ? 0u : h + 1;
+      }
+      if (probe == cp) raise_err(ctl, kErrInternal);
+    }
+    __syncthreads();
+  }
+  // rows compacted to the start of their windows
+  int32_t uniq = 0;
+  for (int32_t c = c_lo + (int32_t)threadIdx.x; c < c_hi; c += blockDim.x) {
+    const int32_t cp = cap[c];
+    if (cp <= 0 || cp > kChunk) continue;
+    const int32_t base = toff[c], lb = base - j0;
+    int32_t out = 0;
+    for (int32_t t = lb; t < lb + cp; ++t) {
+      const int32_t B = kb[t];
+      if (B >= 0) {
+        tbl[base + out] = ((uint64_t)(uint32_t)B << 32) | (uint32_t)kw[t];
+        ++out;
+      }
+    }
+    wl[c] = out;
+    uniq += out;
+  }
+  int32_t tot;
+  block_excl_scan<256>(uniq, wsum, &tot);
+  if (threadIdx.x == 0 && tot) atomicAdd(&ctl->e_next, tot);
+}
+
+// Global path for windows larger than a chunk: the window is cleared, then
+// tiles of 256 members are pre-aggregated in an LDS table (one component per
+// tile, keyed by neighbour) and flushed into the window with atomics.  Rows
+// keep their empty slots.
+__global__ __launch_bounds__(256) void k_clear_big(
+    const int32_t *__restrict__ cbig, const int32_t *__restrict__ toff,
+    const int32_t *__restrict__ cap, uint64_t *tbl, int32_t tcap, Ctl *ctl) {
+  if (!ctl->any_choice) return;
+  const int32_t nb = ctl->n_cbig;
+  for (int32_t bi = blockIdx.x; bi < nb; bi += gridDim.x) {
+    const int32_t c = cbig[bi];
+    const int32_t base = toff[c], cp = cap[c];
+    if (base < 0 || base + cp > tcap) {
+      raise_err(ctl, kErrInternal);
+      continue;
+    }
+    for (int32_t t = threadIdx.x; t < cp; t += blockDim.x)
+      tbl[base + t] = kEmpty;
+  }
+}
+
+// Adds weight w of the edge A -> B to A's window; true for a new slot.
+__device__ __forceinline__ bool table_add(uint64_t *tbl, int32_t base,
+                                          int32_t cap, int32_t B, int32_t w,
+                                          Ctl *ctl) {
+  uint32_t h = ((uint32_t)B * 2654435761u) % (uint32_t)cap;
+  const unsigned long long mine =
+      ((unsigned long long)(uint32_t)B << 32) | (uint32_t)w;
+  for (int32_t probe = 0; probe < cap; ++probe) {
     unsigned long long *slot =
-        reinterpret_cast<unsigned long long *>(&keys[base + h]);
-    const unsigned long long old = atomicCAS(slot, kEmpty, key);
-    if (old == kEmpty) {
-      atomicAdd(&ndeg[A], 1);
-      atomicAdd(&tw[base + h], w[e]);
-      return;
+        reinterpret_cast<unsigned long long *>(tbl + base + h);
+    unsigned long long cur = __atomic_load_n(slot, __ATOMIC_RELAXED);
+    if (cur == kEmpty) {
+      cur = atomicCAS(slot, kEmpty, mine);
+      if (cur == kEmpty) return true;
     }
-    if (old == key) {
-      atomicAdd(&tw[base + h], w[e]);
-      return;
+    if ((int32_t)(cur >> 32) == B) {
+      atomicAdd(slot, (unsigned long long)(uint32_t)w);
+      return false;
     }
-    h = (h + 1 == (uint32_t)c) ? 0u : h + 1;
+    h = (h + 1 == (uint32_t)cap) ? 0u : h + 1;
   }
   raise_err(ctl, kErrInternal);
+  return false;
 }
 
-struct ScanCompact {
-  const uint64_t *keys;
-  const int32_t *tw;
-  const int32_t *slots;
-  int32_t *col, *w, *src;
-  int32_t cap;  // capacity of col/w/src
-  __device__ int32_t value(int32_t s) const {
-    return (s < *slots && keys[s] != kEmpty) ? 1 : 0;
+template <bool FIRST>
+__global__ __launch_bounds__(256) void k_contract_big(
+    int32_t nn, Adj a, const int32_t *__restrict__ L,
+    const int32_t *__restrict__ mem, const int32_t *__restrict__ moff,
+    const int32_t *__restrict__ toff, const int32_t *__restrict__ cap,
+    const int32_t *__restrict__ cbig, uint64_t *tbl, int32_t tcap, Ctl *ctl) {
+  __shared__ int32_t pk[kPreSlots];
+  __shared__ int32_t pw[kPreSlots];
+  __shared__ int32_t pre[kBatch + 1];
+  __shared__ int32_t bm[kBatch];
+  __shared__ int32_t wsum[256 / kWave];
+  __shared__ int32_t tile_c, tile_i;
+  if (!ctl->any_choice) return;
+  const int32_t nb = ctl->n_cbig;
+  int32_t added = 0;
+  for (int32_t t = blockIdx.x;; t += gridDim.x) {
+    if (threadIdx.x == 0) {  // which component and which tile of it
+      int32_t rest = t, c = -1, i = 0;
+      for (int32_t bi = 0; bi < nb; ++bi) {
+        const int32_t cc = cbig[bi];
+        const int32_t tiles = (moff[cc + 1] - moff[cc] + kBatch - 1) / kBatch;
+        if (rest < tiles) {
+          c = cc;
+          i = rest;
+          break;
+        }
+        rest -= tiles;
+      }
+      tile_c = c;
+      tile_i = i;
+    }
+    for (int q = threadIdx.x; q < kPreSlots; q += blockDim.x) {
+      pk[q] = -1;
+      pw[q] = 0;
+    }
+    __syncthreads();
+    const int32_t A = tile_c;
+    if (A < 0) break;
+    const int32_t base = toff[A], cp = cap[A];
+    if (base < 0 || cp <= 0 || base + cp > tcap) {
+      raise_err(ctl, kErrInternal);
+      __syncthreads();
+      continue;
+    }
+    const int32_t i0 = moff[A] + tile_i * kBatch;
+    const int32_t i1 = min(moff[A + 1], i0 + kBatch);
+    const int32_t total = load_batch<FIRST>(a, mem, i0, i1, pre, bm, wsum,
+                                            [](int32_t) { return true; });
+    for (int32_t f = threadIdx.x; f < total; f += blockDim.x) {
+      int32_t slot, j, u, w;
+      batch_find(pre, f, slot, j);
+      const int32_t m = bm[slot];
+      if (!row_entry<FIRST>(a, m, j, u, w)) continue;
+      if ((uint32_t)u >= (uint32_t)nn) {
+        raise_err(ctl, kErrInternal);
+        continue;
+      }
+      const int32_t B = L[u];
+      if (B == A) continue;
+      uint32_t h = ((uint32_t)B * 2654435761u) & (kPreSlots - 1);
+      bool done = false;
+      for (int32_t probe = 0; probe < 32 && !done; ++probe) {
+        const int32_t old = atomicCAS(&pk[h], -1, B);
+        if (old == -1 || old == B) {
+          atomicAdd(&pw[h], w);
+          done = true;
+        }
+        h = (h + 1) & (kPreSlots - 1);
+      }
+      if (!done) added += table_add(tbl, base, cp, B, w, ctl) ? 1 : 0;
+    }
+    __syncthreads();
+    for (int q = threadIdx.x; q < kPreSlots; q += blockDim.x)
+      if (pk[q] >= 0) added += table_add(tbl, base, cp, pk[q], pw[q], ctl);
+    __syncthreads();
   }
-  __device__ void emit(int32_t s, int32_t excl, int32_t val) const {
-    if (!val || excl >= cap) return;
-    const uint64_t k = keys[s];
-    col[excl] = (int32_t)(uint32_t)(k & 0xffffffffull);
-    src[excl] = (int32_t)(k >> 32);
-    w[excl] = tw[s];
-  }
-};
+  added = wave_sum(added);
+  if ((threadIdx.x & (kWave - 1)) == 0 && added)
+    atomicAdd(&ctl->e_next, added);
+}
 
 // point -> current node map, composed every merging round
 template <bool FIRST>
@@ -658,15 +1023,14 @@ __global__ void k_energy_sum(const double *partial, int32_t nb, Ctl *ctl) {
   ctl->fid_total = s;
 }
 
-__global__ __launch_bounds__(256) void k_weight_sum(int32_t ed,
-                                                    const int32_t *w,
+// Sum of the weights of all rows (both directions of every edge).
+__global__ __launch_bounds__(256) void k_weight_sum(int32_t nn, Adj a,
                                                     Ctl *ctl) {
   long long acc = 0;
-  for (int32_t e = blockIdx.x * blockDim.x + threadIdx.x; e < ed;
-       e += gridDim.x * blockDim.x)
-    acc += w[e];
-  for (int off = kWave / 2; off > 0; off >>= 1)
-    acc += __shfl_xor(acc, off, kWave);
+  for (int32_t v = blockIdx.x * blockDim.x + threadIdx.x; v < nn;
+       v += gridDim.x * blockDim.x)
+    for_row<false>(a, v, 0, 1, [&](int32_t, int32_t w) { acc += w; });
+  acc = wave_sum(acc);
   if ((threadIdx.x & (kWave - 1)) == 0 && acc)
     atomicAdd(reinterpret_cast<unsigned long long *>(&ctl->cut_w2),
               (unsigned long long)acc);
@@ -686,52 +1050,57 @@ namespace {
 
 struct Bufs {
   float *emb_int;
-  int32_t *fwd, *rev, *cursor;
-  int32_t *rp[2], *col[2], *w[2], *src[2];
+  int32_t *nbr_clean;                   // sanitised caller table
+  int32_t *rrp, *rcol, *rown, *rev, *cursor;  // first-round reverse list
+  int32_t *ws[2], *wl[2];               // row windows (= toff, cap)
+  uint64_t *tbl[2];
   int32_t *size[2], *minpt[2];
   int64_t *S[2];
   double *mu;
-  int32_t *target, *parent, *newid, *L, *cap, *toff, *ndeg, *long_rows;
-  uint64_t *keys;
-  int32_t *tw;
-  int32_t *M, *mark, *rank;
+  int32_t *target, *deg, *parent, *newid, *L, *cnt, *rank, *moff, *mem;
+  int32_t *long_rows, *big, *cbig, *capn;
+  int32_t *M, *mark, *lrank;
   int32_t *bsum, *tmp;
   double *partial;
 };
 
 int64_t edge_bound(int32_t n, int32_t k) { return 2 * (int64_t)n * k; }
 
-void carve(Arena &a, int32_t n, int32_t d, int32_t k, bool need_emb,
-           Bufs *b) {
+void carve(Arena &a, int32_t n, int32_t d, int32_t k, Bufs *b) {
   const int64_t ed = edge_bound(n, k);
   const size_t n1 = (size_t)n + 1;
-  b->emb_int = need_emb ? a.take<float>((size_t)n * d) : nullptr;
-  b->fwd = a.take<int32_t>(n1);
+  b->emb_int = a.take<float>((size_t)n * d);
+  b->nbr_clean = a.take<int32_t>((size_t)n * k);
+  b->rrp = a.take<int32_t>(n1);
+  b->rcol = a.take<int32_t>((size_t)n * k);
+  b->rown = a.take<int32_t>((size_t)n * k);
   b->rev = a.take<int32_t>(n1);
   b->cursor = a.take<int32_t>(n1);
   for (int j = 0; j < 2; ++j) {
-    b->rp[j] = a.take<int32_t>(n1);
-    b->col[j] = a.take<int32_t>(ed);
-    b->w[j] = a.take<int32_t>(ed);
-    b->src[j] = a.take<int32_t>(ed);
+    b->ws[j] = a.take<int32_t>(n1);
+    b->wl[j] = a.take<int32_t>(n1);
+    b->tbl[j] = a.take<uint64_t>(ed);
     b->size[j] = a.take<int32_t>(n1);
     b->minpt[j] = a.take<int32_t>(n1);
     b->S[j] = a.take<int64_t>((size_t)n * d);
   }
   b->mu = a.take<double>((size_t)n * d);
   b->target = a.take<int32_t>(n1);
+  b->deg = a.take<int32_t>(n1);
   b->parent = a.take<int32_t>(n1);
   b->newid = a.take<int32_t>(n1);
   b->L = a.take<int32_t>(n1);
-  b->cap = a.take<int32_t>(n1);
-  b->toff = a.take<int32_t>(n1);
-  b->ndeg = a.take<int32_t>(n1);
+  b->cnt = a.take<int32_t>(n1);
+  b->rank = a.take<int32_t>(n1);
+  b->moff = a.take<int32_t>(n1);
+  b->mem = a.take<int32_t>(n1);
   b->long_rows = a.take<int32_t>(n1);
-  b->keys = a.take<uint64_t>(ed);
-  b->tw = a.take<int32_t>(ed);
+  b->big = a.take<int32_t>(n1);
+  b->cbig = a.take<int32_t>(n1);
+  b->capn = a.take<int32_t>(n1);
   b->M = a.take<int32_t>(n1);
   b->mark = a.take<int32_t>(n1);
-  b->rank = a.take<int32_t>(n1);
+  b->lrank = a.take<int32_t>(n1);
   b->bsum = a.take<int32_t>(scan_blocks(ed + n1) + 2);
   b->tmp = a.take<int32_t>(8);
   b->partial = a.take<double>(kEnergyBlocks);
@@ -742,6 +1111,7 @@ inline dim3 blocks_for(int64_t n, int nt = 256) {
   if (b < 1) b = 1;
   return dim3((unsigned)b);
 }
+inline dim3 xblocks_for(int64_t n) { return dim3(xcd_grid(blocks_for(n).x)); }
 
 int status_from_err(uint32_t err) {
   if (err & kErrNonFinite) {
@@ -753,7 +1123,7 @@ int status_from_err(uint32_t err) {
     return -3;
   }
   if (err & kErrBadIndex) {
-    set_error("neighbour index or label out of range");
+    set_error("neighbour index out of range");
     return -1;
   }
   if (err & kErrJump) {
@@ -764,20 +1134,22 @@ int status_from_err(uint32_t err) {
   return -5;
 }
 
+// One merge round on nn nodes whose rows hold ed directed entries.
 template <bool FIRST>
-void launch_round(const Bufs &b, int cur, int32_t n, int32_t k, int32_t nn,
-                  int32_t ed, int32_t d, const NodeIn &s, double lambda, int64_t smin,
-                  Ctl *ctl, hipStream_t st) {
+void launch_round(const Bufs &b, const Adj &adj, int cur, int32_t n,
+                  int32_t k, int32_t nn, int32_t ed, int32_t d,
+                  const NodeIn &s, double lambda, int64_t smin, Ctl *ctl,
+                  hipStream_t st) {
   const int nxt = 1 - cur;
   const int32_t tcap = (int32_t)edge_bound(n, k);
   hipLaunchKernelGGL(k_round_init, dim3(1), dim3(64), 0, st, ctl);
   prof_begin("select", st);
-  hipLaunchKernelGGL(k_select<FIRST>, xcd_grid(blocks_for(nn).x), dim3(256), 0,
-                     st, nn, b.rp[cur], b.col[cur], b.w[cur], s, d, lambda,
-                     smin, b.target, b.long_rows, ctl);
+  hipLaunchKernelGGL(k_select<FIRST>, xblocks_for(nn), dim3(256), 0, st, nn,
+                     adj, s, d, lambda, smin, b.target, b.deg, b.long_rows,
+                     ctl);
   hipLaunchKernelGGL(k_select_long<FIRST>, dim3(kLongGrid), dim3(256), 0, st,
-                     b.rp[cur], b.col[cur], b.w[cur], s, d, lambda, smin, nn,
-                     b.target, b.long_rows, ctl);
+                     nn, adj, s, d, lambda, smin, b.target, b.deg, b.long_rows,
+                     ctl);
   prof_end(st);
   prof_begin("union", st);
   hipLaunchKernelGGL(k_hook, blocks_for(nn), dim3(256), 0, st, nn, b.target,
@@ -785,38 +1157,39 @@ void launch_round(const Bufs &b, int cur, int32_t n, int32_t k, int32_t nn,
   hipLaunchKernelGGL(k_jump, blocks_for(nn), dim3(256), 0, st, nn, b.parent,
                      ctl);
   device_scan(ScanRoots{b.parent, b.newid, nn}, nn, b.bsum, &ctl->n_next, st);
+  hipLaunchKernelGGL(k_zero_cnt, blocks_for(nn), dim3(256), 0, st, nn, ctl,
+                     b.cnt);
+  hipLaunchKernelGGL(k_assign, xblocks_for(nn), dim3(256), 0, st, nn,
+                     b.parent, b.newid, b.L, b.cnt, b.rank, ctl);
   prof_end(st);
-  hipLaunchKernelGGL(k_assign, blocks_for(nn), dim3(256), 0, st, nn, b.parent,
-                     b.newid, b.L, ctl);
   prof_begin("stats", st);
-  hipLaunchKernelGGL(k_zero_acc, blocks_for(nn), dim3(256), 0, st, nn, d, ctl,
-                     b.size[nxt], b.S[nxt], b.minpt[nxt], b.cap, b.ndeg);
-  hipLaunchKernelGGL(k_stats_add<FIRST>, xcd_grid(blocks_for(nn).x), dim3(256),
-                     0, st, nn,
-                     b.L, b.rp[cur], s, d, ctl, b.size[nxt], b.S[nxt],
-                     b.minpt[nxt], b.cap);
-  hipLaunchKernelGGL(k_stats_final, blocks_for((int64_t)nn * d), dim3(256), 0,
-                     st, nn, d, ctl, b.size[nxt], b.S[nxt], b.mu);
+  device_scan(ScanArray{b.cnt, b.moff, nn, &ctl->n_next}, nn + 1, b.bsum,
+              b.tmp, st);
+  hipLaunchKernelGGL(k_place, xblocks_for(nn), dim3(256), 0, st, nn, b.L,
+                     b.moff, b.rank, b.mem, ctl);
+  const NodeOut o{b.size[nxt], b.S[nxt], b.mu,    b.minpt[nxt],
+                  b.capn,      b.wl[nxt], b.cbig};
+  hipLaunchKernelGGL(k_stats<FIRST>, xblocks_for(nn), dim3(256), 0, st, nn,
+                     b.mem, b.moff, s, b.deg, d, o, b.big, ctl);
+  hipLaunchKernelGGL(k_stats_big<FIRST>, dim3(kBigGrid), dim3(256), 0, st,
+                     b.mem, b.moff, s, b.deg, d, o, b.big, ctl);
   prof_end(st);
   prof_begin("contract", st);
-  device_scan(ScanArray{b.cap, b.toff, nn, &ctl->n_next}, nn + 1, b.bsum,
+  device_scan(ScanArray{b.capn, b.ws[nxt], nn, &ctl->n_next}, nn + 1, b.bsum,
               &ctl->slots, st);
-  hipLaunchKernelGGL(k_table_clear, blocks_for(ed), dim3(256), 0, st, ed, ctl,
-                     b.keys, b.tw);
-  hipLaunchKernelGGL(k_insert, xcd_grid(blocks_for(ed).x), dim3(256), 0, st,
-                     ed,
-                     b.src[cur], b.col[cur], b.w[cur], b.L, b.toff, b.cap,
-                     b.keys, b.tw, b.ndeg, nn, tcap, ctl);
-  device_scan(ScanArray{b.ndeg, b.rp[nxt], nn, &ctl->n_next}, nn + 1, b.bsum,
-              &ctl->e_next, st);
-  device_scan(ScanCompact{b.keys, b.tw, &ctl->slots, b.col[nxt], b.w[nxt],
-                          b.src[nxt], ed},
-              ed, b.bsum, b.tmp, st);
+  hipLaunchKernelGGL(k_contract_chunk<FIRST>,
+                     dim3(xcd_grid((ed + kChunk - 1) / kChunk)), dim3(256), 0,
+                     st, nn, adj, b.L, b.mem, b.moff, b.ws[nxt], b.capn,
+                     b.tbl[nxt], b.wl[nxt], ctl);
+  hipLaunchKernelGGL(k_clear_big, dim3(kBigGrid), dim3(256), 0, st, b.cbig,
+                     b.ws[nxt], b.capn, b.tbl[nxt], tcap, ctl);
+  hipLaunchKernelGGL(k_contract_big<FIRST>, dim3(kBigGrid), dim3(256), 0, st,
+                     nn, adj, b.L, b.mem, b.moff, b.ws[nxt], b.capn, b.cbig,
+                     b.tbl[nxt], tcap, ctl);
   prof_end(st);
   prof_begin("compose", st);
-  hipLaunchKernelGGL(k_compose<FIRST>, xcd_grid(blocks_for(n).x), dim3(256), 0,
-                     st, n, nn,
-                     b.M, b.L, ctl);
+  hipLaunchKernelGGL(k_compose<FIRST>, xblocks_for(n), dim3(256), 0, st, n,
+                     nn, b.M, b.L, ctl);
   prof_end(st);
 }
 
@@ -824,12 +1197,12 @@ void launch_round(const Bufs &b, int cur, int32_t n, int32_t k, int32_t nn,
 
 void ladder_reserve(Arena &a, int32_t n, int32_t d, int32_t k) {
   Bufs b;
-  carve(a, n, d, k, true, &b);
+  carve(a, n, d, k, &b);
 }
 
 int ladder_run(const LadderArgs &g, Ctl *ctl, Arena &a, hipStream_t st) {
   Bufs b;
-  carve(a, g.n, g.d, g.k, true, &b);
+  carve(a, g.n, g.d, g.k, &b);
   Ctl *h = pinned_ctl();
   if (!h) {
     set_error("hipHostMalloc of the control block failed");
@@ -845,35 +1218,50 @@ int ladder_run(const LadderArgs &g, Ctl *ctl, Arena &a, hipStream_t st) {
                        0, st, g.emb, g.perm, n, d, b.emb_int);
     emb = b.emb_int;
   }
-  hipLaunchKernelGGL(k_maxabs, dim3(256), dim3(256), 0, st, emb,
+  hipLaunchKernelGGL(k_maxabs, dim3(2048), dim3(256), 0, st, emb,
                      (int64_t)n * d, ctl);
   hipLaunchKernelGGL(k_fixshift, dim3(1), dim3(64), 0, st, ctl, n);
 
-  // graph (Step 0: the superpoint adjacency starts as the kNN graph)
+  // first-round graph (Step 0: the superpoint adjacency is the kNN graph)
+  prof_begin("graph_build", st);
+  const int32_t *nbr = g.nbr;
+  if (g.check_nbr) {
+    hipLaunchKernelGGL(k_sanitize, blocks_for(n), dim3(256), 0, st, g.nbr, n,
+                       k, b.nbr_clean, ctl);
+    nbr = b.nbr_clean;
+  }
   hipLaunchKernelGGL(k_fill_i32, blocks_for(n), dim3(256), 0, st, b.rev,
                      (int64_t)n, 0);
   hipLaunchKernelGGL(k_fill_i32, blocks_for(n), dim3(256), 0, st, b.cursor,
                      (int64_t)n, 0);
-  prof_begin("graph_build", st);
-  hipLaunchKernelGGL(k_graph_count, xcd_grid(blocks_for(n).x), dim3(256), 0,
-                     st, g.nbr, n,
-                     k, b.fwd, b.rev, ctl);
-  device_scan(ScanDeg{b.fwd, b.rev, b.rp[0], n}, n + 1, b.bsum, &ctl->e_next,
+  hipLaunchKernelGGL(k_rev_count, xblocks_for(n), dim3(256), 0, st, nbr, n, k,
+                     b.rev, ctl);
+  device_scan(ScanArray{b.rev, b.rrp, n, nullptr}, n + 1, b.bsum, &ctl->e_rev,
               st);
-  hipLaunchKernelGGL(k_graph_fill, xcd_grid(blocks_for(n).x), dim3(256), 0,
-                     st, g.nbr, n,
-                     k, b.fwd, b.rp[0], b.cursor, b.col[0], b.w[0], b.src[0],
-                     ctl);
+  hipLaunchKernelGGL(k_rev_fill, xblocks_for(n), dim3(256), 0, st, nbr, n, k,
+                     b.rrp, b.cursor, b.rcol, b.rown, ctl);
   prof_end(st);
   if ((rc = read_ctl(ctl, h, st))) return rc;
   if (h->err) return status_from_err(h->err);
-  int32_t ed = h->e_next;
-  if ((int64_t)ed > edge_bound(n, k) || ed < 0) {
+  int64_t ed64 = (int64_t)h->e_fwd + h->e_rev;
+  if (ed64 > edge_bound(n, k) || h->e_rev < 0 || h->e_fwd < 0) {
     set_error("graph larger than its bound");
     return -5;
   }
-  // algorithmic bytes: read the n*k table, write 12 bytes per undirected edge
+  int32_t ed = (int32_t)ed64;  // directed entries of the current graph
+  const int32_t ed0 = ed;
   prof_bytes("graph_build", 4.0 * n * k + 12.0 * (ed / 2));
+
+  Adj adj;
+  adj.nbr = nbr;
+  adj.k = k;
+  adj.rrp = b.rrp;
+  adj.rcol = b.rcol;
+  adj.rown = b.rown;
+  adj.n_rev = h->e_rev;
+  adj.ws = nullptr;
+  adj.wl = nullptr;
+  adj.tbl = nullptr;
 
   int cur = 0;
   bool first = true;
@@ -896,13 +1284,15 @@ int ladder_run(const LadderArgs &g, Ctl *ctl, Arena &a, hipStream_t st) {
         s.S = nullptr;
         s.mu = nullptr;
         s.minpt = nullptr;
-        launch_round<true>(b, cur, n, k, nn, ed, d, s, lambda, smin, ctl, st);
+        launch_round<true>(b, adj, cur, n, k, nn, ed, d, s, lambda, smin, ctl,
+                           st);
       } else {
         s.size = b.size[cur];
         s.S = b.S[cur];
         s.mu = b.mu;
         s.minpt = b.minpt[cur];
-        launch_round<false>(b, cur, n, k, nn, ed, d, s, lambda, smin, ctl, st);
+        launch_round<false>(b, adj, cur, n, k, nn, ed, d, s, lambda, smin,
+                            ctl, st);
       }
       if ((rc = read_ctl(ctl, h, st))) return rc;
       if (h->err) return status_from_err(h->err);
@@ -921,15 +1311,19 @@ int ladder_run(const LadderArgs &g, Ctl *ctl, Arena &a, hipStream_t st) {
         }
       }
       if (!h->any_choice) break;  // Step 1: no candidate merge
-      if (h->n_next < 1 || h->n_next >= nn || h->e_next < 0 || h->e_next > ed) {
-        set_error("round sizes out of range (%d nodes, %d edges)", h->n_next,
-                  h->e_next);
+      if (h->n_next < 1 || h->n_next >= nn || h->e_next < 0 ||
+          h->e_next > ed || h->slots != ed) {
+        set_error("round sizes out of range (%d nodes, %d edges, %d slots)",
+                  h->n_next, h->e_next, h->slots);
         return -5;
       }
       cur = 1 - cur;
       first = false;
       nn = h->n_next;
       ed = h->e_next;
+      adj.ws = b.ws[cur];
+      adj.wl = b.wl[cur];
+      adj.tbl = b.tbl[cur];
       if (nn == 1) break;  // a single component is left
     }
 
@@ -942,9 +1336,10 @@ int ladder_run(const LadderArgs &g, Ctl *ctl, Arena &a, hipStream_t st) {
                          (int64_t)n, 0);
       hipLaunchKernelGGL(k_mark, blocks_for(nn), dim3(256), 0, st, nn,
                          b.minpt[cur], b.mark, n, ctl);
-      device_scan(ScanArray{b.mark, b.rank, n, nullptr}, n, b.bsum, b.tmp, st);
+      device_scan(ScanArray{b.mark, b.lrank, n, nullptr}, n, b.bsum, b.tmp,
+                  st);
       hipLaunchKernelGGL(k_labels, blocks_for(n), dim3(256), 0, st, n, nn,
-                         g.inv, b.M, b.minpt[cur], b.rank, out, ctl);
+                         g.inv, b.M, b.minpt[cur], b.lrank, out, ctl);
     }
     g.n_comp[l] = nn;
     if (g.want_energy && g.energy) {
@@ -953,15 +1348,18 @@ int ladder_run(const LadderArgs &g, Ctl *ctl, Arena &a, hipStream_t st) {
         hipLaunchKernelGGL(k_energy_fid<true>, dim3(kEnergyBlocks), dim3(256),
                            0, st, n, d, nn, emb, b.M, b.mu, ctl, b.partial);
       else
-        hipLaunchKernelGGL(k_energy_fid<false>, dim3(kEnergyBlocks), dim3(256),
-                           0, st, n, d, nn, emb, b.M, b.mu, ctl, b.partial);
+        hipLaunchKernelGGL(k_energy_fid<false>, dim3(kEnergyBlocks),
+                           dim3(256), 0, st, n, d, nn, emb, b.M, b.mu, ctl,
+                           b.partial);
       hipLaunchKernelGGL(k_energy_sum, dim3(1), dim3(64), 0, st, b.partial,
                          kEnergyBlocks, ctl);
-      hipLaunchKernelGGL(k_weight_sum, dim3(256), dim3(256), 0, st, ed,
-                         b.w[cur], ctl);
+      if (!first)
+        hipLaunchKernelGGL(k_weight_sum, dim3(256), dim3(256), 0, st, nn, adj,
+                           ctl);
       if ((rc = read_ctl(ctl, h, st))) return rc;
       if (h->err) return status_from_err(h->err);
-      const double cut = (double)(h->cut_w2 / 2);
+      const int64_t cut2 = first ? (int64_t)ed0 : h->cut_w2;
+      const double cut = (double)(cut2 / 2);
       const double reg = lambda * cut;
       g.energy[l] = h->fid_total + reg;
     }

@@ -170,7 +170,10 @@ __global__ void k_ctl_init(Ctl *ctl) {
       ctl->bbox_enc[a] = f2ord(INFINITY);
       ctl->bbox_enc[3 + a] = f2ord(-INFINITY);
     }
-    ctl->pad1[0] = ctl->pad1[1] = 0;
+    ctl->n_big = 0;
+    ctl->e_rev = 0;
+    ctl->e_fwd = 0;
+    ctl->n_cbig = 0;
     ctl->cut_w2 = 0;
     ctl->fid_total = 0.0;
   }
