@@ -301,7 +301,72 @@ __device__ __forceinline__ double edge_gain(const NodeIn &s, int32_t v,
   return cut - fit;
 }
 
-template <bool FIRST>
+// Mean row of a node held in registers when D is a compile-time size DT
+// (a multiple of 4): one vector load per 16 bytes instead of one scalar load
+// per dimension.  Same values as node_mu.
+template <bool FIRST, int DT>
+struct MeanRow {
+  double m[DT > 0 ? DT : 1];
+  __device__ __forceinline__ void load(const NodeIn &s, int32_t v, double sF,
+                                       double sIF) {
+    if constexpr (DT > 0) {
+      if (FIRST) {
+        const float4 *p =
+            reinterpret_cast<const float4 *>(s.emb + (int64_t)v * DT);
+#pragma unroll
+        for (int q = 0; q < DT / 4; ++q) {
+          const float4 x = p[q];
+          m[4 * q + 0] = rint((double)x.x * sF) * sIF;
+          m[4 * q + 1] = rint((double)x.y * sF) * sIF;
+          m[4 * q + 2] = rint((double)x.z * sF) * sIF;
+          m[4 * q + 3] = rint((double)x.w * sF) * sIF;
+        }
+      } else {
+        const double2 *p =
+            reinterpret_cast<const double2 *>(s.mu + (int64_t)v * DT);
+#pragma unroll
+        for (int q = 0; q < DT / 2; ++q) {
+          const double2 x = p[q];
+          m[2 * q + 0] = x.x;
+          m[2 * q + 1] = x.y;
+        }
+      }
+    }
+  }
+};
+
+// Prop. 1 for the edge (v, u) with v's mean row already loaded; the same
+// operations in the same order as edge_gain.
+template <bool FIRST, int DT>
+__device__ __forceinline__ double edge_gain_t(const NodeIn &s,
+                                              const MeanRow<FIRST, DT> &mv,
+                                              int32_t v, double dsv,
+                                              int32_t u, int32_t w, int32_t d,
+                                              double lambda, double sF,
+                                              double sIF) {
+  if constexpr (DT == 0) {
+    return edge_gain<FIRST>(s, v, dsv, u, w, d, lambda, sF, sIF);
+  } else {
+    MeanRow<FIRST, DT> mu;
+    mu.load(s, u, sF, sIF);
+    const double dsu = (double)node_size<FIRST>(s, u);
+    const double num = dsv * dsu;
+    const double den = dsv + dsu;
+    const double f = num / den;
+    double ss = 0.0;
+#pragma unroll
+    for (int i = 0; i < DT; ++i) {
+      const double diff = mv.m[i] - mu.m[i];
+      const double sq = diff * diff;
+      ss = ss + sq;
+    }
+    const double cut = lambda * (double)w;
+    const double fit = f * ss;
+    return cut - fit;
+  }
+}
+
+template <bool FIRST, int DT>
 __global__ __launch_bounds__(256) void k_select(
     int32_t nn, Adj a, NodeIn s, int32_t d, double lambda, int64_t smin,
     int32_t *__restrict__ target, int32_t *__restrict__ deg,
@@ -318,6 +383,8 @@ __global__ __launch_bounds__(256) void k_select(
   const int32_t sv = node_size<FIRST>(s, v);
   const double dsv = (double)sv;
   const bool small = (int64_t)sv < smin;
+  MeanRow<FIRST, DT> mv;
+  mv.load(s, v, sF, sIF);
   Best b{0.0, 0, -1};
   int32_t cnt = 0;
   for_row<FIRST>(a, v, 0, 1, [&](int32_t u, int32_t w) {
@@ -326,7 +393,8 @@ __global__ __launch_bounds__(256) void k_select(
       raise_err(ctl, kErrInternal);
       return;
     }
-    const double g = edge_gain<FIRST>(s, v, dsv, u, w, d, lambda, sF, sIF);
+    const double g =
+        edge_gain_t<FIRST, DT>(s, mv, v, dsv, u, w, d, lambda, sF, sIF);
     if (g > 0.0 || small) {
       const Best c{g, node_minpt<FIRST>(s, u), u};
       if (best_before(c, b)) b = c;
@@ -338,7 +406,7 @@ __global__ __launch_bounds__(256) void k_select(
     ctl->any_choice = 1;
 }
 
-template <bool FIRST>
+template <bool FIRST, int DT>
 __global__ __launch_bounds__(256) void k_select_long(
     int32_t nn, Adj a, NodeIn s, int32_t d, double lambda, int64_t smin,
     int32_t *__restrict__ target, int32_t *__restrict__ deg,
@@ -359,6 +427,8 @@ __global__ __launch_bounds__(256) void k_select_long(
     const int32_t sv = node_size<FIRST>(s, v);
     const double dsv = (double)sv;
     const bool small = (int64_t)sv < smin;
+    MeanRow<FIRST, DT> mv;
+    mv.load(s, v, sF, sIF);
     Best b{0.0, 0, -1};
     int32_t cnt = 0;
     for_row<FIRST>(a, v, lane, kWave, [&](int32_t u, int32_t w) {
@@ -367,7 +437,8 @@ __global__ __launch_bounds__(256) void k_select_long(
         raise_err(ctl, kErrInternal);
         return;
       }
-      const double g = edge_gain<FIRST>(s, v, dsv, u, w, d, lambda, sF, sIF);
+      const double g =
+          edge_gain_t<FIRST, DT>(s, mv, v, dsv, u, w, d, lambda, sF, sIF);
       if (g > 0.0 || small) {
         const Best c{g, node_minpt<FIRST>(s, u), u};
         if (best_before(c, b)) b = c;
@@ -516,7 +587,7 @@ __device__ __forceinline__ void note_window(const NodeOut &o, int32_t c,
 
 constexpr int kDimChunk = 8;
 
-template <bool FIRST>
+template <bool FIRST, int DT>
 __global__ __launch_bounds__(256) void k_stats(
     int32_t bound, const int32_t *__restrict__ mem,
     const int32_t *__restrict__ moff, NodeIn s,
@@ -542,6 +613,45 @@ __global__ __launch_bounds__(256) void k_stats(
   o.minpt[c] = mp;
   note_window(o, c, cap, ctl);
   const double dsz = (double)size;
+  if constexpr (DT > 0) {
+    int64_t acc[DT];
+#pragma unroll
+    for (int q = 0; q < DT; ++q) acc[q] = 0;
+    for (int32_t j = m0; j < m1; ++j) {
+      const int32_t m = mem[j];
+      if (FIRST) {
+        const float4 *p =
+            reinterpret_cast<const float4 *>(s.emb + (int64_t)m * DT);
+#pragma unroll
+        for (int q = 0; q < DT / 4; ++q) {
+          const float4 x = p[q];
+          acc[4 * q + 0] += (int64_t)rint((double)x.x * sF);
+          acc[4 * q + 1] += (int64_t)rint((double)x.y * sF);
+          acc[4 * q + 2] += (int64_t)rint((double)x.z * sF);
+          acc[4 * q + 3] += (int64_t)rint((double)x.w * sF);
+        }
+      } else {
+        const longlong2 *p =
+            reinterpret_cast<const longlong2 *>(s.S + (int64_t)m * DT);
+#pragma unroll
+        for (int q = 0; q < DT / 2; ++q) {
+          const longlong2 x = p[q];
+          acc[2 * q + 0] += x.x;
+          acc[2 * q + 1] += x.y;
+        }
+      }
+    }
+    longlong2 *So = reinterpret_cast<longlong2 *>(o.S + (int64_t)c * DT);
+    double2 *Mo = reinterpret_cast<double2 *>(o.mu + (int64_t)c * DT);
+#pragma unroll
+    for (int q = 0; q < DT / 2; ++q) {
+      So[q] = make_longlong2(acc[2 * q], acc[2 * q + 1]);
+      const double q0 = (double)acc[2 * q] / dsz;
+      const double q1 = (double)acc[2 * q + 1] / dsz;
+      Mo[q] = make_double2(q0 * sIF, q1 * sIF);
+    }
+    return;
+  }
   for (int32_t i0 = 0; i0 < d; i0 += kDimChunk) {
     int64_t acc[kDimChunk];
 #pragma unroll
@@ -1135,7 +1245,7 @@ int status_from_err(uint32_t err) {
 }
 
 // One merge round on nn nodes whose rows hold ed directed entries.
-template <bool FIRST>
+template <bool FIRST, int DT>
 void launch_round(const Bufs &b, const Adj &adj, int cur, int32_t n,
                   int32_t k, int32_t nn, int32_t ed, int32_t d,
                   const NodeIn &s, double lambda, int64_t smin, Ctl *ctl,
@@ -1144,10 +1254,10 @@ void launch_round(const Bufs &b, const Adj &adj, int cur, int32_t n,
   const int32_t tcap = (int32_t)edge_bound(n, k);
   hipLaunchKernelGGL(k_round_init, dim3(1), dim3(64), 0, st, ctl);
   prof_begin("select", st);
-  hipLaunchKernelGGL(k_select<FIRST>, xblocks_for(nn), dim3(256), 0, st, nn,
+  hipLaunchKernelGGL((k_select<FIRST, DT>), xblocks_for(nn), dim3(256), 0, st, nn,
                      adj, s, d, lambda, smin, b.target, b.deg, b.long_rows,
                      ctl);
-  hipLaunchKernelGGL(k_select_long<FIRST>, dim3(kLongGrid), dim3(256), 0, st,
+  hipLaunchKernelGGL((k_select_long<FIRST, DT>), dim3(kLongGrid), dim3(256), 0, st,
                      nn, adj, s, d, lambda, smin, b.target, b.deg, b.long_rows,
                      ctl);
   prof_end(st);
@@ -1169,7 +1279,7 @@ void launch_round(const Bufs &b, const Adj &adj, int cur, int32_t n,
                      b.moff, b.rank, b.mem, ctl);
   const NodeOut o{b.size[nxt], b.S[nxt], b.mu,    b.minpt[nxt],
                   b.capn,      b.wl[nxt], b.cbig};
-  hipLaunchKernelGGL(k_stats<FIRST>, xblocks_for(nn), dim3(256), 0, st, nn,
+  hipLaunchKernelGGL((k_stats<FIRST, DT>), xblocks_for(nn), dim3(256), 0, st, nn,
                      b.mem, b.moff, s, b.deg, d, o, b.big, ctl);
   hipLaunchKernelGGL(k_stats_big<FIRST>, dim3(kBigGrid), dim3(256), 0, st,
                      b.mem, b.moff, s, b.deg, d, o, b.big, ctl);
@@ -1193,6 +1303,30 @@ void launch_round(const Bufs &b, const Adj &adj, int cur, int32_t n,
   prof_end(st);
 }
 
+// Dispatch on the embedding width: 8, 16 and 32 get unrolled kernels.
+template <bool FIRST>
+void round_d(const Bufs &b, const Adj &adj, int cur, int32_t n, int32_t k,
+             int32_t nn, int32_t ed, int32_t d, const NodeIn &s,
+             double lambda, int64_t smin, Ctl *ctl, hipStream_t st) {
+  switch (d) {
+    case 8:
+      launch_round<FIRST, 8>(b, adj, cur, n, k, nn, ed, d, s, lambda, smin,
+                             ctl, st);
+      break;
+    case 16:
+      launch_round<FIRST, 16>(b, adj, cur, n, k, nn, ed, d, s, lambda, smin,
+                              ctl, st);
+      break;
+    case 32:
+      launch_round<FIRST, 32>(b, adj, cur, n, k, nn, ed, d, s, lambda, smin,
+                              ctl, st);
+      break;
+    default:
+      launch_round<FIRST, 0>(b, adj, cur, n, k, nn, ed, d, s, lambda, smin,
+                             ctl, st);
+  }
+}
+
 }  // namespace
 
 void ladder_reserve(Arena &a, int32_t n, int32_t d, int32_t k) {
@@ -1212,11 +1346,16 @@ int ladder_run(const LadderArgs &g, Ctl *ctl, Arena &a, hipStream_t st) {
   int rc;
 
   // embeddings in internal order, fixed-point shift (Step 0)
-  const float *emb = g.emb;
+  // (always a copy in the workspace: aligned rows for vector loads)
+  const float *emb = b.emb_int;
   if (g.perm) {
     hipLaunchKernelGGL(k_gather_rows, blocks_for((int64_t)n * d), dim3(256),
                        0, st, g.emb, g.perm, n, d, b.emb_int);
-    emb = b.emb_int;
+  } else {
+    rc = check_hip(hipMemcpyAsync(b.emb_int, g.emb, sizeof(float) * n * d,
+                                  hipMemcpyDeviceToDevice, st),
+                   "hipMemcpyAsync(emb)");
+    if (rc) return rc;
   }
   hipLaunchKernelGGL(k_maxabs, dim3(2048), dim3(256), 0, st, emb,
                      (int64_t)n * d, ctl);
@@ -1284,15 +1423,14 @@ int ladder_run(const LadderArgs &g, Ctl *ctl, Arena &a, hipStream_t st) {
         s.S = nullptr;
         s.mu = nullptr;
         s.minpt = nullptr;
-        launch_round<true>(b, adj, cur, n, k, nn, ed, d, s, lambda, smin, ctl,
-                           st);
+        round_d<true>(b, adj, cur, n, k, nn, ed, d, s, lambda, smin, ctl, st);
       } else {
         s.size = b.size[cur];
         s.S = b.S[cur];
         s.mu = b.mu;
         s.minpt = b.minpt[cur];
-        launch_round<false>(b, adj, cur, n, k, nn, ed, d, s, lambda, smin,
-                            ctl, st);
+        round_d<false>(b, adj, cur, n, k, nn, ed, d, s, lambda, smin, ctl,
+                       st);
       }
       if ((rc = read_ctl(ctl, h, st))) return rc;
       if (h->err) return status_from_err(h->err);
