@@ -248,12 +248,54 @@ __device__ __forceinline__ void scan_bucket(const float4 *__restrict__ pts,
   BucketStep<K, 0>::run(q, px, py, pz, me, cnt, key);
 }
 
+// Box test of the children first .. first+7 (level lc) of one node: bit c
+// is set when some lane of the group has the child's box within its current
+// k-th distance.  The eight boxes are loaded before any is used.  The box
+// distance uses the same IEEE operations as d2, so it never exceeds the d2
+// of a point inside the box.
+template <int K>
+__device__ __forceinline__ uint32_t child_mask(
+    const float4 *__restrict__ blo, const float4 *__restrict__ bhi,
+    const Tree &tree, int lc, int32_t first, int32_t cnt_lc, const float4 &p,
+    bool act, const uint64_t (&key)[K], int gshift) {
+  const int32_t nchild = min(kFan, cnt_lc - first);
+  const int32_t off = tree.off[lc] + first;
+  float4 lo[kFan], hi[kFan];
+#pragma unroll
+  for (int c = 0; c < kFan; ++c) {
+    const int32_t j = off + min(c, nchild - 1);
+    lo[c] = blo[j];
+    hi[c] = bhi[j];
+  }
+  const uint32_t kth = (uint32_t)(key[K - 1] >> 32);
+  uint32_t m = 0;
+#pragma unroll
+  for (int c = 0; c < kFan; ++c) {
+    const float ex = fmaxf(fmaxf(lo[c].x - p.x, p.x - hi[c].x), 0.f);
+    const float ey = fmaxf(fmaxf(lo[c].y - p.y, p.y - hi[c].y), 0.f);
+    const float ez = fmaxf(fmaxf(lo[c].z - p.z, p.z - hi[c].z), 0.f);
+    const float bx = ex * ex, by = ey * ey, bz = ez * ez;
+    const float d2b = (bx + by) + bz;
+    // d2b <= k-th d2 (an empty list, kNoKey, admits everything)
+    const bool need = act && c < nchild && __float_as_uint(d2b) <= kth;
+    if ((__ballot(need) >> gshift) & 0xffffull) m |= 1u << c;
+  }
+  return m;
+}
+
+__device__ __forceinline__ void set_level_bits(uint64_t &mlo, uint64_t &mhi,
+                                               int l, uint32_t m8) {
+  if (l < 8)
+    mlo |= (uint64_t)m8 << (8 * l);
+  else
+    mhi |= (uint64_t)m8 << (8 * (l - 8));
+}
+
 // One query group = 16 lanes = the 16 points of one bucket.  Every group
 // walks the tree on its own (group-uniform decisions from a 16-lane vote);
 // the four groups of a wave alternate between finding their next bucket and
-// scanning it together.  A box is entered when its fp32 distance (same
-// operations as d2, so never above the d2 of a point inside) does not
-// exceed some lane's current k-th distance.
+// scanning it together.  A node is entered when some lane's box distance
+// does not exceed that lane's current k-th distance.
 template <int K>
 __global__ __launch_bounds__(256) void k_knn_query(
     const float4 *__restrict__ pts, const int32_t *__restrict__ inv,
@@ -282,43 +324,46 @@ __global__ __launch_bounds__(256) void k_knn_query(
   if (grp + 1 < nb0)
     scan_bucket<K>(pts, n, grp + 1, lane16, p.x, p.y, p.z, me, key);
 
-  int level = tree.top;
-  int32_t idx = 0;
-  bool done = false;
+  // Depth-first walk with the pending children of every level of the
+  // current path as bits: bit 8*l + c = child c (level l) of the path node
+  // at level l+1.  The lowest set bit is the deepest pending node, and the
+  // path node at level l+1 is cur >> 3*(l+1-curl) (cur: last node taken, at
+  // level curl), since children of x are 8x..8x+7.
+  uint64_t mlo = 0, mhi = 0;
+  int32_t cur = 0;
+  int curl = tree.top;
+  if (tree.top > 0) {
+    const uint32_t m8 = child_mask<K>(blo, bhi, tree, tree.top - 1, 0,
+                                      tree.cnt[tree.top - 1], p, act, key,
+                                      gshift);
+    set_level_bits(mlo, mhi, tree.top - 1, m8);
+  }
   for (;;) {
     int32_t leaf = -1;
-    while (!done) {
-      const int32_t j = tree.off[level] + idx;
-      const float4 lo = blo[j], hi = bhi[j];
-      const float ex = fmaxf(fmaxf(lo.x - p.x, p.x - hi.x), 0.f);
-      const float ey = fmaxf(fmaxf(lo.y - p.y, p.y - hi.y), 0.f);
-      const float ez = fmaxf(fmaxf(lo.z - p.z, p.z - hi.z), 0.f);
-      const float bx = ex * ex, by = ey * ey, bz = ez * ez;
-      const float d2b = (bx + by) + bz;
-      // d2b <= k-th d2 (an empty list, kNoKey, admits everything)
-      const bool need =
-          act && __float_as_uint(d2b) <= (uint32_t)(key[K - 1] >> 32);
-      const bool any = ((__ballot(need) >> gshift) & 0xffffull) != 0;
-      if (any && level > 0) {
-        --level;
-        idx *= kFan;
+    while ((mlo | mhi) != 0) {
+      int t;
+      if (mlo) {
+        t = __builtin_ctzll(mlo);
+        mlo &= mlo - 1;
+      } else {
+        t = 64 + __builtin_ctzll(mhi);
+        mhi &= mhi - 1;
+      }
+      const int l = t >> 3, c = t & 7;
+      const int32_t node = ((cur >> (3 * (l + 1 - curl))) << 3) | c;
+      cur = node;
+      curl = l;
+      if (l == 0) {
+        if (node < grp - 1 || node > grp + 1) {
+          leaf = node;
+          break;
+        }
         continue;
       }
-      if (any && (idx < grp - 1 || idx > grp + 1)) leaf = idx;
-      // next box in Morton order: a later sibling, else climb
-      for (;;) {
-        if (level == tree.top) {
-          done = true;
-          break;
-        }
-        if ((idx % kFan) != kFan - 1 && idx + 1 < tree.cnt[level]) {
-          ++idx;
-          break;
-        }
-        ++level;
-        idx /= kFan;
-      }
-      if (leaf >= 0) break;
+      const int32_t first = node * kFan;
+      const uint32_t m8 = child_mask<K>(blo, bhi, tree, l - 1, first,
+                                        tree.cnt[l - 1], p, act, key, gshift);
+      set_level_bits(mlo, mhi, l - 1, m8);
     }
     if (__ballot(leaf >= 0) == 0) break;
     if (leaf >= 0)
