@@ -29,6 +29,12 @@ __device__ __forceinline__ int32_t xcd_tid() {
   return xcd_block() * (int32_t)blockDim.x + (int32_t)threadIdx.x;
 }
 
+// Row stride of the internal neighbour tables: k rounded up to a multiple
+// of 4 (16-byte rows for vector loads), padded with -1.
+__host__ __device__ __forceinline__ int32_t pad4(int32_t k) {
+  return (k + 3) & ~3;
+}
+
 // Bump allocator over the caller's workspace.  With base == nullptr it only
 // measures: every take() returns nullptr and `off` ends at the bytes needed.
 struct Arena {
@@ -68,7 +74,8 @@ bool radix_sort_pairs(uint64_t *keys, uint32_t *vals, uint64_t *keys_alt,
 size_t radix_hist_ints(int32_t n);
 
 // kNN: Morton sort, box tree, exact query.  Produces the internal
-// (Morton-order) neighbour table nbr_int (n*k, -1 padded) and the maps
+// (Morton-order) neighbour table nbr_int (n rows of pad4(k), -1 padded) and
+// the maps
 // perm (internal -> original) and inv (original -> internal); optionally the
 // caller-facing tables in original order.
 struct KnnWork {
@@ -88,7 +95,7 @@ hipError_t knn_launch(const float *xyz, int32_t n, int32_t k, Ctl *ctl,
 // Merge ladder on a neighbour table (internal ids; perm/inv may be null
 // when internal == original order).
 struct LadderArgs {
-  const int32_t *nbr;   // n*k
+  const int32_t *nbr;   // n rows: stride pad4(k), or k when check_nbr
   const int32_t *perm;  // nullable
   const int32_t *inv;   // nullable
   const float *emb;     // n*d, caller order

@@ -371,18 +371,20 @@ __global__ __launch_bounds__(256) void k_knn_query(
   }
 
   if (!act) return;
+  const int32_t kp = pad4(k);
 #pragma unroll
   for (int t = 0; t < K; ++t) {
     if (t < k) {
       const bool has = key[t] != kNoKey;
       const int32_t o = (int32_t)(uint32_t)key[t];
-      nbr_int[(int64_t)i * k + t] = has ? inv[o] : -1;
+      nbr_int[(int64_t)i * kp + t] = has ? inv[o] : -1;
       if (nbr_out) nbr_out[(int64_t)me * k + t] = has ? o : -1;
       if (d2_out)
         d2_out[(int64_t)me * k + t] =
             has ? __uint_as_float((uint32_t)(key[t] >> 32)) : INFINITY;
     }
   }
+  for (int32_t t = k; t < kp; ++t) nbr_int[(int64_t)i * kp + t] = -1;
 }
 
 // ---------------------------------------------------------------------------
@@ -399,7 +401,7 @@ void knn_reserve(Arena &a, int32_t n, int32_t k, KnnWork *w) {
   const Tree t = make_tree(n);
   w->perm = a.take<int32_t>(n);
   w->inv = a.take<int32_t>(n);
-  w->nbr_int = a.take<int32_t>((size_t)n * k);
+  w->nbr_int = a.take<int32_t>((size_t)n * pad4(k));
   w->keys = a.take<uint64_t>(n);
   w->keys2 = a.take<uint64_t>(n);
   w->vals = a.take<uint32_t>(n);

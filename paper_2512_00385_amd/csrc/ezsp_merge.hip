@@ -78,15 +78,17 @@ __global__ __launch_bounds__(256) void k_gather_rows(const float *emb,
 // App. Alg. A-2's prepare_graph does)
 // ---------------------------------------------------------------------------
 
-// A caller's neighbour table: entries outside [-1, n) are an error; -1, the
-// point itself and repeats of an earlier entry become -1.
+// A caller's neighbour table (stride k) into the internal one (stride
+// pad4(k)): entries outside [-1, n) are an error; -1, the point itself and
+// repeats of an earlier entry become -1, and so does the padding.
 __global__ __launch_bounds__(256) void k_sanitize(const int32_t *nbr,
                                                   int32_t n, int32_t k,
                                                   int32_t *out, Ctl *ctl) {
   const int32_t i = blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= n) return;
+  const int32_t kp = pad4(k);
   const int32_t *r = nbr + (int64_t)i * k;
-  int32_t *o = out + (int64_t)i * k;
+  int32_t *o = out + (int64_t)i * kp;
   for (int32_t t = 0; t < k; ++t) {
     int32_t j = r[t];
     if (j < -1 || j >= n) {
@@ -98,14 +100,19 @@ __global__ __launch_bounds__(256) void k_sanitize(const int32_t *nbr,
       if (r[s] == j) j = -1;
     o[t] = j;
   }
+  for (int32_t t = k; t < kp; ++t) o[t] = -1;
 }
 
-__device__ __forceinline__ bool row_has(const int32_t *nbr, int32_t k,
+// Row j of the internal table (stride kp, a multiple of 4) contains x?
+__device__ __forceinline__ bool row_has(const int32_t *nbr, int32_t kp,
                                         int32_t j, int32_t x) {
-  const int32_t *r = nbr + (int64_t)j * k;
-  for (int32_t s = 0; s < k; ++s)
-    if (r[s] == x) return true;
-  return false;
+  const int4 *r = reinterpret_cast<const int4 *>(nbr + (int64_t)j * kp);
+  bool hit = false;
+  for (int32_t q = 0; q < kp / 4; ++q) {
+    const int4 v = r[q];
+    hit |= (v.x == x) | (v.y == x) | (v.z == x) | (v.w == x);
+  }
+  return hit;
 }
 
 // Reverse entries: i lists u, u does not list i -> u's row gets i.
@@ -113,14 +120,15 @@ __global__ __launch_bounds__(256) void k_rev_count(const int32_t *nbr,
                                                    int32_t n, int32_t k,
                                                    int32_t *rev, Ctl *ctl) {
   const int32_t i = xcd_tid();
+  const int32_t kp = pad4(k);
   int32_t fwd = 0;
   if (i < n) {
-    const int32_t *r = nbr + (int64_t)i * k;
+    const int32_t *r = nbr + (int64_t)i * kp;
     for (int32_t t = 0; t < k; ++t) {
       const int32_t u = r[t];
       if (u < 0) continue;
       ++fwd;
-      if (!row_has(nbr, k, u, i)) atomicAdd(&rev[u], 1);
+      if (!row_has(nbr, kp, u, i)) atomicAdd(&rev[u], 1);
     }
   }
   fwd = wave_sum(fwd);
@@ -135,10 +143,11 @@ __global__ __launch_bounds__(256) void k_rev_fill(const int32_t *nbr,
                                                   int32_t *rown, Ctl *ctl) {
   const int32_t i = xcd_tid();
   if (i >= n) return;
-  const int32_t *r = nbr + (int64_t)i * k;
+  const int32_t kp = pad4(k);
+  const int32_t *r = nbr + (int64_t)i * kp;
   for (int32_t t = 0; t < k; ++t) {
     const int32_t u = r[t];
-    if (u < 0 || row_has(nbr, k, u, i)) continue;
+    if (u < 0 || row_has(nbr, kp, u, i)) continue;
     const int32_t pos = rrp[u] + atomicAdd(&cursor[u], 1);
     if (pos < rrp[u + 1]) {
       rcol[pos] = i;
@@ -163,8 +172,8 @@ struct NodeIn {
 
 struct Adj {
   // first round
-  const int32_t *nbr;  // n*k, -1 = no entry
-  int32_t k;
+  const int32_t *nbr;  // n rows of stride kp, -1 = no entry
+  int32_t k, kp;
   const int32_t *rrp, *rcol, *rown;  // reverse list and the row it is in
   int32_t n_rev;
   // later rounds
@@ -216,7 +225,7 @@ template <bool FIRST, class Fn>
 __device__ __forceinline__ void for_row(const Adj &a, int32_t v, int32_t begin,
                                         int32_t stride, Fn &&f) {
   if (FIRST) {
-    const int32_t *r = a.nbr + (int64_t)v * a.k;
+    const int32_t *r = a.nbr + (int64_t)v * a.kp;
     const int32_t r0 = a.rrp[v];
     const int32_t len = a.k + (a.rrp[v + 1] - r0);
     for (int32_t j = begin; j < len; j += stride) {
@@ -238,7 +247,8 @@ template <bool FIRST>
 __device__ __forceinline__ bool row_entry(const Adj &a, int32_t v, int32_t j,
                                           int32_t &u, int32_t &w) {
   if (FIRST) {
-    u = (j < a.k) ? a.nbr[(int64_t)v * a.k + j] : a.rcol[a.rrp[v] + (j - a.k)];
+    u = (j < a.k) ? a.nbr[(int64_t)v * a.kp + j]
+                  : a.rcol[a.rrp[v] + (j - a.k)];
     w = 1;
     return u >= 0;
   }
@@ -1180,7 +1190,7 @@ void carve(Arena &a, int32_t n, int32_t d, int32_t k, Bufs *b) {
   const int64_t ed = edge_bound(n, k);
   const size_t n1 = (size_t)n + 1;
   b->emb_int = a.take<float>((size_t)n * d);
-  b->nbr_clean = a.take<int32_t>((size_t)n * k);
+  b->nbr_clean = a.take<int32_t>((size_t)n * pad4(k));
   b->rrp = a.take<int32_t>(n1);
   b->rcol = a.take<int32_t>((size_t)n * k);
   b->rown = a.take<int32_t>((size_t)n * k);
@@ -1394,6 +1404,7 @@ int ladder_run(const LadderArgs &g, Ctl *ctl, Arena &a, hipStream_t st) {
   Adj adj;
   adj.nbr = nbr;
   adj.k = k;
+  adj.kp = pad4(k);
   adj.rrp = b.rrp;
   adj.rcol = b.rcol;
   adj.rown = b.rown;
