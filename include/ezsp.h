@@ -159,7 +159,7 @@ const char *ezsp_last_error(void);
 
 /* Per-stage timing with HIP events recorded on the caller's stream around
  * the launches of each stage ("knn_query", "morton_sort", "graph_build",
- * "select", "union", "stats", "contract", "compose").  Off by default; a
+ * "select", "union", "stats", "contract", "compose", "tail").  Off by default; a
  * diagnostic for benchmarks.  ezsp_profile_enable(1) clears the totals and
  * starts recording, ezsp_profile_enable(0) stops.  ezsp_profile_read gives
  * the number of recorded launches of `stage`, their summed duration in

@@ -18,6 +18,7 @@ enum : uint32_t {
   kErrInternal = 4u,   // an index or capacity check failed
   kErrBadIndex = 8u,   // caller data out of range (neighbour id, label)
   kErrJump = 16u,      // pointer jumping hit its iteration cap
+  kErrNotConv = 32u,   // a level reached max_rounds inside the tail kernel
 };
 
 // Small block of device scalars, one per call, at the start of the
@@ -36,6 +37,8 @@ struct Ctl {
   int32_t e_rev;        // reverse-only entries of the first-round graph
   int32_t e_fwd;        // valid forward entries of the first-round graph
   int32_t n_cbig;       // components whose table window exceeds one chunk
+  int32_t n_tiles;      // member tiles of those components
+  int32_t tail_level;   // level that reached max_rounds in the tail kernel
   int64_t cut_w2;       // 2 * cut weight (directed sum) of the current graph
   double fid_total;     // fidelity term of the energy
 };
@@ -151,11 +154,45 @@ inline int32_t scan_blocks(int64_t n) {
   return (int32_t)((n + kScanTile - 1) / kScanTile);
 }
 
+// Small scans in one launch: one block of 1024 threads, 16 items each.
+constexpr int kOneNT = 1024;
+constexpr int kOneItems = 16;
+constexpr int kOneMax = kOneNT * kOneItems;
+
+template <class Op>
+__global__ __launch_bounds__(kOneNT) void k_scan_one(Op op, int32_t n,
+                                                     int32_t *total) {
+  __shared__ int32_t wsum[kOneNT / kWave];
+  const int32_t base = threadIdx.x * kOneItems;
+  int32_t v[kOneItems];
+  int32_t s = 0;
+#pragma unroll
+  for (int j = 0; j < kOneItems; ++j) {
+    const int32_t i = base + j;
+    v[j] = (i < n) ? op.value(i) : 0;
+    s += v[j];
+  }
+  int32_t tot;
+  int32_t run = block_excl_scan<kOneNT>(s, wsum, &tot);
+#pragma unroll
+  for (int j = 0; j < kOneItems; ++j) {
+    const int32_t i = base + j;
+    if (i < n) op.emit(i, run, v[j]);
+    run += v[j];
+  }
+  if (threadIdx.x == 0) *total = tot;
+}
+
 // Exclusive scan; `bsum` needs scan_blocks(n) ints; `total` (device) gets the
 // sum.  n may be 0.
 template <class Op>
 inline void device_scan(const Op &op, int32_t n, int32_t *bsum, int32_t *total,
                         hipStream_t st) {
+  if (n <= kOneMax) {
+    hipLaunchKernelGGL(k_scan_one<Op>, dim3(1), dim3(kOneNT), 0, st, op, n,
+                       total);
+    return;
+  }
   int32_t nb = scan_blocks(n);
   if (nb == 0) {
     hipLaunchKernelGGL(k_scan_bsums, dim3(1), dim3(1024), 0, st, bsum, 0,

@@ -37,6 +37,9 @@
 //             edges inside a component are dropped; the window is the next
 //             round's row and every occupied slot records its owner
 #include <math.h>
+#include <stdlib.h>
+
+#include <algorithm>
 
 #include "ezsp_internal.h"
 
@@ -47,6 +50,7 @@ constexpr int kJumpCap = 1 << 16;
 constexpr int kLongRow = 128;   // rows longer than this: one wave per row
 constexpr int kLongGrid = 2048; // blocks of 4 waves for the long rows
 constexpr int kBigComp = 128;   // components with more members: one block
+constexpr int kWaveRowsMax = 65536;  // rounds this small: a wave per row
 constexpr int kBigGrid = 512;
 constexpr int kChunk = 2048;    // table slots contracted by one block in LDS
 constexpr int kBatch = 256;     // members taken at a time by a block
@@ -267,6 +271,7 @@ __global__ void k_round_init(Ctl *ctl) {
     ctl->n_long = 0;
     ctl->n_big = 0;
     ctl->n_cbig = 0;
+    ctl->n_tiles = 0;
   }
 }
 
@@ -385,7 +390,8 @@ __global__ __launch_bounds__(256) void k_select(
   if (v >= nn) return;
   if (row_span<FIRST>(a, v) > kLongRow) {  // a whole block takes this row
     const int32_t slot = atomicAdd(&ctl->n_long, 1);
-    long_rows[slot] = v;
+    if (slot < nn) long_rows[slot] = v;
+    else raise_err(ctl, kErrInternal);
     return;
   }
   const int F = ctl->F;
@@ -420,8 +426,8 @@ template <bool FIRST, int DT>
 __global__ __launch_bounds__(256) void k_select_long(
     int32_t nn, Adj a, NodeIn s, int32_t d, double lambda, int64_t smin,
     int32_t *__restrict__ target, int32_t *__restrict__ deg,
-    const int32_t *__restrict__ long_rows, Ctl *ctl) {
-  const int32_t n_long = ctl->n_long;
+    const int32_t *__restrict__ long_rows, bool all_rows, Ctl *ctl) {
+  const int32_t n_long = all_rows ? nn : ctl->n_long;
   const int F = ctl->F;
   const double sF = ldexp(1.0, F), sIF = ldexp(1.0, -F);
   const int lane = threadIdx.x & (kWave - 1);
@@ -429,7 +435,7 @@ __global__ __launch_bounds__(256) void k_select_long(
                                   threadIdx.x / kWave);
   const int32_t nwaves = (int32_t)(gridDim.x * (blockDim.x / kWave));
   for (int32_t li = wave0; li < n_long; li += nwaves) {
-    const int32_t v = long_rows[li];
+    const int32_t v = all_rows ? li : long_rows[li];
     if ((uint32_t)v >= (uint32_t)nn) {
       raise_err(ctl, kErrInternal);
       continue;
@@ -586,13 +592,27 @@ struct NodeOut {
   int32_t *cap;   // summed member degree = window of the next table
   int32_t *wl;    // row length (the window until a chunk compacts it)
   int32_t *cbig;  // components whose window exceeds one chunk
+  int32_t chunk;  // slots per contraction chunk (at most kChunk)
+  int32_t big_members;  // components with more members take a block
+  int32_t *tile_c, *tile_i;  // member tiles of the large windows
 };
 
+// Records the window of component c; a window larger than a chunk goes to
+// the global path, split into tiles of kBatch members.
 __device__ __forceinline__ void note_window(const NodeOut &o, int32_t c,
-                                            int32_t cap, Ctl *ctl) {
+                                            int32_t cap, int32_t members,
+                                            Ctl *ctl) {
   o.cap[c] = cap;
   o.wl[c] = cap;
-  if (cap > kChunk) o.cbig[atomicAdd(&ctl->n_cbig, 1)] = c;
+  if (cap > o.chunk) {
+    o.cbig[atomicAdd(&ctl->n_cbig, 1)] = c;
+    const int32_t tiles = (members + kBatch - 1) / kBatch;
+    const int32_t t0 = atomicAdd(&ctl->n_tiles, tiles);
+    for (int32_t t = 0; t < tiles; ++t) {
+      o.tile_c[t0 + t] = c;
+      o.tile_i[t0 + t] = t;
+    }
+  }
 }
 
 constexpr int kDimChunk = 8;
@@ -607,7 +627,7 @@ __global__ __launch_bounds__(256) void k_stats(
   const int32_t c = xcd_tid();
   if (c >= bound || c >= ctl->n_next) return;
   const int32_t m0 = moff[c], m1 = moff[c + 1];
-  if (m1 - m0 > kBigComp) {
+  if (m1 - m0 > o.big_members) {
     big[atomicAdd(&ctl->n_big, 1)] = c;
     return;
   }
@@ -621,7 +641,7 @@ __global__ __launch_bounds__(256) void k_stats(
   }
   o.size[c] = size;
   o.minpt[c] = mp;
-  note_window(o, c, cap, ctl);
+  note_window(o, c, cap, m1 - m0, ctl);
   const double dsz = (double)size;
   if constexpr (DT > 0) {
     int64_t acc[DT];
@@ -740,7 +760,7 @@ __global__ __launch_bounds__(256) void k_stats_big(
     if (threadIdx.x == 0) {
       o.size[c] = ssize;
       o.minpt[c] = smp;
-      note_window(o, c, scap, ctl);
+      note_window(o, c, scap, m1 - m0, ctl);
     }
     for (int32_t i = threadIdx.x; i < d; i += blockDim.x) {
       const int64_t t = (int64_t)c * d + i;
@@ -819,7 +839,8 @@ __global__ __launch_bounds__(256) void k_contract_chunk(
     int32_t nn, Adj a, const int32_t *__restrict__ L,
     const int32_t *__restrict__ mem, const int32_t *__restrict__ moff,
     const int32_t *__restrict__ toff, const int32_t *__restrict__ cap,
-    uint64_t *__restrict__ tbl, int32_t *__restrict__ wl, Ctl *ctl) {
+    uint64_t *__restrict__ tbl, int32_t *__restrict__ wl, int32_t chunk,
+    Ctl *ctl) {
   __shared__ int32_t kb[2 * kChunk];
   __shared__ int32_t kw[2 * kChunk];
   __shared__ int32_t pre[kBatch + 1];
@@ -828,13 +849,13 @@ __global__ __launch_bounds__(256) void k_contract_chunk(
   __shared__ int32_t crange[2];
   if (!ctl->any_choice) return;
   const int32_t nc = ctl->n_next;
-  const int32_t j0 = xcd_block() * kChunk;
+  const int32_t j0 = xcd_block() * chunk;
   if (j0 >= ctl->slots) return;
   if (threadIdx.x == 0) {
     crange[0] = lower_bound_i32(toff, nc, j0);
-    crange[1] = lower_bound_i32(toff, nc, j0 + kChunk);
+    crange[1] = lower_bound_i32(toff, nc, j0 + chunk);
   }
-  for (int t = threadIdx.x; t < 2 * kChunk; t += blockDim.x) {
+  for (int t = threadIdx.x; t < 2 * chunk; t += blockDim.x) {
     kb[t] = -1;
     kw[t] = 0;
   }
@@ -844,10 +865,10 @@ __global__ __launch_bounds__(256) void k_contract_chunk(
   // a window larger than a chunk can only be the last one starting here
   // (the next window starts past the chunk); its members are not walked
   const int32_t m_hi =
-      (c_hi > c_lo && cap[c_hi - 1] > kChunk) ? moff[c_hi - 1] : moff[c_hi];
+      (c_hi > c_lo && cap[c_hi - 1] > chunk) ? moff[c_hi - 1] : moff[c_hi];
   auto keep = [&](int32_t m) {
     const int32_t c = cap[L[m]];
-    return c > 0 && c <= kChunk;
+    return c > 0 && c <= chunk;
   };
   for (int32_t b0 = m_lo; b0 < m_hi; b0 += kBatch) {
     const int32_t total = load_batch<FIRST>(a, mem, b0, m_hi, pre, bm, wsum,
@@ -864,7 +885,7 @@ __global__ __launch_bounds__(256) void k_contract_chunk(
       const int32_t A = L[m], B = L[u];
       if (A == B) continue;  // edge inside a merged component
       const int32_t lb = toff[A] - j0, cp = cap[A];
-      if (lb < 0 || cp <= 0 || lb + cp > 2 * kChunk) {
+      if (lb < 0 || cp <= 0 || lb + cp > 2 * chunk) {
         raise_err(ctl, kErrInternal);
         continue;
       }
@@ -886,7 +907,7 @@ __global__ __launch_bounds__(256) void k_contract_chunk(
   int32_t uniq = 0;
   for (int32_t c = c_lo + (int32_t)threadIdx.x; c < c_hi; c += blockDim.x) {
     const int32_t cp = cap[c];
-    if (cp <= 0 || cp > kChunk) continue;
+    if (cp <= 0 || cp > chunk) continue;
     const int32_t base = toff[c], lb = base - j0;
     int32_t out = 0;
     for (int32_t t = lb; t < lb + cp; ++t) {
@@ -955,46 +976,30 @@ __global__ __launch_bounds__(256) void k_contract_big(
     int32_t nn, Adj a, const int32_t *__restrict__ L,
     const int32_t *__restrict__ mem, const int32_t *__restrict__ moff,
     const int32_t *__restrict__ toff, const int32_t *__restrict__ cap,
-    const int32_t *__restrict__ cbig, uint64_t *tbl, int32_t tcap, Ctl *ctl) {
+    const int32_t *__restrict__ tile_c, const int32_t *__restrict__ tile_i,
+    uint64_t *tbl, int32_t tcap, Ctl *ctl) {
   __shared__ int32_t pk[kPreSlots];
   __shared__ int32_t pw[kPreSlots];
   __shared__ int32_t pre[kBatch + 1];
   __shared__ int32_t bm[kBatch];
   __shared__ int32_t wsum[256 / kWave];
-  __shared__ int32_t tile_c, tile_i;
   if (!ctl->any_choice) return;
-  const int32_t nb = ctl->n_cbig;
+  const int32_t n_tiles = ctl->n_tiles;
   int32_t added = 0;
-  for (int32_t t = blockIdx.x;; t += gridDim.x) {
-    if (threadIdx.x == 0) {  // which component and which tile of it
-      int32_t rest = t, c = -1, i = 0;
-      for (int32_t bi = 0; bi < nb; ++bi) {
-        const int32_t cc = cbig[bi];
-        const int32_t tiles = (moff[cc + 1] - moff[cc] + kBatch - 1) / kBatch;
-        if (rest < tiles) {
-          c = cc;
-          i = rest;
-          break;
-        }
-        rest -= tiles;
-      }
-      tile_c = c;
-      tile_i = i;
-    }
+  for (int32_t t = blockIdx.x; t < n_tiles; t += gridDim.x) {
+    const int32_t A = tile_c[t];
     for (int q = threadIdx.x; q < kPreSlots; q += blockDim.x) {
       pk[q] = -1;
       pw[q] = 0;
     }
     __syncthreads();
-    const int32_t A = tile_c;
-    if (A < 0) break;
     const int32_t base = toff[A], cp = cap[A];
     if (base < 0 || cp <= 0 || base + cp > tcap) {
       raise_err(ctl, kErrInternal);
       __syncthreads();
       continue;
     }
-    const int32_t i0 = moff[A] + tile_i * kBatch;
+    const int32_t i0 = moff[A] + tile_i[t] * kBatch;
     const int32_t i1 = min(moff[A + 1], i0 + kBatch);
     const int32_t total = load_batch<FIRST>(a, mem, i0, i1, pre, bm, wsum,
                                             [](int32_t) { return true; });
@@ -1064,16 +1069,20 @@ __global__ __launch_bounds__(256) void k_mark(int32_t nc, const int32_t *minpt,
   mark[m] = 1;
 }
 
+// Point p's superpoint at a level: its node M[inv[p]], through Mt when the
+// level ended in the tail (Mt over the nt nodes the tail started from).
 __global__ __launch_bounds__(256) void k_labels(int32_t n, int32_t nc,
                                                 const int32_t *inv,
                                                 const int32_t *M,
+                                                const int32_t *Mt, int32_t nt,
                                                 const int32_t *minpt,
                                                 const int32_t *rank,
                                                 int32_t *out, Ctl *ctl) {
   const int32_t p = blockIdx.x * blockDim.x + threadIdx.x;
   if (p >= n) return;
   const int32_t i = inv ? inv[p] : p;
-  const int32_t c = ((uint32_t)i < (uint32_t)n) ? M[i] : -1;
+  int32_t c = ((uint32_t)i < (uint32_t)n) ? M[i] : -1;
+  if (Mt) c = ((uint32_t)c < (uint32_t)nt) ? Mt[c] : -1;
   if ((uint32_t)c >= (uint32_t)nc) {
     raise_err(ctl, kErrInternal);
     out[p] = -1;
@@ -1102,6 +1111,8 @@ __global__ __launch_bounds__(256) void k_energy_fid(int32_t n, int32_t d,
                                                     int32_t nc,
                                                     const float *emb,
                                                     const int32_t *M,
+                                                    const int32_t *Mt,
+                                                    int32_t nt,
                                                     const double *mu,
                                                     const Ctl *ctl,
                                                     double *partial) {
@@ -1118,7 +1129,8 @@ __global__ __launch_bounds__(256) void k_energy_fid(int32_t n, int32_t d,
     if (FIRST) {
       m = rint(e * sF) * sIF;
     } else {
-      const int32_t c = M[i];
+      int32_t c = M[i];
+      if (Mt) c = ((uint32_t)c < (uint32_t)nt) ? Mt[c] : -1;
       m = ((uint32_t)c < (uint32_t)nc) ? mu[(int64_t)c * d + j] : 0.0;
     }
     const double r = e - m;
@@ -1164,6 +1176,372 @@ __global__ void k_energy_reset(Ctl *ctl) {
 }
 
 // ---------------------------------------------------------------------------
+// Tail: once the graph is small, every remaining round of every remaining
+// level runs inside one block of 1024 threads (16 waves), with barriers
+// between the steps instead of kernel launches and host round trips.  The
+// steps are the same as above, with a thread per row or component since
+// rows are short by then: Steps 1-2, hook, pointer jumping, relabel by a
+// block scan, members, the statistics, and the contraction into the next
+// table (global atomics, rows keep their empty slots).  The point -> node map is not
+// touched: the tail keeps Mt (tail-start node -> current node) and leaves,
+// for each level it ends, a snapshot of Mt, the smallest point of every
+// node and (for the energy) the means and the cut weight.
+// ---------------------------------------------------------------------------
+constexpr int kTailNT = 1024;
+constexpr int kTailWaves = kTailNT / kWave;
+constexpr int kTailNodes = 16384;   // largest graph the tail can take
+constexpr int kTailStart = 1500;    // default switch to the tail
+constexpr int kTailEdges = 1 << 18; // ... and this many directed entries
+constexpr int kTailLevels = 16;
+constexpr int kTailJumps = 64;
+constexpr int kTailShort = 32;  // longer rows (slots) / components (members)
+                                // go to a wave each, lanes over the entries
+
+struct TailState {
+  int32_t *ws[2], *wl[2];
+  uint64_t *tbl[2];
+  int32_t *size[2], *minpt[2];
+  int64_t *S[2];
+  double *mu;
+  int32_t *target, *deg, *parent, *newid, *L, *cnt, *moff, *mem, *capn, *Mt;
+  int32_t *longrow, *longcomp;             // nn0 each
+  int32_t *lvl_map, *lvl_minpt, *lvl_nc;  // kTailLevels x nn0 (nc: levels)
+  double *lvl_mu;                          // kTailLevels x nn0 x d
+  long long *lvl_cut2;                     // kTailLevels
+  int32_t nn0, ed0, cur0, d, tcap, n_levels, level0, round0, max_rounds;
+  int32_t want_energy;
+  double lambda[kTailLevels];
+  long long smin[kTailLevels];
+};
+
+// Exclusive scan of value(0..len) into out[0..len], out[len] = total.
+template <class V>
+__device__ __forceinline__ int32_t tail_scan(int32_t len, V &&value,
+                                             int32_t *out, int32_t *wsum) {
+  const int32_t per = (len + kTailNT - 1) / kTailNT;
+  const int32_t b0 = (int32_t)threadIdx.x * per;
+  int32_t sum = 0;
+  for (int32_t j = 0; j < per; ++j)
+    if (b0 + j < len) sum += value(b0 + j);
+  int32_t tot;
+  int32_t run = block_excl_scan<kTailNT>(sum, wsum, &tot);
+  for (int32_t j = 0; j < per; ++j) {
+    const int32_t i = b0 + j;
+    if (i < len) {
+      const int32_t v = value(i);
+      out[i] = run;
+      run += v;
+    }
+  }
+  if (threadIdx.x == 0) out[len] = tot;
+  __syncthreads();
+  return tot;
+}
+
+template <int DT>
+__global__ __launch_bounds__(kTailNT) void k_tail(TailState t, Ctl *ctl) {
+  __shared__ int32_t wsum[kTailWaves];
+  __shared__ int32_t s_any, s_flag, s_claims, s_nlong, s_nlongc;
+  __shared__ long long s_cut;
+  const int lane = threadIdx.x & (kWave - 1);
+  const int wave = threadIdx.x / kWave;
+  const int32_t d = t.d;
+  const double sF = ldexp(1.0, ctl->F), sIF = ldexp(1.0, -ctl->F);
+  int32_t nn = t.nn0, ed = t.ed0, cur = t.cur0;
+  for (int32_t i = threadIdx.x; i < t.nn0; i += kTailNT) t.Mt[i] = i;
+  __syncthreads();
+  for (int32_t l = t.level0; l < t.n_levels; ++l) {
+    const double lambda = t.lambda[l];
+    const long long smin = t.smin[l];
+    for (int32_t round = (l == t.level0 ? t.round0 : 0);; ++round) {
+      if (ed == 0) break;
+      if (round >= t.max_rounds) {
+        if (threadIdx.x == 0) {
+          ctl->tail_level = l;
+          raise_err(ctl, kErrNotConv);
+        }
+        return;
+      }
+      const int nxt = 1 - cur;
+      Adj a;
+      a.ws = t.ws[cur];
+      a.wl = t.wl[cur];
+      a.tbl = t.tbl[cur];
+      NodeIn s;
+      s.size = t.size[cur];
+      s.S = t.S[cur];
+      s.mu = t.mu;
+      s.minpt = t.minpt[cur];
+      s.emb = nullptr;
+      s.perm = nullptr;
+      // Steps 1-2: a thread per short row, long rows listed for a wave each
+      if (threadIdx.x == 0) {
+        s_any = 0;
+        s_nlong = 0;
+      }
+      __syncthreads();
+      for (int32_t v = threadIdx.x; v < nn; v += kTailNT) {
+        if (a.wl[v] > kTailShort) {
+          t.longrow[atomicAdd(&s_nlong, 1)] = v;
+          continue;
+        }
+        const double dsv = (double)s.size[v];
+        const bool small = (long long)s.size[v] < smin;
+        MeanRow<false, DT> mv;
+        mv.load(s, v, sF, sIF);
+        Best b{0.0, 0, -1};
+        int32_t cnt = 0;
+        for_row<false>(a, v, 0, 1, [&](int32_t u, int32_t w) {
+          ++cnt;
+          if ((uint32_t)u >= (uint32_t)nn) {
+            raise_err(ctl, kErrInternal);
+            return;
+          }
+          const double g =
+              edge_gain_t<false, DT>(s, mv, v, dsv, u, w, d, lambda, sF, sIF);
+          if (g > 0.0 || small) {
+            const Best c{g, s.minpt[u], u};
+            if (best_before(c, b)) b = c;
+          }
+        });
+        t.target[v] = b.u;
+        t.deg[v] = cnt;
+        if (b.u >= 0) s_any = 1;
+      }
+      __syncthreads();
+      const int32_t nlong = s_nlong;
+      for (int32_t j = wave; j < nlong; j += kTailWaves) {
+        const int32_t v = t.longrow[j];
+        const double dsv = (double)s.size[v];
+        const bool small = (long long)s.size[v] < smin;
+        MeanRow<false, DT> mv;
+        mv.load(s, v, sF, sIF);
+        Best b{0.0, 0, -1};
+        int32_t cnt = 0;
+        for_row<false>(a, v, lane, kWave, [&](int32_t u, int32_t w) {
+          ++cnt;
+          if ((uint32_t)u >= (uint32_t)nn) {
+            raise_err(ctl, kErrInternal);
+            return;
+          }
+          const double g =
+              edge_gain_t<false, DT>(s, mv, v, dsv, u, w, d, lambda, sF, sIF);
+          if (g > 0.0 || small) {
+            const Best c{g, s.minpt[u], u};
+            if (best_before(c, b)) b = c;
+          }
+        });
+        cnt = wave_sum(cnt);
+#pragma unroll
+        for (int off = kWave / 2; off > 0; off >>= 1) {
+          Best o;
+          o.g = __shfl_xor(b.g, off, kWave);
+          o.mp = __shfl_xor(b.mp, off, kWave);
+          o.u = __shfl_xor(b.u, off, kWave);
+          if (best_before(o, b)) b = o;
+        }
+        if (lane == 0) {
+          t.target[v] = b.u;
+          t.deg[v] = cnt;
+          if (b.u >= 0) s_any = 1;
+        }
+      }
+      __syncthreads();
+      if (!s_any) break;  // Step 1: no candidate merge
+      // Step 3: hook, jump
+      for (int32_t v = threadIdx.x; v < nn; v += kTailNT) {
+        const int32_t tg = t.target[v];
+        int32_t p = v;
+        if (tg >= 0) {
+          if (tg >= nn) {
+            raise_err(ctl, kErrInternal);
+          } else {
+            p = (t.target[tg] == v && v < tg) ? v : tg;
+          }
+        }
+        t.parent[v] = p;
+      }
+      __syncthreads();
+      for (int pass = 0;; ++pass) {
+        if (threadIdx.x == 0) s_flag = 0;
+        __syncthreads();
+        for (int32_t v = threadIdx.x; v < nn; v += kTailNT) {
+          const int32_t p = t.parent[v];
+          const int32_t pp = t.parent[p];
+          if (pp != p) {
+            t.parent[v] = pp;
+            s_flag = 1;
+          }
+        }
+        __syncthreads();
+        const int more = s_flag;
+        __syncthreads();  // all have read the flag before the next reset
+        if (!more) break;
+        if (pass == kTailJumps) {
+          if (threadIdx.x == 0) raise_err(ctl, kErrJump);
+          return;
+        }
+      }
+      // relabel: roots numbered in node order
+      int32_t *par = t.parent;
+      const int32_t C = tail_scan(
+          nn, [&](int32_t v) { return par[v] == v ? 1 : 0; }, t.newid, wsum);
+      for (int32_t c = threadIdx.x; c < C; c += kTailNT) t.cnt[c] = 0;
+      __syncthreads();
+      for (int32_t v = threadIdx.x; v < nn; v += kTailNT) {
+        const int32_t c = t.newid[t.parent[v]];
+        t.L[v] = c;
+        t.target[v] = atomicAdd(&t.cnt[c], 1);  // place among members
+      }
+      __syncthreads();
+      int32_t *cnt = t.cnt;
+      tail_scan(C, [&](int32_t c) { return cnt[c]; }, t.moff, wsum);
+      for (int32_t v = threadIdx.x; v < nn; v += kTailNT)
+        t.mem[t.moff[t.L[v]] + t.target[v]] = v;
+      __syncthreads();
+      // Step 4 statistics: a thread per small component, big ones listed
+      // for a wave each
+      if (threadIdx.x == 0) s_nlongc = 0;
+      __syncthreads();
+      for (int32_t c = threadIdx.x; c < C; c += kTailNT) {
+        const int32_t m0 = t.moff[c], m1 = t.moff[c + 1];
+        if (m1 - m0 > kTailShort) {
+          t.longcomp[atomicAdd(&s_nlongc, 1)] = c;
+          continue;
+        }
+        int32_t size = 0, mp = INT32_MAX, cap = 0;
+        for (int32_t j = m0; j < m1; ++j) {
+          const int32_t m = t.mem[j];
+          size += s.size[m];
+          mp = min(mp, s.minpt[m]);
+          cap += t.deg[m];
+        }
+        t.size[nxt][c] = size;
+        t.minpt[nxt][c] = mp;
+        t.capn[c] = cap;
+        t.wl[nxt][c] = cap;
+        for (int32_t i = 0; i < d; ++i) {
+          long long acc = 0;
+          for (int32_t j = m0; j < m1; ++j)
+            acc += s.S[(int64_t)t.mem[j] * d + i];
+          t.S[nxt][(int64_t)c * d + i] = acc;
+          const double q = (double)acc / (double)size;
+          t.mu[(int64_t)c * d + i] = q * sIF;
+        }
+      }
+      __syncthreads();
+      const int32_t nlongc = s_nlongc;
+      for (int32_t j = wave; j < nlongc; j += kTailWaves) {
+        const int32_t c = t.longcomp[j];
+        const int32_t m0 = t.moff[c], m1 = t.moff[c + 1];
+        int32_t size = 0, mp = INT32_MAX, cap = 0;
+        for (int32_t q = m0 + lane; q < m1; q += kWave) {
+          const int32_t m = t.mem[q];
+          size += s.size[m];
+          mp = min(mp, s.minpt[m]);
+          cap += t.deg[m];
+        }
+        size = wave_sum(size);
+        cap = wave_sum(cap);
+#pragma unroll
+        for (int off = kWave / 2; off > 0; off >>= 1)
+          mp = min(mp, __shfl_xor(mp, off, kWave));
+        if (lane == 0) {
+          t.size[nxt][c] = size;
+          t.minpt[nxt][c] = mp;
+          t.capn[c] = cap;
+          t.wl[nxt][c] = cap;
+        }
+        for (int32_t i = 0; i < d; ++i) {
+          long long acc = 0;
+          for (int32_t q = m0 + lane; q < m1; q += kWave)
+            acc += s.S[(int64_t)t.mem[q] * d + i];
+          acc = wave_sum(acc);
+          if (lane == 0) {
+            t.S[nxt][(int64_t)c * d + i] = acc;
+            const double q = (double)acc / (double)size;
+            t.mu[(int64_t)c * d + i] = q * sIF;
+          }
+        }
+      }
+      __syncthreads();
+      int32_t *capn = t.capn;
+      const int32_t slots =
+          tail_scan(C, [&](int32_t c) { return capn[c]; }, t.ws[nxt], wsum);
+      if (slots > t.tcap) {
+        if (threadIdx.x == 0) raise_err(ctl, kErrInternal);
+        return;
+      }
+      for (int32_t q = threadIdx.x; q < slots; q += kTailNT)
+        t.tbl[nxt][q] = kEmpty;
+      if (threadIdx.x == 0) s_claims = 0;
+      __syncthreads();
+      // Step 4 contraction: a thread per short row, a wave per long row
+      int32_t claims = 0;
+      auto add_row = [&](int32_t v, int32_t begin, int32_t step) {
+        const int32_t A = t.L[v];
+        const int32_t base = t.ws[nxt][A], cp = t.capn[A];
+        for_row<false>(a, v, begin, step, [&](int32_t u, int32_t w) {
+          if ((uint32_t)u >= (uint32_t)nn) {
+            raise_err(ctl, kErrInternal);
+            return;
+          }
+          const int32_t B = t.L[u];
+          if (B == A) return;
+          if (cp <= 0 || base + cp > slots) {
+            raise_err(ctl, kErrInternal);
+            return;
+          }
+          claims += table_add(t.tbl[nxt], base, cp, B, w, ctl) ? 1 : 0;
+        });
+      };
+      for (int32_t v = threadIdx.x; v < nn; v += kTailNT)
+        if (a.wl[v] <= kTailShort) add_row(v, 0, 1);
+      for (int32_t j = wave; j < nlong; j += kTailWaves)
+        add_row(t.longrow[j], lane, kWave);
+      claims = wave_sum(claims);
+      if (lane == 0 && claims) atomicAdd(&s_claims, claims);
+      for (int32_t i = threadIdx.x; i < t.nn0; i += kTailNT)
+        t.Mt[i] = t.L[t.Mt[i]];
+      __syncthreads();
+      nn = C;
+      ed = s_claims;
+      cur = nxt;
+      __syncthreads();
+      if (nn == 1) break;  // a single component is left
+    }
+    // level end: snapshot for the labels and the energy
+    if (threadIdx.x == 0) {
+      t.lvl_nc[l] = nn;
+      s_cut = 0;
+    }
+    for (int32_t i = threadIdx.x; i < t.nn0; i += kTailNT)
+      t.lvl_map[(int64_t)l * t.nn0 + i] = t.Mt[i];
+    for (int32_t c = threadIdx.x; c < nn; c += kTailNT)
+      t.lvl_minpt[(int64_t)l * t.nn0 + c] = t.minpt[cur][c];
+    __syncthreads();
+    if (t.want_energy) {
+      for (int64_t q = threadIdx.x; q < (int64_t)nn * d; q += kTailNT)
+        t.lvl_mu[(int64_t)l * t.nn0 * d + q] = t.mu[q];
+      Adj a;
+      a.ws = t.ws[cur];
+      a.wl = t.wl[cur];
+      a.tbl = t.tbl[cur];
+      long long acc = 0;
+      for (int32_t v = threadIdx.x; v < nn; v += kTailNT)
+        for_row<false>(a, v, 0, 1, [&](int32_t, int32_t w) { acc += w; });
+      acc = wave_sum(acc);
+      if (lane == 0 && acc)
+        atomicAdd(reinterpret_cast<unsigned long long *>(&s_cut),
+                  (unsigned long long)acc);
+      __syncthreads();
+      if (threadIdx.x == 0) t.lvl_cut2[l] = s_cut;
+    }
+    __syncthreads();
+  }
+}
+
+// ---------------------------------------------------------------------------
 // host driver
 // ---------------------------------------------------------------------------
 namespace {
@@ -1178,8 +1556,12 @@ struct Bufs {
   int64_t *S[2];
   double *mu;
   int32_t *target, *deg, *parent, *newid, *L, *cnt, *rank, *moff, *mem;
-  int32_t *long_rows, *big, *cbig, *capn;
+  int32_t *long_rows, *big, *cbig, *capn, *tile_c, *tile_i;
   int32_t *M, *mark, *lrank;
+  int32_t nt;  // nodes the tail can start from
+  int32_t *Mt, *lvl_map, *lvl_minpt, *lvl_nc;
+  double *lvl_mu;
+  long long *lvl_cut2;
   int32_t *bsum, *tmp;
   double *partial;
 };
@@ -1218,9 +1600,18 @@ void carve(Arena &a, int32_t n, int32_t d, int32_t k, Bufs *b) {
   b->big = a.take<int32_t>(n1);
   b->cbig = a.take<int32_t>(n1);
   b->capn = a.take<int32_t>(n1);
+  b->tile_c = a.take<int32_t>(2 * n1);
+  b->tile_i = a.take<int32_t>(2 * n1);
   b->M = a.take<int32_t>(n1);
   b->mark = a.take<int32_t>(n1);
   b->lrank = a.take<int32_t>(n1);
+  b->nt = std::min<int32_t>(n, kTailNodes);
+  b->Mt = a.take<int32_t>(b->nt);
+  b->lvl_map = a.take<int32_t>((size_t)kTailLevels * b->nt);
+  b->lvl_minpt = a.take<int32_t>((size_t)kTailLevels * b->nt);
+  b->lvl_nc = a.take<int32_t>(kTailLevels);
+  b->lvl_mu = a.take<double>((size_t)kTailLevels * b->nt * d);
+  b->lvl_cut2 = a.take<long long>(kTailLevels);
   b->bsum = a.take<int32_t>(scan_blocks(ed + n1) + 2);
   b->tmp = a.take<int32_t>(8);
   b->partial = a.take<double>(kEnergyBlocks);
@@ -1264,12 +1655,20 @@ void launch_round(const Bufs &b, const Adj &adj, int cur, int32_t n,
   const int32_t tcap = (int32_t)edge_bound(n, k);
   hipLaunchKernelGGL(k_round_init, dim3(1), dim3(64), 0, st, ctl);
   prof_begin("select", st);
-  hipLaunchKernelGGL((k_select<FIRST, DT>), xblocks_for(nn), dim3(256), 0, st, nn,
-                     adj, s, d, lambda, smin, b.target, b.deg, b.long_rows,
-                     ctl);
-  hipLaunchKernelGGL((k_select_long<FIRST, DT>), dim3(kLongGrid), dim3(256), 0, st,
+  // small rounds: every row by a wave (parallel over entries); large rounds:
+  // a thread per row, long rows by waves
+  const bool all_rows = nn <= kWaveRowsMax;
+  const dim3 long_grid((unsigned)std::max<int64_t>(
+      1, std::min<int64_t>(all_rows ? (nn + 3) / 4 : kLongGrid, (nn + 3) / 4)));
+  const dim3 big_grid(
+      (unsigned)std::max<int64_t>(1, std::min<int64_t>(kBigGrid, nn / 16)));
+  if (!all_rows)
+    hipLaunchKernelGGL((k_select<FIRST, DT>), xblocks_for(nn), dim3(256), 0,
+                       st, nn, adj, s, d, lambda, smin, b.target, b.deg,
+                       b.long_rows, ctl);
+  hipLaunchKernelGGL((k_select_long<FIRST, DT>), long_grid, dim3(256), 0, st,
                      nn, adj, s, d, lambda, smin, b.target, b.deg, b.long_rows,
-                     ctl);
+                     all_rows, ctl);
   prof_end(st);
   prof_begin("union", st);
   hipLaunchKernelGGL(k_hook, blocks_for(nn), dim3(256), 0, st, nn, b.target,
@@ -1287,25 +1686,30 @@ void launch_round(const Bufs &b, const Adj &adj, int cur, int32_t n,
               b.tmp, st);
   hipLaunchKernelGGL(k_place, xblocks_for(nn), dim3(256), 0, st, nn, b.L,
                      b.moff, b.rank, b.mem, ctl);
-  const NodeOut o{b.size[nxt], b.S[nxt], b.mu,    b.minpt[nxt],
-                  b.capn,      b.wl[nxt], b.cbig};
+  // contraction chunks: enough blocks to fill the chip, at most kChunk
+  int32_t chunk = kChunk;
+  while (chunk > 64 && (int64_t)ed / chunk < 2048) chunk >>= 1;
+  const NodeOut o{b.size[nxt], b.S[nxt],  b.mu,
+                  b.minpt[nxt], b.capn,    b.wl[nxt],
+                  b.cbig,      chunk,     nn > kWaveRowsMax ? kBigComp : 16,
+                  b.tile_c,    b.tile_i};
   hipLaunchKernelGGL((k_stats<FIRST, DT>), xblocks_for(nn), dim3(256), 0, st, nn,
                      b.mem, b.moff, s, b.deg, d, o, b.big, ctl);
-  hipLaunchKernelGGL(k_stats_big<FIRST>, dim3(kBigGrid), dim3(256), 0, st,
+  hipLaunchKernelGGL(k_stats_big<FIRST>, big_grid, dim3(256), 0, st,
                      b.mem, b.moff, s, b.deg, d, o, b.big, ctl);
   prof_end(st);
   prof_begin("contract", st);
   device_scan(ScanArray{b.capn, b.ws[nxt], nn, &ctl->n_next}, nn + 1, b.bsum,
               &ctl->slots, st);
   hipLaunchKernelGGL(k_contract_chunk<FIRST>,
-                     dim3(xcd_grid((ed + kChunk - 1) / kChunk)), dim3(256), 0,
+                     dim3(xcd_grid((ed + chunk - 1) / chunk)), dim3(256), 0,
                      st, nn, adj, b.L, b.mem, b.moff, b.ws[nxt], b.capn,
-                     b.tbl[nxt], b.wl[nxt], ctl);
-  hipLaunchKernelGGL(k_clear_big, dim3(kBigGrid), dim3(256), 0, st, b.cbig,
+                     b.tbl[nxt], b.wl[nxt], chunk, ctl);
+  hipLaunchKernelGGL(k_clear_big, big_grid, dim3(256), 0, st, b.cbig,
                      b.ws[nxt], b.capn, b.tbl[nxt], tcap, ctl);
-  hipLaunchKernelGGL(k_contract_big<FIRST>, dim3(kBigGrid), dim3(256), 0, st,
-                     nn, adj, b.L, b.mem, b.moff, b.ws[nxt], b.capn, b.cbig,
-                     b.tbl[nxt], tcap, ctl);
+  hipLaunchKernelGGL(k_contract_big<FIRST>, big_grid, dim3(256), 0, st, nn,
+                     adj, b.L, b.mem, b.moff, b.ws[nxt], b.capn, b.tile_c,
+                     b.tile_i, b.tbl[nxt], tcap, ctl);
   prof_end(st);
   prof_begin("compose", st);
   hipLaunchKernelGGL(k_compose<FIRST>, xblocks_for(n), dim3(256), 0, st, n,
@@ -1335,6 +1739,123 @@ void round_d(const Bufs &b, const Adj &adj, int cur, int32_t n, int32_t k,
       launch_round<FIRST, 0>(b, adj, cur, n, k, nn, ed, d, s, lambda, smin,
                              ctl, st);
   }
+}
+
+// The rest of the ladder in the tail kernel, then the labels (and energy)
+// of every level it ended.
+int run_tail(const LadderArgs &g, const Bufs &b, const float *emb,
+             const Adj &adj, int cur, int32_t nn, int32_t ed, int32_t level0,
+             int32_t round0, int32_t max_rounds, Ctl *ctl, Ctl *h,
+             hipStream_t st) {
+  const int32_t n = g.n, d = g.d;
+  TailState t;
+  for (int j = 0; j < 2; ++j) {
+    t.ws[j] = b.ws[j];
+    t.wl[j] = b.wl[j];
+    t.tbl[j] = b.tbl[j];
+    t.size[j] = b.size[j];
+    t.minpt[j] = b.minpt[j];
+    t.S[j] = b.S[j];
+  }
+  t.mu = b.mu;
+  t.target = b.target;
+  t.deg = b.deg;
+  t.parent = b.parent;
+  t.newid = b.newid;
+  t.L = b.L;
+  t.cnt = b.cnt;
+  t.moff = b.moff;
+  t.mem = b.mem;
+  t.capn = b.capn;
+  t.Mt = b.Mt;
+  t.longrow = b.tile_c;  // the tile lists are free while the tail runs
+  t.longcomp = b.tile_i;
+  t.lvl_map = b.lvl_map;
+  t.lvl_minpt = b.lvl_minpt;
+  t.lvl_nc = b.lvl_nc;
+  t.lvl_mu = b.lvl_mu;
+  t.lvl_cut2 = b.lvl_cut2;
+  t.nn0 = nn;
+  t.ed0 = ed;
+  t.cur0 = cur;
+  t.d = d;
+  t.tcap = (int32_t)edge_bound(n, g.k);
+  t.n_levels = g.n_levels;
+  t.level0 = level0;
+  t.round0 = round0;
+  t.max_rounds = max_rounds;
+  t.want_energy = (g.want_energy && g.energy) ? 1 : 0;
+  for (int l = 0; l < kTailLevels; ++l) {
+    t.lambda[l] = l < g.n_levels ? g.lambdas[l] : 0.0;
+    t.smin[l] = (l < g.n_levels && g.min_size) ? g.min_size[l] : 0;
+  }
+  (void)adj;
+  prof_begin("tail", st);
+  switch (d) {
+    case 8:
+      hipLaunchKernelGGL(k_tail<8>, dim3(1), dim3(kTailNT), 0, st, t, ctl);
+      break;
+    case 16:
+      hipLaunchKernelGGL(k_tail<16>, dim3(1), dim3(kTailNT), 0, st, t, ctl);
+      break;
+    case 32:
+      hipLaunchKernelGGL(k_tail<32>, dim3(1), dim3(kTailNT), 0, st, t, ctl);
+      break;
+    default:
+      hipLaunchKernelGGL(k_tail<0>, dim3(1), dim3(kTailNT), 0, st, t, ctl);
+  }
+  prof_end(st);
+  int rc = read_ctl(ctl, h, st);
+  if (rc) return rc;
+  if (h->err & kErrNotConv) {
+    set_error("level %d reached max_rounds = %d", h->tail_level, max_rounds);
+    return -6;
+  }
+  if (h->err) return status_from_err(h->err);
+  int32_t nc[kTailLevels];
+  long long cut2[kTailLevels];
+  rc = check_hip(hipMemcpyAsync(nc, b.lvl_nc, sizeof(nc),
+                                hipMemcpyDeviceToHost, st),
+                 "hipMemcpyAsync(levels)");
+  if (!rc)
+    rc = check_hip(hipMemcpyAsync(cut2, b.lvl_cut2, sizeof(cut2),
+                                  hipMemcpyDeviceToHost, st),
+                   "hipMemcpyAsync(levels)");
+  if (!rc) rc = check_hip(hipStreamSynchronize(st), "hipStreamSynchronize");
+  if (rc) return rc;
+  for (int32_t l = level0; l < g.n_levels; ++l) {
+    const int32_t ncl = nc[l];
+    if (ncl < 1 || ncl > nn) {
+      set_error("tail level %d: %d superpoints", l, ncl);
+      return -5;
+    }
+    // level snapshots have a stride of the tail's start size nn
+    const int32_t *map = b.lvl_map + (int64_t)l * nn;
+    const int32_t *mp = b.lvl_minpt + (int64_t)l * nn;
+    int32_t *out = g.labels + (int64_t)l * n;
+    hipLaunchKernelGGL(k_fill_i32, blocks_for(n), dim3(256), 0, st, b.mark,
+                       (int64_t)n, 0);
+    hipLaunchKernelGGL(k_mark, blocks_for(ncl), dim3(256), 0, st, ncl, mp,
+                       b.mark, n, ctl);
+    device_scan(ScanArray{b.mark, b.lrank, n, nullptr}, n, b.bsum, b.tmp, st);
+    hipLaunchKernelGGL(k_labels, blocks_for(n), dim3(256), 0, st, n, ncl,
+                       g.inv, b.M, map, nn, mp, b.lrank, out, ctl);
+    g.n_comp[l] = ncl;
+    if (t.want_energy) {
+      hipLaunchKernelGGL(k_energy_reset, dim3(1), dim3(64), 0, st, ctl);
+      hipLaunchKernelGGL(k_energy_fid<false>, dim3(kEnergyBlocks), dim3(256),
+                         0, st, n, d, ncl, emb, b.M, map, nn,
+                         b.lvl_mu + (int64_t)l * nn * d, ctl, b.partial);
+      hipLaunchKernelGGL(k_energy_sum, dim3(1), dim3(64), 0, st, b.partial,
+                         kEnergyBlocks, ctl);
+      if ((rc = read_ctl(ctl, h, st))) return rc;
+      if (h->err) return status_from_err(h->err);
+      const double cut = (double)(cut2[l] / 2);
+      const double reg = g.lambdas[l] * cut;
+      g.energy[l] = h->fid_total + reg;
+    }
+  }
+  return 0;
 }
 
 }  // namespace
@@ -1417,11 +1938,24 @@ int ladder_run(const LadderArgs &g, Ctl *ctl, Arena &a, hipStream_t st) {
   bool first = true;
   int32_t nn = n;
   const int32_t max_rounds = g.max_rounds > 0 ? g.max_rounds : 256;
+  int32_t tail_level = -1, tail_round = 0;
+  // EZSP_TAIL_NODES (at most kTailNodes; 0 = never) moves the switch to the
+  // tail kernel, so that both paths can be exercised on small inputs
+  int32_t tail_nodes = kTailStart;
+  if (const char *e = getenv("EZSP_TAIL_NODES")) {
+    const long v = strtol(e, nullptr, 10);
+    tail_nodes = (int32_t)std::max<long>(0, std::min<long>(v, kTailNodes));
+  }
   for (int32_t l = 0; l < g.n_levels; ++l) {
     const double lambda = g.lambdas[l];
     const int64_t smin = g.min_size ? g.min_size[l] : 0;
     for (int32_t round = 0;; ++round) {
       if (ed == 0) break;  // no edge left: nothing can merge
+      if (!first && nn <= tail_nodes && ed <= kTailEdges) {
+        tail_level = l;  // the rest runs in the tail kernel
+        tail_round = round;
+        break;
+      }
       if (round >= max_rounds) {
         set_error("level %d reached max_rounds = %d", l, max_rounds);
         return -6;
@@ -1476,6 +2010,7 @@ int ladder_run(const LadderArgs &g, Ctl *ctl, Arena &a, hipStream_t st) {
       if (nn == 1) break;  // a single component is left
     }
 
+    if (tail_level >= 0) break;
     // level output
     int32_t *out = g.labels + (int64_t)l * n;
     if (first) {
@@ -1488,18 +2023,20 @@ int ladder_run(const LadderArgs &g, Ctl *ctl, Arena &a, hipStream_t st) {
       device_scan(ScanArray{b.mark, b.lrank, n, nullptr}, n, b.bsum, b.tmp,
                   st);
       hipLaunchKernelGGL(k_labels, blocks_for(n), dim3(256), 0, st, n, nn,
-                         g.inv, b.M, b.minpt[cur], b.lrank, out, ctl);
+                         g.inv, b.M, (const int32_t *)nullptr, 0,
+                         b.minpt[cur], b.lrank, out, ctl);
     }
     g.n_comp[l] = nn;
     if (g.want_energy && g.energy) {
       hipLaunchKernelGGL(k_energy_reset, dim3(1), dim3(64), 0, st, ctl);
       if (first)
         hipLaunchKernelGGL(k_energy_fid<true>, dim3(kEnergyBlocks), dim3(256),
-                           0, st, n, d, nn, emb, b.M, b.mu, ctl, b.partial);
+                           0, st, n, d, nn, emb, b.M, (const int32_t *)nullptr,
+                           0, b.mu, ctl, b.partial);
       else
         hipLaunchKernelGGL(k_energy_fid<false>, dim3(kEnergyBlocks),
-                           dim3(256), 0, st, n, d, nn, emb, b.M, b.mu, ctl,
-                           b.partial);
+                           dim3(256), 0, st, n, d, nn, emb, b.M,
+                           (const int32_t *)nullptr, 0, b.mu, ctl, b.partial);
       hipLaunchKernelGGL(k_energy_sum, dim3(1), dim3(64), 0, st, b.partial,
                          kEnergyBlocks, ctl);
       if (!first)
@@ -1512,6 +2049,11 @@ int ladder_run(const LadderArgs &g, Ctl *ctl, Arena &a, hipStream_t st) {
       const double reg = lambda * cut;
       g.energy[l] = h->fid_total + reg;
     }
+  }
+  if (tail_level >= 0) {
+    rc = run_tail(g, b, emb, adj, cur, nn, ed, tail_level, tail_round,
+                  max_rounds, ctl, h, st);
+    if (rc) return rc;
   }
   if ((rc = read_ctl(ctl, h, st))) return rc;
   if (h->err) return status_from_err(h->err);

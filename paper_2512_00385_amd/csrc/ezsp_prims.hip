@@ -174,6 +174,8 @@ __global__ void k_ctl_init(Ctl *ctl) {
     ctl->e_rev = 0;
     ctl->e_fwd = 0;
     ctl->n_cbig = 0;
+    ctl->n_tiles = 0;
+    ctl->tail_level = -1;
     ctl->cut_w2 = 0;
     ctl->fid_total = 0.0;
   }

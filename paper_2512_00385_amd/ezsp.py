@@ -102,7 +102,7 @@ def profile_enable(on: bool = True):
 
 
 STAGES = ("morton_sort", "knn_query", "graph_build", "select", "union",
-          "stats", "contract", "compose")
+          "stats", "contract", "compose", "tail")
 
 
 def profile_read(stage: str):

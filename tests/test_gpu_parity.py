@@ -123,15 +123,31 @@ def check_against_oracle(xyz, emb, k, lambdas, min_size=None, max_rounds=0):
     return labels, nc
 
 
-def test_partition_room_full():
+@pytest.fixture(params=["tail", "no-tail"])
+def tail_mode(request, monkeypatch):
+    """Small graphs finish in the single-block tail kernel; "no-tail" keeps
+    every round on the multi-kernel path (EZSP_TAIL_NODES=0)."""
+    if request.param == "no-tail":
+        monkeypatch.setenv("EZSP_TAIL_NODES", "0")
+    else:
+        monkeypatch.delenv("EZSP_TAIL_NODES", raising=False)
+    return request.param
+
+
+def test_partition_room_full(tail_mode):
     sc = scenes.load("room-20k")
     check_against_oracle(sc.xyz, sc.emb, sc.k, sc.lambdas)
+
+
+def test_partition_room_ladder(tail_mode):
+    sc = scenes.load("room-20k")
+    check_against_oracle(sc.xyz, sc.emb, sc.k, [0.02, 0.05, 0.2, 0.8, 3.2])
 
 
 @pytest.mark.parametrize("seed", range(6))
 @pytest.mark.parametrize("lambdas", [[0.1], [0.05, 0.2, 0.8], [0.8, 0.2],
                                      [0.01, 0.03, 0.1, 0.3, 1.0, 3.0]])
-def test_partition_random_clouds(seed, lambdas):
+def test_partition_random_clouds(seed, lambdas, tail_mode):
     sc = scenes.random_cloud(3000 + 137 * seed, 1 + 5 * seed, seed=seed,
                              sigma=0.05 * (1 + seed % 3))
     check_against_oracle(sc.xyz, sc.emb, 10, lambdas)
@@ -143,7 +159,7 @@ def test_partition_k(k):
     check_against_oracle(sc.xyz, sc.emb, k, [0.05, 0.4])
 
 
-def test_partition_min_size():
+def test_partition_min_size(tail_mode):
     sc = scenes.random_cloud(3000, 6, seed=4, sigma=0.3)
     check_against_oracle(sc.xyz, sc.emb, 8, [0.01, 0.05, 0.05],
                          min_size=[5, 30, 90])
@@ -155,7 +171,7 @@ def test_partition_lambda_zero_and_huge():
     assert nc[0] == sc.n and (labels[0] == np.arange(sc.n)).all()
 
 
-def test_partition_constant_embeddings_ties():
+def test_partition_constant_embeddings_ties(tail_mode):
     """Every gain equal: conflict removal is decided by the tie rule alone."""
     sc = scenes.random_cloud(2000, 3, seed=8)
     emb = np.ones_like(sc.emb) * 0.25
@@ -173,7 +189,7 @@ def test_partition_duplicate_points():
 
 
 @pytest.mark.parametrize("d", [1, 2, 64])
-def test_partition_dims(d):
+def test_partition_dims(d, tail_mode):
     sc = scenes.random_cloud(1500, d, seed=20 + d)
     check_against_oracle(sc.xyz, sc.emb, 10, [0.02 * d, 0.2 * d])
 
@@ -186,7 +202,7 @@ def test_partition_tiny(n):
     check_against_oracle(xyz, emb, 10, [0.5, 2.0, 8.0])
 
 
-def test_partition_max_rounds():
+def test_partition_max_rounds(tail_mode):
     sc = scenes.random_cloud(2000, 4, seed=9)
     with pytest.raises(oracle.OracleError):
         oracle.partition(sc.xyz, sc.emb, 10, [0.2], max_rounds=1)
@@ -231,7 +247,7 @@ def test_partition_deterministic():
 # partition on a given neighbour table
 # --------------------------------------------------------------------------
 
-def test_from_knn_matches_graph_oracle():
+def test_from_knn_matches_graph_oracle(tail_mode):
     sc = scenes.random_cloud(3000, 5, seed=13)
     nbr, _ = oracle.knn(sc.xyz, 8)
     lo, hi, w = oracle.graph(nbr)
