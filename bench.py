@@ -9,10 +9,17 @@ canonical per-level labels.  Prints one JSON line:
                launch over its mean launch duration (HIP events on the
                library's stream), against the 8 TB/s HBM peak
   cpu_baseline the CPU oracle (one thread) on a bounded slab of the same tile
+
+roofline.traffic comes from the committed counter summary
+profiles/knn_query.driving-3m.pmc.md (rocprofv3 FETCH_SIZE and WRITE_SIZE,
+scaled by what the same counters read for a copy kernel of known size; see
+--calib-copy); it is reported only while the kernel sources still hash to
+the values recorded there, and null otherwise.
 """
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import os
 import platform
@@ -25,6 +32,8 @@ if ROOT not in sys.path:
 
 HBM_PEAK_GBS = 8000.0
 WORKLOAD = "driving-3m"
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "knn_query.driving-3m.pmc.md")
+CALIB_ELEMS = 1 << 28  # float32 elements of the calibration copy (1 GiB)
 
 
 def parse():
@@ -35,20 +44,64 @@ def parse():
     ap.add_argument("--workload", default=WORKLOAD)
     ap.add_argument("--no-cpu", action="store_true",
                     help="skip the CPU oracle baseline")
-    ap.add_argument("--cpu-points", type=int, default=400_000)
+    ap.add_argument("--cpu-points", type=int, default=3_000_000)
+    ap.add_argument("--calib-copy", action="store_true",
+                    help="after the timed steps, run one plain copy kernel "
+                    "of 1 GiB in and 1 GiB out (scale for the HBM counters)")
     return ap.parse_args()
 
 
+def source_digest(files):
+    """sha256 over the named sources under paper_2512_00385_amd/csrc."""
+    h = hashlib.sha256()
+    for f in files:
+        with open(os.path.join(ROOT, "paper_2512_00385_amd", "csrc", f),
+                  "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def measured_traffic(stage, n_points, k):
+    """HBM bytes per launch of `stage` from the committed counter summary,
+    or None when there is none for this stage and workload or the kernel
+    sources changed since the counters were taken."""
+    if not os.path.exists(TRAFFIC_FILE):
+        return None
+    kv = {}
+    with open(TRAFFIC_FILE) as fh:
+        for line in fh:
+            line = line.strip()
+            if line.startswith("- ") and ":" in line:
+                key, val = line[2:].split(":", 1)
+                kv[key.strip()] = val.strip().strip("`")
+    try:
+        if kv.get("stage") != stage or int(kv["n_points"]) != n_points or \
+                int(kv["k"]) != k:
+            return None
+        files = kv["sources"].split(",")
+        if source_digest([f.strip() for f in files]) != kv["sources_sha256"]:
+            return None
+        return float(kv["traffic_bytes_per_launch"])
+    except (KeyError, ValueError, OSError):
+        return None
+
+
 def cpu_baseline(sc, n_sample):
-    """Oracle (single-threaded C) on the slab of the tile around x = 0 that
-    holds n_sample points: full density profile of the scene, sensor
-    included."""
+    """Oracle (single-threaded C) on the whole tile, or, when n_sample is
+    smaller, on the slab of the tile around x = 0 that holds n_sample points
+    (full density profile of the scene, sensor included)."""
     import numpy as np
     import oracle
-    order = np.argsort(np.abs(sc.xyz[:, 0]), kind="stable")[:n_sample]
-    idx = np.sort(order)
-    xyz = np.ascontiguousarray(sc.xyz[idx])
-    emb = np.ascontiguousarray(sc.emb[idx])
+    if n_sample >= sc.n:
+        xyz, emb = sc.xyz, sc.emb
+        what = f"the whole {sc.name} tile ({sc.n} points)"
+    else:
+        order = np.argsort(np.abs(sc.xyz[:, 0]), kind="stable")[:n_sample]
+        idx = np.sort(order)
+        xyz = np.ascontiguousarray(sc.xyz[idx])
+        emb = np.ascontiguousarray(sc.emb[idx])
+        what = (f"{n_sample} points of the {sc.name} tile nearest the x = 0 "
+                "plane (sensor slab)")
     oracle.build()
     t0 = time.perf_counter()
     nbr, _ = oracle.knn(xyz, sc.k)
@@ -59,9 +112,8 @@ def cpu_baseline(sc, n_sample):
     return {
         "value": n_sample / (t2 - t0), "unit": "points/s", "cores": 1,
         "kind": "oracle",
-        "sample": (f"{n_sample} points of the {sc.name} tile nearest the "
-                   f"x = 0 plane (sensor slab), k={sc.k}, ladder "
-                   f"{sc.lambdas}; kNN {t1 - t0:.2f} s, graph+ladder "
+        "sample": (f"{what}, k={sc.k}, ladder {list(sc.lambdas)}; one "
+                   f"thread; kNN {t1 - t0:.2f} s, graph+ladder "
                    f"{t2 - t1:.2f} s; host {platform.processor() or 'cpu'} "
                    f"with {os.cpu_count()} logical cores"),
     }
@@ -117,10 +169,11 @@ def main():
     achieved = per_launch_bytes / (per_launch_ms * 1e-3) / 1e9 \
         if per_launch_ms > 0 else 0.0
     alg_total = sum(v["bytes"] for v in stages.values()) / args.steps
+    traffic = measured_traffic(dom, sc.n, sc.k)
     roofline = {
         "bound": "hbm", "kernel": dom, "achieved": round(achieved, 2),
         "peak": HBM_PEAK_GBS, "unit": "GB/s",
-        "frac": round(achieved / HBM_PEAK_GBS, 5), "traffic": None,
+        "frac": round(achieved / HBM_PEAK_GBS, 5), "traffic": traffic,
         "launch_ms": round(per_launch_ms, 5),
         "alg_bytes_per_launch": per_launch_bytes,
         "step_alg_bytes": alg_total,
@@ -128,6 +181,14 @@ def main():
                                HBM_PEAK_GBS, 5),
     }
     split = {s: round(v["ms"] / args.steps, 4) for s, v in stages.items()}
+    if args.calib_copy:
+        # one plain elementwise copy, outside the timed region: the HBM
+        # counters of the profiled kernels are scaled by what they read for it
+        src = torch.ones(CALIB_ELEMS, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        torch.neg(src, out=dst)
+        torch.cuda.synchronize()
+        del src, dst
 
     out = {
         "metric": "points/sec partitioned (kNN+merge) on 3M-pt tile",

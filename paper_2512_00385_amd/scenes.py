@@ -96,7 +96,7 @@ def _finish(rng, name, pts, obj, d, sigma, k, lambdas, shuffle=True):
         pts, obj, emb = pts[perm], obj[perm], emb[perm]
     return Scene(name, np.ascontiguousarray(pts, dtype=np.float32),
                  np.ascontiguousarray(emb), obj.astype(np.int32), k,
-                 list(lambdas))
+                 [float(x) for x in lambdas])
 
 
 # --------------------------------------------------------------------------
@@ -385,7 +385,7 @@ def load(name: str, seed: int = 0, cache: bool = True) -> Scene:
     if cache and os.path.exists(path):
         z = np.load(path, allow_pickle=False)
         return Scene(name, z["xyz"], z["emb"], z["obj"], int(z["k"]),
-                     list(z["lambdas"]))
+                     [float(x) for x in z["lambdas"]])
     sc = SCENES[name](seed)
     if cache:
         os.makedirs(_cache_dir(), exist_ok=True)
