@@ -3,18 +3,21 @@
 //
 // Grid build: each point gets a 48-bit Morton key of its 16-bit-per-axis
 // voxel in the bounding box; a radix sort lays the points out in Morton
-// order.  Consecutive runs of 32 sorted points form buckets, and an implicit
+// order.  Consecutive runs of 16 sorted points form buckets, and an implicit
 // 8-ary tree of axis-aligned boxes sits over the buckets, so the voxel
 // hierarchy adapts to any density.
 //
-// Query: one wavefront per 64 consecutive sorted points.  Each lane keeps its
-// own sorted top-k of (d2, original index) in registers.  The wave scans its
-// own two buckets first, then walks the tree without a stack in Morton order
-// and enters a box whenever some lane's box distance does not exceed that
-// lane's current k-th distance; bucket points are broadcast lane to lane
-// with readlane.  The box distance is built from the same IEEE operations as
-// d2 and rounding is monotone, so it never exceeds the d2 of a point inside
-// the box: no neighbour, and no tie with a smaller index, can be skipped.
+// Query: one bucket per 16-lane DPP row (four buckets per wavefront), one
+// query point per lane.  Each lane keeps its own sorted top-k of 64-bit keys
+// (d2 bits, original index) in registers.  A group scans its own bucket and
+// the two next to it in Morton order first, then walks the tree depth first:
+// at each visited node the eight child boxes are loaded together and tested
+// against every lane's current k-th distance, and the children that some
+// lane needs are kept as bits of a per-level mask (the lowest set bit is the
+// next to enter).  Bucket points are broadcast within the row by DPP.  The
+// box distance is built from the same IEEE operations as d2 and rounding is
+// monotone, so it never exceeds the d2 of a point inside the box: no
+// neighbour, and no tie with a smaller index, can be skipped.
 #include "ezsp_internal.h"
 
 namespace ezsp {
