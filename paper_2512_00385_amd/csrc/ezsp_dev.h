@@ -23,12 +23,21 @@ enum : uint32_t {
 
 // Small block of device scalars, one per call, at the start of the
 // workspace.  The host reads it back once per merge round.
+// Counters that many blocks add to at once are spread over kStripes cache
+// lines: device-scope atomics on one address are serialised at the memory
+// side.  Only the host reads them (read_ctl folds the stripes).
+constexpr int kStripes = 32;
+struct alignas(128) Stripe {
+  int32_t v;
+  int32_t pad[31];
+};
+
 struct Ctl {
   uint32_t err;
   int32_t F;            // fixed-point shift of the embeddings
   int32_t any_choice;   // some node kept a merge edge this round
   int32_t n_next;       // components after this round
-  int32_t e_next;       // directed edges after this round
+  int32_t e_next;       // directed edges after this round (host: folded)
   int32_t slots;        // adjacency-table slots of the next round
   uint32_t maxabs_bits; // max |e| as fp32 bits (monotone for >= 0)
   int32_t n_long;       // nodes whose row goes to the block-per-row kernels
@@ -36,12 +45,22 @@ struct Ctl {
   int32_t n_big;        // components that go to the block-per-component path
   int32_t e_rev;        // reverse-only entries of the first-round graph
   int32_t e_fwd;        // valid forward entries of the first-round graph
+                        // (host: folded)
   int32_t n_cbig;       // components whose table window exceeds one chunk
   int32_t n_tiles;      // member tiles of those components
   int32_t tail_level;   // level that reached max_rounds in the tail kernel
   int64_t cut_w2;       // 2 * cut weight (directed sum) of the current graph
   double fid_total;     // fidelity term of the energy
+  Stripe e_next_s[kStripes];  // device side of e_next
+  Stripe e_fwd_s[kStripes];   // device side of e_fwd
 };
+
+__device__ __forceinline__ void stripe_add(Stripe *s, int32_t v) {
+  atomicAdd(&s[blockIdx.x % kStripes].v, v);
+}
+__device__ __forceinline__ void stripe_zero(Stripe *s) {
+  for (int i = threadIdx.x; i < kStripes; i += blockDim.x) s[i].v = 0;
+}
 
 // --- order-preserving float <-> int (for atomic min/max on floats) --------
 __device__ __forceinline__ int32_t f2ord(float f) {

@@ -28,6 +28,19 @@ __device__ __forceinline__ int32_t xcd_block() {
 __device__ __forceinline__ int32_t xcd_tid() {
   return xcd_block() * (int32_t)blockDim.x + (int32_t)threadIdx.x;
 }
+// Item of this thread when only m <= gridDim.x * blockDim.x items are live
+// (m known on the device only, grid sized by an upper bound): XCD x takes
+// the x-th contiguous eighth of [0, m), so every XCD gets work however small
+// m is.  Needs gridDim.x % kXcd == 0 (xcd_grid); then each XCD has
+// (gridDim.x / kXcd) * blockDim.x >= ceil(m / kXcd) threads.  Returns false
+// for threads without an item.
+__device__ __forceinline__ bool xcd_item(int32_t m, int32_t &c) {
+  const int32_t per = (m + kXcd - 1) / kXcd;
+  const int32_t j =
+      (int32_t)(blockIdx.x / kXcd) * (int32_t)blockDim.x + (int32_t)threadIdx.x;
+  c = (int32_t)(blockIdx.x % kXcd) * per + j;
+  return j < per && c < m;
+}
 
 // Row stride of the internal neighbour tables: k rounded up to a multiple
 // of 4 (16-byte rows for vector loads), padded with -1.

@@ -136,7 +136,7 @@ __global__ __launch_bounds__(256) void k_rev_count(const int32_t *nbr,
     }
   }
   fwd = wave_sum(fwd);
-  if ((threadIdx.x & (kWave - 1)) == 0 && fwd) atomicAdd(&ctl->e_fwd, fwd);
+  if ((threadIdx.x & (kWave - 1)) == 0 && fwd) stripe_add(ctl->e_fwd_s, fwd);
 }
 
 __global__ __launch_bounds__(256) void k_rev_fill(const int32_t *nbr,
@@ -273,6 +273,7 @@ __global__ void k_round_init(Ctl *ctl) {
     ctl->n_cbig = 0;
     ctl->n_tiles = 0;
   }
+  if (blockIdx.x == 0) stripe_zero(ctl->e_next_s);
 }
 
 // ---------------------------------------------------------------------------
@@ -624,8 +625,8 @@ __global__ __launch_bounds__(256) void k_stats(
     const int32_t *__restrict__ deg, int32_t d, NodeOut o,
     int32_t *__restrict__ big, Ctl *ctl) {
   if (!ctl->any_choice) return;
-  const int32_t c = xcd_tid();
-  if (c >= bound || c >= ctl->n_next) return;
+  int32_t c;
+  if (!xcd_item(min(bound, ctl->n_next), c)) return;
   const int32_t m0 = moff[c], m1 = moff[c + 1];
   if (m1 - m0 > o.big_members) {
     big[atomicAdd(&ctl->n_big, 1)] = c;
@@ -922,7 +923,7 @@ __global__ __launch_bounds__(256) void k_contract_chunk(
   }
   int32_t tot;
   block_excl_scan<256>(uniq, wsum, &tot);
-  if (threadIdx.x == 0 && tot) atomicAdd(&ctl->e_next, tot);
+  if (threadIdx.x == 0 && tot) stripe_add(ctl->e_next_s, tot);
 }
 
 // Global path for windows larger than a chunk: the window is cleared, then
@@ -1033,7 +1034,7 @@ __global__ __launch_bounds__(256) void k_contract_big(
   }
   added = wave_sum(added);
   if ((threadIdx.x & (kWave - 1)) == 0 && added)
-    atomicAdd(&ctl->e_next, added);
+    stripe_add(ctl->e_next_s, added);
 }
 
 // point -> current node map, composed every merging round

@@ -179,6 +179,10 @@ __global__ void k_ctl_init(Ctl *ctl) {
     ctl->cut_w2 = 0;
     ctl->fid_total = 0.0;
   }
+  if (blockIdx.x == 0) {
+    stripe_zero(ctl->e_next_s);
+    stripe_zero(ctl->e_fwd_s);
+  }
 }
 
 __global__ __launch_bounds__(256) void k_maxabs(const float *v, int64_t count,
@@ -362,6 +366,15 @@ int read_ctl(Ctl *ctl, Ctl *host, hipStream_t st) {
                  "hipMemcpyAsync(ctl)");
   if (rc) return rc;
   rc = check_hip(hipStreamSynchronize(st), "hipStreamSynchronize");
+  if (rc == 0) {
+    int64_t en = 0, ef = 0;
+    for (int i = 0; i < kStripes; ++i) {
+      en += host->e_next_s[i].v;
+      ef += host->e_fwd_s[i].v;
+    }
+    host->e_next = en > INT32_MAX ? -1 : (int32_t)en;
+    host->e_fwd = ef > INT32_MAX ? -1 : (int32_t)ef;
+  }
   prof_flush();
   return rc;
 }
