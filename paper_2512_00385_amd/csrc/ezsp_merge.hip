@@ -119,21 +119,30 @@ __device__ __forceinline__ bool row_has(const int32_t *nbr, int32_t kp,
   return hit;
 }
 
-// Reverse entries: i lists u, u does not list i -> u's row gets i.
+// Reverse entries: i lists u, u does not list i -> u's row gets i.  The
+// count pass keeps, per point, the bit mask of its entries that are not
+// mutual (k <= 64), so the fill pass does not look at the rows again.  All
+// row checks of a point are made before its atomics.
 __global__ __launch_bounds__(256) void k_rev_count(const int32_t *nbr,
                                                    int32_t n, int32_t k,
-                                                   int32_t *rev, Ctl *ctl) {
+                                                   int32_t *rev,
+                                                   uint64_t *nmask, Ctl *ctl) {
   const int32_t i = xcd_tid();
   const int32_t kp = pad4(k);
   int32_t fwd = 0;
   if (i < n) {
     const int32_t *r = nbr + (int64_t)i * kp;
+    uint64_t mask = 0;
+#pragma unroll 4
     for (int32_t t = 0; t < k; ++t) {
       const int32_t u = r[t];
       if (u < 0) continue;
       ++fwd;
-      if (!row_has(nbr, kp, u, i)) atomicAdd(&rev[u], 1);
+      if (!row_has(nbr, kp, u, i)) mask |= 1ull << t;
     }
+    nmask[i] = mask;
+    for (uint64_t m = mask; m; m &= m - 1)
+      atomicAdd(&rev[r[__builtin_ctzll(m)]], 1);
   }
   fwd = wave_sum(fwd);
   if ((threadIdx.x & (kWave - 1)) == 0 && fwd) stripe_add(ctl->e_fwd_s, fwd);
@@ -141,17 +150,16 @@ __global__ __launch_bounds__(256) void k_rev_count(const int32_t *nbr,
 
 __global__ __launch_bounds__(256) void k_rev_fill(const int32_t *nbr,
                                                   int32_t n, int32_t k,
+                                                  const uint64_t *nmask,
                                                   const int32_t *rrp,
                                                   int32_t *cursor,
                                                   int32_t *rcol,
                                                   int32_t *rown, Ctl *ctl) {
   const int32_t i = xcd_tid();
   if (i >= n) return;
-  const int32_t kp = pad4(k);
-  const int32_t *r = nbr + (int64_t)i * kp;
-  for (int32_t t = 0; t < k; ++t) {
-    const int32_t u = r[t];
-    if (u < 0 || row_has(nbr, kp, u, i)) continue;
+  const int32_t *r = nbr + (int64_t)i * pad4(k);
+  for (uint64_t m = nmask[i]; m; m &= m - 1) {
+    const int32_t u = r[__builtin_ctzll(m)];
     const int32_t pos = rrp[u] + atomicAdd(&cursor[u], 1);
     if (pos < rrp[u + 1]) {
       rcol[pos] = i;
@@ -257,6 +265,29 @@ __device__ __forceinline__ bool row_entry(const Adj &a, int32_t v, int32_t j,
     return u >= 0;
   }
   const uint64_t e = a.tbl[a.ws[v] + j];
+  u = (int32_t)(e >> 32);
+  w = (int32_t)(uint32_t)e;
+  return e != kEmpty;
+}
+
+// Row base of v for row_entry_at: the start of v's reverse list (first
+// round) or of its table window (later rounds).
+template <bool FIRST>
+__device__ __forceinline__ int32_t row_base(const Adj &a, int32_t v) {
+  return FIRST ? a.rrp[v] : a.ws[v];
+}
+
+// row_entry with v's row base already known.
+template <bool FIRST>
+__device__ __forceinline__ bool row_entry_at(const Adj &a, int32_t v,
+                                             int32_t base, int32_t j,
+                                             int32_t &u, int32_t &w) {
+  if (FIRST) {
+    u = (j < a.k) ? a.nbr[(int64_t)v * a.kp + j] : a.rcol[base + (j - a.k)];
+    w = 1;
+    return u >= 0;
+  }
+  const uint64_t e = a.tbl[base + j];
   u = (int32_t)(e >> 32);
   w = (int32_t)(uint32_t)e;
   return e != kEmpty;
@@ -788,17 +819,6 @@ __global__ __launch_bounds__(256) void k_stats_big(
 // edges inside a component are dropped), then writes each row compacted to
 // the start of its window.  Larger windows go through the global path.
 // ---------------------------------------------------------------------------
-__device__ __forceinline__ int32_t lower_bound_i32(const int32_t *a,
-                                                   int32_t n, int32_t x) {
-  int32_t lo = 0, hi = n;
-  while (lo < hi) {
-    const int32_t mid = (lo + hi) >> 1;
-    if (a[mid] < x) lo = mid + 1;
-    else hi = mid;
-  }
-  return lo;
-}
-
 // Loads a batch of members into LDS with the exclusive prefix of their row
 // spans (members of skipped components count 0); returns the entry total.
 template <bool FIRST, class Keep>
@@ -835,91 +855,149 @@ __device__ __forceinline__ void batch_find(const int32_t *pre, int32_t f,
   j = f - pre[lo];
 }
 
+// First component of every chunk of the next table: cstart[q] is the first
+// c with toff[c] >= q * chunk, for q = 0 .. ceil(slots / chunk).  Component
+// c takes the q with q * chunk in (toff[c - 1], toff[c]]; c = nc takes the
+// rest (toff[nc] = slots), so every q is written exactly once.
+__global__ __launch_bounds__(256) void k_chunk_starts(
+    int32_t bound, const int32_t *__restrict__ toff, int32_t chunk,
+    int32_t *__restrict__ cstart, int32_t qcap, Ctl *ctl) {
+  if (!ctl->any_choice) return;
+  const int32_t nc = ctl->n_next;
+  const int32_t c = blockIdx.x * blockDim.x + threadIdx.x;
+  if (c > nc || c > bound) return;
+  const int32_t lo = c == 0 ? 0 : toff[c - 1] / chunk + 1;
+  int32_t hi = c == nc ? (toff[nc] + chunk - 1) / chunk : toff[c] / chunk;
+  if (hi >= qcap) {
+    raise_err(ctl, kErrInternal);
+    hi = qcap - 1;
+  }
+  for (int32_t q = lo; q <= hi; ++q) cstart[q] = c;
+}
+
 template <bool FIRST>
 __global__ __launch_bounds__(256) void k_contract_chunk(
     int32_t nn, Adj a, const int32_t *__restrict__ L,
     const int32_t *__restrict__ mem, const int32_t *__restrict__ moff,
     const int32_t *__restrict__ toff, const int32_t *__restrict__ cap,
-    uint64_t *__restrict__ tbl, int32_t *__restrict__ wl, int32_t chunk,
-    Ctl *ctl) {
+    const int32_t *__restrict__ cstart, uint64_t *__restrict__ tbl,
+    int32_t *__restrict__ wl, int32_t chunk, Ctl *ctl) {
   __shared__ int32_t kb[2 * kChunk];
   __shared__ int32_t kw[2 * kChunk];
   __shared__ int32_t pre[kBatch + 1];
-  __shared__ int32_t bm[kBatch];
+  // members of the batch: node, component, window start in the chunk,
+  // window capacity, row base
+  __shared__ int32_t bm[kBatch], bA[kBatch], blb[kBatch], bcp[kBatch];
+  __shared__ int32_t bbase[kBatch];
   __shared__ int32_t wsum[256 / kWave];
-  __shared__ int32_t crange[2];
   if (!ctl->any_choice) return;
-  const int32_t nc = ctl->n_next;
-  const int32_t j0 = xcd_block() * chunk;
+  const int32_t q = xcd_block();
+  const int32_t j0 = q * chunk;
   if (j0 >= ctl->slots) return;
-  if (threadIdx.x == 0) {
-    crange[0] = lower_bound_i32(toff, nc, j0);
-    crange[1] = lower_bound_i32(toff, nc, j0 + chunk);
-  }
+  // components whose windows start in [j0, j0 + chunk)
+  const int32_t c_lo = cstart[q], c_hi = cstart[q + 1];
   for (int t = threadIdx.x; t < 2 * chunk; t += blockDim.x) {
     kb[t] = -1;
     kw[t] = 0;
   }
   __syncthreads();
-  const int32_t c_lo = crange[0], c_hi = crange[1];
   const int32_t m_lo = moff[c_lo];
   // a window larger than a chunk can only be the last one starting here
   // (the next window starts past the chunk); its members are not walked
   const int32_t m_hi =
       (c_hi > c_lo && cap[c_hi - 1] > chunk) ? moff[c_hi - 1] : moff[c_hi];
-  auto keep = [&](int32_t m) {
-    const int32_t c = cap[L[m]];
-    return c > 0 && c <= chunk;
-  };
+  constexpr int kUnroll = 4;  // entries per thread with their loads in flight
   for (int32_t b0 = m_lo; b0 < m_hi; b0 += kBatch) {
-    const int32_t total = load_batch<FIRST>(a, mem, b0, m_hi, pre, bm, wsum,
-                                            keep);
-    for (int32_t f = threadIdx.x; f < total; f += blockDim.x) {
-      int32_t slot, j, u, w;
-      batch_find(pre, f, slot, j);
-      const int32_t m = bm[slot];
-      if (!row_entry<FIRST>(a, m, j, u, w)) continue;
-      if ((uint32_t)u >= (uint32_t)nn) {
-        raise_err(ctl, kErrInternal);
-        continue;
-      }
-      const int32_t A = L[m], B = L[u];
-      if (A == B) continue;  // edge inside a merged component
-      const int32_t lb = toff[A] - j0, cp = cap[A];
-      if (lb < 0 || cp <= 0 || lb + cp > 2 * chunk) {
-        raise_err(ctl, kErrInternal);
-        continue;
-      }
-      uint32_t h = ((uint32_t)B * 2654435761u) % (uint32_t)cp;
-      int32_t probe = 0;
-      for (; probe < cp; ++probe) {
-        const int32_t old = atomicCAS(&kb[lb + h], -1, B);
-        if (old == -1 || old == B) {
-          atomicAdd(&kw[lb + h], w);
-          break;
+    const int32_t idx = b0 + (int32_t)threadIdx.x;
+    int32_t span = 0;
+    if (idx < m_hi) {
+      const int32_t m = mem[idx];
+      const int32_t A = L[m];
+      const int32_t cp = cap[A];
+      if (cp > 0 && cp <= chunk) {
+        const int32_t lb = toff[A] - j0;
+        if (lb < 0 || lb + cp > 2 * chunk) {
+          raise_err(ctl, kErrInternal);
+        } else {
+          span = row_span<FIRST>(a, m);
+          bm[threadIdx.x] = m;
+          bA[threadIdx.x] = A;
+          blb[threadIdx.x] = lb;
+          bcp[threadIdx.x] = cp;
+          bbase[threadIdx.x] = row_base<FIRST>(a, m);
         }
-        h = (h + 1 == (uint32_t)cp) ? 0u : h + 1;
       }
-      if (probe == cp) raise_err(ctl, kErrInternal);
+    }
+    int32_t total;
+    pre[threadIdx.x] = block_excl_scan<256>(span, wsum, &total);
+    if (threadIdx.x == 0) pre[kBatch] = total;
+    __syncthreads();
+    for (int32_t f0 = threadIdx.x; f0 < total; f0 += kUnroll * 256) {
+      int32_t slot[kUnroll], u[kUnroll], w[kUnroll], B[kUnroll];
+      bool ok[kUnroll];
+#pragma unroll
+      for (int e = 0; e < kUnroll; ++e) {
+        const int32_t f = f0 + e * 256;
+        ok[e] = false;
+        if (f < total) {
+          int32_t j;
+          batch_find(pre, f, slot[e], j);
+          ok[e] = row_entry_at<FIRST>(a, bm[slot[e]], bbase[slot[e]], j, u[e],
+                                      w[e]);
+        }
+      }
+#pragma unroll
+      for (int e = 0; e < kUnroll; ++e) {
+        if (ok[e] && (uint32_t)u[e] >= (uint32_t)nn) {
+          raise_err(ctl, kErrInternal);
+          ok[e] = false;
+        }
+        B[e] = ok[e] ? L[u[e]] : -1;
+      }
+#pragma unroll
+      for (int e = 0; e < kUnroll; ++e) {
+        const int32_t A = ok[e] ? bA[slot[e]] : -1;
+        if (!ok[e] || A == B[e]) continue;  // edge inside a merged component
+        const int32_t lb = blb[slot[e]], cp = bcp[slot[e]];
+        uint32_t h = ((uint32_t)B[e] * 2654435761u) % (uint32_t)cp;
+        int32_t probe = 0;
+        for (; probe < cp; ++probe) {
+          const int32_t old = atomicCAS(&kb[lb + h], -1, B[e]);
+          if (old == -1 || old == B[e]) {
+            atomicAdd(&kw[lb + h], w[e]);
+            break;
+          }
+          h = (h + 1 == (uint32_t)cp) ? 0u : h + 1;
+        }
+        if (probe == cp) raise_err(ctl, kErrInternal);
+      }
     }
     __syncthreads();
   }
-  // rows compacted to the start of their windows
+  // rows compacted to the start of their windows, a wave per window:
+  // occupied slots ranked by ballot, written in slot order
+  const int lane = threadIdx.x & (kWave - 1);
+  const uint64_t below = (1ull << lane) - 1;
   int32_t uniq = 0;
-  for (int32_t c = c_lo + (int32_t)threadIdx.x; c < c_hi; c += blockDim.x) {
+  for (int32_t c = c_lo + (int32_t)threadIdx.x / kWave; c < c_hi;
+       c += blockDim.x / kWave) {
     const int32_t cp = cap[c];
     if (cp <= 0 || cp > chunk) continue;
     const int32_t base = toff[c], lb = base - j0;
     int32_t out = 0;
-    for (int32_t t = lb; t < lb + cp; ++t) {
-      const int32_t B = kb[t];
-      if (B >= 0) {
-        tbl[base + out] = ((uint64_t)(uint32_t)B << 32) | (uint32_t)kw[t];
-        ++out;
-      }
+    for (int32_t t0 = 0; t0 < cp; t0 += kWave) {
+      const int32_t t = t0 + lane;
+      const int32_t B = t < cp ? kb[lb + t] : -1;
+      const uint64_t occ = __ballot(B >= 0);
+      if (B >= 0)
+        tbl[base + out + __popcll(occ & below)] =
+            ((uint64_t)(uint32_t)B << 32) | (uint32_t)kw[lb + t];
+      out += __popcll(occ);
     }
-    wl[c] = out;
-    uniq += out;
+    if (lane == 0) {
+      wl[c] = out;
+      uniq += out;
+    }
   }
   int32_t tot;
   block_excl_scan<256>(uniq, wsum, &tot);
@@ -1551,6 +1629,7 @@ struct Bufs {
   float *emb_int;
   int32_t *nbr_clean;                   // sanitised caller table
   int32_t *rrp, *rcol, *rown, *rev, *cursor;  // first-round reverse list
+  uint64_t *nmask;                      // non-mutual entries of each row
   int32_t *ws[2], *wl[2];               // row windows (= toff, cap)
   uint64_t *tbl[2];
   int32_t *size[2], *minpt[2];
@@ -1558,6 +1637,8 @@ struct Bufs {
   double *mu;
   int32_t *target, *deg, *parent, *newid, *L, *cnt, *rank, *moff, *mem;
   int32_t *long_rows, *big, *cbig, *capn, *tile_c, *tile_i;
+  int32_t *cstart;  // first component of every contraction chunk
+  int32_t qcap;     // entries of cstart
   int32_t *M, *mark, *lrank;
   int32_t nt;  // nodes the tail can start from
   int32_t *Mt, *lvl_map, *lvl_minpt, *lvl_nc;
@@ -1579,6 +1660,7 @@ void carve(Arena &a, int32_t n, int32_t d, int32_t k, Bufs *b) {
   b->rown = a.take<int32_t>((size_t)n * k);
   b->rev = a.take<int32_t>(n1);
   b->cursor = a.take<int32_t>(n1);
+  b->nmask = a.take<uint64_t>(n1);
   for (int j = 0; j < 2; ++j) {
     b->ws[j] = a.take<int32_t>(n1);
     b->wl[j] = a.take<int32_t>(n1);
@@ -1603,6 +1685,8 @@ void carve(Arena &a, int32_t n, int32_t d, int32_t k, Bufs *b) {
   b->capn = a.take<int32_t>(n1);
   b->tile_c = a.take<int32_t>(2 * n1);
   b->tile_i = a.take<int32_t>(2 * n1);
+  b->qcap = (int32_t)(ed / 64 + 16);  // chunks are >= 64 slots
+  b->cstart = a.take<int32_t>(b->qcap);
   b->M = a.take<int32_t>(n1);
   b->mark = a.take<int32_t>(n1);
   b->lrank = a.take<int32_t>(n1);
@@ -1702,10 +1786,12 @@ void launch_round(const Bufs &b, const Adj &adj, int cur, int32_t n,
   prof_begin("contract", st);
   device_scan(ScanArray{b.capn, b.ws[nxt], nn, &ctl->n_next}, nn + 1, b.bsum,
               &ctl->slots, st);
+  hipLaunchKernelGGL(k_chunk_starts, blocks_for((int64_t)nn + 1), dim3(256), 0,
+                     st, nn, b.ws[nxt], chunk, b.cstart, b.qcap, ctl);
   hipLaunchKernelGGL(k_contract_chunk<FIRST>,
                      dim3(xcd_grid((ed + chunk - 1) / chunk)), dim3(256), 0,
                      st, nn, adj, b.L, b.mem, b.moff, b.ws[nxt], b.capn,
-                     b.tbl[nxt], b.wl[nxt], chunk, ctl);
+                     b.cstart, b.tbl[nxt], b.wl[nxt], chunk, ctl);
   hipLaunchKernelGGL(k_clear_big, big_grid, dim3(256), 0, st, b.cbig,
                      b.ws[nxt], b.capn, b.tbl[nxt], tcap, ctl);
   hipLaunchKernelGGL(k_contract_big<FIRST>, big_grid, dim3(256), 0, st, nn,
@@ -1906,11 +1992,11 @@ int ladder_run(const LadderArgs &g, Ctl *ctl, Arena &a, hipStream_t st) {
   hipLaunchKernelGGL(k_fill_i32, blocks_for(n), dim3(256), 0, st, b.cursor,
                      (int64_t)n, 0);
   hipLaunchKernelGGL(k_rev_count, xblocks_for(n), dim3(256), 0, st, nbr, n, k,
-                     b.rev, ctl);
+                     b.rev, b.nmask, ctl);
   device_scan(ScanArray{b.rev, b.rrp, n, nullptr}, n + 1, b.bsum, &ctl->e_rev,
               st);
   hipLaunchKernelGGL(k_rev_fill, xblocks_for(n), dim3(256), 0, st, nbr, n, k,
-                     b.rrp, b.cursor, b.rcol, b.rown, ctl);
+                     b.nmask, b.rrp, b.cursor, b.rcol, b.rown, ctl);
   prof_end(st);
   if ((rc = read_ctl(ctl, h, st))) return rc;
   if (h->err) return status_from_err(h->err);
