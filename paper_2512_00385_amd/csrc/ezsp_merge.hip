@@ -1256,25 +1256,33 @@ __global__ void k_energy_reset(Ctl *ctl) {
 
 // ---------------------------------------------------------------------------
 // Tail: once the graph is small, every remaining round of every remaining
-// level runs inside one block of 1024 threads (16 waves), with barriers
-// between the steps instead of kernel launches and host round trips.  The
-// steps are the same as above, with a thread per row or component since
-// rows are short by then: Steps 1-2, hook, pointer jumping, relabel by a
-// block scan, members, the statistics, and the contraction into the next
-// table (global atomics, rows keep their empty slots).  The point -> node map is not
-// touched: the tail keeps Mt (tail-start node -> current node) and leaves,
-// for each level it ends, a snapshot of Mt, the smallest point of every
-// node and (for the energy) the means and the cut weight.
+// level runs inside one block of 1024 threads, with barriers between the
+// steps instead of kernel launches and host round trips.  The arithmetic is
+// the same as above; the work is spread over table slots (entries) rather
+// than rows, and the per-node arrays live in LDS:
+//   select    three passes over the slots: gain of every entry, then per
+//             row the largest gain (max of an order-preserving key), the
+//             smallest minpt among the entries with that gain, and the
+//             entry that has both (Steps 1-2, same choice as best_before)
+//   union     hook and pointer jumping on LDS arrays (Step 3)
+//   relabel   roots numbered by a block scan
+//   stats     node-parallel adds into the next node state (int64 sums,
+//             size, smallest point, summed degree) with workgroup-scope
+//             atomics, then the means (Step 4)
+//   contract  every entry relabelled and added into its component's window
+//             of the next table (windows keep their empty slots)
+// The point -> node map is not touched: the tail keeps Mt (tail-start node
+// -> current node) and leaves, for each level it ends, a snapshot of Mt, the
+// smallest point of every node and (for the energy) the means and the cut
+// weight.
 // ---------------------------------------------------------------------------
 constexpr int kTailNT = 1024;
-constexpr int kTailWaves = kTailNT / kWave;
-constexpr int kTailNodes = 16384;   // largest graph the tail can take
+constexpr int kTailNodes = 1536;    // largest graph the tail can take (LDS)
 constexpr int kTailStart = 1500;    // default switch to the tail
-constexpr int kTailEdges = 1 << 18; // ... and this many directed entries
+constexpr int kTailEdges = 1 << 16; // ... directed entries at the switch
+constexpr int kTailSlots = 1 << 18; // ... table slots at the switch
 constexpr int kTailLevels = 16;
 constexpr int kTailJumps = 64;
-constexpr int kTailShort = 32;  // longer rows (slots) / components (members)
-                                // go to a wave each, lanes over the entries
 
 struct TailState {
   int32_t *ws[2], *wl[2];
@@ -1282,16 +1290,54 @@ struct TailState {
   int32_t *size[2], *minpt[2];
   int64_t *S[2];
   double *mu;
-  int32_t *target, *deg, *parent, *newid, *L, *cnt, *moff, *mem, *capn, *Mt;
-  int32_t *longrow, *longcomp;             // nn0 each
+  double *gain;                            // one per slot
+  int32_t *Mt;
   int32_t *lvl_map, *lvl_minpt, *lvl_nc;  // kTailLevels x nn0 (nc: levels)
   double *lvl_mu;                          // kTailLevels x nn0 x d
   long long *lvl_cut2;                     // kTailLevels
-  int32_t nn0, ed0, cur0, d, tcap, n_levels, level0, round0, max_rounds;
+  int32_t nn0, ed0, cur0, d, tcap, gcap, n_levels, level0, round0,
+      max_rounds;
   int32_t want_energy;
   double lambda[kTailLevels];
   long long smin[kTailLevels];
 };
+
+// The tail is one block, so its global read-modify-writes only need
+// workgroup scope: they are performed in this XCD's L2 instead of going out
+// to memory as device-scope atomics do.  Kernel end still publishes them.
+__device__ __forceinline__ void wg_add(int32_t *p, int32_t v) {
+  __hip_atomic_fetch_add(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+}
+__device__ __forceinline__ void wg_add64(int64_t *p, int64_t v) {
+  __hip_atomic_fetch_add(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+}
+__device__ __forceinline__ void wg_min(int32_t *p, int32_t v) {
+  __hip_atomic_fetch_min(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+}
+
+// table_add for the tail (same probing, workgroup-scope atomics).
+__device__ __forceinline__ bool tail_table_add(uint64_t *tbl, int32_t base,
+                                               int32_t cap, int32_t B,
+                                               int32_t w, Ctl *ctl) {
+  uint32_t h = ((uint32_t)B * 2654435761u) % (uint32_t)cap;
+  const uint64_t mine = ((uint64_t)(uint32_t)B << 32) | (uint32_t)w;
+  for (int32_t probe = 0; probe < cap; ++probe) {
+    uint64_t *slot = tbl + base + h;
+    uint64_t cur = kEmpty;
+    if (__hip_atomic_compare_exchange_strong(slot, &cur, mine,
+                                             __ATOMIC_RELAXED, __ATOMIC_RELAXED,
+                                             __HIP_MEMORY_SCOPE_WORKGROUP))
+      return true;
+    if ((int32_t)(cur >> 32) == B) {
+      __hip_atomic_fetch_add(slot, (uint64_t)(uint32_t)w, __ATOMIC_RELAXED,
+                             __HIP_MEMORY_SCOPE_WORKGROUP);
+      return false;
+    }
+    h = (h + 1 == (uint32_t)cap) ? 0u : h + 1;
+  }
+  raise_err(ctl, kErrInternal);
+  return false;
+}
 
 // Exclusive scan of value(0..len) into out[0..len], out[len] = total.
 template <class V>
@@ -1317,23 +1363,64 @@ __device__ __forceinline__ int32_t tail_scan(int32_t len, V &&value,
   return tot;
 }
 
+// Row of slot q: the last v < nn with ws[v] <= q (ws ascending, ws[nn] = Q).
+__device__ __forceinline__ int32_t tail_row(const int32_t *ws, int32_t nn,
+                                            int32_t q) {
+  int32_t lo = 0, hi = nn;
+  while (hi - lo > 1) {
+    const int32_t mid = (lo + hi) >> 1;
+    if (ws[mid] <= q) lo = mid;
+    else hi = mid;
+  }
+  return lo;
+}
+
+// Order-preserving key of a finite double; 0 is below every key.
+__device__ __forceinline__ unsigned long long gain_key(double g) {
+  const unsigned long long b = (unsigned long long)__double_as_longlong(g);
+  return (b >> 63) ? ~b : (b | (1ull << 63));
+}
+
 template <int DT>
 __global__ __launch_bounds__(kTailNT) void k_tail(TailState t, Ctl *ctl) {
-  __shared__ int32_t wsum[kTailWaves];
-  __shared__ int32_t s_any, s_flag, s_claims, s_nlong, s_nlongc;
+  __shared__ int32_t s_size[kTailNodes], s_minpt[kTailNodes];
+  __shared__ int32_t s_deg[kTailNodes], s_L[kTailNodes];
+  __shared__ int32_t s_sel[kTailNodes];
+  __shared__ int32_t s_wsa[kTailNodes + 1], s_wsb[kTailNodes + 1];
+  __shared__ unsigned long long s_key[kTailNodes + 1];
+  __shared__ int32_t wsum[kTailNT / kWave];
+  __shared__ int32_t s_any, s_flag, s_claims;
   __shared__ long long s_cut;
   const int lane = threadIdx.x & (kWave - 1);
-  const int wave = threadIdx.x / kWave;
   const int32_t d = t.d;
   const double sF = ldexp(1.0, ctl->F), sIF = ldexp(1.0, -ctl->F);
+  // s_key doubles as int32 scratch once the choices are made
+  int32_t *s_aux = reinterpret_cast<int32_t *>(s_key);  // 2 kTailNodes + 2
+  int32_t *s_newid = s_aux, *s_cap = s_aux + kTailNodes + 1;
+  int32_t *s_ws = s_wsa, *s_wn = s_wsb;  // current / next row starts
   int32_t nn = t.nn0, ed = t.ed0, cur = t.cur0;
-  for (int32_t i = threadIdx.x; i < t.nn0; i += kTailNT) t.Mt[i] = i;
+  if (nn > kTailNodes || nn < 1) {
+    if (threadIdx.x == 0) raise_err(ctl, kErrInternal);
+    return;
+  }
+  for (int32_t i = threadIdx.x; i <= nn; i += kTailNT) {
+    s_ws[i] = t.ws[cur][i];
+    if (i < nn) t.Mt[i] = i;
+  }
+  __syncthreads();
+  int32_t Q = s_ws[nn];  // slots of the current table
+  // rows of the incoming table may end before their window does: clear the
+  // rest so that every slot is either an entry or empty
+  for (int32_t q = threadIdx.x; q < Q; q += kTailNT) {
+    const int32_t v = tail_row(s_ws, nn, q);
+    if (q - s_ws[v] >= t.wl[cur][v]) t.tbl[cur][q] = kEmpty;
+  }
   __syncthreads();
   for (int32_t l = t.level0; l < t.n_levels; ++l) {
     const double lambda = t.lambda[l];
     const long long smin = t.smin[l];
     for (int32_t round = (l == t.level0 ? t.round0 : 0);; ++round) {
-      if (ed == 0) break;
+      if (ed == 0) break;  // no edge left: nothing can merge
       if (round >= t.max_rounds) {
         if (threadIdx.x == 0) {
           ctl->tail_level = l;
@@ -1342,10 +1429,7 @@ __global__ __launch_bounds__(kTailNT) void k_tail(TailState t, Ctl *ctl) {
         return;
       }
       const int nxt = 1 - cur;
-      Adj a;
-      a.ws = t.ws[cur];
-      a.wl = t.wl[cur];
-      a.tbl = t.tbl[cur];
+      const uint64_t *tb = t.tbl[cur];
       NodeIn s;
       s.size = t.size[cur];
       s.S = t.S[cur];
@@ -1353,102 +1437,81 @@ __global__ __launch_bounds__(kTailNT) void k_tail(TailState t, Ctl *ctl) {
       s.minpt = t.minpt[cur];
       s.emb = nullptr;
       s.perm = nullptr;
-      // Steps 1-2: a thread per short row, long rows listed for a wave each
-      if (threadIdx.x == 0) {
-        s_any = 0;
-        s_nlong = 0;
+      if (threadIdx.x == 0) s_any = 0;
+      for (int32_t v = threadIdx.x; v < nn; v += kTailNT) {
+        s_size[v] = s.size[v];
+        s_minpt[v] = s.minpt[v];
+        s_deg[v] = 0;
+        s_key[v] = 0ull;
+        s_sel[v] = INT32_MAX;
+        s_L[v] = -1;
       }
       __syncthreads();
-      for (int32_t v = threadIdx.x; v < nn; v += kTailNT) {
-        if (a.wl[v] > kTailShort) {
-          t.longrow[atomicAdd(&s_nlong, 1)] = v;
+      // Steps 1-2, pass 1: gains, degrees, largest candidate gain per row
+      for (int32_t q = threadIdx.x; q < Q; q += kTailNT) {
+        const uint64_t e = tb[q];
+        if (e == kEmpty) continue;
+        const int32_t v = tail_row(s_ws, nn, q);
+        const int32_t u = (int32_t)(e >> 32), w = (int32_t)(uint32_t)e;
+        if ((uint32_t)u >= (uint32_t)nn) {
+          raise_err(ctl, kErrInternal);
           continue;
         }
-        const double dsv = (double)s.size[v];
-        const bool small = (long long)s.size[v] < smin;
-        MeanRow<false, DT> mv;
-        mv.load(s, v, sF, sIF);
-        Best b{0.0, 0, -1};
-        int32_t cnt = 0;
-        for_row<false>(a, v, 0, 1, [&](int32_t u, int32_t w) {
-          ++cnt;
-          if ((uint32_t)u >= (uint32_t)nn) {
-            raise_err(ctl, kErrInternal);
-            return;
-          }
-          const double g =
-              edge_gain_t<false, DT>(s, mv, v, dsv, u, w, d, lambda, sF, sIF);
-          if (g > 0.0 || small) {
-            const Best c{g, s.minpt[u], u};
-            if (best_before(c, b)) b = c;
-          }
-        });
-        t.target[v] = b.u;
-        t.deg[v] = cnt;
-        if (b.u >= 0) s_any = 1;
+        atomicAdd(&s_deg[v], 1);
+        double g;
+        if constexpr (DT > 0) {
+          MeanRow<false, DT> mv;
+          mv.load(s, v, sF, sIF);
+          g = edge_gain_t<false, DT>(s, mv, v, (double)s_size[v], u, w, d,
+                                     lambda, sF, sIF);
+        } else {
+          g = edge_gain<false>(s, v, (double)s_size[v], u, w, d, lambda, sF,
+                               sIF);
+        }
+        t.gain[q] = g;
+        if (g > 0.0 || (long long)s_size[v] < smin)
+          atomicMax(&s_key[v], gain_key(g));
       }
       __syncthreads();
-      const int32_t nlong = s_nlong;
-      for (int32_t j = wave; j < nlong; j += kTailWaves) {
-        const int32_t v = t.longrow[j];
-        const double dsv = (double)s.size[v];
-        const bool small = (long long)s.size[v] < smin;
-        MeanRow<false, DT> mv;
-        mv.load(s, v, sF, sIF);
-        Best b{0.0, 0, -1};
-        int32_t cnt = 0;
-        for_row<false>(a, v, lane, kWave, [&](int32_t u, int32_t w) {
-          ++cnt;
-          if ((uint32_t)u >= (uint32_t)nn) {
-            raise_err(ctl, kErrInternal);
-            return;
-          }
-          const double g =
-              edge_gain_t<false, DT>(s, mv, v, dsv, u, w, d, lambda, sF, sIF);
-          if (g > 0.0 || small) {
-            const Best c{g, s.minpt[u], u};
-            if (best_before(c, b)) b = c;
-          }
-        });
-        cnt = wave_sum(cnt);
-#pragma unroll
-        for (int off = kWave / 2; off > 0; off >>= 1) {
-          Best o;
-          o.g = __shfl_xor(b.g, off, kWave);
-          o.mp = __shfl_xor(b.mp, off, kWave);
-          o.u = __shfl_xor(b.u, off, kWave);
-          if (best_before(o, b)) b = o;
-        }
-        if (lane == 0) {
-          t.target[v] = b.u;
-          t.deg[v] = cnt;
-          if (b.u >= 0) s_any = 1;
+      // pass 2: smallest minpt among the entries with the row's best gain
+      for (int32_t q = threadIdx.x; q < Q; q += kTailNT) {
+        const uint64_t e = tb[q];
+        if (e == kEmpty) continue;
+        const int32_t v = tail_row(s_ws, nn, q);
+        const unsigned long long kv = s_key[v];
+        if (kv != 0ull && gain_key(t.gain[q]) == kv)
+          atomicMin(&s_sel[v], s_minpt[(int32_t)(e >> 32)]);
+      }
+      __syncthreads();
+      // pass 3: the chosen neighbour (minpt is unique per node)
+      for (int32_t q = threadIdx.x; q < Q; q += kTailNT) {
+        const uint64_t e = tb[q];
+        if (e == kEmpty) continue;
+        const int32_t v = tail_row(s_ws, nn, q);
+        const int32_t u = (int32_t)(e >> 32);
+        const unsigned long long kv = s_key[v];
+        if (kv != 0ull && s_minpt[u] == s_sel[v] &&
+            gain_key(t.gain[q]) == kv) {
+          s_L[v] = u;  // target
+          s_any = 1;
         }
       }
       __syncthreads();
       if (!s_any) break;  // Step 1: no candidate merge
-      // Step 3: hook, jump
+      // Step 3: hook (s_sel = parent), pointer jumping
       for (int32_t v = threadIdx.x; v < nn; v += kTailNT) {
-        const int32_t tg = t.target[v];
-        int32_t p = v;
-        if (tg >= 0) {
-          if (tg >= nn) {
-            raise_err(ctl, kErrInternal);
-          } else {
-            p = (t.target[tg] == v && v < tg) ? v : tg;
-          }
-        }
-        t.parent[v] = p;
+        const int32_t tg = s_L[v];
+        s_sel[v] = tg < 0 ? v : ((s_L[tg] == v && v < tg) ? v : tg);
       }
       __syncthreads();
       for (int pass = 0;; ++pass) {
         if (threadIdx.x == 0) s_flag = 0;
         __syncthreads();
         for (int32_t v = threadIdx.x; v < nn; v += kTailNT) {
-          const int32_t p = t.parent[v];
-          const int32_t pp = t.parent[p];
+          const int32_t p = s_sel[v];
+          const int32_t pp = s_sel[p];
           if (pp != p) {
-            t.parent[v] = pp;
+            s_sel[v] = pp;
             s_flag = 1;
           }
         }
@@ -1461,93 +1524,46 @@ __global__ __launch_bounds__(kTailNT) void k_tail(TailState t, Ctl *ctl) {
           return;
         }
       }
-      // relabel: roots numbered in node order
-      int32_t *par = t.parent;
+      // relabel: roots numbered in node order; L = new id of the root
       const int32_t C = tail_scan(
-          nn, [&](int32_t v) { return par[v] == v ? 1 : 0; }, t.newid, wsum);
-      for (int32_t c = threadIdx.x; c < C; c += kTailNT) t.cnt[c] = 0;
-      __syncthreads();
-      for (int32_t v = threadIdx.x; v < nn; v += kTailNT) {
-        const int32_t c = t.newid[t.parent[v]];
-        t.L[v] = c;
-        t.target[v] = atomicAdd(&t.cnt[c], 1);  // place among members
-      }
-      __syncthreads();
-      int32_t *cnt = t.cnt;
-      tail_scan(C, [&](int32_t c) { return cnt[c]; }, t.moff, wsum);
-      for (int32_t v = threadIdx.x; v < nn; v += kTailNT)
-        t.mem[t.moff[t.L[v]] + t.target[v]] = v;
-      __syncthreads();
-      // Step 4 statistics: a thread per small component, big ones listed
-      // for a wave each
-      if (threadIdx.x == 0) s_nlongc = 0;
-      __syncthreads();
+          nn, [&](int32_t v) { return s_sel[v] == v ? 1 : 0; }, s_newid,
+          wsum);
       for (int32_t c = threadIdx.x; c < C; c += kTailNT) {
-        const int32_t m0 = t.moff[c], m1 = t.moff[c + 1];
-        if (m1 - m0 > kTailShort) {
-          t.longcomp[atomicAdd(&s_nlongc, 1)] = c;
-          continue;
-        }
-        int32_t size = 0, mp = INT32_MAX, cap = 0;
-        for (int32_t j = m0; j < m1; ++j) {
-          const int32_t m = t.mem[j];
-          size += s.size[m];
-          mp = min(mp, s.minpt[m]);
-          cap += t.deg[m];
-        }
-        t.size[nxt][c] = size;
-        t.minpt[nxt][c] = mp;
-        t.capn[c] = cap;
-        t.wl[nxt][c] = cap;
-        for (int32_t i = 0; i < d; ++i) {
-          long long acc = 0;
-          for (int32_t j = m0; j < m1; ++j)
-            acc += s.S[(int64_t)t.mem[j] * d + i];
-          t.S[nxt][(int64_t)c * d + i] = acc;
-          const double q = (double)acc / (double)size;
-          t.mu[(int64_t)c * d + i] = q * sIF;
-        }
+        s_cap[c] = 0;
+        t.size[nxt][c] = 0;
+        t.minpt[nxt][c] = INT32_MAX;
+      }
+      for (int32_t q = threadIdx.x; q < C * d; q += kTailNT) t.S[nxt][q] = 0;
+      for (int32_t v = threadIdx.x; v < nn; v += kTailNT)
+        s_L[v] = s_newid[s_sel[v]];
+      __syncthreads();
+      // Step 4 statistics: every node adds itself to its component, the
+      // sums one (node, dimension) pair per thread so that loads coalesce.
+      // A window gets twice its summed degree when the table has room
+      // (ed entries in all): open addressing at load factor <= 1/2 keeps
+      // the probe chains short.
+      const int32_t spread =
+          2 * (int64_t)ed <= (int64_t)min(t.tcap, t.gcap) ? 2 : 1;
+      for (int32_t v = threadIdx.x; v < nn; v += kTailNT) {
+        const int32_t c = s_L[v];
+        wg_add(&t.size[nxt][c], s_size[v]);
+        wg_min(&t.minpt[nxt][c], s_minpt[v]);
+        atomicAdd(&s_cap[c], spread * s_deg[v]);
+      }
+      for (int32_t q = threadIdx.x; q < nn * d; q += kTailNT) {
+        const int32_t v = q / d;
+        wg_add64(&t.S[nxt][(int64_t)s_L[v] * d + (q - v * d)], s.S[q]);
       }
       __syncthreads();
-      const int32_t nlongc = s_nlongc;
-      for (int32_t j = wave; j < nlongc; j += kTailWaves) {
-        const int32_t c = t.longcomp[j];
-        const int32_t m0 = t.moff[c], m1 = t.moff[c + 1];
-        int32_t size = 0, mp = INT32_MAX, cap = 0;
-        for (int32_t q = m0 + lane; q < m1; q += kWave) {
-          const int32_t m = t.mem[q];
-          size += s.size[m];
-          mp = min(mp, s.minpt[m]);
-          cap += t.deg[m];
-        }
-        size = wave_sum(size);
-        cap = wave_sum(cap);
-#pragma unroll
-        for (int off = kWave / 2; off > 0; off >>= 1)
-          mp = min(mp, __shfl_xor(mp, off, kWave));
-        if (lane == 0) {
-          t.size[nxt][c] = size;
-          t.minpt[nxt][c] = mp;
-          t.capn[c] = cap;
-          t.wl[nxt][c] = cap;
-        }
-        for (int32_t i = 0; i < d; ++i) {
-          long long acc = 0;
-          for (int32_t q = m0 + lane; q < m1; q += kWave)
-            acc += s.S[(int64_t)t.mem[q] * d + i];
-          acc = wave_sum(acc);
-          if (lane == 0) {
-            t.S[nxt][(int64_t)c * d + i] = acc;
-            const double q = (double)acc / (double)size;
-            t.mu[(int64_t)c * d + i] = q * sIF;
-          }
-        }
+      for (int32_t q = threadIdx.x; q < C * d; q += kTailNT) {
+        const int32_t c = q / d;
+        const double m = (double)t.S[nxt][q] / (double)t.size[nxt][c];
+        t.mu[q] = m * sIF;
       }
-      __syncthreads();
-      int32_t *capn = t.capn;
+      // next table: windows of summed degree, cleared
       const int32_t slots =
-          tail_scan(C, [&](int32_t c) { return capn[c]; }, t.ws[nxt], wsum);
-      if (slots > t.tcap) {
+          tail_scan(C, [&](int32_t c) { return s_cap[c]; }, s_wn, wsum);
+      if (slots > t.tcap || slots > t.gcap) {
         if (threadIdx.x == 0) raise_err(ctl, kErrInternal);
         return;
       }
@@ -1555,37 +1571,31 @@ __global__ __launch_bounds__(kTailNT) void k_tail(TailState t, Ctl *ctl) {
         t.tbl[nxt][q] = kEmpty;
       if (threadIdx.x == 0) s_claims = 0;
       __syncthreads();
-      // Step 4 contraction: a thread per short row, a wave per long row
+      // Step 4 contraction, a thread per entry
       int32_t claims = 0;
-      auto add_row = [&](int32_t v, int32_t begin, int32_t step) {
-        const int32_t A = t.L[v];
-        const int32_t base = t.ws[nxt][A], cp = t.capn[A];
-        for_row<false>(a, v, begin, step, [&](int32_t u, int32_t w) {
-          if ((uint32_t)u >= (uint32_t)nn) {
-            raise_err(ctl, kErrInternal);
-            return;
-          }
-          const int32_t B = t.L[u];
-          if (B == A) return;
-          if (cp <= 0 || base + cp > slots) {
-            raise_err(ctl, kErrInternal);
-            return;
-          }
-          claims += table_add(t.tbl[nxt], base, cp, B, w, ctl) ? 1 : 0;
-        });
-      };
-      for (int32_t v = threadIdx.x; v < nn; v += kTailNT)
-        if (a.wl[v] <= kTailShort) add_row(v, 0, 1);
-      for (int32_t j = wave; j < nlong; j += kTailWaves)
-        add_row(t.longrow[j], lane, kWave);
+      for (int32_t q = threadIdx.x; q < Q; q += kTailNT) {
+        const uint64_t e = tb[q];
+        if (e == kEmpty) continue;
+        const int32_t v = tail_row(s_ws, nn, q);
+        const int32_t A = s_L[v], B = s_L[(int32_t)(e >> 32)];
+        if (A == B) continue;  // edge inside a merged component
+        claims += tail_table_add(t.tbl[nxt], s_wn[A], s_cap[A], B,
+                                 (int32_t)(uint32_t)e, ctl)
+                      ? 1
+                      : 0;
+      }
       claims = wave_sum(claims);
       if (lane == 0 && claims) atomicAdd(&s_claims, claims);
       for (int32_t i = threadIdx.x; i < t.nn0; i += kTailNT)
-        t.Mt[i] = t.L[t.Mt[i]];
+        t.Mt[i] = s_L[t.Mt[i]];
       __syncthreads();
-      nn = C;
       ed = s_claims;
+      nn = C;
+      Q = slots;
       cur = nxt;
+      int32_t *sw = s_ws;
+      s_ws = s_wn;
+      s_wn = sw;
       __syncthreads();
       if (nn == 1) break;  // a single component is left
     }
@@ -1602,13 +1612,11 @@ __global__ __launch_bounds__(kTailNT) void k_tail(TailState t, Ctl *ctl) {
     if (t.want_energy) {
       for (int64_t q = threadIdx.x; q < (int64_t)nn * d; q += kTailNT)
         t.lvl_mu[(int64_t)l * t.nn0 * d + q] = t.mu[q];
-      Adj a;
-      a.ws = t.ws[cur];
-      a.wl = t.wl[cur];
-      a.tbl = t.tbl[cur];
       long long acc = 0;
-      for (int32_t v = threadIdx.x; v < nn; v += kTailNT)
-        for_row<false>(a, v, 0, 1, [&](int32_t, int32_t w) { acc += w; });
+      for (int32_t q = threadIdx.x; q < Q; q += kTailNT) {
+        const uint64_t e = t.tbl[cur][q];
+        if (e != kEmpty) acc += (int32_t)(uint32_t)e;
+      }
       acc = wave_sum(acc);
       if (lane == 0 && acc)
         atomicAdd(reinterpret_cast<unsigned long long *>(&s_cut),
@@ -1641,6 +1649,8 @@ struct Bufs {
   int32_t qcap;     // entries of cstart
   int32_t *M, *mark, *lrank;
   int32_t nt;  // nodes the tail can start from
+  double *tgain;    // per-slot gains in the tail
+  int32_t tslots;   // entries of tgain
   int32_t *Mt, *lvl_map, *lvl_minpt, *lvl_nc;
   double *lvl_mu;
   long long *lvl_cut2;
@@ -1692,6 +1702,8 @@ void carve(Arena &a, int32_t n, int32_t d, int32_t k, Bufs *b) {
   b->lrank = a.take<int32_t>(n1);
   b->nt = std::min<int32_t>(n, kTailNodes);
   b->Mt = a.take<int32_t>(b->nt);
+  b->tslots = (int32_t)std::min<int64_t>(ed, kTailSlots);
+  b->tgain = a.take<double>(b->tslots);
   b->lvl_map = a.take<int32_t>((size_t)kTailLevels * b->nt);
   b->lvl_minpt = a.take<int32_t>((size_t)kTailLevels * b->nt);
   b->lvl_nc = a.take<int32_t>(kTailLevels);
@@ -1845,18 +1857,8 @@ int run_tail(const LadderArgs &g, const Bufs &b, const float *emb,
     t.S[j] = b.S[j];
   }
   t.mu = b.mu;
-  t.target = b.target;
-  t.deg = b.deg;
-  t.parent = b.parent;
-  t.newid = b.newid;
-  t.L = b.L;
-  t.cnt = b.cnt;
-  t.moff = b.moff;
-  t.mem = b.mem;
-  t.capn = b.capn;
+  t.gain = b.tgain;
   t.Mt = b.Mt;
-  t.longrow = b.tile_c;  // the tile lists are free while the tail runs
-  t.longcomp = b.tile_i;
   t.lvl_map = b.lvl_map;
   t.lvl_minpt = b.lvl_minpt;
   t.lvl_nc = b.lvl_nc;
@@ -1867,6 +1869,7 @@ int run_tail(const LadderArgs &g, const Bufs &b, const float *emb,
   t.cur0 = cur;
   t.d = d;
   t.tcap = (int32_t)edge_bound(n, g.k);
+  t.gcap = b.tslots;
   t.n_levels = g.n_levels;
   t.level0 = level0;
   t.round0 = round0;
@@ -2026,6 +2029,7 @@ int ladder_run(const LadderArgs &g, Ctl *ctl, Arena &a, hipStream_t st) {
   int32_t nn = n;
   const int32_t max_rounds = g.max_rounds > 0 ? g.max_rounds : 256;
   int32_t tail_level = -1, tail_round = 0;
+  int64_t slots = 0;  // slots of the current table (its windows' total)
   // EZSP_TAIL_NODES (at most kTailNodes; 0 = never) moves the switch to the
   // tail kernel, so that both paths can be exercised on small inputs
   int32_t tail_nodes = kTailStart;
@@ -2038,7 +2042,8 @@ int ladder_run(const LadderArgs &g, Ctl *ctl, Arena &a, hipStream_t st) {
     const int64_t smin = g.min_size ? g.min_size[l] : 0;
     for (int32_t round = 0;; ++round) {
       if (ed == 0) break;  // no edge left: nothing can merge
-      if (!first && nn <= tail_nodes && ed <= kTailEdges) {
+      if (!first && nn <= tail_nodes && ed <= kTailEdges &&
+          slots <= b.tslots) {
         tail_level = l;  // the rest runs in the tail kernel
         tail_round = round;
         break;
@@ -2089,6 +2094,7 @@ int ladder_run(const LadderArgs &g, Ctl *ctl, Arena &a, hipStream_t st) {
       }
       cur = 1 - cur;
       first = false;
+      slots = h->slots;
       nn = h->n_next;
       ed = h->e_next;
       adj.ws = b.ws[cur];
