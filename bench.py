@@ -5,10 +5,12 @@ HBM: exact kNN (k = 10) of 3,000,000 points, graph build, and the merge
 ladder over lambda = {0.05, 0.2, 0.8} with D = 16 embeddings, down to the
 canonical per-level labels.  Prints one JSON line:
   value        points partitioned per second (n / seconds per step)
-  roofline     the stage that takes the most time: its algorithmic bytes per
-               launch over its mean launch duration (HIP events on the
-               library's stream), against the 8 TB/s HBM peak
-  cpu_baseline the CPU oracle (one thread) on a bounded slab of the same tile
+  roofline     the stage that takes the most time (found in untimed steps
+               with every stage timed): its algorithmic bytes per launch
+               over its mean launch duration, from HIP events on the
+               library's stream around that stage only during the timed
+               steps, against the 8 TB/s HBM peak
+  cpu_baseline the CPU oracle (one thread) on the same tile
 
 roofline.traffic comes from the committed counter summary
 profiles/knn_query.driving-3m.pmc.md (rocprofv3 FETCH_SIZE and WRITE_SIZE,
@@ -41,6 +43,9 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--split-steps", type=int, default=3,
+                    help="untimed steps with every stage timed (the split "
+                    "and the dominant stage)")
     ap.add_argument("--workload", default=WORKLOAD)
     ap.add_argument("--no-cpu", action="store_true",
                     help="skip the CPU oracle baseline")
@@ -145,7 +150,17 @@ def main():
     for _ in range(args.warmup):
         part(xyz, emb)
     torch.cuda.synchronize()
+    # untimed steps with every stage timed: the split and the dominant stage
     ezsp.profile_enable(True)
+    ezsp.profile_only(None)
+    for _ in range(args.split_steps):
+        part(xyz, emb)
+    torch.cuda.synchronize()
+    split_stats = {s: ezsp.profile_read(s) for s in ezsp.STAGES}
+    dom = max(split_stats, key=lambda s: split_stats[s][1])
+    # timed steps: HIP events around the dominant stage only
+    ezsp.profile_enable(True)
+    ezsp.profile_only(dom)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(args.steps):
@@ -157,12 +172,12 @@ def main():
         launches, ms, nbytes = ezsp.profile_read(s)
         stages[s] = {"launches": launches, "ms": ms, "bytes": nbytes}
     ezsp.profile_enable(False)
+    ezsp.profile_only(None)
     ms_per_step = (t1 - t0) * 1e3 / args.steps
     value = sc.n / (ms_per_step / 1e3)
     print(f"[bench] {ms_per_step:.3f} ms/step, n_comp {n_comp.tolist()}",
           file=sys.stderr, flush=True)
 
-    dom = max(stages, key=lambda s: stages[s]["ms"])
     d = stages[dom]
     per_launch_ms = d["ms"] / max(d["launches"], 1)
     per_launch_bytes = d["bytes"] / max(d["launches"], 1)
@@ -180,7 +195,8 @@ def main():
         "step_alg_frac": round(alg_total / (ms_per_step * 1e-3) / 1e9 /
                                HBM_PEAK_GBS, 5),
     }
-    split = {s: round(v["ms"] / args.steps, 4) for s, v in stages.items()}
+    split = {s: round(v[1] / max(args.split_steps, 1), 4)
+             for s, v in split_stats.items()}
     if args.calib_copy:
         # one plain elementwise copy, outside the timed region: the HBM
         # counters of the profiled kernels are scaled by what they read for it

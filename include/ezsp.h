@@ -171,6 +171,12 @@ int ezsp_profile_enable(int on);
 int ezsp_profile_read(const char *stage, int64_t *launches, double *ms,
                       double *alg_bytes);
 
+/* Restricts the event recording to one stage (NULL or "" = every stage,
+ * the default); the other stages still add their algorithmic bytes.  Lets a
+ * benchmark time one stage inside otherwise untouched steps.  Returns 0.
+ * Process-wide state like the above. */
+int ezsp_profile_only(const char *stage);
+
 #ifdef __cplusplus
 }
 #endif

@@ -10,6 +10,7 @@
 namespace ezsp {
 const char *last_error_text();
 int prof_enable(int on);
+int prof_only(const char *name);
 int prof_read(const char *name, int64_t *launches, double *ms,
               double *bytes);
 }
@@ -139,6 +140,8 @@ const char *ezsp_status_string(int status) {
 const char *ezsp_last_error(void) { return last_error_text(); }
 
 int ezsp_profile_enable(int on) { return prof_enable(on); }
+
+int ezsp_profile_only(const char *stage) { return prof_only(stage); }
 
 int ezsp_profile_read(const char *stage, int64_t *launches, double *ms,
                       double *alg_bytes) {

@@ -281,6 +281,7 @@ bool g_prof = false;
 std::vector<hipEvent_t> g_pool;
 std::vector<ProfRec> g_pending;
 std::unordered_map<std::string, ProfTotal> g_totals;
+std::string g_only;  // record events for this stage only ("" = all)
 
 hipEvent_t pool_get() {
   if (!g_pool.empty()) {
@@ -299,6 +300,10 @@ bool prof_on() { return g_prof; }
 void prof_begin(const char *name, hipStream_t st) {
   if (!g_prof) return;
   std::lock_guard<std::mutex> lk(g_prof_mu);
+  if (!g_only.empty() && g_only != name) {
+    g_pending.push_back(ProfRec{name, nullptr, nullptr});  // not timed
+    return;
+  }
   ProfRec r{name, pool_get(), pool_get()};
   if (!r.a || !r.b) return;
   hipEventRecord(r.a, st);
@@ -308,13 +313,15 @@ void prof_begin(const char *name, hipStream_t st) {
 void prof_end(hipStream_t st) {
   if (!g_prof) return;
   std::lock_guard<std::mutex> lk(g_prof_mu);
-  if (!g_pending.empty()) hipEventRecord(g_pending.back().b, st);
+  if (!g_pending.empty() && g_pending.back().b)
+    hipEventRecord(g_pending.back().b, st);
 }
 
 void prof_flush() {
   if (!g_prof) return;
   std::lock_guard<std::mutex> lk(g_prof_mu);
   for (const ProfRec &r : g_pending) {
+    if (!r.a) continue;
     float ms = 0.0f;
     if (hipEventSynchronize(r.b) == hipSuccess &&
         hipEventElapsedTime(&ms, r.a, r.b) == hipSuccess) {
@@ -339,6 +346,12 @@ int prof_enable(int on) {
   g_prof = on != 0;
   g_totals.clear();
   g_pending.clear();
+  return 0;
+}
+
+int prof_only(const char *name) {
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  g_only = name ? name : "";
   return 0;
 }
 

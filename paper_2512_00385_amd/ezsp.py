@@ -32,7 +32,7 @@ ENTRY_POINTS = (
     "ezsp_partition_from_knn",
     "ezsp_component_stats_workspace_size", "ezsp_component_stats",
     "ezsp_status_string", "ezsp_last_error",
-    "ezsp_profile_enable", "ezsp_profile_read",
+    "ezsp_profile_enable", "ezsp_profile_read", "ezsp_profile_only",
 )
 
 
@@ -79,6 +79,7 @@ def load() -> ctypes.CDLL:
         "ezsp_last_error": (ctypes.c_char_p, []),
         "ezsp_profile_enable": (ctypes.c_int, [ctypes.c_int]),
         "ezsp_profile_read": (ctypes.c_int, [ctypes.c_char_p, P, P, P]),
+        "ezsp_profile_only": (ctypes.c_int, [ctypes.c_char_p]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -99,6 +100,11 @@ def last_error() -> str:
 def profile_enable(on: bool = True):
     """Start (clearing the totals) or stop per-stage event timing."""
     load().ezsp_profile_enable(1 if on else 0)
+
+
+def profile_only(stage=None):
+    """Time only `stage` (None: every stage) while profiling is on."""
+    load().ezsp_profile_only(stage.encode() if stage else None)
 
 
 STAGES = ("morton_sort", "knn_query", "graph_build", "select", "union",
