@@ -253,9 +253,10 @@ __device__ __forceinline__ void scan_bucket(const float4 *__restrict__ pts,
 
 // Box test of the children first .. first+7 (level lc) of one node: bit c
 // is set when some lane of the group has the child's box within its current
-// k-th distance.  The eight boxes are loaded before any is used.  The box
-// distance uses the same IEEE operations as d2, so it never exceeds the d2
-// of a point inside the box.
+// k-th distance.  The boxes are loaded four at a time (all four before any
+// is used): fewer registers, more waves per SIMD to hide the latency.  The
+// box distance uses the same IEEE operations as d2, so it never exceeds the
+// d2 of a point inside the box.
 template <int K>
 __device__ __forceinline__ uint32_t child_mask(
     const float4 *__restrict__ blo, const float4 *__restrict__ bhi,
@@ -263,25 +264,28 @@ __device__ __forceinline__ uint32_t child_mask(
     bool act, const uint64_t (&key)[K], int gshift) {
   const int32_t nchild = min(kFan, cnt_lc - first);
   const int32_t off = tree.off[lc] + first;
-  float4 lo[kFan], hi[kFan];
-#pragma unroll
-  for (int c = 0; c < kFan; ++c) {
-    const int32_t j = off + min(c, nchild - 1);
-    lo[c] = blo[j];
-    hi[c] = bhi[j];
-  }
   const uint32_t kth = (uint32_t)(key[K - 1] >> 32);
   uint32_t m = 0;
 #pragma unroll
-  for (int c = 0; c < kFan; ++c) {
-    const float ex = fmaxf(fmaxf(lo[c].x - p.x, p.x - hi[c].x), 0.f);
-    const float ey = fmaxf(fmaxf(lo[c].y - p.y, p.y - hi[c].y), 0.f);
-    const float ez = fmaxf(fmaxf(lo[c].z - p.z, p.z - hi[c].z), 0.f);
-    const float bx = ex * ex, by = ey * ey, bz = ez * ez;
-    const float d2b = (bx + by) + bz;
-    // d2b <= k-th d2 (an empty list, kNoKey, admits everything)
-    const bool need = act && c < nchild && __float_as_uint(d2b) <= kth;
-    if ((__ballot(need) >> gshift) & 0xffffull) m |= 1u << c;
+  for (int h = 0; h < kFan; h += kFan / 2) {
+    float4 lo[kFan / 2], hi[kFan / 2];
+#pragma unroll
+    for (int c = 0; c < kFan / 2; ++c) {
+      const int32_t j = off + min(h + c, nchild - 1);
+      lo[c] = blo[j];
+      hi[c] = bhi[j];
+    }
+#pragma unroll
+    for (int c = 0; c < kFan / 2; ++c) {
+      const float ex = fmaxf(fmaxf(lo[c].x - p.x, p.x - hi[c].x), 0.f);
+      const float ey = fmaxf(fmaxf(lo[c].y - p.y, p.y - hi[c].y), 0.f);
+      const float ez = fmaxf(fmaxf(lo[c].z - p.z, p.z - hi[c].z), 0.f);
+      const float bx = ex * ex, by = ey * ey, bz = ez * ez;
+      const float d2b = (bx + by) + bz;
+      // d2b <= k-th d2 (an empty list, kNoKey, admits everything)
+      const bool need = act && h + c < nchild && __float_as_uint(d2b) <= kth;
+      if ((__ballot(need) >> gshift) & 0xffffull) m |= 1u << (h + c);
+    }
   }
   return m;
 }

@@ -1293,6 +1293,7 @@ struct TailState {
   double *gain;                            // one per slot
   int32_t *Mt;
   int32_t *lvl_map, *lvl_minpt, *lvl_nc;  // kTailLevels x nn0 (nc: levels)
+  int32_t *lvl_rank;                       // kTailLevels x nn0
   double *lvl_mu;                          // kTailLevels x nn0 x d
   long long *lvl_cut2;                     // kTailLevels
   int32_t nn0, ed0, cur0, d, tcap, gcap, n_levels, level0, round0,
@@ -1383,7 +1384,8 @@ __device__ __forceinline__ unsigned long long gain_key(double g) {
 
 template <int DT>
 __global__ __launch_bounds__(kTailNT) void k_tail(TailState t, Ctl *ctl) {
-  __shared__ int32_t s_size[kTailNodes], s_minpt[kTailNodes];
+  __shared__ int32_t s_size[kTailNodes];
+  __shared__ __align__(16) int32_t s_minpt[kTailNodes];
   __shared__ int32_t s_deg[kTailNodes], s_L[kTailNodes];
   __shared__ int32_t s_sel[kTailNodes];
   __shared__ int32_t s_wsa[kTailNodes + 1], s_wsb[kTailNodes + 1];
@@ -1606,8 +1608,28 @@ __global__ __launch_bounds__(kTailNT) void k_tail(TailState t, Ctl *ctl) {
     }
     for (int32_t i = threadIdx.x; i < t.nn0; i += kTailNT)
       t.lvl_map[(int64_t)l * t.nn0 + i] = t.Mt[i];
-    for (int32_t c = threadIdx.x; c < nn; c += kTailNT)
-      t.lvl_minpt[(int64_t)l * t.nn0 + c] = t.minpt[cur][c];
+    for (int32_t c = threadIdx.x; c < nn; c += kTailNT) {
+      const int32_t m = t.minpt[cur][c];
+      t.lvl_minpt[(int64_t)l * t.nn0 + c] = m;
+      s_minpt[c] = m;
+    }
+    __syncthreads();
+    // canonical number of every component: its rank by smallest point
+    {
+      const int4 *m4 = reinterpret_cast<const int4 *>(s_minpt);
+      const int32_t n4 = nn >> 2;
+      for (int32_t c = threadIdx.x; c < nn; c += kTailNT) {
+        const int32_t m = s_minpt[c];
+        int32_t r = 0;
+#pragma unroll 4
+        for (int32_t j = 0; j < n4; ++j) {
+          const int4 x = m4[j];
+          r += (x.x < m) + (x.y < m) + (x.z < m) + (x.w < m);
+        }
+        for (int32_t c2 = 4 * n4; c2 < nn; ++c2) r += s_minpt[c2] < m ? 1 : 0;
+        t.lvl_rank[(int64_t)l * t.nn0 + c] = r;
+      }
+    }
     __syncthreads();
     if (t.want_energy) {
       for (int64_t q = threadIdx.x; q < (int64_t)nn * d; q += kTailNT)
@@ -1625,6 +1647,29 @@ __global__ __launch_bounds__(kTailNT) void k_tail(TailState t, Ctl *ctl) {
       if (threadIdx.x == 0) t.lvl_cut2[l] = s_cut;
     }
     __syncthreads();
+  }
+}
+
+// Point labels of every level the tail ended: point p -> its node at the
+// tail's start -> that level's component -> the component's canonical rank.
+__global__ __launch_bounds__(256) void k_tail_labels(
+    int32_t n, const int32_t *__restrict__ inv, const int32_t *__restrict__ M,
+    const int32_t *__restrict__ lvl_map, const int32_t *__restrict__ lvl_rank,
+    const int32_t *__restrict__ lvl_nc, int32_t nt, int32_t level0,
+    int32_t n_levels, int32_t *__restrict__ labels, Ctl *ctl) {
+  const int32_t p = blockIdx.x * blockDim.x + threadIdx.x;
+  if (p >= n) return;
+  const int32_t i = inv ? inv[p] : p;
+  const int32_t c0 = ((uint32_t)i < (uint32_t)n) ? M[i] : -1;
+  for (int32_t l = level0; l < n_levels; ++l) {
+    int32_t out = -1;
+    if ((uint32_t)c0 < (uint32_t)nt) {
+      const int32_t c = lvl_map[(int64_t)l * nt + c0];
+      if ((uint32_t)c < (uint32_t)min(lvl_nc[l], nt))
+        out = lvl_rank[(int64_t)l * nt + c];
+    }
+    if (out < 0) raise_err(ctl, kErrInternal);
+    labels[(int64_t)l * n + p] = out;
   }
 }
 
@@ -1651,7 +1696,7 @@ struct Bufs {
   int32_t nt;  // nodes the tail can start from
   double *tgain;    // per-slot gains in the tail
   int32_t tslots;   // entries of tgain
-  int32_t *Mt, *lvl_map, *lvl_minpt, *lvl_nc;
+  int32_t *Mt, *lvl_map, *lvl_minpt, *lvl_nc, *lvl_rank;
   double *lvl_mu;
   long long *lvl_cut2;
   int32_t *bsum, *tmp;
@@ -1707,6 +1752,7 @@ void carve(Arena &a, int32_t n, int32_t d, int32_t k, Bufs *b) {
   b->lvl_map = a.take<int32_t>((size_t)kTailLevels * b->nt);
   b->lvl_minpt = a.take<int32_t>((size_t)kTailLevels * b->nt);
   b->lvl_nc = a.take<int32_t>(kTailLevels);
+  b->lvl_rank = a.take<int32_t>((size_t)kTailLevels * b->nt);
   b->lvl_mu = a.take<double>((size_t)kTailLevels * b->nt * d);
   b->lvl_cut2 = a.take<long long>(kTailLevels);
   b->bsum = a.take<int32_t>(scan_blocks(ed + n1) + 2);
@@ -1862,6 +1908,7 @@ int run_tail(const LadderArgs &g, const Bufs &b, const float *emb,
   t.lvl_map = b.lvl_map;
   t.lvl_minpt = b.lvl_minpt;
   t.lvl_nc = b.lvl_nc;
+  t.lvl_rank = b.lvl_rank;
   t.lvl_mu = b.lvl_mu;
   t.lvl_cut2 = b.lvl_cut2;
   t.nn0 = nn;
@@ -1895,46 +1942,41 @@ int run_tail(const LadderArgs &g, const Bufs &b, const float *emb,
       hipLaunchKernelGGL(k_tail<0>, dim3(1), dim3(kTailNT), 0, st, t, ctl);
   }
   prof_end(st);
-  int rc = read_ctl(ctl, h, st);
+  // labels straight from the snapshots (no host round trip in between);
+  // on a device error they are discarded
+  hipLaunchKernelGGL(k_tail_labels, blocks_for(n), dim3(256), 0, st, n, g.inv,
+                     b.M, b.lvl_map, b.lvl_rank, b.lvl_nc, nn, level0,
+                     g.n_levels, g.labels, ctl);
+  int32_t nc[kTailLevels];
+  long long cut2[kTailLevels];
+  int rc = check_hip(hipMemcpyAsync(nc, b.lvl_nc, sizeof(nc),
+                                    hipMemcpyDeviceToHost, st),
+                     "hipMemcpyAsync(levels)");
+  if (!rc)
+    rc = check_hip(hipMemcpyAsync(cut2, b.lvl_cut2, sizeof(cut2),
+                                  hipMemcpyDeviceToHost, st),
+                   "hipMemcpyAsync(levels)");
+  if (!rc) rc = read_ctl(ctl, h, st);
   if (rc) return rc;
   if (h->err & kErrNotConv) {
     set_error("level %d reached max_rounds = %d", h->tail_level, max_rounds);
     return -6;
   }
   if (h->err) return status_from_err(h->err);
-  int32_t nc[kTailLevels];
-  long long cut2[kTailLevels];
-  rc = check_hip(hipMemcpyAsync(nc, b.lvl_nc, sizeof(nc),
-                                hipMemcpyDeviceToHost, st),
-                 "hipMemcpyAsync(levels)");
-  if (!rc)
-    rc = check_hip(hipMemcpyAsync(cut2, b.lvl_cut2, sizeof(cut2),
-                                  hipMemcpyDeviceToHost, st),
-                   "hipMemcpyAsync(levels)");
-  if (!rc) rc = check_hip(hipStreamSynchronize(st), "hipStreamSynchronize");
-  if (rc) return rc;
   for (int32_t l = level0; l < g.n_levels; ++l) {
-    const int32_t ncl = nc[l];
-    if (ncl < 1 || ncl > nn) {
-      set_error("tail level %d: %d superpoints", l, ncl);
+    if (nc[l] < 1 || nc[l] > nn) {
+      set_error("tail level %d: %d superpoints", l, nc[l]);
       return -5;
     }
-    // level snapshots have a stride of the tail's start size nn
-    const int32_t *map = b.lvl_map + (int64_t)l * nn;
-    const int32_t *mp = b.lvl_minpt + (int64_t)l * nn;
-    int32_t *out = g.labels + (int64_t)l * n;
-    hipLaunchKernelGGL(k_fill_i32, blocks_for(n), dim3(256), 0, st, b.mark,
-                       (int64_t)n, 0);
-    hipLaunchKernelGGL(k_mark, blocks_for(ncl), dim3(256), 0, st, ncl, mp,
-                       b.mark, n, ctl);
-    device_scan(ScanArray{b.mark, b.lrank, n, nullptr}, n, b.bsum, b.tmp, st);
-    hipLaunchKernelGGL(k_labels, blocks_for(n), dim3(256), 0, st, n, ncl,
-                       g.inv, b.M, map, nn, mp, b.lrank, out, ctl);
-    g.n_comp[l] = ncl;
-    if (t.want_energy) {
+    g.n_comp[l] = nc[l];
+  }
+  if (t.want_energy) {
+    for (int32_t l = level0; l < g.n_levels; ++l) {
+      // level snapshots have a stride of the tail's start size nn
+      const int32_t *map = b.lvl_map + (int64_t)l * nn;
       hipLaunchKernelGGL(k_energy_reset, dim3(1), dim3(64), 0, st, ctl);
       hipLaunchKernelGGL(k_energy_fid<false>, dim3(kEnergyBlocks), dim3(256),
-                         0, st, n, d, ncl, emb, b.M, map, nn,
+                         0, st, n, d, nc[l], emb, b.M, map, nn,
                          b.lvl_mu + (int64_t)l * nn * d, ctl, b.partial);
       hipLaunchKernelGGL(k_energy_sum, dim3(1), dim3(64), 0, st, b.partial,
                          kEnergyBlocks, ctl);
