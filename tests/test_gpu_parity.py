@@ -144,6 +144,39 @@ def test_partition_room_ladder(tail_mode):
     check_against_oracle(sc.xyz, sc.emb, sc.k, [0.02, 0.05, 0.2, 0.8, 3.2])
 
 
+_FULL = {}
+
+
+def _oracle_full(name):
+    """The oracle's own kNN, graph and ladder on a whole workload (computed
+    once per module)."""
+    if name not in _FULL:
+        sc = scenes.load(name)
+        rl, rnc, ren, _ = oracle.partition(sc.xyz, sc.emb, sc.k, sc.lambdas)
+        _FULL[name] = (sc, rl, rnc, ren)
+    return _FULL[name]
+
+
+@pytest.mark.parametrize("name", ["room-1m", "driving-3m"])
+def test_partition_full_size(name, tail_mode):
+    """Whole 1M-point room and 3M-point driving tile in the benchmark's
+    launch configuration (a reused Partitioner workspace, no energy pass),
+    every label of every level against the oracle's own full run; then the
+    energy through ezsp.partition."""
+    sc, rl, rnc, ren = _oracle_full(name)
+    part = ezsp.Partitioner(sc.n, sc.d, sc.k, sc.lambdas,
+                            device=torch.device("cuda:0"))
+    xyz, emb = dev(sc.xyz), dev(sc.emb)
+    for _ in range(2):  # the second call reuses the workspace
+        labels, nc, _ = part(xyz, emb)
+        assert np.array_equal(nc, rnc), (nc, rnc)
+        labels = labels.cpu().numpy()
+        for l in range(len(sc.lambdas)):
+            assert np.array_equal(labels[l], rl[l]), l
+    _, _, en = ezsp.partition(xyz, emb, sc.k, sc.lambdas, energy=True)
+    np.testing.assert_allclose(en, ren, rtol=ENERGY_RTOL, atol=0)
+
+
 @pytest.mark.parametrize("seed", range(6))
 @pytest.mark.parametrize("lambdas", [[0.1], [0.05, 0.2, 0.8], [0.8, 0.2],
                                      [0.01, 0.03, 0.1, 0.3, 1.0, 3.0]])
