@@ -53,10 +53,14 @@ struct Ctl {
   double fid_total;     // fidelity term of the energy
   Stripe e_next_s[kStripes];  // device side of e_next
   Stripe e_fwd_s[kStripes];   // device side of e_fwd
+  Stripe maxabs_s[kStripes];  // max |e| bits from the fused gather
 };
 
 __device__ __forceinline__ void stripe_add(Stripe *s, int32_t v) {
   atomicAdd(&s[blockIdx.x % kStripes].v, v);
+}
+__device__ __forceinline__ void stripe_max(Stripe *s, int32_t v) {
+  atomicMax(&s[blockIdx.x % kStripes].v, v);
 }
 __device__ __forceinline__ void stripe_zero(Stripe *s) {
   for (int i = threadIdx.x; i < kStripes; i += blockDim.x) s[i].v = 0;

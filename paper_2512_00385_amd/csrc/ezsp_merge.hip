@@ -65,6 +65,45 @@ __global__ void k_fill_i32(int32_t *p, int64_t n, int32_t v) {
     p[i] = v;
 }
 
+// Rows of 4k floats: 16-byte moves, and the max |e| of Step 0's fixed-point
+// shift (with the non-finite check) taken on the way, striped per block.
+__global__ __launch_bounds__(256) void k_gather_rows4(const float4 *emb,
+                                                      const int32_t *perm,
+                                                      int32_t n, int32_t d4,
+                                                      float4 *out, Ctl *ctl) {
+  uint32_t m = 0;
+  bool bad = false;
+  const int64_t total = (int64_t)n * d4;
+  for (int64_t t = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; t < total;
+       t += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t i = t / d4;
+    const float4 x = emb[(int64_t)perm[i] * d4 + (t - i * d4)];
+    out[t] = x;
+    const float v[4] = {x.x, x.y, x.z, x.w};
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      if (!isfinite(v[j])) bad = true;
+      else m = max(m, __float_as_uint(fabsf(v[j])));
+    }
+  }
+#pragma unroll
+  for (int off = kWave / 2; off > 0; off >>= 1)
+    m = max(m, (uint32_t)__shfl_xor((int)m, off, kWave));
+  __shared__ uint32_t sm[256 / kWave];
+  __shared__ int sbad;
+  if (threadIdx.x == 0) sbad = 0;
+  __syncthreads();
+  if ((threadIdx.x & (kWave - 1)) == 0) sm[threadIdx.x / kWave] = m;
+  if (__ballot(bad) && (threadIdx.x & (kWave - 1)) == 0) sbad = 1;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint32_t r = sm[0];
+    for (int q = 1; q < 256 / kWave; ++q) r = max(r, sm[q]);
+    stripe_max(ctl->maxabs_s, (int32_t)r);  // |e| bits < 2^31
+    if (sbad) raise_err(ctl, kErrNonFinite);
+  }
+}
+
 __global__ __launch_bounds__(256) void k_gather_rows(const float *emb,
                                                      const int32_t *perm,
                                                      int32_t n, int32_t d,
@@ -568,6 +607,10 @@ struct ScanRoots {
 
 // Component of every node; also counts members (the rank is the node's
 // place among its component's members).
+// Component of every node and its place among the component's members.
+// Nodes of one component mostly sit together in node order, so the lanes
+// of a wave are grouped by component (ballot per distinct value) and each
+// group takes its places with one atomic, made by its lowest lane.
 __global__ __launch_bounds__(256) void k_assign(int32_t nn,
                                                 const int32_t *parent,
                                                 const int32_t *newid,
@@ -575,20 +618,40 @@ __global__ __launch_bounds__(256) void k_assign(int32_t nn,
                                                 int32_t *rank, Ctl *ctl) {
   if (!ctl->any_choice) return;
   const int32_t v = xcd_tid();
-  if (v >= nn) return;
-  const int32_t r = parent[v];
-  int32_t c = 0;
-  if ((uint32_t)r < (uint32_t)nn) {
-    c = newid[r];
-  } else {
-    raise_err(ctl, kErrInternal);
-  }
-  if ((uint32_t)c >= (uint32_t)ctl->n_next) {
-    raise_err(ctl, kErrInternal);
+  const bool act = v < nn;
+  int32_t c = -1;
+  if (act) {
+    const int32_t r = parent[v];
     c = 0;
+    if ((uint32_t)r < (uint32_t)nn) {
+      c = newid[r];
+    } else {
+      raise_err(ctl, kErrInternal);
+    }
+    if ((uint32_t)c >= (uint32_t)ctl->n_next) {
+      raise_err(ctl, kErrInternal);
+      c = 0;
+    }
+    L[v] = c;
   }
-  L[v] = c;
-  rank[v] = atomicAdd(&cnt[c], 1);
+  const int lane = threadIdx.x & (kWave - 1);
+  uint64_t todo = __ballot(act);
+  uint64_t mine = 0;
+  int leader = 0;
+  while (todo) {
+    const int l = __builtin_ctzll(todo);
+    const int32_t cl = __shfl(c, l, kWave);
+    const uint64_t m = __ballot(c == cl) & todo;
+    if ((m >> lane) & 1) {
+      mine = m;
+      leader = l;
+    }
+    todo &= ~m;
+  }
+  int32_t base = 0;
+  if (act && lane == leader) base = atomicAdd(&cnt[c], __popcll(mine));
+  base = __shfl(base, leader, kWave);
+  if (act) rank[v] = base + __popcll(mine & ((1ull << lane) - 1));
 }
 
 __global__ __launch_bounds__(256) void k_zero_cnt(int32_t bound, const Ctl *ctl,
@@ -2011,17 +2074,31 @@ int ladder_run(const LadderArgs &g, Ctl *ctl, Arena &a, hipStream_t st) {
   // embeddings in internal order, fixed-point shift (Step 0)
   // (always a copy in the workspace: aligned rows for vector loads)
   const float *emb = b.emb_int;
+  // rows of 4k floats at a 16-byte aligned base: vector gather with the
+  // max |e| reduction fused in
+  const bool fused = g.perm && d % 4 == 0 &&
+                     (reinterpret_cast<uintptr_t>(g.emb) & 15) == 0;
   if (g.perm) {
-    hipLaunchKernelGGL(k_gather_rows, blocks_for((int64_t)n * d), dim3(256),
-                       0, st, g.emb, g.perm, n, d, b.emb_int);
+    if (fused) {
+      const int64_t t4 = (int64_t)n * (d / 4);
+      const unsigned grid =
+          (unsigned)std::min<int64_t>((t4 + 255) / 256, 8192);
+      hipLaunchKernelGGL(k_gather_rows4, dim3(grid), dim3(256), 0, st,
+                         reinterpret_cast<const float4 *>(g.emb), g.perm, n,
+                         d / 4, reinterpret_cast<float4 *>(b.emb_int), ctl);
+    } else {
+      hipLaunchKernelGGL(k_gather_rows, blocks_for((int64_t)n * d), dim3(256),
+                         0, st, g.emb, g.perm, n, d, b.emb_int);
+    }
   } else {
     rc = check_hip(hipMemcpyAsync(b.emb_int, g.emb, sizeof(float) * n * d,
                                   hipMemcpyDeviceToDevice, st),
                    "hipMemcpyAsync(emb)");
     if (rc) return rc;
   }
-  hipLaunchKernelGGL(k_maxabs, dim3(2048), dim3(256), 0, st, emb,
-                     (int64_t)n * d, ctl);
+  if (!fused)
+    hipLaunchKernelGGL(k_maxabs, dim3(2048), dim3(256), 0, st, emb,
+                       (int64_t)n * d, ctl);
   hipLaunchKernelGGL(k_fixshift, dim3(1), dim3(64), 0, st, ctl, n);
 
   // first-round graph (Step 0: the superpoint adjacency is the kNN graph)

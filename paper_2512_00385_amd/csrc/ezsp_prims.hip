@@ -182,6 +182,7 @@ __global__ void k_ctl_init(Ctl *ctl) {
   if (blockIdx.x == 0) {
     stripe_zero(ctl->e_next_s);
     stripe_zero(ctl->e_fwd_s);
+    stripe_zero(ctl->maxabs_s);
   }
 }
 
@@ -216,7 +217,10 @@ __global__ __launch_bounds__(256) void k_maxabs(const float *v, int64_t count,
 // F = min(40, 61 - ceil(log2 n) - max(0, ceil(log2 A))), A = max |e|.
 __global__ void k_fixshift(Ctl *ctl, int32_t n) {
   if (threadIdx.x != 0 || blockIdx.x != 0) return;
-  const float A = __uint_as_float(ctl->maxabs_bits);
+  uint32_t bits = ctl->maxabs_bits;
+  for (int i = 0; i < kStripes; ++i)
+    bits = max(bits, (uint32_t)ctl->maxabs_s[i].v);
+  const float A = __uint_as_float(bits);
   int cn = 0;
   while (((int64_t)1 << cn) < (int64_t)n) ++cn;
   int ca = 0;
