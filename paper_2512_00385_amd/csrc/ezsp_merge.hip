@@ -52,7 +52,7 @@ constexpr int kLongGrid = 2048; // blocks of 4 waves for the long rows
 constexpr int kBigComp = 128;   // components with more members: one block
 constexpr int kWaveRowsMax = 65536;  // rounds this small: a wave per row
 constexpr int kBigGrid = 512;
-constexpr int kChunk = 2048;    // table slots contracted by one block in LDS
+constexpr int kChunk = 1024;    // table slots contracted by one block in LDS
 constexpr int kBatch = 256;     // members taken at a time by a block
 constexpr int kPreSlots = 4096; // LDS pre-aggregation table of a big tile
 
@@ -975,19 +975,22 @@ __global__ __launch_bounds__(256) void k_contract_chunk(
     int32_t span = 0;
     if (idx < m_hi) {
       const int32_t m = mem[idx];
+      // the row's span and base depend on m only: loaded with L[m]
+      const int32_t sp = row_span<FIRST>(a, m);
+      const int32_t rb = row_base<FIRST>(a, m);
       const int32_t A = L[m];
       const int32_t cp = cap[A];
+      const int32_t lb = toff[A] - j0;
       if (cp > 0 && cp <= chunk) {
-        const int32_t lb = toff[A] - j0;
         if (lb < 0 || lb + cp > 2 * chunk) {
           raise_err(ctl, kErrInternal);
         } else {
-          span = row_span<FIRST>(a, m);
+          span = sp;
           bm[threadIdx.x] = m;
           bA[threadIdx.x] = A;
           blb[threadIdx.x] = lb;
           bcp[threadIdx.x] = cp;
-          bbase[threadIdx.x] = row_base<FIRST>(a, m);
+          bbase[threadIdx.x] = rb;
         }
       }
     }
