@@ -51,6 +51,8 @@ constexpr int kLongRow = 128;   // rows longer than this: one wave per row
 constexpr int kLongGrid = 2048; // blocks of 4 waves for the long rows
 constexpr int kBigComp = 128;   // components with more members: one block
 constexpr int kWaveRowsMax = 65536;  // rounds this small: a wave per row
+constexpr int kSelLanesFirst = 2;  // lanes per row in the first round's select
+constexpr int kSelLanes = 4;       // ... in later rounds
 constexpr int kBigGrid = 512;
 constexpr int kChunk = 1024;    // table slots contracted by one block in LDS
 constexpr int kBatch = 256;     // members taken at a time by a block
@@ -452,44 +454,64 @@ __device__ __forceinline__ double edge_gain_t(const NodeIn &s,
   }
 }
 
-template <bool FIRST, int DT>
+// Steps 1-2 for rows of up to kLongRow entries, G lanes per row: the lanes
+// take every G-th entry of the row (shorter dependent chains per lane than
+// a thread per row, and a wave waits for its longest rows only G-fold
+// shortened), then the group combines its candidates.
+template <bool FIRST, int DT, int G>
 __global__ __launch_bounds__(256) void k_select(
     int32_t nn, Adj a, NodeIn s, int32_t d, double lambda, int64_t smin,
     int32_t *__restrict__ target, int32_t *__restrict__ deg,
     int32_t *__restrict__ long_rows, Ctl *ctl) {
-  const int32_t v = xcd_tid();
-  if (v >= nn) return;
-  if (row_span<FIRST>(a, v) > kLongRow) {  // a whole block takes this row
+  const int32_t tid = xcd_tid();
+  const int32_t v = tid / G;
+  const int lg = tid & (G - 1);
+  const bool live = v < nn && row_span<FIRST>(a, v) <= kLongRow;
+  if (v < nn && !live && lg == 0) {  // a whole block takes this row
     const int32_t slot = atomicAdd(&ctl->n_long, 1);
     if (slot < nn) long_rows[slot] = v;
     else raise_err(ctl, kErrInternal);
-    return;
   }
-  const int F = ctl->F;
-  const double sF = ldexp(1.0, F), sIF = ldexp(1.0, -F);
-  const int32_t sv = node_size<FIRST>(s, v);
-  const double dsv = (double)sv;
-  const bool small = (int64_t)sv < smin;
-  MeanRow<FIRST, DT> mv;
-  mv.load(s, v, sF, sIF);
   Best b{0.0, 0, -1};
   int32_t cnt = 0;
-  for_row<FIRST>(a, v, 0, 1, [&](int32_t u, int32_t w) {
-    ++cnt;
-    if ((uint32_t)u >= (uint32_t)nn) {
-      raise_err(ctl, kErrInternal);
-      return;
+  if (live) {
+    const int F = ctl->F;
+    const double sF = ldexp(1.0, F), sIF = ldexp(1.0, -F);
+    const int32_t sv = node_size<FIRST>(s, v);
+    const double dsv = (double)sv;
+    const bool small = (int64_t)sv < smin;
+    MeanRow<FIRST, DT> mv;
+    mv.load(s, v, sF, sIF);
+    for_row<FIRST>(a, v, lg, G, [&](int32_t u, int32_t w) {
+      ++cnt;
+      if ((uint32_t)u >= (uint32_t)nn) {
+        raise_err(ctl, kErrInternal);
+        return;
+      }
+      const double g =
+          edge_gain_t<FIRST, DT>(s, mv, v, dsv, u, w, d, lambda, sF, sIF);
+      if (g > 0.0 || small) {
+        const Best c{g, node_minpt<FIRST>(s, u), u};
+        if (best_before(c, b)) b = c;
+      }
+    });
+  }
+  if constexpr (G > 1) {
+#pragma unroll
+    for (int off = G / 2; off > 0; off >>= 1) {
+      Best o;
+      o.g = __shfl_xor(b.g, off, kWave);
+      o.mp = __shfl_xor(b.mp, off, kWave);
+      o.u = __shfl_xor(b.u, off, kWave);
+      if (best_before(o, b)) b = o;
+      cnt += __shfl_xor(cnt, off, kWave);
     }
-    const double g =
-        edge_gain_t<FIRST, DT>(s, mv, v, dsv, u, w, d, lambda, sF, sIF);
-    if (g > 0.0 || small) {
-      const Best c{g, node_minpt<FIRST>(s, u), u};
-      if (best_before(c, b)) b = c;
-    }
-  });
-  target[v] = b.u;
-  deg[v] = cnt;
-  if (__ballot(b.u >= 0) && (threadIdx.x & (kWave - 1)) == 0)
+  }
+  if (live && lg == 0) {
+    target[v] = b.u;
+    deg[v] = cnt;
+  }
+  if (__ballot(live && lg == 0 && b.u >= 0) && (threadIdx.x & (kWave - 1)) == 0)
     ctl->any_choice = 1;
 }
 
@@ -1871,10 +1893,11 @@ void launch_round(const Bufs &b, const Adj &adj, int cur, int32_t n,
       1, std::min<int64_t>(all_rows ? (nn + 3) / 4 : kLongGrid, (nn + 3) / 4)));
   const dim3 big_grid(
       (unsigned)std::max<int64_t>(1, std::min<int64_t>(kBigGrid, nn / 16)));
+  constexpr int G = FIRST ? kSelLanesFirst : kSelLanes;
   if (!all_rows)
-    hipLaunchKernelGGL((k_select<FIRST, DT>), xblocks_for(nn), dim3(256), 0,
-                       st, nn, adj, s, d, lambda, smin, b.target, b.deg,
-                       b.long_rows, ctl);
+    hipLaunchKernelGGL((k_select<FIRST, DT, G>), xblocks_for((int64_t)nn * G),
+                       dim3(256), 0, st, nn, adj, s, d, lambda, smin, b.target,
+                       b.deg, b.long_rows, ctl);
   hipLaunchKernelGGL((k_select_long<FIRST, DT>), long_grid, dim3(256), 0, st,
                      nn, adj, s, d, lambda, smin, b.target, b.deg, b.long_rows,
                      all_rows, ctl);
