@@ -53,6 +53,7 @@ constexpr int kBigComp = 128;   // components with more members: one block
 constexpr int kWaveRowsMax = 65536;  // rounds this small: a wave per row
 constexpr int kSelLanesFirst = 2;  // lanes per row in the first round's select
 constexpr int kSelLanes = 4;       // ... in later rounds
+constexpr int kStatsLanes = 4;     // lanes per component in the statistics
 constexpr int kBigGrid = 512;
 constexpr int kChunk = 1024;    // table slots contracted by one block in LDS
 constexpr int kBatch = 256;     // members taken at a time by a block
@@ -824,6 +825,90 @@ __global__ __launch_bounds__(256) void k_stats(
 // Components with many members: one block each, threads stride over the
 // members and the sums are combined in shared memory (integer, so the
 // order does not matter).
+// Step 4 statistics with G lanes per component (rows of DT values): the
+// lanes take every G-th member, each summing whole rows, then the group
+// adds its partial sums (exact int64) and spreads the stores over its lanes.
+// Components are laid out over the XCDs like xcd_item, in whole groups.
+template <bool FIRST, int DT, int G>
+__global__ __launch_bounds__(256) void k_stats_g(
+    int32_t bound, const int32_t *__restrict__ mem,
+    const int32_t *__restrict__ moff, NodeIn s,
+    const int32_t *__restrict__ deg, NodeOut o,
+    int32_t *__restrict__ big, Ctl *ctl) {
+  static_assert(DT % G == 0 && (DT / G) % 2 == 0, "dims per lane");
+  if (!ctl->any_choice) return;
+  const int32_t total = min(bound, ctl->n_next) * G;
+  const int32_t per = ((total + kXcd - 1) / kXcd + G - 1) / G * G;
+  const int32_t j =
+      (int32_t)(blockIdx.x / kXcd) * (int32_t)blockDim.x + (int32_t)threadIdx.x;
+  const int32_t sub = (int32_t)(blockIdx.x % kXcd) * per + j;
+  if (j >= per || sub >= total) return;  // whole groups
+  const int32_t c = sub / G;
+  const int lg = sub & (G - 1);
+  const int32_t m0 = moff[c], m1 = moff[c + 1];
+  if (m1 - m0 > o.big_members) {
+    if (lg == 0) big[atomicAdd(&ctl->n_big, 1)] = c;
+    return;
+  }
+  const double sF = ldexp(1.0, ctl->F), sIF = ldexp(1.0, -ctl->F);
+  int32_t size = 0, mp = INT32_MAX, cap = 0;
+  int64_t acc[DT];
+#pragma unroll
+  for (int q = 0; q < DT; ++q) acc[q] = 0;
+  for (int32_t t = m0 + lg; t < m1; t += G) {
+    const int32_t m = mem[t];
+    size += node_size<FIRST>(s, m);
+    mp = min(mp, node_minpt<FIRST>(s, m));
+    cap += deg[m];
+    if (FIRST) {
+      const float4 *p = reinterpret_cast<const float4 *>(s.emb + (int64_t)m * DT);
+#pragma unroll
+      for (int q = 0; q < DT / 4; ++q) {
+        const float4 x = p[q];
+        acc[4 * q + 0] += (int64_t)rint((double)x.x * sF);
+        acc[4 * q + 1] += (int64_t)rint((double)x.y * sF);
+        acc[4 * q + 2] += (int64_t)rint((double)x.z * sF);
+        acc[4 * q + 3] += (int64_t)rint((double)x.w * sF);
+      }
+    } else {
+      const longlong2 *p =
+          reinterpret_cast<const longlong2 *>(s.S + (int64_t)m * DT);
+#pragma unroll
+      for (int q = 0; q < DT / 2; ++q) {
+        const longlong2 x = p[q];
+        acc[2 * q + 0] += x.x;
+        acc[2 * q + 1] += x.y;
+      }
+    }
+  }
+#pragma unroll
+  for (int off = G / 2; off > 0; off >>= 1) {
+    size += __shfl_xor(size, off, kWave);
+    cap += __shfl_xor(cap, off, kWave);
+    mp = min(mp, __shfl_xor(mp, off, kWave));
+#pragma unroll
+    for (int q = 0; q < DT; ++q)
+      acc[q] += __shfl_xor((long long)acc[q], off, kWave);
+  }
+  if (lg == 0) {
+    o.size[c] = size;
+    o.minpt[c] = mp;
+    note_window(o, c, cap, m1 - m0, ctl);
+  }
+  const double dsz = (double)size;
+  constexpr int kPer = DT / G;
+  longlong2 *So = reinterpret_cast<longlong2 *>(o.S + (int64_t)c * DT);
+  double2 *Mo = reinterpret_cast<double2 *>(o.mu + (int64_t)c * DT);
+#pragma unroll
+  for (int q = 0; q < DT / 2; ++q) {
+    if (q / (kPer / 2) != lg) continue;  // this lane's share of the row
+    So[q] = make_longlong2(acc[2 * q], acc[2 * q + 1]);
+    const double q0 = (double)acc[2 * q] / dsz;
+    const double q1 = (double)acc[2 * q + 1] / dsz;
+    Mo[q] = make_double2(q0 * sIF, q1 * sIF);
+  }
+}
+
 template <bool FIRST>
 __global__ __launch_bounds__(256) void k_stats_big(
     const int32_t *__restrict__ mem, const int32_t *__restrict__ moff,
@@ -1925,8 +2010,15 @@ void launch_round(const Bufs &b, const Adj &adj, int cur, int32_t n,
                   b.minpt[nxt], b.capn,    b.wl[nxt],
                   b.cbig,      chunk,     nn > kWaveRowsMax ? kBigComp : 16,
                   b.tile_c,    b.tile_i};
-  hipLaunchKernelGGL((k_stats<FIRST, DT>), xblocks_for(nn), dim3(256), 0, st, nn,
-                     b.mem, b.moff, s, b.deg, d, o, b.big, ctl);
+  if constexpr (DT > 0) {
+    constexpr int G = kStatsLanes;
+    hipLaunchKernelGGL((k_stats_g<FIRST, DT, G>),
+                       xblocks_for((int64_t)nn * G + kXcd * G), dim3(256), 0,
+                       st, nn, b.mem, b.moff, s, b.deg, o, b.big, ctl);
+  } else {
+    hipLaunchKernelGGL((k_stats<FIRST, DT>), xblocks_for(nn), dim3(256), 0,
+                       st, nn, b.mem, b.moff, s, b.deg, d, o, b.big, ctl);
+  }
   hipLaunchKernelGGL(k_stats_big<FIRST>, big_grid, dim3(256), 0, st,
                      b.mem, b.moff, s, b.deg, d, o, b.big, ctl);
   prof_end(st);
