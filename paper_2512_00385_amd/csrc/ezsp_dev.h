@@ -173,6 +173,44 @@ __global__ __launch_bounds__(kScanNT) void k_scan_apply(Op op, int32_t n,
   }
 }
 
+// Apply pass that finds its own tile offset: the sum of the raw tile sums
+// before it (a few thousand at most, read from L2), so no separate pass
+// scans the tile sums.  Tile 0 also writes the total.
+template <class Op>
+__global__ __launch_bounds__(kScanNT) void k_scan_apply_sum(
+    Op op, int32_t n, const int32_t *bsum, int32_t nb, int32_t *total) {
+  __shared__ int32_t wsum[kScanNT / kWave];
+  const int32_t b = blockIdx.x;
+  const int32_t upto = b == 0 ? nb : b;
+  int32_t pre = 0, all = 0;
+  for (int32_t t = threadIdx.x; t < upto; t += kScanNT) {
+    const int32_t x = bsum[t];
+    all += x;
+    pre += t < b ? x : 0;
+  }
+  int32_t pre_tot, all_tot;
+  block_excl_scan<kScanNT>(pre, wsum, &pre_tot);
+  block_excl_scan<kScanNT>(all, wsum, &all_tot);
+  if (b == 0 && threadIdx.x == 0) *total = all_tot;
+  const int32_t base = b * kScanTile + threadIdx.x * kScanItems;
+  int32_t v[kScanItems];
+  int32_t s = 0;
+#pragma unroll
+  for (int j = 0; j < kScanItems; ++j) {
+    int32_t i = base + j;
+    v[j] = (i < n) ? op.value(i) : 0;
+    s += v[j];
+  }
+  int32_t tot;
+  int32_t run = block_excl_scan<kScanNT>(s, wsum, &tot) + pre_tot;
+#pragma unroll
+  for (int j = 0; j < kScanItems; ++j) {
+    int32_t i = base + j;
+    if (i < n) op.emit(i, run, v[j]);
+    run += v[j];
+  }
+}
+
 inline int32_t scan_blocks(int64_t n) {
   return (int32_t)((n + kScanTile - 1) / kScanTile);
 }
@@ -224,10 +262,8 @@ inline void device_scan(const Op &op, int32_t n, int32_t *bsum, int32_t *total,
   }
   hipLaunchKernelGGL(k_scan_reduce<Op>, dim3(nb), dim3(kScanNT), 0, st, op, n,
                      bsum);
-  hipLaunchKernelGGL(k_scan_bsums, dim3(1), dim3(1024), 0, st, bsum, nb,
-                     total);
-  hipLaunchKernelGGL(k_scan_apply<Op>, dim3(nb), dim3(kScanNT), 0, st, op, n,
-                     bsum);
+  hipLaunchKernelGGL(k_scan_apply_sum<Op>, dim3(nb), dim3(kScanNT), 0, st, op,
+                     n, bsum, nb, total);
 }
 
 // Common functor: exclusive scan of an int32 array into another.  The real
