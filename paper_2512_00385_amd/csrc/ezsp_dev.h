@@ -54,6 +54,8 @@ struct Ctl {
   Stripe e_next_s[kStripes];  // device side of e_next
   Stripe e_fwd_s[kStripes];   // device side of e_fwd
   Stripe maxabs_s[kStripes];  // max |e| bits from the fused gather
+  int32_t tail_nc[16];        // superpoints of every level the tail ended
+  int64_t tail_cut2[16];      // ... and 2 x their cut weight
 };
 
 __device__ __forceinline__ void stripe_add(Stripe *s, int32_t v) {

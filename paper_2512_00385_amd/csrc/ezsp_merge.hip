@@ -1455,6 +1455,8 @@ constexpr int kTailStart = 1500;    // default switch to the tail
 constexpr int kTailEdges = 1 << 16; // ... directed entries at the switch
 constexpr int kTailSlots = 1 << 18; // ... table slots at the switch
 constexpr int kTailLevels = 16;
+static_assert(sizeof(((Ctl *)nullptr)->tail_nc) == kTailLevels * 4,
+              "tail level counts travel in the control block");
 constexpr int kTailJumps = 64;
 
 struct TailState {
@@ -1869,9 +1871,8 @@ struct Bufs {
   int32_t nt;  // nodes the tail can start from
   double *tgain;    // per-slot gains in the tail
   int32_t tslots;   // entries of tgain
-  int32_t *Mt, *lvl_map, *lvl_minpt, *lvl_nc, *lvl_rank;
+  int32_t *Mt, *lvl_map, *lvl_minpt, *lvl_rank;
   double *lvl_mu;
-  long long *lvl_cut2;
   int32_t *bsum, *tmp;
   double *partial;
 };
@@ -1924,10 +1925,8 @@ void carve(Arena &a, int32_t n, int32_t d, int32_t k, Bufs *b) {
   b->tgain = a.take<double>(b->tslots);
   b->lvl_map = a.take<int32_t>((size_t)kTailLevels * b->nt);
   b->lvl_minpt = a.take<int32_t>((size_t)kTailLevels * b->nt);
-  b->lvl_nc = a.take<int32_t>(kTailLevels);
   b->lvl_rank = a.take<int32_t>((size_t)kTailLevels * b->nt);
   b->lvl_mu = a.take<double>((size_t)kTailLevels * b->nt * d);
-  b->lvl_cut2 = a.take<long long>(kTailLevels);
   b->bsum = a.take<int32_t>(scan_blocks(ed + n1) + 2);
   b->tmp = a.take<int32_t>(8);
   b->partial = a.take<double>(kEnergyBlocks);
@@ -2088,10 +2087,10 @@ int run_tail(const LadderArgs &g, const Bufs &b, const float *emb,
   t.Mt = b.Mt;
   t.lvl_map = b.lvl_map;
   t.lvl_minpt = b.lvl_minpt;
-  t.lvl_nc = b.lvl_nc;
+  t.lvl_nc = ctl->tail_nc;  // read back with the control block
   t.lvl_rank = b.lvl_rank;
   t.lvl_mu = b.lvl_mu;
-  t.lvl_cut2 = b.lvl_cut2;
+  t.lvl_cut2 = reinterpret_cast<long long *>(ctl->tail_cut2);
   t.nn0 = nn;
   t.ed0 = ed;
   t.cur0 = cur;
@@ -2126,19 +2125,12 @@ int run_tail(const LadderArgs &g, const Bufs &b, const float *emb,
   // labels straight from the snapshots (no host round trip in between);
   // on a device error they are discarded
   hipLaunchKernelGGL(k_tail_labels, blocks_for(n), dim3(256), 0, st, n, g.inv,
-                     b.M, b.lvl_map, b.lvl_rank, b.lvl_nc, nn, level0,
+                     b.M, b.lvl_map, b.lvl_rank, t.lvl_nc, nn, level0,
                      g.n_levels, g.labels, ctl);
-  int32_t nc[kTailLevels];
-  long long cut2[kTailLevels];
-  int rc = check_hip(hipMemcpyAsync(nc, b.lvl_nc, sizeof(nc),
-                                    hipMemcpyDeviceToHost, st),
-                     "hipMemcpyAsync(levels)");
-  if (!rc)
-    rc = check_hip(hipMemcpyAsync(cut2, b.lvl_cut2, sizeof(cut2),
-                                  hipMemcpyDeviceToHost, st),
-                   "hipMemcpyAsync(levels)");
-  if (!rc) rc = read_ctl(ctl, h, st);
+  int rc = read_ctl(ctl, h, st);
   if (rc) return rc;
+  const int32_t *nc = h->tail_nc;
+  const int64_t *cut2 = h->tail_cut2;
   if (h->err & kErrNotConv) {
     set_error("level %d reached max_rounds = %d", h->tail_level, max_rounds);
     return -6;
@@ -2381,9 +2373,9 @@ int ladder_run(const LadderArgs &g, Ctl *ctl, Arena &a, hipStream_t st) {
     }
   }
   if (tail_level >= 0) {
-    rc = run_tail(g, b, emb, adj, cur, nn, ed, tail_level, tail_round,
-                  max_rounds, ctl, h, st);
-    if (rc) return rc;
+    // the tail's own readback comes after its last kernel
+    return run_tail(g, b, emb, adj, cur, nn, ed, tail_level, tail_round,
+                    max_rounds, ctl, h, st);
   }
   if ((rc = read_ctl(ctl, h, st))) return rc;
   if (h->err) return status_from_err(h->err);
