@@ -616,20 +616,57 @@ __global__ __launch_bounds__(256) void k_jump(int32_t nn, int32_t *parent,
   __atomic_store_n(&parent[v], p, __ATOMIC_RELAXED);
 }
 
+// Roots numbered in node order; the pass also clears the member counters
+// of the next components (c < n_next <= nn).
 struct ScanRoots {
   const int32_t *parent;
   int32_t *newid;
+  int32_t *cnt;
   int32_t nn;
   __device__ int32_t value(int32_t v) const {
     return (v < nn && parent[v] == v) ? 1 : 0;
   }
   __device__ void emit(int32_t v, int32_t excl, int32_t val) const {
     if (val) newid[v] = excl;
+    if (v < nn) cnt[v] = 0;
   }
 };
 
-// Component of every node; also counts members (the rank is the node's
-// place among its component's members).
+// Window offsets of the next table (exclusive scan of the capacities, the
+// total at [len]) and the first component of every contraction chunk:
+// cstart[q] = the first c with toff[c] >= q * chunk, for q = 0 ..
+// ceil(slots / chunk).  Component i takes the q with q * chunk in
+// (toff[i], toff[i + 1]] (they start at component i + 1); q = 0 starts at 0
+// and a last partial chunk at len.
+struct ScanWindows {
+  const int32_t *cap;
+  int32_t *toff;
+  const int32_t *n_dev;
+  int32_t *cstart;
+  int32_t chunk, qcap;
+  Ctl *ctl;
+  __device__ int32_t value(int32_t i) const {
+    return (i < *n_dev) ? cap[i] : 0;
+  }
+  __device__ void put(int32_t q, int32_t c) const {
+    if ((uint32_t)q < (uint32_t)qcap) cstart[q] = c;
+    else raise_err(ctl, kErrInternal);
+  }
+  __device__ void emit(int32_t i, int32_t excl, int32_t v) const {
+    if (!ctl->any_choice) return;  // nothing merged: capacities are stale
+    const int32_t len = *n_dev;
+    if (i > len) return;
+    toff[i] = excl;
+    if (i == 0) put(0, 0);
+    if (i < len) {
+      for (int32_t q = excl / chunk + 1; q <= (excl + v) / chunk; ++q)
+        put(q, i + 1);
+    } else if (excl % chunk != 0) {
+      put(excl / chunk + 1, len);
+    }
+  }
+};
+
 // Component of every node and its place among the component's members.
 // Nodes of one component mostly sit together in node order, so the lanes
 // of a wave are grouped by component (ballot per distinct value) and each
@@ -675,13 +712,6 @@ __global__ __launch_bounds__(256) void k_assign(int32_t nn,
   if (act && lane == leader) base = atomicAdd(&cnt[c], __popcll(mine));
   base = __shfl(base, leader, kWave);
   if (act) rank[v] = base + __popcll(mine & ((1ull << lane) - 1));
-}
-
-__global__ __launch_bounds__(256) void k_zero_cnt(int32_t bound, const Ctl *ctl,
-                                                  int32_t *cnt) {
-  if (!ctl->any_choice) return;
-  const int32_t c = blockIdx.x * blockDim.x + threadIdx.x;
-  if (c < bound && c < ctl->n_next) cnt[c] = 0;
 }
 
 __global__ __launch_bounds__(256) void k_place(int32_t nn, const int32_t *L,
@@ -1023,26 +1053,6 @@ __device__ __forceinline__ void batch_find(const int32_t *pre, int32_t f,
   }
   slot = lo;
   j = f - pre[lo];
-}
-
-// First component of every chunk of the next table: cstart[q] is the first
-// c with toff[c] >= q * chunk, for q = 0 .. ceil(slots / chunk).  Component
-// c takes the q with q * chunk in (toff[c - 1], toff[c]]; c = nc takes the
-// rest (toff[nc] = slots), so every q is written exactly once.
-__global__ __launch_bounds__(256) void k_chunk_starts(
-    int32_t bound, const int32_t *__restrict__ toff, int32_t chunk,
-    int32_t *__restrict__ cstart, int32_t qcap, Ctl *ctl) {
-  if (!ctl->any_choice) return;
-  const int32_t nc = ctl->n_next;
-  const int32_t c = blockIdx.x * blockDim.x + threadIdx.x;
-  if (c > nc || c > bound) return;
-  const int32_t lo = c == 0 ? 0 : toff[c - 1] / chunk + 1;
-  int32_t hi = c == nc ? (toff[nc] + chunk - 1) / chunk : toff[c] / chunk;
-  if (hi >= qcap) {
-    raise_err(ctl, kErrInternal);
-    hi = qcap - 1;
-  }
-  for (int32_t q = lo; q <= hi; ++q) cstart[q] = c;
 }
 
 template <bool FIRST>
@@ -1991,9 +2001,8 @@ void launch_round(const Bufs &b, const Adj &adj, int cur, int32_t n,
                      b.parent, ctl);
   hipLaunchKernelGGL(k_jump, blocks_for(nn), dim3(256), 0, st, nn, b.parent,
                      ctl);
-  device_scan(ScanRoots{b.parent, b.newid, nn}, nn, b.bsum, &ctl->n_next, st);
-  hipLaunchKernelGGL(k_zero_cnt, blocks_for(nn), dim3(256), 0, st, nn, ctl,
-                     b.cnt);
+  device_scan(ScanRoots{b.parent, b.newid, b.cnt, nn}, nn, b.bsum,
+              &ctl->n_next, st);
   hipLaunchKernelGGL(k_assign, xblocks_for(nn), dim3(256), 0, st, nn,
                      b.parent, b.newid, b.L, b.cnt, b.rank, ctl);
   prof_end(st);
@@ -2022,10 +2031,9 @@ void launch_round(const Bufs &b, const Adj &adj, int cur, int32_t n,
                      b.mem, b.moff, s, b.deg, d, o, b.big, ctl);
   prof_end(st);
   prof_begin("contract", st);
-  device_scan(ScanArray{b.capn, b.ws[nxt], nn, &ctl->n_next}, nn + 1, b.bsum,
-              &ctl->slots, st);
-  hipLaunchKernelGGL(k_chunk_starts, blocks_for((int64_t)nn + 1), dim3(256), 0,
-                     st, nn, b.ws[nxt], chunk, b.cstart, b.qcap, ctl);
+  device_scan(ScanWindows{b.capn, b.ws[nxt], &ctl->n_next, b.cstart, chunk,
+                          b.qcap, ctl},
+              nn + 1, b.bsum, &ctl->slots, st);
   hipLaunchKernelGGL(k_contract_chunk<FIRST>,
                      dim3(xcd_grid((ed + chunk - 1) / chunk)), dim3(256), 0,
                      st, nn, adj, b.L, b.mem, b.moff, b.ws[nxt], b.capn,
