@@ -98,6 +98,8 @@ int run_partition(const float *xyz, const int32_t *nbr_in, const float *emb,
         "knn launch");
     if (rc) return rc;
     g.nbr = w.nbr_int;
+    g.pts = w.pts;
+    g.kth = w.kth;
     g.perm = w.perm;
     g.inv = w.inv;
     g.check_nbr = false;

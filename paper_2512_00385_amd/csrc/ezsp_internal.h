@@ -98,6 +98,7 @@ struct KnnWork {
   uint64_t *keys = nullptr, *keys2 = nullptr;
   uint32_t *vals = nullptr, *vals2 = nullptr;
   float4 *pts = nullptr, *blo = nullptr, *bhi = nullptr;
+  uint64_t *kth = nullptr;     // n: every point's k-th key (d2 bits, index)
   int32_t *hist = nullptr, *bsum = nullptr, *total = nullptr;
 };
 void knn_reserve(Arena &a, int32_t n, int32_t k, KnnWork *w);
@@ -109,6 +110,8 @@ hipError_t knn_launch(const float *xyz, int32_t n, int32_t k, Ctl *ctl,
 // when internal == original order).
 struct LadderArgs {
   const int32_t *nbr;   // n rows: stride pad4(k), or k when check_nbr
+  const float4 *pts;    // nullable: points in internal order (x, y, z, index)
+  const uint64_t *kth;  // nullable: each point's k-th key from the kNN
   const int32_t *perm;  // nullable
   const int32_t *inv;   // nullable
   const float *emb;     // n*d, caller order

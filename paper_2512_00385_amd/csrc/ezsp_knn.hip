@@ -309,7 +309,7 @@ __global__ __launch_bounds__(256) void k_knn_query(
     int32_t n, const float4 *__restrict__ blo, const float4 *__restrict__ bhi,
     Tree tree, int32_t k, int32_t *__restrict__ nbr_int,
     int32_t *__restrict__ nbr_out, float *__restrict__ d2_out,
-    int32_t n_blocks) {
+    uint64_t *__restrict__ kth_out, int32_t n_blocks) {
   const int32_t lb = xcd_block();
   if (lb >= n_blocks) return;
   const int lane16 = threadIdx.x & (kBucket - 1);
@@ -379,6 +379,11 @@ __global__ __launch_bounds__(256) void k_knn_query(
 
   if (!act) return;
   const int32_t kp = pad4(k);
+  // the k-th key (kNoKey when fewer than k points exist): later, q is among
+  // p's neighbours exactly when q's key as seen from p does not exceed it
+#pragma unroll
+  for (int t = 0; t < K; ++t)
+    if (t == k - 1) kth_out[i] = key[t];
 #pragma unroll
   for (int t = 0; t < K; ++t) {
     if (t < k) {
@@ -414,6 +419,7 @@ void knn_reserve(Arena &a, int32_t n, int32_t k, KnnWork *w) {
   w->vals = a.take<uint32_t>(n);
   w->vals2 = a.take<uint32_t>(n);
   w->pts = a.take<float4>(n);
+  w->kth = a.take<uint64_t>(n);
   w->blo = a.take<float4>(t.total);
   w->bhi = a.take<float4>(t.total);
   w->hist = a.take<int32_t>(radix_hist_ints(n));
@@ -454,7 +460,7 @@ hipError_t knn_launch(const float *xyz, int32_t n, int32_t k, Ctl *ctl,
     hipLaunchKernelGGL(k_knn_query<KK>, grid, dim3(nt), 0, st, s.pts, w.inv, \
                        n,                                                    \
                        s.blo, s.bhi, tree, k, w.nbr_int, nbr_out, d2_out,    \
-                       qblocks);                                             \
+                       w.kth, qblocks);                                      \
     break;
     EZSP_KNN_CASE(4)
     EZSP_KNN_CASE(8)

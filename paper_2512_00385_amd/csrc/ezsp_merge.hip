@@ -190,6 +190,42 @@ __global__ __launch_bounds__(256) void k_rev_count(const int32_t *nbr,
   if ((threadIdx.x & (kWave - 1)) == 0 && fwd) stripe_add(ctl->e_fwd_s, fwd);
 }
 
+// The same count when the table came from this library's kNN: u lists i
+// exactly when i's key as seen from u, (d2 bits, original index) with d2 in
+// the kNN's own operation order, does not exceed u's k-th key.  That needs
+// u's point and k-th key (24 bytes) instead of u's whole row.
+__global__ __launch_bounds__(256) void k_rev_count_kth(
+    const int32_t *nbr, int32_t n, int32_t k, const float4 *__restrict__ pts,
+    const uint64_t *__restrict__ kth, int32_t *rev, uint64_t *nmask,
+    Ctl *ctl) {
+  const int32_t i = xcd_tid();
+  const int32_t kp = pad4(k);
+  int32_t fwd = 0;
+  if (i < n) {
+    const int32_t *r = nbr + (int64_t)i * kp;
+    const float4 pi = pts[i];
+    uint64_t mask = 0;
+#pragma unroll 4
+    for (int32_t t = 0; t < k; ++t) {
+      const int32_t u = r[t];
+      if (u < 0) continue;
+      ++fwd;
+      const float4 pu = pts[u];
+      const float dx = pi.x - pu.x, dy = pi.y - pu.y, dz = pi.z - pu.z;
+      const float xx = dx * dx, yy = dy * dy, zz = dz * dz;
+      const float d2 = (xx + yy) + zz;
+      const uint64_t key = ((uint64_t)__float_as_uint(d2) << 32) |
+                           (uint32_t)__float_as_int(pi.w);
+      if (key > kth[u]) mask |= 1ull << t;
+    }
+    nmask[i] = mask;
+    for (uint64_t m = mask; m; m &= m - 1)
+      atomicAdd(&rev[r[__builtin_ctzll(m)]], 1);
+  }
+  fwd = wave_sum(fwd);
+  if ((threadIdx.x & (kWave - 1)) == 0 && fwd) stripe_add(ctl->e_fwd_s, fwd);
+}
+
 __global__ __launch_bounds__(256) void k_rev_fill(const int32_t *nbr,
                                                   int32_t n, int32_t k,
                                                   const uint64_t *nmask,
@@ -2231,8 +2267,12 @@ int ladder_run(const LadderArgs &g, Ctl *ctl, Arena &a, hipStream_t st) {
                      (int64_t)n, 0);
   hipLaunchKernelGGL(k_fill_i32, blocks_for(n), dim3(256), 0, st, b.cursor,
                      (int64_t)n, 0);
-  hipLaunchKernelGGL(k_rev_count, xblocks_for(n), dim3(256), 0, st, nbr, n, k,
-                     b.rev, b.nmask, ctl);
+  if (g.kth && g.pts)
+    hipLaunchKernelGGL(k_rev_count_kth, xblocks_for(n), dim3(256), 0, st, nbr,
+                       n, k, g.pts, g.kth, b.rev, b.nmask, ctl);
+  else
+    hipLaunchKernelGGL(k_rev_count, xblocks_for(n), dim3(256), 0, st, nbr, n,
+                       k, b.rev, b.nmask, ctl);
   device_scan(ScanArray{b.rev, b.rrp, n, nullptr}, n + 1, b.bsum, &ctl->e_rev,
               st);
   hipLaunchKernelGGL(k_rev_fill, xblocks_for(n), dim3(256), 0, st, nbr, n, k,
