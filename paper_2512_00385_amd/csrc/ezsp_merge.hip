@@ -1496,7 +1496,7 @@ __global__ void k_energy_reset(Ctl *ctl) {
 // weight.
 // ---------------------------------------------------------------------------
 constexpr int kTailNT = 1024;
-constexpr int kTailNodes = 1536;    // largest graph the tail can take (LDS)
+constexpr int kTailNodes = 4096;    // largest graph the tail can take (LDS)
 constexpr int kTailStart = 1500;    // default switch to the tail
 constexpr int kTailEdges = 1 << 16; // ... directed entries at the switch
 constexpr int kTailSlots = 1 << 18; // ... table slots at the switch
@@ -1517,7 +1517,7 @@ struct TailState {
   int32_t *lvl_rank;                       // kTailLevels x nn0
   double *lvl_mu;                          // kTailLevels x nn0 x d
   long long *lvl_cut2;                     // kTailLevels
-  int32_t nn0, ed0, cur0, d, tcap, gcap, n_levels, level0, round0,
+  int32_t nn0, ed0, cur0, tcur0, d, tcap, gcap, n_levels, level0, round0,
       max_rounds;
   int32_t want_energy;
   double lambda[kTailLevels];
@@ -1621,13 +1621,14 @@ __global__ __launch_bounds__(kTailNT) void k_tail(TailState t, Ctl *ctl) {
   int32_t *s_aux = reinterpret_cast<int32_t *>(s_key);  // 2 kTailNodes + 2
   int32_t *s_newid = s_aux, *s_cap = s_aux + kTailNodes + 1;
   int32_t *s_ws = s_wsa, *s_wn = s_wsb;  // current / next row starts
-  int32_t nn = t.nn0, ed = t.ed0, cur = t.cur0;
+  // cur: node state, tc: table (they may start on different buffers)
+  int32_t nn = t.nn0, ed = t.ed0, cur = t.cur0, tc = t.tcur0;
   if (nn > kTailNodes || nn < 1) {
     if (threadIdx.x == 0) raise_err(ctl, kErrInternal);
     return;
   }
   for (int32_t i = threadIdx.x; i <= nn; i += kTailNT) {
-    s_ws[i] = t.ws[cur][i];
+    s_ws[i] = t.ws[tc][i];
     if (i < nn) t.Mt[i] = i;
   }
   __syncthreads();
@@ -1636,7 +1637,7 @@ __global__ __launch_bounds__(kTailNT) void k_tail(TailState t, Ctl *ctl) {
   // rest so that every slot is either an entry or empty
   for (int32_t q = threadIdx.x; q < Q; q += kTailNT) {
     const int32_t v = tail_row(s_ws, nn, q);
-    if (q - s_ws[v] >= t.wl[cur][v]) t.tbl[cur][q] = kEmpty;
+    if (q - s_ws[v] >= t.wl[tc][v]) t.tbl[tc][q] = kEmpty;
   }
   __syncthreads();
   for (int32_t l = t.level0; l < t.n_levels; ++l) {
@@ -1652,7 +1653,7 @@ __global__ __launch_bounds__(kTailNT) void k_tail(TailState t, Ctl *ctl) {
         return;
       }
       const int nxt = 1 - cur;
-      const uint64_t *tb = t.tbl[cur];
+      const uint64_t *tb = t.tbl[tc];
       NodeIn s;
       s.size = t.size[cur];
       s.S = t.S[cur];
@@ -1791,7 +1792,7 @@ __global__ __launch_bounds__(kTailNT) void k_tail(TailState t, Ctl *ctl) {
         return;
       }
       for (int32_t q = threadIdx.x; q < slots; q += kTailNT)
-        t.tbl[nxt][q] = kEmpty;
+        t.tbl[1 - tc][q] = kEmpty;
       if (threadIdx.x == 0) s_claims = 0;
       __syncthreads();
       // Step 4 contraction, a thread per entry
@@ -1802,7 +1803,7 @@ __global__ __launch_bounds__(kTailNT) void k_tail(TailState t, Ctl *ctl) {
         const int32_t v = tail_row(s_ws, nn, q);
         const int32_t A = s_L[v], B = s_L[(int32_t)(e >> 32)];
         if (A == B) continue;  // edge inside a merged component
-        claims += tail_table_add(t.tbl[nxt], s_wn[A], s_cap[A], B,
+        claims += tail_table_add(t.tbl[1 - tc], s_wn[A], s_cap[A], B,
                                  (int32_t)(uint32_t)e, ctl)
                       ? 1
                       : 0;
@@ -1816,6 +1817,7 @@ __global__ __launch_bounds__(kTailNT) void k_tail(TailState t, Ctl *ctl) {
       nn = C;
       Q = slots;
       cur = nxt;
+      tc = 1 - tc;
       int32_t *sw = s_ws;
       s_ws = s_wn;
       s_wn = sw;
@@ -1857,7 +1859,7 @@ __global__ __launch_bounds__(kTailNT) void k_tail(TailState t, Ctl *ctl) {
         t.lvl_mu[(int64_t)l * t.nn0 * d + q] = t.mu[q];
       long long acc = 0;
       for (int32_t q = threadIdx.x; q < Q; q += kTailNT) {
-        const uint64_t e = t.tbl[cur][q];
+        const uint64_t e = t.tbl[tc][q];
         if (e != kEmpty) acc += (int32_t)(uint32_t)e;
       }
       acc = wave_sum(acc);
@@ -1892,6 +1894,21 @@ __global__ __launch_bounds__(256) void k_tail_labels(
     if (out < 0) raise_err(ctl, kErrInternal);
     labels[(int64_t)l * n + p] = out;
   }
+}
+
+// Rows of the table the tail starts from, packed end to end (the windows of
+// the multi-kernel path hold their rows at the front and may be larger).
+__global__ __launch_bounds__(256) void k_repack(
+    int32_t nn, const int32_t *__restrict__ ws, const int32_t *__restrict__ wl,
+    const uint64_t *__restrict__ tbl, const int32_t *__restrict__ ws2,
+    int32_t *__restrict__ wl2, uint64_t *__restrict__ tbl2) {
+  const int32_t v = blockIdx.x * blockDim.x + threadIdx.x;
+  if (v >= nn) return;
+  const int32_t len = wl[v];
+  const uint64_t *src = tbl + ws[v];
+  uint64_t *dst = tbl2 + ws2[v];
+  for (int32_t j = 0; j < len; ++j) dst[j] = src[j];
+  wl2[v] = len;
 }
 
 // ---------------------------------------------------------------------------
@@ -2138,6 +2155,14 @@ int run_tail(const LadderArgs &g, const Bufs &b, const float *emb,
   t.nn0 = nn;
   t.ed0 = ed;
   t.cur0 = cur;
+  // the table goes to the other buffer, its rows packed: the tail's passes
+  // run over the entries only
+  const int nxt = 1 - cur;
+  device_scan(ScanArray{b.wl[cur], b.ws[nxt], nn, nullptr}, nn + 1, b.bsum,
+              b.tmp, st);
+  hipLaunchKernelGGL(k_repack, blocks_for(nn), dim3(256), 0, st, nn, b.ws[cur],
+                     b.wl[cur], b.tbl[cur], b.ws[nxt], b.wl[nxt], b.tbl[nxt]);
+  t.tcur0 = nxt;
   t.d = d;
   t.tcap = (int32_t)edge_bound(n, g.k);
   t.gcap = b.tslots;
