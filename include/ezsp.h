@@ -111,7 +111,8 @@ size_t ezsp_partition_workspace_size(int64_t n, int32_t d,
  * depend on summation order.  Conflict removal keeps, per component, the
  * candidate edge with the largest gain, ties to the smaller neighbour (in the
  * order of smallest point index).
- * Errors: INVALID_ARG, NONFINITE, RANGE (F < 16), WORKSPACE, DEVICE,
+ * Errors: INVALID_ARG (also when 4*k*n >= 2^31: the adjacency tables are
+ *         int32-indexed), NONFINITE, RANGE (F < 16), WORKSPACE, DEVICE,
  *         NOT_CONVERGED. */
 int ezsp_partition(const float *xyz, const float *emb, int64_t n, int32_t d,
                    const ezsp_params *p, int32_t *labels, int64_t *n_comp,

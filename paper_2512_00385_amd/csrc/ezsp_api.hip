@@ -38,9 +38,10 @@ int fail(int code, const char *msg) {
 
 bool n_ok(int64_t n) { return n >= 1 && n < kMaxN; }
 
-// Graph arrays are indexed with int32: 2*k*n directed entries must fit.
+// Graph tables are indexed with int32: 2*k*n directed entries, and windows
+// of up to twice that, must fit.
 bool edges_ok(int64_t n, int32_t k) {
-  return 2 * n * (int64_t)k < kMaxN - 1;
+  return 4 * n * (int64_t)k < kMaxN - 1;
 }
 
 int check_params(int64_t n, int32_t d, const ezsp_params *p) {
@@ -50,7 +51,7 @@ int check_params(int64_t n, int32_t d, const ezsp_params *p) {
   if (p->k < 1 || p->k > 64)
     return fail(EZSP_ERR_INVALID_ARG, "k must be in 1..64");
   if (!edges_ok(n, p->k))
-    return fail(EZSP_ERR_INVALID_ARG, "2*k*n must stay below 2^31");
+    return fail(EZSP_ERR_INVALID_ARG, "4*k*n must stay below 2^31");
   if ((int64_t)n * d >= kMaxN)
     return fail(EZSP_ERR_INVALID_ARG, "n*d must stay below 2^31");
   if (p->n_levels < 1 || p->n_levels > 16)

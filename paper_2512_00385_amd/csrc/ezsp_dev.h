@@ -40,7 +40,8 @@ struct Ctl {
   int32_t e_next;       // directed edges after this round (host: folded)
   int32_t slots;        // adjacency-table slots of the next round
   uint32_t maxabs_bits; // max |e| as fp32 bits (monotone for >= 0)
-  int32_t n_long;       // nodes whose row goes to the block-per-row kernels
+  int32_t n_long;       // rows longer than a short-row group takes
+  int32_t n_lchunk;     // entry chunks of those rows
   int32_t bbox_enc[6];  // min xyz, max xyz in order-preserving int form
   int32_t n_big;        // components that go to the block-per-component path
   int32_t e_rev;        // reverse-only entries of the first-round graph

@@ -47,10 +47,10 @@ namespace ezsp {
 
 constexpr uint64_t kEmpty = ~0ull;
 constexpr int kJumpCap = 1 << 16;
-constexpr int kLongRow = 128;   // rows longer than this: one wave per row
-constexpr int kLongGrid = 2048; // blocks of 4 waves for the long rows
+constexpr int kLongRow = 128;    // longer rows go in entry chunks ...
+constexpr int kLongChunk = 1024; // ... of this many entries, a wave each
+constexpr int kLongGrid = 2048;  // blocks of 4 waves for the chunks
 constexpr int kBigComp = 128;   // components with more members: one block
-constexpr int kWaveRowsMax = 65536;  // rounds this small: a wave per row
 constexpr int kSelLanesFirst = 2;  // lanes per row in the first round's select
 constexpr int kSelLanes = 4;       // ... in later rounds
 constexpr int kStatsLanes = 4;     // lanes per component in the statistics
@@ -378,6 +378,7 @@ __global__ void k_round_init(Ctl *ctl) {
     ctl->e_next = 0;
     ctl->slots = 0;
     ctl->n_long = 0;
+    ctl->n_lchunk = 0;
     ctl->n_big = 0;
     ctl->n_cbig = 0;
     ctl->n_tiles = 0;
@@ -491,6 +492,17 @@ __device__ __forceinline__ double edge_gain_t(const NodeIn &s,
   }
 }
 
+// Long rows: every row longer than kLongRow is split into chunks of
+// kLongChunk entries; chunk item i belongs to long row item[i], which starts
+// at chunk base[slot] and has nch[slot] chunks.  Per chunk: the best
+// candidate (g, mp, u) and the count of valid entries.
+struct LongWork {
+  int32_t *rows, *base, *nch, *item;
+  double *g;
+  int32_t *mp, *u, *cnt;
+  int32_t cap;  // chunk items available
+};
+
 // Steps 1-2 for rows of up to kLongRow entries, G lanes per row: the lanes
 // take every G-th entry of the row (shorter dependent chains per lane than
 // a thread per row, and a wave waits for its longest rows only G-fold
@@ -498,16 +510,25 @@ __device__ __forceinline__ double edge_gain_t(const NodeIn &s,
 template <bool FIRST, int DT, int G>
 __global__ __launch_bounds__(256) void k_select(
     int32_t nn, Adj a, NodeIn s, int32_t d, double lambda, int64_t smin,
-    int32_t *__restrict__ target, int32_t *__restrict__ deg,
-    int32_t *__restrict__ long_rows, Ctl *ctl) {
+    int32_t *__restrict__ target, int32_t *__restrict__ deg, LongWork lw,
+    Ctl *ctl) {
   const int32_t tid = xcd_tid();
   const int32_t v = tid / G;
   const int lg = tid & (G - 1);
-  const bool live = v < nn && row_span<FIRST>(a, v) <= kLongRow;
-  if (v < nn && !live && lg == 0) {  // a whole block takes this row
+  const int32_t span = v < nn ? row_span<FIRST>(a, v) : 0;
+  const bool live = v < nn && span <= kLongRow;
+  if (v < nn && !live && lg == 0) {  // listed with its chunks
+    const int32_t nch = (span + kLongChunk - 1) / kLongChunk;
     const int32_t slot = atomicAdd(&ctl->n_long, 1);
-    if (slot < nn) long_rows[slot] = v;
-    else raise_err(ctl, kErrInternal);
+    const int32_t base = atomicAdd(&ctl->n_lchunk, nch);
+    if (slot < nn && base + nch <= lw.cap) {
+      lw.rows[slot] = v;
+      lw.base[slot] = base;
+      lw.nch[slot] = nch;
+      for (int32_t c = 0; c < nch; ++c) lw.item[base + c] = slot;
+    } else {
+      raise_err(ctl, kErrInternal);
+    }
   }
   Best b{0.0, 0, -1};
   int32_t cnt = 0;
@@ -552,24 +573,28 @@ __global__ __launch_bounds__(256) void k_select(
     ctl->any_choice = 1;
 }
 
+// Steps 1-2 over the chunks of the long rows, a wave per chunk.
 template <bool FIRST, int DT>
 __global__ __launch_bounds__(256) void k_select_long(
     int32_t nn, Adj a, NodeIn s, int32_t d, double lambda, int64_t smin,
-    int32_t *__restrict__ target, int32_t *__restrict__ deg,
-    const int32_t *__restrict__ long_rows, bool all_rows, Ctl *ctl) {
-  const int32_t n_long = all_rows ? nn : ctl->n_long;
+    LongWork lw, Ctl *ctl) {
+  const int32_t n_items = ctl->n_lchunk;
   const int F = ctl->F;
   const double sF = ldexp(1.0, F), sIF = ldexp(1.0, -F);
   const int lane = threadIdx.x & (kWave - 1);
   const int32_t wave0 = (int32_t)(blockIdx.x * (blockDim.x / kWave) +
                                   threadIdx.x / kWave);
   const int32_t nwaves = (int32_t)(gridDim.x * (blockDim.x / kWave));
-  for (int32_t li = wave0; li < n_long; li += nwaves) {
-    const int32_t v = all_rows ? li : long_rows[li];
+  for (int32_t it = wave0; it < n_items; it += nwaves) {
+    const int32_t slot = lw.item[it];
+    const int32_t v = lw.rows[slot];
     if ((uint32_t)v >= (uint32_t)nn) {
       raise_err(ctl, kErrInternal);
       continue;
     }
+    const int32_t j0 = (it - lw.base[slot]) * kLongChunk;
+    const int32_t j1 = min(row_span<FIRST>(a, v), j0 + kLongChunk);
+    const int32_t rb = row_base<FIRST>(a, v);
     const int32_t sv = node_size<FIRST>(s, v);
     const double dsv = (double)sv;
     const bool small = (int64_t)sv < smin;
@@ -577,11 +602,13 @@ __global__ __launch_bounds__(256) void k_select_long(
     mv.load(s, v, sF, sIF);
     Best b{0.0, 0, -1};
     int32_t cnt = 0;
-    for_row<FIRST>(a, v, lane, kWave, [&](int32_t u, int32_t w) {
+    for (int32_t j = j0 + lane; j < j1; j += kWave) {
+      int32_t u, w;
+      if (!row_entry_at<FIRST>(a, v, rb, j, u, w)) continue;
       ++cnt;
       if ((uint32_t)u >= (uint32_t)nn) {
         raise_err(ctl, kErrInternal);
-        return;
+        continue;
       }
       const double g =
           edge_gain_t<FIRST, DT>(s, mv, v, dsv, u, w, d, lambda, sF, sIF);
@@ -589,7 +616,7 @@ __global__ __launch_bounds__(256) void k_select_long(
         const Best c{g, node_minpt<FIRST>(s, u), u};
         if (best_before(c, b)) b = c;
       }
-    });
+    }
     cnt = wave_sum(cnt);
 #pragma unroll
     for (int off = kWave / 2; off > 0; off >>= 1) {
@@ -600,10 +627,33 @@ __global__ __launch_bounds__(256) void k_select_long(
       if (best_before(o, b)) b = o;
     }
     if (lane == 0) {
-      target[v] = b.u;
-      deg[v] = cnt;
-      if (b.u >= 0) ctl->any_choice = 1;
+      lw.g[it] = b.g;
+      lw.mp[it] = b.mp;
+      lw.u[it] = b.u;
+      lw.cnt[it] = cnt;
     }
+  }
+}
+
+// The long rows' choices from their chunks (same order as best_before).
+__global__ __launch_bounds__(256) void k_select_combine(
+    LongWork lw, int32_t *__restrict__ target, int32_t *__restrict__ deg,
+    Ctl *ctl) {
+  const int32_t n_long = ctl->n_long;
+  for (int32_t slot = blockIdx.x * blockDim.x + threadIdx.x; slot < n_long;
+       slot += gridDim.x * blockDim.x) {
+    const int32_t b0 = lw.base[slot], nch = lw.nch[slot];
+    Best b{0.0, 0, -1};
+    int32_t cnt = 0;
+    for (int32_t c = b0; c < b0 + nch; ++c) {
+      const Best o{lw.g[c], lw.mp[c], lw.u[c]};
+      if (best_before(o, b)) b = o;
+      cnt += lw.cnt[c];
+    }
+    const int32_t v = lw.rows[slot];
+    target[v] = b.u;
+    deg[v] = cnt;
+    if (b.u >= 0) ctl->any_choice = 1;
   }
 }
 
@@ -783,9 +833,12 @@ struct NodeOut {
 
 // Records the window of component c; a window larger than a chunk goes to
 // the global path, split into tiles of kBatch members.
+// A window larger than an LDS chunk is filled with global atomics: it gets
+// twice its summed degree, so open addressing stays at load factor <= 1/2.
 __device__ __forceinline__ void note_window(const NodeOut &o, int32_t c,
                                             int32_t cap, int32_t members,
                                             Ctl *ctl) {
+  if (cap > o.chunk) cap *= 2;
   o.cap[c] = cap;
   o.wl[c] = cap;
   if (cap > o.chunk) {
@@ -1107,116 +1160,120 @@ __global__ __launch_bounds__(256) void k_contract_chunk(
   __shared__ int32_t bbase[kBatch];
   __shared__ int32_t wsum[256 / kWave];
   if (!ctl->any_choice) return;
-  const int32_t q = xcd_block();
-  const int32_t j0 = q * chunk;
-  if (j0 >= ctl->slots) return;
-  // components whose windows start in [j0, j0 + chunk)
-  const int32_t c_lo = cstart[q], c_hi = cstart[q + 1];
-  for (int t = threadIdx.x; t < 2 * chunk; t += blockDim.x) {
-    kb[t] = -1;
-    kw[t] = 0;
-  }
-  __syncthreads();
-  const int32_t m_lo = moff[c_lo];
-  // a window larger than a chunk can only be the last one starting here
-  // (the next window starts past the chunk); its members are not walked
-  const int32_t m_hi =
-      (c_hi > c_lo && cap[c_hi - 1] > chunk) ? moff[c_hi - 1] : moff[c_hi];
-  constexpr int kUnroll = 4;  // entries per thread with their loads in flight
-  for (int32_t b0 = m_lo; b0 < m_hi; b0 += kBatch) {
-    const int32_t idx = b0 + (int32_t)threadIdx.x;
-    int32_t span = 0;
-    if (idx < m_hi) {
-      const int32_t m = mem[idx];
-      // the row's span and base depend on m only: loaded with L[m]
-      const int32_t sp = row_span<FIRST>(a, m);
-      const int32_t rb = row_base<FIRST>(a, m);
-      const int32_t A = L[m];
-      const int32_t cp = cap[A];
-      const int32_t lb = toff[A] - j0;
-      if (cp > 0 && cp <= chunk) {
-        if (lb < 0 || lb + cp > 2 * chunk) {
-          raise_err(ctl, kErrInternal);
-        } else {
-          span = sp;
-          bm[threadIdx.x] = m;
-          bA[threadIdx.x] = A;
-          blb[threadIdx.x] = lb;
-          bcp[threadIdx.x] = cp;
-          bbase[threadIdx.x] = rb;
-        }
-      }
-    }
-    int32_t total;
-    pre[threadIdx.x] = block_excl_scan<256>(span, wsum, &total);
-    if (threadIdx.x == 0) pre[kBatch] = total;
-    __syncthreads();
-    for (int32_t f0 = threadIdx.x; f0 < total; f0 += kUnroll * 256) {
-      int32_t slot[kUnroll], u[kUnroll], w[kUnroll], B[kUnroll];
-      bool ok[kUnroll];
-#pragma unroll
-      for (int e = 0; e < kUnroll; ++e) {
-        const int32_t f = f0 + e * 256;
-        ok[e] = false;
-        if (f < total) {
-          int32_t j;
-          batch_find(pre, f, slot[e], j);
-          ok[e] = row_entry_at<FIRST>(a, bm[slot[e]], bbase[slot[e]], j, u[e],
-                                      w[e]);
-        }
-      }
-#pragma unroll
-      for (int e = 0; e < kUnroll; ++e) {
-        if (ok[e] && (uint32_t)u[e] >= (uint32_t)nn) {
-          raise_err(ctl, kErrInternal);
-          ok[e] = false;
-        }
-        B[e] = ok[e] ? L[u[e]] : -1;
-      }
-#pragma unroll
-      for (int e = 0; e < kUnroll; ++e) {
-        const int32_t A = ok[e] ? bA[slot[e]] : -1;
-        if (!ok[e] || A == B[e]) continue;  // edge inside a merged component
-        const int32_t lb = blb[slot[e]], cp = bcp[slot[e]];
-        uint32_t h = ((uint32_t)B[e] * 2654435761u) % (uint32_t)cp;
-        int32_t probe = 0;
-        for (; probe < cp; ++probe) {
-          const int32_t old = atomicCAS(&kb[lb + h], -1, B[e]);
-          if (old == -1 || old == B[e]) {
-            atomicAdd(&kw[lb + h], w[e]);
-            break;
-          }
-          h = (h + 1 == (uint32_t)cp) ? 0u : h + 1;
-        }
-        if (probe == cp) raise_err(ctl, kErrInternal);
-      }
-    }
-    __syncthreads();
-  }
-  // rows compacted to the start of their windows, a wave per window:
-  // occupied slots ranked by ballot, written in slot order
+  // chunks q = this block's, then every gridDim.x-th: the grid is sized for
+  // the entries, the windows may span up to twice as many slots
+  const int32_t slots = ctl->slots;
   const int lane = threadIdx.x & (kWave - 1);
   const uint64_t below = (1ull << lane) - 1;
   int32_t uniq = 0;
-  for (int32_t c = c_lo + (int32_t)threadIdx.x / kWave; c < c_hi;
-       c += blockDim.x / kWave) {
-    const int32_t cp = cap[c];
-    if (cp <= 0 || cp > chunk) continue;
-    const int32_t base = toff[c], lb = base - j0;
-    int32_t out = 0;
-    for (int32_t t0 = 0; t0 < cp; t0 += kWave) {
-      const int32_t t = t0 + lane;
-      const int32_t B = t < cp ? kb[lb + t] : -1;
-      const uint64_t occ = __ballot(B >= 0);
-      if (B >= 0)
-        tbl[base + out + __popcll(occ & below)] =
-            ((uint64_t)(uint32_t)B << 32) | (uint32_t)kw[lb + t];
-      out += __popcll(occ);
+  for (int32_t q = xcd_block(); (int64_t)q * chunk < slots; q += gridDim.x) {
+    const int32_t j0 = q * chunk;
+    // components whose windows start in [j0, j0 + chunk)
+    const int32_t c_lo = cstart[q], c_hi = cstart[q + 1];
+    for (int t = threadIdx.x; t < 2 * chunk; t += blockDim.x) {
+      kb[t] = -1;
+      kw[t] = 0;
     }
-    if (lane == 0) {
-      wl[c] = out;
-      uniq += out;
+    __syncthreads();
+    const int32_t m_lo = moff[c_lo];
+    // a window larger than a chunk can only be the last one starting here
+    // (the next window starts past the chunk); its members are not walked
+    const int32_t m_hi =
+        (c_hi > c_lo && cap[c_hi - 1] > chunk) ? moff[c_hi - 1] : moff[c_hi];
+    constexpr int kUnroll = 4;  // entries per thread with their loads in flight
+    for (int32_t b0 = m_lo; b0 < m_hi; b0 += kBatch) {
+      const int32_t idx = b0 + (int32_t)threadIdx.x;
+      int32_t span = 0;
+      if (idx < m_hi) {
+        const int32_t m = mem[idx];
+        // the row's span and base depend on m only: loaded with L[m]
+        const int32_t sp = row_span<FIRST>(a, m);
+        const int32_t rb = row_base<FIRST>(a, m);
+        const int32_t A = L[m];
+        const int32_t cp = cap[A];
+        const int32_t lb = toff[A] - j0;
+        if (cp > 0 && cp <= chunk) {
+          if (lb < 0 || lb + cp > 2 * chunk) {
+            raise_err(ctl, kErrInternal);
+          } else {
+            span = sp;
+            bm[threadIdx.x] = m;
+            bA[threadIdx.x] = A;
+            blb[threadIdx.x] = lb;
+            bcp[threadIdx.x] = cp;
+            bbase[threadIdx.x] = rb;
+          }
+        }
+      }
+      int32_t total;
+      pre[threadIdx.x] = block_excl_scan<256>(span, wsum, &total);
+      if (threadIdx.x == 0) pre[kBatch] = total;
+      __syncthreads();
+      for (int32_t f0 = threadIdx.x; f0 < total; f0 += kUnroll * 256) {
+        int32_t slot[kUnroll], u[kUnroll], w[kUnroll], B[kUnroll];
+        bool ok[kUnroll];
+  #pragma unroll
+        for (int e = 0; e < kUnroll; ++e) {
+          const int32_t f = f0 + e * 256;
+          ok[e] = false;
+          if (f < total) {
+            int32_t j;
+            batch_find(pre, f, slot[e], j);
+            ok[e] = row_entry_at<FIRST>(a, bm[slot[e]], bbase[slot[e]], j, u[e],
+                                        w[e]);
+          }
+        }
+  #pragma unroll
+        for (int e = 0; e < kUnroll; ++e) {
+          if (ok[e] && (uint32_t)u[e] >= (uint32_t)nn) {
+            raise_err(ctl, kErrInternal);
+            ok[e] = false;
+          }
+          B[e] = ok[e] ? L[u[e]] : -1;
+        }
+  #pragma unroll
+        for (int e = 0; e < kUnroll; ++e) {
+          const int32_t A = ok[e] ? bA[slot[e]] : -1;
+          if (!ok[e] || A == B[e]) continue;  // edge inside a merged component
+          const int32_t lb = blb[slot[e]], cp = bcp[slot[e]];
+          uint32_t h = ((uint32_t)B[e] * 2654435761u) % (uint32_t)cp;
+          int32_t probe = 0;
+          for (; probe < cp; ++probe) {
+            const int32_t old = atomicCAS(&kb[lb + h], -1, B[e]);
+            if (old == -1 || old == B[e]) {
+              atomicAdd(&kw[lb + h], w[e]);
+              break;
+            }
+            h = (h + 1 == (uint32_t)cp) ? 0u : h + 1;
+          }
+          if (probe == cp) raise_err(ctl, kErrInternal);
+        }
+      }
+      __syncthreads();
     }
+    // rows compacted to the start of their windows, a wave per window:
+    // occupied slots ranked by ballot, written in slot order
+    for (int32_t c = c_lo + (int32_t)threadIdx.x / kWave; c < c_hi;
+         c += blockDim.x / kWave) {
+      const int32_t cp = cap[c];
+      if (cp <= 0 || cp > chunk) continue;
+      const int32_t base = toff[c], lb = base - j0;
+      int32_t out = 0;
+      for (int32_t t0 = 0; t0 < cp; t0 += kWave) {
+        const int32_t t = t0 + lane;
+        const int32_t B = t < cp ? kb[lb + t] : -1;
+        const uint64_t occ = __ballot(B >= 0);
+        if (B >= 0)
+          tbl[base + out + __popcll(occ & below)] =
+              ((uint64_t)(uint32_t)B << 32) | (uint32_t)kw[lb + t];
+        out += __popcll(occ);
+      }
+      if (lane == 0) {
+        wl[c] = out;
+        uniq += out;
+      }
+    }
+    __syncthreads();  // the LDS table is reused by the next chunk
   }
   int32_t tot;
   block_excl_scan<256>(uniq, wsum, &tot);
@@ -1299,8 +1356,11 @@ __global__ __launch_bounds__(256) void k_contract_big(
     }
     const int32_t i0 = moff[A] + tile_i[t] * kBatch;
     const int32_t i1 = min(moff[A + 1], i0 + kBatch);
-    const int32_t total = load_batch<FIRST>(a, mem, i0, i1, pre, bm, wsum,
-                                            [](int32_t) { return true; });
+    // long rows (listed with their chunks in the select) are contracted
+    // chunk by chunk by k_contract_long
+    const int32_t total = load_batch<FIRST>(
+        a, mem, i0, i1, pre, bm, wsum,
+        [&](int32_t m) { return row_span<FIRST>(a, m) <= kLongRow; });
     for (int32_t f = threadIdx.x; f < total; f += blockDim.x) {
       int32_t slot, j, u, w;
       batch_find(pre, f, slot, j);
@@ -1323,6 +1383,68 @@ __global__ __launch_bounds__(256) void k_contract_big(
         h = (h + 1) & (kPreSlots - 1);
       }
       if (!done) added += table_add(tbl, base, cp, B, w, ctl) ? 1 : 0;
+    }
+    __syncthreads();
+    for (int q = threadIdx.x; q < kPreSlots; q += blockDim.x)
+      if (pk[q] >= 0) added += table_add(tbl, base, cp, pk[q], pw[q], ctl);
+    __syncthreads();
+  }
+  added = wave_sum(added);
+  if ((threadIdx.x & (kWave - 1)) == 0 && added)
+    stripe_add(ctl->e_next_s, added);
+}
+
+// The chunks of long rows whose component has a window larger than an LDS
+// chunk: a block per chunk item, pre-aggregated in LDS (a chunk has fewer
+// entries than the LDS table has slots), then added to the window.
+template <bool FIRST>
+__global__ __launch_bounds__(256) void k_contract_long(
+    int32_t nn, Adj a, const int32_t *__restrict__ L,
+    const int32_t *__restrict__ toff, const int32_t *__restrict__ cap,
+    int32_t chunk, LongWork lw, uint64_t *tbl, int32_t tcap, Ctl *ctl) {
+  static_assert(kLongChunk <= kPreSlots / 2, "a chunk fits the LDS table");
+  __shared__ int32_t pk[kPreSlots];
+  __shared__ int32_t pw[kPreSlots];
+  if (!ctl->any_choice) return;
+  const int32_t n_items = ctl->n_lchunk;
+  int32_t added = 0;
+  for (int32_t it = blockIdx.x; it < n_items; it += gridDim.x) {
+    const int32_t slot = lw.item[it];
+    const int32_t v = lw.rows[slot];
+    const int32_t A = L[v];
+    const int32_t cp = cap[A];
+    if (cp <= chunk) continue;  // block-uniform: the LDS path has this row
+    const int32_t base = toff[A];
+    if (base < 0 || base + cp > tcap) {
+      if (threadIdx.x == 0) raise_err(ctl, kErrInternal);
+      continue;
+    }
+    for (int q = threadIdx.x; q < kPreSlots; q += blockDim.x) {
+      pk[q] = -1;
+      pw[q] = 0;
+    }
+    __syncthreads();
+    const int32_t j0 = (it - lw.base[slot]) * kLongChunk;
+    const int32_t j1 = min(row_span<FIRST>(a, v), j0 + kLongChunk);
+    const int32_t rb = row_base<FIRST>(a, v);
+    for (int32_t j = j0 + (int32_t)threadIdx.x; j < j1; j += blockDim.x) {
+      int32_t u, w;
+      if (!row_entry_at<FIRST>(a, v, rb, j, u, w)) continue;
+      if ((uint32_t)u >= (uint32_t)nn) {
+        raise_err(ctl, kErrInternal);
+        continue;
+      }
+      const int32_t B = L[u];
+      if (B == A) continue;
+      uint32_t h = ((uint32_t)B * 2654435761u) & (kPreSlots - 1);
+      for (int32_t probe = 0; probe < kPreSlots; ++probe) {
+        const int32_t old = atomicCAS(&pk[h], -1, B);
+        if (old == -1 || old == B) {
+          atomicAdd(&pw[h], w);
+          break;
+        }
+        h = (h + 1) & (kPreSlots - 1);
+      }
     }
     __syncthreads();
     for (int q = threadIdx.x; q < kPreSlots; q += blockDim.x)
@@ -1928,6 +2050,9 @@ struct Bufs {
   double *mu;
   int32_t *target, *deg, *parent, *newid, *L, *cnt, *rank, *moff, *mem;
   int32_t *long_rows, *big, *cbig, *capn, *tile_c, *tile_i;
+  int32_t *lbase, *lnch, *litem, *lmp, *lu, *lcnt;  // long-row chunks
+  double *lg;
+  int32_t lcap;
   int32_t *cstart;  // first component of every contraction chunk
   int32_t qcap;     // entries of cstart
   int32_t *M, *mark, *lrank;
@@ -1956,7 +2081,7 @@ void carve(Arena &a, int32_t n, int32_t d, int32_t k, Bufs *b) {
   for (int j = 0; j < 2; ++j) {
     b->ws[j] = a.take<int32_t>(n1);
     b->wl[j] = a.take<int32_t>(n1);
-    b->tbl[j] = a.take<uint64_t>(ed);
+    b->tbl[j] = a.take<uint64_t>(2 * ed);  // big windows take twice
     b->size[j] = a.take<int32_t>(n1);
     b->minpt[j] = a.take<int32_t>(n1);
     b->S[j] = a.take<int64_t>((size_t)n * d);
@@ -1972,12 +2097,20 @@ void carve(Arena &a, int32_t n, int32_t d, int32_t k, Bufs *b) {
   b->moff = a.take<int32_t>(n1);
   b->mem = a.take<int32_t>(n1);
   b->long_rows = a.take<int32_t>(n1);
+  b->lbase = a.take<int32_t>(n1);
+  b->lnch = a.take<int32_t>(n1);
+  b->lcap = (int32_t)(n1 + ed / kLongChunk + 64);
+  b->litem = a.take<int32_t>(b->lcap);
+  b->lmp = a.take<int32_t>(b->lcap);
+  b->lu = a.take<int32_t>(b->lcap);
+  b->lcnt = a.take<int32_t>(b->lcap);
+  b->lg = a.take<double>(b->lcap);
   b->big = a.take<int32_t>(n1);
   b->cbig = a.take<int32_t>(n1);
   b->capn = a.take<int32_t>(n1);
   b->tile_c = a.take<int32_t>(2 * n1);
   b->tile_i = a.take<int32_t>(2 * n1);
-  b->qcap = (int32_t)(ed / 64 + 16);  // chunks are >= 64 slots
+  b->qcap = (int32_t)(2 * ed / 64 + 16);  // chunks are >= 64 slots
   b->cstart = a.take<int32_t>(b->qcap);
   b->M = a.take<int32_t>(n1);
   b->mark = a.take<int32_t>(n1);
@@ -2030,24 +2163,24 @@ void launch_round(const Bufs &b, const Adj &adj, int cur, int32_t n,
                   const NodeIn &s, double lambda, int64_t smin, Ctl *ctl,
                   hipStream_t st) {
   const int nxt = 1 - cur;
-  const int32_t tcap = (int32_t)edge_bound(n, k);
+  const int32_t tcap = (int32_t)(2 * edge_bound(n, k));
   hipLaunchKernelGGL(k_round_init, dim3(1), dim3(64), 0, st, ctl);
   prof_begin("select", st);
-  // small rounds: every row by a wave (parallel over entries); large rounds:
-  // a thread per row, long rows by waves
-  const bool all_rows = nn <= kWaveRowsMax;
+  // G lanes per short row; long rows in chunks of entries, a wave each
+  const LongWork lw{b.long_rows, b.lbase, b.lnch, b.litem, b.lg,
+                    b.lmp,       b.lu,    b.lcnt, b.lcap};
   const dim3 long_grid((unsigned)std::max<int64_t>(
-      1, std::min<int64_t>(all_rows ? (nn + 3) / 4 : kLongGrid, (nn + 3) / 4)));
+      1, std::min<int64_t>(kLongGrid, ((int64_t)ed / kLongChunk + nn) / 4 + 1)));
   const dim3 big_grid(
       (unsigned)std::max<int64_t>(1, std::min<int64_t>(kBigGrid, nn / 16)));
   constexpr int G = FIRST ? kSelLanesFirst : kSelLanes;
-  if (!all_rows)
-    hipLaunchKernelGGL((k_select<FIRST, DT, G>), xblocks_for((int64_t)nn * G),
-                       dim3(256), 0, st, nn, adj, s, d, lambda, smin, b.target,
-                       b.deg, b.long_rows, ctl);
+  hipLaunchKernelGGL((k_select<FIRST, DT, G>), xblocks_for((int64_t)nn * G),
+                     dim3(256), 0, st, nn, adj, s, d, lambda, smin, b.target,
+                     b.deg, lw, ctl);
   hipLaunchKernelGGL((k_select_long<FIRST, DT>), long_grid, dim3(256), 0, st,
-                     nn, adj, s, d, lambda, smin, b.target, b.deg, b.long_rows,
-                     all_rows, ctl);
+                     nn, adj, s, d, lambda, smin, lw, ctl);
+  hipLaunchKernelGGL(k_select_combine, dim3(64), dim3(256), 0, st, lw,
+                     b.target, b.deg, ctl);
   prof_end(st);
   prof_begin("union", st);
   hipLaunchKernelGGL(k_hook, blocks_for(nn), dim3(256), 0, st, nn, b.target,
@@ -2069,7 +2202,7 @@ void launch_round(const Bufs &b, const Adj &adj, int cur, int32_t n,
   while (chunk > 64 && (int64_t)ed / chunk < 2048) chunk >>= 1;
   const NodeOut o{b.size[nxt], b.S[nxt],  b.mu,
                   b.minpt[nxt], b.capn,    b.wl[nxt],
-                  b.cbig,      chunk,     nn > kWaveRowsMax ? kBigComp : 16,
+                  b.cbig,      chunk,     kBigComp,
                   b.tile_c,    b.tile_i};
   if constexpr (DT > 0) {
     constexpr int G = kStatsLanes;
@@ -2096,6 +2229,9 @@ void launch_round(const Bufs &b, const Adj &adj, int cur, int32_t n,
   hipLaunchKernelGGL(k_contract_big<FIRST>, big_grid, dim3(256), 0, st, nn,
                      adj, b.L, b.mem, b.moff, b.ws[nxt], b.capn, b.tile_c,
                      b.tile_i, b.tbl[nxt], tcap, ctl);
+  hipLaunchKernelGGL(k_contract_long<FIRST>, long_grid, dim3(256), 0, st, nn,
+                     adj, b.L, b.ws[nxt], b.capn, chunk, lw, b.tbl[nxt], tcap,
+                     ctl);
   prof_end(st);
   prof_begin("compose", st);
   hipLaunchKernelGGL(k_compose<FIRST>, xblocks_for(n), dim3(256), 0, st, n,
@@ -2164,7 +2300,7 @@ int run_tail(const LadderArgs &g, const Bufs &b, const float *emb,
                      b.wl[cur], b.tbl[cur], b.ws[nxt], b.wl[nxt], b.tbl[nxt]);
   t.tcur0 = nxt;
   t.d = d;
-  t.tcap = (int32_t)edge_bound(n, g.k);
+  t.tcap = (int32_t)(2 * edge_bound(n, g.k));
   t.gcap = b.tslots;
   t.n_levels = g.n_levels;
   t.level0 = level0;
@@ -2389,7 +2525,7 @@ int ladder_run(const LadderArgs &g, Ctl *ctl, Arena &a, hipStream_t st) {
       }
       if (!h->any_choice) break;  // Step 1: no candidate merge
       if (h->n_next < 1 || h->n_next >= nn || h->e_next < 0 ||
-          h->e_next > ed || h->slots != ed) {
+          h->e_next > ed || h->slots < ed || h->slots > 2 * (int64_t)ed) {
         set_error("round sizes out of range (%d nodes, %d edges, %d slots)",
                   h->n_next, h->e_next, h->slots);
         return -5;

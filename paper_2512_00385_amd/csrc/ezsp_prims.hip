@@ -166,6 +166,7 @@ __global__ void k_ctl_init(Ctl *ctl) {
     ctl->slots = 0;
     ctl->maxabs_bits = 0;
     ctl->n_long = 0;
+    ctl->n_lchunk = 0;
     for (int a = 0; a < 3; ++a) {
       ctl->bbox_enc[a] = f2ord(INFINITY);
       ctl->bbox_enc[3 + a] = f2ord(-INFINITY);

@@ -102,8 +102,8 @@ def test_partition_rejects_bad_arguments():
     assert call_partition(xyz=None) == E
     assert call_partition(labels=None) == E
     assert call_partition(n_comp=None) == E
-    # 2*k*n must stay below 2^31 (int32 edge indices)
-    assert call_partition(n=200_000_000, k=10) == E
+    # 4*k*n must stay below 2^31 (int32 table indices)
+    assert call_partition(n=60_000_000, k=10) == E
     assert call_partition(ws_bytes=1024) == ezsp.ERR_WORKSPACE
 
 
