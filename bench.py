@@ -34,6 +34,16 @@ if ROOT not in sys.path:
 
 HBM_PEAK_GBS = 8000.0
 WORKLOAD = "driving-3m"
+KINDS = {
+    "room-20k": "synthetic indoor room",
+    "room-1m": "synthetic indoor room, 2 cm voxel subsampled",
+    "driving-3m": "synthetic driving tile",
+    "aerial-10m": "synthetic aerial tile",
+    "room-20k-paper": "synthetic indoor room, the paper's settings",
+    "room-1m-paper": "synthetic indoor room, the paper's settings",
+    "driving-3m-paper": "synthetic driving tile, the paper's settings",
+    "aerial-10m-paper": "synthetic aerial tile, the paper's settings",
+}
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "knn_query.driving-3m.pmc.md")
 CALIB_ELEMS = 1 << 28  # float32 elements of the calibration copy (1 GiB)
 
@@ -112,12 +122,14 @@ def cpu_baseline(sc, n_sample):
     nbr, _ = oracle.knn(xyz, sc.k)
     t1 = time.perf_counter()
     lo, hi, w = oracle.graph(nbr)
-    oracle.partition_graph(emb, lo, hi, w, sc.lambdas, want_energy=False)
+    oracle.partition_graph(emb, lo, hi, w, sc.lambdas, min_size=sc.min_size,
+                           want_energy=False)
     t2 = time.perf_counter()
     return {
         "value": n_sample / (t2 - t0), "unit": "points/s", "cores": 1,
         "kind": "oracle",
-        "sample": (f"{what}, k={sc.k}, ladder {list(sc.lambdas)}; one "
+        "sample": (f"{what}, k={sc.k}, ladder {list(sc.lambdas)}, "
+                   f"s_min {sc.min_size}; one "
                    f"thread; kNN {t1 - t0:.2f} s, graph+ladder "
                    f"{t2 - t1:.2f} s; host {platform.processor() or 'cpu'} "
                    f"with {os.cpu_count()} logical cores"),
@@ -144,7 +156,8 @@ def main():
     dev = torch.device("cuda:0")
     xyz = torch.from_numpy(sc.xyz).to(dev)
     emb = torch.from_numpy(sc.emb).to(dev)
-    part = ezsp.Partitioner(sc.n, sc.d, sc.k, sc.lambdas, device=dev)
+    part = ezsp.Partitioner(sc.n, sc.d, sc.k, sc.lambdas,
+                            min_size=sc.min_size, device=dev)
     print(f"[bench] n={sc.n} d={sc.d} k={sc.k} ws={part.nbytes / 2**30:.2f} "
           "GiB; warmup", file=sys.stderr, flush=True)
     for _ in range(args.warmup):
@@ -213,11 +226,13 @@ def main():
         "ms_per_step": round(ms_per_step, 4), "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": "f64",
         "data": "synthetic",
-        "config": {"workload": f"{sc.name}: synthetic driving tile, "
-                               f"{sc.n} points, D={sc.d}, k={sc.k}, "
-                               f"lambda ladder {sc.lambdas}",
+        "config": {"workload": f"{sc.name}: {KINDS.get(sc.name, 'synthetic')}"
+                               f", {sc.n} points, D={sc.d}, k={sc.k}, "
+                               f"lambda ladder {sc.lambdas}"
+                               + (f", s_min {sc.min_size}" if sc.min_size
+                                  else ""),
                    "n_points": sc.n, "d": sc.d, "k": sc.k,
-                   "lambdas": sc.lambdas},
+                   "lambdas": sc.lambdas, "min_size": sc.min_size},
         "roofline": roofline,
         "stage_ms_per_step": split,
         "n_comp": [int(x) for x in n_comp],

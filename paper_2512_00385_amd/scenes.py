@@ -31,6 +31,7 @@ class Scene:
     obj: np.ndarray          # [n] int32 primitive id (diagnostics only)
     k: int
     lambdas: list = field(default_factory=list)
+    min_size: list | None = None  # s_min per level (None: off)
 
     @property
     def n(self) -> int:
@@ -364,6 +365,43 @@ def aerial_tile(seed: int = 0, n_points: int = 10_000_000) -> Scene:
 
 
 # --------------------------------------------------------------------------
+# the paper's own partition settings on the same geometry (Sec. 4.1:
+# embeddings of dimension 32, 8 nearest neighbours, one lambda = 0.02 and
+# minimal superpoint sizes [5, 30, 90] for the indoor and mobile-mapping
+# data, [5, 15, 70] for the aerial data)
+# --------------------------------------------------------------------------
+
+def _paper_variant(base, name, sigma, min_size, seed):
+    """The base scene's points and primitives with D = 32 embeddings drawn
+    from their own generator stream (the base scene's draws are untouched)."""
+    sc = base(seed)
+    rng = np.random.default_rng([seed, 32])
+    n_obj = int(sc.obj.max()) + 1
+    emb = np.ascontiguousarray(_embed(rng, sc.obj, n_obj, 32, sigma))
+    return Scene(name, sc.xyz, emb, sc.obj, 8, [0.02, 0.02, 0.02],
+                 list(min_size))
+
+
+def room_small_paper(seed: int = 0) -> Scene:
+    return _paper_variant(room_small, "room-20k-paper", 0.05, [5, 30, 90],
+                          seed)
+
+
+def room_1m_paper(seed: int = 0) -> Scene:
+    return _paper_variant(room_1m, "room-1m-paper", 0.05, [5, 30, 90], seed)
+
+
+def driving_tile_paper(seed: int = 0) -> Scene:
+    return _paper_variant(driving_tile, "driving-3m-paper", 0.05, [5, 30, 90],
+                          seed)
+
+
+def aerial_tile_paper(seed: int = 0) -> Scene:
+    return _paper_variant(aerial_tile, "aerial-10m-paper", 0.1, [5, 15, 70],
+                          seed)
+
+
+# --------------------------------------------------------------------------
 # registry and cache
 # --------------------------------------------------------------------------
 
@@ -372,6 +410,10 @@ SCENES = {
     "room-1m": room_1m,
     "driving-3m": driving_tile,
     "aerial-10m": aerial_tile,
+    "room-20k-paper": room_small_paper,
+    "room-1m-paper": room_1m_paper,
+    "driving-3m-paper": driving_tile_paper,
+    "aerial-10m-paper": aerial_tile_paper,
 }
 
 
@@ -384,14 +426,18 @@ def load(name: str, seed: int = 0, cache: bool = True) -> Scene:
     path = os.path.join(_cache_dir(), f"{name}-s{seed}.npz")
     if cache and os.path.exists(path):
         z = np.load(path, allow_pickle=False)
+        ms = (z["min_size"] if "min_size" in z.files
+              else np.zeros(0, np.int64))
         return Scene(name, z["xyz"], z["emb"], z["obj"], int(z["k"]),
-                     [float(x) for x in z["lambdas"]])
+                     [float(x) for x in z["lambdas"]],
+                     [int(x) for x in ms] if ms.size else None)
     sc = SCENES[name](seed)
     if cache:
         os.makedirs(_cache_dir(), exist_ok=True)
         tmp = path + ".tmp%d.npz" % os.getpid()
         np.savez(tmp, xyz=sc.xyz, emb=sc.emb, obj=sc.obj, k=sc.k,
-                 lambdas=np.array(sc.lambdas))
+                 lambdas=np.array(sc.lambdas),
+                 min_size=np.array(sc.min_size or [], np.int64))
         os.replace(tmp, path)
     return sc
 

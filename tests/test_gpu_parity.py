@@ -152,19 +152,23 @@ def _oracle_full(name):
     once per module)."""
     if name not in _FULL:
         sc = scenes.load(name)
-        rl, rnc, ren, _ = oracle.partition(sc.xyz, sc.emb, sc.k, sc.lambdas)
+        rl, rnc, ren, _ = oracle.partition(sc.xyz, sc.emb, sc.k, sc.lambdas,
+                                           sc.min_size)
         _FULL[name] = (sc, rl, rnc, ren)
     return _FULL[name]
 
 
-@pytest.mark.parametrize("name", ["room-1m", "driving-3m"])
+@pytest.mark.parametrize("name", ["room-20k-paper", "room-1m", "driving-3m",
+                                  "room-1m-paper", "driving-3m-paper"])
 def test_partition_full_size(name, tail_mode):
-    """Whole 1M-point room and 3M-point driving tile in the benchmark's
-    launch configuration (a reused Partitioner workspace, no energy pass),
-    every label of every level against the oracle's own full run; then the
-    energy through ezsp.partition."""
+    """Whole workloads in the benchmark's launch configuration (a reused
+    Partitioner workspace, no energy pass): the 1M-point room and the
+    3M-point driving tile with the benchmark ladder and with the paper's own
+    settings (D = 32, k = 8, lambda = 0.02, s_min ladder [5, 30, 90]), every
+    label of every level against the oracle's own full run; then the energy
+    through ezsp.partition."""
     sc, rl, rnc, ren = _oracle_full(name)
-    part = ezsp.Partitioner(sc.n, sc.d, sc.k, sc.lambdas,
+    part = ezsp.Partitioner(sc.n, sc.d, sc.k, sc.lambdas, sc.min_size,
                             device=torch.device("cuda:0"))
     xyz, emb = dev(sc.xyz), dev(sc.emb)
     for _ in range(2):  # the second call reuses the workspace
@@ -173,7 +177,8 @@ def test_partition_full_size(name, tail_mode):
         labels = labels.cpu().numpy()
         for l in range(len(sc.lambdas)):
             assert np.array_equal(labels[l], rl[l]), l
-    _, _, en = ezsp.partition(xyz, emb, sc.k, sc.lambdas, energy=True)
+    _, _, en = ezsp.partition(xyz, emb, sc.k, sc.lambdas, sc.min_size,
+                              energy=True)
     np.testing.assert_allclose(en, ren, rtol=ENERGY_RTOL, atol=0)
 
 
