@@ -70,6 +70,10 @@ def _load():
         "or_energy": (dbl, [P, i64, i32, i32, P, i64, i64, P, P, P, dbl]),
         "or_component_stats": (ctypes.c_int, [P, i64, i64, P, i32, P, P, P,
                                               P]),
+        "or_grid_subsample": (i64, [P, i64, ctypes.c_float, P]),
+        "or_edge_loss": (ctypes.c_int, [P, i64, i32, P, i32, P, P, dbl, dbl,
+                                        P, P, P, P]),
+        "or_purity": (ctypes.c_int, [P, i64, i64, P, i32, P, P, P]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -77,6 +81,17 @@ def _load():
         fn.argtypes = args
     _lib = lib
     return lib
+
+
+class LossOut(ctypes.Structure):
+    _fields_ = [("loss", ctypes.c_double), ("n_edges", ctypes.c_int64),
+                ("n_intra", ctypes.c_int64), ("n_inter", ctypes.c_int64),
+                ("n_intra_kept", ctypes.c_int64)]
+
+
+class PurityOut(ctypes.Structure):
+    _fields_ = [("miou", ctypes.c_double), ("purity", ctypes.c_double),
+                ("n_present", ctypes.c_int64)]
 
 
 class OracleError(RuntimeError):
@@ -287,3 +302,59 @@ def component_stats(label, n_comp: int, emb, xyz=None):
     if rc:
         raise OracleError(rc, "component_stats")
     return size, mean, cen
+
+
+# --------------------------------------------------------------------------
+# grid subsampling (Sec. 4.1), contrastive edge loss (Sec. 3.1), purity and
+# oracle mIoU (Sec. 4.2 "Metrics")
+# --------------------------------------------------------------------------
+
+def grid_subsample(xyz, h: float):
+    """Indices (increasing) of the smallest-index point of every grid cell."""
+    xyz = _c(xyz, np.float32).reshape(-1, 3)
+    keep = np.empty(max(xyz.shape[0], 1), np.int32)
+    m = _load().or_grid_subsample(_p(xyz), xyz.shape[0], float(h), _p(keep))
+    if m < 0:
+        raise OracleError(m, "grid_subsample")
+    return keep[:m].copy()
+
+
+def edge_loss(emb, nbr, cls, word, tau: float, rho: float,
+              want_affinity=True, want_grad=True):
+    """Eq. loss over the sampled kNN pairs.  Returns (dict of the sums and
+    counts, affinity [n,k] fp64 or None, grad [n,d] fp64 or None,
+    sampled [n,k] uint8: 1 where the slot owns a sampled edge)."""
+    emb = _c(emb, np.float32)
+    if emb.ndim == 1:
+        emb = emb[:, None]
+    n, d = emb.shape
+    nbr = _c(nbr, np.int32).reshape(n, -1)
+    k = nbr.shape[1]
+    cls = _c(cls, np.int32)
+    word = _c(word, np.uint32).reshape(n, k)
+    aff = np.empty((n, k), np.float64) if want_affinity else None
+    grad = np.empty((n, d), np.float64) if want_grad else None
+    sampled = np.empty((n, k), np.uint8)
+    out = LossOut()
+    rc = _load().or_edge_loss(_p(emb), n, d, _p(nbr), k, _p(cls), _p(word),
+                              float(tau), float(rho), _p(aff), _p(grad),
+                              _p(sampled), ctypes.byref(out))
+    if rc:
+        raise OracleError(rc, "edge_loss")
+    res = {f: getattr(out, f) for f, _ in LossOut._fields_}
+    return res, aff, grad, sampled
+
+
+def purity(label, n_comp: int, cls, n_cls: int):
+    """Majority class per component, per-class IoU, mIoU and purity."""
+    label, cls = _c(label, np.int32), _c(cls, np.int32)
+    n = label.shape[0]
+    maj = np.empty(n_comp, np.int32)
+    iou = np.empty(n_cls, np.float64)
+    out = PurityOut()
+    rc = _load().or_purity(_p(label), n, int(n_comp), _p(cls), int(n_cls),
+                           _p(maj), _p(iou), ctypes.byref(out))
+    if rc:
+        raise OracleError(rc, "purity")
+    return ({"miou": out.miou, "purity": out.purity,
+             "n_present": out.n_present}, maj, iou)

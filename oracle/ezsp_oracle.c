@@ -735,3 +735,312 @@ int or_component_stats(const int32_t *label, int64_t n, int64_t nc,
   if (xyz && centroid) rc = fixed_means(label, n, nc, xyz, 3, size, centroid);
   return rc;
 }
+
+/* ======================================================================== */
+/* Grid subsampling (Sec. 4.1 subsamples every cloud on a regular grid      */
+/* before partitioning).  Reading R11: the cell of a point is               */
+/* floor((x_i - o_i) / h) per axis in IEEE fp32, o the coordinate-wise      */
+/* minimum of the cloud; the point kept for a cell is its smallest index;   */
+/* kept indices are returned in increasing order.                           */
+/* ======================================================================== */
+
+typedef struct {
+  int64_t cell; /* cx * 2^42 + cy * 2^21 + cz */
+  int32_t idx;
+} cell_rec;
+
+static int cell_rec_cmp(const void *a, const void *b) {
+  const cell_rec *x = (const cell_rec *)a, *y = (const cell_rec *)b;
+  if (x->cell != y->cell) return (x->cell < y->cell) ? -1 : 1;
+  return (x->idx < y->idx) ? -1 : (x->idx > y->idx);
+}
+
+static int int32_cmp(const void *a, const void *b) {
+  int32_t x = *(const int32_t *)a, y = *(const int32_t *)b;
+  return (x < y) ? -1 : (x > y);
+}
+
+int64_t or_grid_subsample(const float *xyz, int64_t n, float h,
+                          int32_t *keep) {
+  if (!xyz || !keep || n < 1 || n > INT32_MAX || !(h > 0.0f) || !isfinite(h))
+    return OR_EINVAL;
+  float o[3];
+  for (int a = 0; a < 3; ++a) o[a] = xyz[a];
+  for (int64_t p = 0; p < n; ++p)
+    for (int a = 0; a < 3; ++a) {
+      float v = xyz[3 * p + a];
+      if (!isfinite(v)) return OR_ENONFINITE;
+      if (v < o[a]) o[a] = v;
+    }
+  cell_rec *r = (cell_rec *)malloc(sizeof(cell_rec) * (size_t)n);
+  if (!r) return OR_ENOMEM;
+  for (int64_t p = 0; p < n; ++p) {
+    int64_t c[3];
+    for (int a = 0; a < 3; ++a) {
+      float off = xyz[3 * p + a] - o[a];
+      float q = off / h;
+      float f = floorf(q);
+      if (!(f < 2097152.0f)) { /* 2^21 cells per axis */
+        free(r);
+        return OR_ERANGE;
+      }
+      c[a] = (int64_t)f;
+    }
+    r[p].cell = (c[0] << 42) | (c[1] << 21) | c[2];
+    r[p].idx = (int32_t)p;
+  }
+  qsort(r, (size_t)n, sizeof(cell_rec), cell_rec_cmp);
+  int64_t m = 0;
+  for (int64_t i = 0; i < n; ++i)
+    if (i == 0 || r[i].cell != r[i - 1].cell) keep[m++] = r[i].idx;
+  free(r);
+  qsort(keep, (size_t)m, sizeof(int32_t), int32_cmp);
+  return m;
+}
+
+/* ======================================================================== */
+/* Affinity and contrastive edge loss (Sec. 3.1, Eq. softmax and Eq. loss). */
+/* Readings R12-R15:                                                        */
+/*   R12 the edges are the unordered pairs of the kNN relation (as R2); an  */
+/*       edge belongs to the smallest slot p*k + j that lists it, and that  */
+/*       slot's random word draws it.                                        */
+/*   R13 with rho < 1 the sample keeps m = min(n_intra,                      */
+/*       floor(rho * n_inter / (1 - rho))) intra edges, those with the       */
+/*       smallest (word, slot); rho = 1 keeps them all.  Every inter edge is */
+/*       kept.                                                               */
+/*   R14 -log(a) = d / tau and -log(1 - a) = -log(-expm1(-d / tau)); the     */
+/*       loss is the plain sum over the sampled edges.                       */
+/*   R15 the gradient of |e_p - e_q| at e_p = e_q is taken as 0.             */
+/* ======================================================================== */
+
+typedef struct {
+  int32_t a, b; /* a < b */
+  int64_t slot;
+} pair_rec;
+
+static int pair_rec_cmp(const void *x, const void *y) {
+  const pair_rec *s = (const pair_rec *)x, *t = (const pair_rec *)y;
+  if (s->a != t->a) return (s->a < t->a) ? -1 : 1;
+  if (s->b != t->b) return (s->b < t->b) ? -1 : 1;
+  return (s->slot < t->slot) ? -1 : (s->slot > t->slot);
+}
+
+typedef struct {
+  uint32_t word;
+  int64_t slot;
+  int64_t edge;
+} draw_rec;
+
+static int draw_rec_cmp(const void *x, const void *y) {
+  const draw_rec *s = (const draw_rec *)x, *t = (const draw_rec *)y;
+  if (s->word != t->word) return (s->word < t->word) ? -1 : 1;
+  return (s->slot < t->slot) ? -1 : (s->slot > t->slot);
+}
+
+/* |e_p - e_q| in fp64, squares summed in dimension order. */
+static double emb_dist(const float *emb, int32_t d, int64_t p, int64_t q) {
+  double s = 0.0;
+  for (int32_t i = 0; i < d; ++i) {
+    double t = (double)emb[p * d + i] - (double)emb[q * d + i];
+    double t2 = t * t;
+    s = s + t2;
+  }
+  return sqrt(s);
+}
+
+int or_edge_loss(const float *emb, int64_t n, int32_t d, const int32_t *nbr,
+                 int32_t k, const int32_t *cls, const uint32_t *word,
+                 double tau, double rho, double *affinity, double *grad,
+                 uint8_t *sampled, or_loss_out *out) {
+  if (!emb || !nbr || !cls || !word || !out || n < 1 || n > INT32_MAX ||
+      d < 1 || d > 1024 || k < 1 || !(tau > 0.0) || !isfinite(tau) ||
+      !(rho >= 0.0 && rho <= 1.0))
+    return OR_EINVAL;
+  int64_t ns = n * k;
+  for (int64_t s = 0; s < ns; ++s)
+    if (nbr[s] < -1 || nbr[s] >= n) return OR_EINVAL;
+  for (int64_t v = 0; v < n * d; ++v)
+    if (!isfinite(emb[v])) return OR_ENONFINITE;
+
+  /* Eq. softmax for every slot; an empty slot has affinity 0. */
+  if (affinity)
+    for (int64_t s = 0; s < ns; ++s) {
+      int32_t q = nbr[s];
+      affinity[s] = (q < 0) ? 0.0 : exp(-emb_dist(emb, d, s / k, q) / tau);
+    }
+
+  /* the unordered pairs and the slot each one belongs to */
+  pair_rec *pr = (pair_rec *)malloc(sizeof(pair_rec) * (size_t)(ns > 0 ? ns : 1));
+  if (!pr) return OR_ENOMEM;
+  int64_t m = 0;
+  for (int64_t s = 0; s < ns; ++s) {
+    int32_t p = (int32_t)(s / k), q = nbr[s];
+    if (q < 0 || q == p) continue;
+    pr[m].a = (p < q) ? p : q;
+    pr[m].b = (p < q) ? q : p;
+    pr[m].slot = s;
+    ++m;
+  }
+  qsort(pr, (size_t)m, sizeof(pair_rec), pair_rec_cmp);
+  int64_t ne = 0;
+  for (int64_t i = 0; i < m; ++i)
+    if (i == 0 || pr[i].a != pr[i - 1].a || pr[i].b != pr[i - 1].b)
+      pr[ne++] = pr[i];
+
+  /* R13: the intra-edge sample */
+  int64_t n_intra = 0, n_inter = 0;
+  for (int64_t e = 0; e < ne; ++e) {
+    if (cls[pr[e].a] == cls[pr[e].b]) ++n_intra;
+    else ++n_inter;
+  }
+  int64_t keep_intra = n_intra;
+  if (rho < 1.0) {
+    double cap = floor(rho * (double)n_inter / (1.0 - rho));
+    if (cap < (double)keep_intra) keep_intra = (int64_t)cap;
+  }
+  char *kept = (char *)calloc((size_t)(ne > 0 ? ne : 1), 1);
+  draw_rec *dr = (draw_rec *)malloc(sizeof(draw_rec) * (size_t)(n_intra > 0 ? n_intra : 1));
+  if (!kept || !dr) {
+    free(pr);
+    free(kept);
+    free(dr);
+    return OR_ENOMEM;
+  }
+  int64_t ni = 0;
+  for (int64_t e = 0; e < ne; ++e) {
+    if (cls[pr[e].a] != cls[pr[e].b]) {
+      kept[e] = 1;
+      continue;
+    }
+    dr[ni].word = word[pr[e].slot];
+    dr[ni].slot = pr[e].slot;
+    dr[ni].edge = e;
+    ++ni;
+  }
+  qsort(dr, (size_t)ni, sizeof(draw_rec), draw_rec_cmp);
+  for (int64_t i = 0; i < keep_intra; ++i) kept[dr[i].edge] = 1;
+  if (sampled) {
+    memset(sampled, 0, (size_t)ns);
+    for (int64_t e = 0; e < ne; ++e)
+      if (kept[e]) sampled[pr[e].slot] = 1;
+  }
+
+  /* Eq. loss over the sample, and its gradient */
+  if (grad)
+    for (int64_t v = 0; v < n * d; ++v) grad[v] = 0.0;
+  double loss = 0.0;
+  for (int64_t e = 0; e < ne; ++e) {
+    if (!kept[e]) continue;
+    int32_t p = (int32_t)(pr[e].slot / k), q = nbr[pr[e].slot];
+    double dist = emb_dist(emb, d, p, q);
+    int intra = cls[p] == cls[q];
+    double term, coef;
+    if (intra) {
+      term = dist / tau;
+      coef = (dist > 0.0) ? 1.0 / (tau * dist) : 0.0;
+    } else {
+      double em = expm1(-dist / tau); /* a - 1 */
+      term = -log(-em);
+      /* d/d(dist) of -log(1 - exp(-dist/tau)) = -1 / (tau * expm1(dist/tau)) */
+      coef = (dist > 0.0) ? -1.0 / (tau * expm1(dist / tau) * dist) : 0.0;
+    }
+    loss = loss + term;
+    if (grad)
+      for (int32_t i = 0; i < d; ++i) {
+        double diff = (double)emb[(int64_t)p * d + i] - (double)emb[(int64_t)q * d + i];
+        double g = coef * diff;
+        grad[(int64_t)p * d + i] += g;
+        grad[(int64_t)q * d + i] -= g;
+      }
+  }
+  out->loss = loss;
+  out->n_edges = ne;
+  out->n_intra = n_intra;
+  out->n_inter = n_inter;
+  out->n_intra_kept = keep_intra;
+  free(pr);
+  free(kept);
+  free(dr);
+  return OR_OK;
+}
+
+/* ======================================================================== */
+/* Partition purity and oracle mIoU (Sec. 4.2 "Metrics": each superpoint    */
+/* takes its majority ground-truth label).  Reading R16: a majority tie     */
+/* goes to the smallest class; IoU_c = TP / (|gt = c| + |pred = c| - TP)    */
+/* over the classes present in the ground truth, averaged in class order;   */
+/* purity = sum TP / n.                                                     */
+/* ======================================================================== */
+
+typedef struct {
+  int32_t comp, cls;
+} cc_rec;
+
+static int cc_rec_cmp(const void *x, const void *y) {
+  const cc_rec *s = (const cc_rec *)x, *t = (const cc_rec *)y;
+  if (s->comp != t->comp) return (s->comp < t->comp) ? -1 : 1;
+  return (s->cls < t->cls) ? -1 : (s->cls > t->cls);
+}
+
+int or_purity(const int32_t *label, int64_t n, int64_t nc, const int32_t *cls,
+              int32_t n_cls, int32_t *majority, double *iou,
+              or_purity_out *out) {
+  if (!label || !cls || !out || n < 1 || n > INT32_MAX || nc < 1 ||
+      nc > INT32_MAX || n_cls < 1)
+    return OR_EINVAL;
+  for (int64_t p = 0; p < n; ++p)
+    if (label[p] < 0 || label[p] >= nc || cls[p] < 0 || cls[p] >= n_cls)
+      return OR_EINVAL;
+  cc_rec *r = (cc_rec *)malloc(sizeof(cc_rec) * (size_t)n);
+  int32_t *maj = (int32_t *)malloc(sizeof(int32_t) * (size_t)nc);
+  int64_t *best = (int64_t *)calloc((size_t)nc, sizeof(int64_t));
+  int64_t *tp = (int64_t *)calloc((size_t)n_cls, sizeof(int64_t));
+  int64_t *ngt = (int64_t *)calloc((size_t)n_cls, sizeof(int64_t));
+  int64_t *npred = (int64_t *)calloc((size_t)n_cls, sizeof(int64_t));
+  if (!r || !maj || !best || !tp || !ngt || !npred) {
+    free(r); free(maj); free(best); free(tp); free(ngt); free(npred);
+    return OR_ENOMEM;
+  }
+  for (int64_t p = 0; p < n; ++p) {
+    r[p].comp = label[p];
+    r[p].cls = cls[p];
+  }
+  qsort(r, (size_t)n, sizeof(cc_rec), cc_rec_cmp);
+  for (int64_t c = 0; c < nc; ++c) maj[c] = -1;
+  /* runs of equal (comp, cls), classes ascending inside a component: a
+   * strictly larger count replaces the majority, so ties keep the smaller */
+  for (int64_t i = 0; i < n;) {
+    int64_t j = i;
+    while (j < n && r[j].comp == r[i].comp && r[j].cls == r[i].cls) ++j;
+    int64_t cnt = j - i;
+    if (cnt > best[r[i].comp]) {
+      best[r[i].comp] = cnt;
+      maj[r[i].comp] = r[i].cls;
+    }
+    i = j;
+  }
+  for (int64_t p = 0; p < n; ++p) {
+    int32_t g = cls[p], y = maj[label[p]];
+    ngt[g] += 1;
+    npred[y] += 1;
+    if (g == y) tp[g] += 1;
+  }
+  double sum = 0.0;
+  int64_t present = 0, tp_all = 0;
+  for (int32_t c = 0; c < n_cls; ++c) {
+    tp_all += tp[c];
+    double v = NAN;
+    if (ngt[c] > 0) {
+      v = (double)tp[c] / (double)(ngt[c] + npred[c] - tp[c]);
+      sum = sum + v;
+      ++present;
+    }
+    if (iou) iou[c] = v;
+  }
+  out->miou = sum / (double)present;
+  out->purity = (double)tp_all / (double)n;
+  out->n_present = present;
+  if (majority) memcpy(majority, maj, sizeof(int32_t) * (size_t)nc);
+  free(r); free(maj); free(best); free(tp); free(ngt); free(npred);
+  return OR_OK;
+}

@@ -18,7 +18,11 @@
  *     removal, weakly-connected-component merging, recalibration
  *     (Sec. 3.2 "Parallel Implementation", Steps 0-4; App. Alg. A-1, A-2),
  *     applied recursively over a ladder of regularisation strengths
- *     (Sec. 3.2 "Hierarchical Partition").
+ *     (Sec. 3.2 "Hierarchical Partition");
+ *   - the grid subsampling applied before partitioning (Sec. 4.1);
+ *   - the pairwise affinity and the contrastive edge loss with intra-edge
+ *     dropping (Sec. 3.1, Eq. softmax, Eq. loss);
+ *   - partition purity and oracle mIoU (Sec. 4.2 "Metrics").
  *
  * Readings taken where the paper is silent (each one is listed, with the
  * reason, in the design notes of the repository):
@@ -38,6 +42,16 @@
  *       components.
  *   R9  level l+1 starts from level l's contracted graph and statistics.
  *   R10 Delta > 0 is strict.
+ *   R11 grid cells are floor((x_i - o_i) / h) in IEEE fp32 with o the
+ *       coordinate-wise minimum; each cell keeps its smallest point index.
+ *   R12 loss edges are the unordered kNN pairs; an edge belongs to the
+ *       smallest slot p*k + j that lists it, whose random word draws it.
+ *   R13 rho < 1 keeps the m = min(n_intra, floor(rho*n_inter/(1-rho)))
+ *       intra edges with the smallest (word, slot); rho = 1 keeps all.
+ *   R14 -log(a) = d/tau, -log(1 - a) = -log(-expm1(-d/tau)), summed.
+ *   R15 the gradient of |e_p - e_q| at e_p = e_q is 0.
+ *   R16 majority ties go to the smallest class; IoU over the classes present
+ *       in the ground truth; purity = matched points / n.
  *
  * Conventions: all pointers are host pointers owned by the caller.
  * Functions return 0 on success and a negative code on error:
@@ -154,6 +168,48 @@ double or_energy(const float *emb, int64_t n, int32_t d, int32_t F,
 int or_component_stats(const int32_t *label, int64_t n, int64_t nc,
                        const float *emb, int32_t d, const float *xyz,
                        int64_t *size, float *mean, float *centroid);
+
+/* ---- grid subsampling (Sec. 4.1; reading R11) ---------------------------- */
+
+/* keep: capacity n, receives the kept point indices in increasing order.
+ * Returns the kept count, or -1 (bad argument), -2 (non-finite coordinate),
+ * -3 (a cell index reaches 2^21 on some axis). */
+int64_t or_grid_subsample(const float *xyz, int64_t n, float h,
+                          int32_t *keep);
+
+/* ---- affinity and contrastive loss (Sec. 3.1; readings R12-R15) ---------- */
+
+typedef struct {
+  double loss;          /* Eq. loss over the sampled edges              */
+  int64_t n_edges;      /* unordered kNN pairs                          */
+  int64_t n_intra;      /* pairs with equal classes                     */
+  int64_t n_inter;      /* pairs with different classes (all sampled)   */
+  int64_t n_intra_kept; /* intra pairs in the sample                    */
+} or_loss_out;
+
+/*   emb       n*d fp32        nbr  n*k int32 (-1 = empty slot)
+ *   cls       n int32 class   word n*k uint32 random words, one per slot
+ *   affinity  n*k fp64 out (nullable): Eq. softmax per slot, 0 when empty
+ *   grad      n*d fp64 out (nullable): d loss / d emb
+ *   sampled   n*k out (nullable): 1 where the slot owns a sampled edge */
+int or_edge_loss(const float *emb, int64_t n, int32_t d, const int32_t *nbr,
+                 int32_t k, const int32_t *cls, const uint32_t *word,
+                 double tau, double rho, double *affinity, double *grad,
+                 uint8_t *sampled, or_loss_out *out);
+
+/* ---- purity and oracle mIoU (Sec. 4.2 "Metrics"; reading R16) ------------- */
+
+typedef struct {
+  double miou;       /* mean IoU over the classes present          */
+  double purity;     /* points whose class is their superpoint's majority, / n */
+  int64_t n_present; /* classes present in the ground truth         */
+} or_purity_out;
+
+/* label n in [0, nc), cls n in [0, n_cls); majority nc out (nullable, -1 for
+ * an empty component); iou n_cls out (nullable, NaN for absent classes). */
+int or_purity(const int32_t *label, int64_t n, int64_t nc, const int32_t *cls,
+              int32_t n_cls, int32_t *majority, double *iou,
+              or_purity_out *out);
 
 #ifdef __cplusplus
 }

@@ -1,0 +1,262 @@
+"""Pins for the oracle's grid subsampling (Sec. 4.1), contrastive edge loss
+(Sec. 3.1, Eq. softmax, Eq. loss) and purity / oracle mIoU (Sec. 4.2
+"Metrics"): hand-worked examples, closed forms, finite differences, brute
+force on tiny inputs and library special cases -- never a re-typed copy of the
+oracle's own formula."""
+import itertools
+import math
+
+import numpy as np
+import pytest
+
+import oracle
+
+
+# --------------------------------------------------------------------------
+# grid subsampling (reading R11)
+# --------------------------------------------------------------------------
+
+def test_grid_hand_example():
+    # h = 1, origin (0, 0, 0) from the minimum; cells by hand:
+    # p0 (0,0,0), p1 (0,0,0), p2 (1,0,0), p3 (2,0,0), p4 (0,0,0), p5 (0,1,1)
+    xyz = np.array([[0.0, 0.0, 0.0], [0.5, 0.2, 0.9], [1.0, 0.0, 0.0],
+                    [2.5, 0.0, 0.0], [0.99, 0.99, 0.99], [0.1, 1.5, 1.0]],
+                   np.float32)
+    assert oracle.grid_subsample(xyz, 1.0).tolist() == [0, 2, 3, 5]
+
+
+def test_grid_first_index_wins():
+    # the same cell visited by later indices keeps the first one
+    xyz = np.array([[3.0, 3.0, 3.0], [0.0, 0.0, 0.0], [3.2, 3.1, 3.3],
+                    [0.1, 0.1, 0.1]], np.float32)
+    assert oracle.grid_subsample(xyz, 1.0).tolist() == [0, 1]
+
+
+def test_grid_lattice_one_per_cell():
+    # points at cell centres of a lattice of spacing h = 0.25 (exact binary
+    # fractions), each repeated three times in shuffled order
+    g = np.stack(np.meshgrid(np.arange(6), np.arange(5), np.arange(4),
+                             indexing="ij"), -1).reshape(-1, 3)
+    xyz = ((g + 0.5) * 0.25).astype(np.float32)
+    rep = np.concatenate([xyz, xyz, xyz])
+    perm = np.random.default_rng(1).permutation(rep.shape[0])
+    rep = rep[perm]
+    keep = oracle.grid_subsample(rep, 0.25)
+    assert keep.size == g.shape[0]
+    # each kept point is the first occurrence of its lattice site
+    first = {}
+    for i, row in enumerate(map(tuple, rep)):
+        first.setdefault(row, i)
+    assert sorted(first.values()) == keep.tolist()
+
+
+def test_grid_numpy_unique():
+    # special case reducing to a library routine: numpy fp32 cells, then
+    # np.unique's first-occurrence index per distinct cell
+    rng = np.random.default_rng(2)
+    xyz = (rng.random((5000, 3)) * np.array([4.0, 3.0, 1.5]) - 1.0)
+    xyz = xyz.astype(np.float32)
+    for h in (0.05, 0.2, 0.7):
+        o = xyz.min(0)
+        cells = np.floor((xyz - o) / np.float32(h)).astype(np.int64)
+        _, first = np.unique(cells, axis=0, return_index=True)
+        assert oracle.grid_subsample(xyz, h).tolist() == sorted(first.tolist())
+
+
+def test_grid_limits():
+    xyz = np.array([[0, 0, 0], [1, 1, 1]], np.float32)
+    assert oracle.grid_subsample(xyz, 100.0).tolist() == [0]
+    assert oracle.grid_subsample(xyz, 1e-3).tolist() == [0, 1]
+    with pytest.raises(oracle.OracleError) as e:
+        oracle.grid_subsample(np.array([[0, 0, 0], [3000, 0, 0]], np.float32),
+                              1e-3)
+    assert e.value.code == -3
+    with pytest.raises(oracle.OracleError) as e:
+        oracle.grid_subsample(np.array([[0, 0, np.nan]], np.float32), 1.0)
+    assert e.value.code == -2
+    with pytest.raises(oracle.OracleError):
+        oracle.grid_subsample(xyz, 0.0)
+
+
+# --------------------------------------------------------------------------
+# affinity and contrastive loss (readings R12-R15)
+# --------------------------------------------------------------------------
+
+def _two_points(c0, c1, tau, rho=1.0):
+    emb = np.array([[0.0, 0.0], [3.0, 4.0]], np.float32)  # |e0 - e1| = 5
+    nbr = np.array([[1], [0]], np.int32)
+    cls = np.array([c0, c1], np.int32)
+    word = np.array([[7], [3]], np.uint32)
+    return oracle.edge_loss(emb, nbr, cls, word, tau, rho)
+
+
+def test_loss_two_points_intra():
+    res, aff, grad, smp = _two_points(0, 0, 2.5)
+    # one unordered pair, owned by slot 0; -log(exp(-5/2.5)) = 2
+    assert res["n_edges"] == 1 and res["n_intra"] == 1
+    assert smp.ravel().tolist() == [1, 0]
+    assert res["loss"] == pytest.approx(2.0, rel=1e-15)
+    assert aff.ravel() == pytest.approx([math.exp(-2.0)] * 2, rel=1e-15)
+    # d/de0 of |e0 - e1| / tau = (e0 - e1) / (tau |e0 - e1|)
+    assert grad[0] == pytest.approx([-3 / 12.5, -4 / 12.5], rel=1e-14)
+    assert grad[1] == pytest.approx([3 / 12.5, 4 / 12.5], rel=1e-14)
+
+
+def test_loss_two_points_inter():
+    res, aff, grad, _ = _two_points(0, 1, 1.0)
+    assert res["n_inter"] == 1 and res["n_intra"] == 0
+    assert res["loss"] == pytest.approx(-math.log1p(-math.exp(-5.0)),
+                                        rel=1e-13)
+    # d/dd of -log(1 - e^-d) = -e^-d / (1 - e^-d); times (e0 - e1)/5
+    s = -math.exp(-5.0) / (1.0 - math.exp(-5.0))
+    assert grad[0] == pytest.approx([s * -3 / 5, s * -4 / 5], rel=1e-12)
+    assert grad[1] == pytest.approx([-s * -3 / 5, -s * -4 / 5], rel=1e-12)
+
+
+def test_loss_coincident_intra_is_zero():
+    emb = np.ones((3, 4), np.float32)
+    nbr = np.array([[1, 2], [0, 2], [0, 1]], np.int32)
+    res, aff, grad, _ = oracle.edge_loss(emb, nbr, np.zeros(3, np.int32),
+                                         np.arange(6, dtype=np.uint32), 0.5,
+                                         1.0)
+    assert res["n_edges"] == 3 and res["loss"] == 0.0
+    assert np.all(aff == 1.0) and np.all(grad == 0.0)
+
+
+def _random_case(n=60, d=4, k=5, n_cls=3, seed=0):
+    rng = np.random.default_rng(seed)
+    emb = rng.standard_normal((n, d)).astype(np.float32)
+    nbr = np.stack([rng.choice(np.delete(np.arange(n), p), k, replace=False)
+                    for p in range(n)]).astype(np.int32)
+    nbr[rng.random((n, k)) < 0.1] = -1  # some empty slots
+    cls = rng.integers(0, n_cls, n).astype(np.int32)
+    word = rng.integers(0, 64, (n, k)).astype(np.uint32)  # many equal words
+    return emb, nbr, cls, word
+
+
+@pytest.mark.parametrize("rho", [0.0, 0.1, 0.3, 0.5, 0.9, 1.0])
+def test_loss_sample_brute_force(rho):
+    emb, nbr, cls, word = _random_case(seed=3)
+    n, k = nbr.shape
+    # brute force: every unordered pair, its smallest listing slot
+    owner = {}
+    for p, j in itertools.product(range(n), range(k)):
+        q = int(nbr[p, j])
+        if q < 0 or q == p:
+            continue
+        key = frozenset((p, q))
+        owner[key] = min(owner.get(key, 1 << 60), p * k + j)
+    intra = [s for key, s in owner.items() if len({cls[v] for v in key}) == 1]
+    n_inter = len(owner) - len(intra)
+    m = len(intra)
+    if rho < 1.0:
+        # largest m with m / (m + n_inter) <= rho
+        m = 0
+        while m < len(intra) and (m + 1) <= rho * (m + 1 + n_inter) + 1e-12:
+            m += 1
+    chosen = sorted(intra, key=lambda s: (int(word.flat[s]), s))[:m]
+    expect = np.zeros(n * k, np.uint8)
+    expect[chosen] = 1
+    for key, s in owner.items():
+        if len({cls[v] for v in key}) == 2:
+            expect[s] = 1
+    res, _, _, smp = oracle.edge_loss(emb, nbr, cls, word, 0.7, rho)
+    assert res["n_edges"] == len(owner)
+    assert res["n_inter"] == n_inter and res["n_intra_kept"] == m
+    assert smp.ravel().tolist() == expect.tolist()
+
+
+@pytest.mark.parametrize("rho", [0.3, 1.0])
+def test_loss_gradient_finite_differences(rho):
+    emb, nbr, cls, word = _random_case(n=30, d=3, k=4, seed=5)
+    res, _, grad, _ = oracle.edge_loss(emb, nbr, cls, word, 0.7, rho)
+    eps = 1e-3
+    num = np.zeros_like(grad)
+    for i, j in itertools.product(range(emb.shape[0]), range(emb.shape[1])):
+        ep, em = emb.copy(), emb.copy()
+        ep[i, j] += eps
+        em[i, j] -= eps
+        step = float(ep[i, j]) - float(em[i, j])  # the fp32 step taken
+        lp = oracle.edge_loss(ep, nbr, cls, word, 0.7, rho, False, False)[0]
+        lm = oracle.edge_loss(em, nbr, cls, word, 0.7, rho, False, False)[0]
+        num[i, j] = (lp["loss"] - lm["loss"]) / step
+    np.testing.assert_allclose(grad, num, rtol=1e-4, atol=1e-5)
+
+
+def test_loss_affinity_symmetric_and_bounded():
+    emb, nbr, cls, word = _random_case(seed=7)
+    _, aff, _, _ = oracle.edge_loss(emb, nbr, cls, word, 0.4, 1.0)
+    n, k = nbr.shape
+    for p, j in itertools.product(range(n), range(k)):
+        q = nbr[p, j]
+        if q < 0:
+            assert aff[p, j] == 0.0
+            continue
+        assert 0.0 < aff[p, j] <= 1.0
+        back = np.nonzero(nbr[q] == p)[0]
+        if back.size:
+            assert aff[q, back[0]] == aff[p, j]
+
+
+def test_loss_rejects():
+    emb, nbr, cls, word = _random_case()
+    with pytest.raises(oracle.OracleError):
+        oracle.edge_loss(emb, nbr, cls, word, 0.0, 0.5)
+    with pytest.raises(oracle.OracleError):
+        oracle.edge_loss(emb, nbr, cls, word, 1.0, 1.5)
+    bad = nbr.copy()
+    bad[0, 0] = emb.shape[0]
+    with pytest.raises(oracle.OracleError):
+        oracle.edge_loss(emb, bad, cls, word, 1.0, 0.5)
+
+
+# --------------------------------------------------------------------------
+# purity and oracle mIoU (reading R16)
+# --------------------------------------------------------------------------
+
+def test_purity_hand_example():
+    label = np.array([0, 0, 0, 1, 1, 1, 1, 2, 2, 2], np.int32)
+    cls = np.array([0, 0, 1, 1, 1, 2, 2, 2, 0, 0], np.int32)
+    res, maj, iou = oracle.purity(label, 3, cls, 3)
+    # majorities: {0:2, 1:1} -> 0; {1:2, 2:2} tie -> 1; {2:1, 0:2} -> 0
+    assert maj.tolist() == [0, 1, 0]
+    # class 0: TP 4, gt 4, pred 6; class 1: TP 2, gt 3, pred 4; class 2: 0
+    assert iou.tolist() == [4 / 6, 2 / 5, 0.0]
+    assert res["miou"] == pytest.approx((4 / 6 + 2 / 5) / 3, rel=1e-15)
+    assert res["purity"] == 0.6 and res["n_present"] == 3
+
+
+def test_purity_sklearn():
+    from sklearn.metrics import jaccard_score
+    rng = np.random.default_rng(4)
+    n, nc, n_cls = 3000, 70, 9
+    label = rng.integers(0, nc, n).astype(np.int32)
+    cls = (label % n_cls + (rng.random(n) < 0.3) *
+           rng.integers(0, n_cls, n)) % n_cls
+    cls = cls.astype(np.int32)
+    res, maj, _ = oracle.purity(label, nc, cls, n_cls)
+    for c in range(nc):  # brute-force majority with the smallest-class tie
+        cnt = np.bincount(cls[label == c], minlength=n_cls)
+        assert maj[c] == (int(np.argmax(cnt)) if cnt.sum() else -1)
+    pred = maj[label]
+    present = np.unique(cls)
+    ref = jaccard_score(cls, pred, labels=present, average="macro")
+    assert res["miou"] == pytest.approx(ref, rel=1e-12)
+    assert res["purity"] == pytest.approx(np.mean(pred == cls), rel=1e-15)
+
+
+def test_purity_special_partitions():
+    rng = np.random.default_rng(6)
+    cls = rng.integers(0, 5, 400).astype(np.int32)
+    # the partition equal to the classes, and the singleton partition: exact
+    for label, nc in ((cls, 5), (np.arange(400, dtype=np.int32), 400)):
+        res, _, iou = oracle.purity(label, nc, cls, 5)
+        assert res["miou"] == 1.0 and res["purity"] == 1.0
+    # one component: purity is the largest class share, one IoU is non-zero
+    res, maj, iou = oracle.purity(np.zeros(400, np.int32), 1, cls, 5)
+    top = np.bincount(cls).max()
+    assert res["purity"] == top / 400
+    assert np.count_nonzero(iou) == 1
+    # an empty component has no majority
+    res, maj, _ = oracle.purity(np.zeros(400, np.int32), 2, cls, 5)
+    assert maj[1] == -1
