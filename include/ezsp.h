@@ -150,6 +150,96 @@ int ezsp_component_stats(const int32_t *labels, int64_t n, int64_t n_comp,
                          int64_t *size, float *emb_mean, float *centroid,
                          void *ws, size_t ws_bytes, void *stream);
 
+/* ---- grid subsampling (Sec. 4.1: every cloud is subsampled on a regular
+ * grid before it is partitioned) ------------------------------------------ */
+
+size_t ezsp_grid_subsample_workspace_size(int64_t n);
+
+/* Keeps one point per occupied cell of a regular grid of spacing h.
+ *   xyz      n*3 fp32 (in)
+ *   h        cell size, finite and > 0
+ *   keep     n int32 (out): the first *n_keep entries are the kept point
+ *            indices in increasing order; the rest is unspecified
+ *   n_keep   (host, out) number of kept points
+ * A point's cell is floor((x_i - o_i) / h) on each axis, computed in IEEE
+ * fp32 (one subtraction, one correctly rounded division), o the
+ * coordinate-wise minimum of xyz; each cell keeps its smallest point index.
+ * Errors: INVALID_ARG, NONFINITE, RANGE (2^21 or more cells on an axis),
+ *         WORKSPACE, DEVICE. */
+int ezsp_grid_subsample(const float *xyz, int64_t n, float h, int32_t *keep,
+                        int64_t *n_keep, void *ws, size_t ws_bytes,
+                        void *stream);
+
+/* ---- affinity and contrastive edge loss (Sec. 3.1, Eq. softmax and
+ * Eq. loss) --------------------------------------------------------------- */
+
+typedef struct {
+  double loss;          /* Eq. loss summed over the sampled pairs          */
+  int64_t n_edges;      /* unordered pairs of the kNN relation             */
+  int64_t n_intra;      /* pairs whose end points share a class            */
+  int64_t n_inter;      /* the others; every inter pair is sampled         */
+  int64_t n_intra_kept; /* intra pairs in the sample                       */
+} ezsp_loss_stats;
+
+size_t ezsp_edge_loss_workspace_size(int64_t n, int32_t k);
+
+/* Affinity a_pq = exp(-|e_p - e_q| / tau) and the contrastive loss
+ *   L = sum_intra -log a_pq + sum_inter -log(1 - a_pq)
+ * over the unordered pairs of a neighbour table, intra pairs sampled.
+ *   emb       n*d fp32 (in), d in 1..1024
+ *   nbr       n*k int32 (in): neighbour ids in [0, n) or -1 (empty slot)
+ *   cls       n int32 (in): class of every point (only equality matters)
+ *   word      n*k uint32 (in): one random word per slot
+ *   tau       temperature, finite and > 0; rho in [0, 1]
+ *   affinity  n*k fp32 (out, nullable): a for every non-empty slot, 0 for
+ *             empty ones
+ *   grad      n*d fp32 (out, nullable): dL/d emb
+ *   sampled   n*k uint8 (out, nullable): 1 where the slot owns a pair of
+ *             the sample
+ *   out       (host, out) the loss and the pair counts
+ * A pair {p, q} belongs to the smallest slot p*k + j listing it, and that
+ * slot's word draws it.  With rho < 1 the sample keeps the
+ * m = min(n_intra, floor(rho * n_inter / (1 - rho))) intra pairs with the
+ * smallest (word, slot); rho = 1 keeps them all.  -log a is evaluated as
+ * d / tau and -log(1 - a) as -log(-expm1(-d / tau)); the gradient of
+ * |e_p - e_q| at e_p = e_q is taken as 0.  Distances, affinities and the
+ * gradient are fp32 (the gradient is accumulated with atomics, so its last
+ * bits vary between runs); the loss is summed in fp64.
+ * Errors: INVALID_ARG (also a neighbour id outside [-1, n), detected on the
+ *         device), NONFINITE, WORKSPACE, DEVICE. */
+int ezsp_edge_loss(const float *emb, int64_t n, int32_t d, const int32_t *nbr,
+                   int32_t k, const int32_t *cls, const uint32_t *word,
+                   double tau, double rho, float *affinity, float *grad,
+                   uint8_t *sampled, ezsp_loss_stats *out, void *ws,
+                   size_t ws_bytes, void *stream);
+
+/* ---- purity and oracle mIoU (Sec. 4.2 "Metrics") ------------------------- */
+
+typedef struct {
+  double miou;       /* mean over the classes present of the IoU between
+                        the classes and the superpoints' majority classes */
+  double purity;     /* share of points whose class is their superpoint's
+                        majority class                                     */
+  int64_t n_present; /* classes that occur in cls                          */
+} ezsp_purity_stats;
+
+size_t ezsp_purity_workspace_size(int64_t n, int64_t n_comp, int32_t n_cls);
+
+/* Gives every superpoint its majority class and scores that labelling.
+ *   labels    n int32 (in), each in [0, n_comp)
+ *   cls       n int32 (in), each in [0, n_cls)
+ *   majority  n_comp int32 (out, nullable): majority class, ties to the
+ *             smallest class, -1 for an empty superpoint
+ *   iou       n_cls fp64 (out, nullable): TP / (|cls = c| + |pred = c| - TP),
+ *             NaN for a class absent from cls
+ *   out       (host, out) mIoU (IoUs summed in class order), purity
+ * Errors: INVALID_ARG (also ids out of range, detected on the device),
+ *         WORKSPACE, DEVICE. */
+int ezsp_purity(const int32_t *labels, int64_t n, int64_t n_comp,
+                const int32_t *cls, int32_t n_cls, int32_t *majority,
+                double *iou, ezsp_purity_stats *out, void *ws,
+                size_t ws_bytes, void *stream);
+
 /* ---- diagnostics --------------------------------------------------------- */
 
 /* Static text for a status code. */
@@ -160,7 +250,8 @@ const char *ezsp_last_error(void);
 
 /* Per-stage timing with HIP events recorded on the caller's stream around
  * the launches of each stage ("knn_query", "morton_sort", "graph_build",
- * "select", "union", "stats", "contract", "compose", "tail").  Off by default; a
+ * "select", "union", "stats", "contract", "compose", "tail",
+ * "grid_subsample", "edge_loss", "purity").  Off by default; a
  * diagnostic for benchmarks.  ezsp_profile_enable(1) clears the totals and
  * starts recording, ezsp_profile_enable(0) stops.  ezsp_profile_read gives
  * the number of recorded launches of `stage`, their summed duration in

@@ -259,4 +259,127 @@ int ezsp_component_stats(const int32_t *labels, int64_t n, int64_t n_comp,
                    emb_mean, centroid, ctl, a, st);
 }
 
+size_t ezsp_grid_subsample_workspace_size(int64_t n) {
+  if (!n_ok(n)) return 0;
+  Arena a;
+  a.take<Ctl>(1);
+  grid_reserve(a, (int32_t)n);
+  return a.off + 512;
+}
+
+int ezsp_grid_subsample(const float *xyz, int64_t n, float h, int32_t *keep,
+                        int64_t *n_keep, void *ws, size_t ws_bytes,
+                        void *stream) {
+  set_error("%s", "");
+  if (!xyz || !keep || !n_keep || !ws)
+    return fail(EZSP_ERR_INVALID_ARG,
+                "xyz, keep, n_keep and ws must not be NULL");
+  if (!n_ok(n)) return fail(EZSP_ERR_INVALID_ARG, "n must be in [1, 2^31)");
+  if (!(h > 0.0f) || !isfinite(h))
+    return fail(EZSP_ERR_INVALID_ARG, "h must be finite and > 0");
+  if (ws_bytes < ezsp_grid_subsample_workspace_size(n))
+    return fail(EZSP_ERR_WORKSPACE, "workspace smaller than the queried size");
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  Arena a = open_ws(ws, ws_bytes);
+  Ctl *ctl = a.take<Ctl>(1);
+  hipLaunchKernelGGL(k_ctl_init, dim3(1), dim3(64), 0, st, ctl);
+  return grid_run(xyz, (int32_t)n, h, keep, n_keep, ctl, a, st);
+}
+
+size_t ezsp_edge_loss_workspace_size(int64_t n, int32_t k) {
+  if (!n_ok(n) || k < 1 || n * (int64_t)k >= kMaxN) return 0;
+  Arena a;
+  a.take<Ctl>(1);
+  loss_reserve(a, (int32_t)n, k);
+  return a.off + 512;
+}
+
+int ezsp_edge_loss(const float *emb, int64_t n, int32_t d, const int32_t *nbr,
+                   int32_t k, const int32_t *cls, const uint32_t *word,
+                   double tau, double rho, float *affinity, float *grad,
+                   uint8_t *sampled, ezsp_loss_stats *out, void *ws,
+                   size_t ws_bytes, void *stream) {
+  set_error("%s", "");
+  if (!emb || !nbr || !cls || !word || !out || !ws)
+    return fail(EZSP_ERR_INVALID_ARG,
+                "emb, nbr, cls, word, out and ws must not be NULL");
+  if (!n_ok(n)) return fail(EZSP_ERR_INVALID_ARG, "n must be in [1, 2^31)");
+  if (d < 1 || d > 1024)
+    return fail(EZSP_ERR_INVALID_ARG, "d must be in 1..1024");
+  if (k < 1 || n * (int64_t)k >= kMaxN)
+    return fail(EZSP_ERR_INVALID_ARG, "k must be >= 1 with n*k below 2^31");
+  if (n * (int64_t)d >= kMaxN)
+    return fail(EZSP_ERR_INVALID_ARG, "n*d must stay below 2^31");
+  if (!(tau > 0.0) || !isfinite(tau))
+    return fail(EZSP_ERR_INVALID_ARG, "tau must be finite and > 0");
+  if (!(rho >= 0.0 && rho <= 1.0))
+    return fail(EZSP_ERR_INVALID_ARG, "rho must be in [0, 1]");
+  if (ws_bytes < ezsp_edge_loss_workspace_size(n, k))
+    return fail(EZSP_ERR_WORKSPACE, "workspace smaller than the queried size");
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  Arena a = open_ws(ws, ws_bytes);
+  Ctl *ctl = a.take<Ctl>(1);
+  hipLaunchKernelGGL(k_ctl_init, dim3(1), dim3(64), 0, st, ctl);
+  LossArgs g;
+  g.emb = emb;
+  g.n = (int32_t)n;
+  g.d = d;
+  g.nbr = nbr;
+  g.k = k;
+  g.cls = cls;
+  g.word = word;
+  g.tau = tau;
+  g.rho = rho;
+  g.affinity = affinity;
+  g.grad = grad;
+  g.sampled = sampled;
+  LossResult r;
+  int rc = loss_run(g, &r, ctl, a, st);
+  if (rc) return rc;
+  out->loss = r.loss;
+  out->n_edges = r.n_edges;
+  out->n_intra = r.n_intra;
+  out->n_inter = r.n_inter;
+  out->n_intra_kept = r.n_intra_kept;
+  return EZSP_OK;
+}
+
+size_t ezsp_purity_workspace_size(int64_t n, int64_t n_comp, int32_t n_cls) {
+  if (!n_ok(n) || n_comp < 1 || n_comp >= kMaxN || n_cls < 1 ||
+      n_comp > ((int64_t)1 << 62) / n_cls)
+    return 0;
+  Arena a;
+  a.take<Ctl>(1);
+  purity_reserve(a, (int32_t)n, (int32_t)n_comp, n_cls);
+  return a.off + 512;
+}
+
+int ezsp_purity(const int32_t *labels, int64_t n, int64_t n_comp,
+                const int32_t *cls, int32_t n_cls, int32_t *majority,
+                double *iou, ezsp_purity_stats *out, void *ws,
+                size_t ws_bytes, void *stream) {
+  set_error("%s", "");
+  if (!labels || !cls || !out || !ws)
+    return fail(EZSP_ERR_INVALID_ARG,
+                "labels, cls, out and ws must not be NULL");
+  if (!n_ok(n)) return fail(EZSP_ERR_INVALID_ARG, "n must be in [1, 2^31)");
+  if (n_comp < 1 || n_comp >= kMaxN || n_cls < 1 ||
+      n_comp > ((int64_t)1 << 62) / n_cls)
+    return fail(EZSP_ERR_INVALID_ARG, "n_comp or n_cls out of range");
+  if (ws_bytes < ezsp_purity_workspace_size(n, n_comp, n_cls))
+    return fail(EZSP_ERR_WORKSPACE, "workspace smaller than the queried size");
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  Arena a = open_ws(ws, ws_bytes);
+  Ctl *ctl = a.take<Ctl>(1);
+  hipLaunchKernelGGL(k_ctl_init, dim3(1), dim3(64), 0, st, ctl);
+  PurityResult r;
+  int rc = purity_run(labels, (int32_t)n, (int32_t)n_comp, cls, n_cls,
+                      majority, iou, &r, ctl, a, st);
+  if (rc) return rc;
+  out->miou = r.miou;
+  out->purity = r.purity;
+  out->n_present = r.n_present;
+  return EZSP_OK;
+}
+
 }  // extern "C"

@@ -57,6 +57,16 @@ struct Ctl {
   Stripe maxabs_s[kStripes];  // max |e| bits from the fused gather
   int32_t tail_nc[16];        // superpoints of every level the tail ended
   int64_t tail_cut2[16];      // ... and 2 x their cut weight
+  // results of the grid-subsampling, edge-loss and purity entry points
+  int32_t n_out;              // points kept by the grid subsampling
+  int32_t sel_mode;           // intra sample: 0 none, 1 all, 2 by threshold
+  uint64_t sel_prefix;        // radix select: key bits fixed so far
+  uint64_t sel_mask;          // ... and which bits those are
+  int64_t sel_rank;           // rank still wanted below the prefix
+  unsigned long long le_edges, le_intra, le_keep;
+  double le_loss;             // Eq. loss over the sample
+  double pu_miou, pu_purity;
+  int64_t pu_present;
 };
 
 __device__ __forceinline__ void stripe_add(Stripe *s, int32_t v) {

@@ -137,12 +137,50 @@ int stats_run(const int32_t *labels, int32_t n, int32_t n_comp,
               float *emb_mean, float *centroid, Ctl *ctl, Arena &a,
               hipStream_t st);
 
+// Grid subsampling: kept point indices in increasing order.
+void grid_reserve(Arena &a, int32_t n);
+int grid_run(const float *xyz, int32_t n, float h, int32_t *keep,
+             int64_t *n_keep, Ctl *ctl, Arena &a, hipStream_t st);
+
+// Affinity and contrastive edge loss over a neighbour table.
+struct LossArgs {
+  const float *emb;
+  int32_t n, d;
+  const int32_t *nbr;
+  int32_t k;
+  const int32_t *cls;
+  const uint32_t *word;
+  double tau, rho;
+  float *affinity;   // n*k, nullable
+  float *grad;       // n*d, nullable
+  uint8_t *sampled;  // n*k, nullable
+};
+struct LossResult {
+  double loss;
+  int64_t n_edges, n_intra, n_inter, n_intra_kept;
+};
+void loss_reserve(Arena &a, int32_t n, int32_t k);
+int loss_run(const LossArgs &g, LossResult *res, Ctl *ctl, Arena &a,
+             hipStream_t st);
+
+// Purity and oracle mIoU of a labelling against class ids.
+struct PurityResult {
+  double miou, purity;
+  int64_t n_present;
+};
+void purity_reserve(Arena &a, int32_t n, int32_t n_comp, int32_t n_cls);
+int purity_run(const int32_t *labels, int32_t n, int32_t n_comp,
+               const int32_t *cls, int32_t n_cls, int32_t *majority,
+               double *iou, PurityResult *res, Ctl *ctl, Arena &a,
+               hipStream_t st);
+
 // Shared host helpers.
 void set_error(const char *fmt, ...);
 int read_ctl(Ctl *ctl, Ctl *host, hipStream_t st);  // sync + copy back
 int check_hip(hipError_t e, const char *what);
 Ctl *pinned_ctl();
 __global__ void k_ctl_init(Ctl *ctl);
+__global__ void k_bbox(const float *xyz, int32_t n, Ctl *ctl);
 __global__ void k_maxabs(const float *v, int64_t count, Ctl *ctl);
 __global__ void k_fixshift(Ctl *ctl, int32_t n);
 

@@ -179,6 +179,18 @@ __global__ void k_ctl_init(Ctl *ctl) {
     ctl->tail_level = -1;
     ctl->cut_w2 = 0;
     ctl->fid_total = 0.0;
+    ctl->n_out = 0;
+    ctl->sel_mode = 0;
+    ctl->sel_prefix = 0;
+    ctl->sel_mask = 0;
+    ctl->sel_rank = 0;
+    ctl->le_edges = 0;
+    ctl->le_intra = 0;
+    ctl->le_keep = 0;
+    ctl->le_loss = 0.0;
+    ctl->pu_miou = 0.0;
+    ctl->pu_purity = 0.0;
+    ctl->pu_present = 0;
   }
   if (blockIdx.x == 0) {
     stripe_zero(ctl->e_next_s);

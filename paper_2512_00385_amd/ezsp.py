@@ -33,6 +33,9 @@ ENTRY_POINTS = (
     "ezsp_component_stats_workspace_size", "ezsp_component_stats",
     "ezsp_status_string", "ezsp_last_error",
     "ezsp_profile_enable", "ezsp_profile_read", "ezsp_profile_only",
+    "ezsp_grid_subsample_workspace_size", "ezsp_grid_subsample",
+    "ezsp_edge_loss_workspace_size", "ezsp_edge_loss",
+    "ezsp_purity_workspace_size", "ezsp_purity",
 )
 
 
@@ -41,6 +44,19 @@ class Params(ctypes.Structure):
     _fields_ = [("k", ctypes.c_int32), ("n_levels", ctypes.c_int32),
                 ("lambdas", ctypes.c_void_p), ("min_size", ctypes.c_void_p),
                 ("max_rounds", ctypes.c_int32), ("flags", ctypes.c_uint32)]
+
+
+class LossStats(ctypes.Structure):
+    """Mirror of ezsp_loss_stats."""
+    _fields_ = [("loss", ctypes.c_double), ("n_edges", ctypes.c_int64),
+                ("n_intra", ctypes.c_int64), ("n_inter", ctypes.c_int64),
+                ("n_intra_kept", ctypes.c_int64)]
+
+
+class PurityStats(ctypes.Structure):
+    """Mirror of ezsp_purity_stats."""
+    _fields_ = [("miou", ctypes.c_double), ("purity", ctypes.c_double),
+                ("n_present", ctypes.c_int64)]
 
 
 class EzspError(RuntimeError):
@@ -80,6 +96,16 @@ def load() -> ctypes.CDLL:
         "ezsp_profile_enable": (ctypes.c_int, [ctypes.c_int]),
         "ezsp_profile_read": (ctypes.c_int, [ctypes.c_char_p, P, P, P]),
         "ezsp_profile_only": (ctypes.c_int, [ctypes.c_char_p]),
+        "ezsp_grid_subsample_workspace_size": (sz, [i64]),
+        "ezsp_grid_subsample": (ctypes.c_int, [P, i64, ctypes.c_float, P, P,
+                                               P, sz, P]),
+        "ezsp_edge_loss_workspace_size": (sz, [i64, i32]),
+        "ezsp_edge_loss": (ctypes.c_int, [P, i64, i32, P, i32, P, P,
+                                          ctypes.c_double, ctypes.c_double,
+                                          P, P, P, P, P, sz, P]),
+        "ezsp_purity_workspace_size": (sz, [i64, i64, i32]),
+        "ezsp_purity": (ctypes.c_int, [P, i64, i64, P, i32, P, P, P, P, sz,
+                                       P]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -109,6 +135,7 @@ def profile_only(stage=None):
 
 STAGES = ("morton_sort", "knn_query", "graph_build", "select", "union",
           "stats", "contract", "compose", "tail")
+EXTRA_STAGES = ("grid_subsample", "edge_loss", "purity")
 
 
 def profile_read(stage: str):
@@ -284,3 +311,81 @@ def component_stats(labels: torch.Tensor, n_comp: int, emb: torch.Tensor,
                                     _ptr(cen), _ptr(ws), nbytes,
                                     _stream(dev)), "ezsp_component_stats")
     return size, mean, cen
+
+
+def grid_subsample(xyz: torch.Tensor, h: float) -> torch.Tensor:
+    """Indices (increasing, int32) of the point kept in every occupied cell
+    of a regular grid of spacing h: the cell's smallest point index."""
+    lib = load()
+    xyz = _dev_tensor(xyz, torch.float32, "xyz", 3)
+    n = xyz.shape[0]
+    keep = torch.empty(n, dtype=torch.int32, device=xyz.device)
+    n_keep = ctypes.c_int64(0)
+    nbytes = lib.ezsp_grid_subsample_workspace_size(n)
+    ws = _workspace(nbytes, xyz.device)
+    _check(lib.ezsp_grid_subsample(_ptr(xyz), n, float(h), _ptr(keep),
+                                   ctypes.byref(n_keep), _ptr(ws), nbytes,
+                                   _stream(xyz.device)),
+           "ezsp_grid_subsample")
+    return keep[:n_keep.value]
+
+
+def edge_loss(emb: torch.Tensor, nbr: torch.Tensor, cls: torch.Tensor,
+              word: torch.Tensor, tau: float, rho: float,
+              want_affinity: bool = True, want_grad: bool = True,
+              want_sampled: bool = True):
+    """Affinity and contrastive edge loss over the kNN pairs.  Returns
+    (stats dict, affinity [n,k] fp32 or None, grad [n,d] fp32 or None,
+    sampled [n,k] uint8 or None)."""
+    lib = load()
+    emb = _dev_tensor(emb, torch.float32, "emb")
+    n, d = emb.shape
+    nbr = _dev_tensor(nbr, torch.int32, "nbr")
+    if nbr.dim() != 2 or nbr.shape[0] != n:
+        raise ValueError("nbr must have shape [n, k]")
+    k = nbr.shape[1]
+    cls = _dev_tensor(cls, torch.int32, "cls")
+    if isinstance(word, torch.Tensor) and word.dtype == torch.uint32:
+        word = word.view(torch.int32)
+    word = _dev_tensor(word, torch.int32, "word (uint32 or its int32 bits)")
+    if cls.shape != (n,) or word.shape != (n, k):
+        raise ValueError("cls must be [n] and word [n, k]")
+    dev = emb.device
+    aff = torch.empty((n, k), dtype=torch.float32, device=dev) \
+        if want_affinity else None
+    grad = torch.empty((n, d), dtype=torch.float32, device=dev) \
+        if want_grad else None
+    smp = torch.empty((n, k), dtype=torch.uint8, device=dev) \
+        if want_sampled else None
+    out = LossStats()
+    nbytes = lib.ezsp_edge_loss_workspace_size(n, k)
+    ws = _workspace(nbytes, dev)
+    _check(lib.ezsp_edge_loss(_ptr(emb), n, d, _ptr(nbr), k, _ptr(cls),
+                              _ptr(word), float(tau), float(rho), _ptr(aff),
+                              _ptr(grad), _ptr(smp), ctypes.byref(out),
+                              _ptr(ws), nbytes, _stream(dev)),
+           "ezsp_edge_loss")
+    stats = {f: getattr(out, f) for f, _ in LossStats._fields_}
+    return stats, aff, grad, smp
+
+
+def purity(labels: torch.Tensor, n_comp: int, cls: torch.Tensor, n_cls: int):
+    """Majority class per superpoint, per-class IoU, mIoU and purity.
+    Returns (stats dict, majority [n_comp] int32, iou [n_cls] fp64)."""
+    lib = load()
+    labels = _dev_tensor(labels, torch.int32, "labels")
+    cls = _dev_tensor(cls, torch.int32, "cls")
+    n = labels.shape[0]
+    if cls.shape != labels.shape:
+        raise ValueError("labels and cls must have the same shape")
+    dev = labels.device
+    maj = torch.empty(int(n_comp), dtype=torch.int32, device=dev)
+    iou = torch.empty(int(n_cls), dtype=torch.float64, device=dev)
+    out = PurityStats()
+    nbytes = lib.ezsp_purity_workspace_size(n, int(n_comp), int(n_cls))
+    ws = _workspace(nbytes, dev)
+    _check(lib.ezsp_purity(_ptr(labels), n, int(n_comp), _ptr(cls),
+                           int(n_cls), _ptr(maj), _ptr(iou), ctypes.byref(out),
+                           _ptr(ws), nbytes, _stream(dev)), "ezsp_purity")
+    stats = {f: getattr(out, f) for f, _ in PurityStats._fields_}
+    return stats, maj, iou

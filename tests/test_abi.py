@@ -136,3 +136,60 @@ def test_params_struct_layout():
     assert ezsp.Params.min_size.offset == 16
     assert ezsp.Params.max_rounds.offset == 24
     assert ezsp.Params.flags.offset == 28
+
+
+def test_grid_loss_purity_reject_bad_arguments():
+    lib = ezsp.load()
+    E, W = ezsp.ERR_INVALID_ARG, ezsp.ERR_WORKSPACE
+    nk = ctypes.byref(ctypes.c_int64(0))
+    assert lib.ezsp_grid_subsample_workspace_size(1000) > 1000 * 4
+    assert lib.ezsp_grid_subsample_workspace_size(0) == 0
+    gs = lib.ezsp_grid_subsample
+    assert gs(None, 10, 0.1, FAKE, nk, FAKE, 1 << 40, None) == E
+    assert gs(FAKE, 10, 0.1, None, nk, FAKE, 1 << 40, None) == E
+    assert gs(FAKE, 10, 0.1, FAKE, None, FAKE, 1 << 40, None) == E
+    assert gs(FAKE, 0, 0.1, FAKE, nk, FAKE, 1 << 40, None) == E
+    assert gs(FAKE, 10, 0.0, FAKE, nk, FAKE, 1 << 40, None) == E
+    assert gs(FAKE, 10, -1.0, FAKE, nk, FAKE, 1 << 40, None) == E
+    assert gs(FAKE, 10, float("inf"), FAKE, nk, FAKE, 1 << 40, None) == E
+    assert gs(FAKE, 10, float("nan"), FAKE, nk, FAKE, 1 << 40, None) == E
+    assert gs(FAKE, 10, 0.1, FAKE, nk, FAKE, 8, None) == W
+
+    assert lib.ezsp_edge_loss_workspace_size(1000, 8) > 1000 * 8
+    assert lib.ezsp_edge_loss_workspace_size(1000, 0) == 0
+    st = ctypes.byref(ezsp.LossStats())
+
+    def loss(n=100, d=8, k=8, tau=1.0, rho=0.3, emb=FAKE, out=st,
+             ws_bytes=1 << 40):
+        return lib.ezsp_edge_loss(emb, n, d, FAKE, k, FAKE, FAKE, tau, rho,
+                                  None, None, None, out, FAKE, ws_bytes, None)
+    assert loss(emb=None) == E
+    assert loss(out=None) == E
+    assert loss(n=0) == E
+    assert loss(d=0) == E
+    assert loss(d=1025) == E
+    assert loss(k=0) == E
+    assert loss(n=300_000_000, k=8) == E
+    assert loss(tau=0.0) == E
+    assert loss(tau=float("inf")) == E
+    assert loss(rho=-0.1) == E
+    assert loss(rho=1.5) == E
+    assert loss(rho=float("nan")) == E
+    assert loss(ws_bytes=8) == W
+
+    assert lib.ezsp_purity_workspace_size(1000, 10, 5) > 0
+    assert lib.ezsp_purity_workspace_size(1000, 0, 5) == 0
+    assert lib.ezsp_purity_workspace_size(1000, 10, 0) == 0
+    ps = ctypes.byref(ezsp.PurityStats())
+    pu = lib.ezsp_purity
+    assert pu(None, 10, 3, FAKE, 2, None, None, ps, FAKE, 1 << 40, None) == E
+    assert pu(FAKE, 10, 3, FAKE, 2, None, None, None, FAKE, 1 << 40, None) == E
+    assert pu(FAKE, 10, 0, FAKE, 2, None, None, ps, FAKE, 1 << 40, None) == E
+    assert pu(FAKE, 10, 3, FAKE, 0, None, None, ps, FAKE, 1 << 40, None) == E
+    assert pu(FAKE, 10, 3, FAKE, 2, None, None, ps, FAKE, 8, None) == W
+
+
+def test_result_struct_layouts():
+    assert ctypes.sizeof(ezsp.LossStats) == 40
+    assert ctypes.sizeof(ezsp.PurityStats) == 24
+    assert ezsp.PurityStats.n_present.offset == 16
