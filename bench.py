@@ -63,6 +63,12 @@ def parse():
     ap.add_argument("--calib-copy", action="store_true",
                     help="after the timed steps, run one plain copy kernel "
                     "of 1 GiB in and 1 GiB out (scale for the HBM counters)")
+    ap.add_argument("--op", default="partition",
+                    choices=["partition", "grid_subsample", "edge_loss",
+                             "purity"],
+                    help="partition (the default) times the whole path; the "
+                    "others time one of the secondary entry points on its "
+                    "own workload and print their own line")
     return ap.parse_args()
 
 
@@ -136,6 +142,119 @@ def cpu_baseline(sc, n_sample):
     }
 
 
+# Secondary entry points, each on the workload of the paper that uses it:
+# grid subsampling at 10 cm of the 3M-point driving tile (the paper's grid
+# for its outdoor sets), and the contrastive loss (tau = 1, rho_intra = 0.3,
+# D = 32, k = 8) and purity of the driving tile with the paper's settings.
+OPS = {
+    "grid_subsample": ("driving-3m", "points/sec grid-subsampled (10 cm)"),
+    "edge_loss": ("driving-3m-paper",
+                  "points/sec through the contrastive edge loss (forward + "
+                  "gradient)"),
+    "purity": ("driving-3m-paper",
+               "points/sec scored (superpoint majority, oracle mIoU)"),
+}
+
+
+def bench_op(args, ezsp, scenes, np, torch):
+    """Times one secondary entry point: args.steps calls after args.warmup,
+    events around the library's launches of that stage."""
+    import oracle
+    name, metric = OPS[args.op]
+    sc = scenes.load(name)
+    dev = torch.device("cuda:0")
+    xyz = torch.from_numpy(sc.xyz).to(dev)
+    if args.op == "grid_subsample":
+        h = 0.10
+
+        def step():
+            return ezsp.grid_subsample(xyz, h)
+
+        def cpu():
+            return oracle.grid_subsample(sc.xyz, h)
+        extra = {"h": h}
+    elif args.op == "edge_loss":
+        nbr = ezsp.knn(xyz, sc.k)
+        emb = torch.from_numpy(sc.emb).to(dev)
+        cls = torch.from_numpy(sc.obj.astype(np.int32)).to(dev)
+        word_np = np.random.default_rng(7).integers(
+            0, 1 << 32, (sc.n, sc.k), dtype=np.uint64).astype(np.uint32)
+        word = torch.from_numpy(word_np.view(np.int32)).to(dev)
+        nbr_np = nbr.cpu().numpy()
+
+        def step():
+            return ezsp.edge_loss(emb, nbr, cls, word, 1.0, 0.3)
+
+        def cpu():
+            return oracle.edge_loss(sc.emb, nbr_np, sc.obj.astype(np.int32),
+                                    word_np, 1.0, 0.3)
+        extra = {"tau": 1.0, "rho_intra": 0.3}
+    else:
+        emb = torch.from_numpy(sc.emb).to(dev)
+        labels, n_comp, _ = ezsp.partition(xyz, emb, sc.k, sc.lambdas,
+                                           min_size=sc.min_size)
+        lab = labels[0].contiguous()
+        nc = int(n_comp[0])
+        cls = torch.from_numpy(sc.obj.astype(np.int32)).to(dev)
+        n_cls = int(sc.obj.max()) + 1
+        lab_np = lab.cpu().numpy()
+
+        def step():
+            return ezsp.purity(lab, nc, cls, n_cls)
+
+        def cpu():
+            return oracle.purity(lab_np, nc, sc.obj.astype(np.int32), n_cls)
+        extra = {"labels": f"level 0 of the partition ({nc} superpoints)",
+                 "n_cls": n_cls}
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    ezsp.profile_enable(True)
+    ezsp.profile_only(args.op)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    launches, ms, nbytes = ezsp.profile_read(args.op)
+    ezsp.profile_enable(False)
+    ezsp.profile_only(None)
+    ms_per_step = (t1 - t0) * 1e3 / args.steps
+    per_ms = ms / max(launches, 1)
+    per_bytes = nbytes / max(launches, 1)
+    achieved = per_bytes / (per_ms * 1e-3) / 1e9 if per_ms > 0 else 0.0
+    out = {
+        "metric": metric, "value": round(sc.n / (ms_per_step / 1e3), 1),
+        "unit": "points/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": {"grid_subsample": "f32", "edge_loss": "f32",
+                  "purity": "int64"}[args.op],
+        "data": "synthetic",
+        "config": {"workload": f"{args.op} on {sc.name}: "
+                               f"{KINDS.get(sc.name, 'synthetic')}, {sc.n} "
+                               f"points, D={sc.d}, k={sc.k}",
+                   "n_points": sc.n, **extra},
+        "roofline": {"bound": "hbm", "kernel": args.op,
+                     "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 5),
+                     "traffic": None, "launch_ms": round(per_ms, 5),
+                     "alg_bytes_per_launch": per_bytes},
+    }
+    if not args.no_cpu:
+        print("[bench] cpu baseline (oracle)", file=sys.stderr, flush=True)
+        c0 = time.perf_counter()
+        cpu()
+        c1 = time.perf_counter()
+        out["cpu_baseline"] = {
+            "value": sc.n / (c1 - c0), "unit": "points/s", "cores": 1,
+            "kind": "oracle",
+            "sample": f"the whole {sc.name} input, one thread, {c1 - c0:.2f} s",
+        }
+    print(json.dumps(out), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -151,6 +270,9 @@ def main():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(1)
     ezsp.load()
+    if args.op != "partition":
+        bench_op(args, ezsp, scenes, np, torch)
+        return
     print(f"[bench] generating {args.workload}", file=sys.stderr, flush=True)
     sc = scenes.load(args.workload)
     dev = torch.device("cuda:0")

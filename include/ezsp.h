@@ -187,7 +187,8 @@ size_t ezsp_edge_loss_workspace_size(int64_t n, int32_t k);
  *   L = sum_intra -log a_pq + sum_inter -log(1 - a_pq)
  * over the unordered pairs of a neighbour table, intra pairs sampled.
  *   emb       n*d fp32 (in), d in 1..1024
- *   nbr       n*k int32 (in): neighbour ids in [0, n) or -1 (empty slot)
+ *   nbr       n*k int32 (in), k in 1..64: neighbour ids in [0, n) or -1
+ *             (empty slot)
  *   cls       n int32 (in): class of every point (only equality matters)
  *   word      n*k uint32 (in): one random word per slot
  *   tau       temperature, finite and > 0; rho in [0, 1]

@@ -287,7 +287,7 @@ int ezsp_grid_subsample(const float *xyz, int64_t n, float h, int32_t *keep,
 }
 
 size_t ezsp_edge_loss_workspace_size(int64_t n, int32_t k) {
-  if (!n_ok(n) || k < 1 || n * (int64_t)k >= kMaxN) return 0;
+  if (!n_ok(n) || k < 1 || k > 64 || n * (int64_t)k >= kMaxN) return 0;
   Arena a;
   a.take<Ctl>(1);
   loss_reserve(a, (int32_t)n, k);
@@ -306,8 +306,8 @@ int ezsp_edge_loss(const float *emb, int64_t n, int32_t d, const int32_t *nbr,
   if (!n_ok(n)) return fail(EZSP_ERR_INVALID_ARG, "n must be in [1, 2^31)");
   if (d < 1 || d > 1024)
     return fail(EZSP_ERR_INVALID_ARG, "d must be in 1..1024");
-  if (k < 1 || n * (int64_t)k >= kMaxN)
-    return fail(EZSP_ERR_INVALID_ARG, "k must be >= 1 with n*k below 2^31");
+  if (k < 1 || k > 64 || n * (int64_t)k >= kMaxN)
+    return fail(EZSP_ERR_INVALID_ARG, "k must be in 1..64 with n*k below 2^31");
   if (n * (int64_t)d >= kMaxN)
     return fail(EZSP_ERR_INVALID_ARG, "n*d must stay below 2^31");
   if (!(tau > 0.0) || !isfinite(tau))

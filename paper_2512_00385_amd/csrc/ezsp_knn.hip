@@ -434,7 +434,7 @@ hipError_t knn_launch(const float *xyz, int32_t n, int32_t k, Ctl *ctl,
   const Tree tree = make_tree(n);
   const int nt = 256;
   const int gb = (n + nt - 1) / nt;
-  hipLaunchKernelGGL(k_bbox, dim3(min(gb, 256)), dim3(nt), 0, st, xyz, n,
+  hipLaunchKernelGGL(k_bbox, dim3(min(gb, 1024)), dim3(nt), 0, st, xyz, n,
                      ctl);
   hipLaunchKernelGGL(k_morton, dim3(gb), dim3(nt), 0, st, xyz, n, ctl, s.keys,
                      s.vals);

@@ -17,13 +17,31 @@
 // Distances, affinities, loss terms and gradient contributions are fp32; the
 // loss is summed in fp64.  -log a is d / tau and -log(1 - a) is
 // -log(-expm1(-d / tau)); the gradient of |e_p - e_q| at e_p = e_q is 0.
+//
+// Layout: a group of G lanes (the power of two >= max(D, k), at most 64) owns
+// one row p of the table, lane i holding embedding dimensions i, i + G, ...;
+// every e_q gather is then one contiguous segment.  The row accumulates the
+// gradient on its own side of every sampled pair it lists in registers; the
+// other end q gets its side from its own row when q lists p too (a mutual
+// pair), and by atomics from the owner slot otherwise.  A slot's 16-bit
+// status carries the pair type, whether it owns the pair, whether the pair is
+// mutual, and where row q lists p, so a mirror slot can read the owner's
+// random word.
 #include "ezsp_internal.h"
 
 namespace ezsp {
 
 namespace {
 
-enum : uint8_t { kSlotNone = 0, kSlotInter = 1, kSlotIntra = 2 };
+// Slot status: bits 0-1 pair type, bit 2 owner, bit 3 mutual, bits 8-15
+// the position of p in row q (mutual pairs).
+enum : uint16_t {
+  kSlotNone = 0,
+  kSlotInter = 1,
+  kSlotIntra = 2,
+  kSlotOwner = 4,
+  kSlotMutual = 8
+};
 
 constexpr int kLeNT = 256;
 constexpr int kLeGrid = 2048;  // grid-stride kernels: one atomic per block
@@ -43,7 +61,8 @@ __device__ __forceinline__ T block_sum(T v, T *sh) {
 // Slot status and the pair counts.
 __global__ __launch_bounds__(kLeNT) void k_le_classify(
     const int32_t *__restrict__ nbr, int32_t n, int32_t k,
-    const int32_t *__restrict__ cls, uint8_t *__restrict__ status, Ctl *ctl) {
+    const int32_t *__restrict__ cls, uint16_t *__restrict__ status,
+    Ctl *ctl) {
   __shared__ unsigned long long sh[kLeNT / kWave];
   const int64_t ns = (int64_t)n * k;
   unsigned long long edges = 0, intra = 0;
@@ -52,21 +71,27 @@ __global__ __launch_bounds__(kLeNT) void k_le_classify(
     const int32_t p = (int32_t)(s / k);
     const int32_t j = (int32_t)(s - (int64_t)p * k);
     const int32_t q = nbr[s];
-    uint8_t v = kSlotNone;
+    uint16_t v = kSlotNone;
     if (q < -1 || q >= n) {
       raise_err(ctl, kErrBadIndex);
     } else if (q >= 0 && q != p) {
-      bool own = true;
+      bool first = true;  // no earlier slot of row p lists q
       const int32_t *row = nbr + (int64_t)p * k;
-      for (int32_t t = 0; t < j && own; ++t) own = row[t] != q;
-      if (own && q < p) {
+      for (int32_t t = 0; t < j && first; ++t) first = row[t] != q;
+      if (first) {
         const int32_t *rq = nbr + (int64_t)q * k;
-        for (int32_t t = 0; t < k && own; ++t) own = rq[t] != p;
-      }
-      if (own) {
+        int32_t jq = -1;
+        for (int32_t t = 0; t < k && jq < 0; ++t)
+          if (rq[t] == p) jq = t;
+        const bool mutual = jq >= 0;
+        const bool owner = p < q || !mutual;
         v = (cls[p] == cls[q]) ? kSlotIntra : kSlotInter;
-        edges += 1;
-        intra += (v == kSlotIntra);
+        if (owner) v |= kSlotOwner;
+        if (mutual) v |= kSlotMutual | (uint16_t)(jq << 8);
+        if (owner) {
+          edges += 1;
+          intra += ((v & 3) == kSlotIntra);
+        }
       }
     }
     status[s] = v;
@@ -105,7 +130,7 @@ __device__ __forceinline__ uint64_t draw_key(const uint32_t *word, int64_t s) {
 // One radix-select pass: histogram of the 8-bit digit at `shift` over the
 // intra keys that match the prefix fixed so far.
 __global__ __launch_bounds__(kLeNT) void k_le_hist(
-    const uint8_t *__restrict__ status, const uint32_t *__restrict__ word,
+    const uint16_t *__restrict__ status, const uint32_t *__restrict__ word,
     int64_t ns, int shift, const Ctl *ctl, uint32_t *hist) {
   if (ctl->sel_mode != 2) return;
   __shared__ uint32_t h[256];
@@ -114,7 +139,7 @@ __global__ __launch_bounds__(kLeNT) void k_le_hist(
   const uint64_t prefix = ctl->sel_prefix, mask = ctl->sel_mask;
   for (int64_t s = blockIdx.x * (int64_t)kLeNT + threadIdx.x; s < ns;
        s += (int64_t)gridDim.x * kLeNT) {
-    if (status[s] != kSlotIntra) continue;
+    if ((status[s] & (3 | kSlotOwner)) != (kSlotIntra | kSlotOwner)) continue;
     const uint64_t key = draw_key(word, s);
     if ((key & mask) == prefix) atomicAdd(&h[(key >> shift) & 255], 1u);
   }
@@ -143,75 +168,136 @@ __global__ __launch_bounds__(256) void k_le_pick(Ctl *ctl, uint32_t *hist,
   }
 }
 
-// Affinity of every slot; loss and gradient of every sampled pair.
-template <bool VEC4>
-__global__ __launch_bounds__(kLeNT) void k_le_edges(
+// Affinity of every slot; loss and gradient of every sampled pair.  G lanes
+// per row (G >= k), NV dimensions per lane (D <= G * NV).  Lane t first reads
+// slot t of the row (id and status, one coalesced load), then the group walks
+// the slots U at a time, with the U embedding gathers issued together.
+constexpr int kLeU = 4;
+
+template <int G, int NV>
+__global__ __launch_bounds__(kLeNT) void k_le_rows(
     const float *__restrict__ emb, int32_t n, int32_t d,
     const int32_t *__restrict__ nbr, int32_t k,
-    const uint8_t *__restrict__ status, const uint32_t *__restrict__ word,
+    const uint16_t *__restrict__ status, const uint32_t *__restrict__ word,
     float tau, const Ctl *sel, float *__restrict__ affinity,
     float *__restrict__ grad, uint8_t *__restrict__ sampled, Ctl *ctl) {
   __shared__ double sh[kLeNT / kWave];
-  const int64_t ns = (int64_t)n * k;
+  constexpr int kRows = kLeNT / G;  // rows per block and step
+  const int lane = threadIdx.x & (G - 1);
   const int mode = sel->sel_mode;
   const uint64_t thr = sel->sel_prefix;
   const float inv_tau = 1.0f / tau;
   double lsum = 0.0;
-  for (int64_t s = blockIdx.x * (int64_t)kLeNT + threadIdx.x; s < ns;
-       s += (int64_t)gridDim.x * kLeNT) {
-    const int32_t q = nbr[s];
-    const uint8_t v = status[s];
-    const bool take =
-        v == kSlotInter ||
-        (v == kSlotIntra && (mode == 1 || (mode == 2 && draw_key(word, s) <= thr)));
-    if (sampled) sampled[s] = take ? 1 : 0;
-    // ids outside [-1, n) were reported by k_le_classify; no read for them
-    if (!take && !(affinity && q >= 0 && q < n)) {
-      if (affinity) affinity[s] = 0.0f;
-      continue;
+  for (int64_t p = (int64_t)blockIdx.x * kRows + threadIdx.x / G; p < n;
+       p += (int64_t)gridDim.x * kRows) {
+    const int32_t my_q = lane < k ? nbr[p * k + lane] : -1;
+    const int32_t my_st = lane < k ? (int32_t)status[p * k + lane] : 0;
+    float ep[NV], acc[NV];
+#pragma unroll
+    for (int v = 0; v < NV; ++v) {
+      const int i = lane + v * G;
+      ep[v] = i < d ? emb[p * d + i] : 0.0f;
+      acc[v] = 0.0f;
     }
-    const int32_t p = (int32_t)(s / k);
-    const float *ep = emb + (int64_t)p * d;
-    const float *eq = emb + (int64_t)q * d;
-    float acc = 0.0f;
-    if (VEC4) {
-      for (int32_t i = 0; i < d; i += 4) {
-        const float4 a = *reinterpret_cast<const float4 *>(ep + i);
-        const float4 b = *reinterpret_cast<const float4 *>(eq + i);
-        const float x = a.x - b.x, y = a.y - b.y, z = a.z - b.z, w = a.w - b.w;
-        acc += x * x + y * y + z * z + w * w;
+    for (int32_t j0 = 0; j0 < k; j0 += kLeU) {
+      int32_t qs[kLeU];
+      float eq[kLeU][NV];
+#pragma unroll
+      for (int u = 0; u < kLeU; ++u) {
+        const int32_t q = __shfl(my_q, j0 + u, G);
+        qs[u] = (j0 + u < k && q >= 0 && q < n) ? q : -1;
+#pragma unroll
+        for (int v = 0; v < NV; ++v) {
+          const int i = lane + v * G;
+          eq[u][v] = (qs[u] >= 0 && i < d) ? emb[(int64_t)qs[u] * d + i] : 0.0f;
+        }
       }
-    } else {
-      for (int32_t i = 0; i < d; ++i) {
-        const float x = ep[i] - eq[i];
-        acc += x * x;
+#pragma unroll
+      for (int u = 0; u < kLeU; ++u) {
+        const int32_t j = j0 + u;
+        if (j >= k) break;
+        const int64_t s = p * k + j;
+        const int32_t q = qs[u];
+        const uint16_t st = (uint16_t)__shfl(my_st, j, G);
+        if (q < 0) {  // empty slot (bad ids were reported already)
+          if (lane == 0) {
+            if (affinity) affinity[s] = 0.0f;
+            if (sampled) sampled[s] = 0;
+          }
+          continue;
+        }
+        float df[NV];
+        float part = 0.0f;
+#pragma unroll
+        for (int v = 0; v < NV; ++v) {
+          df[v] = ep[v] - eq[u][v];
+          part += df[v] * df[v];
+        }
+#pragma unroll
+        for (int off = G / 2; off > 0; off >>= 1)
+          part += __shfl_xor(part, off, G);
+        const float dist = sqrtf(part);
+        const float x = dist * inv_tau;
+        bool take = false;
+        const int type = st & 3;
+        if (type == kSlotInter) {
+          take = true;
+        } else if (type == kSlotIntra) {
+          const int64_t os =
+              (st & kSlotOwner) ? s : (int64_t)q * k + (st >> 8);
+          take = mode == 1 || (mode == 2 && draw_key(word, os) <= thr);
+        }
+        const bool owner = (st & kSlotOwner) != 0;
+        if (lane == 0) {
+          if (affinity) affinity[s] = expf(-x);
+          if (sampled) sampled[s] = (take && owner) ? 1 : 0;
+        }
+        if (!take) continue;
+        float term, coef;
+        if (type == kSlotIntra) {
+          term = x;
+          coef = dist > 0.0f ? inv_tau / dist : 0.0f;
+        } else {
+          term = -logf(-expm1f(-x));
+          coef = dist > 0.0f ? -inv_tau / (expm1f(x) * dist) : 0.0f;
+        }
+        if (owner && lane == 0) lsum += (double)term;
+        if (grad) {
+#pragma unroll
+          for (int v = 0; v < NV; ++v) acc[v] += coef * df[v];
+          if (!(st & kSlotMutual) && coef != 0.0f) {
+            // q does not list p: the owner slot gives q its side
+#pragma unroll
+            for (int v = 0; v < NV; ++v) {
+              const int i = lane + v * G;
+              if (i < d)
+                unsafeAtomicAdd(grad + (int64_t)q * d + i, -coef * df[v]);
+            }
+          }
+        }
       }
     }
-    const float dist = sqrtf(acc);
-    const float x = dist * inv_tau;
-    if (affinity) affinity[s] = expf(-x);
-    if (!take) continue;
-    float term, coef;
-    if (v == kSlotIntra) {
-      term = x;
-      coef = dist > 0.0f ? inv_tau / dist : 0.0f;
-    } else {
-      term = -logf(-expm1f(-x));
-      coef = dist > 0.0f ? -inv_tau / (expm1f(x) * dist) : 0.0f;
-    }
-    lsum += (double)term;
-    if (grad && coef != 0.0f) {
-      float *gp = grad + (int64_t)p * d;
-      float *gq = grad + (int64_t)q * d;
-      for (int32_t i = 0; i < d; ++i) {
-        const float g = coef * (ep[i] - eq[i]);
-        unsafeAtomicAdd(gp + i, g);
-        unsafeAtomicAdd(gq + i, -g);
+    if (grad) {
+#pragma unroll
+      for (int v = 0; v < NV; ++v) {
+        const int i = lane + v * G;
+        if (i < d && acc[v] != 0.0f) unsafeAtomicAdd(grad + p * d + i, acc[v]);
       }
     }
   }
   const double t = block_sum(lsum, sh);
   if (threadIdx.x == 0 && t != 0.0) atomicAdd(&ctl->le_loss, t);
+}
+
+template <int G, int NV>
+void launch_rows(const LossArgs &g, const uint16_t *status, Ctl *ctl,
+                 hipStream_t st) {
+  constexpr int kRows = kLeNT / G;
+  int64_t blocks = ((int64_t)g.n + kRows - 1) / kRows;
+  if (blocks > 16384) blocks = 16384;
+  hipLaunchKernelGGL((k_le_rows<G, NV>), dim3((unsigned)blocks), dim3(kLeNT),
+                     0, st, g.emb, g.n, g.d, g.nbr, g.k, status, g.word,
+                     (float)g.tau, ctl, g.affinity, g.grad, g.sampled, ctl);
 }
 
 __global__ __launch_bounds__(256) void k_fill0(float *x, int64_t count) {
@@ -228,14 +314,14 @@ unsigned grid_for(int64_t items) {
 }  // namespace
 
 void loss_reserve(Arena &a, int32_t n, int32_t k) {
-  a.take<uint8_t>((size_t)n * k);
+  a.take<uint16_t>((size_t)n * k);
   a.take<uint32_t>(256);
 }
 
 int loss_run(const LossArgs &g, LossResult *res, Ctl *ctl, Arena &a,
              hipStream_t st) {
   const int64_t ns = (int64_t)g.n * g.k;
-  uint8_t *status = a.take<uint8_t>((size_t)ns);
+  uint16_t *status = a.take<uint16_t>((size_t)ns);
   uint32_t *hist = a.take<uint32_t>(256);
   Ctl *hc = pinned_ctl();
   if (!hc) {
@@ -248,7 +334,7 @@ int loss_run(const LossArgs &g, LossResult *res, Ctl *ctl, Arena &a,
   if (g.grad)
     hipLaunchKernelGGL(k_fill0, dim3(grid_for((int64_t)g.n * g.d)), dim3(256),
                        0, st, g.grad, (int64_t)g.n * g.d);
-  hipLaunchKernelGGL(k_maxabs, dim3(256), dim3(256), 0, st, g.emb,
+  hipLaunchKernelGGL(k_maxabs, dim3(2048), dim3(256), 0, st, g.emb,
                      (int64_t)g.n * g.d, ctl);
   hipLaunchKernelGGL(k_le_classify, dim3(grid_for(ns)), dim3(kLeNT), 0, st,
                      g.nbr, g.n, g.k, g.cls, status, ctl);
@@ -258,23 +344,24 @@ int loss_run(const LossArgs &g, LossResult *res, Ctl *ctl, Arena &a,
                        status, g.word, ns, shift, ctl, hist);
     hipLaunchKernelGGL(k_le_pick, dim3(1), dim3(256), 0, st, ctl, hist, shift);
   }
-  const bool vec4 = (g.d % 4) == 0 &&
-                    (reinterpret_cast<uintptr_t>(g.emb) & 15) == 0;
-  if (vec4)
-    hipLaunchKernelGGL(k_le_edges<true>, dim3(grid_for(ns)), dim3(kLeNT), 0,
-                       st, g.emb, g.n, g.d, g.nbr, g.k, status, g.word,
-                       (float)g.tau, ctl, g.affinity, g.grad, g.sampled, ctl);
-  else
-    hipLaunchKernelGGL(k_le_edges<false>, dim3(grid_for(ns)), dim3(kLeNT), 0,
-                       st, g.emb, g.n, g.d, g.nbr, g.k, status, g.word,
-                       (float)g.tau, ctl, g.affinity, g.grad, g.sampled, ctl);
+  // lanes per row: the power of two covering both D (up to 64) and k
+  const int32_t span = g.d < 64 ? (g.d > g.k ? g.d : g.k) : 64;
+  if (span <= 4) launch_rows<4, 1>(g, status, ctl, st);
+  else if (span <= 8) launch_rows<8, 1>(g, status, ctl, st);
+  else if (span <= 16) launch_rows<16, 1>(g, status, ctl, st);
+  else if (span <= 32) launch_rows<32, 1>(g, status, ctl, st);
+  else if (g.d <= 64) launch_rows<64, 1>(g, status, ctl, st);
+  else if (g.d <= 128) launch_rows<64, 2>(g, status, ctl, st);
+  else if (g.d <= 256) launch_rows<64, 4>(g, status, ctl, st);
+  else if (g.d <= 512) launch_rows<64, 8>(g, status, ctl, st);
+  else launch_rows<64, 16>(g, status, ctl, st);
   prof_end(st);
   int rc = read_ctl(ctl, hc, st);
   if (rc) return rc;
-  // algorithmic bytes: the table, the words and the classes read once, each
-  // pair's two embedding rows, the per-slot outputs and the gradient
+  // algorithmic bytes: every input read once (embeddings, table, words,
+  // classes) and every output written once
   prof_bytes("edge_loss",
-             ns * 8.0 + 4.0 * g.n + 8.0 * g.d * (double)hc->le_edges +
+             4.0 * g.n * g.d + 8.0 * ns + 4.0 * g.n +
                  (g.affinity ? 4.0 * ns : 0.0) + (g.sampled ? 1.0 * ns : 0.0) +
                  (g.grad ? 4.0 * g.n * g.d : 0.0));
   if (hc->err & kErrNonFinite) {

@@ -109,28 +109,44 @@ __global__ __launch_bounds__(kPuNT) void k_pu_count(
   }
 }
 
-// IoU per class in parallel, then the mean in class order by one thread.
+// IoU per class in parallel, staged in LDS a chunk of classes at a time,
+// then the mean in class order by one thread.
+constexpr int kPuChunk = 4096;
+
 __global__ __launch_bounds__(kPuNT) void k_pu_final(
     const unsigned long long *cnt, int32_t n_cls, int32_t n, double *iou,
     Ctl *ctl) {
-  for (int32_t c = threadIdx.x; c < n_cls; c += kPuNT) {
-    const unsigned long long tp = cnt[c], gt = cnt[n_cls + c],
-                             pr = cnt[2 * n_cls + c];
-    iou[c] = gt ? __ddiv_rn((double)tp, (double)(gt + pr - tp))
-                : __builtin_nan("");
-  }
-  __syncthreads();
-  if (threadIdx.x != 0) return;
+  __shared__ double v[kPuChunk];
+  __shared__ unsigned long long tps[kPuNT];
   double sum = 0.0;
   int64_t present = 0;
-  unsigned long long tp_all = 0;
-  for (int32_t c = 0; c < n_cls; ++c) {
-    tp_all += cnt[c];
-    if (cnt[n_cls + c]) {
-      sum = __dadd_rn(sum, iou[c]);
-      ++present;
+  unsigned long long tp_mine = 0;
+  for (int32_t base = 0; base < n_cls; base += kPuChunk) {
+    const int32_t len = min(kPuChunk, n_cls - base);
+    for (int32_t i = threadIdx.x; i < len; i += kPuNT) {
+      const int32_t c = base + i;
+      const unsigned long long tp = cnt[c], gt = cnt[n_cls + c],
+                               pr = cnt[2 * n_cls + c];
+      tp_mine += tp;
+      const double x = gt ? __ddiv_rn((double)tp, (double)(gt + pr - tp))
+                          : __builtin_nan("");
+      iou[c] = x;
+      v[i] = x;
     }
+    __syncthreads();
+    if (threadIdx.x == 0)
+      for (int32_t i = 0; i < len; ++i)
+        if (v[i] == v[i]) {  // present classes (absent ones are NaN)
+          sum = __dadd_rn(sum, v[i]);
+          ++present;
+        }
+    __syncthreads();
   }
+  tps[threadIdx.x] = tp_mine;
+  __syncthreads();
+  if (threadIdx.x != 0) return;
+  unsigned long long tp_all = 0;
+  for (int t = 0; t < kPuNT; ++t) tp_all += tps[t];
   ctl->pu_miou = __ddiv_rn(sum, (double)present);
   ctl->pu_purity = __ddiv_rn((double)tp_all, (double)n);
   ctl->pu_present = present;

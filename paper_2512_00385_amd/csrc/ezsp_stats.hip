@@ -83,11 +83,11 @@ int stats_run(const int32_t *labels, int32_t n, int32_t nc, const float *emb,
     return -5;
   }
   hipLaunchKernelGGL(k_ctl_init, dim3(1), dim3(64), 0, st, cx);
-  hipLaunchKernelGGL(k_maxabs, dim3(256), dim3(256), 0, st, emb,
+  hipLaunchKernelGGL(k_maxabs, dim3(2048), dim3(256), 0, st, emb,
                      (int64_t)n * d, ctl);
   hipLaunchKernelGGL(k_fixshift, dim3(1), dim3(64), 0, st, ctl, n);
   if (xyz) {
-    hipLaunchKernelGGL(k_maxabs, dim3(256), dim3(256), 0, st, xyz,
+    hipLaunchKernelGGL(k_maxabs, dim3(2048), dim3(256), 0, st, xyz,
                        (int64_t)n * 3, cx);
     hipLaunchKernelGGL(k_fixshift, dim3(1), dim3(64), 0, st, cx, n);
   }

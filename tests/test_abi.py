@@ -169,6 +169,7 @@ def test_grid_loss_purity_reject_bad_arguments():
     assert loss(d=0) == E
     assert loss(d=1025) == E
     assert loss(k=0) == E
+    assert loss(k=65) == E
     assert loss(n=300_000_000, k=8) == E
     assert loss(tau=0.0) == E
     assert loss(tau=float("inf")) == E
