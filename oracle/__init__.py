@@ -67,6 +67,10 @@ def _load():
                               P, P]),
         "or_partition": (ctypes.c_int, [P, i64, i32, i64, P, P, P, i32, P, P,
                                         i32, P, P, P, P, i64, P]),
+        "or_partition_linked": (ctypes.c_int, [P, P, i64, i32, i64, P, P, P,
+                                               i32, P, P, i32, i32, P, P, P,
+                                               P, i64, P]),
+        "or_link_isolated": (i64, [i64, i64, P, P, P, P, i32, P, P]),
         "or_energy": (dbl, [P, i64, i32, i32, P, i64, i64, P, P, P, dbl]),
         "or_component_stats": (ctypes.c_int, [P, i64, i64, P, i32, P, P, P,
                                               P]),
@@ -226,8 +230,9 @@ def contract(lo, hi, w, size, S, label, nc: int):
 # --------------------------------------------------------------------------
 
 def partition_graph(emb, lo, hi, w, lambdas, min_size=None, max_rounds=0,
-                    want_log=False, want_energy=True):
-    """Round-synchronous merge ladder on a given graph.
+                    want_log=False, want_energy=True, xyz=None, link_k=0):
+    """Round-synchronous merge ladder on a given graph; with link_k > 0 and
+    positions xyz, isolated nodes are linked first in every round.
 
     Returns (labels [L,n] int32, n_comp [L] int64, energy [L] or None,
     log list of dicts or None)."""
@@ -246,11 +251,20 @@ def partition_graph(emb, lo, hi, w, lambdas, min_size=None, max_rounds=0,
     cap = 4096 if want_log else 0
     log = (RoundLog * max(cap, 1))()
     log_len = ctypes.c_int64(0)
-    rc = lib.or_partition(_p(emb), n, d, lo.shape[0], _p(lo), _p(hi), _p(w),
-                          L, _p(lam), _p(ms), int(max_rounds), _p(labels),
-                          _p(n_comp), _p(energy),
-                          ctypes.addressof(log) if want_log else None, cap,
-                          ctypes.addressof(log_len))
+    if link_k:
+        xyz = _c(xyz, np.float32).reshape(-1, 3)
+        rc = lib.or_partition_linked(
+            _p(emb), _p(xyz), n, d, lo.shape[0], _p(lo), _p(hi), _p(w), L,
+            _p(lam), _p(ms), int(link_k), int(max_rounds), _p(labels),
+            _p(n_comp), _p(energy),
+            ctypes.addressof(log) if want_log else None, cap,
+            ctypes.addressof(log_len))
+    else:
+        rc = lib.or_partition(_p(emb), n, d, lo.shape[0], _p(lo), _p(hi),
+                              _p(w), L, _p(lam), _p(ms), int(max_rounds),
+                              _p(labels), _p(n_comp), _p(energy),
+                              ctypes.addressof(log) if want_log else None,
+                              cap, ctypes.addressof(log_len))
     if rc:
         raise OracleError(rc, "partition")
     rounds = None
@@ -261,12 +275,29 @@ def partition_graph(emb, lo, hi, w, lambdas, min_size=None, max_rounds=0,
 
 
 def partition(xyz, emb, k: int, lambdas, min_size=None, max_rounds=0,
-              want_log=False, want_energy=True, knn_method="kdtree"):
-    """kNN graph, then the ladder: the whole path the GPU library computes."""
+              want_log=False, want_energy=True, knn_method="kdtree",
+              link=False):
+    """kNN graph, then the ladder: the whole path the GPU library computes
+    (link: prepare_graph's linking of isolated nodes with the same k)."""
     nbr, _ = knn(xyz, k, knn_method)
     lo, hi, w = graph(nbr)
     return partition_graph(emb, lo, hi, w, lambdas, min_size, max_rounds,
-                           want_log, want_energy)
+                           want_log, want_energy, xyz=xyz,
+                           link_k=k if link else 0)
+
+
+def link_isolated(lo, hi, size, Sx, k: int):
+    """One linking step: the new (lo, hi) pairs for the isolated nodes."""
+    lo, hi = _c(lo, np.int32), _c(hi, np.int32)
+    size, Sx = _c(size, np.int64), _c(Sx, np.int64).reshape(-1, 3)
+    nn = size.shape[0]
+    lo_o = np.empty(max(nn * k, 1), np.int32)
+    hi_o = np.empty(max(nn * k, 1), np.int32)
+    m = _load().or_link_isolated(nn, lo.shape[0], _p(lo), _p(hi), _p(size),
+                                 _p(Sx), int(k), _p(lo_o), _p(hi_o))
+    if m < 0:
+        raise OracleError(m, "link_isolated")
+    return lo_o[:m].copy(), hi_o[:m].copy()
 
 
 def energy(emb, label, lo, hi, w, lam: float, F: int | None = None):

@@ -532,19 +532,139 @@ double or_energy(const float *emb, int64_t n, int32_t d, int32_t F,
 }
 
 /* ======================================================================== */
+/* prepare_graph's linking of isolated nodes (App. Alg. A-2).  Reading R7:   */
+/* when more than one node is left, every node without an edge gets an edge */
+/* of weight 1 to each of its min(k, nn - 1) nearest other nodes, nearest by */
+/* the squared distance of their centroids and then by the smaller id; a    */
+/* pair linked from both ends is one edge.  Centroids are exact: position   */
+/* sums in int64 fixed point, c = (double)Sx / |P| per axis, and the        */
+/* squared distance ((dx*dx) + (dy*dy)) + (dz*dz) in fp64.                   */
+/* ======================================================================== */
+
+typedef struct {
+  double d2;
+  int32_t id;
+} near_rec;
+
+static int near_cmp(const void *x, const void *y) {
+  const near_rec *a = (const near_rec *)x, *b = (const near_rec *)y;
+  if (a->d2 != b->d2) return (a->d2 < b->d2) ? -1 : 1;
+  return (a->id < b->id) ? -1 : (a->id > b->id);
+}
+
+static double centroid_axis(const int64_t *Sx, const int64_t *size, int64_t v,
+                            int a) {
+  return (double)Sx[3 * v + a] / (double)size[v];
+}
+
+int64_t or_link_isolated(int64_t nn, int64_t ne, const int32_t *lo,
+                         const int32_t *hi, const int64_t *size,
+                         const int64_t *Sx, int32_t k, int32_t *lo_out,
+                         int32_t *hi_out) {
+  if (nn < 2 || k < 1) return 0;
+  char *has = (char *)calloc((size_t)nn, 1);
+  near_rec *nr = (near_rec *)malloc(sizeof(near_rec) * (size_t)nn);
+  if (!has || !nr) {
+    free(has);
+    free(nr);
+    return OR_ENOMEM;
+  }
+  for (int64_t e = 0; e < ne; ++e) has[lo[e]] = has[hi[e]] = 1;
+  int64_t take = (k < nn - 1) ? k : nn - 1;
+  edge_t *L = NULL;
+  int64_t m = 0, cap = 0;
+  for (int64_t v = 0; v < nn; ++v) {
+    if (has[v]) continue;
+    int64_t c = 0;
+    for (int64_t u = 0; u < nn; ++u) {
+      if (u == v) continue;
+      double dx = centroid_axis(Sx, size, u, 0) - centroid_axis(Sx, size, v, 0);
+      double dy = centroid_axis(Sx, size, u, 1) - centroid_axis(Sx, size, v, 1);
+      double dz = centroid_axis(Sx, size, u, 2) - centroid_axis(Sx, size, v, 2);
+      double xx = dx * dx, yy = dy * dy, zz = dz * dz;
+      double t = xx + yy;
+      nr[c].d2 = t + zz;
+      nr[c].id = (int32_t)u;
+      ++c;
+    }
+    qsort(nr, (size_t)c, sizeof(near_rec), near_cmp);
+    if (m + take > cap) {
+      cap = 2 * (m + take);
+      edge_t *t = (edge_t *)realloc(L, sizeof(edge_t) * (size_t)cap);
+      if (!t) {
+        free(L);
+        free(has);
+        free(nr);
+        return OR_ENOMEM;
+      }
+      L = t;
+    }
+    for (int64_t i = 0; i < take; ++i) {
+      int32_t u = nr[i].id;
+      L[m].lo = (u < v) ? u : (int32_t)v;
+      L[m].hi = (u < v) ? (int32_t)v : u;
+      L[m].w = 1;
+      ++m;
+    }
+  }
+  /* one edge per pair; both ends were isolated, so no weight is added */
+  if (m > 0) qsort(L, (size_t)m, sizeof(edge_t), edge_cmp);
+  int64_t out = 0;
+  for (int64_t i = 0; i < m; ++i) {
+    if (out > 0 && L[i].lo == lo_out[out - 1] && L[i].hi == hi_out[out - 1])
+      continue;
+    lo_out[out] = L[i].lo;
+    hi_out[out] = L[i].hi;
+    ++out;
+  }
+  free(L);
+  free(has);
+  free(nr);
+  return out;
+}
+
+/* ======================================================================== */
 /* The ladder: Steps 0-4 until no candidate merge (Step 1), no edge or one   */
 /* component (Alg. A-2 early exits); level l+1 runs on level l's result.     */
 /* ======================================================================== */
 
-int or_partition(const float *emb, int64_t n, int32_t d, int64_t ne,
-                 const int32_t *lo, const int32_t *hi, const int64_t *w,
-                 int32_t L, const double *lambdas, const int64_t *min_size,
-                 int32_t max_rounds, int32_t *labels, int64_t *n_comp,
-                 double *energy, or_round_log *log, int64_t log_cap,
-                 int64_t *log_len) {
+static int grow_edges(int64_t need, size_t *cap, int32_t **a, int32_t **b,
+                      int64_t **c, int32_t **a2, int32_t **b2, int64_t **c2,
+                      double **dl) {
+  if ((size_t)need <= *cap) return OR_OK;
+  size_t nc = (size_t)need * 2;
+  void *p[7] = {realloc(*a, nc * sizeof(int32_t)), NULL, NULL, NULL, NULL,
+                NULL, NULL};
+  if (p[0]) *a = (int32_t *)p[0];
+  p[1] = realloc(*b, nc * sizeof(int32_t));
+  if (p[1]) *b = (int32_t *)p[1];
+  p[2] = realloc(*c, nc * sizeof(int64_t));
+  if (p[2]) *c = (int64_t *)p[2];
+  p[3] = realloc(*a2, nc * sizeof(int32_t));
+  if (p[3]) *a2 = (int32_t *)p[3];
+  p[4] = realloc(*b2, nc * sizeof(int32_t));
+  if (p[4]) *b2 = (int32_t *)p[4];
+  p[5] = realloc(*c2, nc * sizeof(int64_t));
+  if (p[5]) *c2 = (int64_t *)p[5];
+  p[6] = realloc(*dl, nc * sizeof(double));
+  if (p[6]) *dl = (double *)p[6];
+  for (int i = 0; i < 7; ++i)
+    if (!p[i]) return OR_ENOMEM;
+  *cap = nc;
+  return OR_OK;
+}
+
+static int partition_impl(const float *emb, const float *xyz, int64_t n,
+                          int32_t d, int64_t ne, const int32_t *lo,
+                          const int32_t *hi, const int64_t *w, int32_t L,
+                          const double *lambdas, const int64_t *min_size,
+                          int32_t link_k, int32_t max_rounds, int32_t *labels,
+                          int64_t *n_comp, double *energy, or_round_log *log,
+                          int64_t log_cap, int64_t *log_len) {
   if (!emb || n < 1 || n > INT32_MAX || d < 1 || d > 64 || ne < 0 ||
       L < 1 || !lambdas || !labels || !n_comp || (ne > 0 && (!lo || !hi || !w)))
     return OR_EINVAL;
+  if (link_k < 0 || (link_k > 0 && !xyz)) return OR_EINVAL;
   for (int32_t l = 0; l < L; ++l)
     if (!isfinite(lambdas[l]) || lambdas[l] < 0.0) return OR_EINVAL;
   for (int64_t e = 0; e < ne; ++e)
@@ -554,6 +674,11 @@ int or_partition(const float *emb, int64_t n, int32_t d, int64_t ne,
   if (max_rounds <= 0) max_rounds = 256;
   int32_t F = or_fixed_shift(emb, n, d);
   if (F < 0) return F;
+  int32_t G = 0; /* fixed-point shift of the positions (linking only) */
+  if (link_k > 0) {
+    G = or_fixed_shift(xyz, n, 3);
+    if (G < 0) return G;
+  }
   if (log_len) *log_len = 0;
 
   /* Step 0: every point is its own superpoint, the adjacency is E. */
@@ -573,9 +698,19 @@ int or_partition(const float *emb, int64_t n, int32_t d, int64_t ne,
   int32_t *target = (int32_t *)malloc(sizeof(int32_t) * (size_t)n);
   int32_t *label = (int32_t *)malloc(sizeof(int32_t) * (size_t)n);
   int32_t *plabel = (int32_t *)malloc(sizeof(int32_t) * (size_t)n);
+  int64_t *Sx = NULL;
+  int32_t *llo = NULL, *lhi = NULL;
+  char *has = NULL;
+  if (link_k > 0) {
+    Sx = (int64_t *)malloc(sizeof(int64_t) * (size_t)(3 * n));
+    llo = (int32_t *)malloc(sizeof(int32_t) * (size_t)n * (size_t)link_k);
+    lhi = (int32_t *)malloc(sizeof(int32_t) * (size_t)n * (size_t)link_k);
+    has = (char *)malloc((size_t)n);
+  }
   int rc = OR_OK;
   if (!size || !S || !size2 || !S2 || !elo || !ehi || !ew || !elo2 || !ehi2 ||
-      !ew2 || !delta || !target || !label || !plabel) {
+      !ew2 || !delta || !target || !label || !plabel ||
+      (link_k > 0 && (!Sx || !llo || !lhi || !has))) {
     rc = OR_ENOMEM;
     goto done;
   }
@@ -593,6 +728,35 @@ int or_partition(const float *emb, int64_t n, int32_t d, int64_t ne,
     double lambda = lambdas[l];
     int64_t smin = min_size ? min_size[l] : 0;
     for (int32_t round = 0;; ++round) {
+      if (link_k > 0 && nn > 1) {
+        /* prepare_graph: link the nodes that have no edge (reading R7) */
+        memset(has, 0, (size_t)nn);
+        for (int64_t e = 0; e < me; ++e) has[elo[e]] = has[ehi[e]] = 1;
+        int64_t iso = 0;
+        for (int64_t v = 0; v < nn; ++v) iso += !has[v];
+        if (iso > 0) {
+          memset(Sx, 0, sizeof(int64_t) * (size_t)(3 * nn));
+          for (int64_t p = 0; p < n; ++p)
+            for (int a = 0; a < 3; ++a)
+              Sx[3 * (int64_t)plabel[p] + a] +=
+                  (int64_t)llrint(ldexp((double)xyz[3 * p + a], G));
+          int64_t nl = or_link_isolated(nn, me, elo, ehi, size, Sx, link_k,
+                                        llo, lhi);
+          if (nl < 0) {
+            rc = (int)nl;
+            goto done;
+          }
+          rc = grow_edges(me + nl, &ecap, &elo, &ehi, &ew, &elo2, &ehi2, &ew2,
+                          &delta);
+          if (rc) goto done;
+          for (int64_t i = 0; i < nl; ++i) {
+            elo[me + i] = llo[i];
+            ehi[me + i] = lhi[i];
+            ew[me + i] = 1;
+          }
+          me += nl;
+        }
+      }
       if (me == 0) break; /* no edge left: nothing can merge */
       if (round >= max_rounds) {
         rc = OR_ENOTCONV;
@@ -693,7 +857,35 @@ done:
   free(target);
   free(label);
   free(plabel);
+  free(Sx);
+  free(llo);
+  free(lhi);
+  free(has);
   return rc;
+}
+
+int or_partition(const float *emb, int64_t n, int32_t d, int64_t ne,
+                 const int32_t *lo, const int32_t *hi, const int64_t *w,
+                 int32_t L, const double *lambdas, const int64_t *min_size,
+                 int32_t max_rounds, int32_t *labels, int64_t *n_comp,
+                 double *energy, or_round_log *log, int64_t log_cap,
+                 int64_t *log_len) {
+  return partition_impl(emb, NULL, n, d, ne, lo, hi, w, L, lambdas, min_size,
+                        0, max_rounds, labels, n_comp, energy, log, log_cap,
+                        log_len);
+}
+
+int or_partition_linked(const float *emb, const float *xyz, int64_t n,
+                        int32_t d, int64_t ne, const int32_t *lo,
+                        const int32_t *hi, const int64_t *w, int32_t L,
+                        const double *lambdas, const int64_t *min_size,
+                        int32_t link_k, int32_t max_rounds, int32_t *labels,
+                        int64_t *n_comp, double *energy, or_round_log *log,
+                        int64_t log_cap, int64_t *log_len) {
+  if (!xyz || link_k < 1) return OR_EINVAL;
+  return partition_impl(emb, xyz, n, d, ne, lo, hi, w, L, lambdas, min_size,
+                        link_k, max_rounds, labels, n_comp, energy, log,
+                        log_cap, log_len);
 }
 
 /* ======================================================================== */
@@ -738,7 +930,7 @@ int or_component_stats(const int32_t *label, int64_t n, int64_t nc,
 
 /* ======================================================================== */
 /* Grid subsampling (Sec. 4.1 subsamples every cloud on a regular grid      */
-/* before partitioning).  Reading R11: the cell of a point is               */
+/* before partitioning).  Reading R13: the cell of a point is               */
 /* floor((x_i - o_i) / h) per axis in IEEE fp32, o the coordinate-wise      */
 /* minimum of the cloud; the point kept for a cell is its smallest index;   */
 /* kept indices are returned in increasing order.                           */
@@ -800,17 +992,17 @@ int64_t or_grid_subsample(const float *xyz, int64_t n, float h,
 
 /* ======================================================================== */
 /* Affinity and contrastive edge loss (Sec. 3.1, Eq. softmax and Eq. loss). */
-/* Readings R12-R15:                                                        */
-/*   R12 the edges are the unordered pairs of the kNN relation (as R2); an  */
+/* Readings R14-R17:                                                        */
+/*   R14 the edges are the unordered pairs of the kNN relation (as R2); an  */
 /*       edge belongs to the smallest slot p*k + j that lists it, and that  */
 /*       slot's random word draws it.                                        */
-/*   R13 with rho < 1 the sample keeps m = min(n_intra,                      */
+/*   R15 with rho < 1 the sample keeps m = min(n_intra,                      */
 /*       floor(rho * n_inter / (1 - rho))) intra edges, those with the       */
 /*       smallest (word, slot); rho = 1 keeps them all.  Every inter edge is */
 /*       kept.                                                               */
-/*   R14 -log(a) = d / tau and -log(1 - a) = -log(-expm1(-d / tau)); the     */
+/*   R16 -log(a) = d / tau and -log(1 - a) = -log(-expm1(-d / tau)); the     */
 /*       loss is the plain sum over the sampled edges.                       */
-/*   R15 the gradient of |e_p - e_q| at e_p = e_q is taken as 0.             */
+/*   R17 the gradient of |e_p - e_q| at e_p = e_q is taken as 0.             */
 /* ======================================================================== */
 
 typedef struct {
@@ -887,7 +1079,7 @@ int or_edge_loss(const float *emb, int64_t n, int32_t d, const int32_t *nbr,
     if (i == 0 || pr[i].a != pr[i - 1].a || pr[i].b != pr[i - 1].b)
       pr[ne++] = pr[i];
 
-  /* R13: the intra-edge sample */
+  /* R15: the intra-edge sample */
   int64_t n_intra = 0, n_inter = 0;
   for (int64_t e = 0; e < ne; ++e) {
     if (cls[pr[e].a] == cls[pr[e].b]) ++n_intra;
@@ -966,7 +1158,7 @@ int or_edge_loss(const float *emb, int64_t n, int32_t d, const int32_t *nbr,
 
 /* ======================================================================== */
 /* Partition purity and oracle mIoU (Sec. 4.2 "Metrics": each superpoint    */
-/* takes its majority ground-truth label).  Reading R16: a majority tie     */
+/* takes its majority ground-truth label).  Reading R18: a majority tie     */
 /* goes to the smallest class; IoU_c = TP / (|gt = c| + |pred = c| - TP)    */
 /* over the classes present in the ground truth, averaged in class order;   */
 /* purity = sum TP / n.                                                     */

@@ -37,20 +37,24 @@
  *   R5  conflict removal keeps, per node, the incident candidate edge that is
  *       largest under (Delta desc, lo asc, hi asc).
  *   R6  |P| < s_min is strict; s_min <= 1 disables it.
- *   R7  "connect isolated nodes" is not applied.
+ *   R7  "connect isolated nodes" (prepare_graph), when asked for: at the
+ *       start of every round with more than one node, each node without an
+ *       edge gets an edge of weight 1 to each of its min(k, nn-1) nearest
+ *       nodes (squared distance of exact fixed-point centroids in fp64, then
+ *       the smaller id); a pair linked from both ends is one edge.
  *   R8  the cut term counts edges whose end points lie in different
  *       components.
  *   R9  level l+1 starts from level l's contracted graph and statistics.
  *   R10 Delta > 0 is strict.
- *   R11 grid cells are floor((x_i - o_i) / h) in IEEE fp32 with o the
+ *   R13 grid cells are floor((x_i - o_i) / h) in IEEE fp32 with o the
  *       coordinate-wise minimum; each cell keeps its smallest point index.
- *   R12 loss edges are the unordered kNN pairs; an edge belongs to the
+ *   R14 loss edges are the unordered kNN pairs; an edge belongs to the
  *       smallest slot p*k + j that lists it, whose random word draws it.
- *   R13 rho < 1 keeps the m = min(n_intra, floor(rho*n_inter/(1-rho)))
+ *   R15 rho < 1 keeps the m = min(n_intra, floor(rho*n_inter/(1-rho)))
  *       intra edges with the smallest (word, slot); rho = 1 keeps all.
- *   R14 -log(a) = d/tau, -log(1 - a) = -log(-expm1(-d/tau)), summed.
- *   R15 the gradient of |e_p - e_q| at e_p = e_q is 0.
- *   R16 majority ties go to the smallest class; IoU over the classes present
+ *   R16 -log(a) = d/tau, -log(1 - a) = -log(-expm1(-d/tau)), summed.
+ *   R17 the gradient of |e_p - e_q| at e_p = e_q is 0.
+ *   R18 majority ties go to the smallest class; IoU over the classes present
  *       in the ground truth; purity = matched points / n.
  *
  * Conventions: all pointers are host pointers owned by the caller.
@@ -154,6 +158,24 @@ int or_partition(const float *emb, int64_t n, int32_t d, int64_t ne,
                  double *energy, or_round_log *log, int64_t log_cap,
                  int64_t *log_len);
 
+/* The same ladder with prepare_graph's linking of isolated nodes (reading
+ * R7): xyz n*3 fp32 positions, link_k >= 1 neighbours per isolated node. */
+int or_partition_linked(const float *emb, const float *xyz, int64_t n,
+                        int32_t d, int64_t ne, const int32_t *lo,
+                        const int32_t *hi, const int64_t *w, int32_t L,
+                        const double *lambdas, const int64_t *min_size,
+                        int32_t link_k, int32_t max_rounds, int32_t *labels,
+                        int64_t *n_comp, double *energy, or_round_log *log,
+                        int64_t log_cap, int64_t *log_len);
+
+/* One linking step (reading R7) on nn nodes and ne edges: size nn, Sx nn*3
+ * int64 position sums.  lo_out/hi_out (capacity nn*k) receive the new pairs
+ * sorted by (lo, hi).  Returns their count. */
+int64_t or_link_isolated(int64_t nn, int64_t ne, const int32_t *lo,
+                         const int32_t *hi, const int64_t *size,
+                         const int64_t *Sx, int32_t k, int32_t *lo_out,
+                         int32_t *hi_out);
+
 /* Eq. gmpp evaluated for a labelling (direct form, fp64).  Means are the
  * fixed-point means ((double)S_C / |C|) * 2^-F.  The cut term runs over the
  * given edges. */
@@ -169,7 +191,7 @@ int or_component_stats(const int32_t *label, int64_t n, int64_t nc,
                        const float *emb, int32_t d, const float *xyz,
                        int64_t *size, float *mean, float *centroid);
 
-/* ---- grid subsampling (Sec. 4.1; reading R11) ---------------------------- */
+/* ---- grid subsampling (Sec. 4.1; reading R13) ---------------------------- */
 
 /* keep: capacity n, receives the kept point indices in increasing order.
  * Returns the kept count, or -1 (bad argument), -2 (non-finite coordinate),
@@ -177,7 +199,7 @@ int or_component_stats(const int32_t *label, int64_t n, int64_t nc,
 int64_t or_grid_subsample(const float *xyz, int64_t n, float h,
                           int32_t *keep);
 
-/* ---- affinity and contrastive loss (Sec. 3.1; readings R12-R15) ---------- */
+/* ---- affinity and contrastive loss (Sec. 3.1; readings R14-R17) ---------- */
 
 typedef struct {
   double loss;          /* Eq. loss over the sampled edges              */
@@ -197,7 +219,7 @@ int or_edge_loss(const float *emb, int64_t n, int32_t d, const int32_t *nbr,
                  double tau, double rho, double *affinity, double *grad,
                  uint8_t *sampled, or_loss_out *out);
 
-/* ---- purity and oracle mIoU (Sec. 4.2 "Metrics"; reading R16) ------------- */
+/* ---- purity and oracle mIoU (Sec. 4.2 "Metrics"; reading R18) ------------- */
 
 typedef struct {
   double miou;       /* mean IoU over the classes present          */

@@ -13,7 +13,7 @@ import oracle
 
 
 # --------------------------------------------------------------------------
-# grid subsampling (reading R11)
+# grid subsampling (reading R13)
 # --------------------------------------------------------------------------
 
 def test_grid_hand_example():
@@ -79,7 +79,7 @@ def test_grid_limits():
 
 
 # --------------------------------------------------------------------------
-# affinity and contrastive loss (readings R12-R15)
+# affinity and contrastive loss (readings R14-R17)
 # --------------------------------------------------------------------------
 
 def _two_points(c0, c1, tau, rho=1.0):
@@ -211,7 +211,7 @@ def test_loss_rejects():
 
 
 # --------------------------------------------------------------------------
-# purity and oracle mIoU (reading R16)
+# purity and oracle mIoU (reading R18)
 # --------------------------------------------------------------------------
 
 def test_purity_hand_example():
@@ -260,3 +260,75 @@ def test_purity_special_partitions():
     # an empty component has no majority
     res, maj, _ = oracle.purity(np.zeros(400, np.int32), 2, cls, 5)
     assert maj[1] == -1
+
+
+# --------------------------------------------------------------------------
+# prepare_graph's linking of isolated nodes (reading R7)
+# --------------------------------------------------------------------------
+
+def _two_clusters():
+    a = np.array([[0, 0, 0], [0.1, 0, 0], [0, 0.1, 0]], np.float32)
+    g = np.stack(np.meshgrid(np.arange(4), np.arange(3), [0],
+                             indexing="ij"), -1).reshape(-1, 3)
+    b = (np.array([10.0, 0, 0]) + 0.1 * g).astype(np.float32)
+    xyz = np.concatenate([a, b])
+    emb = np.concatenate([np.zeros((3, 1)), np.full((12, 1), 10.0)])
+    return xyz, emb.astype(np.float32)
+
+
+def test_link_hand_example_with_min_size():
+    # k = 2 keeps the 3-point and the 12-point cluster apart in the kNN graph.
+    # Level 0 (lambda 0.1) merges each cluster; the two nodes are isolated,
+    # so linking joins them with w = 1, but the gain 0.1 - (3*12/15)*100 < 0
+    # keeps them apart.  Level 1 has s_min = 5: the 3-point node is a
+    # candidate whatever its gain and merges into the other.  Without
+    # linking it has no edge and stays alone.
+    xyz, emb = _two_clusters()
+    lam, smin = [0.1, 0.1], [0, 5]
+    lab, nc, en, _ = oracle.partition(xyz, emb, 2, lam, smin, link=True)
+    assert nc.tolist() == [2, 1]
+    assert lab[0].tolist() == [0] * 3 + [1] * 12 and lab[1].tolist() == [0] * 15
+    # Eq. gmpp at level 1 by hand: mean 8, fidelity 3*64 + 12*4, no cut edge
+    assert en[1] == pytest.approx(240.0, rel=1e-12)
+    lab2, nc2, _, _ = oracle.partition(xyz, emb, 2, lam, smin, link=False)
+    assert nc2.tolist() == [2, 2]
+
+
+def test_link_connected_graph_changes_nothing():
+    # a connected kNN graph never leaves an isolated node while two or more
+    # nodes remain, so linking must not change any label
+    rng = np.random.default_rng(8)
+    xyz = rng.random((600, 3), dtype=np.float32)
+    emb = rng.standard_normal((600, 4)).astype(np.float32)
+    a = oracle.partition(xyz, emb, 10, [0.05, 0.5], [3, 20], link=True)
+    b = oracle.partition(xyz, emb, 10, [0.05, 0.5], [3, 20], link=False)
+    assert np.array_equal(a[0], b[0]) and np.array_equal(a[1], b[1])
+
+
+def test_link_step_brute_force():
+    rng = np.random.default_rng(9)
+    for trial in range(20):
+        nn = int(rng.integers(2, 40))
+        k = int(rng.integers(1, 6))
+        m = int(rng.integers(0, nn))
+        lo = rng.integers(0, nn, m)
+        hi = rng.integers(0, nn, m)
+        keep = lo != hi
+        lo, hi = np.minimum(lo, hi)[keep], np.maximum(lo, hi)[keep]
+        size = rng.integers(1, 5, nn)
+        # lattice sums make many equal distances: the id decides
+        Sx = rng.integers(-3, 4, (nn, 3)) * size[:, None] * 8
+        got_lo, got_hi = oracle.link_isolated(lo, hi, size, Sx, k)
+        deg = np.zeros(nn, int)
+        np.add.at(deg, lo, 1)
+        np.add.at(deg, hi, 1)
+        c = Sx / size[:, None]
+        pairs = set()
+        for v in np.nonzero(deg == 0)[0]:
+            d = c - c[v]
+            d2 = (d[:, 0] * d[:, 0] + d[:, 1] * d[:, 1]) + d[:, 2] * d[:, 2]
+            ids = np.array([u for u in range(nn) if u != v])
+            order = np.lexsort((ids, d2[ids]))[:min(k, nn - 1)]
+            for u in ids[order]:
+                pairs.add((min(u, v), max(u, v)))
+        assert list(zip(got_lo.tolist(), got_hi.tolist())) == sorted(pairs)
