@@ -55,6 +55,16 @@ typedef enum {
 
 /* Flags of ezsp_params.flags. */
 #define EZSP_F_ENERGY 1u /* fill energy[] (Eq. gmpp per level) */
+/* prepare_graph's linking of isolated nodes (App. Alg. A-2), ezsp_partition
+ * only: at the start of every round with more than one node, each node
+ * without an edge gets an edge of weight 1 to each of its min(k, nodes - 1)
+ * nearest nodes, by the squared distance of their centroids (exact int64
+ * fixed-point position sums, fp64 means and distance), ties to the
+ * superpoint with the smaller smallest point index; a pair linked from both
+ * ends is one edge.  The energy's cut term stays on the input graph.  Needs
+ * a workspace queried with the flag set; rounds of small graphs then run as
+ * separate launches instead of in one kernel. */
+#define EZSP_F_LINK_ISOLATED 2u
 
 typedef struct {
   int32_t k;                /* neighbours per point, 1..64                   */
@@ -251,7 +261,7 @@ const char *ezsp_last_error(void);
 
 /* Per-stage timing with HIP events recorded on the caller's stream around
  * the launches of each stage ("knn_query", "morton_sort", "graph_build",
- * "select", "union", "stats", "contract", "compose", "tail",
+ * "select", "union", "stats", "contract", "compose", "tail", "link",
  * "grid_subsample", "edge_loss", "purity").  Off by default; a
  * diagnostic for benchmarks.  ezsp_profile_enable(1) clears the totals and
  * starts recording, ezsp_profile_enable(0) stops.  ezsp_profile_read gives

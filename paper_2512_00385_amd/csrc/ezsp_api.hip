@@ -62,19 +62,20 @@ int check_params(int64_t n, int32_t d, const ezsp_params *p) {
       return fail(EZSP_ERR_INVALID_ARG, "every lambda must be finite and >= 0");
   if (p->max_rounds < 0)
     return fail(EZSP_ERR_INVALID_ARG, "max_rounds must be >= 0");
-  if (p->flags & ~EZSP_F_ENERGY)
+  if (p->flags & ~(EZSP_F_ENERGY | EZSP_F_LINK_ISOLATED))
     return fail(EZSP_ERR_INVALID_ARG, "unknown flag bits");
   return EZSP_OK;
 }
 
-size_t partition_bytes(int64_t n, int32_t d, int32_t k, bool with_knn) {
+size_t partition_bytes(int64_t n, int32_t d, int32_t k, bool with_knn,
+                       bool link) {
   Arena a;
   a.take<Ctl>(1);
   if (with_knn) {
     KnnWork w;
     knn_reserve(a, (int32_t)n, k, &w);
   }
-  ladder_reserve(a, (int32_t)n, d, k);
+  ladder_reserve(a, (int32_t)n, d, k, link);
   return a.off + 512;
 }
 
@@ -83,7 +84,11 @@ int run_partition(const float *xyz, const int32_t *nbr_in, const float *emb,
                   int64_t *n_comp, double *energy, void *ws, size_t ws_bytes,
                   void *stream) {
   const bool with_knn = xyz != nullptr;
-  if (ws_bytes < partition_bytes(n, d, p->k, with_knn))
+  const bool link = (p->flags & EZSP_F_LINK_ISOLATED) != 0;
+  if (link && !with_knn)
+    return fail(EZSP_ERR_INVALID_ARG,
+                "EZSP_F_LINK_ISOLATED needs the positions (ezsp_partition)");
+  if (ws_bytes < partition_bytes(n, d, p->k, with_knn, link))
     return fail(EZSP_ERR_WORKSPACE, "workspace smaller than the queried size");
   hipStream_t st = static_cast<hipStream_t>(stream);
   Arena a = open_ws(ws, ws_bytes);
@@ -117,6 +122,7 @@ int run_partition(const float *xyz, const int32_t *nbr_in, const float *emb,
   g.min_size = p->min_size;
   g.max_rounds = p->max_rounds;
   g.want_energy = (p->flags & EZSP_F_ENERGY) != 0;
+  g.link = link;
   g.labels = labels;
   g.n_comp = n_comp;
   g.energy = energy;
@@ -194,7 +200,8 @@ size_t ezsp_partition_workspace_size(int64_t n, int32_t d,
   if (!p || !n_ok(n) || d < 1 || d > 64 || p->k < 1 || p->k > 64 ||
       !edges_ok(n, p->k))
     return 0;
-  return partition_bytes(n, d, p->k, true);
+  return partition_bytes(n, d, p->k, true,
+                         (p->flags & EZSP_F_LINK_ISOLATED) != 0);
 }
 
 int ezsp_partition(const float *xyz, const float *emb, int64_t n, int32_t d,

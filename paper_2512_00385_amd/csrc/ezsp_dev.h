@@ -57,6 +57,11 @@ struct Ctl {
   Stripe maxabs_s[kStripes];  // max |e| bits from the fused gather
   int32_t tail_nc[16];        // superpoints of every level the tail ended
   int64_t tail_cut2[16];      // ... and 2 x their cut weight
+  // linking of isolated nodes
+  uint32_t maxabs_x_bits;     // max |coordinate| as fp32 bits
+  int32_t Fx;                 // fixed-point shift of the positions
+  int32_t n_iso;              // nodes with an empty row this round
+  int32_t n_link;             // links kept this round
   // results of the grid-subsampling, edge-loss and purity entry points
   int32_t n_out;              // points kept by the grid subsampling
   int32_t sel_mode;           // intra sample: 0 none, 1 all, 2 by threshold
@@ -89,6 +94,21 @@ __host__ __device__ __forceinline__ float ord2f(int32_t i) {
   union { int32_t i; float f; } u;
   u.i = b;
   return u.f;
+}
+
+// F = min(40, 61 - ceil(log2 n) - max(0, ceil(log2 A))), A = max |value|.
+__device__ __forceinline__ int fixshift_rule(float A, int32_t n) {
+  int cn = 0;
+  while (((int64_t)1 << cn) < (int64_t)n) ++cn;
+  int ca = 0;
+  if (A > 0.0f) {
+    int e;
+    const float m = frexpf(A, &e);  // A = m * 2^e, m in [0.5, 1)
+    ca = (m == 0.5f) ? e - 1 : e;
+    if (ca < 0) ca = 0;
+  }
+  const int F = 61 - cn - ca;
+  return F > 40 ? 40 : F;
 }
 
 __device__ __forceinline__ void raise_err(Ctl *ctl, uint32_t bits) {

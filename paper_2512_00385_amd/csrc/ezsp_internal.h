@@ -121,12 +121,13 @@ struct LadderArgs {
   const int64_t *min_size;
   int32_t max_rounds;
   bool want_energy;
+  bool link;            // prepare_graph's linking of isolated nodes (needs pts)
   bool check_nbr;       // validate caller-supplied neighbour ids
   int32_t *labels;      // L*n, caller order
   int64_t *n_comp;      // host
   double *energy;       // host, nullable
 };
-void ladder_reserve(Arena &a, int32_t n, int32_t d, int32_t k);
+void ladder_reserve(Arena &a, int32_t n, int32_t d, int32_t k, bool link);
 // Returns an ezsp_status code; detail text goes through set_error().
 int ladder_run(const LadderArgs &args, Ctl *ctl, Arena &a, hipStream_t st);
 

@@ -2038,6 +2038,262 @@ __global__ __launch_bounds__(256) void k_repack(
 // ---------------------------------------------------------------------------
 namespace {
 
+// ---------------------------------------------------------------------------
+// prepare_graph's linking of isolated nodes (App. Alg. A-2), optional: at the
+// start of a round with more than one node, every node whose row is empty
+// gets an edge of weight 1 to each of its min(k, nn - 1) nearest nodes, by
+// the squared distance of the centroids and then the smaller minpt (the
+// canonical order); a pair linked from both ends is one edge.  Centroids are
+// exact: int64 fixed-point position sums, c = (double)Sx / |P|, and the
+// squared distance ((dx*dx) + (dy*dy)) + (dz*dz) in fp64 without
+// contraction.  The table is then rebuilt, rows compacted, with the links
+// appended.
+// ---------------------------------------------------------------------------
+
+// max |coordinate| over the points (x, y, z of the internal float4 array)
+__global__ __launch_bounds__(256) void k_link_maxabs(const float4 *pts,
+                                                     int32_t n, Ctl *ctl) {
+  uint32_t m = 0;
+  for (int32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < n;
+       i += gridDim.x * blockDim.x) {
+    const float4 p = pts[i];
+    m = max(m, __float_as_uint(fabsf(p.x)));
+    m = max(m, __float_as_uint(fabsf(p.y)));
+    m = max(m, __float_as_uint(fabsf(p.z)));
+  }
+#pragma unroll
+  for (int off = kWave / 2; off > 0; off >>= 1)
+    m = max(m, (uint32_t)__shfl_xor((int)m, off, kWave));
+  if ((threadIdx.x & (kWave - 1)) == 0) atomicMax(&ctl->maxabs_x_bits, m);
+}
+
+// fixed-point shift of the positions, the same rule as for the embeddings
+__global__ void k_link_shift(Ctl *ctl, int32_t n) {
+  if (threadIdx.x != 0 || blockIdx.x != 0) return;
+  ctl->Fx = fixshift_rule(__uint_as_float(ctl->maxabs_x_bits), n);
+  if (ctl->Fx < 16) raise_err(ctl, kErrRange);
+}
+
+__global__ void k_link_reset(Ctl *ctl) {
+  if (threadIdx.x == 0 && blockIdx.x == 0) {
+    ctl->n_iso = 0;
+    ctl->n_link = 0;
+  }
+}
+
+// Nodes with an empty row, and every row's count of occupied slots.
+__global__ __launch_bounds__(256) void k_link_detect(int32_t nn, Adj a,
+                                                     int32_t *cntv,
+                                                     int32_t *iso,
+                                                     int32_t *iso_of,
+                                                     Ctl *ctl) {
+  const int32_t v = xcd_tid();
+  if (v >= nn) return;
+  int32_t c = 0;
+  for_row<false>(a, v, 0, 1, [&](int32_t, int32_t) { ++c; });
+  cntv[v] = c;
+  int32_t slot = -1;
+  if (c == 0) {
+    slot = atomicAdd(&ctl->n_iso, 1);
+    iso[slot] = v;
+  }
+  iso_of[v] = slot;
+}
+
+// Position sums of the current nodes: point p adds rint(x * 2^Fx) to M[p].
+__global__ __launch_bounds__(256) void k_link_sums(int32_t n, int32_t nn,
+                                                   const int32_t *M,
+                                                   const float4 *pts,
+                                                   int64_t *Sx, Ctl *ctl) {
+  const int32_t p = xcd_tid();
+  if (p >= n) return;
+  const int32_t v = M[p];
+  if ((uint32_t)v >= (uint32_t)nn) {
+    raise_err(ctl, kErrInternal);
+    return;
+  }
+  const double sF = ldexp(1.0, ctl->Fx);
+  const float4 q = pts[p];
+  unsigned long long *dst = reinterpret_cast<unsigned long long *>(Sx + 3 * (int64_t)v);
+  atomicAdd(dst + 0, (unsigned long long)(int64_t)rint((double)q.x * sF));
+  atomicAdd(dst + 1, (unsigned long long)(int64_t)rint((double)q.y * sF));
+  atomicAdd(dst + 2, (unsigned long long)(int64_t)rint((double)q.z * sF));
+}
+
+struct NearKey {
+  double d2;
+  int32_t mp, u;
+};
+__device__ __forceinline__ bool near_before(const NearKey &a,
+                                            const NearKey &b) {
+  return a.d2 < b.d2 || (a.d2 == b.d2 && a.mp < b.mp);
+}
+
+__device__ __forceinline__ double centroid(const int64_t *Sx,
+                                           const int32_t *size, int32_t v,
+                                           int a) {
+  return __ddiv_rn((double)Sx[3 * (int64_t)v + a], (double)size[v]);
+}
+
+constexpr int kLinkNT = 128;
+
+// One block per isolated node: every thread keeps the best T candidates of
+// its share of the nodes, sorted, in LDS; then T block-wide minima.
+__global__ __launch_bounds__(kLinkNT) void k_link_near(
+    int32_t nn, const int32_t *iso, const Ctl *cn, const int64_t *Sx,
+    const int32_t *size, const int32_t *minpt, int32_t T, int32_t kstride,
+    int32_t *near, Ctl *ctl) {
+  extern __shared__ unsigned char link_lds[];
+  NearKey *lst = reinterpret_cast<NearKey *>(link_lds);  // [kLinkNT][T]
+  __shared__ NearKey red[kLinkNT];
+  __shared__ int32_t red_t[kLinkNT];
+  __shared__ int32_t head[kLinkNT];
+  const int32_t n_iso = cn->n_iso;
+  NearKey *mine = lst + threadIdx.x * T;
+  for (int32_t it = blockIdx.x; it < n_iso; it += gridDim.x) {
+    const int32_t v = iso[it];
+    const double cx = centroid(Sx, size, v, 0), cy = centroid(Sx, size, v, 1),
+                 cz = centroid(Sx, size, v, 2);
+    int32_t cnt = 0;
+    for (int32_t u = threadIdx.x; u < nn; u += kLinkNT) {
+      if (u == v) continue;
+      const double dx = __dsub_rn(centroid(Sx, size, u, 0), cx);
+      const double dy = __dsub_rn(centroid(Sx, size, u, 1), cy);
+      const double dz = __dsub_rn(centroid(Sx, size, u, 2), cz);
+      const double t = __dadd_rn(__dmul_rn(dx, dx), __dmul_rn(dy, dy));
+      const NearKey c{__dadd_rn(t, __dmul_rn(dz, dz)), minpt[u], u};
+      if (cnt == T && !near_before(c, mine[T - 1])) continue;
+      int32_t pos = cnt < T ? cnt++ : T - 1;
+      while (pos > 0 && near_before(c, mine[pos - 1])) {
+        mine[pos] = mine[pos - 1];
+        --pos;
+      }
+      mine[pos] = c;
+    }
+    head[threadIdx.x] = 0;
+    __syncthreads();
+    for (int32_t r = 0; r < T; ++r) {
+      const int32_t h = head[threadIdx.x];
+      red[threadIdx.x] = h < cnt ? mine[h] : NearKey{INFINITY, INT32_MAX, -1};
+      red_t[threadIdx.x] = threadIdx.x;
+      __syncthreads();
+      for (int off = kLinkNT / 2; off > 0; off >>= 1) {
+        if ((int)threadIdx.x < off &&
+            near_before(red[threadIdx.x + off], red[threadIdx.x])) {
+          red[threadIdx.x] = red[threadIdx.x + off];
+          red_t[threadIdx.x] = red_t[threadIdx.x + off];
+        }
+        __syncthreads();
+      }
+      if (threadIdx.x == 0) {
+        near[(int64_t)it * kstride + r] = red[0].u;
+        if (red[0].u < 0) raise_err(ctl, kErrInternal);
+        head[red_t[0]] += 1;
+      }
+      __syncthreads();
+    }
+  }
+}
+
+// The kept links (a pair listed from both isolated ends counts once, from
+// the end with the smaller internal id) and the extra entries per node.
+__global__ __launch_bounds__(256) void k_link_count(
+    const Ctl *cn, const int32_t *iso, const int32_t *iso_of,
+    const int32_t *near, int32_t T, int32_t kstride, int32_t *ext,
+    uint8_t *keep, Ctl *ctl) {
+  const int64_t total = (int64_t)cn->n_iso * T;
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < total;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    const int32_t it = (int32_t)(i / T), r = (int32_t)(i - (int64_t)it * T);
+    const int32_t v = iso[it], u = near[(int64_t)it * kstride + r];
+    bool k = true;
+    const int32_t iu = iso_of[u];
+    if (iu >= 0 && u < v)
+      for (int32_t t = 0; t < T && k; ++t)
+        k = near[(int64_t)iu * kstride + t] != v;
+    keep[i] = k ? 1 : 0;
+    if (k) {
+      atomicAdd(&ext[v], 1);
+      atomicAdd(&ext[u], 1);
+      atomicAdd(&ctl->n_link, 1);
+    }
+  }
+}
+
+// Rebuilt rows: the occupied slots of the old window, compacted, then room
+// for the links (cursor fill[v] starts after the copied entries).
+__global__ __launch_bounds__(256) void k_link_copy(int32_t nn, Adj a,
+                                                   const int32_t *cntv,
+                                                   const int32_t *ext,
+                                                   const int32_t *ws2,
+                                                   int32_t *wl2,
+                                                   uint64_t *tbl2,
+                                                   int32_t *fill) {
+  const int32_t v = xcd_tid();
+  if (v >= nn) return;
+  const int32_t base = ws2[v];
+  int32_t c = 0;
+  const uint64_t *t = a.tbl + a.ws[v];
+  const int32_t len = a.wl[v];
+  for (int32_t j = 0; j < len; ++j) {
+    const uint64_t e = t[j];
+    if (e != kEmpty) tbl2[base + c++] = e;
+  }
+  fill[v] = cntv[v];
+  wl2[v] = cntv[v] + ext[v];
+}
+
+__global__ __launch_bounds__(256) void k_link_append(
+    const Ctl *cn, const int32_t *iso, const int32_t *near, int32_t T,
+    int32_t kstride, const uint8_t *keep, const int32_t *ws2,
+    const int32_t *wl2, uint64_t *tbl2, int32_t *fill, Ctl *ctl) {
+  const int64_t total = (int64_t)cn->n_iso * T;
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < total;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    if (!keep[i]) continue;
+    const int32_t it = (int32_t)(i / T), r = (int32_t)(i - (int64_t)it * T);
+    const int32_t v = iso[it], u = near[(int64_t)it * kstride + r];
+    const int32_t pv = atomicAdd(&fill[v], 1), pu = atomicAdd(&fill[u], 1);
+    if (pv < wl2[v] && pu < wl2[u]) {
+      tbl2[ws2[v] + pv] = ((uint64_t)(uint32_t)u << 32) | 1u;
+      tbl2[ws2[u] + pu] = ((uint64_t)(uint32_t)v << 32) | 1u;
+    } else {
+      raise_err(ctl, kErrInternal);
+    }
+  }
+}
+
+// Scan functor for the rebuilt windows: length cntv + ext.
+struct ScanLinkWin {
+  const int32_t *cntv, *ext;
+  int32_t *ws2;
+  int32_t n;
+  __device__ int32_t value(int32_t i) const {
+    return i < n ? cntv[i] + ext[i] : 0;
+  }
+  __device__ void emit(int32_t i, int32_t excl, int32_t) const {
+    if (i <= n) ws2[i] = excl;
+  }
+};
+
+// Cut weight of the input graph (Eq. gmpp's second term on E0) for the
+// point -> node map M: both directions of every first-round edge.
+__global__ __launch_bounds__(256) void k_cut_e0(int32_t n, Adj a0,
+                                                const int32_t *M, Ctl *ctl) {
+  long long acc = 0;
+  for (int32_t v = blockIdx.x * blockDim.x + threadIdx.x; v < n;
+       v += gridDim.x * blockDim.x) {
+    const int32_t mv = M[v];
+    for_row<true>(a0, v, 0, 1, [&](int32_t u, int32_t w) {
+      if (M[u] != mv) acc += w;
+    });
+  }
+  acc = wave_sum(acc);
+  if ((threadIdx.x & (kWave - 1)) == 0 && acc)
+    atomicAdd(reinterpret_cast<unsigned long long *>(&ctl->cut_w2),
+              (unsigned long long)acc);
+}
+
 struct Bufs {
   float *emb_int;
   int32_t *nbr_clean;                   // sanitised caller table
@@ -2063,11 +2319,15 @@ struct Bufs {
   double *lvl_mu;
   int32_t *bsum, *tmp;
   double *partial;
+  // linking of isolated nodes (only with the flag)
+  int64_t *lk_sx;
+  int32_t *lk_cnt, *lk_iso, *lk_iso_of, *lk_ext, *lk_fill, *lk_near;
+  uint8_t *lk_keep;
 };
 
 int64_t edge_bound(int32_t n, int32_t k) { return 2 * (int64_t)n * k; }
 
-void carve(Arena &a, int32_t n, int32_t d, int32_t k, Bufs *b) {
+void carve(Arena &a, int32_t n, int32_t d, int32_t k, bool link, Bufs *b) {
   const int64_t ed = edge_bound(n, k);
   const size_t n1 = (size_t)n + 1;
   b->emb_int = a.take<float>((size_t)n * d);
@@ -2126,7 +2386,22 @@ void carve(Arena &a, int32_t n, int32_t d, int32_t k, Bufs *b) {
   b->bsum = a.take<int32_t>(scan_blocks(ed + n1) + 2);
   b->tmp = a.take<int32_t>(8);
   b->partial = a.take<double>(kEnergyBlocks);
+  b->lk_sx = nullptr;
+  b->lk_cnt = b->lk_iso = b->lk_iso_of = b->lk_ext = b->lk_fill = nullptr;
+  b->lk_near = nullptr;
+  b->lk_keep = nullptr;
+  if (link) {
+    b->lk_sx = a.take<int64_t>(3 * n1);
+    b->lk_cnt = a.take<int32_t>(n1);
+    b->lk_iso = a.take<int32_t>(n1);
+    b->lk_iso_of = a.take<int32_t>(n1);
+    b->lk_ext = a.take<int32_t>(n1);
+    b->lk_fill = a.take<int32_t>(n1);
+    b->lk_near = a.take<int32_t>(n1 * (size_t)k);
+    b->lk_keep = a.take<uint8_t>(n1 * (size_t)k);
+  }
 }
+
 
 inline dim3 blocks_for(int64_t n, int nt = 256) {
   int64_t b = (n + nt - 1) / nt;
@@ -2370,14 +2645,86 @@ int run_tail(const LadderArgs &g, const Bufs &b, const float *emb,
 
 }  // namespace
 
-void ladder_reserve(Arena &a, int32_t n, int32_t d, int32_t k) {
+// prepare_graph's linking before the next round: isolated nodes of the
+// current table get their links and the table is rebuilt (compacted, links
+// appended) in the idle buffers, then copied back.  Updates ed.
+int link_round(const LadderArgs &g, const Bufs &b, Adj &adj, int cur,
+               int32_t nn, int32_t &ed, Ctl *ctl, Ctl *h, hipStream_t st) {
+  int rc;
+  prof_begin("link", st);
+  hipLaunchKernelGGL(k_link_reset, dim3(1), dim3(64), 0, st, ctl);
+  hipLaunchKernelGGL(k_link_detect, xblocks_for(nn), dim3(256), 0, st, nn,
+                     adj, b.lk_cnt, b.lk_iso, b.lk_iso_of, ctl);
+  prof_end(st);
+  if ((rc = read_ctl(ctl, h, st))) return rc;
+  if (h->err) return status_from_err(h->err);
+  const int32_t n_iso = h->n_iso;
+  if (n_iso == 0) return 0;
+  if (n_iso > nn) {
+    set_error("isolated-node count out of range");
+    return -5;
+  }
+  const int32_t n = g.n, k = g.k;
+  const int32_t T = std::min<int32_t>(k, nn - 1);
+  const int nxt = 1 - cur;
+  prof_begin("link", st);
+  hipLaunchKernelGGL(k_fill_i32, blocks_for(6 * (int64_t)nn), dim3(256), 0, st,
+                     reinterpret_cast<int32_t *>(b.lk_sx), 6 * (int64_t)nn, 0);
+  hipLaunchKernelGGL(k_link_sums, xblocks_for(n), dim3(256), 0, st, n, nn,
+                     b.M, g.pts, b.lk_sx, ctl);
+  const size_t lds = (size_t)kLinkNT * T * sizeof(NearKey);
+  hipLaunchKernelGGL(k_link_near, dim3((unsigned)std::min<int32_t>(n_iso, 2048)),
+                     dim3(kLinkNT), lds, st, nn, b.lk_iso, ctl, b.lk_sx,
+                     b.size[cur], b.minpt[cur], T, k, b.lk_near, ctl);
+  hipLaunchKernelGGL(k_fill_i32, blocks_for(nn + 1), dim3(256), 0, st,
+                     b.lk_ext, (int64_t)nn + 1, 0);
+  hipLaunchKernelGGL(k_link_count, blocks_for((int64_t)n_iso * T), dim3(256),
+                     0, st, ctl, b.lk_iso, b.lk_iso_of, b.lk_near, T, k,
+                     b.lk_ext, b.lk_keep, ctl);
+  device_scan(ScanLinkWin{b.lk_cnt, b.lk_ext, b.ws[nxt], nn}, nn + 1, b.bsum,
+              &ctl->slots, st);
+  hipLaunchKernelGGL(k_link_copy, xblocks_for(nn), dim3(256), 0, st, nn, adj,
+                     b.lk_cnt, b.lk_ext, b.ws[nxt], b.wl[nxt], b.tbl[nxt],
+                     b.lk_fill);
+  hipLaunchKernelGGL(k_link_append, blocks_for((int64_t)n_iso * T), dim3(256),
+                     0, st, ctl, b.lk_iso, b.lk_near, T, k, b.lk_keep,
+                     b.ws[nxt], b.wl[nxt], b.tbl[nxt], b.lk_fill, ctl);
+  prof_end(st);
+  if ((rc = read_ctl(ctl, h, st))) return rc;
+  if (h->err) return status_from_err(h->err);
+  const int64_t total = h->slots;
+  if (total < ed || total > ed + 2 * (int64_t)n_iso * T ||
+      total > 2 * edge_bound(n, k)) {
+    set_error("linked table size out of range (%lld)", (long long)total);
+    return -5;
+  }
+  // back into the current buffers (the idle ones take the next contraction)
+  rc = check_hip(hipMemcpyAsync(b.tbl[cur], b.tbl[nxt], sizeof(uint64_t) * total,
+                                hipMemcpyDeviceToDevice, st), "link copy");
+  if (!rc)
+    rc = check_hip(hipMemcpyAsync(b.ws[cur], b.ws[nxt], sizeof(int32_t) * (nn + 1),
+                                  hipMemcpyDeviceToDevice, st), "link copy");
+  if (!rc)
+    rc = check_hip(hipMemcpyAsync(b.wl[cur], b.wl[nxt], sizeof(int32_t) * (nn + 1),
+                                  hipMemcpyDeviceToDevice, st), "link copy");
+  if (rc) return rc;
+  ed = (int32_t)total;
+  prof_bytes("link", 24.0 * n + 16.0 * total);
+  return 0;
+}
+
+void ladder_reserve(Arena &a, int32_t n, int32_t d, int32_t k, bool link) {
   Bufs b;
-  carve(a, n, d, k, &b);
+  carve(a, n, d, k, link, &b);
 }
 
 int ladder_run(const LadderArgs &g, Ctl *ctl, Arena &a, hipStream_t st) {
   Bufs b;
-  carve(a, g.n, g.d, g.k, &b);
+  carve(a, g.n, g.d, g.k, g.link, &b);
+  if (g.link && !g.pts) {
+    set_error("linking isolated nodes needs the positions");
+    return -1;
+  }
   Ctl *h = pinned_ctl();
   if (!h) {
     set_error("hipHostMalloc of the control block failed");
@@ -2415,6 +2762,11 @@ int ladder_run(const LadderArgs &g, Ctl *ctl, Arena &a, hipStream_t st) {
     hipLaunchKernelGGL(k_maxabs, dim3(2048), dim3(256), 0, st, emb,
                        (int64_t)n * d, ctl);
   hipLaunchKernelGGL(k_fixshift, dim3(1), dim3(64), 0, st, ctl, n);
+  if (g.link) {
+    hipLaunchKernelGGL(k_link_maxabs, dim3(1024), dim3(256), 0, st, g.pts, n,
+                       ctl);
+    hipLaunchKernelGGL(k_link_shift, dim3(1), dim3(64), 0, st, ctl, n);
+  }
 
   // first-round graph (Step 0: the superpoint adjacency is the kNN graph)
   prof_begin("graph_build", st);
@@ -2462,6 +2814,7 @@ int ladder_run(const LadderArgs &g, Ctl *ctl, Arena &a, hipStream_t st) {
   adj.wl = nullptr;
   adj.tbl = nullptr;
 
+  const Adj adj0 = adj;  // the input graph, for the cut term with links
   int cur = 0;
   bool first = true;
   int32_t nn = n;
@@ -2475,6 +2828,7 @@ int ladder_run(const LadderArgs &g, Ctl *ctl, Arena &a, hipStream_t st) {
     const long v = strtol(e, nullptr, 10);
     tail_nodes = (int32_t)std::max<long>(0, std::min<long>(v, kTailNodes));
   }
+  if (g.link) tail_nodes = 0;  // the tail kernel does not link
   for (int32_t l = 0; l < g.n_levels; ++l) {
     const double lambda = g.lambdas[l];
     const int64_t smin = g.min_size ? g.min_size[l] : 0;
@@ -2539,6 +2893,10 @@ int ladder_run(const LadderArgs &g, Ctl *ctl, Arena &a, hipStream_t st) {
       adj.wl = b.wl[cur];
       adj.tbl = b.tbl[cur];
       if (nn == 1) break;  // a single component is left
+      if (g.link) {  // prepare_graph of the next round
+        if ((rc = link_round(g, b, adj, cur, nn, ed, ctl, h, st))) return rc;
+        slots = ed;
+      }
     }
 
     if (tail_level >= 0) break;
@@ -2570,7 +2928,10 @@ int ladder_run(const LadderArgs &g, Ctl *ctl, Arena &a, hipStream_t st) {
                            (const int32_t *)nullptr, 0, b.mu, ctl, b.partial);
       hipLaunchKernelGGL(k_energy_sum, dim3(1), dim3(64), 0, st, b.partial,
                          kEnergyBlocks, ctl);
-      if (!first)
+      if (!first && g.link)  // the cut of the input graph, links aside
+        hipLaunchKernelGGL(k_cut_e0, dim3(1024), dim3(256), 0, st, n, adj0,
+                           b.M, ctl);
+      else if (!first)
         hipLaunchKernelGGL(k_weight_sum, dim3(256), dim3(256), 0, st, nn, adj,
                            ctl);
       if ((rc = read_ctl(ctl, h, st))) return rc;

@@ -179,6 +179,10 @@ __global__ void k_ctl_init(Ctl *ctl) {
     ctl->tail_level = -1;
     ctl->cut_w2 = 0;
     ctl->fid_total = 0.0;
+    ctl->maxabs_x_bits = 0;
+    ctl->Fx = 0;
+    ctl->n_iso = 0;
+    ctl->n_link = 0;
     ctl->n_out = 0;
     ctl->sel_mode = 0;
     ctl->sel_prefix = 0;
@@ -233,18 +237,7 @@ __global__ void k_fixshift(Ctl *ctl, int32_t n) {
   uint32_t bits = ctl->maxabs_bits;
   for (int i = 0; i < kStripes; ++i)
     bits = max(bits, (uint32_t)ctl->maxabs_s[i].v);
-  const float A = __uint_as_float(bits);
-  int cn = 0;
-  while (((int64_t)1 << cn) < (int64_t)n) ++cn;
-  int ca = 0;
-  if (A > 0.0f) {
-    int e;
-    float m = frexpf(A, &e);  // A = m * 2^e, m in [0.5, 1)
-    ca = (m == 0.5f) ? e - 1 : e;
-    if (ca < 0) ca = 0;
-  }
-  int F = 61 - cn - ca;
-  if (F > 40) F = 40;
+  const int F = fixshift_rule(__uint_as_float(bits), n);
   ctl->F = F;
   if (F < 16) raise_err(ctl, kErrRange);
 }

@@ -25,6 +25,7 @@ ERR_WORKSPACE = -4
 ERR_DEVICE = -5
 ERR_NOT_CONVERGED = -6
 F_ENERGY = 1
+F_LINK_ISOLATED = 2
 
 ENTRY_POINTS = (
     "ezsp_knn_workspace_size", "ezsp_knn",
@@ -134,7 +135,7 @@ def profile_only(stage=None):
 
 
 STAGES = ("morton_sort", "knn_query", "graph_build", "select", "union",
-          "stats", "contract", "compose", "tail")
+          "stats", "contract", "compose", "tail", "link")
 EXTRA_STAGES = ("grid_subsample", "edge_loss", "purity")
 
 
@@ -177,7 +178,7 @@ def _workspace(nbytes: int, device):
     return torch.empty(nbytes, dtype=torch.uint8, device=device)
 
 
-def _params(k, lambdas, min_size, max_rounds, energy):
+def _params(k, lambdas, min_size, max_rounds, energy, link=False):
     lam = np.ascontiguousarray(np.atleast_1d(np.asarray(lambdas, np.float64)))
     ms = None
     if min_size is not None:
@@ -187,7 +188,7 @@ def _params(k, lambdas, min_size, max_rounds, energy):
             raise ValueError("min_size needs one value per level")
     p = Params(int(k), int(lam.shape[0]), lam.ctypes.data,
                None if ms is None else ms.ctypes.data, int(max_rounds),
-               F_ENERGY if energy else 0)
+               (F_ENERGY if energy else 0) | (F_LINK_ISOLATED if link else 0))
     return p, lam, ms  # keep the arrays alive with the struct
 
 
@@ -217,12 +218,13 @@ class Partitioner:
     once, so repeated calls on the same sizes allocate nothing new."""
 
     def __init__(self, n: int, d: int, k: int, lambdas, min_size=None,
-                 max_rounds: int = 0, energy: bool = False, device=None):
+                 max_rounds: int = 0, energy: bool = False, device=None,
+                 link: bool = False):
         self.lib = load()
         self.n, self.d, self.k = int(n), int(d), int(k)
         self.device = torch.device(device or "cuda")
         self.params, self._lam, self._ms = _params(k, lambdas, min_size,
-                                                   max_rounds, energy)
+                                                   max_rounds, energy, link)
         self.L = int(self._lam.shape[0])
         self.nbytes = self.lib.ezsp_partition_workspace_size(
             self.n, self.d, ctypes.byref(self.params))
@@ -248,8 +250,10 @@ class Partitioner:
 
 
 def partition(xyz: torch.Tensor, emb: torch.Tensor, k: int, lambdas,
-              min_size=None, max_rounds: int = 0, energy: bool = False):
-    """kNN graph + merge ladder (ezsp_partition).
+              min_size=None, max_rounds: int = 0, energy: bool = False,
+              link: bool = False):
+    """kNN graph + merge ladder (ezsp_partition); link: prepare_graph's
+    linking of isolated nodes (EZSP_F_LINK_ISOLATED).
 
     Returns (labels [L, n] int32 on the device, n_comp int64 numpy [L],
     energy float64 numpy [L] or None)."""
@@ -257,7 +261,7 @@ def partition(xyz: torch.Tensor, emb: torch.Tensor, k: int, lambdas,
     if emb.dim() != 2:
         raise ValueError("emb must have shape [n, d]")
     part = Partitioner(xyz.shape[0], emb.shape[1], k, lambdas, min_size,
-                       max_rounds, energy, xyz.device)
+                       max_rounds, energy, xyz.device, link)
     labels, nc, en = part(xyz, emb)
     return labels, nc, en
 

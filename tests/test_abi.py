@@ -98,7 +98,7 @@ def test_partition_rejects_bad_arguments():
     assert call_partition(lambdas=(float("nan"),)) == E
     assert call_partition(lambdas=(float("inf"),)) == E
     assert call_partition(max_rounds=-1) == E
-    assert call_partition(flags=2) == E
+    assert call_partition(flags=4) == E  # unknown bit
     assert call_partition(xyz=None) == E
     assert call_partition(labels=None) == E
     assert call_partition(n_comp=None) == E
@@ -117,6 +117,14 @@ def test_from_knn_and_stats_reject_bad_arguments():
     assert lib.ezsp_partition_from_knn(FAKE, FAKE, 10, 4, ctypes.byref(p),
                                        FAKE, FAKE, None, FAKE, 10,
                                        None) == ezsp.ERR_WORKSPACE
+    # linking isolated nodes needs positions: not with a given table
+    pl = ezsp.Params(10, 1, lam.ctypes.data, None, 0, ezsp.F_LINK_ISOLATED)
+    assert lib.ezsp_partition_from_knn(FAKE, FAKE, 10, 4, ctypes.byref(pl),
+                                       FAKE, FAKE, None, FAKE, 1 << 40,
+                                       None) == ezsp.ERR_INVALID_ARG
+    # and its workspace is larger
+    assert lib.ezsp_partition_workspace_size(1000, 8, ctypes.byref(pl)) > \
+        lib.ezsp_partition_workspace_size(1000, 8, ctypes.byref(p))
     cs = lib.ezsp_component_stats
     assert cs(FAKE, 10, 0, FAKE, 4, None, FAKE, FAKE, None, FAKE, 1 << 40,
               None) == ezsp.ERR_INVALID_ARG
