@@ -63,6 +63,9 @@ def parse():
     ap.add_argument("--calib-copy", action="store_true",
                     help="after the timed steps, run one plain copy kernel "
                     "of 1 GiB in and 1 GiB out (scale for the HBM counters)")
+    ap.add_argument("--link", action="store_true",
+                    help="partition with prepare_graph's linking of isolated "
+                    "nodes (EZSP_F_LINK_ISOLATED)")
     ap.add_argument("--op", default="partition",
                     choices=["partition", "grid_subsample", "edge_loss",
                              "purity"],
@@ -107,7 +110,7 @@ def measured_traffic(stage, n_points, k):
         return None
 
 
-def cpu_baseline(sc, n_sample):
+def cpu_baseline(sc, n_sample, link=False):
     """Oracle (single-threaded C) on the whole tile, or, when n_sample is
     smaller, on the slab of the tile around x = 0 that holds n_sample points
     (full density profile of the scene, sensor included)."""
@@ -129,13 +132,15 @@ def cpu_baseline(sc, n_sample):
     t1 = time.perf_counter()
     lo, hi, w = oracle.graph(nbr)
     oracle.partition_graph(emb, lo, hi, w, sc.lambdas, min_size=sc.min_size,
-                           want_energy=False)
+                           want_energy=False, xyz=xyz,
+                           link_k=sc.k if link else 0)
     t2 = time.perf_counter()
     return {
         "value": n_sample / (t2 - t0), "unit": "points/s", "cores": 1,
         "kind": "oracle",
         "sample": (f"{what}, k={sc.k}, ladder {list(sc.lambdas)}, "
-                   f"s_min {sc.min_size}; one "
+                   f"s_min {sc.min_size}"
+                   f"{', isolated nodes linked' if link else ''}; one "
                    f"thread; kNN {t1 - t0:.2f} s, graph+ladder "
                    f"{t2 - t1:.2f} s; host {platform.processor() or 'cpu'} "
                    f"with {os.cpu_count()} logical cores"),
@@ -279,7 +284,7 @@ def main():
     xyz = torch.from_numpy(sc.xyz).to(dev)
     emb = torch.from_numpy(sc.emb).to(dev)
     part = ezsp.Partitioner(sc.n, sc.d, sc.k, sc.lambdas,
-                            min_size=sc.min_size, device=dev)
+                            min_size=sc.min_size, device=dev, link=args.link)
     print(f"[bench] n={sc.n} d={sc.d} k={sc.k} ws={part.nbytes / 2**30:.2f} "
           "GiB; warmup", file=sys.stderr, flush=True)
     for _ in range(args.warmup):
@@ -352,16 +357,20 @@ def main():
                                f", {sc.n} points, D={sc.d}, k={sc.k}, "
                                f"lambda ladder {sc.lambdas}"
                                + (f", s_min {sc.min_size}" if sc.min_size
+                                  else "")
+                               + (", isolated nodes linked" if args.link
                                   else ""),
                    "n_points": sc.n, "d": sc.d, "k": sc.k,
-                   "lambdas": sc.lambdas, "min_size": sc.min_size},
+                   "lambdas": sc.lambdas, "min_size": sc.min_size,
+                   "link_isolated": bool(args.link)},
         "roofline": roofline,
         "stage_ms_per_step": split,
         "n_comp": [int(x) for x in n_comp],
     }
     if not args.no_cpu:
         print("[bench] cpu baseline (oracle)", file=sys.stderr, flush=True)
-        out["cpu_baseline"] = cpu_baseline(sc, min(args.cpu_points, sc.n))
+        out["cpu_baseline"] = cpu_baseline(sc, min(args.cpu_points, sc.n),
+                                           args.link)
     print(json.dumps(out), flush=True)
 
 
