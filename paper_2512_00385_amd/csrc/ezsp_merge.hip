@@ -382,6 +382,8 @@ __global__ void k_round_init(Ctl *ctl) {
     ctl->n_big = 0;
     ctl->n_cbig = 0;
     ctl->n_tiles = 0;
+    ctl->n_iso = 0;
+    ctl->n_link = 0;
   }
   if (blockIdx.x == 0) stripe_zero(ctl->e_next_s);
 }
@@ -2074,50 +2076,118 @@ __global__ void k_link_shift(Ctl *ctl, int32_t n) {
   if (ctl->Fx < 16) raise_err(ctl, kErrRange);
 }
 
-__global__ void k_link_reset(Ctl *ctl) {
-  if (threadIdx.x == 0 && blockIdx.x == 0) {
-    ctl->n_iso = 0;
-    ctl->n_link = 0;
-  }
-}
-
-// Nodes with an empty row, and every row's count of occupied slots.
-__global__ __launch_bounds__(256) void k_link_detect(int32_t nn, Adj a,
-                                                     int32_t *cntv,
+// After a contraction: the next table's nodes whose row is empty (a scan
+// that stops at the first occupied slot), listed for the host.  Live count
+// n_next from the control block; nothing to do when the round merged none.
+__global__ __launch_bounds__(256) void k_link_detect(const int32_t *ws,
+                                                     const int32_t *wl,
+                                                     const uint64_t *tbl,
                                                      int32_t *iso,
                                                      int32_t *iso_of,
                                                      Ctl *ctl) {
-  const int32_t v = xcd_tid();
-  if (v >= nn) return;
-  int32_t c = 0;
-  for_row<false>(a, v, 0, 1, [&](int32_t, int32_t) { ++c; });
-  cntv[v] = c;
+  if (!ctl->any_choice) return;
+  int32_t v;
+  if (!xcd_item(ctl->n_next, v)) return;
+  const uint64_t *t = tbl + ws[v];
+  const int32_t len = wl[v];
+  bool empty = true;
+  for (int32_t j = 0; j < len && empty; ++j) empty = t[j] == kEmpty;
   int32_t slot = -1;
-  if (c == 0) {
+  if (empty) {
     slot = atomicAdd(&ctl->n_iso, 1);
     iso[slot] = v;
   }
   iso_of[v] = slot;
 }
 
-// Position sums of the current nodes: point p adds rint(x * 2^Fx) to M[p].
-__global__ __launch_bounds__(256) void k_link_sums(int32_t n, int32_t nn,
-                                                   const int32_t *M,
-                                                   const float4 *pts,
-                                                   int64_t *Sx, Ctl *ctl) {
-  const int32_t p = xcd_tid();
-  if (p >= n) return;
-  const int32_t v = M[p];
-  if ((uint32_t)v >= (uint32_t)nn) {
-    raise_err(ctl, kErrInternal);
-    return;
+// Position sums of the next round's components from their members: int64
+// fixed point, exact in any order.  In the first round the members are
+// points, rint(x * 2^Fx) on the fly.  A thread per component with at most
+// kBigComp members; the larger ones (listed by the statistics) a block each.
+template <bool FIRST>
+__device__ __forceinline__ void member_pos(const float4 *pts,
+                                           const int64_t *sx_in, int32_t m,
+                                           double sF, long long a[3]) {
+  if (FIRST) {
+    const float4 q = pts[m];
+    a[0] += (long long)rint((double)q.x * sF);
+    a[1] += (long long)rint((double)q.y * sF);
+    a[2] += (long long)rint((double)q.z * sF);
+  } else {
+    a[0] += sx_in[3 * (int64_t)m + 0];
+    a[1] += sx_in[3 * (int64_t)m + 1];
+    a[2] += sx_in[3 * (int64_t)m + 2];
   }
+}
+
+template <bool FIRST>
+__global__ __launch_bounds__(256) void k_link_accum(
+    const int32_t *mem, const int32_t *moff, const float4 *pts,
+    const int64_t *sx_in, int64_t *sx_out, Ctl *ctl) {
+  if (!ctl->any_choice) return;
+  int32_t c;
+  if (!xcd_item(ctl->n_next, c)) return;
+  const int32_t m0 = moff[c], m1 = moff[c + 1];
+  if (m1 - m0 > kBigComp) return;
   const double sF = ldexp(1.0, ctl->Fx);
-  const float4 q = pts[p];
-  unsigned long long *dst = reinterpret_cast<unsigned long long *>(Sx + 3 * (int64_t)v);
-  atomicAdd(dst + 0, (unsigned long long)(int64_t)rint((double)q.x * sF));
-  atomicAdd(dst + 1, (unsigned long long)(int64_t)rint((double)q.y * sF));
-  atomicAdd(dst + 2, (unsigned long long)(int64_t)rint((double)q.z * sF));
+  long long a[3] = {0, 0, 0};
+  for (int32_t i = m0; i < m1; ++i) member_pos<FIRST>(pts, sx_in, mem[i], sF, a);
+#pragma unroll
+  for (int q = 0; q < 3; ++q) sx_out[3 * (int64_t)c + q] = a[q];
+}
+
+template <bool FIRST>
+__global__ __launch_bounds__(256) void k_link_accum_big(
+    const int32_t *mem, const int32_t *moff, const float4 *pts,
+    const int64_t *sx_in, int64_t *sx_out, const int32_t *big, Ctl *ctl) {
+  __shared__ unsigned long long acc[3];
+  if (!ctl->any_choice) return;
+  const int32_t n_big = ctl->n_big;
+  const double sF = ldexp(1.0, ctl->Fx);
+  for (int32_t bi = blockIdx.x; bi < n_big; bi += gridDim.x) {
+    const int32_t c = big[bi];
+    if (threadIdx.x < 3) acc[threadIdx.x] = 0ull;
+    __syncthreads();
+    long long a[3] = {0, 0, 0};
+    for (int32_t i = moff[c] + threadIdx.x; i < moff[c + 1]; i += blockDim.x)
+      member_pos<FIRST>(pts, sx_in, mem[i], sF, a);
+#pragma unroll
+    for (int q = 0; q < 3; ++q) {
+      const long long r = wave_sum(a[q]);
+      if ((threadIdx.x & (kWave - 1)) == 0)
+        atomicAdd(&acc[q], (unsigned long long)r);
+    }
+    __syncthreads();
+    if (threadIdx.x < 3) sx_out[3 * (int64_t)c + threadIdx.x] = (int64_t)acc[threadIdx.x];
+    __syncthreads();
+  }
+}
+
+// Occupied slots per row, a wave per row.
+__global__ __launch_bounds__(256) void k_link_rowcount(int32_t nn, Adj a,
+                                                       int32_t *cntv) {
+  const int lane = threadIdx.x & (kWave - 1);
+  const int32_t w0 = (int32_t)(blockIdx.x * (blockDim.x / kWave) +
+                               threadIdx.x / kWave);
+  const int32_t nw = (int32_t)(gridDim.x * (blockDim.x / kWave));
+  for (int32_t v = w0; v < nn; v += nw) {
+    const uint64_t *t = a.tbl + a.ws[v];
+    const int32_t len = a.wl[v];
+    int32_t c = 0;
+    for (int32_t j = lane; j < len; j += kWave) c += t[j] != kEmpty;
+    c = wave_sum(c);
+    if (lane == 0) cntv[v] = c;
+  }
+}
+
+// Centroids of all nodes, (double)Sx / |P| per axis.
+__global__ __launch_bounds__(256) void k_link_centroids(int32_t nn,
+                                                        const int64_t *Sx,
+                                                        const int32_t *size,
+                                                        double *cen) {
+  const int64_t t = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+  if (t >= 3 * (int64_t)nn) return;
+  cen[t] = __ddiv_rn((double)Sx[t], (double)size[t / 3]);
 }
 
 struct NearKey {
@@ -2129,20 +2199,14 @@ __device__ __forceinline__ bool near_before(const NearKey &a,
   return a.d2 < b.d2 || (a.d2 == b.d2 && a.mp < b.mp);
 }
 
-__device__ __forceinline__ double centroid(const int64_t *Sx,
-                                           const int32_t *size, int32_t v,
-                                           int a) {
-  return __ddiv_rn((double)Sx[3 * (int64_t)v + a], (double)size[v]);
-}
-
 constexpr int kLinkNT = 128;
 
 // One block per isolated node: every thread keeps the best T candidates of
 // its share of the nodes, sorted, in LDS; then T block-wide minima.
 __global__ __launch_bounds__(kLinkNT) void k_link_near(
-    int32_t nn, const int32_t *iso, const Ctl *cn, const int64_t *Sx,
-    const int32_t *size, const int32_t *minpt, int32_t T, int32_t kstride,
-    int32_t *near, Ctl *ctl) {
+    int32_t nn, const int32_t *iso, const Ctl *cn, const double *cen,
+    const int32_t *minpt, int32_t T, int32_t kstride, int32_t *near,
+    Ctl *ctl) {
   extern __shared__ unsigned char link_lds[];
   NearKey *lst = reinterpret_cast<NearKey *>(link_lds);  // [kLinkNT][T]
   __shared__ NearKey red[kLinkNT];
@@ -2152,14 +2216,14 @@ __global__ __launch_bounds__(kLinkNT) void k_link_near(
   NearKey *mine = lst + threadIdx.x * T;
   for (int32_t it = blockIdx.x; it < n_iso; it += gridDim.x) {
     const int32_t v = iso[it];
-    const double cx = centroid(Sx, size, v, 0), cy = centroid(Sx, size, v, 1),
-                 cz = centroid(Sx, size, v, 2);
+    const double cx = cen[3 * (int64_t)v], cy = cen[3 * (int64_t)v + 1],
+                 cz = cen[3 * (int64_t)v + 2];
     int32_t cnt = 0;
     for (int32_t u = threadIdx.x; u < nn; u += kLinkNT) {
       if (u == v) continue;
-      const double dx = __dsub_rn(centroid(Sx, size, u, 0), cx);
-      const double dy = __dsub_rn(centroid(Sx, size, u, 1), cy);
-      const double dz = __dsub_rn(centroid(Sx, size, u, 2), cz);
+      const double dx = __dsub_rn(cen[3 * (int64_t)u], cx);
+      const double dy = __dsub_rn(cen[3 * (int64_t)u + 1], cy);
+      const double dz = __dsub_rn(cen[3 * (int64_t)u + 2], cz);
       const double t = __dadd_rn(__dmul_rn(dx, dx), __dmul_rn(dy, dy));
       const NearKey c{__dadd_rn(t, __dmul_rn(dz, dz)), minpt[u], u};
       if (cnt == T && !near_before(c, mine[T - 1])) continue;
@@ -2220,8 +2284,9 @@ __global__ __launch_bounds__(256) void k_link_count(
   }
 }
 
-// Rebuilt rows: the occupied slots of the old window, compacted, then room
-// for the links (cursor fill[v] starts after the copied entries).
+// Rebuilt rows, a wave per row: the occupied slots of the old window,
+// compacted in order by ballot, then room for the links (the cursor fill[v]
+// starts after the copied entries).
 __global__ __launch_bounds__(256) void k_link_copy(int32_t nn, Adj a,
                                                    const int32_t *cntv,
                                                    const int32_t *ext,
@@ -2229,18 +2294,28 @@ __global__ __launch_bounds__(256) void k_link_copy(int32_t nn, Adj a,
                                                    int32_t *wl2,
                                                    uint64_t *tbl2,
                                                    int32_t *fill) {
-  const int32_t v = xcd_tid();
-  if (v >= nn) return;
-  const int32_t base = ws2[v];
-  int32_t c = 0;
-  const uint64_t *t = a.tbl + a.ws[v];
-  const int32_t len = a.wl[v];
-  for (int32_t j = 0; j < len; ++j) {
-    const uint64_t e = t[j];
-    if (e != kEmpty) tbl2[base + c++] = e;
+  const int lane = threadIdx.x & (kWave - 1);
+  const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (kWave - lane));
+  const int32_t w0 = (int32_t)(blockIdx.x * (blockDim.x / kWave) +
+                               threadIdx.x / kWave);
+  const int32_t nw = (int32_t)(gridDim.x * (blockDim.x / kWave));
+  for (int32_t v = w0; v < nn; v += nw) {
+    const int32_t base = ws2[v];
+    const uint64_t *t = a.tbl + a.ws[v];
+    const int32_t len = a.wl[v];
+    int32_t c = 0;
+    for (int32_t j0 = 0; j0 < len; j0 += kWave) {
+      const int32_t j = j0 + lane;
+      const uint64_t e = j < len ? t[j] : kEmpty;
+      const uint64_t occ = __ballot(e != kEmpty);
+      if (e != kEmpty) tbl2[base + c + __popcll(occ & lt)] = e;
+      c += __popcll(occ);
+    }
+    if (lane == 0) {
+      fill[v] = cntv[v];
+      wl2[v] = cntv[v] + ext[v];
+    }
   }
-  fill[v] = cntv[v];
-  wl2[v] = cntv[v] + ext[v];
 }
 
 __global__ __launch_bounds__(256) void k_link_append(
@@ -2320,7 +2395,10 @@ struct Bufs {
   int32_t *bsum, *tmp;
   double *partial;
   // linking of isolated nodes (only with the flag)
-  int64_t *lk_sx;
+  bool link;
+  const float4 *pts;  // points in internal order (linking only)
+  int64_t *lk_sx[2];  // position sums of the nodes, double-buffered
+  double *lk_cen;
   int32_t *lk_cnt, *lk_iso, *lk_iso_of, *lk_ext, *lk_fill, *lk_near;
   uint8_t *lk_keep;
 };
@@ -2386,12 +2464,17 @@ void carve(Arena &a, int32_t n, int32_t d, int32_t k, bool link, Bufs *b) {
   b->bsum = a.take<int32_t>(scan_blocks(ed + n1) + 2);
   b->tmp = a.take<int32_t>(8);
   b->partial = a.take<double>(kEnergyBlocks);
-  b->lk_sx = nullptr;
+  b->link = link;
+  b->pts = nullptr;
+  b->lk_sx[0] = b->lk_sx[1] = nullptr;
+  b->lk_cen = nullptr;
   b->lk_cnt = b->lk_iso = b->lk_iso_of = b->lk_ext = b->lk_fill = nullptr;
   b->lk_near = nullptr;
   b->lk_keep = nullptr;
   if (link) {
-    b->lk_sx = a.take<int64_t>(3 * n1);
+    b->lk_sx[0] = a.take<int64_t>(3 * n1);
+    b->lk_sx[1] = a.take<int64_t>(3 * n1);
+    b->lk_cen = a.take<double>(3 * n1);
     b->lk_cnt = a.take<int32_t>(n1);
     b->lk_iso = a.take<int32_t>(n1);
     b->lk_iso_of = a.take<int32_t>(n1);
@@ -2472,6 +2555,7 @@ void launch_round(const Bufs &b, const Adj &adj, int cur, int32_t n,
               b.tmp, st);
   hipLaunchKernelGGL(k_place, xblocks_for(nn), dim3(256), 0, st, nn, b.L,
                      b.moff, b.rank, b.mem, ctl);
+
   // contraction chunks: enough blocks to fill the chip, at most kChunk
   int32_t chunk = kChunk;
   while (chunk > 64 && (int64_t)ed / chunk < 2048) chunk >>= 1;
@@ -2490,6 +2574,13 @@ void launch_round(const Bufs &b, const Adj &adj, int cur, int32_t n,
   }
   hipLaunchKernelGGL(k_stats_big<FIRST>, big_grid, dim3(256), 0, st,
                      b.mem, b.moff, s, b.deg, d, o, b.big, ctl);
+  if (b.link) {  // position sums of the next round's nodes
+    hipLaunchKernelGGL(k_link_accum<FIRST>, xblocks_for(nn), dim3(256), 0, st,
+                       b.mem, b.moff, b.pts, b.lk_sx[cur], b.lk_sx[nxt], ctl);
+    hipLaunchKernelGGL(k_link_accum_big<FIRST>, big_grid, dim3(256), 0, st,
+                       b.mem, b.moff, b.pts, b.lk_sx[cur], b.lk_sx[nxt], b.big,
+                       ctl);
+  }
   prof_end(st);
   prof_begin("contract", st);
   device_scan(ScanWindows{b.capn, b.ws[nxt], &ctl->n_next, b.cstart, chunk,
@@ -2508,6 +2599,13 @@ void launch_round(const Bufs &b, const Adj &adj, int cur, int32_t n,
                      adj, b.L, b.ws[nxt], b.capn, chunk, lw, b.tbl[nxt], tcap,
                      ctl);
   prof_end(st);
+  if (b.link) {  // the next round's empty rows, read back with the round
+    prof_begin("link", st);
+    hipLaunchKernelGGL(k_link_detect, xblocks_for(nn), dim3(256), 0, st,
+                       b.ws[nxt], b.wl[nxt], b.tbl[nxt], b.lk_iso,
+                       b.lk_iso_of, ctl);
+    prof_end(st);
+  }
   prof_begin("compose", st);
   hipLaunchKernelGGL(k_compose<FIRST>, xblocks_for(n), dim3(256), 0, st, n,
                      nn, b.M, b.L, ctl);
@@ -2645,21 +2743,14 @@ int run_tail(const LadderArgs &g, const Bufs &b, const float *emb,
 
 }  // namespace
 
-// prepare_graph's linking before the next round: isolated nodes of the
-// current table get their links and the table is rebuilt (compacted, links
-// appended) in the idle buffers, then copied back.  Updates ed.
-int link_round(const LadderArgs &g, const Bufs &b, Adj &adj, int cur,
-               int32_t nn, int32_t &ed, Ctl *ctl, Ctl *h, hipStream_t st) {
+// prepare_graph's linking before the next round, when the last round left
+// n_iso nodes with an empty row (listed by k_link_detect): their links, then
+// the table rebuilt (compacted, links appended) in the idle buffers and
+// copied back.  Updates ed.
+int link_round(const LadderArgs &g, const Bufs &b, const Adj &adj, int cur,
+               int32_t nn, int32_t n_iso, int32_t &ed, Ctl *ctl, Ctl *h,
+               hipStream_t st) {
   int rc;
-  prof_begin("link", st);
-  hipLaunchKernelGGL(k_link_reset, dim3(1), dim3(64), 0, st, ctl);
-  hipLaunchKernelGGL(k_link_detect, xblocks_for(nn), dim3(256), 0, st, nn,
-                     adj, b.lk_cnt, b.lk_iso, b.lk_iso_of, ctl);
-  prof_end(st);
-  if ((rc = read_ctl(ctl, h, st))) return rc;
-  if (h->err) return status_from_err(h->err);
-  const int32_t n_iso = h->n_iso;
-  if (n_iso == 0) return 0;
   if (n_iso > nn) {
     set_error("isolated-node count out of range");
     return -5;
@@ -2667,23 +2758,24 @@ int link_round(const LadderArgs &g, const Bufs &b, Adj &adj, int cur,
   const int32_t n = g.n, k = g.k;
   const int32_t T = std::min<int32_t>(k, nn - 1);
   const int nxt = 1 - cur;
+  const unsigned wave_grid = (unsigned)std::min<int64_t>(16384, nn / 4 + 1);
   prof_begin("link", st);
-  hipLaunchKernelGGL(k_fill_i32, blocks_for(6 * (int64_t)nn), dim3(256), 0, st,
-                     reinterpret_cast<int32_t *>(b.lk_sx), 6 * (int64_t)nn, 0);
-  hipLaunchKernelGGL(k_link_sums, xblocks_for(n), dim3(256), 0, st, n, nn,
-                     b.M, g.pts, b.lk_sx, ctl);
+  hipLaunchKernelGGL(k_link_centroids, blocks_for(3 * (int64_t)nn), dim3(256),
+                     0, st, nn, b.lk_sx[cur], b.size[cur], b.lk_cen);
   const size_t lds = (size_t)kLinkNT * T * sizeof(NearKey);
   hipLaunchKernelGGL(k_link_near, dim3((unsigned)std::min<int32_t>(n_iso, 2048)),
-                     dim3(kLinkNT), lds, st, nn, b.lk_iso, ctl, b.lk_sx,
-                     b.size[cur], b.minpt[cur], T, k, b.lk_near, ctl);
+                     dim3(kLinkNT), lds, st, nn, b.lk_iso, ctl, b.lk_cen,
+                     b.minpt[cur], T, k, b.lk_near, ctl);
   hipLaunchKernelGGL(k_fill_i32, blocks_for(nn + 1), dim3(256), 0, st,
                      b.lk_ext, (int64_t)nn + 1, 0);
   hipLaunchKernelGGL(k_link_count, blocks_for((int64_t)n_iso * T), dim3(256),
                      0, st, ctl, b.lk_iso, b.lk_iso_of, b.lk_near, T, k,
                      b.lk_ext, b.lk_keep, ctl);
+  hipLaunchKernelGGL(k_link_rowcount, dim3(wave_grid), dim3(256), 0, st, nn,
+                     adj, b.lk_cnt);
   device_scan(ScanLinkWin{b.lk_cnt, b.lk_ext, b.ws[nxt], nn}, nn + 1, b.bsum,
               &ctl->slots, st);
-  hipLaunchKernelGGL(k_link_copy, xblocks_for(nn), dim3(256), 0, st, nn, adj,
+  hipLaunchKernelGGL(k_link_copy, dim3(wave_grid), dim3(256), 0, st, nn, adj,
                      b.lk_cnt, b.lk_ext, b.ws[nxt], b.wl[nxt], b.tbl[nxt],
                      b.lk_fill);
   hipLaunchKernelGGL(k_link_append, blocks_for((int64_t)n_iso * T), dim3(256),
@@ -2693,7 +2785,7 @@ int link_round(const LadderArgs &g, const Bufs &b, Adj &adj, int cur,
   if ((rc = read_ctl(ctl, h, st))) return rc;
   if (h->err) return status_from_err(h->err);
   const int64_t total = h->slots;
-  if (total < ed || total > ed + 2 * (int64_t)n_iso * T ||
+  if (total < 0 || total > (int64_t)ed + 2 * (int64_t)n_iso * T ||
       total > 2 * edge_bound(n, k)) {
     set_error("linked table size out of range (%lld)", (long long)total);
     return -5;
@@ -2709,7 +2801,7 @@ int link_round(const LadderArgs &g, const Bufs &b, Adj &adj, int cur,
                                   hipMemcpyDeviceToDevice, st), "link copy");
   if (rc) return rc;
   ed = (int32_t)total;
-  prof_bytes("link", 24.0 * n + 16.0 * total);
+  prof_bytes("link", 48.0 * nn + 16.0 * total);
   return 0;
 }
 
@@ -2721,6 +2813,7 @@ void ladder_reserve(Arena &a, int32_t n, int32_t d, int32_t k, bool link) {
 int ladder_run(const LadderArgs &g, Ctl *ctl, Arena &a, hipStream_t st) {
   Bufs b;
   carve(a, g.n, g.d, g.k, g.link, &b);
+  b.pts = g.pts;
   if (g.link && !g.pts) {
     set_error("linking isolated nodes needs the positions");
     return -1;
@@ -2893,8 +2986,9 @@ int ladder_run(const LadderArgs &g, Ctl *ctl, Arena &a, hipStream_t st) {
       adj.wl = b.wl[cur];
       adj.tbl = b.tbl[cur];
       if (nn == 1) break;  // a single component is left
-      if (g.link) {  // prepare_graph of the next round
-        if ((rc = link_round(g, b, adj, cur, nn, ed, ctl, h, st))) return rc;
+      if (g.link && h->n_iso > 0) {  // prepare_graph of the next round
+        if ((rc = link_round(g, b, adj, cur, nn, h->n_iso, ed, ctl, h, st)))
+          return rc;
         slots = ed;
       }
     }
