@@ -78,6 +78,9 @@ def _load():
         "or_edge_loss": (ctypes.c_int, [P, i64, i32, P, i32, P, P, dbl, dbl,
                                         P, P, P, P]),
         "or_purity": (ctypes.c_int, [P, i64, i64, P, i32, P, P, P]),
+        "or_round_bf16": (dbl, [dbl]),
+        "or_embed_mlp": (ctypes.c_int, [P, i64, i32, i32, i32, P, P, P, P, P,
+                                        P, P]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -389,3 +392,27 @@ def purity(label, n_comp: int, cls, n_cls: int):
         raise OracleError(rc, "purity")
     return ({"miou": out.miou, "purity": out.purity,
              "n_present": out.n_present}, maj, iou)
+
+
+# --------------------------------------------------------------------------
+# point-embedding MLP (stand-in for the embedding network of Sec. 3.1)
+# --------------------------------------------------------------------------
+
+def round_bf16(v: float) -> float:
+    return _load().or_round_bf16(float(v))
+
+
+def embed_mlp(x_bits, w1_bits, b1, w2_bits, b2, w3_bits, b3):
+    """The MLP on bfloat16 bit patterns (uint16 arrays): fp64 output [n,
+    d_out] (exact last-layer sums)."""
+    x = _c(x_bits, np.uint16)
+    n, d_in = x.shape
+    w1, w2, w3 = (_c(w, np.uint16) for w in (w1_bits, w2_bits, w3_bits))
+    b1, b2, b3 = (_c(b, np.float32) for b in (b1, b2, b3))
+    d_hid, d_out = w1.shape[1], w3.shape[1]
+    out = np.empty((n, d_out), np.float64)
+    rc = _load().or_embed_mlp(_p(x), n, d_in, d_hid, d_out, _p(w1), _p(b1),
+                              _p(w2), _p(b2), _p(w3), _p(b3), _p(out))
+    if rc:
+        raise OracleError(rc, "embed_mlp")
+    return out

@@ -1236,3 +1236,72 @@ int or_purity(const int32_t *label, int64_t n, int64_t nc, const int32_t *cls,
   free(r); free(maj); free(best); free(tp); free(ngt); free(npred);
   return OR_OK;
 }
+
+/* ======================================================================== */
+/* Point-embedding MLP, a random-weight stand-in for the point embedding     */
+/* network of Sec. 3.1 on the LiDAR-sweep workload.  Reading R20: inputs,    */
+/* weights and hidden activations are bfloat16 (round to nearest even);     */
+/* each layer is an exact dot product plus an fp32 bias, ReLU after the two  */
+/* hidden layers, the hidden values rounded to bfloat16 before the next     */
+/* layer; the output is the last layer's sum rounded to fp32.               */
+/* ======================================================================== */
+
+/* Round to the nearest value with 8 significant bits, ties to even. */
+double or_round_bf16(double v) {
+  if (v == 0.0 || !isfinite(v)) return v;
+  int e;
+  double m = frexp(v, &e); /* v = m * 2^e, 0.5 <= |m| < 1 */
+  double r = nearbyint(ldexp(m, 8)); /* default mode: ties to even */
+  return ldexp(r, e - 8);
+}
+
+static double bf16_bits_to_double(uint16_t b) {
+  uint32_t u = (uint32_t)b << 16;
+  float f;
+  memcpy(&f, &u, 4);
+  return (double)f;
+}
+
+int or_embed_mlp(const uint16_t *x, int64_t n, int32_t d_in, int32_t d_hid,
+                 int32_t d_out, const uint16_t *w1, const float *b1,
+                 const uint16_t *w2, const float *b2, const uint16_t *w3,
+                 const float *b3, double *out) {
+  if (!x || !w1 || !b1 || !w2 || !b2 || !w3 || !b3 || !out || n < 1 ||
+      d_in < 1 || d_hid < 1 || d_out < 1)
+    return OR_EINVAL;
+  double *h1 = (double *)malloc(sizeof(double) * (size_t)d_hid);
+  double *h2 = (double *)malloc(sizeof(double) * (size_t)d_hid);
+  if (!h1 || !h2) {
+    free(h1);
+    free(h2);
+    return OR_ENOMEM;
+  }
+  for (int64_t p = 0; p < n; ++p) {
+    /* layer 1: W1 is d_in x d_hid, row k = input k */
+    for (int32_t j = 0; j < d_hid; ++j) {
+      double s = 0.0;
+      for (int32_t k = 0; k < d_in; ++k)
+        s += bf16_bits_to_double(x[p * d_in + k]) *
+             bf16_bits_to_double(w1[(int64_t)k * d_hid + j]);
+      s += (double)b1[j];
+      h1[j] = or_round_bf16(s > 0.0 ? s : 0.0);
+    }
+    for (int32_t j = 0; j < d_hid; ++j) {
+      double s = 0.0;
+      for (int32_t k = 0; k < d_hid; ++k)
+        s += h1[k] * bf16_bits_to_double(w2[(int64_t)k * d_hid + j]);
+      s += (double)b2[j];
+      h2[j] = or_round_bf16(s > 0.0 ? s : 0.0);
+    }
+    for (int32_t j = 0; j < d_out; ++j) {
+      double s = 0.0;
+      for (int32_t k = 0; k < d_hid; ++k)
+        s += h2[k] * bf16_bits_to_double(w3[(int64_t)k * d_out + j]);
+      s += (double)b3[j];
+      out[p * d_out + j] = s;
+    }
+  }
+  free(h1);
+  free(h2);
+  return OR_OK;
+}

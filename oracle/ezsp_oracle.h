@@ -22,7 +22,9 @@
  *   - the grid subsampling applied before partitioning (Sec. 4.1);
  *   - the pairwise affinity and the contrastive edge loss with intra-edge
  *     dropping (Sec. 3.1, Eq. softmax, Eq. loss);
- *   - partition purity and oracle mIoU (Sec. 4.2 "Metrics").
+ *   - partition purity and oracle mIoU (Sec. 4.2 "Metrics");
+ *   - a random-weight point-embedding MLP standing in for the embedding
+ *     network of Sec. 3.1 (reading R20).
  *
  * Readings taken where the paper is silent (each one is listed, with the
  * reason, in the design notes of the repository):
@@ -56,6 +58,9 @@
  *   R17 the gradient of |e_p - e_q| at e_p = e_q is 0.
  *   R18 majority ties go to the smallest class; IoU over the classes present
  *       in the ground truth; purity = matched points / n.
+ *   R20 the embedding MLP: bfloat16 inputs, weights and hidden activations
+ *       (round to nearest even), exact dot products, fp32 biases, ReLU after
+ *       the hidden layers.
  *
  * Conventions: all pointers are host pointers owned by the caller.
  * Functions return 0 on success and a negative code on error:
@@ -232,6 +237,20 @@ typedef struct {
 int or_purity(const int32_t *label, int64_t n, int64_t nc, const int32_t *cls,
               int32_t n_cls, int32_t *majority, double *iou,
               or_purity_out *out);
+
+/* ---- point-embedding MLP (stand-in for Sec. 3.1's embedding; R20) ------- */
+
+/* Round to the nearest bfloat16 value (8 significant bits), ties to even. */
+double or_round_bf16(double v);
+
+/* out[p] = L3(bf16(relu(L2(bf16(relu(L1(x[p]))))))), L(v) = v W + b with
+ * exact dot products.  x n*d_in, w1 d_in*d_hid, w2 d_hid*d_hid,
+ * w3 d_hid*d_out as bfloat16 bits (row k = input k); biases fp32; out
+ * n*d_out fp64 (the exact last-layer sum). */
+int or_embed_mlp(const uint16_t *x, int64_t n, int32_t d_in, int32_t d_hid,
+                 int32_t d_out, const uint16_t *w1, const float *b1,
+                 const uint16_t *w2, const float *b2, const uint16_t *w3,
+                 const float *b3, double *out);
 
 #ifdef __cplusplus
 }

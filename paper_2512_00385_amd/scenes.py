@@ -452,3 +452,67 @@ def random_cloud(n: int, d: int, seed: int = 0, n_obj: int = 8,
     xyz = c[obj] + rng.standard_normal((n, 3)) * (0.1 * extent)
     emb = _embed(rng, obj, n_obj, d, sigma)
     return Scene(f"random-{n}", xyz.astype(np.float32), emb, obj, 10, [0.1])
+
+
+# --------------------------------------------------------------------------
+# LiDAR-sweep stand-in for the embedding MLP: 1,280,000 points of the
+# driving tile (a random subset: its points are stored shuffled), per-point
+# features [x/50, y/50, z/5, intensity, range/120, ring/63] for a sensor at
+# (0, 0, 1.8) with 64 rings between -24.8 and +2 degrees of elevation, and
+# PyTorch-Linear-style random weights U(+-1/sqrt(fan_in)) from
+# default_rng(seed).  Inputs and weights are handed over as bfloat16 bit
+# patterns (round to nearest even).
+# --------------------------------------------------------------------------
+
+SWEEP_POINTS = 1_280_000
+MLP_DIMS = (6, 32, 16)
+
+
+def to_bf16_bits(a) -> np.ndarray:
+    """float32 -> bfloat16 bit patterns, round to nearest even (finite)."""
+    u = np.ascontiguousarray(a, np.float32).view(np.uint32).astype(np.uint64)
+    u = (u + 0x7FFF + ((u >> 16) & 1)) >> 16
+    return u.astype(np.uint16)
+
+
+def bf16_bits_to_f32(b) -> np.ndarray:
+    return (np.asarray(b, np.uint16).astype(np.uint32) << 16).view(np.float32)
+
+
+def mlp_weights(seed: int = 0, dims=MLP_DIMS):
+    """(w1, b1, w2, b2, w3, b3): weights d_in x d_out as bfloat16 bits,
+    biases fp32."""
+    d_in, d_hid, d_out = dims
+    rng = np.random.default_rng(seed)
+    out = []
+    for fi, fo in ((d_in, d_hid), (d_hid, d_hid), (d_hid, d_out)):
+        bound = 1.0 / np.sqrt(fi)
+        w = rng.uniform(-bound, bound, (fi, fo)).astype(np.float32)
+        b = rng.uniform(-bound, bound, fo).astype(np.float32)
+        out += [to_bf16_bits(w), b]
+    return tuple(out)
+
+
+def sweep_features(xyz, obj, seed: int = 0):
+    """The six per-point features of the sweep, as bfloat16 bits [n, 6]."""
+    rng = np.random.default_rng([seed, 6])
+    xyz = np.asarray(xyz, np.float64)
+    rel = xyz - np.array([0.0, 0.0, 1.8])
+    horiz = np.hypot(rel[:, 0], rel[:, 1])
+    rng_m = np.sqrt(horiz ** 2 + rel[:, 2] ** 2)
+    elev = np.degrees(np.arctan2(rel[:, 2], horiz))
+    ring = np.clip(np.rint((elev + 24.8) / (26.8 / 63)), 0, 63)
+    n_obj = int(np.max(obj)) + 1
+    inten = rng.uniform(0, 1, n_obj)[obj] + rng.normal(0, 0.02, xyz.shape[0])
+    feat = np.stack([xyz[:, 0] / 50, xyz[:, 1] / 50, xyz[:, 2] / 5,
+                     np.clip(inten, 0, 1), rng_m / 120, ring / 63], 1)
+    return to_bf16_bits(feat.astype(np.float32))
+
+
+def sweep(seed: int = 0):
+    """(xyz [n, 3] fp32, features [n, 6] bfloat16 bits, obj) of the sweep
+    stand-in."""
+    sc = load("driving-3m", seed)
+    xyz = np.ascontiguousarray(sc.xyz[:SWEEP_POINTS])
+    obj = np.ascontiguousarray(sc.obj[:SWEEP_POINTS])
+    return xyz, sweep_features(xyz, obj, seed), obj

@@ -332,3 +332,73 @@ def test_link_step_brute_force():
             for u in ids[order]:
                 pairs.add((min(u, v), max(u, v)))
         assert list(zip(got_lo.tolist(), got_hi.tolist())) == sorted(pairs)
+
+
+# --------------------------------------------------------------------------
+# point-embedding MLP (reading R20)
+# --------------------------------------------------------------------------
+
+def test_round_bf16_matches_torch():
+    import torch
+    rng = np.random.default_rng(12)
+    v = np.concatenate([
+        rng.standard_normal(20000).astype(np.float32) * 10.0 ** rng.integers(
+            -6, 6, 20000),
+        # exact halfway cases between neighbouring bfloat16 values
+        (1.0 + (2 * np.arange(64) + 1) * 2.0 ** -8).astype(np.float32),
+        -(3.0 + (2 * np.arange(64) + 1) * 2.0 ** -7).astype(np.float32),
+    ]).astype(np.float32)
+    ref = torch.from_numpy(v).to(torch.bfloat16).to(torch.float64).numpy()
+    got = np.array([oracle.round_bf16(float(x)) for x in v])
+    assert np.array_equal(got, ref)
+
+
+def _bits(a):
+    from paper_2512_00385_amd.scenes import to_bf16_bits
+    return to_bf16_bits(np.asarray(a, np.float32))
+
+
+def test_mlp_hand_example():
+    # x = (1, 2); h1 = relu((1 + 1, -1 + 2) + (0.25, -3)) = (2.25, 0);
+    # h2 = relu((4.5, 2.25) + (0, 0.5)) = (4.5, 2.75); y = 4.5 - 5.5 + 0.125
+    out = oracle.embed_mlp(_bits([[1, 2]]), _bits([[1, -1], [0.5, 1]]),
+                           np.float32([0.25, -3]), _bits([[2, 1], [1, 1]]),
+                           np.float32([0, 0.5]), _bits([[1], [-2]]),
+                           np.float32([0.125]))
+    assert out.tolist() == [[-0.875]]
+
+
+def test_mlp_hidden_rounded_to_bf16():
+    # the hidden value 1 + 2^-8 lies halfway between bfloat16 neighbours 1 and
+    # 1 + 2^-7: ties to even give 1, so the output is 1, not 1.00390625
+    one = _bits([[1.0]])
+    out = oracle.embed_mlp(one, one, np.float32([2.0 ** -8]), one,
+                           np.float32([0]), one, np.float32([0]))
+    assert out.tolist() == [[1.0]]
+    # a negative pre-activation is cut by the ReLU
+    out = oracle.embed_mlp(one, _bits([[-1.0]]), np.float32([0.5]), one,
+                           np.float32([0]), one, np.float32([0.25]))
+    assert out.tolist() == [[0.25]]
+
+
+def test_mlp_against_torch():
+    import torch
+    from paper_2512_00385_amd import scenes
+    rng = np.random.default_rng(13)
+    x = _bits(rng.uniform(-1, 1, (500, 6)))
+    w1, b1, w2, b2, w3, b3 = scenes.mlp_weights(3)
+    got = oracle.embed_mlp(x, w1, b1, w2, b2, w3, b3)
+
+    def t(b):
+        return torch.from_numpy(scenes.bf16_bits_to_f32(b).astype(np.float64))
+
+    def bf(v):  # bfloat16 rounding by torch (fp64 -> fp32 -> bfloat16)
+        return v.to(torch.float32).to(torch.bfloat16).to(torch.float64)
+    h1 = bf(torch.relu(t(x) @ t(w1) + torch.from_numpy(b1).double()))
+    h2 = bf(torch.relu(h1 @ t(w2) + torch.from_numpy(b2).double()))
+    ref = (h2 @ t(w3) + torch.from_numpy(b3).double()).numpy()
+    # fp64 sums of at most 32 products of 8-bit significands are exact up to
+    # the last bits, so only a halfway tie seen differently could differ
+    close = np.isclose(got, ref, rtol=1e-12, atol=1e-12)
+    assert close.mean() > 0.999
+    np.testing.assert_allclose(got, ref, rtol=0, atol=2e-2)
