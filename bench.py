@@ -68,7 +68,7 @@ def parse():
                     "nodes (EZSP_F_LINK_ISOLATED)")
     ap.add_argument("--op", default="partition",
                     choices=["partition", "grid_subsample", "edge_loss",
-                             "purity"],
+                             "purity", "embed_mlp", "sweep"],
                     help="partition (the default) times the whole path; the "
                     "others time one of the secondary entry points on its "
                     "own workload and print their own line")
@@ -158,7 +158,16 @@ OPS = {
                   "gradient)"),
     "purity": ("driving-3m-paper",
                "points/sec scored (superpoint majority, oracle mIoU)"),
+    "embed_mlp": ("sweep-1.28m",
+                  "points/sec through the embedding MLP 6->32->32->16 "
+                  "(bf16, matrix cores)"),
+    "sweep": ("sweep-1.28m",
+              "ms per sweep: embedding MLP + kNN (k=10) + merge ladder "
+              "{0.05, 0.2, 0.8}"),
 }
+SWEEP_KIND = ("1,280,000 points of the synthetic driving tile as one LiDAR "
+              "sweep, features [x/50, y/50, z/5, intensity, range/120, "
+              "ring/63] in bf16, random MLP weights (seed 0)")
 
 
 def bench_op(args, ezsp, scenes, np, torch):
@@ -166,6 +175,8 @@ def bench_op(args, ezsp, scenes, np, torch):
     events around the library's launches of that stage."""
     import oracle
     name, metric = OPS[args.op]
+    if args.op in ("embed_mlp", "sweep"):
+        return bench_sweep(args, ezsp, scenes, np, torch, metric)
     sc = scenes.load(name)
     dev = torch.device("cuda:0")
     xyz = torch.from_numpy(sc.xyz).to(dev)
@@ -256,6 +267,98 @@ def bench_op(args, ezsp, scenes, np, torch):
             "value": sc.n / (c1 - c0), "unit": "points/s", "cores": 1,
             "kind": "oracle",
             "sample": f"the whole {sc.name} input, one thread, {c1 - c0:.2f} s",
+        }
+    print(json.dumps(out), flush=True)
+
+
+def bench_sweep(args, ezsp, scenes, np, torch, metric):
+    """The LiDAR-sweep stand-in: the embedding MLP alone (--op embed_mlp) or
+    the whole per-sweep latency, MLP then partition (--op sweep)."""
+    import oracle
+    dev = torch.device("cuda:0")
+    xyz_np, feat_np, _ = scenes.sweep()
+    wts = scenes.mlp_weights(0)
+    n = xyz_np.shape[0]
+
+    def to_dev(a):
+        a = np.ascontiguousarray(a)
+        return torch.from_numpy(a.view(np.int16) if a.dtype == np.uint16
+                                else a).to(dev)
+    xyz = to_dev(xyz_np)
+    feat = to_dev(feat_np)
+    w = [to_dev(a) for a in wts]
+    lambdas = [0.05, 0.2, 0.8]
+    part = ezsp.Partitioner(n, 16, 10, lambdas, device=dev) \
+        if args.op == "sweep" else None
+
+    def step():
+        emb = ezsp.embed_mlp(feat, *w)
+        if part is not None:
+            return part(xyz, emb)
+        return emb
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    stage_names = list(ezsp.STAGES) + ["embed_mlp"]
+    ezsp.profile_enable(True)
+    ezsp.profile_only(None)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    stats = {s: ezsp.profile_read(s) for s in stage_names}
+    ezsp.profile_enable(False)
+    ms_per_step = (t1 - t0) * 1e3 / args.steps
+    dom = max(stats, key=lambda s: stats[s][1])
+    launches, ms, nbytes = stats[dom]
+    per_ms = ms / max(launches, 1)
+    per_bytes = nbytes / max(launches, 1)
+    achieved = per_bytes / (per_ms * 1e-3) / 1e9 if per_ms > 0 else 0.0
+    mlp_l, mlp_ms, _ = stats["embed_mlp"]
+    mlp_per_ms = mlp_ms / max(mlp_l, 1)
+    flops = 2.0 * n * (6 * 32 + 32 * 32 + 32 * 16)
+    sweep = args.op == "sweep"
+    out = {
+        "metric": metric,
+        "value": round(ms_per_step, 4) if sweep
+        else round(n / (ms_per_step / 1e3), 1),
+        "unit": "ms" if sweep else "points/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": not sweep, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16+f64" if sweep else "bf16",
+        "data": "synthetic",
+        "config": {"workload": f"{args.op} on sweep-1.28m: {SWEEP_KIND}",
+                   "n_points": n, "mlp": "6->32->32->16",
+                   **({"k": 10, "lambdas": lambdas} if sweep else {})},
+        "roofline": {"bound": "hbm", "kernel": dom,
+                     "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s",
+                     "frac": round(achieved / HBM_PEAK_GBS, 5),
+                     "traffic": None, "launch_ms": round(per_ms, 5),
+                     "alg_bytes_per_launch": per_bytes},
+        "mlp": {"launch_ms": round(mlp_per_ms, 5),
+                "tflops": round(flops / (mlp_per_ms * 1e-3) / 1e12, 3)
+                if mlp_per_ms > 0 else 0.0,
+                "bf16_mfma_peak_tflops": 2500.0},
+        "stage_ms_per_step": {s: round(v[1] / args.steps, 4)
+                              for s, v in stats.items()},
+    }
+    if not args.no_cpu:
+        print("[bench] cpu baseline (oracle)", file=sys.stderr, flush=True)
+        c0 = time.perf_counter()
+        e = oracle.embed_mlp(feat_np, *wts).astype(np.float32)
+        if sweep:
+            oracle.partition(xyz_np, e, 10, lambdas, want_energy=False)
+        c1 = time.perf_counter()
+        out["cpu_baseline"] = {
+            "value": round((c1 - c0) * 1e3, 1) if sweep else n / (c1 - c0),
+            "unit": "ms" if sweep else "points/s", "cores": 1,
+            "kind": "oracle",
+            "sample": f"the whole sweep ({n} points), one thread, "
+                      f"{c1 - c0:.2f} s",
         }
     print(json.dumps(out), flush=True)
 

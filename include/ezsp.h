@@ -251,6 +251,24 @@ int ezsp_purity(const int32_t *labels, int64_t n, int64_t n_comp,
                 double *iou, ezsp_purity_stats *out, void *ws,
                 size_t ws_bytes, void *stream);
 
+/* ---- point-embedding MLP (stand-in for the embedding network of
+ * Sec. 3.1 on the LiDAR-sweep workload) ----------------------------------- */
+
+/* out[p] = L3(h2), h2 = bf16(relu(L2(h1))), h1 = bf16(relu(L1(x[p]))),
+ * L(v) = v W + b: a per-point MLP d_in -> 32 -> 32 -> d_out on the matrix
+ * cores.  bf16 = round to nearest even; products of bfloat16 values are
+ * accumulated in fp32 (the summation order is the matrix unit's).
+ *   x    n*d_in bfloat16 bit patterns (in), d_in in 1..8
+ *   w1   d_in*32, w2 32*32, w3 32*d_out bfloat16 bits, row k = input k
+ *   b1   32, b2 32, b3 d_out fp32
+ *   out  n*d_out fp32 (out), d_out in 1..32
+ * d_hid must be 32.  Needs no workspace.
+ * Errors: INVALID_ARG, DEVICE. */
+int ezsp_embed_mlp(const uint16_t *x, int64_t n, int32_t d_in, int32_t d_hid,
+                   int32_t d_out, const uint16_t *w1, const float *b1,
+                   const uint16_t *w2, const float *b2, const uint16_t *w3,
+                   const float *b3, float *out, void *stream);
+
 /* ---- diagnostics --------------------------------------------------------- */
 
 /* Static text for a status code. */
@@ -262,7 +280,7 @@ const char *ezsp_last_error(void);
 /* Per-stage timing with HIP events recorded on the caller's stream around
  * the launches of each stage ("knn_query", "morton_sort", "graph_build",
  * "select", "union", "stats", "contract", "compose", "tail", "link",
- * "grid_subsample", "edge_loss", "purity").  Off by default; a
+ * "grid_subsample", "edge_loss", "purity", "embed_mlp").  Off by default; a
  * diagnostic for benchmarks.  ezsp_profile_enable(1) clears the totals and
  * starts recording, ezsp_profile_enable(0) stops.  ezsp_profile_read gives
  * the number of recorded launches of `stage`, their summed duration in

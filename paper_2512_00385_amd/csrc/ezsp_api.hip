@@ -389,4 +389,21 @@ int ezsp_purity(const int32_t *labels, int64_t n, int64_t n_comp,
   return EZSP_OK;
 }
 
+int ezsp_embed_mlp(const uint16_t *x, int64_t n, int32_t d_in, int32_t d_hid,
+                   int32_t d_out, const uint16_t *w1, const float *b1,
+                   const uint16_t *w2, const float *b2, const uint16_t *w3,
+                   const float *b3, float *out, void *stream) {
+  set_error("%s", "");
+  if (!x || !w1 || !b1 || !w2 || !b2 || !w3 || !b3 || !out)
+    return fail(EZSP_ERR_INVALID_ARG, "no pointer may be NULL");
+  if (!n_ok(n)) return fail(EZSP_ERR_INVALID_ARG, "n must be in [1, 2^31)");
+  if (d_in < 1 || d_in > 8 || d_hid != 32 || d_out < 1 || d_out > 32)
+    return fail(EZSP_ERR_INVALID_ARG,
+                "the MLP is d_in (1..8) -> 32 -> 32 -> d_out (1..32)");
+  if (n * (int64_t)d_out >= kMaxN || n * (int64_t)d_in >= kMaxN)
+    return fail(EZSP_ERR_INVALID_ARG, "n*d_out must stay below 2^31");
+  return mlp_run(x, (int32_t)n, d_in, d_out, w1, b1, w2, b2, w3, b3, out,
+                 static_cast<hipStream_t>(stream));
+}
+
 }  // extern "C"

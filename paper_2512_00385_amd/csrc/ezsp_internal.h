@@ -175,6 +175,12 @@ int purity_run(const int32_t *labels, int32_t n, int32_t n_comp,
                double *iou, PurityResult *res, Ctl *ctl, Arena &a,
                hipStream_t st);
 
+// Point-embedding MLP d_in -> 32 -> 32 -> d_out on the matrix cores.
+int mlp_run(const uint16_t *x, int32_t n, int32_t d_in, int32_t d_out,
+            const uint16_t *w1, const float *b1, const uint16_t *w2,
+            const float *b2, const uint16_t *w3, const float *b3, float *out,
+            hipStream_t st);
+
 // Shared host helpers.
 void set_error(const char *fmt, ...);
 int read_ctl(Ctl *ctl, Ctl *host, hipStream_t st);  // sync + copy back

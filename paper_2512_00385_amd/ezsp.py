@@ -37,6 +37,7 @@ ENTRY_POINTS = (
     "ezsp_grid_subsample_workspace_size", "ezsp_grid_subsample",
     "ezsp_edge_loss_workspace_size", "ezsp_edge_loss",
     "ezsp_purity_workspace_size", "ezsp_purity",
+    "ezsp_embed_mlp",
 )
 
 
@@ -107,6 +108,8 @@ def load() -> ctypes.CDLL:
         "ezsp_purity_workspace_size": (sz, [i64, i64, i32]),
         "ezsp_purity": (ctypes.c_int, [P, i64, i64, P, i32, P, P, P, P, sz,
                                        P]),
+        "ezsp_embed_mlp": (ctypes.c_int, [P, i64, i32, i32, i32, P, P, P, P,
+                                          P, P, P, P]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -136,7 +139,7 @@ def profile_only(stage=None):
 
 STAGES = ("morton_sort", "knn_query", "graph_build", "select", "union",
           "stats", "contract", "compose", "tail", "link")
-EXTRA_STAGES = ("grid_subsample", "edge_loss", "purity")
+EXTRA_STAGES = ("grid_subsample", "edge_loss", "purity", "embed_mlp")
 
 
 def profile_read(stage: str):
@@ -393,3 +396,36 @@ def purity(labels: torch.Tensor, n_comp: int, cls: torch.Tensor, n_cls: int):
                            _ptr(ws), nbytes, _stream(dev)), "ezsp_purity")
     stats = {f: getattr(out, f) for f, _ in PurityStats._fields_}
     return stats, maj, iou
+
+
+def embed_mlp(x_bits: torch.Tensor, w1, b1, w2, b2, w3, b3) -> torch.Tensor:
+    """Per-point MLP d_in -> 32 -> 32 -> d_out on the matrix cores.  x_bits
+    and the weights are bfloat16 tensors (or int16 tensors of their bits) on
+    the device, weights as [fan_in, fan_out]; biases fp32.  Returns
+    [n, d_out] fp32."""
+    lib = load()
+
+    def bits(t, name):
+        if not isinstance(t, torch.Tensor) or not t.is_cuda:
+            raise TypeError(f"{name} must be a device tensor")
+        if t.dtype == torch.bfloat16:
+            t = t.view(torch.int16)
+        if t.dtype != torch.int16:
+            raise TypeError(f"{name} must be bfloat16 (or its int16 bits)")
+        return t.contiguous()
+    x = bits(x_bits, "x")
+    w1, w2, w3 = bits(w1, "w1"), bits(w2, "w2"), bits(w3, "w3")
+    b1 = _dev_tensor(b1, torch.float32, "b1")
+    b2 = _dev_tensor(b2, torch.float32, "b2")
+    b3 = _dev_tensor(b3, torch.float32, "b3")
+    n, d_in = x.shape
+    d_hid, d_out = w1.shape[1], w3.shape[1]
+    if w1.shape[0] != d_in or w2.shape != (d_hid, d_hid) or \
+            w3.shape[0] != d_hid:
+        raise ValueError("weight shapes do not chain")
+    out = torch.empty((n, d_out), dtype=torch.float32, device=x.device)
+    _check(lib.ezsp_embed_mlp(_ptr(x), n, d_in, d_hid, d_out, _ptr(w1),
+                              _ptr(b1), _ptr(w2), _ptr(b2), _ptr(w3),
+                              _ptr(b3), _ptr(out), _stream(x.device)),
+           "ezsp_embed_mlp")
+    return out

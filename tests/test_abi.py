@@ -202,3 +202,21 @@ def test_result_struct_layouts():
     assert ctypes.sizeof(ezsp.LossStats) == 40
     assert ctypes.sizeof(ezsp.PurityStats) == 24
     assert ezsp.PurityStats.n_present.offset == 16
+
+
+def test_embed_mlp_rejects_bad_arguments():
+    lib = ezsp.load()
+    E = ezsp.ERR_INVALID_ARG
+
+    def mlp(n=10, d_in=6, d_hid=32, d_out=16, x=FAKE, out=FAKE):
+        return lib.ezsp_embed_mlp(x, n, d_in, d_hid, d_out, FAKE, FAKE, FAKE,
+                                  FAKE, FAKE, FAKE, out, None)
+    assert mlp(x=None) == E
+    assert mlp(out=None) == E
+    assert mlp(n=0) == E
+    assert mlp(d_in=0) == E
+    assert mlp(d_in=9) == E
+    assert mlp(d_hid=16) == E
+    assert mlp(d_out=0) == E
+    assert mlp(d_out=33) == E
+    assert mlp(n=2 ** 31) == E
