@@ -124,7 +124,7 @@ int grid_run(const float *xyz, int32_t n, float h, int32_t *keep,
   const int nt = 256;
   const int64_t gb = (n + nt - 1) / nt;
   prof_begin("grid_subsample", st);
-  hipLaunchKernelGGL(k_bbox, dim3((unsigned)(gb < 1024 ? gb : 1024)), dim3(nt),
+  hipLaunchKernelGGL(k_bbox, dim3((unsigned)(gb < 256 ? gb : 256)), dim3(nt),
                      0, st, xyz, n, ctl);
   const int64_t cb = (int64_t)((cap + nt - 1) / nt);
   hipLaunchKernelGGL(k_grid_clear, dim3((unsigned)(cb < 4096 ? cb : 4096)),

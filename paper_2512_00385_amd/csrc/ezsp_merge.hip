@@ -2022,17 +2022,20 @@ __global__ __launch_bounds__(256) void k_tail_labels(
 
 // Rows of the table the tail starts from, packed end to end (the windows of
 // the multi-kernel path hold their rows at the front and may be larger).
+// A wave per row, lanes striding over its entries (hub rows are long).
 __global__ __launch_bounds__(256) void k_repack(
     int32_t nn, const int32_t *__restrict__ ws, const int32_t *__restrict__ wl,
     const uint64_t *__restrict__ tbl, const int32_t *__restrict__ ws2,
     int32_t *__restrict__ wl2, uint64_t *__restrict__ tbl2) {
-  const int32_t v = blockIdx.x * blockDim.x + threadIdx.x;
+  const int lane = threadIdx.x & (kWave - 1);
+  const int32_t v = (int32_t)(blockIdx.x * (blockDim.x / kWave) +
+                              threadIdx.x / kWave);
   if (v >= nn) return;
   const int32_t len = wl[v];
   const uint64_t *src = tbl + ws[v];
   uint64_t *dst = tbl2 + ws2[v];
-  for (int32_t j = 0; j < len; ++j) dst[j] = src[j];
-  wl2[v] = len;
+  for (int32_t j = lane; j < len; j += kWave) dst[j] = src[j];
+  if (lane == 0) wl2[v] = len;
 }
 
 // ---------------------------------------------------------------------------
@@ -2669,7 +2672,7 @@ int run_tail(const LadderArgs &g, const Bufs &b, const float *emb,
   const int nxt = 1 - cur;
   device_scan(ScanArray{b.wl[cur], b.ws[nxt], nn, nullptr}, nn + 1, b.bsum,
               b.tmp, st);
-  hipLaunchKernelGGL(k_repack, blocks_for(nn), dim3(256), 0, st, nn, b.ws[cur],
+  hipLaunchKernelGGL(k_repack, blocks_for((int64_t)nn * kWave), dim3(256), 0, st, nn, b.ws[cur],
                      b.wl[cur], b.tbl[cur], b.ws[nxt], b.wl[nxt], b.tbl[nxt]);
   t.tcur0 = nxt;
   t.d = d;
