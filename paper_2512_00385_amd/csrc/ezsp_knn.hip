@@ -1,11 +1,13 @@
 // ezsp_knn.hip -- exact k-nearest-neighbour adjacency (Sec. 3.1: every point
 // linked to its k nearest neighbours; Sec. 4.1: k and unit weights).
 //
-// Grid build: each point gets a 48-bit Morton key of its 16-bit-per-axis
-// voxel in the bounding box; a radix sort lays the points out in Morton
-// order.  Consecutive runs of 16 sorted points form buckets, and an implicit
-// 8-ary tree of axis-aligned boxes sits over the buckets, so the voxel
-// hierarchy adapts to any density.
+// Grid build: each point gets a 39-bit Morton key of its 13-bit-per-axis
+// voxel in the bounding box (cubic voxels of 1/8191 of the largest extent:
+// a 100 m tile gets 1.2 cm voxels, which hold about one point each in the
+// test scenes); a radix sort of five 8-bit passes lays the points out in
+// Morton order.  Consecutive runs of 16 sorted points form buckets, and an
+// implicit 8-ary tree of axis-aligned boxes sits over the buckets, so the
+// voxel hierarchy adapts to any density.
 //
 // Query: one bucket per 16-lane DPP row (four buckets per wavefront), one
 // query point per lane.  Each lane keeps its own sorted top-k of 64-bit keys
@@ -105,7 +107,10 @@ __global__ __launch_bounds__(256) void k_bbox(const float *xyz, int32_t n,
   }
 }
 
-// 16 bits -> every third bit of 48.
+constexpr int kMortonBits = 13;  // per axis
+constexpr float kMortonMax = (float)((1 << kMortonBits) - 1);
+
+// 16 bits -> every third bit of 48 (only the low kMortonBits are set).
 __device__ __forceinline__ uint64_t spread3(uint32_t v) {
   uint64_t x = v & 0xffffu;
   x = (x | (x << 16)) & 0x0000ff0000ffull;
@@ -126,12 +131,12 @@ __global__ __launch_bounds__(256) void k_morton(const float *xyz, int32_t n,
     lo[a] = ord2f(ctl->bbox_enc[a]);
     ext = fmaxf(ext, ord2f(ctl->bbox_enc[3 + a]) - lo[a]);
   }
-  const float scale = (ext > 0.0f) ? 65535.0f / ext : 0.0f;
+  const float scale = (ext > 0.0f) ? kMortonMax / ext : 0.0f;
   uint32_t q[3];
 #pragma unroll
   for (int a = 0; a < 3; ++a) {
     float t = (xyz[3 * (int64_t)i + a] - lo[a]) * scale;
-    t = fminf(fmaxf(t, 0.0f), 65535.0f);  // NaN maps to 0
+    t = fminf(fmaxf(t, 0.0f), kMortonMax);  // NaN maps to 0
     q[a] = (uint32_t)t;
   }
   keys[i] = spread3(q[0]) | (spread3(q[1]) << 1) | (spread3(q[2]) << 2);
@@ -467,7 +472,8 @@ hipError_t knn_launch(const float *xyz, int32_t n, int32_t k, Ctl *ctl,
   hipLaunchKernelGGL(k_morton, dim3(gb), dim3(nt), 0, st, xyz, n, ctl, s.keys,
                      s.vals);
   prof_begin("morton_sort", st);
-  const bool alt = radix_sort_pairs(s.keys, s.vals, s.keys2, s.vals2, n, 48,
+  const bool alt = radix_sort_pairs(s.keys, s.vals, s.keys2, s.vals2, n,
+                                    3 * kMortonBits,
                                     s.hist, s.bsum, s.total, ctl, st);
   prof_end(st);
   const uint32_t *order = alt ? s.vals2 : s.vals;
