@@ -1636,6 +1636,7 @@ struct TailState {
   int64_t *S[2];
   double *mu;
   double *gain;                            // one per slot
+  int32_t *row[2];                         // row of every occupied slot
   int32_t *Mt;
   int32_t *lvl_map, *lvl_minpt, *lvl_nc;  // kTailLevels x nn0 (nc: levels)
   int32_t *lvl_rank;                       // kTailLevels x nn0
@@ -1662,7 +1663,9 @@ __device__ __forceinline__ void wg_min(int32_t *p, int32_t v) {
 }
 
 // table_add for the tail (same probing, workgroup-scope atomics).
-__device__ __forceinline__ bool tail_table_add(uint64_t *tbl, int32_t base,
+// A slot it claims records its row A in row[].
+__device__ __forceinline__ bool tail_table_add(uint64_t *tbl, int32_t *row,
+                                               int32_t A, int32_t base,
                                                int32_t cap, int32_t B,
                                                int32_t w, Ctl *ctl) {
   uint32_t h = ((uint32_t)B * 2654435761u) % (uint32_t)cap;
@@ -1672,8 +1675,10 @@ __device__ __forceinline__ bool tail_table_add(uint64_t *tbl, int32_t base,
     uint64_t cur = kEmpty;
     if (__hip_atomic_compare_exchange_strong(slot, &cur, mine,
                                              __ATOMIC_RELAXED, __ATOMIC_RELAXED,
-                                             __HIP_MEMORY_SCOPE_WORKGROUP))
+                                             __HIP_MEMORY_SCOPE_WORKGROUP)) {
+      row[base + h] = A;
       return true;
+    }
     if ((int32_t)(cur >> 32) == B) {
       __hip_atomic_fetch_add(slot, (uint64_t)(uint32_t)w, __ATOMIC_RELAXED,
                              __HIP_MEMORY_SCOPE_WORKGROUP);
@@ -1762,6 +1767,7 @@ __global__ __launch_bounds__(kTailNT) void k_tail(TailState t, Ctl *ctl) {
   for (int32_t q = threadIdx.x; q < Q; q += kTailNT) {
     const int32_t v = tail_row(s_ws, nn, q);
     if (q - s_ws[v] >= t.wl[tc][v]) t.tbl[tc][q] = kEmpty;
+    t.row[tc][q] = v;
   }
   __syncthreads();
   for (int32_t l = t.level0; l < t.n_levels; ++l) {
@@ -1778,6 +1784,7 @@ __global__ __launch_bounds__(kTailNT) void k_tail(TailState t, Ctl *ctl) {
       }
       const int nxt = 1 - cur;
       const uint64_t *tb = t.tbl[tc];
+      const int32_t *rows = t.row[tc];
       NodeIn s;
       s.size = t.size[cur];
       s.S = t.S[cur];
@@ -1799,7 +1806,7 @@ __global__ __launch_bounds__(kTailNT) void k_tail(TailState t, Ctl *ctl) {
       for (int32_t q = threadIdx.x; q < Q; q += kTailNT) {
         const uint64_t e = tb[q];
         if (e == kEmpty) continue;
-        const int32_t v = tail_row(s_ws, nn, q);
+        const int32_t v = rows[q];
         const int32_t u = (int32_t)(e >> 32), w = (int32_t)(uint32_t)e;
         if ((uint32_t)u >= (uint32_t)nn) {
           raise_err(ctl, kErrInternal);
@@ -1825,7 +1832,7 @@ __global__ __launch_bounds__(kTailNT) void k_tail(TailState t, Ctl *ctl) {
       for (int32_t q = threadIdx.x; q < Q; q += kTailNT) {
         const uint64_t e = tb[q];
         if (e == kEmpty) continue;
-        const int32_t v = tail_row(s_ws, nn, q);
+        const int32_t v = rows[q];
         const unsigned long long kv = s_key[v];
         if (kv != 0ull && gain_key(t.gain[q]) == kv)
           atomicMin(&s_sel[v], s_minpt[(int32_t)(e >> 32)]);
@@ -1835,7 +1842,7 @@ __global__ __launch_bounds__(kTailNT) void k_tail(TailState t, Ctl *ctl) {
       for (int32_t q = threadIdx.x; q < Q; q += kTailNT) {
         const uint64_t e = tb[q];
         if (e == kEmpty) continue;
-        const int32_t v = tail_row(s_ws, nn, q);
+        const int32_t v = rows[q];
         const int32_t u = (int32_t)(e >> 32);
         const unsigned long long kv = s_key[v];
         if (kv != 0ull && s_minpt[u] == s_sel[v] &&
@@ -1924,11 +1931,11 @@ __global__ __launch_bounds__(kTailNT) void k_tail(TailState t, Ctl *ctl) {
       for (int32_t q = threadIdx.x; q < Q; q += kTailNT) {
         const uint64_t e = tb[q];
         if (e == kEmpty) continue;
-        const int32_t v = tail_row(s_ws, nn, q);
+        const int32_t v = rows[q];
         const int32_t A = s_L[v], B = s_L[(int32_t)(e >> 32)];
         if (A == B) continue;  // edge inside a merged component
-        claims += tail_table_add(t.tbl[1 - tc], s_wn[A], s_cap[A], B,
-                                 (int32_t)(uint32_t)e, ctl)
+        claims += tail_table_add(t.tbl[1 - tc], t.row[1 - tc], A, s_wn[A],
+                                 s_cap[A], B, (int32_t)(uint32_t)e, ctl)
                       ? 1
                       : 0;
       }
@@ -2392,6 +2399,7 @@ struct Bufs {
   int32_t *M, *mark, *lrank;
   int32_t nt;  // nodes the tail can start from
   double *tgain;    // per-slot gains in the tail
+  int32_t *trow[2]; // per-slot rows in the tail
   int32_t tslots;   // entries of tgain
   int32_t *Mt, *lvl_map, *lvl_minpt, *lvl_rank;
   double *lvl_mu;
@@ -2460,6 +2468,8 @@ void carve(Arena &a, int32_t n, int32_t d, int32_t k, bool link, Bufs *b) {
   b->Mt = a.take<int32_t>(b->nt);
   b->tslots = (int32_t)std::min<int64_t>(ed, kTailSlots);
   b->tgain = a.take<double>(b->tslots);
+  b->trow[0] = a.take<int32_t>(b->tslots);
+  b->trow[1] = a.take<int32_t>(b->tslots);
   b->lvl_map = a.take<int32_t>((size_t)kTailLevels * b->nt);
   b->lvl_minpt = a.take<int32_t>((size_t)kTailLevels * b->nt);
   b->lvl_rank = a.take<int32_t>((size_t)kTailLevels * b->nt);
@@ -2657,6 +2667,8 @@ int run_tail(const LadderArgs &g, const Bufs &b, const float *emb,
   }
   t.mu = b.mu;
   t.gain = b.tgain;
+  t.row[0] = b.trow[0];
+  t.row[1] = b.trow[1];
   t.Mt = b.Mt;
   t.lvl_map = b.lvl_map;
   t.lvl_minpt = b.lvl_minpt;
