@@ -1732,6 +1732,43 @@ __device__ __forceinline__ unsigned long long gain_key(double g) {
   return (b >> 63) ? ~b : (b | (1ull << 63));
 }
 
+// Prop. 1 for the entry (v, u) in the tail: the operations of edge_gain in
+// the same order, sizes from LDS and the two mean rows streamed two
+// dimensions at a time (few registers: the tail runs 1024 threads).
+template <int DT>
+__device__ __forceinline__ double tail_gain(const double *__restrict__ mu,
+                                            int32_t v, int32_t u, int32_t d,
+                                            double dsv, double dsu, int32_t w,
+                                            double lambda) {
+  const double num = dsv * dsu;
+  const double den = dsv + dsu;
+  const double f = num / den;
+  double ss = 0.0;
+  if constexpr (DT > 0) {
+    const double2 *a = reinterpret_cast<const double2 *>(mu + (int64_t)v * DT);
+    const double2 *b = reinterpret_cast<const double2 *>(mu + (int64_t)u * DT);
+#pragma unroll
+    for (int i = 0; i < DT / 2; ++i) {
+      const double2 x = a[i], y = b[i];
+      const double d0 = x.x - y.x;
+      const double q0 = d0 * d0;
+      ss = ss + q0;
+      const double d1 = x.y - y.y;
+      const double q1 = d1 * d1;
+      ss = ss + q1;
+    }
+  } else {
+    for (int32_t i = 0; i < d; ++i) {
+      const double diff = mu[(int64_t)v * d + i] - mu[(int64_t)u * d + i];
+      const double sq = diff * diff;
+      ss = ss + sq;
+    }
+  }
+  const double cut = lambda * (double)w;
+  const double fit = f * ss;
+  return cut - fit;
+}
+
 template <int DT>
 __global__ __launch_bounds__(kTailNT) void k_tail(TailState t, Ctl *ctl) {
   __shared__ int32_t s_size[kTailNodes];
@@ -1813,16 +1850,8 @@ __global__ __launch_bounds__(kTailNT) void k_tail(TailState t, Ctl *ctl) {
           continue;
         }
         atomicAdd(&s_deg[v], 1);
-        double g;
-        if constexpr (DT > 0) {
-          MeanRow<false, DT> mv;
-          mv.load(s, v, sF, sIF);
-          g = edge_gain_t<false, DT>(s, mv, v, (double)s_size[v], u, w, d,
-                                     lambda, sF, sIF);
-        } else {
-          g = edge_gain<false>(s, v, (double)s_size[v], u, w, d, lambda, sF,
-                               sIF);
-        }
+        const double g = tail_gain<DT>(s.mu, v, u, d, (double)s_size[v],
+                                       (double)s_size[u], w, lambda);
         t.gain[q] = g;
         if (g > 0.0 || (long long)s_size[v] < smin)
           atomicMax(&s_key[v], gain_key(g));
