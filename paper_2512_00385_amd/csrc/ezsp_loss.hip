@@ -59,6 +59,28 @@ __device__ __forceinline__ T block_sum(T v, T *sh) {
 }
 
 // Slot status and the pair counts.
+// Position of p in row r (k entries), or -1; rows of 4k ids are read as
+// int4 (the table is 16-byte aligned then).
+template <bool VEC4>
+__device__ __forceinline__ int32_t find_in_row(const int32_t *r, int32_t k,
+                                               int32_t p) {
+  if (VEC4) {
+    const int4 *r4 = reinterpret_cast<const int4 *>(r);
+    for (int32_t t = 0; t < k / 4; ++t) {
+      const int4 x = r4[t];
+      if (x.x == p) return 4 * t;
+      if (x.y == p) return 4 * t + 1;
+      if (x.z == p) return 4 * t + 2;
+      if (x.w == p) return 4 * t + 3;
+    }
+    return -1;
+  }
+  for (int32_t t = 0; t < k; ++t)
+    if (r[t] == p) return t;
+  return -1;
+}
+
+template <bool VEC4>
 __global__ __launch_bounds__(kLeNT) void k_le_classify(
     const int32_t *__restrict__ nbr, int32_t n, int32_t k,
     const int32_t *__restrict__ cls, uint16_t *__restrict__ status,
@@ -79,10 +101,7 @@ __global__ __launch_bounds__(kLeNT) void k_le_classify(
       const int32_t *row = nbr + (int64_t)p * k;
       for (int32_t t = 0; t < j && first; ++t) first = row[t] != q;
       if (first) {
-        const int32_t *rq = nbr + (int64_t)q * k;
-        int32_t jq = -1;
-        for (int32_t t = 0; t < k && jq < 0; ++t)
-          if (rq[t] == p) jq = t;
+        const int32_t jq = find_in_row<VEC4>(nbr + (int64_t)q * k, k, p);
         const bool mutual = jq >= 0;
         const bool owner = p < q || !mutual;
         v = (cls[p] == cls[q]) ? kSlotIntra : kSlotInter;
@@ -336,8 +355,12 @@ int loss_run(const LossArgs &g, LossResult *res, Ctl *ctl, Arena &a,
                        0, st, g.grad, (int64_t)g.n * g.d);
   hipLaunchKernelGGL(k_maxabs, dim3(2048), dim3(256), 0, st, g.emb,
                      (int64_t)g.n * g.d, ctl);
-  hipLaunchKernelGGL(k_le_classify, dim3(grid_for(ns)), dim3(kLeNT), 0, st,
-                     g.nbr, g.n, g.k, g.cls, status, ctl);
+  if (g.k % 4 == 0 && (reinterpret_cast<uintptr_t>(g.nbr) & 15) == 0)
+    hipLaunchKernelGGL(k_le_classify<true>, dim3(grid_for(ns)), dim3(kLeNT),
+                       0, st, g.nbr, g.n, g.k, g.cls, status, ctl);
+  else
+    hipLaunchKernelGGL(k_le_classify<false>, dim3(grid_for(ns)), dim3(kLeNT),
+                       0, st, g.nbr, g.n, g.k, g.cls, status, ctl);
   hipLaunchKernelGGL(k_le_quota, dim3(1), dim3(64), 0, st, ctl, g.rho);
   for (int shift = 56; shift >= 0; shift -= 8) {
     hipLaunchKernelGGL(k_le_hist, dim3(grid_for(ns)), dim3(kLeNT), 0, st,
