@@ -28,7 +28,7 @@ _lib = None
 
 
 def build(force: bool = False) -> str:
-    """Compile liboracle.so with gcc (the checker is built, never shipped)."""
+    """Compile liboracle.so with gcc (built here for the tests, never shipped)."""
     if force or not os.path.exists(_LIB) or \
             os.path.getmtime(_LIB) < max(os.path.getmtime(_SRC),
                                          os.path.getmtime(_SRC[:-2] + ".h")):
