@@ -258,6 +258,9 @@ struct NodeIn {
   const int32_t *minpt;  // smallest point   (null in the first round)
   const float *emb;      // point embeddings, internal order (first round)
   const int32_t *perm;   // internal -> original point, nullable (identity)
+  const uint8_t *merged; // 1 for a node formed by a merge in the last round;
+                         // null: every node is evaluated (a level's first
+                         // round)
 };
 
 struct Adj {
@@ -534,7 +537,30 @@ __global__ __launch_bounds__(256) void k_select(
   }
   Best b{0.0, 0, -1};
   int32_t cnt = 0;
-  if (live) {
+  bool skip = false;
+  if constexpr (!FIRST) {
+    // A node that did not merge, with no neighbour that merged, has the
+    // gains of the last round, which gave it no candidate: no candidate now.
+    if (s.merged) {
+      int32_t any = 0, c0 = 0;
+      if (live) {
+        any = s.merged[v];
+        if (!any)  // a merged node is evaluated anyway: no scan for it
+          for_row<false>(a, v, lg, G, [&](int32_t u, int32_t) {
+            ++c0;
+            if ((uint32_t)u < (uint32_t)nn) any |= s.merged[u];
+          });
+      }
+#pragma unroll
+      for (int off = G / 2; off > 0; off >>= 1)
+        any |= __shfl_xor(any, off, kWave);
+      if (!any) {
+        skip = true;
+        cnt = c0;
+      }
+    }
+  }
+  if (live && !skip) {
     const int F = ctl->F;
     const double sF = ldexp(1.0, F), sIF = ldexp(1.0, -F);
     const int32_t sv = node_size<FIRST>(s, v);
@@ -657,6 +683,15 @@ __global__ __launch_bounds__(256) void k_select_combine(
     deg[v] = cnt;
     if (b.u >= 0) ctl->any_choice = 1;
   }
+}
+
+// The next round's merged flags: a component of more than one member.
+__global__ __launch_bounds__(256) void k_merged(const int32_t *moff,
+                                                uint8_t *merged, Ctl *ctl) {
+  if (!ctl->any_choice) return;
+  int32_t c;
+  if (!xcd_item(ctl->n_next, c)) return;
+  merged[c] = (moff[c + 1] - moff[c] > 1) ? 1 : 0;
 }
 
 // ---------------------------------------------------------------------------
@@ -1829,6 +1864,7 @@ __global__ __launch_bounds__(kTailNT) void k_tail(TailState t, Ctl *ctl) {
       s.minpt = t.minpt[cur];
       s.emb = nullptr;
       s.perm = nullptr;
+      s.merged = nullptr;
       if (threadIdx.x == 0) s_any = 0;
       for (int32_t v = threadIdx.x; v < nn; v += kTailNT) {
         s_size[v] = s.size[v];
@@ -2426,6 +2462,7 @@ struct Bufs {
   int32_t *cstart;  // first component of every contraction chunk
   int32_t qcap;     // entries of cstart
   int32_t *M, *mark, *lrank;
+  uint8_t *merged;  // per node: formed by a merge in the last round
   int32_t nt;  // nodes the tail can start from
   double *tgain;    // per-slot gains in the tail
   int32_t *trow[2]; // per-slot rows in the tail
@@ -2491,6 +2528,7 @@ void carve(Arena &a, int32_t n, int32_t d, int32_t k, bool link, Bufs *b) {
   b->qcap = (int32_t)(2 * ed / 64 + 16);  // chunks are >= 64 slots
   b->cstart = a.take<int32_t>(b->qcap);
   b->M = a.take<int32_t>(n1);
+  b->merged = a.take<uint8_t>(n1);
   b->mark = a.take<int32_t>(n1);
   b->lrank = a.take<int32_t>(n1);
   b->nt = std::min<int32_t>(n, kTailNodes);
@@ -2597,6 +2635,8 @@ void launch_round(const Bufs &b, const Adj &adj, int cur, int32_t n,
               b.tmp, st);
   hipLaunchKernelGGL(k_place, xblocks_for(nn), dim3(256), 0, st, nn, b.L,
                      b.moff, b.rank, b.mem, ctl);
+  hipLaunchKernelGGL(k_merged, xblocks_for(nn), dim3(256), 0, st, b.moff,
+                     b.merged, ctl);
 
   // contraction chunks: enough blocks to fill the chip, at most kChunk
   int32_t chunk = kChunk;
@@ -2966,6 +3006,7 @@ int ladder_run(const LadderArgs &g, Ctl *ctl, Arena &a, hipStream_t st) {
     tail_nodes = (int32_t)std::max<long>(0, std::min<long>(v, kTailNodes));
   }
   if (g.link) tail_nodes = 0;  // the tail kernel does not link
+  bool relinked = false;
   for (int32_t l = 0; l < g.n_levels; ++l) {
     const double lambda = g.lambdas[l];
     const int64_t smin = g.min_size ? g.min_size[l] : 0;
@@ -2984,6 +3025,10 @@ int ladder_run(const LadderArgs &g, Ctl *ctl, Arena &a, hipStream_t st) {
       NodeIn s;
       s.emb = emb;
       s.perm = g.perm;
+      // merged flags hold from the second round of a level on, when no
+      // link has changed the graph since
+      s.merged = (first || round == 0 || relinked) ? nullptr : b.merged;
+      relinked = false;
       if (first) {
         s.size = nullptr;
         s.S = nullptr;
@@ -3034,6 +3079,7 @@ int ladder_run(const LadderArgs &g, Ctl *ctl, Arena &a, hipStream_t st) {
         if ((rc = link_round(g, b, adj, cur, nn, h->n_iso, ed, ctl, h, st)))
           return rc;
         slots = ed;
+        relinked = true;
       }
     }
 
