@@ -100,3 +100,9 @@ def test_link_paper_settings_driving_full():
     # D = 32, k = 8, lambda 0.02, s_min [5, 30, 90] on the 3M-point tile
     sc = scenes.load("driving-3m-paper")
     check_linked(sc.xyz, sc.emb, sc.k, sc.lambdas, sc.min_size)
+
+
+def test_link_large_k():
+    # k = 64 nearest nodes per isolated node: the largest per-thread lists
+    xyz, emb = clusters(120, 4, 21, size_lo=66, size_hi=80)
+    check_linked(xyz, emb, 64, [0.05, 0.5], [3, 200])

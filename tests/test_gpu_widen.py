@@ -133,7 +133,7 @@ def test_loss_random(d, rho):
     assert ref["n_inter"] > 0 and ref["n_intra"] > 0
 
 
-@pytest.mark.parametrize("k", [1, 3, 10, 16])
+@pytest.mark.parametrize("k", [1, 3, 10, 16, 64])
 def test_loss_messy_tables_and_ties(k):
     # words from a range of 16: the (word, slot) order decides most draws
     emb, nbr, cls, word = loss_case(3000, 12, k, 4, seed=100 + k,
