@@ -203,11 +203,14 @@ __global__ __launch_bounds__(256) void k_rev_count_kth(
   int32_t fwd = 0;
   if (i < n) {
     const int32_t *r = nbr + (int64_t)i * kp;
+    const int4 *r4 = reinterpret_cast<const int4 *>(r);  // rows of pad4(k)
     const float4 pi = pts[i];
     uint64_t mask = 0;
 #pragma unroll 4
     for (int32_t t = 0; t < k; ++t) {
-      const int32_t u = r[t];
+      const int4 c = r4[t >> 2];
+      const int32_t u = (t & 3) == 0 ? c.x : (t & 3) == 1 ? c.y
+                        : (t & 3) == 2 ? c.z : c.w;
       if (u < 0) continue;
       ++fwd;
       const float4 pu = pts[u];
