@@ -12,14 +12,18 @@
 // Query: one bucket per 16-lane DPP row (four buckets per wavefront), one
 // query point per lane.  Each lane keeps its own sorted top-k of 64-bit keys
 // (d2 bits, original index) in registers.  A group scans its own bucket and
-// the two next to it in Morton order first, then walks the tree depth first:
-// at each visited node the eight child boxes are loaded together and tested
-// against every lane's current k-th distance, and the children that some
-// lane needs are kept as bits of a per-level mask (the lowest set bit is the
-// next to enter).  Bucket points are broadcast within the row by DPP.  The
-// box distance is built from the same IEEE operations as d2 and rounding is
-// monotone, so it never exceeds the d2 of a point inside the box: no
-// neighbour, and no tie with a smaller index, can be skipped.
+// the two next to it in Morton order first, then walks the tree depth first.
+// When a node is entered, its eight children are tested at once, one child
+// per lane, against the box of the group's own points widened by the
+// group's largest current k-th distance; the children that pass are kept as
+// bits of a per-level mask (the lowest set bit is the next to take).  When a
+// child is taken, every lane tests its box against its own point and its
+// own current k-th distance, and the child is entered (or, for a bucket,
+// scanned) only if some lane needs it.  Bucket points are broadcast within
+// the row by DPP.  Both box distances are built from the same IEEE
+// operations as d2 and rounding is monotone, so neither exceeds the d2 of a
+// query and a point inside the box: no neighbour, and no tie with a smaller
+// index, can be skipped.
 #include "ezsp_internal.h"
 
 namespace ezsp {
@@ -284,43 +288,64 @@ __device__ __forceinline__ void scan_bucket(const float4 *__restrict__ pts,
   BucketStep<K, 0>::run(q, px, py, pz, me, cnt, key);
 }
 
-// Box test of the children first .. first+7 (level lc) of one node: bit c
-// is set when some lane of the group has the child's box within its current
-// k-th distance.  The boxes are loaded four at a time (all four before any
-// is used): fewer registers, more waves per SIMD to hide the latency.  The
+// Largest k-th d2 (as bits) over the active lanes of each 16-lane group,
+// in every lane of the group: a prefix max along the DPP row, then lane 15
+// broadcast.  An empty list (kNoKey) gives 0xffffffff, which admits every
+// box.
+__device__ __forceinline__ uint32_t group_max_kth(uint32_t v) {
+  v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x111, 0xF, 0xF,
+                                                   false));
+  v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x112, 0xF, 0xF,
+                                                   false));
+  v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x114, 0xF, 0xF,
+                                                   false));
+  v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x118, 0xF, 0xF,
+                                                   false));
+  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x15F, 0xF, 0xF,
+                                               false);
+}
+
+// Coarse test of the children first .. first+7 (level lc) of one node,
+// one child per lane (lane c and c + 8 of the group take child c): bit c is
+// set when the child's box is within the group's largest k-th distance of
+// the box of the group's own points (qlo, qhi).  Per axis the gap to the
+// query box is at most the gap to any query point in it (same IEEE
+// operations, rounding is monotone), so a child that some lane's own test
+// would admit is always admitted here.
+__device__ __forceinline__ uint32_t coarse_mask(
+    const float4 *__restrict__ blo, const float4 *__restrict__ bhi,
+    const Tree &tree, int lc, int32_t first, const float4 &qlo,
+    const float4 &qhi, uint32_t gkth, int lane16, int gshift) {
+  const int32_t nchild = min(kFan, tree.cnt[lc] - first);
+  const int c = lane16 & (kFan - 1);
+  const int32_t j = tree.off[lc] + first + min(c, nchild - 1);
+  const float4 lo = blo[j], hi = bhi[j];
+  const float ex = fmaxf(fmaxf(lo.x - qhi.x, qlo.x - hi.x), 0.f);
+  const float ey = fmaxf(fmaxf(lo.y - qhi.y, qlo.y - hi.y), 0.f);
+  const float ez = fmaxf(fmaxf(lo.z - qhi.z, qlo.z - hi.z), 0.f);
+  const float bx = ex * ex, by = ey * ey, bz = ez * ez;
+  const float d2b = (bx + by) + bz;
+  const bool need = c < nchild && __float_as_uint(d2b) <= gkth;
+  return (uint32_t)(__ballot(need) >> gshift) & 0xffu;
+}
+
+// Exact test of one node's box against every lane's point and current k-th
+// distance: true when some active lane of the group needs the node.  The
 // box distance uses the same IEEE operations as d2, so it never exceeds the
 // d2 of a point inside the box.
-template <int K>
-__device__ __forceinline__ uint32_t child_mask(
-    const float4 *__restrict__ blo, const float4 *__restrict__ bhi,
-    const Tree &tree, int lc, int32_t first, int32_t cnt_lc, const float4 &p,
-    bool act, const uint64_t (&key)[K], int gshift) {
-  const int32_t nchild = min(kFan, cnt_lc - first);
-  const int32_t off = tree.off[lc] + first;
-  const uint32_t kth = (uint32_t)(key[K - 1] >> 32);
-  uint32_t m = 0;
-#pragma unroll
-  for (int h = 0; h < kFan; h += kFan / 2) {
-    float4 lo[kFan / 2], hi[kFan / 2];
-#pragma unroll
-    for (int c = 0; c < kFan / 2; ++c) {
-      const int32_t j = off + min(h + c, nchild - 1);
-      lo[c] = blo[j];
-      hi[c] = bhi[j];
-    }
-#pragma unroll
-    for (int c = 0; c < kFan / 2; ++c) {
-      const float ex = fmaxf(fmaxf(lo[c].x - p.x, p.x - hi[c].x), 0.f);
-      const float ey = fmaxf(fmaxf(lo[c].y - p.y, p.y - hi[c].y), 0.f);
-      const float ez = fmaxf(fmaxf(lo[c].z - p.z, p.z - hi[c].z), 0.f);
-      const float bx = ex * ex, by = ey * ey, bz = ez * ez;
-      const float d2b = (bx + by) + bz;
-      // d2b <= k-th d2 (an empty list, kNoKey, admits everything)
-      const bool need = act && h + c < nchild && __float_as_uint(d2b) <= kth;
-      if ((__ballot(need) >> gshift) & 0xffffull) m |= 1u << (h + c);
-    }
-  }
-  return m;
+__device__ __forceinline__ bool lane_needs(const float4 *__restrict__ blo,
+                                           const float4 *__restrict__ bhi,
+                                           int32_t j, const float4 &p,
+                                           bool act, uint32_t kth,
+                                           int gshift) {
+  const float4 lo = blo[j], hi = bhi[j];
+  const float ex = fmaxf(fmaxf(lo.x - p.x, p.x - hi.x), 0.f);
+  const float ey = fmaxf(fmaxf(lo.y - p.y, p.y - hi.y), 0.f);
+  const float ez = fmaxf(fmaxf(lo.z - p.z, p.z - hi.z), 0.f);
+  const float bx = ex * ex, by = ey * ey, bz = ez * ez;
+  const float d2b = (bx + by) + bz;
+  const bool need = act && __float_as_uint(d2b) <= kth;
+  return ((__ballot(need) >> gshift) & 0xffffull) != 0;
 }
 
 __device__ __forceinline__ void set_level_bits(uint64_t &mlo, uint64_t &mhi,
@@ -368,14 +393,19 @@ __global__ __launch_bounds__(256) void k_knn_query(
   // current path as bits: bit 8*l + c = child c (level l) of the path node
   // at level l+1.  The lowest set bit is the deepest pending node, and the
   // path node at level l+1 is cur >> 3*(l+1-curl) (cur: last node taken, at
-  // level curl), since children of x are 8x..8x+7.
+  // level curl), since children of x are 8x..8x+7.  Children are marked by
+  // the group's coarse test when their parent is entered; a node is entered
+  // only when, as it is taken, some lane's own test against its current
+  // k-th distance still needs it.
+  const float4 qlo = blo[grp], qhi = bhi[grp];  // own bucket (level 0)
   uint64_t mlo = 0, mhi = 0;
   int32_t cur = 0;
   int curl = tree.top;
   if (tree.top > 0) {
-    const uint32_t m8 = child_mask<K>(blo, bhi, tree, tree.top - 1, 0,
-                                      tree.cnt[tree.top - 1], p, act, key,
-                                      gshift);
+    const uint32_t gk =
+        group_max_kth(act ? (uint32_t)(key[K - 1] >> 32) : 0u);
+    const uint32_t m8 = coarse_mask(blo, bhi, tree, tree.top - 1, 0, qlo, qhi,
+                                    gk, lane16, gshift);
     set_level_bits(mlo, mhi, tree.top - 1, m8);
   }
   for (;;) {
@@ -393,16 +423,17 @@ __global__ __launch_bounds__(256) void k_knn_query(
       const int32_t node = ((cur >> (3 * (l + 1 - curl))) << 3) | c;
       cur = node;
       curl = l;
-      if (l == 0) {
-        if (node < grp - 1 || node > grp + 1) {
-          leaf = node;
-          break;
-        }
+      if (l == 0 && node >= grp - 1 && node <= grp + 1) continue;
+      const uint32_t kth = (uint32_t)(key[K - 1] >> 32);
+      if (!lane_needs(blo, bhi, tree.off[l] + node, p, act, kth, gshift))
         continue;
+      if (l == 0) {
+        leaf = node;
+        break;
       }
-      const int32_t first = node * kFan;
-      const uint32_t m8 = child_mask<K>(blo, bhi, tree, l - 1, first,
-                                        tree.cnt[l - 1], p, act, key, gshift);
+      const uint32_t gk = group_max_kth(act ? kth : 0u);
+      const uint32_t m8 = coarse_mask(blo, bhi, tree, l - 1, node * kFan, qlo,
+                                      qhi, gk, lane16, gshift);
       set_level_bits(mlo, mhi, l - 1, m8);
     }
     if (__ballot(leaf >= 0) == 0) break;
