@@ -93,7 +93,7 @@ size_t ezsp_knn_workspace_size(int64_t n, int32_t k);
  *        the smaller index.  When n-1 < k the row ends in -1 entries.
  *   d2   n*k fp32 (out, nullable): the matching squared distances, +inf
  *        where nbr is -1.
- * Errors: INVALID_ARG (n < 1, n >= 2^31, k outside 1..64, NULL pointer),
+ * Errors: INVALID_ARG (n < 1, n > 2^31 - 256, k outside 1..64, NULL pointer),
  *         NONFINITE, WORKSPACE, DEVICE. */
 int ezsp_knn(const float *xyz, int64_t n, int32_t k, int32_t *nbr, float *d2,
              void *ws, size_t ws_bytes, void *stream);

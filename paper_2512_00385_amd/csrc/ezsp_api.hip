@@ -36,7 +36,9 @@ int fail(int code, const char *msg) {
   return code;
 }
 
-bool n_ok(int64_t n) { return n >= 1 && n < kMaxN; }
+// Point counts leave room for grids of 256-thread blocks and whole buckets
+// of padding in int32 arithmetic.
+bool n_ok(int64_t n) { return n >= 1 && n <= kMaxN - 256; }
 
 // Graph tables are indexed with int32: 2*k*n directed entries, and windows
 // of up to twice that, must fit.
@@ -46,7 +48,7 @@ bool edges_ok(int64_t n, int32_t k) {
 
 int check_params(int64_t n, int32_t d, const ezsp_params *p) {
   if (!p) return fail(EZSP_ERR_INVALID_ARG, "params is NULL");
-  if (!n_ok(n)) return fail(EZSP_ERR_INVALID_ARG, "n must be in [1, 2^31)");
+  if (!n_ok(n)) return fail(EZSP_ERR_INVALID_ARG, "n must be in [1, 2^31 - 256]");
   if (d < 1 || d > 64) return fail(EZSP_ERR_INVALID_ARG, "d must be in 1..64");
   if (p->k < 1 || p->k > 64)
     return fail(EZSP_ERR_INVALID_ARG, "k must be in 1..64");
@@ -171,7 +173,7 @@ int ezsp_knn(const float *xyz, int64_t n, int32_t k, int32_t *nbr, float *d2,
   set_error("%s", "");
   if (!xyz || !nbr || !ws)
     return fail(EZSP_ERR_INVALID_ARG, "xyz, nbr and ws must not be NULL");
-  if (!n_ok(n)) return fail(EZSP_ERR_INVALID_ARG, "n must be in [1, 2^31)");
+  if (!n_ok(n)) return fail(EZSP_ERR_INVALID_ARG, "n must be in [1, 2^31 - 256]");
   if (k < 1 || k > 64) return fail(EZSP_ERR_INVALID_ARG, "k must be in 1..64");
   if ((int64_t)n * k >= kMaxN)
     return fail(EZSP_ERR_INVALID_ARG, "n*k must stay below 2^31");
@@ -252,7 +254,7 @@ int ezsp_component_stats(const int32_t *labels, int64_t n, int64_t n_comp,
                 "labels, emb, size, emb_mean and ws must not be NULL");
   if (xyz && !centroid)
     return fail(EZSP_ERR_INVALID_ARG, "centroid must be given with xyz");
-  if (!n_ok(n)) return fail(EZSP_ERR_INVALID_ARG, "n must be in [1, 2^31)");
+  if (!n_ok(n)) return fail(EZSP_ERR_INVALID_ARG, "n must be in [1, 2^31 - 256]");
   if (d < 1 || d > 64) return fail(EZSP_ERR_INVALID_ARG, "d must be in 1..64");
   if (n_comp < 1 || n_comp >= kMaxN || n_comp * d >= kMaxN || n * d >= kMaxN)
     return fail(EZSP_ERR_INVALID_ARG, "n_comp out of range");
@@ -281,7 +283,7 @@ int ezsp_grid_subsample(const float *xyz, int64_t n, float h, int32_t *keep,
   if (!xyz || !keep || !n_keep || !ws)
     return fail(EZSP_ERR_INVALID_ARG,
                 "xyz, keep, n_keep and ws must not be NULL");
-  if (!n_ok(n)) return fail(EZSP_ERR_INVALID_ARG, "n must be in [1, 2^31)");
+  if (!n_ok(n)) return fail(EZSP_ERR_INVALID_ARG, "n must be in [1, 2^31 - 256]");
   if (!(h > 0.0f) || !isfinite(h))
     return fail(EZSP_ERR_INVALID_ARG, "h must be finite and > 0");
   if (ws_bytes < ezsp_grid_subsample_workspace_size(n))
@@ -310,7 +312,7 @@ int ezsp_edge_loss(const float *emb, int64_t n, int32_t d, const int32_t *nbr,
   if (!emb || !nbr || !cls || !word || !out || !ws)
     return fail(EZSP_ERR_INVALID_ARG,
                 "emb, nbr, cls, word, out and ws must not be NULL");
-  if (!n_ok(n)) return fail(EZSP_ERR_INVALID_ARG, "n must be in [1, 2^31)");
+  if (!n_ok(n)) return fail(EZSP_ERR_INVALID_ARG, "n must be in [1, 2^31 - 256]");
   if (d < 1 || d > 1024)
     return fail(EZSP_ERR_INVALID_ARG, "d must be in 1..1024");
   if (k < 1 || k > 64 || n * (int64_t)k >= kMaxN)
@@ -369,7 +371,7 @@ int ezsp_purity(const int32_t *labels, int64_t n, int64_t n_comp,
   if (!labels || !cls || !out || !ws)
     return fail(EZSP_ERR_INVALID_ARG,
                 "labels, cls, out and ws must not be NULL");
-  if (!n_ok(n)) return fail(EZSP_ERR_INVALID_ARG, "n must be in [1, 2^31)");
+  if (!n_ok(n)) return fail(EZSP_ERR_INVALID_ARG, "n must be in [1, 2^31 - 256]");
   if (n_comp < 1 || n_comp >= kMaxN || n_cls < 1 ||
       n_comp > ((int64_t)1 << 62) / n_cls)
     return fail(EZSP_ERR_INVALID_ARG, "n_comp or n_cls out of range");
@@ -396,7 +398,7 @@ int ezsp_embed_mlp(const uint16_t *x, int64_t n, int32_t d_in, int32_t d_hid,
   set_error("%s", "");
   if (!x || !w1 || !b1 || !w2 || !b2 || !w3 || !b3 || !out)
     return fail(EZSP_ERR_INVALID_ARG, "no pointer may be NULL");
-  if (!n_ok(n)) return fail(EZSP_ERR_INVALID_ARG, "n must be in [1, 2^31)");
+  if (!n_ok(n)) return fail(EZSP_ERR_INVALID_ARG, "n must be in [1, 2^31 - 256]");
   if (d_in < 1 || d_in > 8 || d_hid != 32 || d_out < 1 || d_out > 32)
     return fail(EZSP_ERR_INVALID_ARG,
                 "the MLP is d_in (1..8) -> 32 -> 32 -> d_out (1..32)");

@@ -68,6 +68,11 @@ struct Arena {
 // boxes of level l, up to a single root at level `top`.  A bucket is also
 // the query group of the kNN kernel: 16 lanes, one DPP row.
 constexpr int kBucket = 16;
+// n rounded up to whole buckets, and the index carried by padding points.
+__host__ __device__ __forceinline__ int32_t pad_bucket(int32_t n) {
+  return (n + kBucket - 1) / kBucket * kBucket;
+}
+constexpr int32_t kPadIndex = 0x7fffffff;
 constexpr int kFan = 8;
 constexpr int kMaxTreeLevels = 16;
 struct Tree {

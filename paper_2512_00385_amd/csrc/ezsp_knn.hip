@@ -147,12 +147,20 @@ __global__ __launch_bounds__(256) void k_morton(const float *xyz, int32_t n,
   vals[i] = (uint32_t)i;
 }
 
-// Sorted points as float4 (x, y, z, original index bits) plus both maps.
+// Sorted points as float4 (x, y, z, original index bits) plus both maps;
+// the array runs to a whole number of buckets (see k_gather_points).
 __global__ __launch_bounds__(256) void k_gather_points(
     const float *xyz, int32_t n, const uint32_t *order, float4 *pts,
     int32_t *perm, int32_t *inv, Ctl *ctl) {
   const int32_t i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= n) return;
+  if (i >= n) {
+    // the last bucket's missing points: infinitely far, with an index above
+    // every real one, so a bucket scan needs no bounds check
+    if (i < pad_bucket(n))
+      pts[i] = make_float4(INFINITY, INFINITY, INFINITY,
+                           __int_as_float(kPadIndex));
+    return;
+  }
   const uint32_t o = order[i];
   if (o >= (uint32_t)n) {
     raise_err(ctl, kErrInternal);
@@ -238,54 +246,55 @@ __device__ __forceinline__ float row_bcast(float v) {
 }
 template <int J>
 __device__ __forceinline__ int32_t row_bcast_i(int32_t v) {
-  return __builtin_amdgcn_update_dpp(0, v, 0x150 + J, 0xF, 0xF, false);
+  return __builtin_amdgcn_update_dpp(0, v, 0x150 + J, 0xF, 0xF, true);
 }
 
 // Key of candidate J of the bucket held one point per lane in q: d2 in the
-// fixed order ((dx*dx) + (dy*dy)) + (dz*dz), dx = x_q - x_p; the query
-// itself and lanes past the bucket's end give kNoKey.
-template <int J>
+// fixed order ((dx*dx) + (dy*dy)) + (dz*dz), dx = x_q - x_p.  Only the
+// query's own bucket can hold the query itself (SELF), which gives kNoKey.
+// Padding points past the end give an infinite d2 and an index above every
+// real one, so they never displace a real point.
+template <int J, bool SELF>
 __device__ __forceinline__ uint64_t bucket_key(const float4 &q, float px,
-                                               float py, float pz, int32_t me,
-                                               int32_t cnt) {
+                                               float py, float pz,
+                                               int32_t me) {
   const float dx = row_bcast<J>(q.x) - px;
   const float dy = row_bcast<J>(q.y) - py;
   const float dz = row_bcast<J>(q.z) - pz;
   const int32_t qo = row_bcast_i<J>(__float_as_int(q.w));
   const float xx = dx * dx, yy = dy * dy, zz = dz * dz;
   const float d2 = (xx + yy) + zz;
-  return (J < cnt && qo != me) ? cand_key(d2, qo) : kNoKey;
+  if (SELF) return qo != me ? cand_key(d2, qo) : kNoKey;
+  return cand_key(d2, qo);
 }
 
-template <int K, int J>
+template <int K, int J, bool SELF>
 struct BucketStep {
   __device__ __forceinline__ static void run(const float4 &q, float px,
                                              float py, float pz, int32_t me,
-                                             int32_t cnt, uint64_t (&key)[K]) {
-    const uint64_t nk = bucket_key<J>(q, px, py, pz, me, cnt);
+                                             uint64_t (&key)[K]) {
+    const uint64_t nk = bucket_key<J, SELF>(q, px, py, pz, me);
     if (nk < key[K - 1]) topk_insert<K>(key, nk);
-    BucketStep<K, J + 1>::run(q, px, py, pz, me, cnt, key);
+    BucketStep<K, J + 1, SELF>::run(q, px, py, pz, me, key);
   }
 };
-template <int K>
-struct BucketStep<K, kBucket> {
+template <int K, bool SELF>
+struct BucketStep<K, kBucket, SELF> {
   __device__ __forceinline__ static void run(const float4 &, float, float,
-                                             float, int32_t, int32_t,
+                                             float, int32_t,
                                              uint64_t (&)[K]) {}
 };
 
-// All 16 lanes of a group scan bucket b together (group-uniform call).
-// Lanes of an inactive query (me = -1) carry keys too, they are not written.
-template <int K>
+// All 16 lanes of a group scan bucket b together (group-uniform call); the
+// points array is padded to whole buckets.  Lanes of an inactive query
+// (me = -1) carry keys too, they are not written.
+template <int K, bool SELF>
 __device__ __forceinline__ void scan_bucket(const float4 *__restrict__ pts,
-                                            int32_t n, int32_t b, int lane16,
-                                            float px, float py, float pz,
-                                            int32_t me, uint64_t (&key)[K]) {
-  const int32_t base = b * kBucket;
-  const int32_t cnt = min(kBucket, n - base);
-  float4 q = make_float4(0.f, 0.f, 0.f, 0.f);
-  if (lane16 < cnt) q = pts[base + lane16];
-  BucketStep<K, 0>::run(q, px, py, pz, me, cnt, key);
+                                            int32_t b, int lane16, float px,
+                                            float py, float pz, int32_t me,
+                                            uint64_t (&key)[K]) {
+  const float4 q = pts[b * kBucket + lane16];
+  BucketStep<K, 0, SELF>::run(q, px, py, pz, me, key);
 }
 
 // Largest k-th d2 (as bits) over the active lanes of each 16-lane group,
@@ -314,11 +323,12 @@ __device__ __forceinline__ uint32_t group_max_kth(uint32_t v) {
 // would admit is always admitted here.
 __device__ __forceinline__ uint32_t coarse_mask(
     const float4 *__restrict__ blo, const float4 *__restrict__ bhi,
-    const Tree &tree, int lc, int32_t first, const float4 &qlo,
+    const int32_t *lv_off, const int32_t *lv_cnt, int lc, int32_t first,
+    const float4 &qlo,
     const float4 &qhi, uint32_t gkth, int lane16, int gshift) {
-  const int32_t nchild = min(kFan, tree.cnt[lc] - first);
+  const int32_t nchild = min(kFan, lv_cnt[lc] - first);
   const int c = lane16 & (kFan - 1);
-  const int32_t j = tree.off[lc] + first + min(c, nchild - 1);
+  const int32_t j = lv_off[lc] + first + min(c, nchild - 1);
   const float4 lo = blo[j], hi = bhi[j];
   const float ex = fmaxf(fmaxf(lo.x - qhi.x, qlo.x - hi.x), 0.f);
   const float ey = fmaxf(fmaxf(lo.y - qhi.y, qlo.y - hi.y), 0.f);
@@ -370,6 +380,13 @@ __global__ __launch_bounds__(256) void k_knn_query(
     uint64_t *__restrict__ kth_out, int32_t n_blocks) {
   const int32_t lb = xcd_block();
   if (lb >= n_blocks) return;
+  // level offsets and counts of the box tree, indexed per lane in the walk
+  __shared__ int32_t lv_off[kMaxTreeLevels], lv_cnt[kMaxTreeLevels];
+  if (threadIdx.x < kMaxTreeLevels) {
+    lv_off[threadIdx.x] = tree.off[threadIdx.x];
+    lv_cnt[threadIdx.x] = tree.cnt[threadIdx.x];
+  }
+  __syncthreads();
   const int lane16 = threadIdx.x & (kBucket - 1);
   const int gshift = threadIdx.x & (kWave - kBucket);  // 0, 16, 32, 48
   const int32_t nb0 = tree.cnt[0];
@@ -383,11 +400,11 @@ __global__ __launch_bounds__(256) void k_knn_query(
 #pragma unroll
   for (int t = 0; t < K; ++t) key[t] = kNoKey;
   // own bucket and its Morton neighbours first: a tight k-th distance early
-  scan_bucket<K>(pts, n, grp, lane16, p.x, p.y, p.z, me, key);
+  scan_bucket<K, true>(pts, grp, lane16, p.x, p.y, p.z, me, key);
   if (grp > 0)
-    scan_bucket<K>(pts, n, grp - 1, lane16, p.x, p.y, p.z, me, key);
+    scan_bucket<K, false>(pts, grp - 1, lane16, p.x, p.y, p.z, me, key);
   if (grp + 1 < nb0)
-    scan_bucket<K>(pts, n, grp + 1, lane16, p.x, p.y, p.z, me, key);
+    scan_bucket<K, false>(pts, grp + 1, lane16, p.x, p.y, p.z, me, key);
 
   // Depth-first walk with the pending children of every level of the
   // current path as bits: bit 8*l + c = child c (level l) of the path node
@@ -404,8 +421,8 @@ __global__ __launch_bounds__(256) void k_knn_query(
   if (tree.top > 0) {
     const uint32_t gk =
         group_max_kth(act ? (uint32_t)(key[K - 1] >> 32) : 0u);
-    const uint32_t m8 = coarse_mask(blo, bhi, tree, tree.top - 1, 0, qlo, qhi,
-                                    gk, lane16, gshift);
+    const uint32_t m8 = coarse_mask(blo, bhi, lv_off, lv_cnt, tree.top - 1, 0,
+                                    qlo, qhi, gk, lane16, gshift);
     set_level_bits(mlo, mhi, tree.top - 1, m8);
   }
   for (;;) {
@@ -425,33 +442,35 @@ __global__ __launch_bounds__(256) void k_knn_query(
       curl = l;
       if (l == 0 && node >= grp - 1 && node <= grp + 1) continue;
       const uint32_t kth = (uint32_t)(key[K - 1] >> 32);
-      if (!lane_needs(blo, bhi, tree.off[l] + node, p, act, kth, gshift))
+      if (!lane_needs(blo, bhi, lv_off[l] + node, p, act, kth, gshift))
         continue;
       if (l == 0) {
         leaf = node;
         break;
       }
       const uint32_t gk = group_max_kth(act ? kth : 0u);
-      const uint32_t m8 = coarse_mask(blo, bhi, tree, l - 1, node * kFan, qlo,
-                                      qhi, gk, lane16, gshift);
+      const uint32_t m8 = coarse_mask(blo, bhi, lv_off, lv_cnt, l - 1,
+                                      node * kFan, qlo, qhi, gk, lane16,
+                                      gshift);
       set_level_bits(mlo, mhi, l - 1, m8);
     }
     if (__ballot(leaf >= 0) == 0) break;
     if (leaf >= 0)
-      scan_bucket<K>(pts, n, leaf, lane16, p.x, p.y, p.z, me, key);
+      scan_bucket<K, false>(pts, leaf, lane16, p.x, p.y, p.z, me, key);
   }
 
   if (!act) return;
   const int32_t kp = pad4(k);
   // the k-th key (kNoKey when fewer than k points exist): later, q is among
-  // p's neighbours exactly when q's key as seen from p does not exceed it
+  // p's neighbours exactly when q's key as seen from p does not exceed it.
+  // Empty slots and padding points carry an index >= n.
 #pragma unroll
   for (int t = 0; t < K; ++t)
-    if (t == k - 1) kth_out[i] = key[t];
+    if (t == k - 1) kth_out[i] = (uint32_t)key[t] < (uint32_t)n ? key[t] : kNoKey;
 #pragma unroll
   for (int t = 0; t < K; ++t) {
     if (t < k) {
-      const bool has = key[t] != kNoKey;
+      const bool has = (uint32_t)key[t] < (uint32_t)n;
       const int32_t o = (int32_t)(uint32_t)key[t];
       nbr_int[(int64_t)i * kp + t] = has ? inv[o] : -1;
       if (nbr_out) nbr_out[(int64_t)me * k + t] = has ? o : -1;
@@ -482,7 +501,7 @@ void knn_reserve(Arena &a, int32_t n, int32_t k, KnnWork *w) {
   w->keys2 = a.take<uint64_t>(n);
   w->vals = a.take<uint32_t>(n);
   w->vals2 = a.take<uint32_t>(n);
-  w->pts = a.take<float4>(n);
+  w->pts = a.take<float4>(pad_bucket(n));
   w->kth = a.take<uint64_t>(n);
   w->blo = a.take<float4>(t.total);
   w->bhi = a.take<float4>(t.total);
