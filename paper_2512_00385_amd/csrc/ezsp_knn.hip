@@ -400,11 +400,8 @@ __global__ __launch_bounds__(256) void k_knn_query(
 #pragma unroll
   for (int t = 0; t < K; ++t) key[t] = kNoKey;
   // own bucket and its Morton neighbours first: a tight k-th distance early
+  // (the two Morton neighbours are the first buckets of the scan loop below)
   scan_bucket<K, true>(pts, grp, lane16, p.x, p.y, p.z, me, key);
-  if (grp > 0)
-    scan_bucket<K, false>(pts, grp - 1, lane16, p.x, p.y, p.z, me, key);
-  if (grp + 1 < nb0)
-    scan_bucket<K, false>(pts, grp + 1, lane16, p.x, p.y, p.z, me, key);
 
   // Depth-first walk with the pending children of every level of the
   // current path as bits: bit 8*l + c = child c (level l) of the path node
@@ -425,14 +422,22 @@ __global__ __launch_bounds__(256) void k_knn_query(
                                     qlo, qhi, gk, lane16, gshift);
     set_level_bits(mlo, mhi, tree.top - 1, m8);
   }
+  int pre = 0;  // Morton neighbours taken: grp - 1, then grp + 1
   for (;;) {
     int32_t leaf = -1;
-    while ((mlo | mhi) != 0) {
+    while (pre < 2 && leaf < 0) {
+      const int32_t b = pre == 0 ? grp - 1 : grp + 1;
+      ++pre;
+      if (b >= 0 && b < nb0) leaf = b;
+    }
+    while (leaf < 0) {
       int t;
-      if (mlo) {
+      if (mlo != 0) {
         t = __builtin_ctzll(mlo);
         mlo &= mlo - 1;
       } else {
+        // levels 8 and up (trees over more than 8^8 buckets only)
+        if (mhi == 0) break;
         t = 64 + __builtin_ctzll(mhi);
         mhi &= mhi - 1;
       }
