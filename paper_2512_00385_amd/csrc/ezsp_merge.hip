@@ -1641,10 +1641,12 @@ __global__ void k_energy_reset(Ctl *ctl) {
 // steps instead of kernel launches and host round trips.  The arithmetic is
 // the same as above; the work is spread over table slots (entries) rather
 // than rows, and the per-node arrays live in LDS:
-//   select    three passes over the slots: gain of every entry, then per
-//             row the largest gain (max of an order-preserving key), the
-//             smallest minpt among the entries with that gain, and the
-//             entry that has both (Steps 1-2, same choice as best_before)
+//   select    two passes over the slots: the gain of every entry (after a
+//             level's first round only entries with an end that merged in
+//             the last round) and per row the largest candidate gain (max
+//             of an order-preserving key), then among the entries with that
+//             gain the neighbour with the smallest minpt, by a 64-bit min of
+//             (minpt, neighbour) (Steps 1-2, same choice as best_before)
 //   union     hook and pointer jumping on LDS arrays (Step 3)
 //   relabel   roots numbered by a block scan
 //   stats     node-parallel adds into the next node state (int64 sums,
@@ -1658,7 +1660,7 @@ __global__ void k_energy_reset(Ctl *ctl) {
 // weight.
 // ---------------------------------------------------------------------------
 constexpr int kTailNT = 1024;
-constexpr int kTailNodes = 4096;    // largest graph the tail can take (LDS)
+constexpr int kTailNodes = 2048;    // largest graph the tail can take (LDS)
 constexpr int kTailStart = 1500;    // default switch to the tail
 constexpr int kTailEdges = 1 << 16; // ... directed entries at the switch
 constexpr int kTailSlots = 1 << 18; // ... table slots at the switch
@@ -1666,6 +1668,10 @@ constexpr int kTailLevels = 16;
 static_assert(sizeof(((Ctl *)nullptr)->tail_nc) == kTailLevels * 4,
               "tail level counts travel in the control block");
 constexpr int kTailJumps = 64;
+// Slots per thread whose loads are issued together in the tail's slot loops:
+// the block is alone on one CU, so memory latency, not bandwidth, sets the
+// pace of a loop that waits on every slot's loads in turn.
+constexpr int kTU = 4;
 
 struct TailState {
   int32_t *ws[2], *wl[2];
@@ -1815,6 +1821,8 @@ __global__ __launch_bounds__(kTailNT) void k_tail(TailState t, Ctl *ctl) {
   __shared__ int32_t s_sel[kTailNodes];
   __shared__ int32_t s_wsa[kTailNodes + 1], s_wsb[kTailNodes + 1];
   __shared__ unsigned long long s_key[kTailNodes + 1];
+  __shared__ unsigned long long s_pick[kTailNodes];
+  __shared__ int32_t s_mrg[kTailNodes];
   __shared__ int32_t wsum[kTailNT / kWave];
   __shared__ int32_t s_any, s_flag, s_claims;
   __shared__ long long s_cut;
@@ -1850,6 +1858,12 @@ __global__ __launch_bounds__(kTailNT) void k_tail(TailState t, Ctl *ctl) {
     const long long smin = t.smin[l];
     for (int32_t round = (l == t.level0 ? t.round0 : 0);; ++round) {
       if (ed == 0) break;  // no edge left: nothing can merge
+      // Every gain is evaluated in a level's first round and in the tail's
+      // first round.  Later, an entry whose two ends were both left alone by
+      // the last round keeps last round's gain, sizes and weight, which made
+      // no candidate (a node with a candidate merges): only entries with a
+      // merged end (s_mrg) are evaluated.
+      const bool fresh = round == 0 || (l == t.level0 && round == t.round0);
       if (round >= t.max_rounds) {
         if (threadIdx.x == 0) {
           ctl->tail_level = l;
@@ -1874,50 +1888,71 @@ __global__ __launch_bounds__(kTailNT) void k_tail(TailState t, Ctl *ctl) {
         s_minpt[v] = s.minpt[v];
         s_deg[v] = 0;
         s_key[v] = 0ull;
-        s_sel[v] = INT32_MAX;
-        s_L[v] = -1;
+        s_pick[v] = ~0ull;
       }
       __syncthreads();
-      // Steps 1-2, pass 1: gains, degrees, largest candidate gain per row
-      for (int32_t q = threadIdx.x; q < Q; q += kTailNT) {
-        const uint64_t e = tb[q];
-        if (e == kEmpty) continue;
-        const int32_t v = rows[q];
-        const int32_t u = (int32_t)(e >> 32), w = (int32_t)(uint32_t)e;
-        if ((uint32_t)u >= (uint32_t)nn) {
-          raise_err(ctl, kErrInternal);
-          continue;
+      // Steps 1-2, pass 1: gains, degrees, largest candidate gain per row.
+      // The next slot's entry and row are loaded before this one is used
+      // (the index is clamped, so the loads need no branch).
+      {
+        int32_t q = threadIdx.x;
+        const int32_t q0 = min(q, Q - 1);
+        uint64_t e_n = tb[q0];
+        int32_t v_n = rows[q0];
+        for (; q < Q; q += kTailNT) {
+          const uint64_t e = e_n;
+          const int32_t v = v_n;
+          const int32_t qn = min(q + kTailNT, Q - 1);
+          e_n = tb[qn];
+          v_n = rows[qn];
+          if (e == kEmpty) continue;
+          const int32_t u = (int32_t)(e >> 32), w = (int32_t)(uint32_t)e;
+          if ((uint32_t)u >= (uint32_t)nn || (uint32_t)v >= (uint32_t)nn) {
+            raise_err(ctl, kErrInternal);
+            continue;
+          }
+          atomicAdd(&s_deg[v], 1);
+          if (!fresh && !s_mrg[v] && !s_mrg[u]) continue;
+          const double g = tail_gain<DT>(s.mu, v, u, d, (double)s_size[v],
+                                         (double)s_size[u], w, lambda);
+          t.gain[q] = g;
+          if (g > 0.0 || (long long)s_size[v] < smin)
+            atomicMax(&s_key[v], gain_key(g));
         }
-        atomicAdd(&s_deg[v], 1);
-        const double g = tail_gain<DT>(s.mu, v, u, d, (double)s_size[v],
-                                       (double)s_size[u], w, lambda);
-        t.gain[q] = g;
-        if (g > 0.0 || (long long)s_size[v] < smin)
-          atomicMax(&s_key[v], gain_key(g));
       }
       __syncthreads();
-      // pass 2: smallest minpt among the entries with the row's best gain
-      for (int32_t q = threadIdx.x; q < Q; q += kTailNT) {
-        const uint64_t e = tb[q];
-        if (e == kEmpty) continue;
-        const int32_t v = rows[q];
-        const unsigned long long kv = s_key[v];
-        if (kv != 0ull && gain_key(t.gain[q]) == kv)
-          atomicMin(&s_sel[v], s_minpt[(int32_t)(e >> 32)]);
-      }
-      __syncthreads();
-      // pass 3: the chosen neighbour (minpt is unique per node)
-      for (int32_t q = threadIdx.x; q < Q; q += kTailNT) {
-        const uint64_t e = tb[q];
-        if (e == kEmpty) continue;
-        const int32_t v = rows[q];
-        const int32_t u = (int32_t)(e >> 32);
-        const unsigned long long kv = s_key[v];
-        if (kv != 0ull && s_minpt[u] == s_sel[v] &&
-            gain_key(t.gain[q]) == kv) {
-          s_L[v] = u;  // target
-          s_any = 1;
+      // pass 2: among the evaluated entries with the row's best gain, the
+      // neighbour with the smallest minpt (minpt is unique per node, so the
+      // 64-bit minimum of (minpt, neighbour) names it)
+      for (int32_t q0 = threadIdx.x; q0 < Q; q0 += kTU * kTailNT) {
+        uint64_t ev[kTU];
+        int32_t rv[kTU];
+        double gv[kTU];
+#pragma unroll
+        for (int j = 0; j < kTU; ++j) {
+          const int32_t q = min(q0 + j * kTailNT, Q - 1);  // no branch
+          ev[j] = tb[q];
+          rv[j] = rows[q];
+          gv[j] = t.gain[q];  // used only where evaluated
         }
+#pragma unroll
+        for (int j = 0; j < kTU; ++j) {
+          const uint64_t e = ev[j];
+          if (q0 + j * kTailNT >= Q || e == kEmpty) continue;
+          const int32_t v = rv[j];
+          const int32_t u = (int32_t)(e >> 32);
+          const unsigned long long kv = s_key[v];
+          if (kv != 0ull && (fresh || s_mrg[v] || s_mrg[u]) &&
+              gain_key(gv[j]) == kv)
+            atomicMin(&s_pick[v], ((unsigned long long)(uint32_t)s_minpt[u]
+                                   << 32) | (uint32_t)u);
+        }
+      }
+      __syncthreads();
+      for (int32_t v = threadIdx.x; v < nn; v += kTailNT) {
+        const unsigned long long pk = s_pick[v];
+        s_L[v] = pk == ~0ull ? -1 : (int32_t)(uint32_t)pk;  // target
+        if (pk != ~0ull) s_any = 1;
       }
       __syncthreads();
       if (!s_any) break;  // Step 1: no candidate merge
@@ -1947,7 +1982,10 @@ __global__ __launch_bounds__(kTailNT) void k_tail(TailState t, Ctl *ctl) {
           return;
         }
       }
-      // relabel: roots numbered in node order; L = new id of the root
+      // relabel: roots numbered in node order; L = new id of the root.
+      // s_mrg is rebuilt for the next nodes: set when a component has a
+      // member other than its root.
+      for (int32_t v = threadIdx.x; v < nn; v += kTailNT) s_mrg[v] = 0;
       const int32_t C = tail_scan(
           nn, [&](int32_t v) { return s_sel[v] == v ? 1 : 0; }, s_newid,
           wsum);
@@ -1957,8 +1995,11 @@ __global__ __launch_bounds__(kTailNT) void k_tail(TailState t, Ctl *ctl) {
         t.minpt[nxt][c] = INT32_MAX;
       }
       for (int32_t q = threadIdx.x; q < C * d; q += kTailNT) t.S[nxt][q] = 0;
-      for (int32_t v = threadIdx.x; v < nn; v += kTailNT)
-        s_L[v] = s_newid[s_sel[v]];
+      for (int32_t v = threadIdx.x; v < nn; v += kTailNT) {
+        const int32_t r = s_sel[v];
+        s_L[v] = s_newid[r];
+        if (r != v) s_mrg[s_newid[r]] = 1;
+      }
       __syncthreads();
       // Step 4 statistics: every node adds itself to its component, the
       // sums one (node, dimension) pair per thread so that loads coalesce.
@@ -1973,15 +2014,37 @@ __global__ __launch_bounds__(kTailNT) void k_tail(TailState t, Ctl *ctl) {
         wg_min(&t.minpt[nxt][c], s_minpt[v]);
         atomicAdd(&s_cap[c], spread * s_deg[v]);
       }
-      for (int32_t q = threadIdx.x; q < nn * d; q += kTailNT) {
-        const int32_t v = q / d;
-        wg_add64(&t.S[nxt][(int64_t)s_L[v] * d + (q - v * d)], s.S[q]);
+      for (int32_t q0 = threadIdx.x; q0 < nn * d; q0 += kTU * kTailNT) {
+        int64_t sv[kTU];
+#pragma unroll
+        for (int j = 0; j < kTU; ++j) {
+          sv[j] = s.S[min(q0 + j * kTailNT, nn * d - 1)];  // no branch
+        }
+#pragma unroll
+        for (int j = 0; j < kTU; ++j) {
+          const int32_t q = q0 + j * kTailNT;
+          if (q >= nn * d) break;
+          const int32_t v = q / d;
+          wg_add64(&t.S[nxt][(int64_t)s_L[v] * d + (q - v * d)], sv[j]);
+        }
       }
       __syncthreads();
-      for (int32_t q = threadIdx.x; q < C * d; q += kTailNT) {
-        const int32_t c = q / d;
-        const double m = (double)t.S[nxt][q] / (double)t.size[nxt][c];
-        t.mu[q] = m * sIF;
+      for (int32_t q0 = threadIdx.x; q0 < C * d; q0 += kTU * kTailNT) {
+        int64_t sv[kTU];
+        int32_t zv[kTU];
+#pragma unroll
+        for (int j = 0; j < kTU; ++j) {
+          const int32_t q = min(q0 + j * kTailNT, C * d - 1);  // no branch
+          sv[j] = t.S[nxt][q];
+          zv[j] = t.size[nxt][q / d];
+        }
+#pragma unroll
+        for (int j = 0; j < kTU; ++j) {
+          const int32_t q = q0 + j * kTailNT;
+          if (q >= C * d) break;
+          const double m = (double)sv[j] / (double)zv[j];
+          t.mu[q] = m * sIF;
+        }
       }
       // next table: windows of summed degree, cleared
       const int32_t slots =
@@ -1996,16 +2059,26 @@ __global__ __launch_bounds__(kTailNT) void k_tail(TailState t, Ctl *ctl) {
       __syncthreads();
       // Step 4 contraction, a thread per entry
       int32_t claims = 0;
-      for (int32_t q = threadIdx.x; q < Q; q += kTailNT) {
-        const uint64_t e = tb[q];
-        if (e == kEmpty) continue;
-        const int32_t v = rows[q];
-        const int32_t A = s_L[v], B = s_L[(int32_t)(e >> 32)];
-        if (A == B) continue;  // edge inside a merged component
-        claims += tail_table_add(t.tbl[1 - tc], t.row[1 - tc], A, s_wn[A],
-                                 s_cap[A], B, (int32_t)(uint32_t)e, ctl)
-                      ? 1
-                      : 0;
+      for (int32_t q0 = threadIdx.x; q0 < Q; q0 += kTU * kTailNT) {
+        uint64_t ev[kTU];
+        int32_t rv[kTU];
+#pragma unroll
+        for (int j = 0; j < kTU; ++j) {
+          const int32_t q = min(q0 + j * kTailNT, Q - 1);  // no branch
+          ev[j] = tb[q];
+          rv[j] = rows[q];
+        }
+#pragma unroll
+        for (int j = 0; j < kTU; ++j) {
+          const uint64_t e = ev[j];
+          if (q0 + j * kTailNT >= Q || e == kEmpty) continue;
+          const int32_t A = s_L[rv[j]], B = s_L[(int32_t)(e >> 32)];
+          if (A == B) continue;  // edge inside a merged component
+          claims += tail_table_add(t.tbl[1 - tc], t.row[1 - tc], A, s_wn[A],
+                                   s_cap[A], B, (int32_t)(uint32_t)e, ctl)
+                        ? 1
+                        : 0;
+        }
       }
       claims = wave_sum(claims);
       if (lane == 0 && claims) atomicAdd(&s_claims, claims);
