@@ -16,7 +16,11 @@ roofline.traffic comes from the committed counter summary
 profiles/knn_query.driving-3m.pmc.md (rocprofv3 FETCH_SIZE and WRITE_SIZE,
 scaled by what the same counters read for a copy kernel of known size; see
 --calib-copy); it is reported only while the kernel sources still hash to
-the values recorded there, and null otherwise.
+the values recorded there, and null otherwise.  roofline.issue does the same
+with the kernel's VALU instruction count (SQ_INSTS_VALU, committed in
+profiles/knn_query.driving-3m.sq-counters.md) over its launch time measured
+here, against the VALU issue peak: the kNN query is bound by instruction
+issue, not by HBM.
 """
 from __future__ import annotations
 
@@ -45,6 +49,11 @@ KINDS = {
     "aerial-10m-paper": "synthetic aerial tile, the paper's settings",
 }
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "knn_query.driving-3m.pmc.md")
+ISSUE_FILE = os.path.join(ROOT, "profiles",
+                          "knn_query.driving-3m.sq-counters.md")
+# VALU issue peak: 256 CUs x 4 SIMDs x 2.4 GHz, one wave64 instruction every
+# 4 cycles on a 16-lane SIMD
+VALU_ISSUE_PEAK = 256 * 4 * 2.4e9 / 4
 CALIB_ELEMS = 1 << 28  # float32 elements of the calibration copy (1 GiB)
 
 
@@ -85,19 +94,19 @@ def source_digest(files):
     return h.hexdigest()
 
 
-def measured_traffic(stage, n_points, k):
-    """HBM bytes per launch of `stage` from the committed counter summary,
-    or None when there is none for this stage and workload or the kernel
+def committed_value(path, key, stage, n_points, k):
+    """A figure from a committed counter summary ("- key: value" lines), or
+    None when there is none for this stage and workload or the kernel
     sources changed since the counters were taken."""
-    if not os.path.exists(TRAFFIC_FILE):
+    if not os.path.exists(path):
         return None
     kv = {}
-    with open(TRAFFIC_FILE) as fh:
+    with open(path) as fh:
         for line in fh:
             line = line.strip()
             if line.startswith("- ") and ":" in line:
-                key, val = line[2:].split(":", 1)
-                kv[key.strip()] = val.strip().strip("`")
+                name, val = line[2:].split(":", 1)
+                kv[name.strip()] = val.strip().strip("`")
     try:
         if kv.get("stage") != stage or int(kv["n_points"]) != n_points or \
                 int(kv["k"]) != k:
@@ -105,9 +114,21 @@ def measured_traffic(stage, n_points, k):
         files = kv["sources"].split(",")
         if source_digest([f.strip() for f in files]) != kv["sources_sha256"]:
             return None
-        return float(kv["traffic_bytes_per_launch"])
+        return float(kv[key])
     except (KeyError, ValueError, OSError):
         return None
+
+
+def measured_traffic(stage, n_points, k):
+    """HBM bytes per launch of `stage` (FETCH_SIZE + WRITE_SIZE, scaled)."""
+    return committed_value(TRAFFIC_FILE, "traffic_bytes_per_launch", stage,
+                           n_points, k)
+
+
+def measured_valu(stage, n_points, k):
+    """Wave-level VALU instructions per launch of `stage` (SQ_INSTS_VALU)."""
+    return committed_value(ISSUE_FILE, "valu_wave_instr_per_launch", stage,
+                           n_points, k)
 
 
 def cpu_baseline(sc, n_sample, link=False):
@@ -428,6 +449,14 @@ def main():
         if per_launch_ms > 0 else 0.0
     alg_total = sum(v["bytes"] for v in stages.values()) / args.steps
     traffic = measured_traffic(dom, sc.n, sc.k)
+    valu = measured_valu(dom, sc.n, sc.k)
+    issue = None
+    if valu is not None and per_launch_ms > 0:
+        rate = valu / (per_launch_ms * 1e-3)
+        issue = {"valu_wave_instr_per_launch": valu,
+                 "achieved": round(rate, 1), "peak": VALU_ISSUE_PEAK,
+                 "unit": "wave-instr/s",
+                 "frac": round(rate / VALU_ISSUE_PEAK, 4)}
     roofline = {
         "bound": "hbm", "kernel": dom, "achieved": round(achieved, 2),
         "peak": HBM_PEAK_GBS, "unit": "GB/s",
@@ -437,6 +466,7 @@ def main():
         "step_alg_bytes": alg_total,
         "step_alg_frac": round(alg_total / (ms_per_step * 1e-3) / 1e9 /
                                HBM_PEAK_GBS, 5),
+        "issue": issue,
     }
     split = {s: round(v[1] / max(args.split_steps, 1), 4)
              for s, v in split_stats.items()}

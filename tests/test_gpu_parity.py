@@ -69,6 +69,23 @@ def test_knn_tiny_and_ragged(n):
         assert np.array_equal(d2.cpu().numpy(), rd), (n, k)
 
 
+@pytest.mark.parametrize("n", [7, 20, 37])
+def test_knn_overflowing_distances(n):
+    """Coordinates near 1e20: most squared distances overflow to +inf, and
+    ties at +inf go to the smaller index, ahead of the padding that fills
+    the last bucket (n not a multiple of 16; with k >= n every real point
+    is listed and the rest is -1)."""
+    rng = np.random.default_rng(n)
+    xyz = ((rng.random((n, 3)) - 0.5) * 2e20).astype(np.float32)
+    xyz[: n // 3] *= np.float32(1e-19)  # a few finite distances as well
+    for k in (3, 10, 40):
+        ref, rd = oracle.knn(xyz, k, "brute")
+        nbr, d2 = ezsp.knn(dev(xyz), k, want_d2=True)
+        assert np.isinf(rd).any()
+        assert np.array_equal(nbr.cpu().numpy(), ref), (n, k)
+        assert np.array_equal(d2.cpu().numpy(), rd), (n, k)
+
+
 def test_knn_room_full():
     sc = scenes.load("room-20k")
     ref, rd = oracle.knn(sc.xyz, sc.k)
