@@ -415,9 +415,9 @@ __global__ __launch_bounds__(256) void k_knn_query(
   uint64_t mlo = 0, mhi = 0;
   int32_t cur = 0;
   int curl = tree.top;
+  // the group's largest k-th distance changes only in a bucket scan
+  uint32_t gk = group_max_kth(act ? (uint32_t)(key[K - 1] >> 32) : 0u);
   if (tree.top > 0) {
-    const uint32_t gk =
-        group_max_kth(act ? (uint32_t)(key[K - 1] >> 32) : 0u);
     const uint32_t m8 = coarse_mask(blo, bhi, lv_off, lv_cnt, tree.top - 1, 0,
                                     qlo, qhi, gk, lane16, gshift);
     set_level_bits(mlo, mhi, tree.top - 1, m8);
@@ -453,15 +453,16 @@ __global__ __launch_bounds__(256) void k_knn_query(
         leaf = node;
         break;
       }
-      const uint32_t gk = group_max_kth(act ? kth : 0u);
       const uint32_t m8 = coarse_mask(blo, bhi, lv_off, lv_cnt, l - 1,
                                       node * kFan, qlo, qhi, gk, lane16,
                                       gshift);
       set_level_bits(mlo, mhi, l - 1, m8);
     }
     if (__ballot(leaf >= 0) == 0) break;
-    if (leaf >= 0)
+    if (leaf >= 0) {
       scan_bucket<K, false>(pts, leaf, lane16, p.x, p.y, p.z, me, key);
+      gk = group_max_kth(act ? (uint32_t)(key[K - 1] >> 32) : 0u);
+    }
   }
 
   if (!act) return;

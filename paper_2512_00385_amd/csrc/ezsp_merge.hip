@@ -198,30 +198,54 @@ __global__ __launch_bounds__(256) void k_rev_count_kth(
     const int32_t *nbr, int32_t n, int32_t k, const float4 *__restrict__ pts,
     const uint64_t *__restrict__ kth, int32_t *rev, uint64_t *nmask,
     Ctl *ctl) {
+  // Row chunks of four entries taken at once: the row, then every
+  // neighbour's point and k-th key, are loaded before any is used (empty
+  // entries load the point itself), so a row of up to 12 entries costs two
+  // memory round trips.
+  constexpr int kCh = 3;
   const int32_t i = xcd_tid();
   const int32_t kp = pad4(k);
   int32_t fwd = 0;
   if (i < n) {
-    const int32_t *r = nbr + (int64_t)i * kp;
-    const int4 *r4 = reinterpret_cast<const int4 *>(r);  // rows of pad4(k)
+    const int4 *r4 = reinterpret_cast<const int4 *>(nbr + (int64_t)i * kp);
     const float4 pi = pts[i];
+    const int32_t nch = kp / 4;
     uint64_t mask = 0;
-#pragma unroll 4
-    for (int32_t t = 0; t < k; ++t) {
-      const int4 c = r4[t >> 2];
-      const int32_t u = (t & 3) == 0 ? c.x : (t & 3) == 1 ? c.y
-                        : (t & 3) == 2 ? c.z : c.w;
-      if (u < 0) continue;
-      ++fwd;
-      const float4 pu = pts[u];
-      const float dx = pi.x - pu.x, dy = pi.y - pu.y, dz = pi.z - pu.z;
-      const float xx = dx * dx, yy = dy * dy, zz = dz * dz;
-      const float d2 = (xx + yy) + zz;
-      const uint64_t key = ((uint64_t)__float_as_uint(d2) << 32) |
-                           (uint32_t)__float_as_int(pi.w);
-      if (key > kth[u]) mask |= 1ull << t;
+    for (int32_t c0 = 0; c0 < nch; c0 += kCh) {
+      int32_t u[4 * kCh];
+#pragma unroll
+      for (int j = 0; j < kCh; ++j) {
+        const int4 c = r4[min(c0 + j, nch - 1)];
+        const bool in = c0 + j < nch;
+        u[4 * j + 0] = in ? c.x : -1;
+        u[4 * j + 1] = in ? c.y : -1;
+        u[4 * j + 2] = in ? c.z : -1;
+        u[4 * j + 3] = in ? c.w : -1;
+      }
+      float4 pu[4 * kCh];
+      uint64_t ku[4 * kCh];
+#pragma unroll
+      for (int t = 0; t < 4 * kCh; ++t) {
+        const int32_t uc = u[t] >= 0 ? u[t] : i;
+        pu[t] = pts[uc];
+        ku[t] = kth[uc];
+      }
+#pragma unroll
+      for (int t = 0; t < 4 * kCh; ++t) {
+        const int32_t slot = 4 * c0 + t;  // entries past k hold -1
+        if (u[t] < 0) continue;
+        ++fwd;
+        const float dx = pi.x - pu[t].x, dy = pi.y - pu[t].y,
+                    dz = pi.z - pu[t].z;
+        const float xx = dx * dx, yy = dy * dy, zz = dz * dz;
+        const float d2 = (xx + yy) + zz;
+        const uint64_t key = ((uint64_t)__float_as_uint(d2) << 32) |
+                             (uint32_t)__float_as_int(pi.w);
+        if (key > ku[t]) mask |= 1ull << slot;
+      }
     }
     nmask[i] = mask;
+    const int32_t *r = nbr + (int64_t)i * kp;
     for (uint64_t m = mask; m; m &= m - 1)
       atomicAdd(&rev[r[__builtin_ctzll(m)]], 1);
   }
