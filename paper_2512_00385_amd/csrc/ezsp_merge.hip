@@ -2127,28 +2127,10 @@ __global__ __launch_bounds__(kTailNT) void k_tail(TailState t, Ctl *ctl) {
     }
     for (int32_t i = threadIdx.x; i < t.nn0; i += kTailNT)
       t.lvl_map[(int64_t)l * t.nn0 + i] = t.Mt[i];
-    for (int32_t c = threadIdx.x; c < nn; c += kTailNT) {
-      const int32_t m = t.minpt[cur][c];
-      t.lvl_minpt[(int64_t)l * t.nn0 + c] = m;
-      s_minpt[c] = m;
-    }
-    __syncthreads();
-    // canonical number of every component: its rank by smallest point
-    {
-      const int4 *m4 = reinterpret_cast<const int4 *>(s_minpt);
-      const int32_t n4 = nn >> 2;
-      for (int32_t c = threadIdx.x; c < nn; c += kTailNT) {
-        const int32_t m = s_minpt[c];
-        int32_t r = 0;
-#pragma unroll 4
-        for (int32_t j = 0; j < n4; ++j) {
-          const int4 x = m4[j];
-          r += (x.x < m) + (x.y < m) + (x.z < m) + (x.w < m);
-        }
-        for (int32_t c2 = 4 * n4; c2 < nn; ++c2) r += s_minpt[c2] < m ? 1 : 0;
-        t.lvl_rank[(int64_t)l * t.nn0 + c] = r;
-      }
-    }
+    // (the canonical numbers, ranks of these smallest points, are counted
+    // after the tail by k_tail_rank on many CUs)
+    for (int32_t c = threadIdx.x; c < nn; c += kTailNT)
+      t.lvl_minpt[(int64_t)l * t.nn0 + c] = t.minpt[cur][c];
     __syncthreads();
     if (t.want_energy) {
       for (int64_t q = threadIdx.x; q < (int64_t)nn * d; q += kTailNT)
@@ -2167,6 +2149,32 @@ __global__ __launch_bounds__(kTailNT) void k_tail(TailState t, Ctl *ctl) {
     }
     __syncthreads();
   }
+}
+
+// Canonical number of every component of every level the tail ended: the
+// rank of its smallest point among the level's components.  64 components
+// per block, four lanes per component counting a quarter each over the
+// level's smallest points staged in LDS.  A level count out of range (only
+// after a device error, whose outputs are discarded) is clamped to nt.
+__global__ __launch_bounds__(256) void k_tail_rank(
+    const int32_t *__restrict__ lvl_minpt, const int32_t *__restrict__ lvl_nc,
+    int32_t nt, int32_t level0, int32_t *__restrict__ lvl_rank) {
+  __shared__ int32_t sm[kTailNodes];
+  const int32_t l = level0 + (int32_t)blockIdx.y;
+  const int32_t nc = min(max(lvl_nc[l], 0), min(nt, kTailNodes));
+  const int32_t *mp = lvl_minpt + (int64_t)l * nt;
+  for (int32_t c = threadIdx.x; c < nc; c += blockDim.x) sm[c] = mp[c];
+  __syncthreads();
+  const int32_t c = (int32_t)blockIdx.x * 64 + (int32_t)(threadIdx.x >> 2);
+  const int q = threadIdx.x & 3;
+  int32_t r = 0;
+  if (c < nc) {
+    const int32_t m = sm[c];
+    for (int32_t j = q; j < nc; j += 4) r += sm[j] < m ? 1 : 0;
+  }
+  r += __shfl_xor(r, 1, kWave);
+  r += __shfl_xor(r, 2, kWave);
+  if (c < nc && q == 0) lvl_rank[(int64_t)l * nt + c] = r;
 }
 
 // Point labels of every level the tail ended: point p -> its node at the
@@ -2884,8 +2892,11 @@ int run_tail(const LadderArgs &g, const Bufs &b, const float *emb,
       hipLaunchKernelGGL(k_tail<0>, dim3(1), dim3(kTailNT), 0, st, t, ctl);
   }
   prof_end(st);
-  // labels straight from the snapshots (no host round trip in between);
-  // on a device error they are discarded
+  // ranks and labels straight from the snapshots (no host round trip in
+  // between); on a device error they are discarded
+  hipLaunchKernelGGL(k_tail_rank, dim3((nn + 63) / 64, g.n_levels - level0),
+                     dim3(256), 0, st, b.lvl_minpt, t.lvl_nc, nn, level0,
+                     b.lvl_rank);
   hipLaunchKernelGGL(k_tail_labels, blocks_for(n), dim3(256), 0, st, n, g.inv,
                      b.M, b.lvl_map, b.lvl_rank, t.lvl_nc, nn, level0,
                      g.n_levels, g.labels, ctl);
