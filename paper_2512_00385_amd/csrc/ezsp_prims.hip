@@ -79,14 +79,25 @@ __global__ __launch_bounds__(kSortNT) void k_rs_scatter(
     run[d] = offs[d * nb + blockIdx.x];
   const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (kWave - lane));
   const int32_t base = blockIdx.x * kSortTile;
+  // the thread's keys and values of the whole tile, loaded before the first
+  // step (clamped indices, no branch): the steps then wait on LDS only
+  uint64_t kt[kSortItems];
+  uint32_t vt[kSortItems];
+#pragma unroll
+  for (int j = 0; j < kSortItems; ++j) {
+    const int32_t i = min(base + j * kSortNT + (int32_t)threadIdx.x, n - 1);
+    kt[j] = kin[i];
+    vt[j] = vin[i];
+  }
+#pragma unroll
   for (int j = 0; j < kSortItems; ++j) {
     for (int t = threadIdx.x; t < kW * kSortBins; t += kSortNT)
       (&wc[0][0])[t] = 0;
     __syncthreads();
     const int32_t i = base + j * kSortNT + threadIdx.x;
     const bool valid = i < n;
-    const uint64_t key = valid ? kin[i] : 0ull;
-    const uint32_t val = valid ? vin[i] : 0u;
+    const uint64_t key = valid ? kt[j] : 0ull;
+    const uint32_t val = valid ? vt[j] : 0u;
     const int dig = (int)((key >> shift) & (kSortBins - 1));
     uint64_t peers = __ballot(valid);
 #pragma unroll
