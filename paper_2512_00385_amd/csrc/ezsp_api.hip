@@ -101,8 +101,17 @@ int run_partition(const float *xyz, const int32_t *nbr_in, const float *emb,
   if (with_knn) {
     KnnWork w;
     knn_reserve(a, (int32_t)n, p->k, &w);
+    // rows of 4, 8, 12 or 16 floats at a 16-byte aligned base: the kNN
+    // kernel copies them into internal order for the ladder on the way
+    g.emb_ready = d % 4 == 0 && d <= 16 &&
+                  (reinterpret_cast<uintptr_t>(emb) & 15) == 0;
     int rc = check_hip(
-        knn_launch(xyz, (int32_t)n, p->k, ctl, w, nullptr, nullptr, st),
+        g.emb_ready
+            ? knn_launch_emb(xyz, (int32_t)n, p->k, ctl, w, emb, d,
+                             ladder_emb_slot(a, (int32_t)n, d, p->k, link),
+                             st)
+            : knn_launch(xyz, (int32_t)n, p->k, ctl, w, nullptr, nullptr,
+                         st),
         "knn launch");
     if (rc) return rc;
     g.nbr = w.nbr_int;

@@ -110,6 +110,12 @@ void knn_reserve(Arena &a, int32_t n, int32_t k, KnnWork *w);
 hipError_t knn_launch(const float *xyz, int32_t n, int32_t k, Ctl *ctl,
                       const KnnWork &w, int32_t *nbr_out, float *d2_out,
                       hipStream_t st);
+// The same, also copying the embedding rows (n x d floats, d a multiple of
+// 4 up to 16, 16-byte aligned) into internal order in emb_out and taking
+// Step 0's max |e| into the control block, as the ladder's first gather does.
+hipError_t knn_launch_emb(const float *xyz, int32_t n, int32_t k, Ctl *ctl,
+                          const KnnWork &w, const float *emb, int32_t d,
+                          float *emb_out, hipStream_t st);
 
 // Merge ladder on a neighbour table (internal ids; perm/inv may be null
 // when internal == original order).
@@ -128,11 +134,16 @@ struct LadderArgs {
   bool want_energy;
   bool link;            // prepare_graph's linking of isolated nodes (needs pts)
   bool check_nbr;       // validate caller-supplied neighbour ids
+  bool emb_ready;       // the ladder's embedding buffer already holds the
+                        // rows in internal order, max |e| taken (kNN copy)
   int32_t *labels;      // L*n, caller order
   int64_t *n_comp;      // host
   double *energy;       // host, nullable
 };
 void ladder_reserve(Arena &a, int32_t n, int32_t d, int32_t k, bool link);
+// Where ladder_run, given the arena as it is now, keeps the embeddings in
+// internal order (n x d floats).
+float *ladder_emb_slot(Arena a, int32_t n, int32_t d, int32_t k, bool link);
 // Returns an ezsp_status code; detail text goes through set_error().
 int ladder_run(const LadderArgs &args, Ctl *ctl, Arena &a, hipStream_t st);
 

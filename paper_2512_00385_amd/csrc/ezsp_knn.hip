@@ -377,7 +377,9 @@ __global__ __launch_bounds__(256) void k_knn_query(
     int32_t n, const float4 *__restrict__ blo, const float4 *__restrict__ bhi,
     Tree tree, int32_t k, int32_t *__restrict__ nbr_int,
     int32_t *__restrict__ nbr_out, float *__restrict__ d2_out,
-    uint64_t *__restrict__ kth_out, int32_t n_blocks) {
+    uint64_t *__restrict__ kth_out, int32_t n_blocks,
+    const float4 *__restrict__ emb, int32_t d4, float4 *__restrict__ emb_out,
+    Ctl *ctl) {
   const int32_t lb = xcd_block();
   if (lb >= n_blocks) return;
   // level offsets and counts of the box tree, indexed per lane in the walk
@@ -391,17 +393,55 @@ __global__ __launch_bounds__(256) void k_knn_query(
   const int gshift = threadIdx.x & (kWave - kBucket);  // 0, 16, 32, 48
   const int32_t nb0 = tree.cnt[0];
   const int32_t grp = lb * (256 / kBucket) + (int32_t)(threadIdx.x / kBucket);
-  if (grp >= nb0) return;  // whole group past the end
+  const bool gvalid = grp < nb0;  // else the whole group is past the end
   const int32_t i = grp * kBucket + lane16;
-  const bool act = i < n;
+  const bool act = gvalid && i < n;
   const float4 p = act ? pts[i] : make_float4(0.f, 0.f, 0.f, 0.f);
   const int32_t me = act ? __float_as_int(p.w) : -1;
+  // For the merge, optionally: the point's embedding row (d4 <= 4 float4)
+  // copied into internal order, with Step 0's max |e| and the non-finite
+  // check.  The loads are issued here and the stores made after the own
+  // bucket's scan, whose instructions cover their latency.
+  float4 row[4];
+  if (emb && act) {
+    const float4 *src = emb + (int64_t)me * d4;
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      if (q < d4) row[q] = src[q];
+  }
   uint64_t key[K];
 #pragma unroll
   for (int t = 0; t < K; ++t) key[t] = kNoKey;
   // own bucket and its Morton neighbours first: a tight k-th distance early
   // (the two Morton neighbours are the first buckets of the scan loop below)
-  scan_bucket<K, true>(pts, grp, lane16, p.x, p.y, p.z, me, key);
+  if (gvalid) scan_bucket<K, true>(pts, grp, lane16, p.x, p.y, p.z, me, key);
+  if (emb) {  // every lane of the wave is here
+    uint32_t m = 0;
+    bool bad = false;
+    if (act) {
+      float4 *dst = emb_out + (int64_t)i * d4;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        if (q >= d4) break;
+        dst[q] = row[q];
+        const float v[4] = {row[q].x, row[q].y, row[q].z, row[q].w};
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          if (!isfinite(v[j])) bad = true;
+          else m = max(m, __float_as_uint(fabsf(v[j])));
+        }
+      }
+    }
+#pragma unroll
+    for (int off = kWave / 2; off > 0; off >>= 1)
+      m = max(m, (uint32_t)__shfl_xor((int)m, off, kWave));
+    const bool any_bad = __ballot(bad) != 0;
+    if ((threadIdx.x & (kWave - 1)) == 0) {
+      stripe_max(ctl->maxabs_s, (int32_t)m);  // |e| bits < 2^31
+      if (any_bad) raise_err(ctl, kErrNonFinite);
+    }
+  }
+  if (!gvalid) return;
 
   // Depth-first walk with the pending children of every level of the
   // current path as bits: bit 8*l + c = child c (level l) of the path node
@@ -516,9 +556,10 @@ void knn_reserve(Arena &a, int32_t n, int32_t k, KnnWork *w) {
   w->total = a.take<int32_t>(4);
 }
 
-hipError_t knn_launch(const float *xyz, int32_t n, int32_t k, Ctl *ctl,
-                      const KnnWork &s, int32_t *nbr_out, float *d2_out,
-                      hipStream_t st) {
+static hipError_t knn_impl(const float *xyz, int32_t n, int32_t k, Ctl *ctl,
+                           const KnnWork &s, int32_t *nbr_out, float *d2_out,
+                           const float *emb, int32_t d, float *emb_out,
+                           hipStream_t st) {
   const KnnWork &w = s;
   const Tree tree = make_tree(n);
   const int nt = 256;
@@ -543,14 +584,15 @@ hipError_t knn_launch(const float *xyz, int32_t n, int32_t k, Ctl *ctl,
                        tree.off[l], tree.cnt[l]);
   const int32_t qblocks = (tree.cnt[0] + (nt / kBucket) - 1) / (nt / kBucket);
   const dim3 grid(xcd_grid(qblocks));
+  const float4 *emb4 = reinterpret_cast<const float4 *>(emb);
+  float4 *emb_out4 = reinterpret_cast<float4 *>(emb_out);
   prof_begin("knn_query", st);
   switch (knn_template_k(k)) {
 #define EZSP_KNN_CASE(KK)                                                    \
   case KK:                                                                   \
     hipLaunchKernelGGL(k_knn_query<KK>, grid, dim3(nt), 0, st, s.pts, w.inv, \
-                       n,                                                    \
-                       s.blo, s.bhi, tree, k, w.nbr_int, nbr_out, d2_out,    \
-                       w.kth, qblocks);                                      \
+                       n, s.blo, s.bhi, tree, k, w.nbr_int, nbr_out, d2_out, \
+                       w.kth, qblocks, emb4, d / 4, emb_out4, ctl);          \
     break;
     EZSP_KNN_CASE(4)
     EZSP_KNN_CASE(8)
@@ -564,9 +606,26 @@ hipError_t knn_launch(const float *xyz, int32_t n, int32_t k, Ctl *ctl,
       return hipErrorInvalidValue;
   }
   prof_end(st);
-  // algorithmic bytes: read xyz, write the n*k neighbour table
-  prof_bytes("knn_query", (12.0 + 4.0 * k) * n);
+  // algorithmic bytes: read xyz, write the n*k neighbour table (and, with
+  // the embedding copy, read and write n*d floats)
+  prof_bytes("knn_query", (12.0 + 4.0 * k + (emb ? 8.0 * d : 0.0)) * n);
   return hipGetLastError();
+}
+
+hipError_t knn_launch(const float *xyz, int32_t n, int32_t k, Ctl *ctl,
+                      const KnnWork &s, int32_t *nbr_out, float *d2_out,
+                      hipStream_t st) {
+  return knn_impl(xyz, n, k, ctl, s, nbr_out, d2_out, nullptr, 0, nullptr,
+                  st);
+}
+
+hipError_t knn_launch_emb(const float *xyz, int32_t n, int32_t k, Ctl *ctl,
+                          const KnnWork &s, const float *emb, int32_t d,
+                          float *emb_out, hipStream_t st) {
+  if (d % 4 != 0 || d > 16 || (reinterpret_cast<uintptr_t>(emb) & 15) != 0 ||
+      (reinterpret_cast<uintptr_t>(emb_out) & 15) != 0)
+    return hipErrorInvalidValue;
+  return knn_impl(xyz, n, k, ctl, s, nullptr, nullptr, emb, d, emb_out, st);
 }
 
 }  // namespace ezsp

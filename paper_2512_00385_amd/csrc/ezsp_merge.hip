@@ -3005,6 +3005,12 @@ void ladder_reserve(Arena &a, int32_t n, int32_t d, int32_t k, bool link) {
   carve(a, n, d, k, link, &b);
 }
 
+float *ladder_emb_slot(Arena a, int32_t n, int32_t d, int32_t k, bool link) {
+  Bufs b;
+  carve(a, n, d, k, link, &b);  // on a copy of the arena
+  return b.emb_int;
+}
+
 int ladder_run(const LadderArgs &g, Ctl *ctl, Arena &a, hipStream_t st) {
   Bufs b;
   carve(a, g.n, g.d, g.k, g.link, &b);
@@ -3028,7 +3034,9 @@ int ladder_run(const LadderArgs &g, Ctl *ctl, Arena &a, hipStream_t st) {
   // max |e| reduction fused in
   const bool fused = g.perm && d % 4 == 0 &&
                      (reinterpret_cast<uintptr_t>(g.emb) & 15) == 0;
-  if (g.perm) {
+  if (g.emb_ready) {
+    // copied by the kNN kernel, max |e| included
+  } else if (g.perm) {
     if (fused) {
       const int64_t t4 = (int64_t)n * (d / 4);
       const unsigned grid =
@@ -3046,7 +3054,7 @@ int ladder_run(const LadderArgs &g, Ctl *ctl, Arena &a, hipStream_t st) {
                    "hipMemcpyAsync(emb)");
     if (rc) return rc;
   }
-  if (!fused)
+  if (!fused && !g.emb_ready)
     hipLaunchKernelGGL(k_maxabs, dim3(2048), dim3(256), 0, st, emb,
                        (int64_t)n * d, ctl);
   hipLaunchKernelGGL(k_fixshift, dim3(1), dim3(64), 0, st, ctl, n);
