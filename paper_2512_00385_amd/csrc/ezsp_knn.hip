@@ -606,9 +606,9 @@ static hipError_t knn_impl(const float *xyz, int32_t n, int32_t k, Ctl *ctl,
       return hipErrorInvalidValue;
   }
   prof_end(st);
-  // algorithmic bytes: read xyz, write the n*k neighbour table (and, with
-  // the embedding copy, read and write n*d floats)
-  prof_bytes("knn_query", (12.0 + 4.0 * k + (emb ? 8.0 * d : 0.0)) * n);
+  // algorithmic bytes: read xyz, write the n*k neighbour table (the
+  // embedding copy is a reordering for the merge, not counted)
+  prof_bytes("knn_query", (12.0 + 4.0 * k) * n);
   return hipGetLastError();
 }
 
