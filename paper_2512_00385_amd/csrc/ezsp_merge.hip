@@ -46,7 +46,7 @@
 namespace ezsp {
 
 constexpr uint64_t kEmpty = ~0ull;
-constexpr int kJumpCap = 1 << 16;
+constexpr int kJumpWalk = 64;  // steps of a pointer-jumping walk
 constexpr int kLongRow = 128;    // longer rows go in entry chunks ...
 constexpr int kLongChunk = 1024; // ... of this many entries, a wave each
 constexpr int kLongGrid = 2048;  // blocks of 4 waves for the chunks
@@ -715,7 +715,7 @@ __global__ __launch_bounds__(256) void k_select_combine(
 // The next round's merged flags: a component of more than one member.
 __global__ __launch_bounds__(256) void k_merged(const int32_t *moff,
                                                 uint8_t *merged, Ctl *ctl) {
-  if (!ctl->any_choice) return;
+  if (!round_live(ctl)) return;
   int32_t c;
   if (!xcd_item(ctl->n_next, c)) return;
   merged[c] = (moff[c + 1] - moff[c] > 1) ? 1 : 0;
@@ -744,15 +744,22 @@ __global__ __launch_bounds__(256) void k_hook(int32_t nn, const int32_t *target,
   parent[v] = p;
 }
 
-// Pointer jumping: every step moves strictly up the forest, so the loop ends
-// at the root; concurrent updates by other threads only shorten it.
+// Pointer jumping, first pass: each thread walks from its node towards the
+// root, reading parents that other threads may already have moved closer to
+// their roots (every value read is an ancestor, so the walk only shortens).
+// A walk stops after kJumpWalk steps: a long chain (a line of points in
+// index order with tied gains makes one of length n) would otherwise cost
+// n dependent loads per thread.  A stopped walk keeps the ancestor it
+// reached and marks the round unfinished (any_choice = -1), so that the
+// round's later kernels wait; the host then completes the forest with
+// pointer-doubling passes (k_double) and launches them again.
 __global__ __launch_bounds__(256) void k_jump(int32_t nn, int32_t *parent,
                                               Ctl *ctl) {
   const int32_t v = blockIdx.x * blockDim.x + threadIdx.x;
   if (v >= nn) return;
   int32_t p = parent[v];
   int it = 0;
-  for (; it < kJumpCap; ++it) {
+  for (; it < kJumpWalk; ++it) {
     if ((uint32_t)p >= (uint32_t)nn) {
       raise_err(ctl, kErrInternal);
       p = v;
@@ -762,8 +769,38 @@ __global__ __launch_bounds__(256) void k_jump(int32_t nn, int32_t *parent,
     if (pp == p) break;
     p = pp;
   }
-  if (it == kJumpCap) raise_err(ctl, kErrJump);
   __atomic_store_n(&parent[v], p, __ATOMIC_RELAXED);
+  if (it == kJumpWalk) __atomic_store_n(&ctl->any_choice, -1, __ATOMIC_RELAXED);
+}
+
+// One pointer-doubling pass: parent[v] = parent[parent[v]].  Values read
+// concurrently are ancestors at least as high as the pass would see in
+// lockstep, so every pass at least halves the remaining depth, and
+// ceil(log2 depth) passes reach the roots.  jump_changed records whether
+// any parent moved.
+__global__ __launch_bounds__(256) void k_double(int32_t nn, int32_t *parent,
+                                                Ctl *ctl) {
+  const int32_t v = blockIdx.x * blockDim.x + threadIdx.x;
+  if (v >= nn) return;
+  const int32_t p = parent[v];
+  if ((uint32_t)p >= (uint32_t)nn) {
+    raise_err(ctl, kErrInternal);
+    return;
+  }
+  const int32_t pp = __atomic_load_n(&parent[p], __ATOMIC_RELAXED);
+  if (pp != p) {
+    __atomic_store_n(&parent[v], pp, __ATOMIC_RELAXED);
+    ctl->jump_changed = 1;
+  }
+}
+
+// Starts a round of doubling passes (jump_changed = 0); with done set, marks
+// the forest complete so the round's later kernels run (any_choice = 1).
+__global__ void k_jump_state(Ctl *ctl, int done) {
+  if (threadIdx.x == 0 && blockIdx.x == 0) {
+    if (done) ctl->any_choice = 1;
+    else ctl->jump_changed = 0;
+  }
 }
 
 // Roots numbered in node order; the pass also clears the member counters
@@ -803,7 +840,7 @@ struct ScanWindows {
     else raise_err(ctl, kErrInternal);
   }
   __device__ void emit(int32_t i, int32_t excl, int32_t v) const {
-    if (!ctl->any_choice) return;  // nothing merged: capacities are stale
+    if (!round_live(ctl)) return;  // nothing merged: capacities are stale
     const int32_t len = *n_dev;
     if (i > len) return;
     toff[i] = excl;
@@ -826,7 +863,7 @@ __global__ __launch_bounds__(256) void k_assign(int32_t nn,
                                                 const int32_t *newid,
                                                 int32_t *L, int32_t *cnt,
                                                 int32_t *rank, Ctl *ctl) {
-  if (!ctl->any_choice) return;
+  if (!round_live(ctl)) return;
   const int32_t v = xcd_tid();
   const bool act = v < nn;
   int32_t c = -1;
@@ -868,7 +905,7 @@ __global__ __launch_bounds__(256) void k_place(int32_t nn, const int32_t *L,
                                                const int32_t *moff,
                                                const int32_t *rank,
                                                int32_t *mem, Ctl *ctl) {
-  if (!ctl->any_choice) return;
+  if (!round_live(ctl)) return;
   const int32_t v = xcd_tid();
   if (v >= nn) return;
   const int32_t pos = moff[L[v]] + rank[v];
@@ -924,7 +961,7 @@ __global__ __launch_bounds__(256) void k_stats(
     const int32_t *__restrict__ moff, NodeIn s,
     const int32_t *__restrict__ deg, int32_t d, NodeOut o,
     int32_t *__restrict__ big, Ctl *ctl) {
-  if (!ctl->any_choice) return;
+  if (!round_live(ctl)) return;
   int32_t c;
   if (!xcd_item(min(bound, ctl->n_next), c)) return;
   const int32_t m0 = moff[c], m1 = moff[c + 1];
@@ -1019,7 +1056,7 @@ __global__ __launch_bounds__(256) void k_stats_g(
     const int32_t *__restrict__ deg, NodeOut o,
     int32_t *__restrict__ big, Ctl *ctl) {
   static_assert(DT % G == 0 && (DT / G) % 2 == 0, "dims per lane");
-  if (!ctl->any_choice) return;
+  if (!round_live(ctl)) return;
   const int32_t total = min(bound, ctl->n_next) * G;
   const int32_t per = ((total + kXcd - 1) / kXcd + G - 1) / G * G;
   const int32_t j =
@@ -1099,7 +1136,7 @@ __global__ __launch_bounds__(256) void k_stats_big(
     const int32_t *__restrict__ big, Ctl *ctl) {
   __shared__ unsigned long long sS[64];
   __shared__ int32_t ssize, smp, scap;
-  if (!ctl->any_choice) return;
+  if (!round_live(ctl)) return;
   const double sF = ldexp(1.0, ctl->F), sIF = ldexp(1.0, -ctl->F);
   const int32_t n_big = ctl->n_big;
   for (int32_t bi = blockIdx.x; bi < n_big; bi += gridDim.x) {
@@ -1223,7 +1260,7 @@ __global__ __launch_bounds__(256) void k_contract_chunk(
   __shared__ int32_t bm[kBatch], bA[kBatch], blb[kBatch], bcp[kBatch];
   __shared__ int32_t bbase[kBatch];
   __shared__ int32_t wsum[256 / kWave];
-  if (!ctl->any_choice) return;
+  if (!round_live(ctl)) return;
   // chunks q = this block's, then every gridDim.x-th: the grid is sized for
   // the entries, the windows may span up to twice as many slots
   const int32_t slots = ctl->slots;
@@ -1351,7 +1388,7 @@ __global__ __launch_bounds__(256) void k_contract_chunk(
 __global__ __launch_bounds__(256) void k_clear_big(
     const int32_t *__restrict__ cbig, const int32_t *__restrict__ toff,
     const int32_t *__restrict__ cap, uint64_t *tbl, int32_t tcap, Ctl *ctl) {
-  if (!ctl->any_choice) return;
+  if (!round_live(ctl)) return;
   const int32_t nb = ctl->n_cbig;
   for (int32_t bi = blockIdx.x; bi < nb; bi += gridDim.x) {
     const int32_t c = cbig[bi];
@@ -1402,7 +1439,7 @@ __global__ __launch_bounds__(256) void k_contract_big(
   __shared__ int32_t pre[kBatch + 1];
   __shared__ int32_t bm[kBatch];
   __shared__ int32_t wsum[256 / kWave];
-  if (!ctl->any_choice) return;
+  if (!round_live(ctl)) return;
   const int32_t n_tiles = ctl->n_tiles;
   int32_t added = 0;
   for (int32_t t = blockIdx.x; t < n_tiles; t += gridDim.x) {
@@ -1469,7 +1506,7 @@ __global__ __launch_bounds__(256) void k_contract_long(
   static_assert(kLongChunk <= kPreSlots / 2, "a chunk fits the LDS table");
   __shared__ int32_t pk[kPreSlots];
   __shared__ int32_t pw[kPreSlots];
-  if (!ctl->any_choice) return;
+  if (!round_live(ctl)) return;
   const int32_t n_items = ctl->n_lchunk;
   int32_t added = 0;
   for (int32_t it = blockIdx.x; it < n_items; it += gridDim.x) {
@@ -1525,7 +1562,7 @@ template <bool FIRST>
 __global__ __launch_bounds__(256) void k_compose(int32_t n, int32_t nn,
                                                  int32_t *M, const int32_t *L,
                                                  Ctl *ctl) {
-  if (!ctl->any_choice) return;
+  if (!round_live(ctl)) return;
   const int32_t i = xcd_tid();
   if (i >= n) return;
   const int32_t c = FIRST ? i : M[i];
@@ -2268,7 +2305,7 @@ __global__ __launch_bounds__(256) void k_link_detect(const int32_t *ws,
                                                      int32_t *iso,
                                                      int32_t *iso_of,
                                                      Ctl *ctl) {
-  if (!ctl->any_choice) return;
+  if (!round_live(ctl)) return;
   int32_t v;
   if (!xcd_item(ctl->n_next, v)) return;
   const uint64_t *t = tbl + ws[v];
@@ -2307,7 +2344,7 @@ template <bool FIRST>
 __global__ __launch_bounds__(256) void k_link_accum(
     const int32_t *mem, const int32_t *moff, const float4 *pts,
     const int64_t *sx_in, int64_t *sx_out, Ctl *ctl) {
-  if (!ctl->any_choice) return;
+  if (!round_live(ctl)) return;
   int32_t c;
   if (!xcd_item(ctl->n_next, c)) return;
   const int32_t m0 = moff[c], m1 = moff[c + 1];
@@ -2324,7 +2361,7 @@ __global__ __launch_bounds__(256) void k_link_accum_big(
     const int32_t *mem, const int32_t *moff, const float4 *pts,
     const int64_t *sx_in, int64_t *sx_out, const int32_t *big, Ctl *ctl) {
   __shared__ unsigned long long acc[3];
-  if (!ctl->any_choice) return;
+  if (!round_live(ctl)) return;
   const int32_t n_big = ctl->n_big;
   const double sF = ldexp(1.0, ctl->Fx);
   for (int32_t bi = blockIdx.x; bi < n_big; bi += gridDim.x) {
@@ -2681,37 +2718,17 @@ inline dim3 blocks_for(int64_t n, int nt = 256) {
 }
 inline dim3 xblocks_for(int64_t n) { return dim3(xcd_grid(blocks_for(n).x)); }
 
-int status_from_err(uint32_t err) {
-  if (err & kErrNonFinite) {
-    set_error("non-finite value in the input");
-    return -2;
-  }
-  if (err & kErrRange) {
-    set_error("embeddings too large for exact fixed-point sums (F < 16)");
-    return -3;
-  }
-  if (err & kErrBadIndex) {
-    set_error("neighbour index out of range");
-    return -1;
-  }
-  if (err & kErrJump) {
-    set_error("pointer jumping did not reach the roots");
-    return -5;
-  }
-  set_error("internal consistency check failed on the device (0x%x)", err);
-  return -5;
-}
 
 // One merge round on nn nodes whose rows hold ed directed entries.
+// With rest_only, only the kernels after pointer jumping are launched: the
+// second half of a round whose jumping the host completed (finish_jump).
 template <bool FIRST, int DT>
 void launch_round(const Bufs &b, const Adj &adj, int cur, int32_t n,
                   int32_t k, int32_t nn, int32_t ed, int32_t d,
                   const NodeIn &s, double lambda, int64_t smin, Ctl *ctl,
-                  hipStream_t st) {
+                  hipStream_t st, bool rest_only) {
   const int nxt = 1 - cur;
   const int32_t tcap = (int32_t)(2 * edge_bound(n, k));
-  hipLaunchKernelGGL(k_round_init, dim3(1), dim3(64), 0, st, ctl);
-  prof_begin("select", st);
   // G lanes per short row; long rows in chunks of entries, a wave each
   const LongWork lw{b.long_rows, b.lbase, b.lnch, b.litem, b.lg,
                     b.lmp,       b.lu,    b.lcnt, b.lcap};
@@ -2719,20 +2736,26 @@ void launch_round(const Bufs &b, const Adj &adj, int cur, int32_t n,
       1, std::min<int64_t>(kLongGrid, ((int64_t)ed / kLongChunk + nn) / 4 + 1)));
   const dim3 big_grid(
       (unsigned)std::max<int64_t>(1, std::min<int64_t>(kBigGrid, nn / 16)));
-  constexpr int G = FIRST ? kSelLanesFirst : kSelLanes;
-  hipLaunchKernelGGL((k_select<FIRST, DT, G>), xblocks_for((int64_t)nn * G),
-                     dim3(256), 0, st, nn, adj, s, d, lambda, smin, b.target,
-                     b.deg, lw, ctl);
-  hipLaunchKernelGGL((k_select_long<FIRST, DT>), long_grid, dim3(256), 0, st,
-                     nn, adj, s, d, lambda, smin, lw, ctl);
-  hipLaunchKernelGGL(k_select_combine, dim3(64), dim3(256), 0, st, lw,
-                     b.target, b.deg, ctl);
-  prof_end(st);
+  if (!rest_only) {
+    hipLaunchKernelGGL(k_round_init, dim3(1), dim3(64), 0, st, ctl);
+    prof_begin("select", st);
+    constexpr int G = FIRST ? kSelLanesFirst : kSelLanes;
+    hipLaunchKernelGGL((k_select<FIRST, DT, G>), xblocks_for((int64_t)nn * G),
+                       dim3(256), 0, st, nn, adj, s, d, lambda, smin,
+                       b.target, b.deg, lw, ctl);
+    hipLaunchKernelGGL((k_select_long<FIRST, DT>), long_grid, dim3(256), 0,
+                       st, nn, adj, s, d, lambda, smin, lw, ctl);
+    hipLaunchKernelGGL(k_select_combine, dim3(64), dim3(256), 0, st, lw,
+                       b.target, b.deg, ctl);
+    prof_end(st);
+  }
   prof_begin("union", st);
-  hipLaunchKernelGGL(k_hook, blocks_for(nn), dim3(256), 0, st, nn, b.target,
-                     b.parent, ctl);
-  hipLaunchKernelGGL(k_jump, blocks_for(nn), dim3(256), 0, st, nn, b.parent,
-                     ctl);
+  if (!rest_only) {
+    hipLaunchKernelGGL(k_hook, blocks_for(nn), dim3(256), 0, st, nn,
+                       b.target, b.parent, ctl);
+    hipLaunchKernelGGL(k_jump, blocks_for(nn), dim3(256), 0, st, nn,
+                       b.parent, ctl);
+  }
   device_scan(ScanRoots{b.parent, b.newid, b.cnt, nn}, nn, b.bsum,
               &ctl->n_next, st);
   hipLaunchKernelGGL(k_assign, xblocks_for(nn), dim3(256), 0, st, nn,
@@ -2806,24 +2829,52 @@ void launch_round(const Bufs &b, const Adj &adj, int cur, int32_t n,
 template <bool FIRST>
 void round_d(const Bufs &b, const Adj &adj, int cur, int32_t n, int32_t k,
              int32_t nn, int32_t ed, int32_t d, const NodeIn &s,
-             double lambda, int64_t smin, Ctl *ctl, hipStream_t st) {
+             double lambda, int64_t smin, Ctl *ctl, hipStream_t st,
+             bool rest_only = false) {
   switch (d) {
     case 8:
       launch_round<FIRST, 8>(b, adj, cur, n, k, nn, ed, d, s, lambda, smin,
-                             ctl, st);
+                             ctl, st, rest_only);
       break;
     case 16:
       launch_round<FIRST, 16>(b, adj, cur, n, k, nn, ed, d, s, lambda, smin,
-                              ctl, st);
+                              ctl, st, rest_only);
       break;
     case 32:
       launch_round<FIRST, 32>(b, adj, cur, n, k, nn, ed, d, s, lambda, smin,
-                              ctl, st);
+                              ctl, st, rest_only);
       break;
     default:
       launch_round<FIRST, 0>(b, adj, cur, n, k, nn, ed, d, s, lambda, smin,
-                             ctl, st);
+                             ctl, st, rest_only);
   }
+}
+
+// Completes the merge forest of a round whose jumping walks stopped at
+// their cap: doubling passes, four per readback, until a batch moves no
+// parent.  Each pass at least halves the depth, which is below nn, so
+// ceil(log2 nn) passes reach every root and one batch more sees no change;
+// needing more is an internal error.
+int finish_jump(const Bufs &b, int32_t nn, Ctl *ctl, Ctl *h, hipStream_t st) {
+  int lg = 0;
+  while (((int64_t)1 << lg) < (int64_t)nn) ++lg;
+  const int batches = (lg + 3) / 4 + 1;
+  for (int bt = 0; bt < batches; ++bt) {
+    hipLaunchKernelGGL(k_jump_state, dim3(1), dim3(64), 0, st, ctl, 0);
+    for (int j = 0; j < 4; ++j)
+      hipLaunchKernelGGL(k_double, blocks_for(nn), dim3(256), 0, st, nn,
+                         b.parent, ctl);
+    int rc = read_ctl(ctl, h, st);
+    if (rc) return rc;
+    if (h->err) return status_from_err(h->err);
+    if (!h->jump_changed) {
+      hipLaunchKernelGGL(k_jump_state, dim3(1), dim3(64), 0, st, ctl, 1);
+      return 0;
+    }
+  }
+  set_error("pointer jumping did not reach the roots in %d passes",
+            4 * batches);
+  return -5;
 }
 
 // The rest of the ladder in the tail kernel, then the labels (and energy)
@@ -3164,6 +3215,19 @@ int ladder_run(const LadderArgs &g, Ctl *ctl, Arena &a, hipStream_t st) {
       }
       if ((rc = read_ctl(ctl, h, st))) return rc;
       if (h->err) return status_from_err(h->err);
+      if (h->any_choice < 0) {
+        // a merge chain deeper than a jumping walk: complete the forest,
+        // then the rest of the round
+        if ((rc = finish_jump(b, nn, ctl, h, st))) return rc;
+        if (first)
+          round_d<true>(b, adj, cur, n, k, nn, ed, d, s, lambda, smin, ctl,
+                        st, true);
+        else
+          round_d<false>(b, adj, cur, n, k, nn, ed, d, s, lambda, smin, ctl,
+                         st, true);
+        if ((rc = read_ctl(ctl, h, st))) return rc;
+        if (h->err) return status_from_err(h->err);
+      }
       if (prof_on()) {
         // algorithmic bytes of the round (undirected edges of 12 bytes,
         // node statistics of S bytes: 4d fp32 in the first round, then
