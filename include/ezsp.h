@@ -20,9 +20,18 @@
  *     `ws_bytes` bytes (size from the matching *_workspace_size query;
  *     any alignment, the library aligns internally).
  *   - `stream` is a hipStream_t passed as void* (NULL = the null stream).
- *     All device work is enqueued on it.  Every entry point synchronises
- *     `stream` before it returns, so that it can report errors the device
- *     detected; outputs are complete when it returns EZSP_OK.
+ *     All device work is enqueued on it.
+ *   - ezsp_knn, ezsp_component_stats and ezsp_embed_mlp are
+ *     stream-asynchronous: they validate their arguments, enqueue their
+ *     kernels and return; their outputs are ready once `stream` reaches
+ *     that point, and their workspace must stay allocated until then.
+ *     Errors the device detects (a non-finite coordinate, a label out of
+ *     range) are kept in the call's workspace and reported by
+ *     ezsp_sync_status.  The entry points that return host values
+ *     (ezsp_partition, ezsp_partition_from_knn, ezsp_grid_subsample,
+ *     ezsp_edge_loss, ezsp_purity) synchronise `stream` before they return
+ *     and report device errors themselves; their outputs are complete when
+ *     they return EZSP_OK.
  *   - Arguments are validated on the host before anything is launched; an
  *     invalid argument returns EZSP_ERR_INVALID_ARG and touches no memory.
  *   - On any status other than EZSP_OK the outputs are unspecified.
@@ -84,7 +93,7 @@ typedef struct {
 
 size_t ezsp_knn_workspace_size(int64_t n, int32_t k);
 
-/* Exact k nearest neighbours of every point.
+/* Exact k nearest neighbours of every point (stream-asynchronous).
  *   xyz  n*3 fp32 (in)
  *   nbr  n*k int32 (out): row p lists the k points q != p with the smallest
  *        (d2(p,q), q), in increasing order, where
@@ -93,8 +102,9 @@ size_t ezsp_knn_workspace_size(int64_t n, int32_t k);
  *        the smaller index.  When n-1 < k the row ends in -1 entries.
  *   d2   n*k fp32 (out, nullable): the matching squared distances, +inf
  *        where nbr is -1.
- * Errors: INVALID_ARG (n < 1, n > 2^31 - 256, k outside 1..64, NULL pointer),
- *         NONFINITE, WORKSPACE, DEVICE. */
+ * Errors returned: INVALID_ARG (n < 1, n > 2^31 - 256, k outside 1..64, NULL
+ *         pointer), WORKSPACE, DEVICE (a launch failed).
+ * Errors through ezsp_sync_status(ws): NONFINITE, DEVICE. */
 int ezsp_knn(const float *xyz, int64_t n, int32_t k, int32_t *nbr, float *d2,
              void *ws, size_t ws_bytes, void *stream);
 
@@ -144,7 +154,8 @@ int ezsp_partition_from_knn(const int32_t *nbr, const float *emb, int64_t n,
 size_t ezsp_component_stats_workspace_size(int64_t n, int64_t n_comp,
                                            int32_t d);
 
-/* Size, mean embedding and centroid of every superpoint of a labelling.
+/* Size, mean embedding and centroid of every superpoint of a labelling
+ * (stream-asynchronous).
  *   labels    n int32 (in), each in [0, n_comp)
  *   emb       n*d fp32 (in); xyz n*3 fp32 (in, nullable)
  *   size      n_comp int64 (out)
@@ -153,8 +164,9 @@ size_t ezsp_component_stats_workspace_size(int64_t n, int64_t n_comp,
  *             (0 for an empty superpoint)
  *   centroid  n_comp*3 fp32 (out, NULL when xyz is NULL): the same for xyz
  *             with its own F
- * Errors: INVALID_ARG (also for a label outside [0, n_comp), detected on
- *         the device), NONFINITE, RANGE, WORKSPACE, DEVICE. */
+ * Errors returned: INVALID_ARG, WORKSPACE, DEVICE (a launch failed).
+ * Errors through ezsp_sync_status(ws): INVALID_ARG (a label outside
+ *         [0, n_comp)), NONFINITE, RANGE, DEVICE. */
 int ezsp_component_stats(const int32_t *labels, int64_t n, int64_t n_comp,
                          const float *emb, int32_t d, const float *xyz,
                          int64_t *size, float *emb_mean, float *centroid,
@@ -262,14 +274,22 @@ int ezsp_purity(const int32_t *labels, int64_t n, int64_t n_comp,
  *   w1   d_in*32, w2 32*32, w3 32*d_out bfloat16 bits, row k = input k
  *   b1   32, b2 32, b3 d_out fp32
  *   out  n*d_out fp32 (out), d_out in 1..32
- * d_hid must be 32.  Needs no workspace.
- * Errors: INVALID_ARG, DEVICE. */
+ * d_hid must be 32.  Needs no workspace.  Stream-asynchronous; the device
+ * detects no errors.
+ * Errors: INVALID_ARG, DEVICE (the launch failed). */
 int ezsp_embed_mlp(const uint16_t *x, int64_t n, int32_t d_in, int32_t d_hid,
                    int32_t d_out, const uint16_t *w1, const float *b1,
                    const uint16_t *w2, const float *b2, const uint16_t *w3,
                    const float *b3, float *out, void *stream);
 
 /* ---- diagnostics --------------------------------------------------------- */
+
+/* Synchronises `stream` and returns the status of the errors the device
+ * detected in the last call that used the workspace `ws` (ws_bytes as
+ * passed to that call): EZSP_OK, or the error with its detail in
+ * ezsp_last_error().  For the stream-asynchronous entry points; the others
+ * report device errors themselves. */
+int ezsp_sync_status(const void *ws, size_t ws_bytes, void *stream);
 
 /* Static text for a status code. */
 const char *ezsp_status_string(int status);

@@ -194,16 +194,18 @@ int ezsp_knn(const float *xyz, int64_t n, int32_t k, int32_t *nbr, float *d2,
   KnnWork w;
   knn_reserve(a, (int32_t)n, k, &w);
   hipLaunchKernelGGL(k_ctl_init, dim3(1), dim3(64), 0, st, ctl);
-  int rc = check_hip(knn_launch(xyz, (int32_t)n, k, ctl, w, nbr, d2, st),
-                     "knn launch");
-  if (rc) return rc;
-  Ctl *h = pinned_ctl();
-  if (!h) return fail(EZSP_ERR_DEVICE, "hipHostMalloc of the control block");
-  if ((rc = read_ctl(ctl, h, st))) return rc;
-  if (h->err & kErrNonFinite)
-    return fail(EZSP_ERR_NONFINITE, "non-finite coordinate in xyz");
-  if (h->err) return fail(EZSP_ERR_DEVICE, "internal check failed in kNN");
-  return EZSP_OK;
+  // stream-asynchronous: device-detected errors stay in the workspace's
+  // control block for ezsp_sync_status
+  return check_hip(knn_launch(xyz, (int32_t)n, k, ctl, w, nbr, d2, st),
+                   "knn launch");
+}
+
+int ezsp_sync_status(const void *ws, size_t ws_bytes, void *stream) {
+  set_error("%s", "");
+  if (!ws || ws_bytes < sizeof(Ctl) + 256)
+    return fail(EZSP_ERR_INVALID_ARG, "ws must be a call's workspace");
+  Arena a = open_ws(const_cast<void *>(ws), ws_bytes);
+  return device_status(a.take<Ctl>(1), static_cast<hipStream_t>(stream));
 }
 
 size_t ezsp_partition_workspace_size(int64_t n, int32_t d,

@@ -35,7 +35,10 @@ struct alignas(128) Stripe {
 struct Ctl {
   uint32_t err;
   int32_t F;            // fixed-point shift of the embeddings
-  int32_t any_choice;   // some node kept a merge edge this round
+  int32_t any_choice;   // some node kept a merge edge this round; -1 when
+                        // one did but pointer jumping stopped at its walk
+                        // cap (the round's later kernels then wait)
+  int32_t jump_changed; // a pointer-doubling pass moved some parent
   int32_t n_next;       // components after this round
   int32_t e_next;       // directed edges after this round (host: folded)
   int32_t slots;        // adjacency-table slots of the next round
@@ -109,6 +112,12 @@ __device__ __forceinline__ int fixshift_rule(float A, int32_t n) {
   }
   const int F = 61 - cn - ca;
   return F > 40 ? 40 : F;
+}
+
+// The kernels after Step 3 run only when some node chose and every parent
+// reached its root.
+__device__ __forceinline__ bool round_live(const Ctl *ctl) {
+  return ctl->any_choice > 0;
 }
 
 __device__ __forceinline__ void raise_err(Ctl *ctl, uint32_t bits) {

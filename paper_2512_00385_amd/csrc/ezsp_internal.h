@@ -200,6 +200,10 @@ int mlp_run(const uint16_t *x, int32_t n, int32_t d_in, int32_t d_out,
 // Shared host helpers.
 void set_error(const char *fmt, ...);
 int read_ctl(Ctl *ctl, Ctl *host, hipStream_t st);  // sync + copy back
+// ezsp_status of a set of device error bits (detail through set_error).
+int status_from_err(uint32_t err);
+// Synchronises st and returns the status of the error bits in ctl.
+int device_status(const Ctl *ctl, hipStream_t st);
 int check_hip(hipError_t e, const char *what);
 Ctl *pinned_ctl();
 __global__ void k_ctl_init(Ctl *ctl);

@@ -378,6 +378,7 @@ int prof_only(const char *name) {
 
 int prof_read(const char *name, int64_t *launches, double *ms,
               double *bytes) {
+  prof_flush();  // launches of asynchronous entry points still pending
   std::lock_guard<std::mutex> lk(g_prof_mu);
   auto it = g_totals.find(name ? name : "");
   if (it == g_totals.end()) {
@@ -411,6 +412,42 @@ int read_ctl(Ctl *ctl, Ctl *host, hipStream_t st) {
   }
   prof_flush();
   return rc;
+}
+
+int status_from_err(uint32_t err) {
+  if (err & kErrNonFinite) {
+    set_error("non-finite value in the input");
+    return -2;
+  }
+  if (err & kErrRange) {
+    set_error("values too large for exact fixed-point sums (F < 16)");
+    return -3;
+  }
+  if (err & kErrBadIndex) {
+    set_error("an index of the input is out of range");
+    return -1;
+  }
+  if (err & kErrJump) {
+    set_error("pointer jumping did not reach the roots");
+    return -5;
+  }
+  set_error("internal consistency check failed on the device (0x%x)", err);
+  return -5;
+}
+
+int device_status(const Ctl *ctl, hipStream_t st) {
+  int rc = check_hip(hipGetLastError(), "kernel launch");
+  if (rc) return rc;
+  rc = check_hip(hipStreamSynchronize(st), "hipStreamSynchronize");
+  if (rc) return rc;
+  // the stream's work is done: a plain copy of the error word into host
+  // memory (no pinned buffer, so the query allocates nothing)
+  uint32_t err = 0;
+  rc = check_hip(hipMemcpy(&err, &ctl->err, sizeof(err),
+                           hipMemcpyDeviceToHost),
+                 "hipMemcpy(error word)");
+  if (rc) return rc;
+  return err ? status_from_err(err) : 0;
 }
 
 Tree make_tree(int32_t n) {

@@ -77,11 +77,6 @@ int stats_run(const int32_t *labels, int32_t n, int32_t nc, const float *emb,
   Ctl *cx = a.take<Ctl>(1);  // shift of xyz; ctl holds the one of emb
   int64_t *Se = a.take<int64_t>((size_t)nc * d);
   int64_t *Sx = a.take<int64_t>((size_t)nc * 3);
-  Ctl *h = pinned_ctl();
-  if (!h) {
-    set_error("hipHostMalloc of the control block failed");
-    return -5;
-  }
   hipLaunchKernelGGL(k_ctl_init, dim3(1), dim3(64), 0, st, cx);
   hipLaunchKernelGGL(k_maxabs, dim3(2048), dim3(256), 0, st, emb,
                      (int64_t)n * d, ctl);
@@ -105,26 +100,9 @@ int stats_run(const int32_t *labels, int32_t n, int32_t nc, const float *emb,
                        dim3(nt), 0, st, nc, 3, size, Sx, cx, centroid);
   }
   hipLaunchKernelGGL(k_cs_merge_err, dim3(1), dim3(64), 0, st, ctl, cx);
-  int rc = read_ctl(ctl, h, st);
-  if (rc) return rc;
-  const uint32_t err = h->err;
-  if (err & kErrNonFinite) {
-    set_error("non-finite value in emb or xyz");
-    return -2;
-  }
-  if (err & kErrRange) {
-    set_error("values too large for exact fixed-point sums (F < 16)");
-    return -3;
-  }
-  if (err & kErrBadIndex) {
-    set_error("label outside [0, n_comp)");
-    return -1;
-  }
-  if (err) {
-    set_error("internal consistency check failed on the device (0x%x)", err);
-    return -5;
-  }
-  return 0;
+  // stream-asynchronous: device-detected errors stay in ctl for
+  // ezsp_sync_status
+  return check_hip(hipGetLastError(), "component statistics launch");
 }
 
 }  // namespace ezsp

@@ -37,7 +37,7 @@ ENTRY_POINTS = (
     "ezsp_grid_subsample_workspace_size", "ezsp_grid_subsample",
     "ezsp_edge_loss_workspace_size", "ezsp_edge_loss",
     "ezsp_purity_workspace_size", "ezsp_purity",
-    "ezsp_embed_mlp",
+    "ezsp_embed_mlp", "ezsp_sync_status",
 )
 
 
@@ -110,6 +110,7 @@ def load() -> ctypes.CDLL:
                                        P]),
         "ezsp_embed_mlp": (ctypes.c_int, [P, i64, i32, i32, i32, P, P, P, P,
                                           P, P, P, P]),
+        "ezsp_sync_status": (ctypes.c_int, [P, sz, P]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -195,8 +196,23 @@ def _params(k, lambdas, min_size, max_rounds, energy, link=False):
     return p, lam, ms  # keep the arrays alive with the struct
 
 
-def knn(xyz: torch.Tensor, k: int, want_d2: bool = False):
-    """Exact kNN (ezsp_knn): nbr [n, k] int32 (and d2 [n, k] fp32)."""
+class Pending:
+    """The workspace of a stream-asynchronous call, kept alive until its
+    device-detected errors have been checked (ezsp_sync_status)."""
+
+    def __init__(self, ws, nbytes, device, where):
+        self.ws, self.nbytes, self.device, self.where = ws, nbytes, device, where
+
+    def check(self):
+        """Synchronise the stream; raise EzspError for a device error."""
+        _check(load().ezsp_sync_status(_ptr(self.ws), self.nbytes,
+                                       _stream(self.device)), self.where)
+
+
+def knn(xyz: torch.Tensor, k: int, want_d2: bool = False, sync: bool = True):
+    """Exact kNN (ezsp_knn): nbr [n, k] int32 (and d2 [n, k] fp32).  With
+    sync=False the call returns right after enqueuing, with a Pending whose
+    check() reports device errors: (nbr, [d2,] pending)."""
     lib = load()
     xyz = _dev_tensor(xyz, torch.float32, "xyz", 3)
     n = xyz.shape[0]
@@ -208,7 +224,11 @@ def knn(xyz: torch.Tensor, k: int, want_d2: bool = False):
     ws = _workspace(nbytes, dev)
     _check(lib.ezsp_knn(_ptr(xyz), n, int(k), _ptr(nbr), _ptr(d2), _ptr(ws),
                         nbytes, _stream(dev)), "ezsp_knn")
-    return (nbr, d2) if want_d2 else nbr
+    pending = Pending(ws, nbytes, dev, "ezsp_knn")
+    if sync:
+        pending.check()
+        return (nbr, d2) if want_d2 else nbr
+    return ((nbr, d2) if want_d2 else (nbr,)) + (pending,)
 
 
 def partition_workspace_size(n: int, d: int, k: int, n_levels: int = 1):
@@ -298,8 +318,10 @@ def partition_from_knn(nbr: torch.Tensor, emb: torch.Tensor, lambdas,
 
 
 def component_stats(labels: torch.Tensor, n_comp: int, emb: torch.Tensor,
-                    xyz: torch.Tensor | None = None):
-    """Size, mean embedding and centroid per superpoint."""
+                    xyz: torch.Tensor | None = None, sync: bool = True):
+    """Size, mean embedding and centroid per superpoint.  With sync=False
+    the call returns right after enqueuing: (size, mean, centroid,
+    pending), pending.check() reporting device errors."""
     lib = load()
     labels = _dev_tensor(labels, torch.int32, "labels")
     emb = _dev_tensor(emb, torch.float32, "emb")
@@ -317,7 +339,11 @@ def component_stats(labels: torch.Tensor, n_comp: int, emb: torch.Tensor,
                                     d, _ptr(xyz), _ptr(size), _ptr(mean),
                                     _ptr(cen), _ptr(ws), nbytes,
                                     _stream(dev)), "ezsp_component_stats")
-    return size, mean, cen
+    pending = Pending(ws, nbytes, dev, "ezsp_component_stats")
+    if sync:
+        pending.check()
+        return size, mean, cen
+    return size, mean, cen, pending
 
 
 def grid_subsample(xyz: torch.Tensor, h: float) -> torch.Tensor:
@@ -402,7 +428,7 @@ def embed_mlp(x_bits: torch.Tensor, w1, b1, w2, b2, w3, b3) -> torch.Tensor:
     """Per-point MLP d_in -> 32 -> 32 -> d_out on the matrix cores.  x_bits
     and the weights are bfloat16 tensors (or int16 tensors of their bits) on
     the device, weights as [fan_in, fan_out]; biases fp32.  Returns
-    [n, d_out] fp32."""
+    [n, d_out] fp32, computed in stream order (the call does not wait)."""
     lib = load()
 
     def bits(t, name):

@@ -34,6 +34,12 @@ def test_exports_every_declared_symbol():
     assert set(names) == set(ezsp.ENTRY_POINTS)
 
 
+def test_sync_status_rejects_bad_workspace():
+    lib = ezsp.load()
+    assert lib.ezsp_sync_status(None, 1 << 20, None) == ezsp.ERR_INVALID_ARG
+    assert lib.ezsp_sync_status(FAKE, 16, None) == ezsp.ERR_INVALID_ARG
+
+
 def test_status_strings():
     for code in range(0, -7, -1):
         assert ezsp.status_string(code) != "unknown status"
