@@ -208,17 +208,14 @@ def _rect_min_range(x0, x1, y0, y1):
     return np.hypot(dx, dy)
 
 
-def driving_tile(seed: int = 0, n_points: int = 3_000_000) -> Scene:
-    """Driving tile, 3,000,000 points: ground heightfield (8 sinusoids,
-    wavelengths 10-50 m, 1 m peak) over 100x100 m, 200 car boxes, 300 poles
-    (r = 0.15 m), 40 facade planes; density 1/max(r, 2 m)^2 around a sensor at
-    the origin; D = 16, embedding noise 0.05; k = 10; ladder {0.05, 0.2,
-    0.8}."""
-    rng = np.random.default_rng(seed)
-    half = 50.0
+def _street(rng, half):
+    """The street scene of the driving tile: ground heightfield (8
+    sinusoids, wavelengths 10-50 m, 1 m peak) and 200 car boxes, 300 poles
+    (r = 0.15 m) and 40 facade rectangles inside [-half, half]^2, as
+    (h, objects) with objects[i] = (kind, params) for object id i + 1 (the
+    ground is object 0)."""
     h = _heightfield(rng, 8, 10.0, 50.0, 1.0)
-    objs = []  # (kind, params) ; ground is object 0
-
+    objs = []
     for _ in range(200):  # cars: ~4.5 x 1.8 x 1.5 m, +-10 %, axis-aligned
         s = np.array([4.5, 1.8, 1.5]) * rng.uniform(0.9, 1.1, 3)
         if rng.random() < 0.5:
@@ -243,6 +240,18 @@ def driving_tile(seed: int = 0, n_points: int = 3_000_000) -> Scene:
             o = np.array([c[0], c[1] - wdt / 2, z0])
             u = np.array([0, wdt, 0.])
         objs.append(("facade", o, u, np.array([0, 0, ht])))
+    return h, objs
+
+
+def driving_tile(seed: int = 0, n_points: int = 3_000_000) -> Scene:
+    """Driving tile, 3,000,000 points: ground heightfield (8 sinusoids,
+    wavelengths 10-50 m, 1 m peak) over 100x100 m, 200 car boxes, 300 poles
+    (r = 0.15 m), 40 facade planes; density 1/max(r, 2 m)^2 around a sensor at
+    the origin; D = 16, embedding noise 0.05; k = 10; ladder {0.05, 0.2,
+    0.8}."""
+    rng = np.random.default_rng(seed)
+    half = 50.0
+    h, objs = _street(rng, half)
 
     def obj_surface(ob, m):
         if ob[0] == "box":
@@ -455,16 +464,22 @@ def random_cloud(n: int, d: int, seed: int = 0, n_obj: int = 8,
 
 
 # --------------------------------------------------------------------------
-# LiDAR-sweep stand-in for the embedding MLP: 1,280,000 points of the
-# driving tile (a random subset: its points are stored shuffled), per-point
-# features [x/50, y/50, z/5, intensity, range/120, ring/63] for a sensor at
-# (0, 0, 1.8) with 64 rings between -24.8 and +2 degrees of elevation, and
-# PyTorch-Linear-style random weights U(+-1/sqrt(fan_in)) from
-# default_rng(seed).  Inputs and weights are handed over as bfloat16 bit
-# patterns (round to nearest even).
+# LiDAR sweep (the streaming workload): one revolution of a 64-beam rotating
+# sensor ray-cast against the driving tile's street scene, stored ring-major
+# (every azimuth of ring 0, then ring 1, ...), the order in which a scanning
+# sensor's points arrive once sorted by laser.  Per-point features
+# [x/50, y/50, z/5, intensity, range/120, ring/63] in the sensor frame go
+# through a random-weight MLP (PyTorch-Linear-style U(+-1/sqrt(fan_in))
+# weights from default_rng(seed)); inputs and weights are handed over as
+# bfloat16 bit patterns (round to nearest even).
 # --------------------------------------------------------------------------
 
-SWEEP_POINTS = 1_280_000
+SWEEP_RINGS = 64
+SWEEP_AZIMUTHS = 20_000
+SWEEP_ELEV_DEG = (-24.8, 2.0)   # lowest and highest beam
+SWEEP_MAX_RANGE = 120.0         # metres; farther returns are dropped
+SWEEP_SENSOR_HEIGHT = 1.8       # above the ground under the sensor
+SWEEP_STEP_X = 5.0              # sweep i has its sensor at x = 5 i
 MLP_DIMS = (6, 32, 16)
 
 
@@ -493,26 +508,222 @@ def mlp_weights(seed: int = 0, dims=MLP_DIMS):
     return tuple(out)
 
 
-def sweep_features(xyz, obj, seed: int = 0):
-    """The six per-point features of the sweep, as bfloat16 bits [n, 6]."""
+def _ground_hits(h, o, dirs, tmax):
+    """First intersection parameter of every ray o + t*dirs (unit
+    directions, [m, 3]) with the heightfield z = h(x, y), |h| <= 1, or inf.
+    The crossing lies where the ray is inside the band |z| <= 1: that part
+    is marched in steps of 0.25 m of path (the heightfield's wavelengths are
+    10 m and more) and the first sign change refined by 30 bisections."""
+    m = dirs.shape[0]
+    dz = dirs[:, 2]
+    t = np.full(m, np.inf)
+    with np.errstate(divide="ignore", invalid="ignore"):
+        ta = np.where(dz < 0, (o[2] - 1.0) / -dz,
+                      np.where(dz > 0, 0.0, 0.0))
+        tb = np.where(dz < 0, (o[2] + 1.0) / -dz,
+                      np.where(dz > 0, (1.0 - o[2]) / dz, np.inf))
+    ta = np.maximum(ta, 0.0)
+    tb = np.minimum(tb, tmax)
+    live = np.nonzero(tb > ta)[0]
+    step = 0.25
+
+    def f(idx, tt):
+        p = o[None, :] + tt[:, None] * dirs[idx]
+        return p[:, 2] - h(p[:, 0], p[:, 1])
+    lo = ta[live].copy()
+    flo = f(live, lo)
+    todo = flo > 0  # above the ground at the band entry
+    hit_lo = np.full(live.shape[0], np.nan)
+    hit_hi = np.full(live.shape[0], np.nan)
+    cur = lo.copy()
+    while todo.any():
+        idx = np.nonzero(todo)[0]
+        nxt = np.minimum(cur[idx] + step, tb[live[idx]])
+        fn = f(live[idx], nxt)
+        cross = fn <= 0
+        hit_lo[idx[cross]] = cur[idx[cross]]
+        hit_hi[idx[cross]] = nxt[cross]
+        done = cross | (nxt >= tb[live[idx]])
+        cur[idx] = nxt
+        todo[idx[done]] = False
+    ok = np.nonzero(~np.isnan(hit_lo))[0]
+    a, b = hit_lo[ok], hit_hi[ok]
+    for _ in range(30):
+        mid = 0.5 * (a + b)
+        above = f(live[ok], mid) > 0
+        a = np.where(above, mid, a)
+        b = np.where(above, b, mid)
+    t[live[ok]] = b
+    return t
+
+
+def _box_hits(lo, hi, o, dirs):
+    """Slab test: entry parameter of each ray into the box, or inf."""
+    with np.errstate(divide="ignore", invalid="ignore"):
+        inv = 1.0 / dirs
+        t1 = (lo[None, :] - o[None, :]) * inv
+        t2 = (hi[None, :] - o[None, :]) * inv
+    t1 = np.where(np.isnan(t1), -np.inf, t1)
+    t2 = np.where(np.isnan(t2), np.inf, t2)
+    tn = np.minimum(t1, t2).max(1)
+    tf = np.maximum(t1, t2).min(1)
+    return np.where((tn <= tf) & (tn > 0), tn, np.inf)
+
+
+def _pole_hits(base, ht, radius, o, dirs):
+    """Entry parameter into a vertical cylinder (side only), or inf."""
+    dx, dy = dirs[:, 0], dirs[:, 1]
+    ox, oy = o[0] - base[0], o[1] - base[1]
+    a = dx * dx + dy * dy
+    b = 2 * (ox * dx + oy * dy)
+    c = ox * ox + oy * oy - radius * radius
+    disc = b * b - 4 * a * c
+    with np.errstate(invalid="ignore", divide="ignore"):
+        t = (-b - np.sqrt(disc)) / (2 * a)
+    z = o[2] + t * dirs[:, 2]
+    ok = (disc >= 0) & (t > 0) & (z >= base[2]) & (z <= base[2] + ht)
+    return np.where(ok, t, np.inf)
+
+
+def _facade_hits(orig, u, v, o, dirs):
+    """Intersection with the vertical rectangle orig + a*u + b*v, a, b in
+    [0, 1] (u horizontal along x or y, v vertical), or inf."""
+    ax = 0 if abs(u[0]) > 0 else 1      # the axis the facade runs along
+    nx = 1 - ax                          # its normal axis
+    with np.errstate(divide="ignore", invalid="ignore"):
+        t = (orig[nx] - o[nx]) / dirs[:, nx]
+    p_a = o[ax] + t * dirs[:, ax]
+    p_z = o[2] + t * dirs[:, 2]
+    a = (p_a - orig[ax]) / u[ax]
+    ok = (t > 0) & (a >= 0) & (a <= 1) & (p_z >= orig[2]) & \
+        (p_z <= orig[2] + v[2])
+    return np.where(ok, t, np.inf)
+
+
+def _azimuth_span(xs, ys, o):
+    """Azimuth interval (radians, start and width) seen from o that covers
+    the points (xs, ys), or None when o lies inside their hull's box."""
+    ang = np.arctan2(np.asarray(ys) - o[1], np.asarray(xs) - o[0])
+    if (min(xs) <= o[0] <= max(xs)) and (min(ys) <= o[1] <= max(ys)):
+        return None
+    srt = np.sort(np.mod(ang, 2 * np.pi))
+    gaps = np.diff(np.concatenate([srt, srt[:1] + 2 * np.pi]))
+    j = int(np.argmax(gaps))  # the span is the complement of the widest gap
+    start = srt[(j + 1) % srt.shape[0]]
+    return start, 2 * np.pi - gaps[j]
+
+
+SWEEP_ROAD = 8.0     # half width of the road the sensor drives along
+SWEEP_CLEAR = 2.0    # clearance of objects around the sensor's path
+
+
+def _blocks_road(ob, xs, ys):
+    """True for a street object the sensor's road removes: a facade whose
+    footprint reaches into the road |y| < 8 m, or any object within 2 m of
+    the sensor path y = 0, x in [-2, 5 * 3] (the street scene places its
+    objects with no regard to a road)."""
+    x0, x1, y0, y1 = min(xs), max(xs), min(ys), max(ys)
+    if ob[0] == "facade" and y1 > -SWEEP_ROAD and y0 < SWEEP_ROAD:
+        return True
+    return (x1 > -SWEEP_CLEAR and x0 < 3 * SWEEP_STEP_X + SWEEP_CLEAR and
+            y1 > -SWEEP_CLEAR and y0 < SWEEP_CLEAR)
+
+
+def lidar_sweep(seed: int = 0, index: int = 0):
+    """Ray-cast sweep `index` of the street scene of seed `seed`.
+
+    64 beams at elevations linspace(-24.8, +2) degrees times 20,000
+    azimuths, from a sensor at (5 * index, 0) and 1.8 m above the ground
+    there, driving along a road on the x axis that the street's facades
+    leave free.  Each ray keeps its first hit among the ground, the cars,
+    poles and facades within 120 m; rays without one are dropped.  Returns
+    (xyz [n, 3] fp32 in the world frame, obj [n] int32, ring [n] int32,
+    rng_m [n] fp64 range, sensor [3]); points in ring-major order, each
+    with 5 mm of Gaussian position noise."""
+    rng = np.random.default_rng(seed)
+    h, objs = _street(rng, 50.0)
+    sx = SWEEP_STEP_X * index
+    o = np.array([sx, 0.0, float(h(sx, 0.0)) + SWEEP_SENSOR_HEIGHT])
+    elev = np.radians(np.linspace(*SWEEP_ELEV_DEG, SWEEP_RINGS))
+    azim = 2 * np.pi * np.arange(SWEEP_AZIMUTHS) / SWEEP_AZIMUTHS
+    ce, se = np.cos(elev), np.sin(elev)
+    dirs = np.stack([ce[:, None] * np.cos(azim)[None, :],
+                     ce[:, None] * np.sin(azim)[None, :],
+                     np.broadcast_to(se[:, None], (SWEEP_RINGS,
+                                                   SWEEP_AZIMUTHS))],
+                    -1).reshape(-1, 3)   # ring-major
+    t = _ground_hits(h, o, dirs, SWEEP_MAX_RANGE)
+    obj = np.zeros(t.shape[0], np.int32)
+    ray_az = np.tile(np.arange(SWEEP_AZIMUTHS), SWEEP_RINGS)
+    for i, ob in enumerate(objs):
+        if ob[0] == "box":
+            lo, hi = ob[1], ob[2]
+            xs, ys = [lo[0], hi[0], lo[0], hi[0]], [lo[1], lo[1], hi[1], hi[1]]
+        elif ob[0] == "pole":
+            b = ob[1]
+            xs = [b[0] - 0.15, b[0] + 0.15, b[0] - 0.15, b[0] + 0.15]
+            ys = [b[1] - 0.15, b[1] - 0.15, b[1] + 0.15, b[1] + 0.15]
+        else:
+            p0, p1 = ob[1], ob[1] + ob[2]
+            xs, ys = [p0[0], p1[0]], [p0[1], p1[1]]
+        if _blocks_road(ob, xs, ys):
+            continue
+        span = _azimuth_span(xs, ys, o)
+        if span is None:
+            continue  # the sensor stands inside: no surface seen
+        else:
+            start, width = span
+            a0 = int(np.floor(start / (2 * np.pi) * SWEEP_AZIMUTHS)) - 1
+            a1 = int(np.ceil((start + width) / (2 * np.pi) *
+                             SWEEP_AZIMUTHS)) + 1
+            cols = np.mod(np.arange(a0, a1 + 1), SWEEP_AZIMUTHS)
+            mask = np.zeros(SWEEP_AZIMUTHS, bool)
+            mask[cols] = True
+            rays = np.nonzero(mask[ray_az])[0]
+        d = dirs[rays]
+        if ob[0] == "box":
+            ti = _box_hits(ob[1], ob[2], o, d)
+        elif ob[0] == "pole":
+            ti = _pole_hits(ob[1], ob[2], 0.15, o, d)
+        else:
+            ti = _facade_hits(ob[1], ob[2], ob[3], o, d)
+        closer = ti < t[rays]
+        t[rays[closer]] = ti[closer]
+        obj[rays[closer]] = i + 1
+    hit = np.nonzero(t <= SWEEP_MAX_RANGE)[0]   # ring-major order kept
+    p = o[None, :] + t[hit, None] * dirs[hit]
+    p = p + rng.standard_normal(p.shape) * NOISE_XYZ
+    ring = (hit // SWEEP_AZIMUTHS).astype(np.int32)
+    return (np.ascontiguousarray(p, np.float32), obj[hit], ring, t[hit], o)
+
+
+def sweep_features(xyz, obj, ring, sensor, seed: int = 0):
+    """The six per-point features of a sweep in the sensor frame, as
+    bfloat16 bits [n, 6]: [x/50, y/50, z/5, intensity, range/120, ring/63],
+    intensity = U(0, 1) per object plus N(0, 0.02^2), clipped to [0, 1]."""
     rng = np.random.default_rng([seed, 6])
-    xyz = np.asarray(xyz, np.float64)
-    rel = xyz - np.array([0.0, 0.0, 1.8])
-    horiz = np.hypot(rel[:, 0], rel[:, 1])
-    rng_m = np.sqrt(horiz ** 2 + rel[:, 2] ** 2)
-    elev = np.degrees(np.arctan2(rel[:, 2], horiz))
-    ring = np.clip(np.rint((elev + 24.8) / (26.8 / 63)), 0, 63)
+    rel = np.asarray(xyz, np.float64) - np.asarray(sensor)[None, :]
+    rng_m = np.sqrt((rel ** 2).sum(1))
     n_obj = int(np.max(obj)) + 1
     inten = rng.uniform(0, 1, n_obj)[obj] + rng.normal(0, 0.02, xyz.shape[0])
-    feat = np.stack([xyz[:, 0] / 50, xyz[:, 1] / 50, xyz[:, 2] / 5,
-                     np.clip(inten, 0, 1), rng_m / 120, ring / 63], 1)
+    feat = np.stack([rel[:, 0] / 50, rel[:, 1] / 50, rel[:, 2] / 5,
+                     np.clip(inten, 0, 1), rng_m / SWEEP_MAX_RANGE,
+                     np.asarray(ring, np.float64) / (SWEEP_RINGS - 1)], 1)
     return to_bf16_bits(feat.astype(np.float32))
 
 
-def sweep(seed: int = 0):
-    """(xyz [n, 3] fp32, features [n, 6] bfloat16 bits, obj) of the sweep
-    stand-in."""
-    sc = load("driving-3m", seed)
-    xyz = np.ascontiguousarray(sc.xyz[:SWEEP_POINTS])
-    obj = np.ascontiguousarray(sc.obj[:SWEEP_POINTS])
-    return xyz, sweep_features(xyz, obj, seed), obj
+def sweep(seed: int = 0, index: int = 0, cache: bool = True):
+    """(xyz [n, 3] fp32, features [n, 6] bfloat16 bits, obj) of ray-cast
+    sweep `index`; cached on disk like the scenes."""
+    path = os.path.join(_cache_dir(), f"sweep{index}-s{seed}.npz")
+    if cache and os.path.exists(path):
+        z = np.load(path, allow_pickle=False)
+        return z["xyz"], z["feat"], z["obj"]
+    xyz, obj, ring, _, sensor = lidar_sweep(seed, index)
+    feat = sweep_features(xyz, obj, ring, sensor, seed)
+    if cache:
+        os.makedirs(_cache_dir(), exist_ok=True)
+        tmp = path + ".tmp%d.npz" % os.getpid()
+        np.savez(tmp, xyz=xyz, feat=feat, obj=obj)
+        os.replace(tmp, path)
+    return xyz, feat, obj
