@@ -32,6 +32,8 @@ import platform
 import sys
 import time
 
+import numpy as np
+
 ROOT = os.path.dirname(os.path.abspath(__file__))
 if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
@@ -60,8 +62,8 @@ CALIB_ELEMS = 1 << 28  # float32 elements of the calibration copy (1 GiB)
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=10)
-    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--split-steps", type=int, default=3,
                     help="untimed steps with every stage timed (the split "
                     "and the dominant stage)")
@@ -131,6 +133,34 @@ def measured_valu(stage, n_points, k):
                            n_points, k)
 
 
+STEP_TRAFFIC_FILE = os.path.join(ROOT, "profiles",
+                                 "partition_step.driving-3m.pmc.md")
+
+
+def measured_step_traffic(workload, n_points, k):
+    """HBM bytes of one whole step, every kernel's FETCH_SIZE and WRITE_SIZE
+    summed and scaled (committed summary), while every library source still
+    hashes as recorded there."""
+    if workload != WORKLOAD:
+        return None
+    return committed_value(STEP_TRAFFIC_FILE, "traffic_bytes_per_step",
+                           "partition_step", n_points, k)
+
+
+def cpu_model():
+    """The host CPU's model name (from /proc/cpuinfo) and logical cores."""
+    name = platform.processor() or platform.machine()
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    name = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return f"{name}, {os.cpu_count()} logical cores"
+
+
 def cpu_baseline(sc, n_sample, link=False):
     """Oracle (single-threaded C) on the whole tile, or, when n_sample is
     smaller, on the slab of the tile around x = 0 that holds n_sample points
@@ -152,19 +182,19 @@ def cpu_baseline(sc, n_sample, link=False):
     nbr, _ = oracle.knn(xyz, sc.k)
     t1 = time.perf_counter()
     lo, hi, w = oracle.graph(nbr)
-    oracle.partition_graph(emb, lo, hi, w, sc.lambdas, min_size=sc.min_size,
-                           want_energy=False, xyz=xyz,
-                           link_k=sc.k if link else 0)
+    labels, n_comp, _, _ = oracle.partition_graph(
+        emb, lo, hi, w, sc.lambdas, min_size=sc.min_size, want_energy=False,
+        xyz=xyz, link_k=sc.k if link else 0)
     t2 = time.perf_counter()
-    return {
+    whole = n_sample >= sc.n
+    return (labels if whole else None), (n_comp if whole else None), {
         "value": n_sample / (t2 - t0), "unit": "points/s", "cores": 1,
         "kind": "oracle",
         "sample": (f"{what}, k={sc.k}, ladder {list(sc.lambdas)}, "
                    f"s_min {sc.min_size}"
                    f"{', isolated nodes linked' if link else ''}; one "
                    f"thread; kNN {t1 - t0:.2f} s, graph+ladder "
-                   f"{t2 - t1:.2f} s; host {platform.processor() or 'cpu'} "
-                   f"with {os.cpu_count()} logical cores"),
+                   f"{t2 - t1:.2f} s; host {cpu_model()}"),
     }
 
 
@@ -179,16 +209,21 @@ OPS = {
                   "gradient)"),
     "purity": ("driving-3m-paper",
                "points/sec scored (superpoint majority, oracle mIoU)"),
-    "embed_mlp": ("sweep-1.28m",
+    "embed_mlp": ("lidar-sweep-64x20k",
                   "points/sec through the embedding MLP 6->32->32->16 "
                   "(bf16, matrix cores)"),
-    "sweep": ("sweep-1.28m",
+    "sweep": ("lidar-sweep-64x20k",
               "ms per sweep: embedding MLP + kNN (k=10) + merge ladder "
               "{0.05, 0.2, 0.8}"),
 }
-SWEEP_KIND = ("1,280,000 points of the synthetic driving tile as one LiDAR "
-              "sweep, features [x/50, y/50, z/5, intensity, range/120, "
-              "ring/63] in bf16, random MLP weights (seed 0)")
+SWEEP_COUNT = 3
+SWEEP_NAME = "lidar-sweep-64x20k"
+SWEEP_KIND = ("ray-cast 64-beam LiDAR sweeps (64 rings x 20,000 azimuths, "
+              "-24.8 to +2 degrees, 120 m range, ring-major order) of the "
+              "street scene from a sensor 1.8 m above the ground at x = 0, 5 "
+              "and 10 m; features [x/50, y/50, z/5, intensity, range/120, "
+              "ring/63] in the sensor frame, bf16; random MLP weights "
+              "(seed 0)")
 
 
 def bench_op(args, ezsp, scenes, np, torch):
@@ -293,45 +328,58 @@ def bench_op(args, ezsp, scenes, np, torch):
 
 
 def bench_sweep(args, ezsp, scenes, np, torch, metric):
-    """The LiDAR-sweep stand-in: the embedding MLP alone (--op embed_mlp) or
-    the whole per-sweep latency, MLP then partition (--op sweep)."""
+    """The LiDAR sweeps: the embedding MLP alone (--op embed_mlp) or the
+    whole per-sweep latency, MLP then partition (--op sweep).  Steps cycle
+    over three ray-cast sweeps (sensor at x = 0, 5 and 10 m), as a stream of
+    revolutions would arrive."""
     import oracle
     dev = torch.device("cuda:0")
-    xyz_np, feat_np, _ = scenes.sweep()
     wts = scenes.mlp_weights(0)
-    n = xyz_np.shape[0]
 
     def to_dev(a):
         a = np.ascontiguousarray(a)
         return torch.from_numpy(a.view(np.int16) if a.dtype == np.uint16
                                 else a).to(dev)
-    xyz = to_dev(xyz_np)
-    feat = to_dev(feat_np)
+    sweeps = []
+    for i in range(SWEEP_COUNT):
+        print(f"[bench] ray-casting sweep {i}", file=sys.stderr, flush=True)
+        xyz_np, feat_np, _ = scenes.sweep(0, i)
+        sweeps.append((xyz_np, feat_np, to_dev(xyz_np), to_dev(feat_np)))
     w = [to_dev(a) for a in wts]
     lambdas = [0.05, 0.2, 0.8]
-    part = ezsp.Partitioner(n, 16, 10, lambdas, device=dev) \
-        if args.op == "sweep" else None
+    sweep = args.op == "sweep"
+    parts = [ezsp.Partitioner(sw[0].shape[0], 16, 10, lambdas, device=dev)
+             for sw in sweeps] if sweep else None
+    last = {}
 
-    def step():
-        emb = ezsp.embed_mlp(feat, *w)
-        if part is not None:
-            return part(xyz, emb)
+    def step(i):
+        j = i % SWEEP_COUNT
+        emb = ezsp.embed_mlp(sweeps[j][3], *w)
+        if parts is not None:
+            labels, nc, _ = parts[j](sweeps[j][2], emb)
+            last[j] = (emb, labels, nc)
+            return labels
         return emb
-    for _ in range(args.warmup):
-        step()
+    for i in range(args.warmup):
+        step(i)
     torch.cuda.synchronize()
     stage_names = list(ezsp.STAGES) + ["embed_mlp"]
     ezsp.profile_enable(True)
     ezsp.profile_only(None)
     torch.cuda.synchronize()
+    per_step = []
     t0 = time.perf_counter()
-    for _ in range(args.steps):
-        step()
-    torch.cuda.synchronize()
+    for i in range(args.steps):
+        s0 = time.perf_counter()
+        step(i)
+        torch.cuda.synchronize()
+        per_step.append(time.perf_counter() - s0)
     t1 = time.perf_counter()
     stats = {s: ezsp.profile_read(s) for s in stage_names}
     ezsp.profile_enable(False)
-    ms_per_step = (t1 - t0) * 1e3 / args.steps
+    ms_mean = (t1 - t0) * 1e3 / args.steps
+    ms_per_step = float(np.median(per_step)) * 1e3
+    n = int(np.mean([sw[0].shape[0] for sw in sweeps]))
     dom = max(stats, key=lambda s: stats[s][1])
     launches, ms, nbytes = stats[dom]
     per_ms = ms / max(launches, 1)
@@ -340,7 +388,6 @@ def bench_sweep(args, ezsp, scenes, np, torch, metric):
     mlp_l, mlp_ms, _ = stats["embed_mlp"]
     mlp_per_ms = mlp_ms / max(mlp_l, 1)
     flops = 2.0 * n * (6 * 32 + 32 * 32 + 32 * 16)
-    sweep = args.op == "sweep"
     out = {
         "metric": metric,
         "value": round(ms_per_step, 4) if sweep
@@ -351,9 +398,12 @@ def bench_sweep(args, ezsp, scenes, np, torch, metric):
         "higher_is_better": not sweep, "scaling": "weak",
         "vs_baseline": None, "dtype": "bf16+f64" if sweep else "bf16",
         "data": "synthetic",
-        "config": {"workload": f"{args.op} on sweep-1.28m: {SWEEP_KIND}",
-                   "n_points": n, "mlp": "6->32->32->16",
+        "config": {"workload": f"{args.op} on {SWEEP_NAME}: {SWEEP_KIND}",
+                   "n_points": [int(sw[0].shape[0]) for sw in sweeps],
+                   "mlp": "6->32->32->16",
                    **({"k": 10, "lambdas": lambdas} if sweep else {})},
+        "ms_step_stats": {"median": round(ms_per_step, 4),
+                          "mean": round(ms_mean, 4)},
         "roofline": {"bound": "hbm", "kernel": dom,
                      "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s",
@@ -366,22 +416,48 @@ def bench_sweep(args, ezsp, scenes, np, torch, metric):
                 "bf16_mfma_peak_tflops": 2500.0},
         "stage_ms_per_step": {s: round(v[1] / args.steps, 4)
                               for s, v in stats.items()},
+        "parity": None,
     }
+    ok = True
     if not args.no_cpu:
         print("[bench] cpu baseline (oracle)", file=sys.stderr, flush=True)
+        xyz0, feat0 = sweeps[0][0], sweeps[0][1]
         c0 = time.perf_counter()
-        e = oracle.embed_mlp(feat_np, *wts).astype(np.float32)
-        if sweep:
-            oracle.partition(xyz_np, e, 10, lambdas, want_energy=False)
+        oracle.embed_mlp(feat0, *wts)
         c1 = time.perf_counter()
+        what = f"the MLP of sweep 0 ({xyz0.shape[0]} points)"
+        if sweep:
+            # the oracle partitions the GPU's embeddings of sweep 0 (the
+            # MLP's fp32 sums differ from the oracle's exact ones in the
+            # last bits), and its labels gate the GPU's
+            emb, labels, nc = last[0]
+            rl, rnc, _, _ = oracle.partition(xyz0, emb.cpu().numpy(), 10,
+                                             lambdas, want_energy=False)
+            same_nc = bool(np.array_equal(rnc, nc))
+            same = [bool(np.array_equal(rl[l], labels[l].cpu().numpy()))
+                    for l in range(len(lambdas))]
+            ok = same_nc and all(same)
+            out["parity"] = {"ok": ok, "n_comp": same_nc,
+                             "labels_per_level": same,
+                             "compared": "the last GPU partition of sweep 0 "
+                                         "against the oracle's partition of "
+                                         "the same embeddings"}
+            what += " and its partition (kNN, graph, ladder)"
+        c2 = time.perf_counter()
         out["cpu_baseline"] = {
-            "value": round((c1 - c0) * 1e3, 1) if sweep else n / (c1 - c0),
+            "value": round((c2 - c0) * 1e3, 1) if sweep
+            else xyz0.shape[0] / (c1 - c0),
             "unit": "ms" if sweep else "points/s", "cores": 1,
             "kind": "oracle",
-            "sample": f"the whole sweep ({n} points), one thread, "
-                      f"{c1 - c0:.2f} s",
+            "sample": f"{what}, one thread, MLP {c1 - c0:.2f} s"
+                      + (f", partition {c2 - c1:.2f} s" if sweep else "")
+                      + f"; host {cpu_model()}",
         }
     print(json.dumps(out), flush=True)
+    if not ok:
+        print("[bench] PARITY FAILURE: GPU labels differ from the oracle's",
+              file=sys.stderr, flush=True)
+        sys.exit(3)
 
 
 def main():
@@ -422,13 +498,19 @@ def main():
     torch.cuda.synchronize()
     split_stats = {s: ezsp.profile_read(s) for s in ezsp.STAGES}
     dom = max(split_stats, key=lambda s: split_stats[s][1])
-    # timed steps: HIP events around the dominant stage only
+    # timed steps: HIP events around the dominant stage only.  Every step
+    # ends in a host synchronisation (the library reads back the superpoint
+    # counts), so each one is timed on its own as well.
     ezsp.profile_enable(True)
     ezsp.profile_only(dom)
     torch.cuda.synchronize()
+    per_step = []
     t0 = time.perf_counter()
     for _ in range(args.steps):
+        s0 = time.perf_counter()
         labels, n_comp, _ = part(xyz, emb)
+        torch.cuda.synchronize()
+        per_step.append(time.perf_counter() - s0)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     stages = {}
@@ -437,10 +519,12 @@ def main():
         stages[s] = {"launches": launches, "ms": ms, "bytes": nbytes}
     ezsp.profile_enable(False)
     ezsp.profile_only(None)
-    ms_per_step = (t1 - t0) * 1e3 / args.steps
+    gpu_labels = labels.cpu().numpy()  # the last timed step's labels
+    ms_mean = (t1 - t0) * 1e3 / args.steps
+    ms_per_step = float(np.median(per_step)) * 1e3
     value = sc.n / (ms_per_step / 1e3)
-    print(f"[bench] {ms_per_step:.3f} ms/step, n_comp {n_comp.tolist()}",
-          file=sys.stderr, flush=True)
+    print(f"[bench] {ms_per_step:.3f} ms/step (median; mean {ms_mean:.3f}), "
+          f"n_comp {n_comp.tolist()}", file=sys.stderr, flush=True)
 
     d = stages[dom]
     per_launch_ms = d["ms"] / max(d["launches"], 1)
@@ -450,24 +534,33 @@ def main():
     alg_total = sum(v["bytes"] for v in stages.values()) / args.steps
     traffic = measured_traffic(dom, sc.n, sc.k)
     valu = measured_valu(dom, sc.n, sc.k)
-    issue = None
+    hbm = {"achieved": round(achieved, 2), "peak": HBM_PEAK_GBS,
+           "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 5),
+           "traffic": traffic}
+    roofline = {"bound": "hbm", "kernel": dom, **hbm}
     if valu is not None and per_launch_ms > 0:
+        # an issue-bound kernel: its VALU instruction rate against the issue
+        # peak is the binding roof; the HBM figures stay alongside
         rate = valu / (per_launch_ms * 1e-3)
-        issue = {"valu_wave_instr_per_launch": valu,
-                 "achieved": round(rate, 1), "peak": VALU_ISSUE_PEAK,
-                 "unit": "wave-instr/s",
-                 "frac": round(rate / VALU_ISSUE_PEAK, 4)}
-    roofline = {
-        "bound": "hbm", "kernel": dom, "achieved": round(achieved, 2),
-        "peak": HBM_PEAK_GBS, "unit": "GB/s",
-        "frac": round(achieved / HBM_PEAK_GBS, 5), "traffic": traffic,
+        if rate / VALU_ISSUE_PEAK > achieved / HBM_PEAK_GBS:
+            roofline = {"bound": "alu", "kernel": dom,
+                        "achieved": round(rate, 1), "peak": VALU_ISSUE_PEAK,
+                        "unit": "wave-instr/s",
+                        "frac": round(rate / VALU_ISSUE_PEAK, 4),
+                        "traffic": traffic,
+                        "valu_wave_instr_per_launch": valu, "hbm": hbm}
+    roofline.update({
         "launch_ms": round(per_launch_ms, 5),
         "alg_bytes_per_launch": per_launch_bytes,
         "step_alg_bytes": alg_total,
         "step_alg_frac": round(alg_total / (ms_per_step * 1e-3) / 1e9 /
                                HBM_PEAK_GBS, 5),
-        "issue": issue,
-    }
+    })
+    step_traffic = measured_step_traffic(sc.name, sc.n, sc.k)
+    if step_traffic is not None:
+        roofline["step_traffic"] = step_traffic
+        roofline["step_traffic_frac"] = round(
+            step_traffic / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 5)
     split = {s: round(v[1] / max(args.split_steps, 1), 4)
              for s, v in split_stats.items()}
     if args.calib_copy:
@@ -479,8 +572,13 @@ def main():
         torch.cuda.synchronize()
         del src, dst
 
+    if sc.name == WORKLOAD:
+        metric = "points/sec partitioned (kNN+merge) on 3M-pt tile"
+    else:
+        metric = (f"points/sec partitioned (kNN+merge) on the {sc.n}-point "
+                  f"{sc.name} workload")
     out = {
-        "metric": "points/sec partitioned (kNN+merge) on 3M-pt tile",
+        "metric": metric,
         "value": round(value, 1), "unit": "points/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup,
         "ms_per_step": round(ms_per_step, 4), "higher_is_better": True,
@@ -496,15 +594,36 @@ def main():
                    "n_points": sc.n, "d": sc.d, "k": sc.k,
                    "lambdas": sc.lambdas, "min_size": sc.min_size,
                    "link_isolated": bool(args.link)},
+        "ms_step_stats": {"median": round(ms_per_step, 4),
+                          "mean": round(ms_mean, 4),
+                          "min": round(min(per_step) * 1e3, 4),
+                          "max": round(max(per_step) * 1e3, 4)},
         "roofline": roofline,
         "stage_ms_per_step": split,
         "n_comp": [int(x) for x in n_comp],
+        "parity": None,
     }
+    ok = True
     if not args.no_cpu:
         print("[bench] cpu baseline (oracle)", file=sys.stderr, flush=True)
-        out["cpu_baseline"] = cpu_baseline(sc, min(args.cpu_points, sc.n),
-                                           args.link)
+        ref_labels, ref_nc, out["cpu_baseline"] = cpu_baseline(
+            sc, min(args.cpu_points, sc.n), args.link)
+        if ref_labels is not None:
+            # the last timed step against the oracle's own run on the tile
+            same_nc = bool(np.array_equal(ref_nc, n_comp))
+            same = [bool(np.array_equal(ref_labels[l], gpu_labels[l]))
+                    for l in range(ref_labels.shape[0])]
+            ok = same_nc and all(same)
+            out["parity"] = {
+                "ok": ok, "n_comp": same_nc, "labels_per_level": same,
+                "compared": "every label of every level of the last timed "
+                            "step against the CPU oracle's partition of the "
+                            "same tile"}
     print(json.dumps(out), flush=True)
+    if not ok:
+        print("[bench] PARITY FAILURE: GPU labels differ from the oracle's",
+              file=sys.stderr, flush=True)
+        sys.exit(3)
 
 
 if __name__ == "__main__":
