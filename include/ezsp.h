@@ -282,13 +282,31 @@ int ezsp_embed_mlp(const uint16_t *x, int64_t n, int32_t d_in, int32_t d_hid,
                    const uint16_t *w2, const float *b2, const uint16_t *w3,
                    const float *b3, float *out, void *stream);
 
+/* ---- kNN without a workspace --------------------------------------------- */
+
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation): ezsp_knn
+ * with its scratch in a static device array of 160 MiB instead of a caller
+ * workspace.  Same arguments, results and errors as ezsp_knn (bit-identical
+ * outputs); stream-asynchronous, device-detected errors through
+ * ezsp_sync_status(NULL, 0, stream).  The call allocates nothing: no
+ * hipMalloc, hipFree or other allocating routine.  Sizes whose
+ * ezsp_knn_workspace_size(n, k) exceeds 160 MiB (about 1.5M points at
+ * k = 10) return EZSP_ERR_INVALID_ARG.  Each GPU the library runs on holds
+ * its own copy of the array until the process ends; every call on one GPU
+ * uses that copy, so calls that overlap on one GPU (other streams, other
+ * threads) race. */
+int ezsp_knn_noalloc(const float *xyz, int64_t n, int32_t k, int32_t *nbr,
+                     float *d2, void *stream);
+
 /* ---- diagnostics --------------------------------------------------------- */
 
 /* Synchronises `stream` and returns the status of the errors the device
  * detected in the last call that used the workspace `ws` (ws_bytes as
- * passed to that call): EZSP_OK, or the error with its detail in
- * ezsp_last_error().  For the stream-asynchronous entry points; the others
- * report device errors themselves. */
+ * passed to that call), or, with ws = NULL and ws_bytes = 0, in the last
+ * ezsp_knn_noalloc call on the current device: EZSP_OK, or the error with
+ * its detail in ezsp_last_error().  For the stream-asynchronous entry
+ * points; the others report device errors themselves. */
 int ezsp_sync_status(const void *ws, size_t ws_bytes, void *stream);
 
 /* Static text for a status code. */

@@ -19,7 +19,8 @@ LIB = os.path.join(HERE, "libezsp.so")
 BUILD = os.path.join(HERE, "_build")
 SOURCES = ["ezsp_prims.hip", "ezsp_knn.hip", "ezsp_merge.hip",
            "ezsp_stats.hip", "ezsp_grid.hip", "ezsp_loss.hip",
-           "ezsp_purity.hip", "ezsp_mlp.hip", "ezsp_api.hip"]
+           "ezsp_purity.hip", "ezsp_mlp.hip", "ezsp_noalloc.hip",
+           "ezsp_api.hip"]
 ARCH = os.environ.get("EZSP_OFFLOAD_ARCH", "gfx950")
 
 CFLAGS = [

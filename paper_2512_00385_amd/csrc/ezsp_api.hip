@@ -202,6 +202,13 @@ int ezsp_knn(const float *xyz, int64_t n, int32_t k, int32_t *nbr, float *d2,
 
 int ezsp_sync_status(const void *ws, size_t ws_bytes, void *stream) {
   set_error("%s", "");
+  if (!ws && ws_bytes == 0) {  // the static scratch of ezsp_knn_noalloc
+    void *p = nullptr;
+    const int rc = noalloc_scratch(&p);
+    if (rc) return rc;
+    ws = p;
+    ws_bytes = kNoallocScratchBytes;
+  }
   if (!ws || ws_bytes < sizeof(Ctl) + 256)
     return fail(EZSP_ERR_INVALID_ARG, "ws must be a call's workspace");
   Arena a = open_ws(const_cast<void *>(ws), ws_bytes);

@@ -204,6 +204,10 @@ int read_ctl(Ctl *ctl, Ctl *host, hipStream_t st);  // sync + copy back
 int status_from_err(uint32_t err);
 // Synchronises st and returns the status of the error bits in ctl.
 int device_status(const Ctl *ctl, hipStream_t st);
+// The static scratch of ezsp_knn_noalloc: its size, and its address on the
+// current device (looked up once per device); returns an ezsp_status.
+constexpr size_t kNoallocScratchBytes = (size_t)160 << 20;
+int noalloc_scratch(void **ptr);
 int check_hip(hipError_t e, const char *what);
 Ctl *pinned_ctl();
 __global__ void k_ctl_init(Ctl *ctl);

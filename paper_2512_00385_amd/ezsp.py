@@ -37,7 +37,7 @@ ENTRY_POINTS = (
     "ezsp_grid_subsample_workspace_size", "ezsp_grid_subsample",
     "ezsp_edge_loss_workspace_size", "ezsp_edge_loss",
     "ezsp_purity_workspace_size", "ezsp_purity",
-    "ezsp_embed_mlp", "ezsp_sync_status",
+    "ezsp_embed_mlp", "ezsp_sync_status", "ezsp_knn_noalloc",
 )
 
 
@@ -111,6 +111,7 @@ def load() -> ctypes.CDLL:
         "ezsp_embed_mlp": (ctypes.c_int, [P, i64, i32, i32, i32, P, P, P, P,
                                           P, P, P, P]),
         "ezsp_sync_status": (ctypes.c_int, [P, sz, P]),
+        "ezsp_knn_noalloc": (ctypes.c_int, [P, i64, i32, P, P, P]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)

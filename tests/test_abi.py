@@ -34,6 +34,17 @@ def test_exports_every_declared_symbol():
     assert set(names) == set(ezsp.ENTRY_POINTS)
 
 
+def test_knn_noalloc_rejects_sizes_beyond_its_scratch():
+    lib = ezsp.load()
+    assert lib.ezsp_knn_noalloc(FAKE, 3_000_000, 10, FAKE, None, None) == \
+        ezsp.ERR_INVALID_ARG
+    assert "static scratch" in ezsp.last_error()
+    assert lib.ezsp_knn_noalloc(FAKE, 0, 10, FAKE, None, None) == \
+        ezsp.ERR_INVALID_ARG
+    assert lib.ezsp_knn_noalloc(None, 100, 10, FAKE, None, None) == \
+        ezsp.ERR_INVALID_ARG
+
+
 def test_sync_status_rejects_bad_workspace():
     lib = ezsp.load()
     assert lib.ezsp_sync_status(None, 1 << 20, None) == ezsp.ERR_INVALID_ARG
