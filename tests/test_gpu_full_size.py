@@ -1,0 +1,129 @@
+"""Whole workloads compared with values the oracle computed once, on the CPU,
+by tests/golden/make_full_size.py (it calls only oracle/ and the seeded
+scene generators): the kNN tables of the room, driving and aerial tiles,
+and the partitions of the 10M-point aerial tile (the benchmark ladder, and
+the paper's settings with and without prepare_graph's linking), which take
+the oracle minutes.  Hashes of the int32 outputs must match exactly; the
+energy within 1e-9 relative.  A smaller crop of the aerial tile, with as
+many rounds per level, is compared with the oracle run in the test."""
+import hashlib
+import json
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2512_00385_amd import ezsp, scenes
+
+pytestmark = pytest.mark.gpu
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+GOLDEN = os.path.join(HERE, "golden", "full_size.json")
+ENERGY_RTOL = 1e-9
+
+
+@pytest.fixture(scope="module", autouse=True)
+def gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    ezsp.load()
+    yield
+
+
+@pytest.fixture(scope="module")
+def golden():
+    with open(GOLDEN) as fh:
+        return json.load(fh)
+
+
+@pytest.fixture(params=["tail", "no-tail"])
+def tail_mode(request, monkeypatch):
+    if request.param == "no-tail":
+        monkeypatch.setenv("EZSP_TAIL_NODES", "0")
+    else:
+        monkeypatch.delenv("EZSP_TAIL_NODES", raising=False)
+    return request.param
+
+
+def sha(a) -> str:
+    return hashlib.sha256(np.ascontiguousarray(a).tobytes()).hexdigest()
+
+
+def dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+@pytest.mark.parametrize("name", ["room-1m", "driving-3m", "aerial-10m"])
+def test_knn_full_table(name, golden):
+    g = golden[f"knn:{name}"]
+    sc = scenes.load(name)
+    assert sc.digest() == g["scene"]
+    nbr, d2 = ezsp.knn(dev(sc.xyz), sc.k, want_d2=True)
+    nbr, d2 = nbr.cpu().numpy(), d2.cpu().numpy()
+    for r, row in g["rows"].items():
+        assert nbr[int(r)].tolist() == row, r
+    assert sha(nbr.astype("<i4")) == g["nbr_sha256"]
+    assert sha(d2.astype("<f4")) == g["d2_sha256"]
+
+
+@pytest.mark.parametrize("case", ["partition:aerial-10m",
+                                  "partition:aerial-10m-paper",
+                                  "partition:aerial-10m-paper+link"])
+def test_aerial_partition(case, golden, tail_mode):
+    """The aerial tile in the benchmark's launch configuration (a reused
+    Partitioner workspace), every level's labels by hash, then the
+    energy."""
+    g = golden[case]
+    if g["link"] and tail_mode == "no-tail":
+        pytest.skip("linking always runs without the tail kernel")
+    sc = scenes.load(case.split(":")[1].split("+")[0])
+    assert sc.digest() == g["scene"]
+    xyz, emb = dev(sc.xyz), dev(sc.emb)
+    part = ezsp.Partitioner(sc.n, sc.d, sc.k, sc.lambdas, sc.min_size,
+                            device=torch.device("cuda:0"), link=g["link"])
+    labels, nc, _ = part(xyz, emb)
+    assert nc.tolist() == g["n_comp"]
+    labels = labels.cpu().numpy()
+    for l in range(len(sc.lambdas)):
+        assert sha(labels[l].astype("<i4")) == g["labels_sha256"][l], l
+    del part
+    _, _, en = ezsp.partition(xyz, emb, sc.k, sc.lambdas, sc.min_size,
+                              energy=True, link=g["link"])
+    np.testing.assert_allclose(en, g["energy"], rtol=ENERGY_RTOL, atol=0)
+
+
+def aerial_crop(n_keep=1_200_000):
+    """The points of the aerial tile inside a square around its centre, in
+    the tile's own (shuffled) order, with their embeddings."""
+    sc = scenes.load("aerial-10m")
+    c = sc.xyz[:, :2] - np.float32(250.0)
+    half = np.sqrt(n_keep / sc.n) * 250.0
+    keep = np.nonzero((np.abs(c) < half).all(1))[0]
+    return sc, np.ascontiguousarray(sc.xyz[keep]), \
+        np.ascontiguousarray(sc.emb[keep])
+
+
+_CROP = {}
+
+
+def test_aerial_crop_many_rounds(tail_mode):
+    """A 1.2M-point crop of the aerial tile: the oracle's round log shows
+    dozens of level-0 rounds (a few percent of the nodes merge per round,
+    the merged-flag skip of selection active throughout); every label of
+    every level, the counts and the energy against the oracle."""
+    if not _CROP:
+        sc, xyz, emb = aerial_crop()
+        _CROP["v"] = (sc, xyz, emb, oracle.partition(xyz, emb, sc.k,
+                                                     sc.lambdas,
+                                                     want_log=True))
+    sc, xyz, emb, (rl, rnc, ren, log) = _CROP["v"]
+    assert sum(1 for r in log if r["level"] == 0) >= 50
+    labels, nc, en = ezsp.partition(dev(xyz), dev(emb), sc.k, sc.lambdas,
+                                    energy=True)
+    assert np.array_equal(nc, rnc), (nc, rnc)
+    labels = labels.cpu().numpy()
+    for l in range(len(sc.lambdas)):
+        assert np.array_equal(labels[l], rl[l]), l
+    np.testing.assert_allclose(en, ren, rtol=ENERGY_RTOL, atol=0)
