@@ -39,6 +39,20 @@ struct Ctl {
                         // one did but pointer jumping stopped at its walk
                         // cap (the round's later kernels then wait)
   int32_t jump_changed; // a pointer-doubling pass moved some parent
+  // incremental rounds (stable node ids within a level)
+  int32_t n_roots;      // components formed by a merge this round
+  int32_t n_fix;        // unmerged rows that listed a merged node
+  int32_t n_work;       // nodes of the next round's worklist
+  int32_t n_dead;       // nodes merged into another this round
+  int32_t n_live;       // live nodes after compaction
+  int32_t win_total;    // slots of this round's rebuilt windows
+  int32_t n_members;    // contributors that are members of a root
+  int32_t n_contrib;    // rows that go into rebuilt windows
+  int32_t n_owners;     // rows rebuilt into new windows
+  int32_t chunk_total;  // wavefront chunks of the contributors' rows
+  int32_t n_lfill;      // chunks of the long contributor rows
+  long long span_live;  // slots of the live rows (their windows' lengths)
+  long long work_slots; // slots of the worklist rows selection scanned
   int32_t n_next;       // components after this round
   int32_t e_next;       // directed edges after this round (host: folded)
   int32_t slots;        // adjacency-table slots of the next round

@@ -539,17 +539,22 @@ struct LongWork {
 // take every G-th entry of the row (shorter dependent chains per lane than
 // a thread per row, and a wave waits for its longest rows only G-fold
 // shortened), then the group combines its candidates.
-template <bool FIRST, int DT, int G>
+// With a worklist (WL, incremental rounds), group i takes node work[i] of
+// the first n_work; otherwise group v takes node v of the nn.
+template <bool FIRST, int DT, int G, bool WL = false>
 __global__ __launch_bounds__(256) void k_select(
     int32_t nn, Adj a, NodeIn s, int32_t d, double lambda, int64_t smin,
     int32_t *__restrict__ target, int32_t *__restrict__ deg, LongWork lw,
-    Ctl *ctl) {
+    const int32_t *__restrict__ work, int32_t n_work, Ctl *ctl) {
   const int32_t tid = xcd_tid();
-  const int32_t v = tid / G;
+  const int32_t item = tid / G;
   const int lg = tid & (G - 1);
-  const int32_t span = v < nn ? row_span<FIRST>(a, v) : 0;
-  const bool live = v < nn && span <= kLongRow;
-  if (v < nn && !live && lg == 0) {  // listed with its chunks
+  const int32_t n_items = WL ? n_work : nn;
+  const int32_t v = item < n_items ? (WL ? work[item] : item) : nn;
+  const bool in = v < nn;
+  const int32_t span = in ? row_span<FIRST>(a, v) : 0;
+  const bool live = in && span <= kLongRow;
+  if (in && !live && lg == 0) {  // listed with its chunks
     const int32_t nch = (span + kLongChunk - 1) / kLongChunk;
     const int32_t slot = atomicAdd(&ctl->n_long, 1);
     const int32_t base = atomicAdd(&ctl->n_lchunk, nch);
@@ -1402,16 +1407,17 @@ __global__ __launch_bounds__(256) void k_clear_big(
   }
 }
 
-// Adds weight w of the edge A -> B to A's window; true for a new slot.
+// Adds weight w of the edge A -> B to A's window (slots base + base64 ..
+// + cap); true for a new slot.
 __device__ __forceinline__ bool table_add(uint64_t *tbl, int32_t base,
                                           int32_t cap, int32_t B, int32_t w,
-                                          Ctl *ctl) {
+                                          Ctl *ctl, int64_t base64 = 0) {
   uint32_t h = ((uint32_t)B * 2654435761u) % (uint32_t)cap;
   const unsigned long long mine =
       ((unsigned long long)(uint32_t)B << 32) | (uint32_t)w;
   for (int32_t probe = 0; probe < cap; ++probe) {
     unsigned long long *slot =
-        reinterpret_cast<unsigned long long *>(tbl + base + h);
+        reinterpret_cast<unsigned long long *>(tbl + base64 + base + h);
     unsigned long long cur = __atomic_load_n(slot, __ATOMIC_RELAXED);
     if (cur == kEmpty) {
       cur = atomicCAS(slot, kEmpty, mine);
@@ -2589,6 +2595,666 @@ __global__ __launch_bounds__(256) void k_cut_e0(int32_t n, Adj a0,
               (unsigned long long)acc);
 }
 
+// ---------------------------------------------------------------------------
+// Incremental rounds.  In a level whose rounds merge few nodes (the aerial
+// tile merges 2-13 % of its nodes per round over dozens of rounds), node ids
+// stay fixed from one round to the next instead of being renumbered: a
+// component formed by a merge keeps the id of its root and its other
+// members' ids die.  A round then touches only
+//   - its worklist: the nodes formed by a merge in the last round and their
+//     neighbours, the only nodes whose gains changed (every other node had
+//     no candidate in the last round, since a node with one merges, and its
+//     gains are the same now);
+//   - the merged components: their sums (exact int64, added with atomics,
+//     so the order does not matter) and their rows, rebuilt into fresh
+//     windows past the end of the table (open addressing at load <= 1/2,
+//     then compacted);
+//   - the unmerged rows that listed a merged node: relabelled, and their
+//     parallel entries summed, in place.
+// rep[m] records the root a dead node merged into.  Compaction (at the level
+// end, before the tail, or when the table fills) renumbers the live nodes,
+// rewrites their rows and composes the point map through rep.  Marks hold
+// stamps (a round counter), so nothing is cleared between rounds.  The
+// decisions are those of the renumbering rounds: the same sums, means,
+// rows and weights, only under other ids (and the tie rule uses minpt).
+// ---------------------------------------------------------------------------
+// Slot of a list append made by the lanes of a wave with `take` set: one
+// atomic on the counter per wave (millions of appends to one counter
+// would serialise at the memory side).  Every lane of the wave must call
+// it; returns -1 for the lanes that do not append.
+__device__ __forceinline__ int32_t wave_slot(bool take, int32_t *counter) {
+  const uint64_t m = __ballot(take);
+  if (!m) return -1;
+  const int lane = threadIdx.x & (kWave - 1);
+  const int leader = __builtin_ctzll(m);
+  int32_t base = 0;
+  if (lane == leader) base = atomicAdd(counter, __popcll(m));
+  base = __shfl(base, leader, kWave);
+  return take ? base + __popcll(m & ((1ull << lane) - 1)) : -1;
+}
+
+__global__ __launch_bounds__(256) void k_incr_init(
+    int32_t nn, int32_t *target, int32_t *parent, int32_t *rep, int32_t *rcap,
+    int32_t *rmark, int32_t *fixmark, int32_t *wmark, long long span,
+    Ctl *ctl) {
+  const int32_t v = blockIdx.x * blockDim.x + threadIdx.x;
+  if (v == 0) {
+    ctl->n_work = 0;
+    ctl->span_live = span;
+  }
+  if (v >= nn) return;
+  target[v] = -1;
+  parent[v] = v;
+  rep[v] = v;
+  rcap[v] = 0;
+  rmark[v] = -1;
+  fixmark[v] = -1;
+  wmark[v] = -1;
+}
+
+// First worklist after a renumbering round: the nodes formed by a merge and
+// their neighbours (the nodes selection would evaluate).
+__global__ __launch_bounds__(256) void k_build_work(
+    int32_t nn, Adj a, const uint8_t *__restrict__ merged,
+    int32_t *__restrict__ work, int32_t *__restrict__ cnt, Ctl *ctl) {
+  const int32_t v = xcd_tid();
+  bool take = false;
+  if (v < nn) {
+    take = merged[v] != 0;
+    int32_t k = 0;
+    for_row<false>(a, v, 0, 1, [&](int32_t u, int32_t) {
+      ++k;
+      if ((uint32_t)u < (uint32_t)nn && merged[u]) take = true;
+    });
+    cnt[v] = k;  // entries of the row (its span may hold empty slots)
+  }
+  const uint64_t m = __ballot(take);
+  if (!m) return;
+  const int lane = threadIdx.x & (kWave - 1);
+  int32_t base = 0;
+  if (lane == __builtin_ctzll(m)) base = atomicAdd(&ctl->n_work, __popcll(m));
+  base = __shfl(base, __builtin_ctzll(m), kWave);
+  if (take) work[base + __popcll(m & ((1ull << lane) - 1))] = v;
+}
+
+__global__ void k_incr_round_init(Ctl *ctl) {
+  if (threadIdx.x == 0 && blockIdx.x == 0) {
+    ctl->n_roots = 0;
+    ctl->n_fix = 0;
+    ctl->n_work = 0;
+    ctl->n_dead = 0;
+    ctl->win_total = 0;
+    ctl->n_members = 0;
+    ctl->n_contrib = 0;
+    ctl->n_owners = 0;
+    ctl->chunk_total = 0;
+    ctl->n_lfill = 0;
+  }
+}
+
+// Step 3 on the worklist (every other node keeps parent = itself and
+// target = -1): hook, then the capped jumping walk of k_jump.
+__global__ __launch_bounds__(256) void k_hook_w(int32_t n_work,
+                                                const int32_t *work,
+                                                const int32_t *target,
+                                                int32_t *parent, int32_t nn,
+                                                Ctl *ctl) {
+  const int32_t i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n_work) return;
+  const int32_t v = work[i];
+  if ((uint32_t)v >= (uint32_t)nn) {
+    raise_err(ctl, kErrInternal);
+    return;
+  }
+  const int32_t t = target[v];
+  int32_t p = v;
+  if (t >= 0) {
+    if (t >= nn) {
+      raise_err(ctl, kErrInternal);
+    } else {
+      const int32_t tt = target[t];
+      p = (tt == v && v < t) ? v : t;
+    }
+  }
+  parent[v] = p;
+}
+
+__global__ __launch_bounds__(256) void k_jump_w(int32_t n_work,
+                                                const int32_t *work,
+                                                int32_t *parent, int32_t nn,
+                                                Ctl *ctl) {
+  const int32_t i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n_work) return;
+  const int32_t v = work[i];
+  int32_t p = parent[v];
+  int it = 0;
+  for (; it < kJumpWalk; ++it) {
+    if ((uint32_t)p >= (uint32_t)nn) {
+      raise_err(ctl, kErrInternal);
+      p = v;
+      break;
+    }
+    const int32_t pp = __atomic_load_n(&parent[p], __ATOMIC_RELAXED);
+    if (pp == p) break;
+    p = pp;
+  }
+  __atomic_store_n(&parent[v], p, __ATOMIC_RELAXED);
+  if (it == kJumpWalk) __atomic_store_n(&ctl->any_choice, -1, __ATOMIC_RELAXED);
+}
+
+// Step 4 statistics of the merged components: every member adds its size,
+// smallest point, entry count and exact sums into its root and records the
+// root in rep; it enters the contributor list (its row goes into its
+// root's new row); each root enters the root list once.  A block first
+// combines its members' values per root in LDS (a component absorbing
+// thousands of nodes in one round would otherwise serialise on its root's
+// addresses), then adds each root's share with one atomic per value.
+constexpr int kMergeSlots = 256;  // = block size: room for every key
+template <int DT>
+__global__ __launch_bounds__(256) void k_incr_merge(
+    int32_t n_work, const int32_t *__restrict__ work,
+    const int32_t *__restrict__ parent, int32_t *size, int64_t *S,
+    int32_t *minpt, const int32_t *__restrict__ wl,
+    const int32_t *__restrict__ cnt, int32_t *rep, int32_t *rmark,
+    int32_t *roots, int32_t *rcap, int32_t *cy, int32_t *cY, int32_t d,
+    int32_t stamp, Ctl *ctl) {
+  constexpr int SD = DT > 0 ? DT : 1;
+  __shared__ int32_t h_key[kMergeSlots], h_size[kMergeSlots],
+      h_min[kMergeSlots], h_cnt[kMergeSlots];
+  __shared__ unsigned long long h_S[kMergeSlots * SD];
+  if (!round_live(ctl)) return;
+  const int t = threadIdx.x;
+  h_key[t] = -1;
+  h_size[t] = 0;
+  h_min[t] = INT32_MAX;
+  h_cnt[t] = 0;
+  if constexpr (DT > 0)
+    for (int q = 0; q < DT; ++q) h_S[q * kMergeSlots + t] = 0ull;
+  __syncthreads();
+  const int32_t i = blockIdx.x * blockDim.x + t;
+  int32_t v = -1, r = -1;
+  if (i < n_work) {
+    v = work[i];
+    r = parent[v];
+  }
+  const bool member = v >= 0 && r != v;
+  long long gone = 0;
+  if (member) {
+    uint32_t h = ((uint32_t)r * 2654435761u) % kMergeSlots;
+    for (;;) {  // at most one key per thread: a slot is always found
+      const int32_t k = atomicCAS(&h_key[h], -1, r);
+      if (k == -1 || k == r) break;
+      h = (h + 1) % kMergeSlots;
+    }
+    atomicAdd(&h_size[h], size[v]);
+    atomicMin(&h_min[h], minpt[v]);
+    atomicAdd(&h_cnt[h], cnt[v]);
+    if constexpr (DT > 0) {
+      const longlong2 *p = reinterpret_cast<const longlong2 *>(S + (int64_t)v * DT);
+#pragma unroll
+      for (int q = 0; q < DT / 2; ++q) {
+        const longlong2 x = p[q];
+        atomicAdd(&h_S[(2 * q) * kMergeSlots + h], (unsigned long long)x.x);
+        atomicAdd(&h_S[(2 * q + 1) * kMergeSlots + h], (unsigned long long)x.y);
+      }
+    } else {
+      for (int32_t q = 0; q < d; ++q)
+        atomicAdd(reinterpret_cast<unsigned long long *>(&S[(int64_t)r * d + q]),
+                  (unsigned long long)S[(int64_t)v * d + q]);
+    }
+    rep[v] = r;
+    gone = wl[v];
+  }
+  const int32_t c = wave_slot(member, &ctl->n_contrib);
+  if (c >= 0) {
+    cy[c] = v;
+    cY[c] = r;
+  }
+  const int32_t dead = wave_sum(member ? 1 : 0);
+  gone = wave_sum(gone);
+  if ((t & (kWave - 1)) == 0 && dead) {
+    atomicAdd(&ctl->n_dead, dead);
+    atomicAdd(reinterpret_cast<unsigned long long *>(&ctl->span_live),
+              (unsigned long long)(-gone));
+  }
+  __syncthreads();
+  // flush: one thread per slot
+  const int32_t R = h_key[t];
+  bool fresh = false;
+  if (R >= 0) {
+    atomicAdd(&size[R], h_size[t]);
+    atomicMin(&minpt[R], h_min[t]);
+    atomicAdd(&rcap[R], h_cnt[t]);
+    if constexpr (DT > 0)
+      for (int q = 0; q < DT; ++q)
+        atomicAdd(reinterpret_cast<unsigned long long *>(&S[(int64_t)R * DT + q]),
+                  h_S[q * kMergeSlots + t]);
+    fresh = atomicExch(&rmark[R], stamp) != stamp;
+  }
+  const int32_t o = wave_slot(fresh, &ctl->n_roots);
+  if (o >= 0) roots[o] = R;
+}
+
+// Per root: its new means, the capacity of its new window (twice the
+// entries of its own row and its members'), its place in the owner list
+// (roots first), and itself as a contributor and on the next worklist.
+__global__ __launch_bounds__(256) void k_incr_roots(
+    const int32_t *__restrict__ roots, const int32_t *__restrict__ size,
+    const int64_t *__restrict__ S, double *mu, const int32_t *__restrict__ wl,
+    const int32_t *__restrict__ cnt, int32_t *rcap, int32_t *ocap,
+    int32_t *rpos, int32_t *cy, int32_t *cY, int32_t *wmark, int32_t d,
+    int32_t stamp, Ctl *ctl) {
+  if (!round_live(ctl)) return;
+  const int32_t nr = ctl->n_roots;
+  const int32_t nm = ctl->n_members;  // members' contributor entries
+  const double sIF = ldexp(1.0, -ctl->F);
+  long long gone = 0;
+  const int lane = threadIdx.x & (kWave - 1);
+  for (int32_t i0 = blockIdx.x * blockDim.x + (threadIdx.x - lane); i0 < nr;
+       i0 += gridDim.x * blockDim.x) {  // wave-uniform: wave_slot below
+    const int32_t i = i0 + lane;
+    if (i >= nr) continue;
+    const int32_t r = roots[i];
+    wmark[r] = stamp;  // on the next worklist
+    const int64_t ent = (int64_t)rcap[r] + cnt[r];
+    rcap[r] = 0;
+    gone += wl[r];
+    // the host keeps top + 2 * (live slots) within the table, so a window
+    // fits; the clamp only keeps a corrupt count from wrapping
+    ocap[i] = (int32_t)std::min<int64_t>(std::max<int64_t>(2 * ent, 1),
+                                         INT32_MAX / 2);
+    rpos[r] = i;
+    cy[nm + i] = r;
+    cY[nm + i] = r;
+    const double dsz = (double)size[r];
+    for (int32_t q = 0; q < d; ++q) {
+      const double qv = (double)S[(int64_t)r * d + q] / dsz;
+      mu[(int64_t)r * d + q] = qv * sIF;
+    }
+  }
+  gone = wave_sum(gone);
+  if ((threadIdx.x & (kWave - 1)) == 0 && gone)
+    atomicAdd(reinterpret_cast<unsigned long long *>(&ctl->span_live),
+              (unsigned long long)(-gone));
+}
+
+// Counts fixed between the kernels of a round: the members' contributor
+// entries, then the owners (roots, then long rebuilt rows) and all
+// contributors.
+__global__ void k_incr_counts(Ctl *ctl, int stage) {
+  if (threadIdx.x != 0 || blockIdx.x != 0) return;
+  if (stage == 0) {
+    ctl->n_members = ctl->n_contrib;
+  } else if (stage == 1) {
+    ctl->n_contrib = ctl->n_members + ctl->n_roots;
+    ctl->n_owners = ctl->n_roots;
+  }
+}
+
+// Rows to fix, kIncrLanes lanes per member (from the contributor list):
+// every unmerged live node the member lists is flagged (its entry for the
+// member now belongs to the member's root).
+constexpr int kIncrLanes = 8;
+__global__ __launch_bounds__(256) void k_incr_mark(
+    const int32_t *__restrict__ cy, const int32_t *__restrict__ parent,
+    const int32_t *__restrict__ rmark, Adj a, int32_t *fixmark, int32_t nn,
+    int32_t stamp, Ctl *ctl) {
+  if (!round_live(ctl)) return;
+  const int32_t nm = ctl->n_members;
+  const int32_t tid = blockIdx.x * blockDim.x + threadIdx.x;
+  const int lg = tid & (kIncrLanes - 1);
+  for (int32_t i = tid / kIncrLanes; i < nm;
+       i += gridDim.x * blockDim.x / kIncrLanes) {
+    for_row<false>(a, cy[i], lg, kIncrLanes, [&](int32_t u, int32_t) {
+      if ((uint32_t)u >= (uint32_t)nn) {
+        raise_err(ctl, kErrInternal);
+        return;
+      }
+      if (parent[u] == u && rmark[u] != stamp) fixmark[u] = stamp;
+    });
+  }
+}
+
+// A pass over all nodes: each flagged row to fix either goes to the owner
+// list (rows longer than kFixInPlace slots are rebuilt like a root's, with
+// themselves as the one contributor) or is fixed in place: every entry
+// whose relabelled neighbour X (its root) was formed this round is, at the
+// first entry with that X, replaced by (X, the summed weights of all of
+// them), and emptied at the others.  Entries are taken in order, so an
+// earlier entry already rewritten still carries its X (a root is its own
+// parent).
+constexpr int32_t kFixInPlace = 64;
+__global__ __launch_bounds__(256) void k_incr_fixpass(
+    int32_t nn, const int32_t *__restrict__ fixmark,
+    const int32_t *__restrict__ parent, const int32_t *__restrict__ rmark,
+    const int32_t *__restrict__ ws, const int32_t *__restrict__ wl,
+    uint64_t *tbl, int32_t *cnt, int32_t *owners, int32_t *ocap,
+    int32_t *rpos, int32_t *cy, int32_t *cY, int32_t stamp, Ctl *ctl) {
+  if (!round_live(ctl)) return;
+  const int32_t v = xcd_tid();
+  const bool fix = v < nn && fixmark[v] == stamp;
+  const bool rebuild = fix && wl[v] > kFixInPlace;
+  const int32_t o = wave_slot(rebuild, &ctl->n_owners);
+  const int32_t c = wave_slot(rebuild, &ctl->n_contrib);
+  long long gone = 0;
+  if (rebuild) {
+    owners[o] = v;
+    ocap[o] = (int32_t)std::min<int64_t>(
+        std::max<int64_t>(2 * (int64_t)cnt[v], 1), INT32_MAX / 2);
+    rpos[v] = o;
+    cy[c] = v;
+    cY[c] = v;
+    gone = wl[v];
+  } else if (fix) {
+    uint64_t *row = tbl + ws[v];
+    const int32_t len = wl[v];
+    auto label = [&](uint64_t e) {
+      const int32_t y = (int32_t)(e >> 32);
+      return (uint32_t)y < (uint32_t)nn ? parent[y] : -1;
+    };
+    int32_t emptied = 0;
+    for (int32_t j = 0; j < len; ++j) {
+      const uint64_t e = row[j];
+      if (e == kEmpty) continue;
+      const int32_t X = label(e);
+      if (X < 0) {
+        raise_err(ctl, kErrInternal);
+        continue;
+      }
+      if (rmark[X] != stamp) continue;  // not a merged component
+      bool first = true;
+      for (int32_t i = 0; i < j && first; ++i) {
+        const uint64_t q = row[i];
+        if (q != kEmpty && label(q) == X) first = false;
+      }
+      if (!first) {
+        row[j] = kEmpty;
+        ++emptied;
+        continue;
+      }
+      uint32_t w = (uint32_t)e;
+      for (int32_t i = j + 1; i < len; ++i) {
+        const uint64_t q = row[i];
+        if (q != kEmpty && label(q) == X) w += (uint32_t)q;
+      }
+      row[j] = ((uint64_t)(uint32_t)X << 32) | w;
+    }
+    if (emptied) cnt[v] -= emptied;
+  }
+  gone = wave_sum(gone);
+  if ((threadIdx.x & (kWave - 1)) == 0 && gone)
+    atomicAdd(reinterpret_cast<unsigned long long *>(&ctl->span_live),
+              (unsigned long long)(-gone));
+}
+
+// The owners' new windows start at `top`, past every live window; each
+// owner's entry count restarts at 0 for the fill to count.
+__global__ __launch_bounds__(256) void k_incr_clear(
+    const int32_t *__restrict__ owners, const int32_t *__restrict__ obase,
+    const int32_t *__restrict__ ocap, uint64_t *tbl, int32_t *cnt,
+    int64_t top, int64_t tcap, Ctl *ctl) {
+  if (!round_live(ctl)) return;
+  const int32_t no = ctl->n_owners;
+  for (int32_t o = blockIdx.x; o < no; o += gridDim.x) {
+    const int64_t base = top + obase[o];
+    const int32_t cp = ocap[o];
+    if (base + cp > tcap) {
+      raise_err(ctl, kErrInternal);
+      continue;
+    }
+    if (threadIdx.x == 0) cnt[owners[o]] = 0;
+    for (int32_t t = threadIdx.x; t < cp; t += blockDim.x)
+      tbl[base + t] = kEmpty;
+  }
+}
+
+// Contraction into the owners' new windows: every entry of a contributor's
+// row, relabelled to its root, is added to its owner's window (edges inside
+// the owner's component are dropped, parallel edges add their weights);
+// new slots are counted, and a root's neighbours are flagged for the next
+// worklist.  kIncrLanes lanes per contributor; rows longer than kLongFill
+// slots are listed in chunks of kLongFill for k_incr_fill_long.
+constexpr int32_t kLongFill = 1024;
+__device__ __forceinline__ int32_t incr_add(
+    uint64_t e, int32_t Y, bool root, const int32_t *__restrict__ parent,
+    uint64_t *tbl, int64_t base, int32_t cp, int32_t *wmark, int32_t nn,
+    int32_t stamp, Ctl *ctl) {
+  if (e == kEmpty) return 0;
+  const int32_t u = (int32_t)(e >> 32);
+  if ((uint32_t)u >= (uint32_t)nn) {
+    raise_err(ctl, kErrInternal);
+    return 0;
+  }
+  const int32_t U = parent[u];
+  if (U == Y) return 0;
+  if (!table_add(tbl, 0, cp, U, (int32_t)(uint32_t)e, ctl, base)) return 0;
+  if (root) wmark[U] = stamp;
+  return 1;
+}
+
+__global__ __launch_bounds__(256) void k_incr_fill(
+    const int32_t *__restrict__ cy, const int32_t *__restrict__ cY,
+    const int32_t *__restrict__ parent, const int32_t *__restrict__ rmark,
+    const int32_t *__restrict__ rpos, const int32_t *__restrict__ obase,
+    const int32_t *__restrict__ ocap, Adj a, uint64_t *tbl, int32_t *cnt,
+    int32_t *wmark, int32_t *lch_i, int32_t *lch_j, int32_t lch_cap,
+    int64_t top, int64_t tcap, int32_t nn, int32_t stamp, Ctl *ctl) {
+  if (!round_live(ctl)) return;
+  const int32_t nc = ctl->n_contrib;
+  const int32_t tid = blockIdx.x * blockDim.x + threadIdx.x;
+  const int lg = tid & (kIncrLanes - 1);
+  for (int32_t i = tid / kIncrLanes; i < nc;
+       i += gridDim.x * blockDim.x / kIncrLanes) {
+    const int32_t y = cy[i], Y = cY[i];
+    const int32_t o = rpos[Y];
+    const int64_t base = top + obase[o];
+    const int32_t cp = ocap[o];
+    if (base + cp > tcap) continue;  // k_incr_clear raised the error
+    const int32_t span = a.wl[y];
+    if (span > kLongFill) {
+      if (lg == 0) {
+        const int32_t nch = (span + kLongFill - 1) / kLongFill;
+        const int32_t c0 = atomicAdd(&ctl->n_lfill, nch);
+        if (c0 + nch > lch_cap) {
+          raise_err(ctl, kErrInternal);
+        } else {
+          for (int32_t q = 0; q < nch; ++q) {
+            lch_i[c0 + q] = i;
+            lch_j[c0 + q] = q * kLongFill;
+          }
+        }
+      }
+      continue;
+    }
+    const bool root = rmark[Y] == stamp;
+    const uint64_t *row = a.tbl + a.ws[y];
+    int32_t added = 0;
+    for (int32_t j = lg; j < span; j += kIncrLanes)
+      added += incr_add(row[j], Y, root, parent, tbl, base, cp, wmark, nn,
+                        stamp, ctl);
+    if (added) atomicAdd(&cnt[Y], added);
+  }
+}
+
+// The chunks of the long contributor rows, a wave each.
+__global__ __launch_bounds__(256) void k_incr_fill_long(
+    const int32_t *__restrict__ cy, const int32_t *__restrict__ cY,
+    const int32_t *__restrict__ parent, const int32_t *__restrict__ rmark,
+    const int32_t *__restrict__ rpos, const int32_t *__restrict__ obase,
+    const int32_t *__restrict__ ocap, Adj a, uint64_t *tbl, int32_t *cnt,
+    int32_t *wmark, const int32_t *__restrict__ lch_i,
+    const int32_t *__restrict__ lch_j, int64_t top, int32_t nn,
+    int32_t stamp, Ctl *ctl) {
+  if (!round_live(ctl)) return;
+  const int32_t nch = ctl->n_lfill;
+  const int lane = threadIdx.x & (kWave - 1);
+  const int32_t wave0 = (int32_t)(blockIdx.x * (blockDim.x / kWave) +
+                                  threadIdx.x / kWave);
+  const int32_t nwaves = (int32_t)(gridDim.x * (blockDim.x / kWave));
+  for (int32_t c = wave0; c < nch; c += nwaves) {
+    const int32_t i = lch_i[c];
+    const int32_t y = cy[i], Y = cY[i];
+    const int32_t o = rpos[Y];
+    const int64_t base = top + obase[o];
+    const int32_t cp = ocap[o];
+    const bool root = rmark[Y] == stamp;
+    const uint64_t *row = a.tbl + a.ws[y];
+    const int32_t j1 = min(a.wl[y], lch_j[c] + kLongFill);
+    int32_t added = 0;
+    for (int32_t j = lch_j[c] + lane; j < j1; j += kWave)
+      added += incr_add(row[j], Y, root, parent, tbl, base, cp, wmark, nn,
+                        stamp, ctl);
+    added = wave_sum(added);
+    if (lane == 0 && added) atomicAdd(&cnt[Y], added);
+  }
+}
+
+// The owners' rows are their new windows (empty slots included).
+__global__ __launch_bounds__(256) void k_incr_owners(
+    const int32_t *__restrict__ owners, const int32_t *__restrict__ obase,
+    const int32_t *__restrict__ ocap, int32_t *ws, int32_t *wl, int64_t top,
+    Ctl *ctl) {
+  if (!round_live(ctl)) return;
+  const int32_t no = ctl->n_owners;
+  long long added = 0;
+  for (int32_t o = blockIdx.x * blockDim.x + threadIdx.x; o < no;
+       o += gridDim.x * blockDim.x) {
+    const int32_t Y = owners[o];
+    ws[Y] = (int32_t)(top + obase[o]);
+    wl[Y] = ocap[o];
+    added += ocap[o];
+  }
+  added = wave_sum(added);
+  if ((threadIdx.x & (kWave - 1)) == 0 && added)
+    atomicAdd(reinterpret_cast<unsigned long long *>(&ctl->span_live),
+              (unsigned long long)added);
+}
+
+// The next worklist: every node flagged with this round's stamp (the roots
+// and their neighbours), in id order within each wave.
+__global__ __launch_bounds__(256) void k_incr_nextwork(
+    int32_t nn, const int32_t *__restrict__ wmark, int32_t *work_next,
+    int32_t stamp, Ctl *ctl) {
+  if (!round_live(ctl)) return;
+  const int32_t v = xcd_tid();
+  const int32_t slot = wave_slot(v < nn && wmark[v] == stamp, &ctl->n_work);
+  if (slot >= 0) work_next[slot] = v;
+}
+
+// The worklist's nodes back to target = -1 and parent = themselves.
+__global__ __launch_bounds__(256) void k_incr_cleanup(
+    int32_t n_work, const int32_t *__restrict__ work, int32_t *target,
+    int32_t *parent, Ctl *ctl) {
+  if (!round_live(ctl)) return;
+  const int32_t i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n_work) return;
+  const int32_t v = work[i];
+  target[v] = -1;
+  parent[v] = v;
+}
+
+// Compaction: live nodes (rep[v] == v once rep is resolved to roots)
+// numbered in id order.
+struct ScanLive {
+  const int32_t *rep;
+  int32_t *newid;
+  int32_t nn;
+  __device__ int32_t value(int32_t v) const {
+    return (v < nn && rep[v] == v) ? 1 : 0;
+  }
+  __device__ void emit(int32_t v, int32_t excl, int32_t val) const {
+    if (val) newid[v] = excl;
+  }
+};
+
+// One pointer-doubling pass over rep (dead nodes' chains to their roots).
+__global__ __launch_bounds__(256) void k_rep_double(int32_t nn, int32_t *rep,
+                                                    Ctl *ctl) {
+  const int32_t v = blockIdx.x * blockDim.x + threadIdx.x;
+  if (v >= nn) return;
+  const int32_t p = rep[v];
+  if ((uint32_t)p >= (uint32_t)nn) {
+    raise_err(ctl, kErrInternal);
+    return;
+  }
+  const int32_t pp = rep[p];
+  if (pp != p) {
+    rep[v] = pp;
+    ctl->jump_changed = 1;
+  }
+}
+
+// Node state of the live nodes under their new ids (means recomputed from
+// the sums, bit for bit as the statistics compute them), the entry count
+// of their rows, and the merged flag of the last round's roots.
+__global__ __launch_bounds__(256) void k_compact_nodes(
+    int32_t nn, const int32_t *__restrict__ rep,
+    const int32_t *__restrict__ newid, NodeIn s, int32_t *size_o,
+    int32_t *minpt_o, int64_t *S_o, double *mu, Adj a, int32_t *cnt,
+    const int32_t *__restrict__ rmark, int32_t last_stamp, uint8_t *merged,
+    int32_t d, Ctl *ctl) {
+  const int32_t v = xcd_tid();
+  if (v >= nn || rep[v] != v) return;
+  const int32_t c = newid[v];
+  size_o[c] = s.size[v];
+  minpt_o[c] = s.minpt[v];
+  for (int32_t q = 0; q < d; ++q)
+    S_o[(int64_t)c * d + q] = s.S[(int64_t)v * d + q];
+  int32_t k = 0;
+  for_row<false>(a, v, 0, 1, [&](int32_t, int32_t) { ++k; });
+  cnt[c] = k;
+  merged[c] = rmark[v] == last_stamp ? 1 : 0;
+}
+
+// Means of the compacted nodes (a second pass: the old means of other
+// nodes may sit where a new one goes).
+__global__ __launch_bounds__(256) void k_compact_mu(int32_t nl,
+                                                    const int32_t *size,
+                                                    const int64_t *S,
+                                                    double *mu, int32_t d,
+                                                    Ctl *ctl) {
+  const int32_t t = blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= nl * d) return;
+  const double sIF = ldexp(1.0, -ctl->F);
+  const double qv = (double)S[t] / (double)size[t / d];
+  mu[t] = qv * sIF;
+}
+
+// Rows of the live nodes, their entries relabelled, packed into the other
+// table buffer from the offsets of the scan.
+__global__ __launch_bounds__(256) void k_compact_rows(
+    int32_t nn, const int32_t *__restrict__ rep,
+    const int32_t *__restrict__ newid, Adj a, const int32_t *__restrict__ ws_o,
+    int32_t *wl_o, uint64_t *tbl_o, Ctl *ctl) {
+  const int32_t v = xcd_tid();
+  if (v >= nn || rep[v] != v) return;
+  const int32_t c = newid[v];
+  uint64_t *out = tbl_o + ws_o[c];
+  int32_t k = 0;
+  for_row<false>(a, v, 0, 1, [&](int32_t u, int32_t w) {
+    if ((uint32_t)u >= (uint32_t)nn || rep[u] != u) {
+      raise_err(ctl, kErrInternal);
+      return;
+    }
+    out[k++] = ((uint64_t)(uint32_t)newid[u] << 32) | (uint32_t)w;
+  });
+  wl_o[c] = k;
+}
+
+// The point map through the dead nodes' roots and the new ids.
+__global__ __launch_bounds__(256) void k_compose_rep(
+    int32_t n, int32_t nn, int32_t *M, const int32_t *__restrict__ rep,
+    const int32_t *__restrict__ newid, Ctl *ctl) {
+  const int32_t i = xcd_tid();
+  if (i >= n) return;
+  const int32_t c = M[i];
+  if ((uint32_t)c >= (uint32_t)nn) {
+    raise_err(ctl, kErrInternal);
+    return;
+  }
+  M[i] = newid[rep[c]];
+}
+
 struct Bufs {
   float *emb_int;
   int32_t *nbr_clean;                   // sanitised caller table
@@ -2608,6 +3274,14 @@ struct Bufs {
   int32_t qcap;     // entries of cstart
   int32_t *M, *mark, *lrank;
   uint8_t *merged;  // per node: formed by a merge in the last round
+  // incremental rounds
+  int32_t *work[2];  // this round's worklist, the next one
+  int32_t *rep, *rcap, *rmark, *fixmark, *wmark, *roots, *rcapl, *rbase,
+      *rpos, *fixl;
+  int32_t *ecnt;      // entries of every row
+  int32_t *cy, *cY;   // contributor rows and their owners
+  int32_t *lch_i, *lch_j;  // chunks of long contributor rows
+  int32_t lch_cap;
   int32_t nt;  // nodes the tail can start from
   double *tgain;    // per-slot gains in the tail
   int32_t *trow[2]; // per-slot rows in the tail
@@ -2674,6 +3348,24 @@ void carve(Arena &a, int32_t n, int32_t d, int32_t k, bool link, Bufs *b) {
   b->cstart = a.take<int32_t>(b->qcap);
   b->M = a.take<int32_t>(n1);
   b->merged = a.take<uint8_t>(n1);
+  b->work[0] = a.take<int32_t>(n1);
+  b->work[1] = a.take<int32_t>(n1);
+  b->rep = a.take<int32_t>(n1);
+  b->rcap = a.take<int32_t>(n1);
+  b->rmark = a.take<int32_t>(n1);
+  b->fixmark = a.take<int32_t>(n1);
+  b->wmark = a.take<int32_t>(n1);
+  b->roots = a.take<int32_t>(n1);
+  b->rcapl = a.take<int32_t>(n1 + 1);
+  b->rbase = a.take<int32_t>(n1 + 1);
+  b->rpos = a.take<int32_t>(n1);
+  b->fixl = a.take<int32_t>(n1);
+  b->ecnt = a.take<int32_t>(n1);
+  b->cy = a.take<int32_t>(n1);
+  b->cY = a.take<int32_t>(n1);
+  b->lch_cap = (int32_t)(n1 + 2 * ed / kLongFill + 64);
+  b->lch_i = a.take<int32_t>(b->lch_cap);
+  b->lch_j = a.take<int32_t>(b->lch_cap);
   b->mark = a.take<int32_t>(n1);
   b->lrank = a.take<int32_t>(n1);
   b->nt = std::min<int32_t>(n, kTailNodes);
@@ -2742,7 +3434,7 @@ void launch_round(const Bufs &b, const Adj &adj, int cur, int32_t n,
     constexpr int G = FIRST ? kSelLanesFirst : kSelLanes;
     hipLaunchKernelGGL((k_select<FIRST, DT, G>), xblocks_for((int64_t)nn * G),
                        dim3(256), 0, st, nn, adj, s, d, lambda, smin,
-                       b.target, b.deg, lw, ctl);
+                       b.target, b.deg, lw, (const int32_t *)nullptr, 0, ctl);
     hipLaunchKernelGGL((k_select_long<FIRST, DT>), long_grid, dim3(256), 0,
                        st, nn, adj, s, d, lambda, smin, lw, ctl);
     hipLaunchKernelGGL(k_select_combine, dim3(64), dim3(256), 0, st, lw,
@@ -2875,6 +3567,250 @@ int finish_jump(const Bufs &b, int32_t nn, Ctl *ctl, Ctl *h, hipStream_t st) {
   set_error("pointer jumping did not reach the roots in %d passes",
             4 * batches);
   return -5;
+}
+
+// ---- incremental rounds: host side --------------------------------------
+struct IncrState {
+  bool on = false;
+  int32_t n_work = 0;     // nodes of the current worklist
+  int wc = 0;             // buffer of the current worklist
+  int32_t stamp = 0;      // this round's mark value
+  int64_t top = 0;        // table slots in use (windows lie below)
+  int64_t span_live = 0;  // slots of the live rows (an upper bound)
+  int32_t n_live = 0;     // live nodes
+};
+
+// A level switches to incremental rounds when a round kept more than this
+// share of its nodes, on graphs of at least kIncrMinNodes nodes.
+constexpr double kIncrKeep = 0.8;
+constexpr int32_t kIncrMinNodes = 1 << 15;
+constexpr int kIncrFlatBlocks = 4096;  // grid of the chunk-flattened kernels
+
+// Starts incremental rounds on the nn nodes of the current table (its
+// windows end at slot `slots`): identity forest, no marks, and the first
+// worklist from the merged flags of the renumbering round just done.
+int incr_enter(const Bufs &b, const Adj &adj, int32_t nn, int64_t slots,
+               IncrState &is, Ctl *ctl, Ctl *h, hipStream_t st) {
+  hipLaunchKernelGGL(k_incr_init, blocks_for(nn), dim3(256), 0, st, nn,
+                     b.target, b.parent, b.rep, b.rcap, b.rmark, b.fixmark,
+                     b.wmark, (long long)slots, ctl);
+  hipLaunchKernelGGL(k_build_work, xblocks_for(nn), dim3(256), 0, st, nn, adj,
+                     (const uint8_t *)b.merged, b.work[0], b.ecnt, ctl);
+  int rc = read_ctl(ctl, h, st);
+  if (rc) return rc;
+  if (h->err) return status_from_err(h->err);
+  is.on = true;
+  is.n_work = h->n_work;
+  is.wc = 0;
+  is.stamp = 0;
+  is.top = slots;
+  is.span_live = slots;
+  is.n_live = nn;
+  return 0;
+}
+
+// One incremental round on the worklist (rest_only: the kernels after
+// pointer jumping, as in launch_round).
+template <int DT>
+void incr_round(const Bufs &b, const Adj &adj, int cur, int32_t n, int32_t k,
+                int32_t nn, int32_t d, double lambda, int64_t smin,
+                const IncrState &is, Ctl *ctl, hipStream_t st,
+                bool rest_only) {
+  const int32_t nw = is.n_work;
+  const int32_t *work = b.work[is.wc];
+  int32_t *work_next = b.work[1 - is.wc];
+  const int64_t tcap = 2 * edge_bound(n, k);
+  const int32_t stamp = is.stamp;
+  const int nblk = (int)std::max<int64_t>(1, std::min<int64_t>(4096, (nw + 255) / 256));
+  if (!rest_only) {
+    hipLaunchKernelGGL(k_round_init, dim3(1), dim3(64), 0, st, ctl);
+    hipLaunchKernelGGL(k_incr_round_init, dim3(1), dim3(64), 0, st, ctl);
+    prof_begin("select", st);
+    const LongWork lw{b.long_rows, b.lbase, b.lnch, b.litem, b.lg,
+                      b.lmp,       b.lu,    b.lcnt, b.lcap};
+    const dim3 long_grid((unsigned)std::max<int64_t>(
+        1, std::min<int64_t>(kLongGrid,
+                             (is.span_live / kLongChunk + nw) / 4 + 1)));
+    NodeIn s;
+    s.size = b.size[cur];
+    s.S = b.S[cur];
+    s.mu = b.mu;
+    s.minpt = b.minpt[cur];
+    s.emb = nullptr;
+    s.perm = nullptr;
+    s.merged = nullptr;  // every worklist node is evaluated
+    constexpr int G = kSelLanes;
+    hipLaunchKernelGGL((k_select<false, DT, G, true>),
+                       xblocks_for((int64_t)nw * G), dim3(256), 0, st, nn,
+                       adj, s, d, lambda, smin, b.target, b.deg, lw, work, nw,
+                       ctl);
+    hipLaunchKernelGGL((k_select_long<false, DT>), long_grid, dim3(256), 0,
+                       st, nn, adj, s, d, lambda, smin, lw, ctl);
+    hipLaunchKernelGGL(k_select_combine, dim3(64), dim3(256), 0, st, lw,
+                       b.target, b.deg, ctl);
+    prof_end(st);
+    prof_begin("union", st);
+    hipLaunchKernelGGL(k_hook_w, blocks_for(nw), dim3(256), 0, st, nw, work,
+                       (const int32_t *)b.target, b.parent, nn, ctl);
+    hipLaunchKernelGGL(k_jump_w, blocks_for(nw), dim3(256), 0, st, nw, work,
+                       b.parent, nn, ctl);
+    prof_end(st);
+  }
+  prof_begin("stats", st);
+  hipLaunchKernelGGL(k_incr_merge<DT>, blocks_for(nw), dim3(256), 0, st, nw,
+                     work,
+                     (const int32_t *)b.parent, b.size[cur], b.S[cur],
+                     b.minpt[cur], (const int32_t *)b.wl[cur],
+                     (const int32_t *)b.ecnt, b.rep, b.rmark, b.roots, b.rcap,
+                     b.cy, b.cY, d, stamp, ctl);
+  hipLaunchKernelGGL(k_incr_counts, dim3(1), dim3(64), 0, st, ctl, 0);
+  hipLaunchKernelGGL(k_incr_roots, dim3(nblk), dim3(256), 0, st,
+                     (const int32_t *)b.roots, (const int32_t *)b.size[cur],
+                     (const int64_t *)b.S[cur], b.mu,
+                     (const int32_t *)b.wl[cur], (const int32_t *)b.ecnt, b.rcap,
+                     b.rcapl, b.rpos, b.cy, b.cY, b.wmark, d, stamp, ctl);
+  hipLaunchKernelGGL(k_incr_counts, dim3(1), dim3(64), 0, st, ctl, 1);
+  prof_end(st);
+  prof_begin("contract", st);
+  const dim3 flat(kIncrFlatBlocks);
+  // rows to fix: flagged from the members' rows, then fixed in place or
+  // listed as owners by a pass over all nodes
+  hipLaunchKernelGGL(k_incr_mark, flat, dim3(256), 0, st,
+                     (const int32_t *)b.cy, (const int32_t *)b.parent,
+                     (const int32_t *)b.rmark, adj, b.fixmark, nn, stamp, ctl);
+  hipLaunchKernelGGL(k_incr_fixpass, xblocks_for(nn), dim3(256), 0, st, nn,
+                     (const int32_t *)b.fixmark, (const int32_t *)b.parent,
+                     (const int32_t *)b.rmark, (const int32_t *)b.ws[cur],
+                     (const int32_t *)b.wl[cur], b.tbl[cur], b.ecnt, b.roots,
+                     b.rcapl, b.rpos, b.cy, b.cY, stamp, ctl);
+  // windows of the owners (roots, long rows to fix), then every
+  // contributor's row into its owner's window
+  device_scan(ScanArray{b.rcapl, b.rbase, nn, &ctl->n_owners}, nn + 1, b.bsum,
+              &ctl->win_total, st);
+  hipLaunchKernelGGL(k_incr_clear, flat, dim3(256), 0, st,
+                     (const int32_t *)b.roots, (const int32_t *)b.rbase,
+                     (const int32_t *)b.rcapl, b.tbl[cur], b.ecnt,
+                     (int64_t)is.top, tcap, ctl);
+  hipLaunchKernelGGL(k_incr_fill, flat, dim3(256), 0, st,
+                     (const int32_t *)b.cy, (const int32_t *)b.cY,
+                     (const int32_t *)b.parent, (const int32_t *)b.rmark,
+                     (const int32_t *)b.rpos, (const int32_t *)b.rbase,
+                     (const int32_t *)b.rcapl, adj, b.tbl[cur], b.ecnt,
+                     b.wmark, b.lch_i, b.lch_j, b.lch_cap, (int64_t)is.top,
+                     tcap, nn, stamp, ctl);
+  hipLaunchKernelGGL(k_incr_fill_long, flat, dim3(256), 0, st,
+                     (const int32_t *)b.cy, (const int32_t *)b.cY,
+                     (const int32_t *)b.parent, (const int32_t *)b.rmark,
+                     (const int32_t *)b.rpos, (const int32_t *)b.rbase,
+                     (const int32_t *)b.rcapl, adj, b.tbl[cur], b.ecnt,
+                     b.wmark, (const int32_t *)b.lch_i,
+                     (const int32_t *)b.lch_j, (int64_t)is.top, nn, stamp,
+                     ctl);
+  hipLaunchKernelGGL(k_incr_owners, dim3(nblk), dim3(256), 0, st,
+                     (const int32_t *)b.roots, (const int32_t *)b.rbase,
+                     (const int32_t *)b.rcapl, b.ws[cur], b.wl[cur],
+                     (int64_t)is.top, ctl);
+  hipLaunchKernelGGL(k_incr_nextwork, xblocks_for(nn), dim3(256), 0, st, nn,
+                     (const int32_t *)b.wmark, work_next, stamp, ctl);
+  hipLaunchKernelGGL(k_incr_cleanup, blocks_for(nw), dim3(256), 0, st, nw,
+                     work, b.target, b.parent, ctl);
+  prof_end(st);
+}
+
+void incr_round_any(const Bufs &b, const Adj &adj, int cur, int32_t n,
+                    int32_t k, int32_t nn, int32_t d, double lambda,
+                    int64_t smin, const IncrState &is, Ctl *ctl,
+                    hipStream_t st, bool rest_only) {
+  switch (d) {
+    case 8:
+      incr_round<8>(b, adj, cur, n, k, nn, d, lambda, smin, is, ctl, st,
+                    rest_only);
+      break;
+    case 16:
+      incr_round<16>(b, adj, cur, n, k, nn, d, lambda, smin, is, ctl, st,
+                     rest_only);
+      break;
+    case 32:
+      incr_round<32>(b, adj, cur, n, k, nn, d, lambda, smin, is, ctl, st,
+                     rest_only);
+      break;
+    default:
+      incr_round<0>(b, adj, cur, n, k, nn, d, lambda, smin, is, ctl, st,
+                    rest_only);
+  }
+}
+
+// Leaves incremental rounds: the dead nodes' rep chains resolved to their
+// roots (doubling passes until one moves nothing), the live nodes numbered
+// in id order, their state and rows copied into the other buffers under the
+// new ids, and the point map composed.  Updates nn, ed (= the slots of the
+// packed table) and cur.
+int incr_compact(const Bufs &b, Adj &adj, int &cur, int32_t n, int32_t &nn,
+                 int32_t &ed, int32_t d, IncrState &is, Ctl *ctl, Ctl *h,
+                 hipStream_t st) {
+  int rc;
+  int lg = 0;
+  while (((int64_t)1 << lg) < (int64_t)nn) ++lg;
+  bool done = false;
+  for (int bt = 0; bt < (lg + 3) / 4 + 1 && !done; ++bt) {
+    hipLaunchKernelGGL(k_jump_state, dim3(1), dim3(64), 0, st, ctl, 0);
+    for (int j = 0; j < 4; ++j)
+      hipLaunchKernelGGL(k_rep_double, blocks_for(nn), dim3(256), 0, st, nn,
+                         b.rep, ctl);
+    if ((rc = read_ctl(ctl, h, st))) return rc;
+    if (h->err) return status_from_err(h->err);
+    done = !h->jump_changed;
+  }
+  if (!done) {
+    set_error("merge aliases did not reach their roots");
+    return -5;
+  }
+  const int nxt = 1 - cur;
+  device_scan(ScanLive{b.rep, b.newid, nn}, nn, b.bsum, &ctl->n_live, st);
+  NodeIn s;
+  s.size = b.size[cur];
+  s.S = b.S[cur];
+  s.mu = b.mu;
+  s.minpt = b.minpt[cur];
+  s.emb = nullptr;
+  s.perm = nullptr;
+  s.merged = nullptr;
+  hipLaunchKernelGGL(k_compact_nodes, xblocks_for(nn), dim3(256), 0, st, nn,
+                     (const int32_t *)b.rep, (const int32_t *)b.newid, s,
+                     b.size[nxt], b.minpt[nxt], b.S[nxt], b.mu, adj, b.capn,
+                     (const int32_t *)b.rmark, is.stamp - 1, b.merged, d, ctl);
+  if ((rc = read_ctl(ctl, h, st))) return rc;
+  if (h->err) return status_from_err(h->err);
+  const int32_t nl = h->n_live;
+  if (nl < 1 || nl > nn) {
+    set_error("live node count out of range (%d of %d)", nl, nn);
+    return -5;
+  }
+  hipLaunchKernelGGL(k_compact_mu, blocks_for((int64_t)nl * d), dim3(256), 0,
+                     st, nl, (const int32_t *)b.size[nxt],
+                     (const int64_t *)b.S[nxt], b.mu, d, ctl);
+  device_scan(ScanArray{b.capn, b.ws[nxt], nl, nullptr}, nl + 1, b.bsum,
+              &ctl->slots, st);
+  hipLaunchKernelGGL(k_compact_rows, xblocks_for(nn), dim3(256), 0, st, nn,
+                     (const int32_t *)b.rep, (const int32_t *)b.newid, adj,
+                     (const int32_t *)b.ws[nxt], b.wl[nxt], b.tbl[nxt], ctl);
+  hipLaunchKernelGGL(k_compose_rep, xblocks_for(n), dim3(256), 0, st, n, nn,
+                     b.M, (const int32_t *)b.rep, (const int32_t *)b.newid,
+                     ctl);
+  if ((rc = read_ctl(ctl, h, st))) return rc;
+  if (h->err) return status_from_err(h->err);
+  if (h->slots < 0 || h->slots > is.span_live) {
+    set_error("packed table out of range (%d slots)", h->slots);
+    return -5;
+  }
+  nn = nl;
+  ed = h->slots;
+  cur = nxt;
+  adj.ws = b.ws[cur];
+  adj.wl = b.wl[cur];
+  adj.tbl = b.tbl[cur];
+  is.on = false;
+  return 0;
 }
 
 // The rest of the ladder in the tail kernel, then the labels (and energy)
@@ -3177,20 +4113,91 @@ int ladder_run(const LadderArgs &g, Ctl *ctl, Arena &a, hipStream_t st) {
   }
   if (g.link) tail_nodes = 0;  // the tail kernel does not link
   bool relinked = false;
+  // incremental rounds (stable ids within a level) are opt-in:
+  // EZSP_INCREMENTAL=1 switches graphs of kIncrMinNodes nodes and more,
+  // larger values set the smallest graph that switches (so that tests reach
+  // these rounds on small inputs); unset or 0 keeps every round on the
+  // renumbering path, which measured faster on the aerial tile
+  IncrState is;
+  bool incr_allowed = false;
+  int32_t incr_min = kIncrMinNodes;
+  if (const char *e = getenv("EZSP_INCREMENTAL")) {
+    const long v = strtol(e, nullptr, 10);
+    incr_allowed = v > 0 && !g.link;
+    if (v > 1) incr_min = (int32_t)std::min<long>(v, INT32_MAX);
+  }
+  // EZSP_INCR_COMPACT_EVERY=r renumbers after every r incremental rounds
+  // (the path a filling table takes), for tests
+  int32_t compact_every = 0;
+  if (const char *e = getenv("EZSP_INCR_COMPACT_EVERY"))
+    compact_every = (int32_t)std::max<long>(0, strtol(e, nullptr, 10));
+  const int64_t tcap = 2 * edge_bound(n, k);
   for (int32_t l = 0; l < g.n_levels; ++l) {
     const double lambda = g.lambdas[l];
     const int64_t smin = g.min_size ? g.min_size[l] : 0;
     for (int32_t round = 0;; ++round) {
-      if (ed == 0) break;  // no edge left: nothing can merge
-      if (!first && nn <= tail_nodes && ed <= kTailEdges &&
-          slots <= b.tslots) {
-        tail_level = l;  // the rest runs in the tail kernel
-        tail_round = round;
-        break;
+      if (is.on && (is.n_live <= tail_nodes ||
+                    is.top + 2 * is.span_live > tcap ||
+                    (compact_every > 0 && is.stamp >= compact_every))) {
+        // back to renumbered ids: for the tail, or for table room
+        if ((rc = incr_compact(b, adj, cur, n, nn, ed, d, is, ctl, h, st)))
+          return rc;
+        slots = ed;
+      }
+      if (!is.on) {
+        if (ed == 0) break;  // no edge left: nothing can merge
+        if (!first && nn <= tail_nodes && ed <= kTailEdges &&
+            slots <= b.tslots) {
+          tail_level = l;  // the rest runs in the tail kernel
+          tail_round = round;
+          break;
+        }
       }
       if (round >= max_rounds) {
         set_error("level %d reached max_rounds = %d", l, max_rounds);
         return -6;
+      }
+      if (is.on) {
+        incr_round_any(b, adj, cur, n, k, nn, d, lambda, smin, is, ctl, st,
+                       false);
+        if ((rc = read_ctl(ctl, h, st))) return rc;
+        if (h->err) return status_from_err(h->err);
+        if (h->any_choice < 0) {
+          if ((rc = finish_jump(b, nn, ctl, h, st))) return rc;
+          incr_round_any(b, adj, cur, n, k, nn, d, lambda, smin, is, ctl, st,
+                         true);
+          if ((rc = read_ctl(ctl, h, st))) return rc;
+          if (h->err) return status_from_err(h->err);
+        }
+        if (prof_on()) {
+          // algorithmic bytes, from the round's counts: the worklist's rows
+          // (at the mean row span) and node statistics, the members' sums,
+          // the rebuilt windows written and read back
+          const double S1 = 8.0 * d + 8.0;
+          const double span = is.n_live ? (double)is.span_live / is.n_live : 0;
+          prof_bytes("select", is.n_work * (8.0 * span + S1 + 4.0));
+          if (h->any_choice) {
+            prof_bytes("union", 8.0 * is.n_work);
+            prof_bytes("stats", 2.0 * S1 * h->n_dead + S1 * h->n_roots);
+            prof_bytes("contract", 8.0 * span * (h->n_dead + h->n_roots) +
+                                       16.0 * h->win_total);
+          }
+        }
+        if (!h->any_choice) break;  // Step 1: no candidate merge
+        if (h->n_dead < 1 || h->n_dead >= is.n_live || h->n_work < 0 ||
+            h->n_work > nn || h->win_total < 0 || h->span_live < 0) {
+          set_error("incremental round sizes out of range (%d merged, %d "
+                    "listed)", h->n_dead, h->n_work);
+          return -5;
+        }
+        is.n_live -= h->n_dead;
+        is.top += h->win_total;
+        is.span_live = h->span_live;
+        is.n_work = h->n_work;
+        is.wc = 1 - is.wc;
+        ++is.stamp;
+        if (is.n_live == 1) break;  // a single component is left
+        continue;
       }
       NodeIn s;
       s.emb = emb;
@@ -3249,6 +4256,7 @@ int ladder_run(const LadderArgs &g, Ctl *ctl, Arena &a, hipStream_t st) {
                   h->n_next, h->e_next, h->slots);
         return -5;
       }
+      const int32_t nn_before = nn;
       cur = 1 - cur;
       first = false;
       slots = h->slots;
@@ -3258,6 +4266,11 @@ int ladder_run(const LadderArgs &g, Ctl *ctl, Arena &a, hipStream_t st) {
       adj.wl = b.wl[cur];
       adj.tbl = b.tbl[cur];
       if (nn == 1) break;  // a single component is left
+      if (incr_allowed && nn >= incr_min &&
+          (double)nn > kIncrKeep * (double)nn_before) {
+        // few nodes merged: the next rounds keep their ids
+        if ((rc = incr_enter(b, adj, nn, slots, is, ctl, h, st))) return rc;
+      }
       if (g.link && h->n_iso > 0) {  // prepare_graph of the next round
         if ((rc = link_round(g, b, adj, cur, nn, h->n_iso, ed, ctl, h, st)))
           return rc;
@@ -3266,6 +4279,11 @@ int ladder_run(const LadderArgs &g, Ctl *ctl, Arena &a, hipStream_t st) {
       }
     }
 
+    if (is.on) {  // the level's nodes under consecutive ids again
+      if ((rc = incr_compact(b, adj, cur, n, nn, ed, d, is, ctl, h, st)))
+        return rc;
+      slots = ed;
+    }
     if (tail_level >= 0) break;
     // level output
     int32_t *out = g.labels + (int64_t)l * n;

@@ -108,11 +108,14 @@ def aerial_crop(n_keep=1_200_000):
 _CROP = {}
 
 
-def test_aerial_crop_many_rounds(tail_mode):
+@pytest.mark.parametrize("incremental", ["0", "1"])
+def test_aerial_crop_many_rounds(tail_mode, incremental, monkeypatch):
     """A 1.2M-point crop of the aerial tile: the oracle's round log shows
     dozens of level-0 rounds (a few percent of the nodes merge per round,
     the merged-flag skip of selection active throughout); every label of
-    every level, the counts and the energy against the oracle."""
+    every level, the counts and the energy against the oracle, with
+    renumbering rounds only and with the incremental rounds."""
+    monkeypatch.setenv("EZSP_INCREMENTAL", incremental)
     if not _CROP:
         sc, xyz, emb = aerial_crop()
         _CROP["v"] = (sc, xyz, emb, oracle.partition(xyz, emb, sc.k,
