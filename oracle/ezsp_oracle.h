@@ -39,7 +39,7 @@
  *   R5  conflict removal keeps, per node, the incident candidate edge that is
  *       largest under (Delta desc, lo asc, hi asc).
  *   R6  |P| < s_min is strict; s_min <= 1 disables it.
- *   R7  "connect isolated nodes" (prepare_graph), when asked for: at the
+ *   R7  linking of isolated nodes (prepare_graph), when asked for: at the
  *       start of every round with more than one node, each node without an
  *       edge gets an edge of weight 1 to each of its min(k, nn-1) nearest
  *       nodes (squared distance of exact fixed-point centroids in fp64, then
