@@ -89,6 +89,7 @@ struct Ctl {
   double le_loss;             // Eq. loss over the sample
   double pu_miou, pu_purity;
   int64_t pu_present;
+  uint32_t seq;               // host copy only: export number, written last
 };
 
 __device__ __forceinline__ void stripe_add(Stripe *s, int32_t v) {

@@ -6,6 +6,7 @@
 #include <unordered_map>
 #include <vector>
 #include <stdio.h>
+#include <stddef.h>
 #include <string.h>
 
 #include "ezsp_internal.h"
@@ -273,15 +274,68 @@ int check_hip(hipError_t e, const char *what) {
   return -5;  // EZSP_ERR_DEVICE
 }
 
+// The host copy of the control block: fine-grained (coherent) pinned
+// memory, mapped into the device's address space, so that a kernel can
+// write it directly (k_ctl_export) instead of a DMA copy.
+namespace {
+thread_local Ctl *t_host_ctl = nullptr;
+thread_local Ctl *t_host_ctl_dev = nullptr;
+}  // namespace
+
 Ctl *pinned_ctl() {
-  static thread_local Ctl *p = nullptr;
-  if (!p) {
+  if (!t_host_ctl) {
     void *q = nullptr;
-    if (hipHostMalloc(&q, sizeof(Ctl), hipHostMallocDefault) != hipSuccess)
+    if (hipHostMalloc(&q, sizeof(Ctl),
+                      hipHostMallocMapped | hipHostMallocCoherent) !=
+        hipSuccess)
       return nullptr;
-    p = static_cast<Ctl *>(q);
+    void *d = nullptr;
+    if (hipHostGetDevicePointer(&d, q, 0) != hipSuccess || !d) {
+      hipHostFree(q);
+      return nullptr;
+    }
+    t_host_ctl = static_cast<Ctl *>(q);
+    t_host_ctl_dev = static_cast<Ctl *>(d);
   }
-  return p;
+  return t_host_ctl;
+}
+
+// Copies the control block to its host copy: every field but the striped
+// counters word by word, then e_next and e_fwd as the sums of their
+// stripes (-1 beyond int32).
+__global__ __launch_bounds__(256) void k_ctl_export(const Ctl *ctl,
+                                                    Ctl *host, uint32_t seq) {
+  const uint32_t *src = reinterpret_cast<const uint32_t *>(ctl);
+  uint32_t *dst = reinterpret_cast<uint32_t *>(host);
+  constexpr uint32_t s0 = offsetof(Ctl, e_next_s) / 4;
+  constexpr uint32_t s1 = offsetof(Ctl, tail_nc) / 4;
+  constexpr uint32_t nw = sizeof(Ctl) / 4;
+  constexpr uint32_t en = offsetof(Ctl, e_next) / 4;
+  constexpr uint32_t ef = offsetof(Ctl, e_fwd) / 4;
+  constexpr uint32_t sq = offsetof(Ctl, seq) / 4;
+  static_assert(offsetof(Ctl, e_fwd_s) > offsetof(Ctl, e_next_s) &&
+                    offsetof(Ctl, maxabs_s) < offsetof(Ctl, tail_nc),
+                "the striped counters lie between e_next_s and tail_nc");
+  for (uint32_t i = threadIdx.x; i < nw; i += blockDim.x)
+    if ((i < s0 || i >= s1) && i != en && i != ef && i != sq) dst[i] = src[i];
+  if (threadIdx.x < kWave) {
+    const int lane = threadIdx.x;
+    long long a = lane < kStripes ? ctl->e_next_s[lane].v : 0;
+    long long b = lane < kStripes ? ctl->e_fwd_s[lane].v : 0;
+    a = wave_sum(a);
+    b = wave_sum(b);
+    if (lane == 0) {
+      host->e_next = a > INT32_MAX ? -1 : (int32_t)a;
+      host->e_fwd = b > INT32_MAX ? -1 : (int32_t)b;
+    }
+  }
+  // every field above is in host memory before the export number
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    __threadfence_system();
+    __hip_atomic_store(&host->seq, seq, __ATOMIC_RELEASE,
+                       __HIP_MEMORY_SCOPE_SYSTEM);
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -396,22 +450,33 @@ int prof_read(const char *name, int64_t *launches, double *ms,
 int read_ctl(Ctl *ctl, Ctl *host, hipStream_t st) {
   int rc = check_hip(hipGetLastError(), "kernel launch");
   if (rc) return rc;
-  rc = check_hip(hipMemcpyAsync(host, ctl, sizeof(Ctl), hipMemcpyDeviceToHost,
-                                st),
-                 "hipMemcpyAsync(ctl)");
+  if (host != t_host_ctl || !t_host_ctl_dev) {
+    set_error("read_ctl needs the thread's pinned control block");
+    return -5;
+  }
+  // the host waits for the export number instead of a stream
+  // synchronisation (whose wake-up takes tens of microseconds); the stream
+  // is polled now and then so that a failed kernel ends the wait
+  static thread_local uint32_t t_seq = 0;
+  const uint32_t want = ++t_seq;
+  hipLaunchKernelGGL(k_ctl_export, dim3(1), dim3(256), 0, st,
+                     (const Ctl *)ctl, t_host_ctl_dev, want);
+  rc = check_hip(hipGetLastError(), "k_ctl_export launch");
   if (rc) return rc;
-  rc = check_hip(hipStreamSynchronize(st), "hipStreamSynchronize");
-  if (rc == 0) {
-    int64_t en = 0, ef = 0;
-    for (int i = 0; i < kStripes; ++i) {
-      en += host->e_next_s[i].v;
-      ef += host->e_fwd_s[i].v;
+  for (uint32_t spin = 1;; ++spin) {
+    if (__atomic_load_n(&host->seq, __ATOMIC_ACQUIRE) == want) break;
+    if ((spin & 1023) == 0) {
+      const hipError_t e = hipStreamQuery(st);
+      if (e == hipSuccess) {  // the stream drained: the number is there
+        if (__atomic_load_n(&host->seq, __ATOMIC_ACQUIRE) == want) break;
+        set_error("control block export did not arrive");
+        return -5;
+      }
+      if (e != hipErrorNotReady) return check_hip(e, "stream");
     }
-    host->e_next = en > INT32_MAX ? -1 : (int32_t)en;
-    host->e_fwd = ef > INT32_MAX ? -1 : (int32_t)ef;
   }
   prof_flush();
-  return rc;
+  return 0;
 }
 
 int status_from_err(uint32_t err) {
