@@ -1706,55 +1706,60 @@ __global__ void k_energy_reset(Ctl *ctl) {
 // Tail: once the graph is small, every remaining round of every remaining
 // level runs inside one block of 1024 threads, with barriers between the
 // steps instead of kernel launches and host round trips.  The arithmetic is
-// the same as above; the work is spread over table slots (entries) rather
-// than rows, and the per-node arrays live in LDS:
-//   select    two passes over the slots: the gain of every entry (after a
-//             level's first round only entries with an end that merged in
-//             the last round) and per row the largest candidate gain (max
-//             of an order-preserving key), then among the entries with that
-//             gain the neighbour with the smallest minpt, by a 64-bit min of
-//             (minpt, neighbour) (Steps 1-2, same choice as best_before)
+// the same as above.  Node ids stay fixed inside the tail: a component
+// formed by a merge keeps its root's id, its other members die.  The
+// per-node arrays (size, smallest point, row window, parent, the tail-start
+// node -> current node map) live in LDS; the fp64 means, the int64 sums and
+// the table stay in global memory.  A round:
+//   select    the gain of every undirected edge once, from the row of its
+//             smaller end (after a level's first round only the edges of
+//             nodes formed by a merge in the last round: every other gain
+//             is unchanged and gave no candidate), each end's largest
+//             candidate gain by a max of an order-preserving key, then
+//             among the edges with that gain the neighbour with the
+//             smallest minpt, by a 64-bit min of (minpt, neighbour) (Steps
+//             1-2, the same choice as best_before)
 //   union     hook and pointer jumping on LDS arrays (Step 3)
-//   relabel   roots numbered by a block scan
-//   stats     node-parallel adds into the next node state (int64 sums,
-//             size, smallest point, summed degree) with workgroup-scope
-//             atomics, then the means (Step 4)
-//   contract  every entry relabelled and added into its component's window
-//             of the next table (windows keep their empty slots)
-// The point -> node map is not touched: the tail keeps Mt (tail-start node
-// -> current node) and leaves, for each level it ends, a snapshot of Mt, the
-// smallest point of every node and (for the energy) the means and the cut
-// weight.
+//   stats     every member adds its size, smallest point and int64 sums
+//             into its root; the merged roots' means are recomputed (Step 4)
+//   contract  a new window, past the end of the table, for every merged
+//             root (its members' rows and its own, relabelled) and for
+//             every row that listed a member; the other rows stay as they
+//             are, since every node they list keeps its id (Step 4).  When
+//             the table is full, every live row is rebuilt into the other
+//             buffer instead.
+// At a level's end the live nodes are numbered in id order for the
+// snapshots that the labels and the energy read.
 // ---------------------------------------------------------------------------
 constexpr int kTailNT = 1024;
 constexpr int kTailNodes = 2048;    // largest graph the tail can take (LDS)
 constexpr int kTailStart = 1500;    // default switch to the tail
 constexpr int kTailEdges = 1 << 16; // ... directed entries at the switch
-constexpr int kTailSlots = 1 << 18; // ... table slots at the switch
+constexpr int kTailSlots = 1 << 17; // gains: the live windows span at most
+                                    // twice the entries at the switch
 constexpr int kTailLevels = 16;
 static_assert(sizeof(((Ctl *)nullptr)->tail_nc) == kTailLevels * 4,
               "tail level counts travel in the control block");
 constexpr int kTailJumps = 64;
-// Slots per thread whose loads are issued together in the tail's slot loops:
-// the block is alone on one CU, so memory latency, not bandwidth, sets the
-// pace of a loop that waits on every slot's loads in turn.
+// Entries per thread whose loads are issued together in the tail's entry
+// loops: the block is alone on one CU, so memory latency, not bandwidth,
+// sets the pace of a loop that waits on every entry's loads in turn.
 constexpr int kTU = 4;
 
 struct TailState {
   int32_t *ws[2], *wl[2];
   uint64_t *tbl[2];
-  int32_t *size[2], *minpt[2];
-  int64_t *S[2];
-  double *mu;
-  double *gain;                            // one per slot
-  int32_t *row[2];                         // row of every occupied slot
-  int32_t *Mt;
+  const int32_t *size, *minpt;             // node state at the tail's start
+  int64_t *S;                              // sums, updated in place
+  double *mu;                              // means, updated in place
+  double *gain;                            // per listed edge
+  uint64_t *elist;                         // edges to evaluate:
+                                           // (v | u << 16) << 32 | w
   int32_t *lvl_map, *lvl_minpt, *lvl_nc;  // kTailLevels x nn0 (nc: levels)
   int32_t *lvl_rank;                       // kTailLevels x nn0
   double *lvl_mu;                          // kTailLevels x nn0 x d
   long long *lvl_cut2;                     // kTailLevels
-  int32_t nn0, ed0, cur0, tcur0, d, tcap, gcap, n_levels, level0, round0,
-      max_rounds;
+  int32_t nn0, tcur0, d, tcap, gcap, n_levels, level0, round0, max_rounds;
   int32_t want_energy;
   double lambda[kTailLevels];
   long long smin[kTailLevels];
@@ -1763,42 +1768,8 @@ struct TailState {
 // The tail is one block, so its global read-modify-writes only need
 // workgroup scope: they are performed in this XCD's L2 instead of going out
 // to memory as device-scope atomics do.  Kernel end still publishes them.
-__device__ __forceinline__ void wg_add(int32_t *p, int32_t v) {
-  __hip_atomic_fetch_add(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-}
 __device__ __forceinline__ void wg_add64(int64_t *p, int64_t v) {
   __hip_atomic_fetch_add(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-}
-__device__ __forceinline__ void wg_min(int32_t *p, int32_t v) {
-  __hip_atomic_fetch_min(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-}
-
-// table_add for the tail (same probing, workgroup-scope atomics).
-// A slot it claims records its row A in row[].
-__device__ __forceinline__ bool tail_table_add(uint64_t *tbl, int32_t *row,
-                                               int32_t A, int32_t base,
-                                               int32_t cap, int32_t B,
-                                               int32_t w, Ctl *ctl) {
-  uint32_t h = ((uint32_t)B * 2654435761u) % (uint32_t)cap;
-  const uint64_t mine = ((uint64_t)(uint32_t)B << 32) | (uint32_t)w;
-  for (int32_t probe = 0; probe < cap; ++probe) {
-    uint64_t *slot = tbl + base + h;
-    uint64_t cur = kEmpty;
-    if (__hip_atomic_compare_exchange_strong(slot, &cur, mine,
-                                             __ATOMIC_RELAXED, __ATOMIC_RELAXED,
-                                             __HIP_MEMORY_SCOPE_WORKGROUP)) {
-      row[base + h] = A;
-      return true;
-    }
-    if ((int32_t)(cur >> 32) == B) {
-      __hip_atomic_fetch_add(slot, (uint64_t)(uint32_t)w, __ATOMIC_RELAXED,
-                             __HIP_MEMORY_SCOPE_WORKGROUP);
-      return false;
-    }
-    h = (h + 1 == (uint32_t)cap) ? 0u : h + 1;
-  }
-  raise_err(ctl, kErrInternal);
-  return false;
 }
 
 // Exclusive scan of value(0..len) into out[0..len], out[len] = total.
@@ -1825,16 +1796,23 @@ __device__ __forceinline__ int32_t tail_scan(int32_t len, V &&value,
   return tot;
 }
 
-// Row of slot q: the last v < nn with ws[v] <= q (ws ascending, ws[nn] = Q).
-__device__ __forceinline__ int32_t tail_row(const int32_t *ws, int32_t nn,
-                                            int32_t q) {
-  int32_t lo = 0, hi = nn;
-  while (hi - lo > 1) {
-    const int32_t mid = (lo + hi) >> 1;
-    if (ws[mid] <= q) lo = mid;
-    else hi = mid;
+// Rows of U flattened positions p[j]: the last v < nn with pos[v] <= p[j]
+// (pos ascending, pos[0] = 0, rows of no span share their successor's
+// start).  The U searches take their steps together (the step sizes depend
+// on nn only), so each step's LDS reads are issued back to back.
+template <int U>
+__device__ __forceinline__ void tail_rows(const int32_t *pos, int32_t nn,
+                                          const int32_t (&p)[U],
+                                          int32_t (&v)[U]) {
+#pragma unroll
+  for (int j = 0; j < U; ++j) v[j] = 0;
+  for (int32_t len = nn; len > 1;) {
+    const int32_t half = len >> 1;
+#pragma unroll
+    for (int j = 0; j < U; ++j)
+      v[j] = pos[v[j] + half] <= p[j] ? v[j] + half : v[j];
+    len -= half;
   }
-  return lo;
 }
 
 // Order-preserving key of a finite double; 0 is below every key.
@@ -1845,7 +1823,8 @@ __device__ __forceinline__ unsigned long long gain_key(double g) {
 
 // Prop. 1 for the entry (v, u) in the tail: the operations of edge_gain in
 // the same order, sizes from LDS and the two mean rows streamed two
-// dimensions at a time (few registers: the tail runs 1024 threads).
+// dimensions at a time (few registers: the tail runs 1024 threads).  The
+// value is symmetric bit for bit in (v, u).
 template <int DT>
 __device__ __forceinline__ double tail_gain(const double *__restrict__ mu,
                                             int32_t v, int32_t u, int32_t d,
@@ -1858,7 +1837,7 @@ __device__ __forceinline__ double tail_gain(const double *__restrict__ mu,
   if constexpr (DT > 0) {
     const double2 *a = reinterpret_cast<const double2 *>(mu + (int64_t)v * DT);
     const double2 *b = reinterpret_cast<const double2 *>(mu + (int64_t)u * DT);
-#pragma unroll
+#pragma unroll 4
     for (int i = 0; i < DT / 2; ++i) {
       const double2 x = a[i], y = b[i];
       const double d0 = x.x - y.x;
@@ -1880,56 +1859,95 @@ __device__ __forceinline__ double tail_gain(const double *__restrict__ mu,
   return cut - fit;
 }
 
+// Calls f(p, v, e) for every non-empty entry e of the rows whose flattened
+// positions pos[] spans (P positions in all): row v, table tb.  The entries
+// and rows of kTU positions per thread are loaded before any is used.
+template <int U = kTU, class Fn>
+__device__ __forceinline__ void tail_entries(const int32_t *pos, int32_t nn,
+                                             int32_t P, const int32_t *s_ws,
+                                             const uint64_t *tb, Fn &&f) {
+  for (int32_t p0 = threadIdx.x; p0 < P; p0 += U * kTailNT) {
+    uint64_t ev[U];
+    int32_t pp[U], vv[U];
+#pragma unroll
+    for (int j = 0; j < U; ++j) pp[j] = min(p0 + j * kTailNT, P - 1);
+    tail_rows<U>(pos, nn, pp, vv);
+#pragma unroll
+    for (int j = 0; j < U; ++j) ev[j] = tb[s_ws[vv[j]] + (pp[j] - pos[vv[j]])];
+#pragma unroll
+    for (int j = 0; j < U; ++j) {
+      const int32_t p = p0 + j * kTailNT;
+      if (p >= P || ev[j] == kEmpty) continue;
+      f(p, vv[j], ev[j]);
+    }
+  }
+}
+
 template <int DT>
 __global__ __launch_bounds__(kTailNT) void k_tail(TailState t, Ctl *ctl) {
-  __shared__ int32_t s_size[kTailNodes];
-  __shared__ __align__(16) int32_t s_minpt[kTailNodes];
-  __shared__ int32_t s_deg[kTailNodes], s_L[kTailNodes];
-  __shared__ int32_t s_sel[kTailNodes];
-  __shared__ int32_t s_wsa[kTailNodes + 1], s_wsb[kTailNodes + 1];
-  __shared__ unsigned long long s_key[kTailNodes + 1];
-  __shared__ unsigned long long s_pick[kTailNodes];
-  __shared__ int32_t s_mrg[kTailNodes];
+  __shared__ int32_t s_size[kTailNodes], s_minpt[kTailNodes];
+  __shared__ int32_t s_ws[kTailNodes], s_wl[kTailNodes], s_deg[kTailNodes];
+  __shared__ int32_t s_L[kTailNodes], s_sel[kTailNodes], s_Mt[kTailNodes];
+  __shared__ int32_t s_pos[kTailNodes + 1], s_nws[kTailNodes + 1];
+  __shared__ int32_t s_cap[kTailNodes];
+  __shared__ unsigned long long s_key[kTailNodes], s_pick[kTailNodes];
+  // node flags: live; formed by a merge in the last round; root with
+  // members in this round; row to rebuild in this round
+  __shared__ uint8_t s_live[kTailNodes], s_mrg[kTailNodes], s_new[kTailNodes],
+      s_touch[kTailNodes];
   __shared__ int32_t wsum[kTailNT / kWave];
-  __shared__ int32_t s_any, s_flag, s_claims;
+  __shared__ int32_t s_any, s_flag, s_cnt, s_ne;
   __shared__ long long s_cut;
+  __shared__ double s_lambda[kTailLevels];
+  __shared__ long long s_smin[kTailLevels];
   const int lane = threadIdx.x & (kWave - 1);
   const int32_t d = t.d;
-  const double sF = ldexp(1.0, ctl->F), sIF = ldexp(1.0, -ctl->F);
-  // s_key doubles as int32 scratch once the choices are made
-  int32_t *s_aux = reinterpret_cast<int32_t *>(s_key);  // 2 kTailNodes + 2
-  int32_t *s_newid = s_aux, *s_cap = s_aux + kTailNodes + 1;
-  int32_t *s_ws = s_wsa, *s_wn = s_wsb;  // current / next row starts
-  // cur: node state, tc: table (they may start on different buffers)
-  int32_t nn = t.nn0, ed = t.ed0, cur = t.cur0, tc = t.tcur0;
-  if (nn > kTailNodes || nn < 1) {
+  const int32_t N = t.nn0;
+  const double sIF = ldexp(1.0, -ctl->F);
+  // s_key doubles as the new entry counts once the choices are made
+  int32_t *s_ndeg = reinterpret_cast<int32_t *>(s_key);
+  if (N > kTailNodes || N < 1) {
     if (threadIdx.x == 0) raise_err(ctl, kErrInternal);
     return;
   }
-  for (int32_t i = threadIdx.x; i <= nn; i += kTailNT) {
-    s_ws[i] = t.ws[tc][i];
-    if (i < nn) t.Mt[i] = i;
+  int32_t tc = t.tcur0;
+  if (threadIdx.x < kTailLevels) {
+    s_lambda[threadIdx.x] = t.lambda[threadIdx.x];
+    s_smin[threadIdx.x] = t.smin[threadIdx.x];
   }
-  __syncthreads();
-  int32_t Q = s_ws[nn];  // slots of the current table
-  // rows of the incoming table may end before their window does: clear the
-  // rest so that every slot is either an entry or empty
-  for (int32_t q = threadIdx.x; q < Q; q += kTailNT) {
-    const int32_t v = tail_row(s_ws, nn, q);
-    if (q - s_ws[v] >= t.wl[tc][v]) t.tbl[tc][q] = kEmpty;
-    t.row[tc][q] = v;
+  for (int32_t v = threadIdx.x; v < N; v += kTailNT) {
+    s_size[v] = t.size[v];
+    s_minpt[v] = t.minpt[v];
+    s_ws[v] = t.ws[tc][v];
+    s_wl[v] = t.wl[tc][v];
+    s_Mt[v] = v;
+    s_live[v] = 1;
+    s_mrg[v] = 0;
+    s_new[v] = 0;
+    s_touch[v] = 0;
+    s_sel[v] = v;
   }
+  if (threadIdx.x == 0) s_cnt = 0;
   __syncthreads();
+  // every live row's entries (the incoming windows are packed end to end)
+  int32_t top = 0;
+  {
+    const int32_t P =
+        tail_scan(N, [&](int32_t v) { return s_wl[v]; }, s_pos, wsum);
+    top = s_ws[N - 1] + s_wl[N - 1];
+    for (int32_t v = threadIdx.x; v < N; v += kTailNT) s_deg[v] = 0;
+    __syncthreads();
+    tail_entries(s_pos, N, P, s_ws, t.tbl[tc],
+                 [&](int32_t, int32_t v, uint64_t) { atomicAdd(&s_deg[v], 1); });
+    __syncthreads();
+  }
+  int32_t nn = N;  // live nodes
+  int32_t ed = tail_scan(N, [&](int32_t v) { return s_deg[v]; }, s_nws, wsum);
   for (int32_t l = t.level0; l < t.n_levels; ++l) {
-    const double lambda = t.lambda[l];
-    const long long smin = t.smin[l];
+    const double lambda = s_lambda[l];
+    const long long smin = s_smin[l];
     for (int32_t round = (l == t.level0 ? t.round0 : 0);; ++round) {
-      if (ed == 0) break;  // no edge left: nothing can merge
-      // Every gain is evaluated in a level's first round and in the tail's
-      // first round.  Later, an entry whose two ends were both left alone by
-      // the last round keeps last round's gain, sizes and weight, which made
-      // no candidate (a node with a candidate merges): only entries with a
-      // merged end (s_mrg) are evaluated.
+      if (ed == 0 || nn == 1) break;  // nothing can merge
       const bool fresh = round == 0 || (l == t.level0 && round == t.round0);
       if (round >= t.max_rounds) {
         if (threadIdx.x == 0) {
@@ -1938,93 +1956,100 @@ __global__ __launch_bounds__(kTailNT) void k_tail(TailState t, Ctl *ctl) {
         }
         return;
       }
-      const int nxt = 1 - cur;
       const uint64_t *tb = t.tbl[tc];
-      const int32_t *rows = t.row[tc];
-      NodeIn s;
-      s.size = t.size[cur];
-      s.S = t.S[cur];
-      s.mu = t.mu;
-      s.minpt = t.minpt[cur];
-      s.emb = nullptr;
-      s.perm = nullptr;
-      s.merged = nullptr;
       if (threadIdx.x == 0) s_any = 0;
-      for (int32_t v = threadIdx.x; v < nn; v += kTailNT) {
-        s_size[v] = s.size[v];
-        s_minpt[v] = s.minpt[v];
-        s_deg[v] = 0;
+      for (int32_t v = threadIdx.x; v < N; v += kTailNT) {
         s_key[v] = 0ull;
         s_pick[v] = ~0ull;
       }
+      // rows whose entries are evaluated: every live row in a fresh round,
+      // else the rows of the nodes formed by a merge in the last round
+      auto scanned = [&](int32_t v) {
+        return s_live[v] && (fresh || s_mrg[v]);
+      };
+      if (threadIdx.x == 0) s_ne = 0;
+      const int32_t P = tail_scan(
+          N, [&](int32_t v) { return scanned(v) ? s_wl[v] : 0; }, s_pos, wsum);
+      // the edges to evaluate, each once: from the row of its smaller end
+      // when both rows are scanned
+      tail_entries<8>(s_pos, N, P, s_ws, tb, [&](int32_t, int32_t v,
+                                                 uint64_t e) {
+        const int32_t u = (int32_t)(e >> 32);
+        if ((uint32_t)u >= (uint32_t)N || !s_live[u]) {
+          raise_err(ctl, kErrInternal);
+          return;
+        }
+        if (u < v && scanned(u)) return;
+        const int32_t i = atomicAdd(&s_ne, 1);
+        if (i < t.gcap)
+          t.elist[i] = ((uint64_t)(uint32_t)(v | (u << 16)) << 32) |
+                       (uint32_t)e;
+        else
+          raise_err(ctl, kErrInternal);
+      });
       __syncthreads();
-      // Steps 1-2, pass 1: gains, degrees, largest candidate gain per row.
-      // The next slot's entry and row are loaded before this one is used
-      // (the index is clamped, so the loads need no branch).
-      {
-        int32_t q = threadIdx.x;
-        const int32_t q0 = min(q, Q - 1);
-        uint64_t e_n = tb[q0];
-        int32_t v_n = rows[q0];
-        for (; q < Q; q += kTailNT) {
-          const uint64_t e = e_n;
-          const int32_t v = v_n;
-          const int32_t qn = min(q + kTailNT, Q - 1);
-          e_n = tb[qn];
-          v_n = rows[qn];
-          if (e == kEmpty) continue;
-          const int32_t u = (int32_t)(e >> 32), w = (int32_t)(uint32_t)e;
-          if ((uint32_t)u >= (uint32_t)nn || (uint32_t)v >= (uint32_t)nn) {
-            raise_err(ctl, kErrInternal);
-            continue;
-          }
-          atomicAdd(&s_deg[v], 1);
-          if (!fresh && !s_mrg[v] && !s_mrg[u]) continue;
-          const double g = tail_gain<DT>(s.mu, v, u, d, (double)s_size[v],
+      const int32_t ne = min(s_ne, t.gcap);
+      // Steps 1-2, pass 1: each listed edge's gain, and each end's largest
+      // candidate gain (two edges per thread in flight)
+      for (int32_t i0 = threadIdx.x; i0 < ne; i0 += 2 * kTailNT) {
+        uint64_t ev[2];
+#pragma unroll
+        for (int j = 0; j < 2; ++j) ev[j] = t.elist[min(i0 + j * kTailNT, ne - 1)];
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+          const int32_t i = i0 + j * kTailNT;
+          if (i >= ne) break;
+          const uint32_t vu = (uint32_t)(ev[j] >> 32);
+          const int32_t v = (int32_t)(vu & 0xffffu), u = (int32_t)(vu >> 16);
+          const int32_t w = (int32_t)(uint32_t)ev[j];
+          const double g = tail_gain<DT>(t.mu, v, u, d, (double)s_size[v],
                                          (double)s_size[u], w, lambda);
-          t.gain[q] = g;
-          if (g > 0.0 || (long long)s_size[v] < smin)
-            atomicMax(&s_key[v], gain_key(g));
+          t.gain[i] = g;
+          const unsigned long long kg = gain_key(g);
+          if (g > 0.0 || (long long)s_size[v] < smin) atomicMax(&s_key[v], kg);
+          if (g > 0.0 || (long long)s_size[u] < smin) atomicMax(&s_key[u], kg);
         }
       }
       __syncthreads();
-      // pass 2: among the evaluated entries with the row's best gain, the
-      // neighbour with the smallest minpt (minpt is unique per node, so the
-      // 64-bit minimum of (minpt, neighbour) names it)
-      for (int32_t q0 = threadIdx.x; q0 < Q; q0 += kTU * kTailNT) {
+      // pass 2: the same edges; at each end whose largest candidate gain
+      // this is, the neighbour with the smallest minpt (minpt is unique per
+      // node, so the 64-bit minimum of (minpt, neighbour) names it)
+      for (int32_t i0 = threadIdx.x; i0 < ne; i0 += kTU * kTailNT) {
         uint64_t ev[kTU];
-        int32_t rv[kTU];
         double gv[kTU];
 #pragma unroll
         for (int j = 0; j < kTU; ++j) {
-          const int32_t q = min(q0 + j * kTailNT, Q - 1);  // no branch
-          ev[j] = tb[q];
-          rv[j] = rows[q];
-          gv[j] = t.gain[q];  // used only where evaluated
+          const int32_t i = min(i0 + j * kTailNT, ne - 1);  // no branch
+          ev[j] = t.elist[i];
+          gv[j] = t.gain[i];
         }
 #pragma unroll
         for (int j = 0; j < kTU; ++j) {
-          const uint64_t e = ev[j];
-          if (q0 + j * kTailNT >= Q || e == kEmpty) continue;
-          const int32_t v = rv[j];
-          const int32_t u = (int32_t)(e >> 32);
-          const unsigned long long kv = s_key[v];
-          if (kv != 0ull && (fresh || s_mrg[v] || s_mrg[u]) &&
-              gain_key(gv[j]) == kv)
-            atomicMin(&s_pick[v], ((unsigned long long)(uint32_t)s_minpt[u]
-                                   << 32) | (uint32_t)u);
+          if (i0 + j * kTailNT >= ne) break;
+          const uint32_t vu = (uint32_t)(ev[j] >> 32);
+          const int32_t v = (int32_t)(vu & 0xffffu), u = (int32_t)(vu >> 16);
+          const unsigned long long kv = s_key[v], ku = s_key[u];
+          const unsigned long long kg = gain_key(gv[j]);
+          if (kv != 0ull && kg == kv)
+            atomicMin(&s_pick[v],
+                      ((unsigned long long)(uint32_t)s_minpt[u] << 32) |
+                          (uint32_t)u);
+          if (ku != 0ull && kg == ku)
+            atomicMin(&s_pick[u],
+                      ((unsigned long long)(uint32_t)s_minpt[v] << 32) |
+                          (uint32_t)v);
         }
       }
       __syncthreads();
-      for (int32_t v = threadIdx.x; v < nn; v += kTailNT) {
+      for (int32_t v = threadIdx.x; v < N; v += kTailNT) {
         const unsigned long long pk = s_pick[v];
-        s_L[v] = pk == ~0ull ? -1 : (int32_t)(uint32_t)pk;  // target
-        if (pk != ~0ull) s_any = 1;
+        s_L[v] = (s_live[v] && pk != ~0ull) ? (int32_t)(uint32_t)pk : -1;
+        if (s_L[v] >= 0) s_any = 1;
       }
       __syncthreads();
       if (!s_any) break;  // Step 1: no candidate merge
       // Step 3: hook (s_sel = parent), pointer jumping
-      for (int32_t v = threadIdx.x; v < nn; v += kTailNT) {
+      for (int32_t v = threadIdx.x; v < N; v += kTailNT) {
         const int32_t tg = s_L[v];
         s_sel[v] = tg < 0 ? v : ((s_L[tg] == v && v < tg) ? v : tg);
       }
@@ -2032,7 +2057,7 @@ __global__ __launch_bounds__(kTailNT) void k_tail(TailState t, Ctl *ctl) {
       for (int pass = 0;; ++pass) {
         if (threadIdx.x == 0) s_flag = 0;
         __syncthreads();
-        for (int32_t v = threadIdx.x; v < nn; v += kTailNT) {
+        for (int32_t v = threadIdx.x; v < N; v += kTailNT) {
           const int32_t p = s_sel[v];
           const int32_t pp = s_sel[p];
           if (pp != p) {
@@ -2049,140 +2074,258 @@ __global__ __launch_bounds__(kTailNT) void k_tail(TailState t, Ctl *ctl) {
           return;
         }
       }
-      // relabel: roots numbered in node order; L = new id of the root.
-      // s_mrg is rebuilt for the next nodes: set when a component has a
-      // member other than its root.
-      for (int32_t v = threadIdx.x; v < nn; v += kTailNT) s_mrg[v] = 0;
-      const int32_t C = tail_scan(
-          nn, [&](int32_t v) { return s_sel[v] == v ? 1 : 0; }, s_newid,
-          wsum);
-      for (int32_t c = threadIdx.x; c < C; c += kTailNT) {
-        s_cap[c] = 0;
-        t.size[nxt][c] = 0;
-        t.minpt[nxt][c] = INT32_MAX;
-      }
-      for (int32_t q = threadIdx.x; q < C * d; q += kTailNT) t.S[nxt][q] = 0;
-      for (int32_t v = threadIdx.x; v < nn; v += kTailNT) {
+      // Step 4 statistics: members add into their roots (size and smallest
+      // point in LDS, the sums in global memory)
+      int32_t members = 0;
+      for (int32_t v = threadIdx.x; v < N; v += kTailNT) {
         const int32_t r = s_sel[v];
-        s_L[v] = s_newid[r];
-        if (r != v) s_mrg[s_newid[r]] = 1;
+        if (s_live[v] && r != v) {
+          ++members;
+          s_new[r] = 1;
+          atomicAdd(&s_size[r], s_size[v]);
+          atomicMin(&s_minpt[r], s_minpt[v]);
+        }
       }
+      members = wave_sum(members);
+      if (lane == 0 && members) atomicAdd(&s_cnt, members);
+      // lists of the members (in s_L, free after the hook) and of the
+      // merged roots (in s_pick, free after the choices)
+      int32_t *s_ml = s_L;
+      int32_t *s_rl = reinterpret_cast<int32_t *>(s_pick);
+      const int32_t nm = tail_scan(
+          N, [&](int32_t v) { return (s_live[v] && s_sel[v] != v) ? 1 : 0; },
+          s_pos, wsum);
+      for (int32_t v = threadIdx.x; v < N; v += kTailNT)
+        if (s_live[v] && s_sel[v] != v) s_ml[s_pos[v]] = v;
+      const int32_t nr =
+          tail_scan(N, [&](int32_t v) { return (int32_t)s_new[v]; }, s_nws, wsum);
+      for (int32_t v = threadIdx.x; v < N; v += kTailNT)
+        if (s_new[v]) s_rl[s_nws[v]] = v;
       __syncthreads();
-      // Step 4 statistics: every node adds itself to its component, the
-      // sums one (node, dimension) pair per thread so that loads coalesce.
-      // A window gets twice its summed degree when the table has room
-      // (ed entries in all): open addressing at load factor <= 1/2 keeps
-      // the probe chains short.
-      const int32_t spread =
-          2 * (int64_t)ed <= (int64_t)min(t.tcap, t.gcap) ? 2 : 1;
-      for (int32_t v = threadIdx.x; v < nn; v += kTailNT) {
-        const int32_t c = s_L[v];
-        wg_add(&t.size[nxt][c], s_size[v]);
-        wg_min(&t.minpt[nxt][c], s_minpt[v]);
-        atomicAdd(&s_cap[c], spread * s_deg[v]);
-      }
-      for (int32_t q0 = threadIdx.x; q0 < nn * d; q0 += kTU * kTailNT) {
+      // the members' sums, one (member, dimension) pair per thread
+      for (int32_t q0 = threadIdx.x; q0 < nm * d; q0 += kTU * kTailNT) {
         int64_t sv[kTU];
+        int32_t mv[kTU];
 #pragma unroll
         for (int j = 0; j < kTU; ++j) {
-          sv[j] = s.S[min(q0 + j * kTailNT, nn * d - 1)];  // no branch
+          const int32_t q = min(q0 + j * kTailNT, nm * d - 1);  // no branch
+          const int32_t m = s_ml[q / d];
+          mv[j] = m;
+          sv[j] = t.S[(int64_t)m * d + (q - (q / d) * d)];
         }
 #pragma unroll
         for (int j = 0; j < kTU; ++j) {
           const int32_t q = q0 + j * kTailNT;
-          if (q >= nn * d) break;
-          const int32_t v = q / d;
-          wg_add64(&t.S[nxt][(int64_t)s_L[v] * d + (q - v * d)], sv[j]);
+          if (q >= nm * d) break;
+          wg_add64(&t.S[(int64_t)s_sel[mv[j]] * d + (q - (q / d) * d)], sv[j]);
         }
       }
+      // rows that list a member are rebuilt: by symmetry, they are the
+      // rows that a member lists
+      const int32_t Pm = tail_scan(
+          N,
+          [&](int32_t v) {
+            return (s_live[v] && s_sel[v] != v) ? s_wl[v] : 0;
+          },
+          s_pos, wsum);
+      tail_entries<8>(s_pos, N, Pm, s_ws, tb,
+                      [&](int32_t, int32_t, uint64_t e) {
+                        const int32_t u = (int32_t)(e >> 32);
+                        if ((uint32_t)u < (uint32_t)N && s_sel[u] == u &&
+                            !s_new[u])
+                          s_touch[u] = 1;
+                      });
       __syncthreads();
-      for (int32_t q0 = threadIdx.x; q0 < C * d; q0 += kTU * kTailNT) {
+      // Step 4 means of the merged roots (their sums are complete)
+      for (int32_t q0 = threadIdx.x; q0 < nr * d; q0 += kTU * kTailNT) {
         int64_t sv[kTU];
-        int32_t zv[kTU];
 #pragma unroll
         for (int j = 0; j < kTU; ++j) {
-          const int32_t q = min(q0 + j * kTailNT, C * d - 1);  // no branch
-          sv[j] = t.S[nxt][q];
-          zv[j] = t.size[nxt][q / d];
+          const int32_t q = min(q0 + j * kTailNT, nr * d - 1);  // no branch
+          sv[j] = t.S[(int64_t)s_rl[q / d] * d + (q - (q / d) * d)];
         }
 #pragma unroll
         for (int j = 0; j < kTU; ++j) {
           const int32_t q = q0 + j * kTailNT;
-          if (q >= C * d) break;
-          const double m = (double)sv[j] / (double)zv[j];
-          t.mu[q] = m * sIF;
+          if (q >= nr * d) break;
+          const int32_t r = s_rl[q / d];
+          const double m = (double)sv[j] / (double)s_size[r];
+          t.mu[(int64_t)r * d + (q - (q / d) * d)] = m * sIF;
         }
       }
-      // next table: windows of summed degree, cleared
-      const int32_t slots =
-          tail_scan(C, [&](int32_t c) { return s_cap[c]; }, s_wn, wsum);
-      if (slots > t.tcap || slots > t.gcap) {
-        if (threadIdx.x == 0) raise_err(ctl, kErrInternal);
-        return;
-      }
-      for (int32_t q = threadIdx.x; q < slots; q += kTailNT)
-        t.tbl[1 - tc][q] = kEmpty;
-      if (threadIdx.x == 0) s_claims = 0;
+      // Step 4 contraction.  Windows: every rebuilt row gets its sources'
+      // summed entry count, twice when the table has room (open addressing
+      // at load factor <= 1/2 keeps the probe chains short).
+      auto rebuilt = [&](int32_t A) { return s_new[A] || s_touch[A]; };
+      for (int32_t v = threadIdx.x; v < N; v += kTailNT) s_cap[v] = 0;
       __syncthreads();
-      // Step 4 contraction, a thread per entry
-      int32_t claims = 0;
-      for (int32_t q0 = threadIdx.x; q0 < Q; q0 += kTU * kTailNT) {
-        uint64_t ev[kTU];
-        int32_t rv[kTU];
+      for (int32_t v = threadIdx.x; v < N; v += kTailNT)
+        if (s_live[v] && rebuilt(s_sel[v])) atomicAdd(&s_cap[s_sel[v]], s_deg[v]);
+      __syncthreads();
+      int32_t need = tail_scan(
+          N, [&](int32_t A) { return rebuilt(A) ? s_cap[A] : 0; }, s_nws, wsum);
+      // room for the new windows past the end of the table, else every
+      // live row is rebuilt into the other buffer
+      int spread = 2;
+      bool whole = false;
+      if (top + 2 * need > t.tcap) {
+        if (top + need <= t.tcap) {
+          spread = 1;
+        } else {
+          whole = true;
+          for (int32_t v = threadIdx.x; v < N; v += kTailNT) {
+            s_cap[v] = 0;
+            if (s_live[v] && s_sel[v] == v) s_touch[v] = 1;
+          }
+          __syncthreads();
+          for (int32_t v = threadIdx.x; v < N; v += kTailNT)
+            if (s_live[v]) atomicAdd(&s_cap[s_sel[v]], s_deg[v]);
+          __syncthreads();
+          need = tail_scan(
+              N, [&](int32_t A) { return rebuilt(A) ? s_cap[A] : 0; }, s_nws,
+              wsum);
+          spread = 2 * need <= t.tcap ? 2 : 1;
+          if (need > t.tcap) {
+            if (threadIdx.x == 0) raise_err(ctl, kErrInternal);
+            return;
+          }
+        }
+      }
+      const int tn = whole ? 1 - tc : tc;
+      const int32_t base = whole ? 0 : top;
+      uint64_t *tn_tbl = t.tbl[tn];
+      for (int32_t q = threadIdx.x; q < spread * need; q += kTailNT)
+        tn_tbl[base + q] = kEmpty;
+      for (int32_t v = threadIdx.x; v < N; v += kTailNT) s_ndeg[v] = 0;
+      // sources: the rows of every live node whose root is rebuilt
+      const int32_t Ps = tail_scan(
+          N,
+          [&](int32_t v) {
+            return (s_live[v] && rebuilt(s_sel[v])) ? s_wl[v] : 0;
+          },
+          s_pos, wsum);  // (its barrier also orders the clears above)
+      // every source entry (v, u, w) becomes (root of v, root of u, w) in
+      // the root's new window.  A thread's kIU entries probe together: each
+      // step issues one compare-and-swap per pending entry before waiting.
+      constexpr int kIU = 4;
+      for (int32_t p0 = threadIdx.x; p0 < Ps; p0 += kIU * kTailNT) {
+        int32_t A[kIU], B[kIU], W[kIU], np[kIU], pp[kIU], vv[kIU];
+        uint32_t h[kIU];
+        bool pend[kIU];
 #pragma unroll
-        for (int j = 0; j < kTU; ++j) {
-          const int32_t q = min(q0 + j * kTailNT, Q - 1);  // no branch
-          ev[j] = tb[q];
-          rv[j] = rows[q];
-        }
+        for (int j = 0; j < kIU; ++j) pp[j] = min(p0 + j * kTailNT, Ps - 1);
+        tail_rows<kIU>(s_pos, N, pp, vv);
 #pragma unroll
-        for (int j = 0; j < kTU; ++j) {
-          const uint64_t e = ev[j];
-          if (q0 + j * kTailNT >= Q || e == kEmpty) continue;
-          const int32_t A = s_L[rv[j]], B = s_L[(int32_t)(e >> 32)];
-          if (A == B) continue;  // edge inside a merged component
-          claims += tail_table_add(t.tbl[1 - tc], t.row[1 - tc], A, s_wn[A],
-                                   s_cap[A], B, (int32_t)(uint32_t)e, ctl)
-                        ? 1
-                        : 0;
+        for (int j = 0; j < kIU; ++j) {
+          const int32_t v = vv[j];
+          const uint64_t e = tb[s_ws[v] + (pp[j] - s_pos[v])];
+          const int32_t u = (int32_t)(e >> 32);
+          A[j] = s_sel[v];
+          B[j] = (e != kEmpty && (uint32_t)u < (uint32_t)N &&
+                  p0 + j * kTailNT < Ps)
+                     ? s_sel[u]
+                     : A[j];  // nothing to add
+          W[j] = (int32_t)(uint32_t)e;
+          pend[j] = A[j] != B[j];  // not inside a component
+          np[j] = 0;
+          h[j] = pend[j] ? ((uint32_t)B[j] * 2654435761u) %
+                               (uint32_t)(spread * s_cap[A[j]])
+                         : 0u;
+        }
+        for (bool any = true; any;) {
+          uint64_t cur[kIU];
+          bool got[kIU];
+#pragma unroll
+          for (int j = 0; j < kIU; ++j) {
+            cur[j] = kEmpty;
+            got[j] = false;
+            if (pend[j])
+              got[j] = __hip_atomic_compare_exchange_strong(
+                  tn_tbl + base + spread * s_nws[A[j]] + h[j], &cur[j],
+                  ((uint64_t)(uint32_t)B[j] << 32) | (uint32_t)W[j],
+                  __ATOMIC_RELAXED, __ATOMIC_RELAXED,
+                  __HIP_MEMORY_SCOPE_WORKGROUP);
+          }
+          any = false;
+#pragma unroll
+          for (int j = 0; j < kIU; ++j) {
+            if (!pend[j]) continue;
+            const int32_t cap = spread * s_cap[A[j]];
+            if (got[j]) {
+              atomicAdd(&s_ndeg[A[j]], 1);
+              pend[j] = false;
+            } else if ((int32_t)(cur[j] >> 32) == B[j]) {
+              __hip_atomic_fetch_add(tn_tbl + base + spread * s_nws[A[j]] + h[j],
+                                     (uint64_t)(uint32_t)W[j], __ATOMIC_RELAXED,
+                                     __HIP_MEMORY_SCOPE_WORKGROUP);
+              pend[j] = false;
+            } else if (++np[j] >= cap) {
+              raise_err(ctl, kErrInternal);
+              pend[j] = false;
+            } else {
+              h[j] = h[j] + 1 == (uint32_t)cap ? 0u : h[j] + 1;
+              any = true;
+            }
+          }
         }
       }
-      claims = wave_sum(claims);
-      if (lane == 0 && claims) atomicAdd(&s_claims, claims);
-      for (int32_t i = threadIdx.x; i < t.nn0; i += kTailNT)
-        t.Mt[i] = s_L[t.Mt[i]];
       __syncthreads();
-      ed = s_claims;
-      nn = C;
-      Q = slots;
-      cur = nxt;
-      tc = 1 - tc;
-      int32_t *sw = s_ws;
-      s_ws = s_wn;
-      s_wn = sw;
+      // the new state: rebuilt windows, members dead, merge flags for the
+      // next round's selection, the map of the tail's start nodes
+      for (int32_t v = threadIdx.x; v < N; v += kTailNT) {
+        if (s_live[v] && s_sel[v] != v) {
+          s_live[v] = 0;
+          s_deg[v] = 0;
+          s_wl[v] = 0;
+        } else if (s_live[v] && rebuilt(v)) {
+          s_ws[v] = base + spread * s_nws[v];
+          s_wl[v] = spread * s_cap[v];
+          s_deg[v] = s_ndeg[v];
+        }
+        s_mrg[v] = s_new[v];
+        s_Mt[v] = s_sel[s_Mt[v]];
+      }
       __syncthreads();
-      if (nn == 1) break;  // a single component is left
+      for (int32_t v = threadIdx.x; v < N; v += kTailNT) {
+        s_new[v] = 0;
+        s_touch[v] = 0;
+        s_sel[v] = v;
+      }
+      nn -= s_cnt;
+      top = base + spread * need;
+      tc = tn;
+      ed = tail_scan(N, [&](int32_t v) { return s_deg[v]; }, s_nws, wsum);
+      if (threadIdx.x == 0) s_cnt = 0;
+      __syncthreads();
     }
-    // level end: snapshot for the labels and the energy
+    // level end: live nodes numbered in id order, snapshots for the labels
+    // and the energy
+    const int32_t C = tail_scan(
+        N, [&](int32_t v) { return (int32_t)s_live[v]; }, s_pos, wsum);
     if (threadIdx.x == 0) {
-      t.lvl_nc[l] = nn;
+      t.lvl_nc[l] = C;
       s_cut = 0;
     }
-    for (int32_t i = threadIdx.x; i < t.nn0; i += kTailNT)
-      t.lvl_map[(int64_t)l * t.nn0 + i] = t.Mt[i];
+    for (int32_t i = threadIdx.x; i < N; i += kTailNT) {
+      t.lvl_map[(int64_t)l * N + i] = s_pos[s_Mt[i]];
+      if (s_live[i]) t.lvl_minpt[(int64_t)l * N + s_pos[i]] = s_minpt[i];
+    }
     // (the canonical numbers, ranks of these smallest points, are counted
     // after the tail by k_tail_rank on many CUs)
-    for (int32_t c = threadIdx.x; c < nn; c += kTailNT)
-      t.lvl_minpt[(int64_t)l * t.nn0 + c] = t.minpt[cur][c];
     __syncthreads();
     if (t.want_energy) {
-      for (int64_t q = threadIdx.x; q < (int64_t)nn * d; q += kTailNT)
-        t.lvl_mu[(int64_t)l * t.nn0 * d + q] = t.mu[q];
-      long long acc = 0;
-      for (int32_t q = threadIdx.x; q < Q; q += kTailNT) {
-        const uint64_t e = t.tbl[tc][q];
-        if (e != kEmpty) acc += (int32_t)(uint32_t)e;
+      for (int32_t q = threadIdx.x; q < N * d; q += kTailNT) {
+        const int32_t v = q / d;
+        if (s_live[v])
+          t.lvl_mu[((int64_t)l * N + s_pos[v]) * d + (q - v * d)] = t.mu[q];
       }
+      const int32_t Pc = tail_scan(
+          N, [&](int32_t v) { return s_live[v] ? s_wl[v] : 0; }, s_nws, wsum);
+      long long acc = 0;
+      tail_entries(s_nws, N, Pc, s_ws, t.tbl[tc],
+                   [&](int32_t, int32_t, uint64_t e) {
+                     acc += (int32_t)(uint32_t)e;
+                   });
       acc = wave_sum(acc);
       if (lane == 0 && acc)
         atomicAdd(reinterpret_cast<unsigned long long *>(&s_cut),
@@ -2243,9 +2386,10 @@ __global__ __launch_bounds__(256) void k_tail_labels(
   }
 }
 
-// Rows of the table the tail starts from, packed end to end (the windows of
-// the multi-kernel path hold their rows at the front and may be larger).
-// A wave per row, lanes striding over its entries (hub rows are long).
+// Rows of the table the tail starts from, copied into windows packed end
+// to end, each row's entries moved to the front of its window (wl2 = the
+// entry count).  A wave per row, lanes striding over its slots (hub rows
+// are long).
 __global__ __launch_bounds__(256) void k_repack(
     int32_t nn, const int32_t *__restrict__ ws, const int32_t *__restrict__ wl,
     const uint64_t *__restrict__ tbl, const int32_t *__restrict__ ws2,
@@ -2257,8 +2401,16 @@ __global__ __launch_bounds__(256) void k_repack(
   const int32_t len = wl[v];
   const uint64_t *src = tbl + ws[v];
   uint64_t *dst = tbl2 + ws2[v];
-  for (int32_t j = lane; j < len; j += kWave) dst[j] = src[j];
-  if (lane == 0) wl2[v] = len;
+  int32_t cnt = 0;
+  for (int32_t j0 = 0; j0 < len; j0 += kWave) {
+    const int32_t j = j0 + lane;
+    const uint64_t e = j < len ? src[j] : kEmpty;
+    const uint64_t m = __ballot(e != kEmpty);
+    if (e != kEmpty)
+      dst[cnt + __popcll(m & ((1ull << lane) - 1ull))] = e;
+    cnt += __popcll(m);
+  }
+  if (lane == 0) wl2[v] = cnt;
 }
 
 // ---------------------------------------------------------------------------
@@ -3283,10 +3435,10 @@ struct Bufs {
   int32_t *lch_i, *lch_j;  // chunks of long contributor rows
   int32_t lch_cap;
   int32_t nt;  // nodes the tail can start from
-  double *tgain;    // per-slot gains in the tail
-  int32_t *trow[2]; // per-slot rows in the tail
-  int32_t tslots;   // entries of tgain
-  int32_t *Mt, *lvl_map, *lvl_minpt, *lvl_rank;
+  double *tgain;    // per-edge gains in the tail
+  uint64_t *telist; // the tail's edges to evaluate
+  int32_t tslots;   // entries of tgain and telist
+  int32_t *lvl_map, *lvl_minpt, *lvl_rank;
   double *lvl_mu;
   int32_t *bsum, *tmp;
   double *partial;
@@ -3369,11 +3521,9 @@ void carve(Arena &a, int32_t n, int32_t d, int32_t k, bool link, Bufs *b) {
   b->mark = a.take<int32_t>(n1);
   b->lrank = a.take<int32_t>(n1);
   b->nt = std::min<int32_t>(n, kTailNodes);
-  b->Mt = a.take<int32_t>(b->nt);
-  b->tslots = (int32_t)std::min<int64_t>(ed, kTailSlots);
+  b->tslots = (int32_t)std::min<int64_t>(2 * ed, kTailSlots);
   b->tgain = a.take<double>(b->tslots);
-  b->trow[0] = a.take<int32_t>(b->tslots);
-  b->trow[1] = a.take<int32_t>(b->tslots);
+  b->telist = a.take<uint64_t>(b->tslots);
   b->lvl_map = a.take<int32_t>((size_t)kTailLevels * b->nt);
   b->lvl_minpt = a.take<int32_t>((size_t)kTailLevels * b->nt);
   b->lvl_rank = a.take<int32_t>((size_t)kTailLevels * b->nt);
@@ -3825,15 +3975,13 @@ int run_tail(const LadderArgs &g, const Bufs &b, const float *emb,
     t.ws[j] = b.ws[j];
     t.wl[j] = b.wl[j];
     t.tbl[j] = b.tbl[j];
-    t.size[j] = b.size[j];
-    t.minpt[j] = b.minpt[j];
-    t.S[j] = b.S[j];
   }
+  t.size = b.size[cur];
+  t.minpt = b.minpt[cur];
+  t.S = b.S[cur];
   t.mu = b.mu;
   t.gain = b.tgain;
-  t.row[0] = b.trow[0];
-  t.row[1] = b.trow[1];
-  t.Mt = b.Mt;
+  t.elist = b.telist;
   t.lvl_map = b.lvl_map;
   t.lvl_minpt = b.lvl_minpt;
   t.lvl_nc = ctl->tail_nc;  // read back with the control block
@@ -3841,8 +3989,6 @@ int run_tail(const LadderArgs &g, const Bufs &b, const float *emb,
   t.lvl_mu = b.lvl_mu;
   t.lvl_cut2 = reinterpret_cast<long long *>(ctl->tail_cut2);
   t.nn0 = nn;
-  t.ed0 = ed;
-  t.cur0 = cur;
   // the table goes to the other buffer, its rows packed: the tail's passes
   // run over the entries only
   const int nxt = 1 - cur;
