@@ -5,15 +5,18 @@
 // hidden layers.
 //
 // The layers are dense contractions, so they run on the matrix cores:
-// v_mfma_f32_32x32x8_bf16 in transposed form, D[unit][point] =
+// v_mfma_f32_32x32x16_bf16 (CDNA4) in transposed form, D[unit][point] =
 // sum_k W[k][unit] * X[point][k], one wave per tile of 32 points.  With the
 // weights as the A operand and the activations as the B operand, the
-// accumulator layout of one layer (lane l holds point l % 32, units
-// 8 (r / 4) + 4 (l / 32) + r % 4 in register r) is exactly the B-operand
-// layout of the next layer's four K = 8 steps (step s takes registers
-// 4s .. 4s + 3).  So the three layers chain in registers: the weights are
-// loaded once per wave, and every point costs one read of its features and
-// one write of its embedding.
+// accumulator of one layer (lane l holds point l % 32, units
+// 8 (r / 4) + 4 (l / 32) + r % 4 in register r) feeds the next layer's two
+// K = 16 steps directly: step s takes registers 8s .. 8s + 7 of each lane
+// as its eight B elements, and the A operand pairs each of those K slots
+// with the weight row of the unit that register holds (the pairing of A and
+// B elements to K slots is the same for both operands, so only the unit of
+// each slot has to match).  The three layers chain in registers: the
+// weights are loaded once per wave, and every point costs one read of its
+// features and one write of its embedding.
 #include <algorithm>
 
 #include "ezsp_internal.h"
@@ -22,7 +25,8 @@ namespace ezsp {
 
 namespace {
 
-typedef short bf16x4 __attribute__((ext_vector_type(4)));
+typedef short s16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 
 constexpr int kMlpHidden = 32;
@@ -39,32 +43,56 @@ __device__ __forceinline__ int acc_unit(int r, int lane) {
   return 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
 }
 
-// A operand of K-step s: lane l gives W[8 s + 4 (l / 32) + i][l % 32],
-// zero outside d_rows x d_cols.
-__device__ __forceinline__ bf16x4 weight_operand(const uint16_t *w,
-                                                 int d_rows, int d_cols,
-                                                 int s, int lane) {
-  bf16x4 a;
-  const int m = lane & 31;
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int k = 8 * s + 4 * (lane >> 5) + i;
-    a[i] = (k < d_rows && m < d_cols) ? (short)w[k * d_cols + m] : (short)0;
-  }
-  return a;
+// Input unit of element i of lane l's operands in K-step s of a hidden
+// layer: the unit of accumulator register 8 s + i in lane l.
+__device__ __forceinline__ int step_unit(int s, int i, int lane) {
+  return acc_unit(8 * s + i, lane);
 }
 
-// bias + ReLU, then the next layer's B operands (four K-steps)
+// A operand of K-step s of a hidden layer: lane l gives
+// W[step_unit(s, i, l)][l % 32], zero outside d_rows x d_cols.
+__device__ __forceinline__ bf16x8 weight_operand(const uint16_t *w,
+                                                 int d_rows, int d_cols,
+                                                 int s, int lane) {
+  s16x8 a;
+  const int m = lane & 31;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const int k = step_unit(s, i, lane);
+    a[i] = (k < d_rows && m < d_cols) ? (short)w[k * d_cols + m] : (short)0;
+  }
+  return __builtin_bit_cast(bf16x8, a);
+}
+
+// A operand of the first layer: element i of lane l is input feature
+// 8 (l / 32) + i (the B operand holds the same feature of each point).
+__device__ __forceinline__ bf16x8 input_weight_operand(const uint16_t *w,
+                                                       int d_rows, int d_cols,
+                                                       int lane) {
+  s16x8 a;
+  const int m = lane & 31;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const int k = 8 * (lane >> 5) + i;
+    a[i] = (k < d_rows && m < d_cols) ? (short)w[k * d_cols + m] : (short)0;
+  }
+  return __builtin_bit_cast(bf16x8, a);
+}
+
+// bias + ReLU, then the next layer's B operands (two K-steps)
 __device__ __forceinline__ void hidden_operands(const f32x16 &acc,
                                                 const float *bias_r,
-                                                bf16x4 h[4]) {
+                                                bf16x8 h[2]) {
 #pragma unroll
-  for (int s = 0; s < 4; ++s)
+  for (int s = 0; s < 2; ++s) {
+    s16x8 b;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const float v = acc[4 * s + i] + bias_r[4 * s + i];
-      h[s][i] = to_bf16(v > 0.0f ? v : 0.0f);
+    for (int i = 0; i < 8; ++i) {
+      const float v = acc[8 * s + i] + bias_r[8 * s + i];
+      b[i] = to_bf16(v > 0.0f ? v : 0.0f);
     }
+    h[s] = __builtin_bit_cast(bf16x8, b);
+  }
 }
 
 template <bool VEC4>
@@ -79,10 +107,10 @@ __global__ __launch_bounds__(256) void k_mlp(
                                  threadIdx.x / kWave);
   const int32_t n_waves = (int32_t)(gridDim.x * (blockDim.x / kWave));
   // weights (A operands) and the biases of this lane's accumulator rows
-  const bf16x4 a1 = weight_operand(w1, d_in, kMlpHidden, 0, lane);
-  bf16x4 a2[4], a3[4];
+  const bf16x8 a1 = input_weight_operand(w1, d_in, kMlpHidden, lane);
+  bf16x8 a2[2], a3[2];
 #pragma unroll
-  for (int s = 0; s < 4; ++s) {
+  for (int s = 0; s < 2; ++s) {
     a2[s] = weight_operand(w2, kMlpHidden, kMlpHidden, s, lane);
     a3[s] = weight_operand(w3, kMlpHidden, d_out, s, lane);
   }
@@ -97,30 +125,29 @@ __global__ __launch_bounds__(256) void k_mlp(
   const int32_t n_tiles = (n + 31) / 32;
   for (int32_t t = wave; t < n_tiles; t += n_waves) {
     const int32_t p = t * 32 + (lane & 31);
-    // layer 1: B operand = features 4 (l / 32) .. + 3 of point p
-    bf16x4 xb;
+    // layer 1: B operand = features 8 (l / 32) .. + 7 of point p
+    s16x8 xs;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int k = 4 * (lane >> 5) + i;
-      xb[i] = (p < n && k < d_in) ? (short)x[(int64_t)p * d_in + k] : (short)0;
+    for (int i = 0; i < 8; ++i) {
+      const int k = 8 * (lane >> 5) + i;
+      xs[i] = (p < n && k < d_in) ? (short)x[(int64_t)p * d_in + k] : (short)0;
     }
     f32x16 acc = {0};
-    acc = __builtin_amdgcn_mfma_f32_32x32x8bf16_1k(a1, xb, acc, 0, 0, 0);
-    bf16x4 h[4];
+    acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+        a1, __builtin_bit_cast(bf16x8, xs), acc, 0, 0, 0);
+    bf16x8 h[2];
     hidden_operands(acc, c1, h);
     // layer 2
     acc = f32x16{0};
 #pragma unroll
-    for (int s = 0; s < 4; ++s)
-      acc = __builtin_amdgcn_mfma_f32_32x32x8bf16_1k(a2[s], h[s], acc, 0, 0,
-                                                     0);
+    for (int s = 0; s < 2; ++s)
+      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a2[s], h[s], acc, 0, 0, 0);
     hidden_operands(acc, c2, h);
     // layer 3
     acc = f32x16{0};
 #pragma unroll
-    for (int s = 0; s < 4; ++s)
-      acc = __builtin_amdgcn_mfma_f32_32x32x8bf16_1k(a3[s], h[s], acc, 0, 0,
-                                                     0);
+    for (int s = 0; s < 2; ++s)
+      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a3[s], h[s], acc, 0, 0, 0);
     if (p < n) {
       float *o = out + (int64_t)p * d_out;
       if (VEC4) {  // registers 4g .. 4g + 3 are four consecutive units
