@@ -603,6 +603,19 @@ def main():
         "n_comp": [int(x) for x in n_comp],
         "parity": None,
     }
+    if dom == "knn_query":
+        # the kNN's walk, from its counting instantiation, after the timed
+        # steps: buckets of 16 candidates scanned and inner nodes entered
+        # per 16-point query group
+        _, scans, nodes = ezsp.knn_walk_stats(xyz, sc.k)
+        scans = scans.double()
+        out["knn_walk"] = {
+            "groups": int(scans.numel()),
+            "scans_per_group": round(float(scans.mean()), 3),
+            "scans_per_group_max": int(scans.max()),
+            "nodes_per_group": round(float(nodes.double().mean()), 3),
+            "candidates_per_query": round(16.0 * float(scans.mean()), 1)}
+        del scans, nodes
     ok = True
     if not args.no_cpu:
         print("[bench] cpu baseline (oracle)", file=sys.stderr, flush=True)

@@ -108,6 +108,18 @@ size_t ezsp_knn_workspace_size(int64_t n, int32_t k);
 int ezsp_knn(const float *xyz, int64_t n, int32_t k, int32_t *nbr, float *d2,
              void *ws, size_t ws_bytes, void *stream);
 
+/* ezsp_knn (same nbr, workspace and errors) with the statistics of its
+ * tree walk, for inspection outside timed work: points are sorted into
+ * Morton order and cut into groups of 16 consecutive points that walk the
+ * box tree together; group g (0 <= g < ceil(n / 16)) gets
+ *   group_scans[g]  the buckets of 16 points whose candidates it scanned,
+ *                   its own included
+ *   group_nodes[g]  the inner tree nodes it entered
+ * (both int32, device memory, written in full).  Stream-asynchronous. */
+int ezsp_knn_walk_stats(const float *xyz, int64_t n, int32_t k, int32_t *nbr,
+                        int32_t *group_scans, int32_t *group_nodes, void *ws,
+                        size_t ws_bytes, void *stream);
+
 /* ---- partition (Sec. 3.2: Eq. gmpp, Prop. 1, Steps 0-4, hierarchical
  * partition; App. Alg. A-1, A-2) ----------------------------------------- */
 

@@ -200,6 +200,29 @@ int ezsp_knn(const float *xyz, int64_t n, int32_t k, int32_t *nbr, float *d2,
                    "knn launch");
 }
 
+int ezsp_knn_walk_stats(const float *xyz, int64_t n, int32_t k, int32_t *nbr,
+                        int32_t *group_scans, int32_t *group_nodes, void *ws,
+                        size_t ws_bytes, void *stream) {
+  set_error("%s", "");
+  if (!xyz || !nbr || !group_scans || !group_nodes || !ws)
+    return fail(EZSP_ERR_INVALID_ARG, "pointers must not be NULL");
+  if (!n_ok(n)) return fail(EZSP_ERR_INVALID_ARG, "n must be in [1, 2^31 - 256]");
+  if (k < 1 || k > 64) return fail(EZSP_ERR_INVALID_ARG, "k must be in 1..64");
+  if ((int64_t)n * k >= kMaxN)
+    return fail(EZSP_ERR_INVALID_ARG, "n*k must stay below 2^31");
+  if (ws_bytes < ezsp_knn_workspace_size(n, k))
+    return fail(EZSP_ERR_WORKSPACE, "workspace smaller than the queried size");
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  Arena a = open_ws(ws, ws_bytes);
+  Ctl *ctl = a.take<Ctl>(1);
+  KnnWork w;
+  knn_reserve(a, (int32_t)n, k, &w);
+  hipLaunchKernelGGL(k_ctl_init, dim3(1), dim3(64), 0, st, ctl);
+  return check_hip(knn_launch_stats(xyz, (int32_t)n, k, ctl, w, nbr,
+                                    group_scans, group_nodes, st),
+                   "knn launch");
+}
+
 int ezsp_sync_status(const void *ws, size_t ws_bytes, void *stream) {
   set_error("%s", "");
   if (!ws && ws_bytes == 0) {  // the static scratch of ezsp_knn_noalloc

@@ -116,6 +116,12 @@ hipError_t knn_launch(const float *xyz, int32_t n, int32_t k, Ctl *ctl,
 hipError_t knn_launch_emb(const float *xyz, int32_t n, int32_t k, Ctl *ctl,
                           const KnnWork &w, const float *emb, int32_t d,
                           float *emb_out, hipStream_t st);
+// knn_launch with the walk statistics: per 16-point query group, the
+// buckets scanned (st_scan) and the inner tree nodes entered (st_node).
+hipError_t knn_launch_stats(const float *xyz, int32_t n, int32_t k, Ctl *ctl,
+                            const KnnWork &w, int32_t *nbr_out,
+                            int32_t *st_scan, int32_t *st_node,
+                            hipStream_t st);
 
 // Merge ladder on a neighbour table (internal ids; perm/inv may be null
 // when internal == original order).

@@ -370,8 +370,10 @@ __device__ __forceinline__ void set_level_bits(uint64_t &mlo, uint64_t &mhi,
 // walks the tree on its own (group-uniform decisions from a 16-lane vote);
 // the four groups of a wave alternate between finding their next bucket and
 // scanning it together.  A node is entered when some lane's box distance
-// does not exceed that lane's current k-th distance.
-template <int K>
+// does not exceed that lane's current k-th distance.  ST: also count, per
+// group, the buckets it scans (its own included) and the inner nodes it
+// enters (st_scan, st_node; the walk statistics, a separate instantiation).
+template <int K, bool ST = false>
 __global__ __launch_bounds__(256) void k_knn_query(
     const float4 *__restrict__ pts, const int32_t *__restrict__ inv,
     int32_t n, const float4 *__restrict__ blo, const float4 *__restrict__ bhi,
@@ -379,7 +381,7 @@ __global__ __launch_bounds__(256) void k_knn_query(
     int32_t *__restrict__ nbr_out, float *__restrict__ d2_out,
     uint64_t *__restrict__ kth_out, int32_t n_blocks,
     const float4 *__restrict__ emb, int32_t d4, float4 *__restrict__ emb_out,
-    Ctl *ctl) {
+    Ctl *ctl, int32_t *__restrict__ st_scan, int32_t *__restrict__ st_node) {
   const int32_t lb = xcd_block();
   if (lb >= n_blocks) return;
   // level offsets and counts of the box tree, indexed per lane in the walk
@@ -415,6 +417,7 @@ __global__ __launch_bounds__(256) void k_knn_query(
   // own bucket and its Morton neighbours first: a tight k-th distance early
   // (the two Morton neighbours are the first buckets of the scan loop below)
   if (gvalid) scan_bucket<K, true>(pts, grp, lane16, p.x, p.y, p.z, me, key);
+  int32_t c_scan = 1, c_node = 0;  // walk statistics (ST only)
   if (emb) {  // every lane of the wave is here
     uint32_t m = 0;
     bool bad = false;
@@ -497,11 +500,19 @@ __global__ __launch_bounds__(256) void k_knn_query(
                                       node * kFan, qlo, qhi, gk, lane16,
                                       gshift);
       set_level_bits(mlo, mhi, l - 1, m8);
+      if constexpr (ST) ++c_node;
     }
     if (__ballot(leaf >= 0) == 0) break;
     if (leaf >= 0) {
       scan_bucket<K, false>(pts, leaf, lane16, p.x, p.y, p.z, me, key);
       gk = group_max_kth(act ? (uint32_t)(key[K - 1] >> 32) : 0u);
+      if constexpr (ST) ++c_scan;
+    }
+  }
+  if constexpr (ST) {
+    if (lane16 == 0) {  // the walk is uniform over the group
+      st_scan[grp] = c_scan;
+      st_node[grp] = c_node;
     }
   }
 
@@ -559,6 +570,7 @@ void knn_reserve(Arena &a, int32_t n, int32_t k, KnnWork *w) {
 static hipError_t knn_impl(const float *xyz, int32_t n, int32_t k, Ctl *ctl,
                            const KnnWork &s, int32_t *nbr_out, float *d2_out,
                            const float *emb, int32_t d, float *emb_out,
+                           int32_t *st_scan, int32_t *st_node,
                            hipStream_t st) {
   const KnnWork &w = s;
   const Tree tree = make_tree(n);
@@ -590,9 +602,17 @@ static hipError_t knn_impl(const float *xyz, int32_t n, int32_t k, Ctl *ctl,
   switch (knn_template_k(k)) {
 #define EZSP_KNN_CASE(KK)                                                    \
   case KK:                                                                   \
-    hipLaunchKernelGGL(k_knn_query<KK>, grid, dim3(nt), 0, st, s.pts, w.inv, \
-                       n, s.blo, s.bhi, tree, k, w.nbr_int, nbr_out, d2_out, \
-                       w.kth, qblocks, emb4, d / 4, emb_out4, ctl);          \
+    if (st_scan)                                                             \
+      hipLaunchKernelGGL((k_knn_query<KK, true>), grid, dim3(nt), 0, st,     \
+                         s.pts, w.inv, n, s.blo, s.bhi, tree, k, w.nbr_int,  \
+                         nbr_out, d2_out, w.kth, qblocks, emb4, d / 4,       \
+                         emb_out4, ctl, st_scan, st_node);                   \
+    else                                                                     \
+      hipLaunchKernelGGL(k_knn_query<KK>, grid, dim3(nt), 0, st, s.pts,      \
+                         w.inv, n, s.blo, s.bhi, tree, k, w.nbr_int,         \
+                         nbr_out, d2_out, w.kth, qblocks, emb4, d / 4,       \
+                         emb_out4, ctl, (int32_t *)nullptr,                  \
+                         (int32_t *)nullptr);                                \
     break;
     EZSP_KNN_CASE(4)
     EZSP_KNN_CASE(8)
@@ -616,7 +636,15 @@ hipError_t knn_launch(const float *xyz, int32_t n, int32_t k, Ctl *ctl,
                       const KnnWork &s, int32_t *nbr_out, float *d2_out,
                       hipStream_t st) {
   return knn_impl(xyz, n, k, ctl, s, nbr_out, d2_out, nullptr, 0, nullptr,
-                  st);
+                  nullptr, nullptr, st);
+}
+
+hipError_t knn_launch_stats(const float *xyz, int32_t n, int32_t k, Ctl *ctl,
+                            const KnnWork &s, int32_t *nbr_out,
+                            int32_t *st_scan, int32_t *st_node,
+                            hipStream_t st) {
+  return knn_impl(xyz, n, k, ctl, s, nbr_out, nullptr, nullptr, 0, nullptr,
+                  st_scan, st_node, st);
 }
 
 hipError_t knn_launch_emb(const float *xyz, int32_t n, int32_t k, Ctl *ctl,
@@ -625,7 +653,8 @@ hipError_t knn_launch_emb(const float *xyz, int32_t n, int32_t k, Ctl *ctl,
   if (d % 4 != 0 || d > 16 || (reinterpret_cast<uintptr_t>(emb) & 15) != 0 ||
       (reinterpret_cast<uintptr_t>(emb_out) & 15) != 0)
     return hipErrorInvalidValue;
-  return knn_impl(xyz, n, k, ctl, s, nullptr, nullptr, emb, d, emb_out, st);
+  return knn_impl(xyz, n, k, ctl, s, nullptr, nullptr, emb, d, emb_out,
+                  nullptr, nullptr, st);
 }
 
 }  // namespace ezsp

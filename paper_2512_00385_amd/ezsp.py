@@ -38,6 +38,7 @@ ENTRY_POINTS = (
     "ezsp_edge_loss_workspace_size", "ezsp_edge_loss",
     "ezsp_purity_workspace_size", "ezsp_purity",
     "ezsp_embed_mlp", "ezsp_sync_status", "ezsp_knn_noalloc",
+    "ezsp_knn_walk_stats",
 )
 
 
@@ -112,6 +113,8 @@ def load() -> ctypes.CDLL:
                                           P, P, P, P]),
         "ezsp_sync_status": (ctypes.c_int, [P, sz, P]),
         "ezsp_knn_noalloc": (ctypes.c_int, [P, i64, i32, P, P, P]),
+        "ezsp_knn_walk_stats": (ctypes.c_int, [P, i64, i32, P, P, P, P, sz,
+                                               P]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -230,6 +233,26 @@ def knn(xyz: torch.Tensor, k: int, want_d2: bool = False, sync: bool = True):
         pending.check()
         return (nbr, d2) if want_d2 else nbr
     return ((nbr, d2) if want_d2 else (nbr,)) + (pending,)
+
+
+def knn_walk_stats(xyz: torch.Tensor, k: int):
+    """ezsp_knn_walk_stats: (nbr [n, k] int32, buckets scanned and inner
+    nodes entered per 16-point query group, each [ceil(n / 16)] int32)."""
+    lib = load()
+    xyz = _dev_tensor(xyz, torch.float32, "xyz", 3)
+    n = xyz.shape[0]
+    dev = xyz.device
+    g = (n + 15) // 16
+    nbr = torch.empty((n, k), dtype=torch.int32, device=dev)
+    scans = torch.empty(g, dtype=torch.int32, device=dev)
+    nodes = torch.empty(g, dtype=torch.int32, device=dev)
+    nbytes = lib.ezsp_knn_workspace_size(n, k)
+    ws = _workspace(nbytes, dev)
+    _check(lib.ezsp_knn_walk_stats(_ptr(xyz), n, int(k), _ptr(nbr),
+                                   _ptr(scans), _ptr(nodes), _ptr(ws), nbytes,
+                                   _stream(dev)), "ezsp_knn_walk_stats")
+    Pending(ws, nbytes, dev, "ezsp_knn_walk_stats").check()
+    return nbr, scans, nodes
 
 
 def partition_workspace_size(n: int, d: int, k: int, n_levels: int = 1):

@@ -89,6 +89,20 @@ def test_knn_rejects_bad_arguments():
     assert "workspace" in ezsp.last_error()
 
 
+def test_knn_walk_stats_rejects_bad_arguments():
+    lib = ezsp.load()
+
+    def call(n=100, k=10, xyz=FAKE, nbr=FAKE, scans=FAKE, nodes=FAKE,
+             ws=FAKE, ws_bytes=1 << 40):
+        return lib.ezsp_knn_walk_stats(xyz, n, k, nbr, scans, nodes, ws,
+                                       ws_bytes, None)
+    assert call(n=0) == ezsp.ERR_INVALID_ARG
+    assert call(k=65) == ezsp.ERR_INVALID_ARG
+    assert call(scans=None) == ezsp.ERR_INVALID_ARG
+    assert call(nodes=None) == ezsp.ERR_INVALID_ARG
+    assert call(ws_bytes=16) == ezsp.ERR_WORKSPACE
+
+
 def call_partition(n=100, d=8, k=10, lambdas=(0.1,), min_size=None,
                    max_rounds=0, flags=0, ws_bytes=1 << 40, xyz=FAKE,
                    labels=FAKE, n_comp=FAKE, params="ok"):
