@@ -717,15 +717,6 @@ __global__ __launch_bounds__(256) void k_select_combine(
   }
 }
 
-// The next round's merged flags: a component of more than one member.
-__global__ __launch_bounds__(256) void k_merged(const int32_t *moff,
-                                                uint8_t *merged, Ctl *ctl) {
-  if (!round_live(ctl)) return;
-  int32_t c;
-  if (!xcd_item(ctl->n_next, c)) return;
-  merged[c] = (moff[c + 1] - moff[c] > 1) ? 1 : 0;
-}
-
 // ---------------------------------------------------------------------------
 // Step 3: merge graph -> forest -> components
 // ---------------------------------------------------------------------------
@@ -906,16 +897,24 @@ __global__ __launch_bounds__(256) void k_assign(int32_t nn,
   if (act) rank[v] = base + __popcll(mine & ((1ull << lane) - 1));
 }
 
+// Members in component order; the first member of each component also
+// writes the next round's merged flag (a component of more than one
+// member), so every component's flag is written once.
 __global__ __launch_bounds__(256) void k_place(int32_t nn, const int32_t *L,
                                                const int32_t *moff,
                                                const int32_t *rank,
-                                               int32_t *mem, Ctl *ctl) {
+                                               int32_t *mem, uint8_t *merged,
+                                               Ctl *ctl) {
   if (!round_live(ctl)) return;
   const int32_t v = xcd_tid();
   if (v >= nn) return;
-  const int32_t pos = moff[L[v]] + rank[v];
+  const int32_t c = L[v];
+  const int32_t r = rank[v];
+  const int32_t m0 = moff[c];
+  const int32_t pos = m0 + r;
   if ((uint32_t)pos < (uint32_t)nn) {
     mem[pos] = v;
+    if (r == 0) merged[c] = (moff[c + 1] - m0 > 1) ? 1 : 0;
   } else {
     raise_err(ctl, kErrInternal);
   }
@@ -3607,9 +3606,7 @@ void launch_round(const Bufs &b, const Adj &adj, int cur, int32_t n,
   device_scan(ScanArray{b.cnt, b.moff, nn, &ctl->n_next}, nn + 1, b.bsum,
               b.tmp, st);
   hipLaunchKernelGGL(k_place, xblocks_for(nn), dim3(256), 0, st, nn, b.L,
-                     b.moff, b.rank, b.mem, ctl);
-  hipLaunchKernelGGL(k_merged, xblocks_for(nn), dim3(256), 0, st, b.moff,
-                     b.merged, ctl);
+                     b.moff, b.rank, b.mem, b.merged, ctl);
 
   // contraction chunks: enough blocks to fill the chip, at most kChunk
   int32_t chunk = kChunk;
