@@ -1562,20 +1562,50 @@ __global__ __launch_bounds__(256) void k_contract_long(
     stripe_add(ctl->e_next_s, added);
 }
 
-// point -> current node map, composed every merging round
-template <bool FIRST>
-__global__ __launch_bounds__(256) void k_compose(int32_t n, int32_t nn,
-                                                 int32_t *M, const int32_t *L,
-                                                 Ctl *ctl) {
+// point -> node map after the first round (internal point i -> node L[i])
+__global__ __launch_bounds__(256) void k_compose_first(int32_t n, int32_t *M,
+                                                       const int32_t *L,
+                                                       Ctl *ctl) {
   if (!round_live(ctl)) return;
   const int32_t i = xcd_tid();
   if (i >= n) return;
-  const int32_t c = FIRST ? i : M[i];
+  M[i] = L[i];
+}
+
+// Later rounds compose a node map instead, over the m nodes the point map
+// last pointed to (a fifth of the points after the first round on the
+// driving tile): Mn[v] = L[v] in the first such round (INIT), then
+// Mn[v] = L[Mn[v]]; nn is the round's node count.
+template <bool INIT>
+__global__ __launch_bounds__(256) void k_compose_nodes(int32_t m, int32_t nn,
+                                                       int32_t *Mn,
+                                                       const int32_t *L,
+                                                       Ctl *ctl) {
+  if (!round_live(ctl)) return;
+  const int32_t v = xcd_tid();
+  if (v >= m) return;
+  const int32_t c = INIT ? v : Mn[v];
   if ((uint32_t)c >= (uint32_t)nn) {
     raise_err(ctl, kErrInternal);
     return;
   }
-  M[i] = L[c];
+  Mn[v] = L[c];
+}
+
+// The point map brought up to date where it is read (level outputs, the
+// tail, the incremental rounds): M[i] = Mn[M[i]].
+__global__ __launch_bounds__(256) void k_sync_map(int32_t n, int32_t m,
+                                                  int32_t *M,
+                                                  const int32_t *Mn,
+                                                  Ctl *ctl) {
+  const int32_t i = xcd_tid();
+  if (i >= n) return;
+  const int32_t c = M[i];
+  if ((uint32_t)c >= (uint32_t)m) {
+    raise_err(ctl, kErrInternal);
+    return;
+  }
+  M[i] = Mn[c];
 }
 
 // ---------------------------------------------------------------------------
@@ -3424,6 +3454,7 @@ struct Bufs {
   int32_t *cstart;  // first component of every contraction chunk
   int32_t qcap;     // entries of cstart
   int32_t *M, *mark, *lrank;
+  int32_t *Mn;  // node map of the rounds since M was last brought up to date
   uint8_t *merged;  // per node: formed by a merge in the last round
   // incremental rounds
   int32_t *work[2];  // this round's worklist, the next one
@@ -3498,6 +3529,7 @@ void carve(Arena &a, int32_t n, int32_t d, int32_t k, bool link, Bufs *b) {
   b->qcap = (int32_t)(2 * ed / 64 + 16);  // chunks are >= 64 slots
   b->cstart = a.take<int32_t>(b->qcap);
   b->M = a.take<int32_t>(n1);
+  b->Mn = a.take<int32_t>(n1);
   b->merged = a.take<uint8_t>(n1);
   b->work[0] = a.take<int32_t>(n1);
   b->work[1] = a.take<int32_t>(n1);
@@ -3560,14 +3592,25 @@ inline dim3 blocks_for(int64_t n, int nt = 256) {
 inline dim3 xblocks_for(int64_t n) { return dim3(xcd_grid(blocks_for(n).x)); }
 
 
+// Brings the point map up to date through the node map of the rounds since
+// (mn nodes; nothing to do when mn is 0), and resets mn.
+void sync_map(const Bufs &b, int32_t n, int32_t &mn, Ctl *ctl,
+              hipStream_t st) {
+  if (mn == 0) return;
+  hipLaunchKernelGGL(k_sync_map, xblocks_for(n), dim3(256), 0, st, n, mn, b.M,
+                     b.Mn, ctl);
+  mn = 0;
+}
+
 // One merge round on nn nodes whose rows hold ed directed entries.
 // With rest_only, only the kernels after pointer jumping are launched: the
 // second half of a round whose jumping the host completed (finish_jump).
+// mn: nodes of the node map Mn (0: the point map M is up to date).
 template <bool FIRST, int DT>
 void launch_round(const Bufs &b, const Adj &adj, int cur, int32_t n,
                   int32_t k, int32_t nn, int32_t ed, int32_t d,
                   const NodeIn &s, double lambda, int64_t smin, Ctl *ctl,
-                  hipStream_t st, bool rest_only) {
+                  hipStream_t st, bool rest_only, int32_t mn) {
   const int nxt = 1 - cur;
   const int32_t tcap = (int32_t)(2 * edge_bound(n, k));
   // G lanes per short row; long rows in chunks of entries, a wave each
@@ -3659,8 +3702,15 @@ void launch_round(const Bufs &b, const Adj &adj, int cur, int32_t n,
     prof_end(st);
   }
   prof_begin("compose", st);
-  hipLaunchKernelGGL(k_compose<FIRST>, xblocks_for(n), dim3(256), 0, st, n,
-                     nn, b.M, b.L, ctl);
+  if (FIRST)
+    hipLaunchKernelGGL(k_compose_first, xblocks_for(n), dim3(256), 0, st, n,
+                       b.M, b.L, ctl);
+  else if (mn == 0)
+    hipLaunchKernelGGL(k_compose_nodes<true>, xblocks_for(nn), dim3(256), 0,
+                       st, nn, nn, b.Mn, b.L, ctl);
+  else
+    hipLaunchKernelGGL(k_compose_nodes<false>, xblocks_for(mn), dim3(256), 0,
+                       st, mn, nn, b.Mn, b.L, ctl);
   prof_end(st);
 }
 
@@ -3669,23 +3719,23 @@ template <bool FIRST>
 void round_d(const Bufs &b, const Adj &adj, int cur, int32_t n, int32_t k,
              int32_t nn, int32_t ed, int32_t d, const NodeIn &s,
              double lambda, int64_t smin, Ctl *ctl, hipStream_t st,
-             bool rest_only = false) {
+             int32_t mn, bool rest_only = false) {
   switch (d) {
     case 8:
       launch_round<FIRST, 8>(b, adj, cur, n, k, nn, ed, d, s, lambda, smin,
-                             ctl, st, rest_only);
+                             ctl, st, rest_only, mn);
       break;
     case 16:
       launch_round<FIRST, 16>(b, adj, cur, n, k, nn, ed, d, s, lambda, smin,
-                              ctl, st, rest_only);
+                              ctl, st, rest_only, mn);
       break;
     case 32:
       launch_round<FIRST, 32>(b, adj, cur, n, k, nn, ed, d, s, lambda, smin,
-                              ctl, st, rest_only);
+                              ctl, st, rest_only, mn);
       break;
     default:
       launch_round<FIRST, 0>(b, adj, cur, n, k, nn, ed, d, s, lambda, smin,
-                             ctl, st, rest_only);
+                             ctl, st, rest_only, mn);
   }
 }
 
@@ -4256,6 +4306,7 @@ int ladder_run(const LadderArgs &g, Ctl *ctl, Arena &a, hipStream_t st) {
   }
   if (g.link) tail_nodes = 0;  // the tail kernel does not link
   bool relinked = false;
+  int32_t mn = 0;  // nodes of the node map b.Mn (0: b.M is up to date)
   // incremental rounds (stable ids within a level) are opt-in:
   // EZSP_INCREMENTAL=1 switches graphs of kIncrMinNodes nodes and more,
   // larger values set the smallest graph that switches (so that tests reach
@@ -4354,14 +4405,15 @@ int ladder_run(const LadderArgs &g, Ctl *ctl, Arena &a, hipStream_t st) {
         s.S = nullptr;
         s.mu = nullptr;
         s.minpt = nullptr;
-        round_d<true>(b, adj, cur, n, k, nn, ed, d, s, lambda, smin, ctl, st);
+        round_d<true>(b, adj, cur, n, k, nn, ed, d, s, lambda, smin, ctl, st,
+                      mn);
       } else {
         s.size = b.size[cur];
         s.S = b.S[cur];
         s.mu = b.mu;
         s.minpt = b.minpt[cur];
         round_d<false>(b, adj, cur, n, k, nn, ed, d, s, lambda, smin, ctl,
-                       st);
+                       st, mn);
       }
       if ((rc = read_ctl(ctl, h, st))) return rc;
       if (h->err) return status_from_err(h->err);
@@ -4371,10 +4423,10 @@ int ladder_run(const LadderArgs &g, Ctl *ctl, Arena &a, hipStream_t st) {
         if ((rc = finish_jump(b, nn, ctl, h, st))) return rc;
         if (first)
           round_d<true>(b, adj, cur, n, k, nn, ed, d, s, lambda, smin, ctl,
-                        st, true);
+                        st, mn, true);
         else
           round_d<false>(b, adj, cur, n, k, nn, ed, d, s, lambda, smin, ctl,
-                         st, true);
+                         st, mn, true);
         if ((rc = read_ctl(ctl, h, st))) return rc;
         if (h->err) return status_from_err(h->err);
       }
@@ -4389,7 +4441,7 @@ int ladder_run(const LadderArgs &g, Ctl *ctl, Arena &a, hipStream_t st) {
           prof_bytes("union", 8.0 * nn);
           prof_bytes("stats", S0 * nn + S1 * h->n_next);
           prof_bytes("contract", 12.0 * E0 + 4.0 * nn + 12.0 * E1);
-          prof_bytes("compose", 8.0 * n);
+          prof_bytes("compose", 8.0 * (first ? n : (mn ? mn : nn)));
         }
       }
       if (!h->any_choice) break;  // Step 1: no candidate merge
@@ -4400,6 +4452,7 @@ int ladder_run(const LadderArgs &g, Ctl *ctl, Arena &a, hipStream_t st) {
         return -5;
       }
       const int32_t nn_before = nn;
+      if (!first && mn == 0) mn = nn;  // the node map now spans this graph
       cur = 1 - cur;
       first = false;
       slots = h->slots;
@@ -4412,6 +4465,7 @@ int ladder_run(const LadderArgs &g, Ctl *ctl, Arena &a, hipStream_t st) {
       if (incr_allowed && nn >= incr_min &&
           (double)nn > kIncrKeep * (double)nn_before) {
         // few nodes merged: the next rounds keep their ids
+        sync_map(b, n, mn, ctl, st);
         if ((rc = incr_enter(b, adj, nn, slots, is, ctl, h, st))) return rc;
       }
       if (g.link && h->n_iso > 0) {  // prepare_graph of the next round
@@ -4427,6 +4481,7 @@ int ladder_run(const LadderArgs &g, Ctl *ctl, Arena &a, hipStream_t st) {
         return rc;
       slots = ed;
     }
+    sync_map(b, n, mn, ctl, st);  // the point map, for the outputs and tail
     if (tail_level >= 0) break;
     // level output
     int32_t *out = g.labels + (int64_t)l * n;
