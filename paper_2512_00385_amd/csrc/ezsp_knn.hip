@@ -374,7 +374,8 @@ __device__ __forceinline__ void set_level_bits(uint64_t &mlo, uint64_t &mhi,
 // group, the buckets it scans (its own included) and the inner nodes it
 // enters (st_scan, st_node; the walk statistics, a separate instantiation).
 template <int K, bool ST = false>
-__global__ __launch_bounds__(256) void k_knn_query(
+__global__ __launch_bounds__(256)
+__attribute__((amdgpu_waves_per_eu(8, 8))) void k_knn_query(
     const float4 *__restrict__ pts, const int32_t *__restrict__ inv,
     int32_t n, const float4 *__restrict__ blo, const float4 *__restrict__ bhi,
     Tree tree, int32_t k, int32_t *__restrict__ nbr_int,
