@@ -68,6 +68,9 @@ def parse():
                     help="untimed steps with every stage timed (the split "
                     "and the dominant stage)")
     ap.add_argument("--workload", default=WORKLOAD)
+    ap.add_argument("--no-walk", action="store_true",
+                    help="skip the kNN walk statistics after the timed steps "
+                         "(for profiles of the step alone)")
     ap.add_argument("--no-cpu", action="store_true",
                     help="skip the CPU oracle baseline")
     ap.add_argument("--cpu-points", type=int, default=3_000_000)
@@ -603,7 +606,7 @@ def main():
         "n_comp": [int(x) for x in n_comp],
         "parity": None,
     }
-    if dom == "knn_query":
+    if dom == "knn_query" and not args.no_walk:
         # the kNN's walk, from its counting instantiation, after the timed
         # steps: buckets of 16 candidates scanned and inner nodes entered
         # per 16-point query group
