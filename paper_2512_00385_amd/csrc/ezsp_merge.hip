@@ -1790,6 +1790,7 @@ struct TailState {
   long long *lvl_cut2;                     // kTailLevels
   int32_t nn0, tcur0, d, tcap, gcap, n_levels, level0, round0, max_rounds;
   int32_t want_energy;
+  int32_t rebuild_all;  // every round rebuilds every live row (tests)
   double lambda[kTailLevels];
   long long smin[kTailLevels];
 };
@@ -2197,8 +2198,8 @@ __global__ __launch_bounds__(kTailNT) void k_tail(TailState t, Ctl *ctl) {
       // live row is rebuilt into the other buffer
       int spread = 2;
       bool whole = false;
-      if (top + 2 * need > t.tcap) {
-        if (top + need <= t.tcap) {
+      if (t.rebuild_all || top + 2 * need > t.tcap) {
+        if (!t.rebuild_all && top + need <= t.tcap) {
           spread = 1;
         } else {
           whole = true;
@@ -4052,6 +4053,10 @@ int run_tail(const LadderArgs &g, const Bufs &b, const float *emb,
   t.round0 = round0;
   t.max_rounds = max_rounds;
   t.want_energy = (g.want_energy && g.energy) ? 1 : 0;
+  // EZSP_TAIL_REBUILD=1: the path a full table takes (every live row
+  // rebuilt into the other buffer) in every round, for tests
+  const char *rb = getenv("EZSP_TAIL_REBUILD");
+  t.rebuild_all = (rb && strtol(rb, nullptr, 10) > 0) ? 1 : 0;
   for (int l = 0; l < kTailLevels; ++l) {
     t.lambda[l] = l < g.n_levels ? g.lambdas[l] : 0.0;
     t.smin[l] = (l < g.n_levels && g.min_size) ? g.min_size[l] : 0;

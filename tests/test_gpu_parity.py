@@ -239,6 +239,33 @@ def test_partition_random_clouds(seed, lambdas, tail_mode):
     check_against_oracle(sc.xyz, sc.emb, 10, lambdas)
 
 
+@pytest.mark.parametrize("case", ["room", "ladder", "clouds", "smin",
+                                  "ties"])
+def test_partition_tail_rebuild_every_round(case, monkeypatch):
+    """The tail kernel with every round taking the path of a full table
+    (every live row rebuilt into the other buffer, EZSP_TAIL_REBUILD=1)."""
+    monkeypatch.delenv("EZSP_TAIL_NODES", raising=False)
+    monkeypatch.setenv("EZSP_TAIL_REBUILD", "1")
+    if case == "room":
+        sc = scenes.load("room-20k")
+        check_against_oracle(sc.xyz, sc.emb, sc.k, sc.lambdas)
+    elif case == "ladder":
+        sc = scenes.load("room-20k")
+        check_against_oracle(sc.xyz, sc.emb, sc.k, [0.02, 0.05, 0.2, 0.8, 3.2])
+    elif case == "clouds":
+        for seed in range(3):
+            sc = scenes.random_cloud(3000 + 137 * seed, 1 + 5 * seed,
+                                     seed=seed, sigma=0.05 * (1 + seed))
+            check_against_oracle(sc.xyz, sc.emb, 10, [0.05, 0.2, 0.8])
+    elif case == "smin":
+        sc = scenes.random_cloud(3000, 6, seed=4, sigma=0.3)
+        check_against_oracle(sc.xyz, sc.emb, 8, [0.01, 0.05, 0.05],
+                             min_size=[5, 30, 90])
+    else:
+        sc = scenes.random_cloud(1500, 3, seed=5)
+        check_against_oracle(sc.xyz, np.ones_like(sc.emb), 10, [0.5, 2.0])
+
+
 @pytest.mark.parametrize("k", [1, 4, 16])
 def test_partition_k(k):
     sc = scenes.random_cloud(2500, 8, seed=11)
