@@ -1236,18 +1236,28 @@ __device__ __forceinline__ int32_t load_batch(const Adj &a,
   return total;
 }
 
-// Member and entry of flat index f of the batch.
-__device__ __forceinline__ void batch_find(const int32_t *pre, int32_t f,
-                                           int32_t &slot, int32_t &j) {
-  int32_t lo = 0, hi = kBatch;
-  while (hi - lo > 1) {
-    const int32_t mid = (lo + hi) >> 1;
-    if (pre[mid] <= f) lo = mid;
-    else hi = mid;
+// Members and entries of U flat indices f[e] of the batch: the U searches
+// over pre[0..kBatch) take their (fixed) steps together, so each step's LDS
+// reads are issued back to back.
+template <int U>
+__device__ __forceinline__ void batch_find_n(const int32_t *pre,
+                                             const int32_t (&f)[U],
+                                             int32_t (&slot)[U],
+                                             int32_t (&j)[U]) {
+#pragma unroll
+  for (int e = 0; e < U; ++e) slot[e] = 0;
+#pragma unroll
+  for (int32_t len = kBatch; len > 1;) {
+    const int32_t half = len >> 1;
+#pragma unroll
+    for (int e = 0; e < U; ++e)
+      slot[e] = pre[slot[e] + half] <= f[e] ? slot[e] + half : slot[e];
+    len -= half;
   }
-  slot = lo;
-  j = f - pre[lo];
+#pragma unroll
+  for (int e = 0; e < U; ++e) j[e] = f[e] - pre[slot[e]];
 }
+
 
 template <bool FIRST>
 __global__ __launch_bounds__(256) void k_contract_chunk(
@@ -1316,17 +1326,17 @@ __global__ __launch_bounds__(256) void k_contract_chunk(
       __syncthreads();
       for (int32_t f0 = threadIdx.x; f0 < total; f0 += kUnroll * 256) {
         int32_t slot[kUnroll], u[kUnroll], w[kUnroll], B[kUnroll];
+        int32_t fe[kUnroll], je[kUnroll];
         bool ok[kUnroll];
   #pragma unroll
+        for (int e = 0; e < kUnroll; ++e) fe[e] = min(f0 + e * 256, total - 1);
+        batch_find_n<kUnroll>(pre, fe, slot, je);
+  #pragma unroll
         for (int e = 0; e < kUnroll; ++e) {
-          const int32_t f = f0 + e * 256;
           ok[e] = false;
-          if (f < total) {
-            int32_t j;
-            batch_find(pre, f, slot[e], j);
-            ok[e] = row_entry_at<FIRST>(a, bm[slot[e]], bbase[slot[e]], j, u[e],
-                                        w[e]);
-          }
+          if (f0 + e * 256 < total)
+            ok[e] = row_entry_at<FIRST>(a, bm[slot[e]], bbase[slot[e]], je[e],
+                                        u[e], w[e]);
         }
   #pragma unroll
         for (int e = 0; e < kUnroll; ++e) {
@@ -1467,28 +1477,39 @@ __global__ __launch_bounds__(256) void k_contract_big(
     const int32_t total = load_batch<FIRST>(
         a, mem, i0, i1, pre, bm, wsum,
         [&](int32_t m) { return row_span<FIRST>(a, m) <= kLongRow; });
-    for (int32_t f = threadIdx.x; f < total; f += blockDim.x) {
-      int32_t slot, j, u, w;
-      batch_find(pre, f, slot, j);
-      const int32_t m = bm[slot];
-      if (!row_entry<FIRST>(a, m, j, u, w)) continue;
-      if ((uint32_t)u >= (uint32_t)nn) {
-        raise_err(ctl, kErrInternal);
-        continue;
-      }
-      const int32_t B = L[u];
-      if (B == A) continue;
-      uint32_t h = ((uint32_t)B * 2654435761u) & (kPreSlots - 1);
-      bool done = false;
-      for (int32_t probe = 0; probe < 32 && !done; ++probe) {
-        const int32_t old = atomicCAS(&pk[h], -1, B);
-        if (old == -1 || old == B) {
-          atomicAdd(&pw[h], w);
-          done = true;
+    constexpr int kU = 4;  // entries per thread with their loads in flight
+    for (int32_t f0 = threadIdx.x; f0 < total; f0 += kU * 256) {
+      int32_t fe[kU], slot[kU], je[kU], u[kU], w[kU], B[kU];
+      bool ok[kU];
+#pragma unroll
+      for (int e = 0; e < kU; ++e) fe[e] = min(f0 + e * 256, total - 1);
+      batch_find_n<kU>(pre, fe, slot, je);
+#pragma unroll
+      for (int e = 0; e < kU; ++e) {
+        ok[e] = f0 + e * 256 < total &&
+                row_entry<FIRST>(a, bm[slot[e]], je[e], u[e], w[e]);
+        if (ok[e] && (uint32_t)u[e] >= (uint32_t)nn) {
+          raise_err(ctl, kErrInternal);
+          ok[e] = false;
         }
-        h = (h + 1) & (kPreSlots - 1);
       }
-      if (!done) added += table_add(tbl, base, cp, B, w, ctl) ? 1 : 0;
+#pragma unroll
+      for (int e = 0; e < kU; ++e) B[e] = ok[e] ? L[u[e]] : A;
+#pragma unroll
+      for (int e = 0; e < kU; ++e) {
+        if (B[e] == A) continue;  // no entry, or inside the component
+        uint32_t h = ((uint32_t)B[e] * 2654435761u) & (kPreSlots - 1);
+        bool done = false;
+        for (int32_t probe = 0; probe < 32 && !done; ++probe) {
+          const int32_t old = atomicCAS(&pk[h], -1, B[e]);
+          if (old == -1 || old == B[e]) {
+            atomicAdd(&pw[h], w[e]);
+            done = true;
+          }
+          h = (h + 1) & (kPreSlots - 1);
+        }
+        if (!done) added += table_add(tbl, base, cp, B[e], w[e], ctl) ? 1 : 0;
+      }
     }
     __syncthreads();
     for (int q = threadIdx.x; q < kPreSlots; q += blockDim.x)
