@@ -245,9 +245,22 @@ __global__ __launch_bounds__(256) void k_rev_count_kth(
       }
     }
     nmask[i] = mask;
+    // u gets i as a reverse entry: four neighbours reloaded at a time
     const int32_t *r = nbr + (int64_t)i * kp;
-    for (uint64_t m = mask; m; m &= m - 1)
-      atomicAdd(&rev[r[__builtin_ctzll(m)]], 1);
+    for (uint64_t m = mask; m;) {
+      int32_t uu[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        uu[q] = -1;
+        if (m) {
+          uu[q] = r[__builtin_ctzll(m)];
+          m &= m - 1;
+        }
+      }
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        if (uu[q] >= 0) atomicAdd(&rev[uu[q]], 1);
+    }
   }
   fwd = wave_sum(fwd);
   if ((threadIdx.x & (kWave - 1)) == 0 && fwd) stripe_add(ctl->e_fwd_s, fwd);
@@ -263,14 +276,39 @@ __global__ __launch_bounds__(256) void k_rev_fill(const int32_t *nbr,
   const int32_t i = xcd_tid();
   if (i >= n) return;
   const int32_t *r = nbr + (int64_t)i * pad4(k);
-  for (uint64_t m = nmask[i]; m; m &= m - 1) {
-    const int32_t u = r[__builtin_ctzll(m)];
-    const int32_t pos = rrp[u] + atomicAdd(&cursor[u], 1);
-    if (pos < rrp[u + 1]) {
-      rcol[pos] = i;
-      rown[pos] = u;
-    } else {
-      raise_err(ctl, kErrInternal);
+  // four entries at a time: their cursor increments (atomics that return a
+  // position) and list bounds are issued before any is used
+  constexpr int kQ = 4;
+  for (uint64_t m = nmask[i]; m;) {
+    int32_t u[kQ], pos[kQ], lo[kQ], hi[kQ];
+#pragma unroll
+    for (int q = 0; q < kQ; ++q) {
+      u[q] = -1;
+      if (m) {
+        u[q] = r[__builtin_ctzll(m)];
+        m &= m - 1;
+      }
+    }
+#pragma unroll
+    for (int q = 0; q < kQ; ++q) {
+      pos[q] = 0;
+      lo[q] = hi[q] = 0;
+      if (u[q] >= 0) {
+        pos[q] = atomicAdd(&cursor[u[q]], 1);
+        lo[q] = rrp[u[q]];
+        hi[q] = rrp[u[q] + 1];
+      }
+    }
+#pragma unroll
+    for (int q = 0; q < kQ; ++q) {
+      if (u[q] < 0) continue;
+      const int32_t p = lo[q] + pos[q];
+      if (p < hi[q]) {
+        rcol[p] = i;
+        rown[p] = u[q];
+      } else {
+        raise_err(ctl, kErrInternal);
+      }
     }
   }
 }
