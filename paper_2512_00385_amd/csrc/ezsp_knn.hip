@@ -219,23 +219,45 @@ __global__ __launch_bounds__(256) void k_up_boxes(float4 *blo, float4 *bhi,
 
 // A candidate is the 64-bit key (fp32 bits of d2) << 32 | original index.
 // d2 >= 0, so the bits of d2 are ordered like d2 and the key order is the
-// order (d2, index).  An empty slot holds ~0.
+// order (d2, index).  An empty slot of the output holds ~0 (kNoKey); the
+// lists being built use kEmpty instead, the largest finite fp64 pattern:
+// above every real key (d2 bits <= 0x7f800000 for the padding's infinity),
+// its upper half above every d2 (so it admits every box) and its lower
+// half above every index.
 constexpr uint64_t kNoKey = ~0ull;
+constexpr uint64_t kEmpty = 0x7fefffffffffffffull;
 
 __device__ __forceinline__ uint64_t cand_key(float d2, int32_t o) {
   return ((uint64_t)__float_as_uint(d2) << 32) | (uint32_t)o;
 }
 
-// Insert nk into the sorted top-K; nk is known to beat the last entry.
+// A key read as an fp64 value: its sign bit is clear and its exponent
+// field below 0x7ff (at most kEmpty), so it is a non-negative finite number
+// (denormal when d2 < 2^-126) and the fp64 order is the integer order.
+// v_min_f64 / v_max_f64 then return the bits of the smaller / larger key
+// (fp64 denormals are kept in these kernels, and no key is a NaN).  They
+// are written out because the compiler's fmin / fmax first quiet each
+// operand with a further instruction, which no key needs.
+__device__ __forceinline__ uint64_t key_min(uint64_t a, uint64_t b) {
+  uint64_t r;
+  asm("v_min_f64 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
+  return r;
+}
+__device__ __forceinline__ uint64_t key_max(uint64_t a, uint64_t b) {
+  uint64_t r;
+  asm("v_max_f64 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
+  return r;
+}
+
+// Insert nk into the sorted top-K (a no-op when nk is not below the last
+// entry): the new entry t is min(key[t], max(key[t-1], nk)), which keeps
+// key[t] when nk >= key[t], takes nk when key[t-1] <= nk < key[t], and
+// shifts key[t-1] up when nk < key[t-1].
 template <int K>
 __device__ __forceinline__ void topk_insert(uint64_t (&key)[K], uint64_t nk) {
 #pragma unroll
-  for (int t = K - 1; t > 0; --t) {
-    const bool before_prev = nk < key[t - 1];
-    const uint64_t cur = (nk < key[t]) ? nk : key[t];
-    key[t] = before_prev ? key[t - 1] : cur;
-  }
-  key[0] = (nk < key[0]) ? nk : key[0];
+  for (int t = K - 1; t > 0; --t) key[t] = key_min(key[t], key_max(key[t - 1], nk));
+  key[0] = key_min(key[0], nk);
 }
 
 // Broadcast lane J of every 16-lane row (one DPP row = one query group).
@@ -264,7 +286,7 @@ __device__ __forceinline__ uint64_t bucket_key(const float4 &q, float px,
   const int32_t qo = row_bcast_i<J>(__float_as_int(q.w));
   const float xx = dx * dx, yy = dy * dy, zz = dz * dz;
   const float d2 = (xx + yy) + zz;
-  if (SELF) return qo != me ? cand_key(d2, qo) : kNoKey;
+  if (SELF) return qo != me ? cand_key(d2, qo) : kEmpty;
   return cand_key(d2, qo);
 }
 
@@ -299,8 +321,8 @@ __device__ __forceinline__ void scan_bucket(const float4 *__restrict__ pts,
 
 // Largest k-th d2 (as bits) over the active lanes of each 16-lane group,
 // in every lane of the group: a prefix max along the DPP row, then lane 15
-// broadcast.  An empty list (kNoKey) gives 0xffffffff, which admits every
-// box.
+// broadcast.  An empty list (kEmpty) gives 0x7fefffff, above every d2's
+// bits, which admits every box.
 __device__ __forceinline__ uint32_t group_max_kth(uint32_t v) {
   v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x111, 0xF, 0xF,
                                                    false));
@@ -414,7 +436,7 @@ __attribute__((amdgpu_waves_per_eu(8, 8))) void k_knn_query(
   }
   uint64_t key[K];
 #pragma unroll
-  for (int t = 0; t < K; ++t) key[t] = kNoKey;
+  for (int t = 0; t < K; ++t) key[t] = kEmpty;
   // own bucket and its Morton neighbours first: a tight k-th distance early
   // (the two Morton neighbours are the first buckets of the scan loop below)
   if (gvalid) scan_bucket<K, true>(pts, grp, lane16, p.x, p.y, p.z, me, key);
