@@ -110,10 +110,11 @@ int ezsp_knn(const float *xyz, int64_t n, int32_t k, int32_t *nbr, float *d2,
 
 /* ezsp_knn (same nbr, workspace and errors) with the statistics of its
  * tree walk, for inspection outside timed work: points are sorted into
- * Morton order and cut into groups of 16 consecutive points that walk the
- * box tree together; group g (0 <= g < ceil(n / 16)) gets
- *   group_scans[g]  the buckets of 16 points whose candidates it scanned,
- *                   its own included
+ * Morton order, cut into buckets of 16 consecutive points, and groups of 64
+ * consecutive points (four buckets) walk the box tree together; group g
+ * (0 <= g < ceil(n / 64)) gets
+ *   group_scans[g]  the buckets whose candidates it scanned, its own
+ *                   included
  *   group_nodes[g]  the inner tree nodes it entered
  * (both int32, device memory, written in full).  Stream-asynchronous. */
 int ezsp_knn_walk_stats(const float *xyz, int64_t n, int32_t k, int32_t *nbr,

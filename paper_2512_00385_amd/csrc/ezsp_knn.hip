@@ -9,21 +9,23 @@
 // implicit 8-ary tree of axis-aligned boxes sits over the buckets, so the
 // voxel hierarchy adapts to any density.
 //
-// Query: one bucket per 16-lane DPP row (four buckets per wavefront), one
-// query point per lane.  Each lane keeps its own sorted top-k of 64-bit keys
-// (d2 bits, original index) in registers.  A group scans its own bucket and
-// the two next to it in Morton order first, then walks the tree depth first.
-// When a node is entered, its eight children are tested at once, one child
-// per lane, against the box of the group's own points widened by the
-// group's largest current k-th distance; the children that pass are kept as
-// bits of a per-level mask (the lowest set bit is the next to take).  When a
-// child is taken, every lane tests its box against its own point and its
-// own current k-th distance, and the child is entered (or, for a bucket,
-// scanned) only if some lane needs it.  Bucket points are broadcast within
-// the row by DPP.  Both box distances are built from the same IEEE
-// operations as d2 and rounding is monotone, so neither exceeds the d2 of a
-// query and a point inside the box: no neighbour, and no tie with a smaller
-// index, can be skipped.
+// Query: one query point per lane, one wavefront per four consecutive
+// buckets (64 points).  Each lane keeps its own sorted top-k of 64-bit keys
+// (d2 bits, original index) in registers.  A wave scans its own buckets and
+// the two next to them in Morton order first, then walks the tree depth
+// first; the walk is the wave's, so its state is uniform and runs on the
+// scalar unit, with box loads through the scalar cache.  When a node is
+// entered, its eight children are tested at once, one child per lane,
+// against the box of the wave's own points widened by the wave's largest
+// current k-th distance; the children that pass are kept as bits of a
+// per-level mask (the lowest set bit is the next to take).  When a child is
+// taken, every lane tests its box against its own point and its own current
+// k-th distance, and the child is entered (or, for a bucket, scanned) only
+// if some lane needs it.  A scanned bucket is loaded by each 16-lane DPP row
+// and its points broadcast within the row.  Both box distances are built
+// from the same IEEE operations as d2 and rounding is monotone, so neither
+// exceeds the d2 of a query and a point inside the box: no neighbour, and no
+// tie with a smaller index, can be skipped.
 #include "ezsp_internal.h"
 
 namespace ezsp {
@@ -319,11 +321,11 @@ __device__ __forceinline__ void scan_bucket(const float4 *__restrict__ pts,
   BucketStep<K, 0, SELF>::run(q, px, py, pz, me, key);
 }
 
-// Largest k-th d2 (as bits) over the active lanes of each 16-lane group,
-// in every lane of the group: a prefix max along the DPP row, then lane 15
-// broadcast.  An empty list (kEmpty) gives 0x7fefffff, above every d2's
-// bits, which admits every box.
-__device__ __forceinline__ uint32_t group_max_kth(uint32_t v) {
+// Largest k-th d2 (as bits) over the active lanes of the wave, the same
+// value in every lane: a prefix max along each 16-lane DPP row, then the
+// four rows' last lanes.  An empty list (kEmpty) gives 0x7fefffff, above
+// every d2's bits, which admits every box.
+__device__ __forceinline__ uint32_t wave_max_kth(uint32_t v) {
   v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x111, 0xF, 0xF,
                                                    false));
   v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x112, 0xF, 0xF,
@@ -332,25 +334,39 @@ __device__ __forceinline__ uint32_t group_max_kth(uint32_t v) {
                                                    false));
   v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x118, 0xF, 0xF,
                                                    false));
-  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x15F, 0xF, 0xF,
-                                               false);
+  const uint32_t r0 = (uint32_t)__builtin_amdgcn_readlane((int)v, 15);
+  const uint32_t r1 = (uint32_t)__builtin_amdgcn_readlane((int)v, 31);
+  const uint32_t r2 = (uint32_t)__builtin_amdgcn_readlane((int)v, 47);
+  const uint32_t r3 = (uint32_t)__builtin_amdgcn_readlane((int)v, 63);
+  return max(max(r0, r1), max(r2, r3));
+}
+
+// Squared distance from point p to box [lo, hi], from the same IEEE
+// operations as d2 (per axis the gap max(lo - p, p - hi, 0)); it never
+// exceeds the d2 of p and a point inside the box.
+__device__ __forceinline__ float box_d2(const float4 &lo, const float4 &hi,
+                                        float px, float py, float pz) {
+  const float ex = fmaxf(fmaxf(lo.x - px, px - hi.x), 0.f);
+  const float ey = fmaxf(fmaxf(lo.y - py, py - hi.y), 0.f);
+  const float ez = fmaxf(fmaxf(lo.z - pz, pz - hi.z), 0.f);
+  const float bx = ex * ex, by = ey * ey, bz = ez * ez;
+  return (bx + by) + bz;
 }
 
 // Coarse test of the children first .. first+7 (level lc) of one node,
-// one child per lane (lane c and c + 8 of the group take child c): bit c is
-// set when the child's box is within the group's largest k-th distance of
-// the box of the group's own points (qlo, qhi).  Per axis the gap to the
+// one child per lane (lane c and every lane c mod 8 take child c): bit c is
+// set when the child's box is within the wave's largest k-th distance of
+// the box of the wave's own points (qlo, qhi).  Per axis the gap to the
 // query box is at most the gap to any query point in it (same IEEE
 // operations, rounding is monotone), so a child that some lane's own test
 // would admit is always admitted here.
 __device__ __forceinline__ uint32_t coarse_mask(
     const float4 *__restrict__ blo, const float4 *__restrict__ bhi,
-    const int32_t *lv_off, const int32_t *lv_cnt, int lc, int32_t first,
-    const float4 &qlo,
-    const float4 &qhi, uint32_t gkth, int lane16, int gshift) {
-  const int32_t nchild = min(kFan, lv_cnt[lc] - first);
-  const int c = lane16 & (kFan - 1);
-  const int32_t j = lv_off[lc] + first + min(c, nchild - 1);
+    int32_t lv_off, int32_t lv_cnt, int32_t first, const float4 &qlo,
+    const float4 &qhi, uint32_t gkth, int lane) {
+  const int32_t nchild = min(kFan, lv_cnt - first);
+  const int c = lane & (kFan - 1);
+  const int32_t j = lv_off + first + min(c, nchild - 1);
   const float4 lo = blo[j], hi = bhi[j];
   const float ex = fmaxf(fmaxf(lo.x - qhi.x, qlo.x - hi.x), 0.f);
   const float ey = fmaxf(fmaxf(lo.y - qhi.y, qlo.y - hi.y), 0.f);
@@ -358,26 +374,7 @@ __device__ __forceinline__ uint32_t coarse_mask(
   const float bx = ex * ex, by = ey * ey, bz = ez * ez;
   const float d2b = (bx + by) + bz;
   const bool need = c < nchild && __float_as_uint(d2b) <= gkth;
-  return (uint32_t)(__ballot(need) >> gshift) & 0xffu;
-}
-
-// Exact test of one node's box against every lane's point and current k-th
-// distance: true when some active lane of the group needs the node.  The
-// box distance uses the same IEEE operations as d2, so it never exceeds the
-// d2 of a point inside the box.
-__device__ __forceinline__ bool lane_needs(const float4 *__restrict__ blo,
-                                           const float4 *__restrict__ bhi,
-                                           int32_t j, const float4 &p,
-                                           bool act, uint32_t kth,
-                                           int gshift) {
-  const float4 lo = blo[j], hi = bhi[j];
-  const float ex = fmaxf(fmaxf(lo.x - p.x, p.x - hi.x), 0.f);
-  const float ey = fmaxf(fmaxf(lo.y - p.y, p.y - hi.y), 0.f);
-  const float ez = fmaxf(fmaxf(lo.z - p.z, p.z - hi.z), 0.f);
-  const float bx = ex * ex, by = ey * ey, bz = ez * ez;
-  const float d2b = (bx + by) + bz;
-  const bool need = act && __float_as_uint(d2b) <= kth;
-  return ((__ballot(need) >> gshift) & 0xffffull) != 0;
+  return (uint32_t)__ballot(need) & 0xffu;
 }
 
 __device__ __forceinline__ void set_level_bits(uint64_t &mlo, uint64_t &mhi,
@@ -388,13 +385,15 @@ __device__ __forceinline__ void set_level_bits(uint64_t &mlo, uint64_t &mhi,
     mhi |= (uint64_t)m8 << (8 * (l - 8));
 }
 
-// One query group = 16 lanes = the 16 points of one bucket.  Every group
-// walks the tree on its own (group-uniform decisions from a 16-lane vote);
-// the four groups of a wave alternate between finding their next bucket and
-// scanning it together.  A node is entered when some lane's box distance
-// does not exceed that lane's current k-th distance.  ST: also count, per
-// group, the buckets it scans (its own included) and the inner nodes it
-// enters (st_scan, st_node; the walk statistics, a separate instantiation).
+// One query group = one wavefront = the 64 points of four consecutive
+// buckets, one query per lane.  The walk is the wave's own, so its state
+// (pending children, path, bucket to scan) is uniform and lives in scalar
+// registers; only the distance tests and the bucket scans are per lane.
+// The wave scans its own buckets and the two next to them in Morton order
+// first.  A node is entered when some lane's box distance does not exceed
+// that lane's current k-th distance.  ST: also count, per wave, the
+// buckets it scans (its own included) and the inner nodes it enters
+// (st_scan, st_node; the walk statistics, a separate instantiation).
 template <int K, bool ST = false>
 __global__ __launch_bounds__(256)
 __attribute__((amdgpu_waves_per_eu(8, 8))) void k_knn_query(
@@ -402,31 +401,26 @@ __attribute__((amdgpu_waves_per_eu(8, 8))) void k_knn_query(
     int32_t n, const float4 *__restrict__ blo, const float4 *__restrict__ bhi,
     Tree tree, int32_t k, int32_t *__restrict__ nbr_int,
     int32_t *__restrict__ nbr_out, float *__restrict__ d2_out,
-    uint64_t *__restrict__ kth_out, int32_t n_blocks,
+    uint64_t *__restrict__ kth_out, int32_t n_waves,
     const float4 *__restrict__ emb, int32_t d4, float4 *__restrict__ emb_out,
     Ctl *ctl, int32_t *__restrict__ st_scan, int32_t *__restrict__ st_node) {
-  const int32_t lb = xcd_block();
-  if (lb >= n_blocks) return;
-  // level offsets and counts of the box tree, indexed per lane in the walk
-  __shared__ int32_t lv_off[kMaxTreeLevels], lv_cnt[kMaxTreeLevels];
-  if (threadIdx.x < kMaxTreeLevels) {
-    lv_off[threadIdx.x] = tree.off[threadIdx.x];
-    lv_cnt[threadIdx.x] = tree.cnt[threadIdx.x];
-  }
-  __syncthreads();
-  const int lane16 = threadIdx.x & (kBucket - 1);
-  const int gshift = threadIdx.x & (kWave - kBucket);  // 0, 16, 32, 48
+  constexpr int kOwn = kWave / kBucket;  // buckets per wave
+  const int32_t wv = __builtin_amdgcn_readfirstlane(
+      xcd_block() * (256 / kWave) + (int32_t)(threadIdx.x / kWave));
+  if (wv >= n_waves) return;  // whole waves only
+  const int lane = threadIdx.x & (kWave - 1);
+  const int lane16 = lane & (kBucket - 1);
   const int32_t nb0 = tree.cnt[0];
-  const int32_t grp = lb * (256 / kBucket) + (int32_t)(threadIdx.x / kBucket);
-  const bool gvalid = grp < nb0;  // else the whole group is past the end
-  const int32_t i = grp * kBucket + lane16;
-  const bool act = gvalid && i < n;
+  const int32_t b0 = wv * kOwn;               // first own bucket
+  const int32_t nown = min(kOwn, nb0 - b0);   // 1 .. 4
+  const int32_t i = b0 * kBucket + lane;
+  const bool act = i < n;
   const float4 p = act ? pts[i] : make_float4(0.f, 0.f, 0.f, 0.f);
   const int32_t me = act ? __float_as_int(p.w) : -1;
   // For the merge, optionally: the point's embedding row (d4 <= 4 float4)
   // copied into internal order, with Step 0's max |e| and the non-finite
   // check.  The loads are issued here and the stores made after the own
-  // bucket's scan, whose instructions cover their latency.
+  // buckets' scans, whose instructions cover their latency.
   float4 row[4];
   if (emb && act) {
     const float4 *src = emb + (int64_t)me * d4;
@@ -437,10 +431,11 @@ __attribute__((amdgpu_waves_per_eu(8, 8))) void k_knn_query(
   uint64_t key[K];
 #pragma unroll
   for (int t = 0; t < K; ++t) key[t] = kEmpty;
-  // own bucket and its Morton neighbours first: a tight k-th distance early
-  // (the two Morton neighbours are the first buckets of the scan loop below)
-  if (gvalid) scan_bucket<K, true>(pts, grp, lane16, p.x, p.y, p.z, me, key);
-  int32_t c_scan = 1, c_node = 0;  // walk statistics (ST only)
+  // own buckets first: a tight k-th distance early (the two Morton
+  // neighbours are the first buckets of the scan loop below)
+  for (int32_t j = 0; j < nown; ++j)
+    scan_bucket<K, true>(pts, b0 + j, lane16, p.x, p.y, p.z, me, key);
+  int32_t c_scan = nown, c_node = 0;  // walk statistics (ST only)
   if (emb) {  // every lane of the wave is here
     uint32_t m = 0;
     bool bad = false;
@@ -462,37 +457,46 @@ __attribute__((amdgpu_waves_per_eu(8, 8))) void k_knn_query(
     for (int off = kWave / 2; off > 0; off >>= 1)
       m = max(m, (uint32_t)__shfl_xor((int)m, off, kWave));
     const bool any_bad = __ballot(bad) != 0;
-    if ((threadIdx.x & (kWave - 1)) == 0) {
+    if (lane == 0) {
       stripe_max(ctl->maxabs_s, (int32_t)m);  // |e| bits < 2^31
       if (any_bad) raise_err(ctl, kErrNonFinite);
     }
   }
-  if (!gvalid) return;
 
   // Depth-first walk with the pending children of every level of the
   // current path as bits: bit 8*l + c = child c (level l) of the path node
   // at level l+1.  The lowest set bit is the deepest pending node, and the
   // path node at level l+1 is cur >> 3*(l+1-curl) (cur: last node taken, at
   // level curl), since children of x are 8x..8x+7.  Children are marked by
-  // the group's coarse test when their parent is entered; a node is entered
+  // the wave's coarse test when their parent is entered; a node is entered
   // only when, as it is taken, some lane's own test against its current
   // k-th distance still needs it.
-  const float4 qlo = blo[grp], qhi = bhi[grp];  // own bucket (level 0)
+  float4 qlo = blo[b0], qhi = bhi[b0];  // the own buckets' box
+  for (int32_t j = 1; j < nown; ++j) {
+    const float4 lo = blo[b0 + j], hi = bhi[b0 + j];
+    qlo.x = fminf(qlo.x, lo.x);
+    qlo.y = fminf(qlo.y, lo.y);
+    qlo.z = fminf(qlo.z, lo.z);
+    qhi.x = fmaxf(qhi.x, hi.x);
+    qhi.y = fmaxf(qhi.y, hi.y);
+    qhi.z = fmaxf(qhi.z, hi.z);
+  }
   uint64_t mlo = 0, mhi = 0;
   int32_t cur = 0;
   int curl = tree.top;
-  // the group's largest k-th distance changes only in a bucket scan
-  uint32_t gk = group_max_kth(act ? (uint32_t)(key[K - 1] >> 32) : 0u);
+  // the wave's largest k-th distance changes only in a bucket scan
+  uint32_t gk = wave_max_kth(act ? (uint32_t)(key[K - 1] >> 32) : 0u);
   if (tree.top > 0) {
-    const uint32_t m8 = coarse_mask(blo, bhi, lv_off, lv_cnt, tree.top - 1, 0,
-                                    qlo, qhi, gk, lane16, gshift);
+    const uint32_t m8 =
+        coarse_mask(blo, bhi, tree.off[tree.top - 1], tree.cnt[tree.top - 1],
+                    0, qlo, qhi, gk, lane);
     set_level_bits(mlo, mhi, tree.top - 1, m8);
   }
-  int pre = 0;  // Morton neighbours taken: grp - 1, then grp + 1
+  int pre = 0;  // Morton neighbours taken: b0 - 1, then b0 + nown
   for (;;) {
     int32_t leaf = -1;
     while (pre < 2 && leaf < 0) {
-      const int32_t b = pre == 0 ? grp - 1 : grp + 1;
+      const int32_t b = pre == 0 ? b0 - 1 : b0 + nown;
       ++pre;
       if (b >= 0 && b < nb0) leaf = b;
     }
@@ -511,31 +515,30 @@ __attribute__((amdgpu_waves_per_eu(8, 8))) void k_knn_query(
       const int32_t node = ((cur >> (3 * (l + 1 - curl))) << 3) | c;
       cur = node;
       curl = l;
-      if (l == 0 && node >= grp - 1 && node <= grp + 1) continue;
+      if (l == 0 && node >= b0 - 1 && node <= b0 + nown) continue;
+      const int32_t j = tree.off[l] + node;
       const uint32_t kth = (uint32_t)(key[K - 1] >> 32);
-      if (!lane_needs(blo, bhi, lv_off[l] + node, p, act, kth, gshift))
-        continue;
+      const float d2b = box_d2(blo[j], bhi[j], p.x, p.y, p.z);
+      if (__ballot(act && __float_as_uint(d2b) <= kth) == 0) continue;
       if (l == 0) {
         leaf = node;
         break;
       }
-      const uint32_t m8 = coarse_mask(blo, bhi, lv_off, lv_cnt, l - 1,
-                                      node * kFan, qlo, qhi, gk, lane16,
-                                      gshift);
+      const uint32_t m8 = coarse_mask(blo, bhi, tree.off[l - 1],
+                                      tree.cnt[l - 1], node * kFan, qlo, qhi,
+                                      gk, lane);
       set_level_bits(mlo, mhi, l - 1, m8);
       if constexpr (ST) ++c_node;
     }
-    if (__ballot(leaf >= 0) == 0) break;
-    if (leaf >= 0) {
-      scan_bucket<K, false>(pts, leaf, lane16, p.x, p.y, p.z, me, key);
-      gk = group_max_kth(act ? (uint32_t)(key[K - 1] >> 32) : 0u);
-      if constexpr (ST) ++c_scan;
-    }
+    if (leaf < 0) break;
+    scan_bucket<K, false>(pts, leaf, lane16, p.x, p.y, p.z, me, key);
+    gk = wave_max_kth(act ? (uint32_t)(key[K - 1] >> 32) : 0u);
+    if constexpr (ST) ++c_scan;
   }
   if constexpr (ST) {
-    if (lane16 == 0) {  // the walk is uniform over the group
-      st_scan[grp] = c_scan;
-      st_node[grp] = c_node;
+    if (lane == 0) {  // the walk is uniform over the wave
+      st_scan[wv] = c_scan;
+      st_node[wv] = c_node;
     }
   }
 
@@ -617,7 +620,10 @@ static hipError_t knn_impl(const float *xyz, int32_t n, int32_t k, Ctl *ctl,
     hipLaunchKernelGGL(k_up_boxes, dim3((tree.cnt[l] + nt - 1) / nt), dim3(nt),
                        0, st, s.blo, s.bhi, tree.off[l - 1], tree.cnt[l - 1],
                        tree.off[l], tree.cnt[l]);
-  const int32_t qblocks = (tree.cnt[0] + (nt / kBucket) - 1) / (nt / kBucket);
+  // a wave per four buckets, four waves per block
+  constexpr int kOwn = kWave / kBucket;
+  const int32_t n_waves = (tree.cnt[0] + kOwn - 1) / kOwn;
+  const int32_t qblocks = (n_waves + (nt / kWave) - 1) / (nt / kWave);
   const dim3 grid(xcd_grid(qblocks));
   const float4 *emb4 = reinterpret_cast<const float4 *>(emb);
   float4 *emb_out4 = reinterpret_cast<float4 *>(emb_out);
@@ -628,12 +634,12 @@ static hipError_t knn_impl(const float *xyz, int32_t n, int32_t k, Ctl *ctl,
     if (st_scan)                                                             \
       hipLaunchKernelGGL((k_knn_query<KK, true>), grid, dim3(nt), 0, st,     \
                          s.pts, w.inv, n, s.blo, s.bhi, tree, k, w.nbr_int,  \
-                         nbr_out, d2_out, w.kth, qblocks, emb4, d / 4,       \
+                         nbr_out, d2_out, w.kth, n_waves, emb4, d / 4,       \
                          emb_out4, ctl, st_scan, st_node);                   \
     else                                                                     \
       hipLaunchKernelGGL(k_knn_query<KK>, grid, dim3(nt), 0, st, s.pts,      \
                          w.inv, n, s.blo, s.bhi, tree, k, w.nbr_int,         \
-                         nbr_out, d2_out, w.kth, qblocks, emb4, d / 4,       \
+                         nbr_out, d2_out, w.kth, n_waves, emb4, d / 4,       \
                          emb_out4, ctl, (int32_t *)nullptr,                  \
                          (int32_t *)nullptr);                                \
     break;

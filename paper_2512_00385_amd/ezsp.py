@@ -236,13 +236,14 @@ def knn(xyz: torch.Tensor, k: int, want_d2: bool = False, sync: bool = True):
 
 
 def knn_walk_stats(xyz: torch.Tensor, k: int):
-    """ezsp_knn_walk_stats: (nbr [n, k] int32, buckets scanned and inner
-    nodes entered per 16-point query group, each [ceil(n / 16)] int32)."""
+    """ezsp_knn_walk_stats: (nbr [n, k] int32, 16-point buckets scanned and
+    inner nodes entered per 64-point query group, each [ceil(n / 64)]
+    int32)."""
     lib = load()
     xyz = _dev_tensor(xyz, torch.float32, "xyz", 3)
     n = xyz.shape[0]
     dev = xyz.device
-    g = (n + 15) // 16
+    g = (n + 63) // 64
     nbr = torch.empty((n, k), dtype=torch.int32, device=dev)
     scans = torch.empty(g, dtype=torch.int32, device=dev)
     nodes = torch.empty(g, dtype=torch.int32, device=dev)

@@ -53,7 +53,7 @@ def clouds():
 @pytest.mark.parametrize("k", [1, 10, 64])
 def test_knn_walk_stats(name, k):
     """The kNN with its walk statistics: the same table as ezsp_knn and the
-    oracle; every 16-point group scans at least its own bucket and at most
+    oracle; every 64-point group scans at least its own buckets and at most
     every bucket."""
     xyz = clouds()[name]
     n = xyz.shape[0]
@@ -61,19 +61,19 @@ def test_knn_walk_stats(name, k):
     ref, _ = oracle.knn(xyz, k, "brute")
     assert np.array_equal(nbr.cpu().numpy(), ref)
     assert np.array_equal(nbr.cpu().numpy(), ezsp.knn(dev(xyz), k).cpu().numpy())
-    g = (n + 15) // 16
+    g, nb = (n + 63) // 64, (n + 15) // 16
+    own = np.minimum(4, nb - 4 * np.arange(g))
     scans, nodes = scans.cpu().numpy(), nodes.cpu().numpy()
     assert scans.shape == (g,) and nodes.shape == (g,)
-    assert (scans >= 1).all() and (scans <= g).all()
+    assert (scans >= own).all() and (scans <= nb).all()
     assert (nodes >= 0).all()
 
 
-@pytest.mark.parametrize("n,want", [(1, [1]), (16, [1]), (17, [2, 2]),
-                                    (32, [2, 2])])
+@pytest.mark.parametrize("n,want", [(1, [1]), (16, [1]), (17, [2]),
+                                    (32, [2]), (49, [4]), (64, [4])])
 def test_knn_walk_stats_small(n, want):
-    """One bucket: only its own scan.  Two buckets: each group scans its own
-    and its Morton neighbour first, and the walk then finds both already
-    taken; no inner node is entered."""
+    """Up to four buckets, one group: it scans its own buckets, and the walk
+    then finds every bucket already taken; no inner node is entered."""
     xyz = np.random.default_rng(n).random((n, 3), dtype=np.float32)
     _, scans, nodes = ezsp.knn_walk_stats(dev(xyz), min(4, max(n - 1, 1)))
     assert scans.cpu().numpy().tolist() == want
