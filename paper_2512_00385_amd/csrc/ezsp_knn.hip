@@ -149,51 +149,105 @@ __global__ __launch_bounds__(256) void k_morton(const float *xyz, int32_t n,
   vals[i] = (uint32_t)i;
 }
 
-// Sorted points as float4 (x, y, z, original index bits) plus both maps;
-// the array runs to a whole number of buckets (see k_gather_points).
-__global__ __launch_bounds__(256) void k_gather_points(
-    const float *xyz, int32_t n, const uint32_t *order, float4 *pts,
-    int32_t *perm, int32_t *inv, Ctl *ctl) {
-  const int32_t i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= n) {
-    // the last bucket's missing points: infinitely far, with an index above
-    // every real one, so a bucket scan needs no bounds check
-    if (i < pad_bucket(n))
-      pts[i] = make_float4(INFINITY, INFINITY, INFINITY,
-                           __int_as_float(kPadIndex));
-    return;
-  }
-  const uint32_t o = order[i];
-  if (o >= (uint32_t)n) {
-    raise_err(ctl, kErrInternal);
-    return;
-  }
-  const float *p = xyz + 3 * (int64_t)o;
-  pts[i] = make_float4(p[0], p[1], p[2], __int_as_float((int32_t)o));
-  perm[i] = (int32_t)o;
-  inv[o] = i;
+// Min and max along each 16-lane DPP row (a bucket of points): after the
+// four shifted steps lane 15 of the row holds the row's value (lanes whose
+// source is outside the row keep their own value).
+__device__ __forceinline__ float row_min15(float v) {
+  v = fminf(v, __int_as_float(__builtin_amdgcn_update_dpp(
+                   __float_as_int(v), __float_as_int(v), 0x111, 0xF, 0xF, false)));
+  v = fminf(v, __int_as_float(__builtin_amdgcn_update_dpp(
+                   __float_as_int(v), __float_as_int(v), 0x112, 0xF, 0xF, false)));
+  v = fminf(v, __int_as_float(__builtin_amdgcn_update_dpp(
+                   __float_as_int(v), __float_as_int(v), 0x114, 0xF, 0xF, false)));
+  v = fminf(v, __int_as_float(__builtin_amdgcn_update_dpp(
+                   __float_as_int(v), __float_as_int(v), 0x118, 0xF, 0xF, false)));
+  return v;
+}
+__device__ __forceinline__ float row_max15(float v) {
+  v = fmaxf(v, __int_as_float(__builtin_amdgcn_update_dpp(
+                   __float_as_int(v), __float_as_int(v), 0x111, 0xF, 0xF, false)));
+  v = fmaxf(v, __int_as_float(__builtin_amdgcn_update_dpp(
+                   __float_as_int(v), __float_as_int(v), 0x112, 0xF, 0xF, false)));
+  v = fmaxf(v, __int_as_float(__builtin_amdgcn_update_dpp(
+                   __float_as_int(v), __float_as_int(v), 0x114, 0xF, 0xF, false)));
+  v = fmaxf(v, __int_as_float(__builtin_amdgcn_update_dpp(
+                   __float_as_int(v), __float_as_int(v), 0x118, 0xF, 0xF, false)));
+  return v;
 }
 
-__global__ __launch_bounds__(256) void k_leaf_boxes(const float4 *pts,
-                                                    int32_t n, int32_t nb,
-                                                    float4 *blo, float4 *bhi) {
-  const int32_t b = blockIdx.x * blockDim.x + threadIdx.x;
-  if (b >= nb) return;
-  const int32_t s = b * kBucket;
-  const int32_t e = min(n, s + kBucket);
-  float4 lo = make_float4(INFINITY, INFINITY, INFINITY, 0.f);
-  float4 hi = make_float4(-INFINITY, -INFINITY, -INFINITY, 0.f);
-  for (int32_t i = s; i < e; ++i) {
-    float4 p = pts[i];
-    lo.x = fminf(lo.x, p.x);
-    lo.y = fminf(lo.y, p.y);
-    lo.z = fminf(lo.z, p.z);
-    hi.x = fmaxf(hi.x, p.x);
-    hi.y = fmaxf(hi.y, p.y);
-    hi.z = fmaxf(hi.z, p.z);
+__device__ __forceinline__ void box_join(float4 &lo, float4 &hi,
+                                         const float4 &a, const float4 &b) {
+  lo.x = fminf(lo.x, a.x);
+  lo.y = fminf(lo.y, a.y);
+  lo.z = fminf(lo.z, a.z);
+  hi.x = fmaxf(hi.x, b.x);
+  hi.y = fmaxf(hi.y, b.y);
+  hi.z = fmaxf(hi.z, b.z);
+}
+
+// Sorted points as float4 (x, y, z, original index bits) plus both maps;
+// the array runs to a whole number of buckets.  The same pass builds the
+// tree's two lowest levels: each bucket's box (16 consecutive points, one
+// DPP row) and the box of every 8 buckets (16 buckets per block).
+__global__ __launch_bounds__(256) void k_gather_points(
+    const float *xyz, int32_t n, const uint32_t *order, float4 *pts,
+    int32_t *perm, int32_t *inv, float4 *blo, float4 *bhi, Tree tree,
+    Ctl *ctl) {
+  __shared__ float4 s_lo[256 / kBucket], s_hi[256 / kBucket];
+  const int32_t i = blockIdx.x * blockDim.x + threadIdx.x;
+  // points past the end (the last bucket's missing ones) are infinitely
+  // far, with an index above every real one, so a bucket scan needs no
+  // bounds check; they take no part in the boxes
+  float4 p = make_float4(INFINITY, INFINITY, INFINITY,
+                         __int_as_float(kPadIndex));
+  bool real = false;
+  if (i < n) {
+    const uint32_t o = order[i];
+    if (o >= (uint32_t)n) {
+      raise_err(ctl, kErrInternal);
+    } else {
+      const float *q = xyz + 3 * (int64_t)o;
+      p = make_float4(q[0], q[1], q[2], __int_as_float((int32_t)o));
+      perm[i] = (int32_t)o;
+      inv[o] = i;
+      real = true;
+    }
   }
-  blo[b] = lo;
-  bhi[b] = hi;
+  if (i < pad_bucket(n)) pts[i] = p;
+  float4 lo = real ? p : make_float4(INFINITY, INFINITY, INFINITY, 0.f);
+  float4 hi = real ? p : make_float4(-INFINITY, -INFINITY, -INFINITY, 0.f);
+  lo.x = row_min15(lo.x);
+  lo.y = row_min15(lo.y);
+  lo.z = row_min15(lo.z);
+  hi.x = row_max15(hi.x);
+  hi.y = row_max15(hi.y);
+  hi.z = row_max15(hi.z);
+  lo.w = hi.w = 0.f;
+  const int32_t nb0 = tree.cnt[0];
+  const int32_t b = i / kBucket;
+  if ((threadIdx.x & (kBucket - 1)) == kBucket - 1) {
+    s_lo[threadIdx.x / kBucket] = lo;
+    s_hi[threadIdx.x / kBucket] = hi;
+    if (b < nb0) {
+      blo[b] = lo;
+      bhi[b] = hi;
+    }
+  }
+  __syncthreads();
+  constexpr int kPer = 256 / kBucket / kFan;  // level-1 nodes per block
+  if (tree.top >= 1 && threadIdx.x < kPer) {
+    const int32_t j = blockIdx.x * kPer + (int32_t)threadIdx.x;
+    if (j < tree.cnt[1]) {
+      float4 l1 = make_float4(INFINITY, INFINITY, INFINITY, 0.f);
+      float4 h1 = make_float4(-INFINITY, -INFINITY, -INFINITY, 0.f);
+      for (int c = 0; c < kFan; ++c)
+        if (j * kFan + c < nb0)
+          box_join(l1, h1, s_lo[threadIdx.x * kFan + c],
+                   s_hi[threadIdx.x * kFan + c]);
+      blo[tree.off[1] + j] = l1;
+      bhi[tree.off[1] + j] = h1;
+    }
+  }
 }
 
 __global__ __launch_bounds__(256) void k_up_boxes(float4 *blo, float4 *bhi,
@@ -206,17 +260,31 @@ __global__ __launch_bounds__(256) void k_up_boxes(float4 *blo, float4 *bhi,
   const int32_t e = min(child_cnt, s + kFan);
   float4 lo = make_float4(INFINITY, INFINITY, INFINITY, 0.f);
   float4 hi = make_float4(-INFINITY, -INFINITY, -INFINITY, 0.f);
-  for (int32_t c = s; c < e; ++c) {
-    float4 a = blo[child_off + c], b = bhi[child_off + c];
-    lo.x = fminf(lo.x, a.x);
-    lo.y = fminf(lo.y, a.y);
-    lo.z = fminf(lo.z, a.z);
-    hi.x = fmaxf(hi.x, b.x);
-    hi.y = fmaxf(hi.y, b.y);
-    hi.z = fmaxf(hi.z, b.z);
-  }
+  for (int32_t c = s; c < e; ++c)
+    box_join(lo, hi, blo[child_off + c], bhi[child_off + c]);
   blo[off + j] = lo;
   bhi[off + j] = hi;
+}
+
+// Levels l0 .. top in one block, a barrier between levels (the upper
+// levels are small: a launch per level would cost more than its work).
+__global__ __launch_bounds__(1024) void k_top_boxes(float4 *blo, float4 *bhi,
+                                                    Tree tree, int l0) {
+  for (int l = l0; l <= tree.top; ++l) {
+    const int32_t cnt = tree.cnt[l], child_cnt = tree.cnt[l - 1];
+    for (int32_t j = threadIdx.x; j < cnt; j += blockDim.x) {
+      const int32_t s = j * kFan;
+      const int32_t e = min(child_cnt, s + kFan);
+      float4 lo = make_float4(INFINITY, INFINITY, INFINITY, 0.f);
+      float4 hi = make_float4(-INFINITY, -INFINITY, -INFINITY, 0.f);
+      for (int32_t c = s; c < e; ++c)
+        box_join(lo, hi, blo[tree.off[l - 1] + c], bhi[tree.off[l - 1] + c]);
+      blo[tree.off[l] + j] = lo;
+      bhi[tree.off[l] + j] = hi;
+    }
+    __threadfence_block();
+    __syncthreads();
+  }
 }
 
 // A candidate is the 64-bit key (fp32 bits of d2) << 32 | original index.
@@ -593,6 +661,9 @@ void knn_reserve(Arena &a, int32_t n, int32_t k, KnnWork *w) {
   w->total = a.take<int32_t>(4);
 }
 
+// the largest level left to the single-block kernel
+constexpr int32_t kTopBoxes = 512;
+
 static hipError_t knn_impl(const float *xyz, int32_t n, int32_t k, Ctl *ctl,
                            const KnnWork &s, int32_t *nbr_out, float *d2_out,
                            const float *emb, int32_t d, float *emb_out,
@@ -612,14 +683,18 @@ static hipError_t knn_impl(const float *xyz, int32_t n, int32_t k, Ctl *ctl,
                                     s.hist, s.bsum, s.total, ctl, st);
   prof_end(st);
   const uint32_t *order = alt ? s.vals2 : s.vals;
+  // points in Morton order with the two lowest box levels, then a launch
+  // per level while a level is large, the rest in one block
   hipLaunchKernelGGL(k_gather_points, dim3(gb), dim3(nt), 0, st, xyz, n, order,
-                     s.pts, w.perm, w.inv, ctl);
-  hipLaunchKernelGGL(k_leaf_boxes, dim3((tree.cnt[0] + nt - 1) / nt), dim3(nt),
-                     0, st, s.pts, n, tree.cnt[0], s.blo, s.bhi);
-  for (int l = 1; l <= tree.top; ++l)
+                     s.pts, w.perm, w.inv, s.blo, s.bhi, tree, ctl);
+  int l = 2;
+  for (; l <= tree.top && tree.cnt[l] > kTopBoxes; ++l)
     hipLaunchKernelGGL(k_up_boxes, dim3((tree.cnt[l] + nt - 1) / nt), dim3(nt),
                        0, st, s.blo, s.bhi, tree.off[l - 1], tree.cnt[l - 1],
                        tree.off[l], tree.cnt[l]);
+  if (l <= tree.top)
+    hipLaunchKernelGGL(k_top_boxes, dim3(1), dim3(1024), 0, st, s.blo, s.bhi,
+                       tree, l);
   // a wave per four buckets, four waves per block
   constexpr int kOwn = kWave / kBucket;
   const int32_t n_waves = (tree.cnt[0] + kOwn - 1) / kOwn;
