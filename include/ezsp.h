@@ -97,8 +97,8 @@ size_t ezsp_knn_workspace_size(int64_t n, int32_t k);
  *   xyz  n*3 fp32 (in)
  *   nbr  n*k int32 (out): row p lists the k points q != p with the smallest
  *        (d2(p,q), q), in increasing order, where
- *        d2 = ((dx*dx) + (dy*dy)) + (dz*dz), dx = x_q - x_p, each operation
- *        one IEEE fp32 rounding (no fused multiply-add).  Ties in d2 go to
+ *        d2 = fma(dz, dz, fma(dy, dy, dx*dx)), dx = x_q - x_p, IEEE fp32,
+ *        each multiply, subtract and fused multiply-add one rounding.  Ties in d2 go to
  *        the smaller index.  When n-1 < k the row ends in -1 entries.
  *   d2   n*k fp32 (out, nullable): the matching squared distances, +inf
  *        where nbr is -1.

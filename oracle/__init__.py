@@ -4,7 +4,8 @@ TEST INFRASTRUCTURE ONLY.  Only ``tests/``, ``__graft_entry__.smoke()`` and the
 ``cpu_baseline`` leg of ``bench.py`` may import this package.  It shares no
 code with the HIP path (``paper_2512_00385_amd``) and never imports it.
 
-The arithmetic lives in ``ezsp_oracle.c`` (single-threaded C, no FMA); this
+The arithmetic lives in ``ezsp_oracle.c`` (single-threaded C, no implicit
+FMA: the kNN's fused steps are explicit ``fmaf`` calls); this
 module only loads it with ctypes and moves numpy arrays in and out.  Every
 function cites the passage of the paper it follows in the C header.
 """

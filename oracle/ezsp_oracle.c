@@ -26,16 +26,14 @@
 /* arithmetic and the order.                                                 */
 /* ======================================================================== */
 
-/* Squared distance between points p and q, IEEE fp32, fixed order. */
+/* Squared distance between points p and q, IEEE fp32, fixed order:
+ * fma(dz, dz, fma(dy, dy, dx * dx)), each fma one rounding (C99 fmaf). */
 static float sqdist(const float *xyz, int64_t p, int64_t q) {
   float dx = xyz[3 * q + 0] - xyz[3 * p + 0];
   float dy = xyz[3 * q + 1] - xyz[3 * p + 1];
   float dz = xyz[3 * q + 2] - xyz[3 * p + 2];
   float xx = dx * dx;
-  float yy = dy * dy;
-  float zz = dz * dz;
-  float s = xx + yy;
-  return s + zz;
+  return fmaf(dz, dz, fmaf(dy, dy, xx));
 }
 
 /* A sorted list of the k best (d2, index) pairs seen so far. */

@@ -29,7 +29,7 @@
  * Readings taken where the paper is silent (each one is listed, with the
  * reason, in the design notes of the repository):
  *   R1  kNN excludes the point itself by index; d2 is IEEE fp32,
- *       d2 = ((dx*dx) + (dy*dy)) + (dz*dz) with dx = x_q - x_p, no FMA;
+ *       d2 = fma(dz, dz, fma(dy, dy, dx*dx)) with dx = x_q - x_p, fp32;
  *       neighbours ordered by (d2, index); -1 padding when n-1 < k.
  *   R2  the graph is the union of the kNN relations, one edge per unordered
  *       pair, w = 1.

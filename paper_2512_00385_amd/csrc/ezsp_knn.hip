@@ -342,7 +342,7 @@ __device__ __forceinline__ int32_t row_bcast_i(int32_t v) {
 }
 
 // Key of candidate J of the bucket held one point per lane in q: d2 in the
-// fixed order ((dx*dx) + (dy*dy)) + (dz*dz), dx = x_q - x_p.  Only the
+// fixed order fma(dz, dz, fma(dy, dy, dx*dx)), dx = x_q - x_p.  Only the
 // query's own bucket can hold the query itself (SELF), which gives kNoKey.
 // Padding points past the end give an infinite d2 and an index above every
 // real one, so they never displace a real point.
@@ -354,8 +354,7 @@ __device__ __forceinline__ uint64_t bucket_key(const float4 &q, float px,
   const float dy = row_bcast<J>(q.y) - py;
   const float dz = row_bcast<J>(q.z) - pz;
   const int32_t qo = row_bcast_i<J>(__float_as_int(q.w));
-  const float xx = dx * dx, yy = dy * dy, zz = dz * dz;
-  const float d2 = (xx + yy) + zz;
+  const float d2 = fmaf(dz, dz, fmaf(dy, dy, dx * dx));
   if (SELF) return qo != me ? cand_key(d2, qo) : kEmpty;
   return cand_key(d2, qo);
 }
@@ -417,8 +416,7 @@ __device__ __forceinline__ float box_d2(const float4 &lo, const float4 &hi,
   const float ex = fmaxf(fmaxf(lo.x - px, px - hi.x), 0.f);
   const float ey = fmaxf(fmaxf(lo.y - py, py - hi.y), 0.f);
   const float ez = fmaxf(fmaxf(lo.z - pz, pz - hi.z), 0.f);
-  const float bx = ex * ex, by = ey * ey, bz = ez * ez;
-  return (bx + by) + bz;
+  return fmaf(ez, ez, fmaf(ey, ey, ex * ex));
 }
 
 // Coarse test of the children first .. first+7 (level lc) of one node,
@@ -439,8 +437,7 @@ __device__ __forceinline__ uint32_t coarse_mask(
   const float ex = fmaxf(fmaxf(lo.x - qhi.x, qlo.x - hi.x), 0.f);
   const float ey = fmaxf(fmaxf(lo.y - qhi.y, qlo.y - hi.y), 0.f);
   const float ez = fmaxf(fmaxf(lo.z - qhi.z, qlo.z - hi.z), 0.f);
-  const float bx = ex * ex, by = ey * ey, bz = ez * ez;
-  const float d2b = (bx + by) + bz;
+  const float d2b = fmaf(ez, ez, fmaf(ey, ey, ex * ex));
   const bool need = c < nchild && __float_as_uint(d2b) <= gkth;
   return (uint32_t)__ballot(need) & 0xffu;
 }

@@ -237,8 +237,7 @@ __global__ __launch_bounds__(256) void k_rev_count_kth(
         ++fwd;
         const float dx = pi.x - pu[t].x, dy = pi.y - pu[t].y,
                     dz = pi.z - pu[t].z;
-        const float xx = dx * dx, yy = dy * dy, zz = dz * dz;
-        const float d2 = (xx + yy) + zz;
+        const float d2 = fmaf(dz, dz, fmaf(dy, dy, dx * dx));
         const uint64_t key = ((uint64_t)__float_as_uint(d2) << 32) |
                              (uint32_t)__float_as_int(pi.w);
         if (key > ku[t]) mask |= 1ull << slot;

@@ -21,17 +21,49 @@ GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
 # kNN
 # --------------------------------------------------------------------------
 
+def fma32(a, b, c):
+    """Correctly rounded fp32 fused multiply-add, from fp64 without an FMA:
+    a*b is exact in fp64 (48-bit product), the fp64 sum s = a*b + c is
+    rounded to odd (TwoSum gives its exact error; an inexact s with an even
+    last bit moves one ulp towards the error), and rounding to odd with 29
+    spare bits makes the final rounding to fp32 the correct one."""
+    a, b, c = (np.asarray(x, np.float32).astype(np.float64) for x in (a, b, c))
+    p = a * b
+    s = p + c
+    bb = s - p
+    err = (p - (s - bb)) + (c - bb)
+    even = (s.view(np.uint64) & np.uint64(1)) == 0
+    bump = (err != 0) & even
+    s = np.where(bump, np.nextafter(s, np.where(err > 0, np.inf, -np.inf)), s)
+    return s.astype(np.float32)
+
+
+def test_fma32_by_hand():
+    """The emulated FMA keeps what an unfused sum loses: (1 + 2^-12)^2 - 1
+    needs the product's low bit, which an fp32 multiply rounds away."""
+    a = np.float32(1 + 2.0 ** -12)
+    fused = fma32(a, a, np.float32(-1.0))
+    assert fused == np.float32(2.0 ** -11 + 2.0 ** -24)
+    unfused = np.float32(a * a) - np.float32(1.0)
+    assert unfused == np.float32(2.0 ** -11)
+    # exact results stay exact; a tie of the fp32 rounding goes to the even
+    # neighbour; otherwise the nearer one
+    assert fma32(np.float32(3), np.float32(5), np.float32(7)) == 22
+    assert fma32(np.float32(1), np.float32(1), np.float32(2 ** 24)) == 2 ** 24
+    assert fma32(np.float32(1.5), np.float32(1.5), np.float32(2 ** 24)) == 2 ** 24 + 2
+
+
 def numpy_knn(xyz, k):
     """Independent brute force: numpy fp32 arithmetic in the same operation
-    order (numpy float32 ops are single IEEE roundings, no FMA), then a
-    lexicographic sort by (d2, index)."""
+    order (numpy float32 ops are single IEEE roundings; the two fused steps
+    emulated exactly by fma32), then a lexicographic sort by (d2, index)."""
     xyz = np.asarray(xyz, np.float32)
     n = xyz.shape[0]
     nbr = -np.ones((n, k), np.int32)
     d2o = np.full((n, k), np.inf, np.float32)
     for p in range(n):
         d = xyz - xyz[p]
-        d2 = (d[:, 0] * d[:, 0] + d[:, 1] * d[:, 1]) + d[:, 2] * d[:, 2]
+        d2 = fma32(d[:, 2], d[:, 2], fma32(d[:, 1], d[:, 1], d[:, 0] * d[:, 0]))
         idx = np.arange(n)
         m = idx != p
         order = np.lexsort((idx[m], d2[m]))[:k]
