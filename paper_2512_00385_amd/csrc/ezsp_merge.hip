@@ -1819,7 +1819,8 @@ __global__ void k_energy_reset(Ctl *ctl) {
 // snapshots that the labels and the energy read.
 // ---------------------------------------------------------------------------
 constexpr int kTailNT = 1024;
-constexpr int kTailNodes = 2048;    // largest graph the tail can take (LDS)
+constexpr int kTailNodes = 1536;    // largest graph the tail can take (LDS)
+constexpr int kTailWin = 8000;      // slots of new windows built in LDS
 constexpr int kTailStart = 1500;    // default switch to the tail
 constexpr int kTailEdges = 1 << 16; // ... directed entries at the switch
 constexpr int kTailSlots = 1 << 17; // gains: the live windows span at most
@@ -1983,6 +1984,8 @@ __global__ __launch_bounds__(kTailNT) void k_tail(TailState t, Ctl *ctl) {
   // members in this round; row to rebuild in this round
   __shared__ uint8_t s_live[kTailNodes], s_mrg[kTailNodes], s_new[kTailNodes],
       s_touch[kTailNodes];
+  // a round's new windows when they fit: built here, then copied out
+  __shared__ uint64_t s_win[kTailWin];
   __shared__ int32_t wsum[kTailNT / kWave];
   __shared__ int32_t s_any, s_flag, s_cnt, s_ne;
   __shared__ long long s_cut;
@@ -2282,8 +2285,15 @@ __global__ __launch_bounds__(kTailNT) void k_tail(TailState t, Ctl *ctl) {
       const int tn = whole ? 1 - tc : tc;
       const int32_t base = whole ? 0 : top;
       uint64_t *tn_tbl = t.tbl[tn];
-      for (int32_t q = threadIdx.x; q < spread * need; q += kTailNT)
-        tn_tbl[base + q] = kEmpty;
+      // the windows are built in LDS when they fit (their probes are then
+      // LDS atomics, not L2 round trips), else in place in the table
+      const bool in_lds = spread * need <= kTailWin;
+      for (int32_t q = threadIdx.x; q < spread * need; q += kTailNT) {
+        if (in_lds)
+          s_win[q] = kEmpty;
+        else
+          tn_tbl[base + q] = kEmpty;
+      }
       for (int32_t v = threadIdx.x; v < N; v += kTailNT) s_ndeg[v] = 0;
       // sources: the rows of every live node whose root is rebuilt
       const int32_t Ps = tail_scan(
@@ -2296,6 +2306,7 @@ __global__ __launch_bounds__(kTailNT) void k_tail(TailState t, Ctl *ctl) {
       // the root's new window.  A thread's kIU entries probe together: each
       // step issues one compare-and-swap per pending entry before waiting.
       constexpr int kIU = 4;
+      auto insert_all = [&](auto *win) {
       for (int32_t p0 = threadIdx.x; p0 < Ps; p0 += kIU * kTailNT) {
         int32_t A[kIU], B[kIU], W[kIU], np[kIU], pp[kIU], vv[kIU];
         uint32_t h[kIU];
@@ -2329,7 +2340,7 @@ __global__ __launch_bounds__(kTailNT) void k_tail(TailState t, Ctl *ctl) {
             got[j] = false;
             if (pend[j])
               got[j] = __hip_atomic_compare_exchange_strong(
-                  tn_tbl + base + spread * s_nws[A[j]] + h[j], &cur[j],
+                  win + spread * s_nws[A[j]] + h[j], &cur[j],
                   ((uint64_t)(uint32_t)B[j] << 32) | (uint32_t)W[j],
                   __ATOMIC_RELAXED, __ATOMIC_RELAXED,
                   __HIP_MEMORY_SCOPE_WORKGROUP);
@@ -2343,7 +2354,7 @@ __global__ __launch_bounds__(kTailNT) void k_tail(TailState t, Ctl *ctl) {
               atomicAdd(&s_ndeg[A[j]], 1);
               pend[j] = false;
             } else if ((int32_t)(cur[j] >> 32) == B[j]) {
-              __hip_atomic_fetch_add(tn_tbl + base + spread * s_nws[A[j]] + h[j],
+              __hip_atomic_fetch_add(win + spread * s_nws[A[j]] + h[j],
                                      (uint64_t)(uint32_t)W[j], __ATOMIC_RELAXED,
                                      __HIP_MEMORY_SCOPE_WORKGROUP);
               pend[j] = false;
@@ -2356,6 +2367,15 @@ __global__ __launch_bounds__(kTailNT) void k_tail(TailState t, Ctl *ctl) {
             }
           }
         }
+      }
+      };
+      if (in_lds) {
+        insert_all(s_win);
+        __syncthreads();
+        for (int32_t q = threadIdx.x; q < spread * need; q += kTailNT)
+          tn_tbl[base + q] = s_win[q];
+      } else {
+        insert_all(tn_tbl + base);
       }
       __syncthreads();
       // the new state: rebuilt windows, members dead, merge flags for the
