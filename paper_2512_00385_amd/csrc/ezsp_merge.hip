@@ -1170,6 +1170,91 @@ __global__ __launch_bounds__(256) void k_stats_g(
   }
 }
 
+// Step 4 statistics after the first round, G lanes per component with the
+// row's dimensions split among them: lane lg sums dimensions
+// [lg*DT/G, (lg+1)*DT/G) of every member (two 16-byte loads a member), so a
+// component of one member, most of them in a level with few merges, keeps
+// all G lanes loading; sizes, smallest points and degrees are summed over
+// every G-th member and combined in the group.  Same outputs as k_stats_g.
+template <int DT, int G>
+__global__ __launch_bounds__(256) void k_stats_s(
+    int32_t bound, const int32_t *__restrict__ mem,
+    const int32_t *__restrict__ moff, NodeIn s,
+    const int32_t *__restrict__ deg, NodeOut o,
+    int32_t *__restrict__ big, Ctl *ctl) {
+  constexpr int kPer = DT / G;  // dimensions per lane
+  static_assert(DT % G == 0 && kPer % 2 == 0, "dims per lane");
+  constexpr int kU = 4;  // members a step, their loads in flight together
+  if (!round_live(ctl)) return;
+  const int32_t total = min(bound, ctl->n_next) * G;
+  const int32_t per = ((total + kXcd - 1) / kXcd + G - 1) / G * G;
+  const int32_t j =
+      (int32_t)(blockIdx.x / kXcd) * (int32_t)blockDim.x + (int32_t)threadIdx.x;
+  const int32_t sub = (int32_t)(blockIdx.x % kXcd) * per + j;
+  if (j >= per || sub >= total) return;  // whole groups
+  const int32_t c = sub / G;
+  const int lg = sub & (G - 1);
+  const int32_t m0 = moff[c], m1 = moff[c + 1];
+  if (m1 - m0 > o.big_members) {
+    if (lg == 0) big[atomicAdd(&ctl->n_big, 1)] = c;
+    return;
+  }
+  const double sIF = ldexp(1.0, -ctl->F);
+  int32_t size = 0, mp = INT32_MAX, cap = 0;
+  int64_t acc[kPer];
+#pragma unroll
+  for (int q = 0; q < kPer; ++q) acc[q] = 0;
+  for (int32_t t0 = m0; t0 < m1; t0 += kU) {
+    int32_t mm[kU];
+#pragma unroll
+    for (int e = 0; e < kU; ++e) mm[e] = mem[min(t0 + e, m1 - 1)];
+    longlong2 x[kU][kPer / 2];
+#pragma unroll
+    for (int e = 0; e < kU; ++e) {
+      const longlong2 *p = reinterpret_cast<const longlong2 *>(
+          s.S + (int64_t)mm[e] * DT + lg * kPer);
+#pragma unroll
+      for (int q = 0; q < kPer / 2; ++q) x[e][q] = p[q];
+    }
+#pragma unroll
+    for (int e = 0; e < kU; ++e) {
+      const int32_t t = t0 + e;
+      if (t >= m1) break;
+#pragma unroll
+      for (int q = 0; q < kPer / 2; ++q) {
+        acc[2 * q + 0] += x[e][q].x;
+        acc[2 * q + 1] += x[e][q].y;
+      }
+      if ((t - m0) % G == lg) {  // this lane's share of the scalars
+        size += s.size[mm[e]];
+        mp = min(mp, s.minpt[mm[e]]);
+        cap += deg[mm[e]];
+      }
+    }
+  }
+#pragma unroll
+  for (int off = G / 2; off > 0; off >>= 1) {
+    size += __shfl_xor(size, off, kWave);
+    cap += __shfl_xor(cap, off, kWave);
+    mp = min(mp, __shfl_xor(mp, off, kWave));
+  }
+  if (lg == 0) {
+    o.size[c] = size;
+    o.minpt[c] = mp;
+    note_window(o, c, cap, m1 - m0, ctl);
+  }
+  const double dsz = (double)size;
+  longlong2 *So = reinterpret_cast<longlong2 *>(o.S + (int64_t)c * DT + lg * kPer);
+  double2 *Mo = reinterpret_cast<double2 *>(o.mu + (int64_t)c * DT + lg * kPer);
+#pragma unroll
+  for (int q = 0; q < kPer / 2; ++q) {
+    So[q] = make_longlong2(acc[2 * q], acc[2 * q + 1]);
+    const double q0 = (double)acc[2 * q] / dsz;
+    const double q1 = (double)acc[2 * q + 1] / dsz;
+    Mo[q] = make_double2(q0 * sIF, q1 * sIF);
+  }
+}
+
 template <bool FIRST>
 __global__ __launch_bounds__(256) void k_stats_big(
     const int32_t *__restrict__ mem, const int32_t *__restrict__ moff,
@@ -3737,7 +3822,12 @@ void launch_round(const Bufs &b, const Adj &adj, int cur, int32_t n,
                   b.minpt[nxt], b.capn,    b.wl[nxt],
                   b.cbig,      chunk,     kBigComp,
                   b.tile_c,    b.tile_i};
-  if constexpr (DT > 0) {
+  if constexpr (DT > 0 && !FIRST) {
+    constexpr int G = kStatsLanes;
+    hipLaunchKernelGGL((k_stats_s<DT, G>),
+                       xblocks_for((int64_t)nn * G + kXcd * G), dim3(256), 0,
+                       st, nn, b.mem, b.moff, s, b.deg, o, b.big, ctl);
+  } else if constexpr (DT > 0) {
     constexpr int G = kStatsLanes;
     hipLaunchKernelGGL((k_stats_g<FIRST, DT, G>),
                        xblocks_for((int64_t)nn * G + kXcd * G), dim3(256), 0,
