@@ -72,12 +72,18 @@ __global__ __launch_bounds__(kSortNT) void k_rs_scatter(
     uint64_t *__restrict__ kout, uint32_t *__restrict__ vout, int32_t n,
     int shift, const int32_t *__restrict__ offs, int32_t nb, Ctl *ctl) {
   constexpr int kW = kSortNT / kWave;
+  static_assert(kSortBins == kSortNT, "one digit per thread in the prefix");
   __shared__ int32_t run[kSortBins];
-  __shared__ int32_t wc[kW][kSortBins];
+  // per step: the waves' counts per digit, and the positions they turn
+  // into (kept apart so that the counts can be reset while the positions
+  // are read: two barriers a step)
+  __shared__ int32_t cnt[kW][kSortBins];
+  __shared__ int32_t pos0[kW][kSortBins];
   const int lane = threadIdx.x & (kWave - 1);
   const int wid = threadIdx.x / kWave;
-  for (int d = threadIdx.x; d < kSortBins; d += kSortNT)
-    run[d] = offs[d * nb + blockIdx.x];
+  run[threadIdx.x] = offs[threadIdx.x * nb + blockIdx.x];
+#pragma unroll
+  for (int w = 0; w < kW; ++w) cnt[w][threadIdx.x] = 0;
   const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (kWave - lane));
   const int32_t base = blockIdx.x * kSortTile;
   // the thread's keys and values of the whole tile, loaded before the first
@@ -90,11 +96,9 @@ __global__ __launch_bounds__(kSortNT) void k_rs_scatter(
     kt[j] = kin[i];
     vt[j] = vin[i];
   }
+  __syncthreads();
 #pragma unroll
   for (int j = 0; j < kSortItems; ++j) {
-    for (int t = threadIdx.x; t < kW * kSortBins; t += kSortNT)
-      (&wc[0][0])[t] = 0;
-    __syncthreads();
     const int32_t i = base + j * kSortNT + threadIdx.x;
     const bool valid = i < n;
     const uint64_t key = valid ? kt[j] : 0ull;
@@ -108,21 +112,23 @@ __global__ __launch_bounds__(kSortNT) void k_rs_scatter(
       peers &= bit ? bal : ~bal;
     }
     const int rank = __popcll(peers & lt_mask);
-    if (valid && rank == 0) wc[wid][dig] = __popcll(peers);
+    if (valid && rank == 0) cnt[wid][dig] = __popcll(peers);
     __syncthreads();
-    for (int d = threadIdx.x; d < kSortBins; d += kSortNT) {
+    {
+      const int d = threadIdx.x;
       int32_t p = run[d];
 #pragma unroll
       for (int w = 0; w < kW; ++w) {
-        int32_t c = wc[w][d];
-        wc[w][d] = p;
+        const int32_t c = cnt[w][d];
+        cnt[w][d] = 0;
+        pos0[w][d] = p;
         p += c;
       }
       run[d] = p;
     }
     __syncthreads();
     if (valid) {
-      const int32_t pos = wc[wid][dig] + rank;
+      const int32_t pos = pos0[wid][dig] + rank;
       if ((uint32_t)pos < (uint32_t)n) {
         kout[pos] = key;
         vout[pos] = val;
@@ -130,7 +136,6 @@ __global__ __launch_bounds__(kSortNT) void k_rs_scatter(
         raise_err(ctl, kErrInternal);
       }
     }
-    __syncthreads();
   }
 }
 
