@@ -67,12 +67,17 @@ __global__ __launch_bounds__(kSortNT) void k_rs_hist(const uint64_t *keys,
     hist[d * nb + blockIdx.x] = h[d];
 }
 
-__global__ __launch_bounds__(kSortNT) void k_rs_scatter(
+// The scatter takes a tile with twice the histogram's threads, half the
+// steps: fewer barriers for the same tile.
+constexpr int kScatNT = 2 * kSortNT;
+constexpr int kScatItems = kSortTile / kScatNT;
+
+__global__ __launch_bounds__(kScatNT) void k_rs_scatter(
     const uint64_t *__restrict__ kin, const uint32_t *__restrict__ vin,
     uint64_t *__restrict__ kout, uint32_t *__restrict__ vout, int32_t n,
     int shift, const int32_t *__restrict__ offs, int32_t nb, Ctl *ctl) {
-  constexpr int kW = kSortNT / kWave;
-  static_assert(kSortBins == kSortNT, "one digit per thread in the prefix");
+  constexpr int kW = kScatNT / kWave;
+  static_assert(kSortBins <= kScatNT, "one digit per thread in the prefix");
   __shared__ int32_t run[kSortBins];
   // per step: the waves' counts per digit, and the positions they turn
   // into (kept apart so that the counts can be reset while the positions
@@ -81,25 +86,27 @@ __global__ __launch_bounds__(kSortNT) void k_rs_scatter(
   __shared__ int32_t pos0[kW][kSortBins];
   const int lane = threadIdx.x & (kWave - 1);
   const int wid = threadIdx.x / kWave;
-  run[threadIdx.x] = offs[threadIdx.x * nb + blockIdx.x];
+  if (threadIdx.x < kSortBins) {
+    run[threadIdx.x] = offs[threadIdx.x * nb + blockIdx.x];
 #pragma unroll
-  for (int w = 0; w < kW; ++w) cnt[w][threadIdx.x] = 0;
+    for (int w = 0; w < kW; ++w) cnt[w][threadIdx.x] = 0;
+  }
   const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (kWave - lane));
   const int32_t base = blockIdx.x * kSortTile;
   // the thread's keys and values of the whole tile, loaded before the first
   // step (clamped indices, no branch): the steps then wait on LDS only
-  uint64_t kt[kSortItems];
-  uint32_t vt[kSortItems];
+  uint64_t kt[kScatItems];
+  uint32_t vt[kScatItems];
 #pragma unroll
-  for (int j = 0; j < kSortItems; ++j) {
-    const int32_t i = min(base + j * kSortNT + (int32_t)threadIdx.x, n - 1);
+  for (int j = 0; j < kScatItems; ++j) {
+    const int32_t i = min(base + j * kScatNT + (int32_t)threadIdx.x, n - 1);
     kt[j] = kin[i];
     vt[j] = vin[i];
   }
   __syncthreads();
 #pragma unroll
-  for (int j = 0; j < kSortItems; ++j) {
-    const int32_t i = base + j * kSortNT + threadIdx.x;
+  for (int j = 0; j < kScatItems; ++j) {
+    const int32_t i = base + j * kScatNT + threadIdx.x;
     const bool valid = i < n;
     const uint64_t key = valid ? kt[j] : 0ull;
     const uint32_t val = valid ? vt[j] : 0u;
@@ -114,7 +121,7 @@ __global__ __launch_bounds__(kSortNT) void k_rs_scatter(
     const int rank = __popcll(peers & lt_mask);
     if (valid && rank == 0) cnt[wid][dig] = __popcll(peers);
     __syncthreads();
-    {
+    if (threadIdx.x < kSortBins) {
       const int d = threadIdx.x;
       int32_t p = run[d];
 #pragma unroll
@@ -157,7 +164,7 @@ bool radix_sort_pairs(uint64_t *keys, uint32_t *vals, uint64_t *keys_alt,
                        shift, hist, nb);
     const int32_t nh = kSortBins * nb;
     device_scan(ScanArray{hist, hist, nh, nullptr}, nh, bsum, total, st);
-    hipLaunchKernelGGL(k_rs_scatter, dim3(nb), dim3(kSortNT), 0, st, kin, vin,
+    hipLaunchKernelGGL(k_rs_scatter, dim3(nb), dim3(kScatNT), 0, st, kin, vin,
                        kout, vout, n, shift, hist, nb, ctl);
     uint64_t *tk = kin;
     kin = kout;
