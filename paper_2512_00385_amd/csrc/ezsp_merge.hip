@@ -1086,97 +1086,17 @@ __global__ __launch_bounds__(256) void k_stats(
 // Components with many members: one block each, threads stride over the
 // members and the sums are combined in shared memory (integer, so the
 // order does not matter).
-// Step 4 statistics with G lanes per component (rows of DT values): the
-// lanes take every G-th member, each summing whole rows, then the group
-// adds its partial sums (exact int64) and spreads the stores over its lanes.
-// Components are laid out over the XCDs like xcd_item, in whole groups.
-template <bool FIRST, int DT, int G>
-__global__ __launch_bounds__(256) void k_stats_g(
-    int32_t bound, const int32_t *__restrict__ mem,
-    const int32_t *__restrict__ moff, NodeIn s,
-    const int32_t *__restrict__ deg, NodeOut o,
-    int32_t *__restrict__ big, Ctl *ctl) {
-  static_assert(DT % G == 0 && (DT / G) % 2 == 0, "dims per lane");
-  if (!round_live(ctl)) return;
-  const int32_t total = min(bound, ctl->n_next) * G;
-  const int32_t per = ((total + kXcd - 1) / kXcd + G - 1) / G * G;
-  const int32_t j =
-      (int32_t)(blockIdx.x / kXcd) * (int32_t)blockDim.x + (int32_t)threadIdx.x;
-  const int32_t sub = (int32_t)(blockIdx.x % kXcd) * per + j;
-  if (j >= per || sub >= total) return;  // whole groups
-  const int32_t c = sub / G;
-  const int lg = sub & (G - 1);
-  const int32_t m0 = moff[c], m1 = moff[c + 1];
-  if (m1 - m0 > o.big_members) {
-    if (lg == 0) big[atomicAdd(&ctl->n_big, 1)] = c;
-    return;
-  }
-  const double sF = ldexp(1.0, ctl->F), sIF = ldexp(1.0, -ctl->F);
-  int32_t size = 0, mp = INT32_MAX, cap = 0;
-  int64_t acc[DT];
-#pragma unroll
-  for (int q = 0; q < DT; ++q) acc[q] = 0;
-  for (int32_t t = m0 + lg; t < m1; t += G) {
-    const int32_t m = mem[t];
-    size += node_size<FIRST>(s, m);
-    mp = min(mp, node_minpt<FIRST>(s, m));
-    cap += deg[m];
-    if (FIRST) {
-      const float4 *p = reinterpret_cast<const float4 *>(s.emb + (int64_t)m * DT);
-#pragma unroll
-      for (int q = 0; q < DT / 4; ++q) {
-        const float4 x = p[q];
-        acc[4 * q + 0] += (int64_t)rint((double)x.x * sF);
-        acc[4 * q + 1] += (int64_t)rint((double)x.y * sF);
-        acc[4 * q + 2] += (int64_t)rint((double)x.z * sF);
-        acc[4 * q + 3] += (int64_t)rint((double)x.w * sF);
-      }
-    } else {
-      const longlong2 *p =
-          reinterpret_cast<const longlong2 *>(s.S + (int64_t)m * DT);
-#pragma unroll
-      for (int q = 0; q < DT / 2; ++q) {
-        const longlong2 x = p[q];
-        acc[2 * q + 0] += x.x;
-        acc[2 * q + 1] += x.y;
-      }
-    }
-  }
-#pragma unroll
-  for (int off = G / 2; off > 0; off >>= 1) {
-    size += __shfl_xor(size, off, kWave);
-    cap += __shfl_xor(cap, off, kWave);
-    mp = min(mp, __shfl_xor(mp, off, kWave));
-#pragma unroll
-    for (int q = 0; q < DT; ++q)
-      acc[q] += __shfl_xor((long long)acc[q], off, kWave);
-  }
-  if (lg == 0) {
-    o.size[c] = size;
-    o.minpt[c] = mp;
-    note_window(o, c, cap, m1 - m0, ctl);
-  }
-  const double dsz = (double)size;
-  constexpr int kPer = DT / G;
-  longlong2 *So = reinterpret_cast<longlong2 *>(o.S + (int64_t)c * DT);
-  double2 *Mo = reinterpret_cast<double2 *>(o.mu + (int64_t)c * DT);
-#pragma unroll
-  for (int q = 0; q < DT / 2; ++q) {
-    if (q / (kPer / 2) != lg) continue;  // this lane's share of the row
-    So[q] = make_longlong2(acc[2 * q], acc[2 * q + 1]);
-    const double q0 = (double)acc[2 * q] / dsz;
-    const double q1 = (double)acc[2 * q + 1] / dsz;
-    Mo[q] = make_double2(q0 * sIF, q1 * sIF);
-  }
-}
-
-// Step 4 statistics after the first round, G lanes per component with the
+// Step 4 statistics with G lanes per component (rows of DT values) and the
 // row's dimensions split among them: lane lg sums dimensions
-// [lg*DT/G, (lg+1)*DT/G) of every member (two 16-byte loads a member), so a
+// [lg*DT/G, (lg+1)*DT/G) of every member, four members a step, so a
 // component of one member, most of them in a level with few merges, keeps
-// all G lanes loading; sizes, smallest points and degrees are summed over
-// every G-th member and combined in the group.  Same outputs as k_stats_g.
-template <int DT, int G>
+// all G lanes loading, and the loads of a member's row are side by side;
+// sizes, smallest points and degrees are summed over every G-th member and
+// combined in the group (exact int64, so the order does not matter).
+// Components are laid out over the XCDs like xcd_item, in whole groups.
+// FIRST: the members are points, their sums rint(e * 2^F) of the fp32
+// embedding; later: the members' int64 sums.
+template <bool FIRST, int DT, int G>
 __global__ __launch_bounds__(256) void k_stats_s(
     int32_t bound, const int32_t *__restrict__ mem,
     const int32_t *__restrict__ moff, NodeIn s,
@@ -1199,7 +1119,7 @@ __global__ __launch_bounds__(256) void k_stats_s(
     if (lg == 0) big[atomicAdd(&ctl->n_big, 1)] = c;
     return;
   }
-  const double sIF = ldexp(1.0, -ctl->F);
+  const double sF = ldexp(1.0, ctl->F), sIF = ldexp(1.0, -ctl->F);
   int32_t size = 0, mp = INT32_MAX, cap = 0;
   int64_t acc[kPer];
 #pragma unroll
@@ -1208,27 +1128,53 @@ __global__ __launch_bounds__(256) void k_stats_s(
     int32_t mm[kU];
 #pragma unroll
     for (int e = 0; e < kU; ++e) mm[e] = mem[min(t0 + e, m1 - 1)];
-    longlong2 x[kU][kPer / 2];
+    if constexpr (FIRST) {
+      float2 x[kU][kPer / 2];
 #pragma unroll
-    for (int e = 0; e < kU; ++e) {
-      const longlong2 *p = reinterpret_cast<const longlong2 *>(
-          s.S + (int64_t)mm[e] * DT + lg * kPer);
+      for (int e = 0; e < kU; ++e) {
+        const float2 *p = reinterpret_cast<const float2 *>(
+            s.emb + (int64_t)mm[e] * DT + lg * kPer);
 #pragma unroll
-      for (int q = 0; q < kPer / 2; ++q) x[e][q] = p[q];
-    }
-#pragma unroll
-    for (int e = 0; e < kU; ++e) {
-      const int32_t t = t0 + e;
-      if (t >= m1) break;
-#pragma unroll
-      for (int q = 0; q < kPer / 2; ++q) {
-        acc[2 * q + 0] += x[e][q].x;
-        acc[2 * q + 1] += x[e][q].y;
+        for (int q = 0; q < kPer / 2; ++q) x[e][q] = p[q];
       }
-      if ((t - m0) % G == lg) {  // this lane's share of the scalars
-        size += s.size[mm[e]];
-        mp = min(mp, s.minpt[mm[e]]);
-        cap += deg[mm[e]];
+#pragma unroll
+      for (int e = 0; e < kU; ++e) {
+        const int32_t t = t0 + e;
+        if (t >= m1) break;
+#pragma unroll
+        for (int q = 0; q < kPer / 2; ++q) {
+          acc[2 * q + 0] += (int64_t)rint((double)x[e][q].x * sF);
+          acc[2 * q + 1] += (int64_t)rint((double)x[e][q].y * sF);
+        }
+        if ((t - m0) % G == lg) {  // this lane's share of the scalars
+          size += 1;
+          mp = min(mp, node_minpt<true>(s, mm[e]));
+          cap += deg[mm[e]];
+        }
+      }
+    } else {
+      longlong2 x[kU][kPer / 2];
+#pragma unroll
+      for (int e = 0; e < kU; ++e) {
+        const longlong2 *p = reinterpret_cast<const longlong2 *>(
+            s.S + (int64_t)mm[e] * DT + lg * kPer);
+#pragma unroll
+        for (int q = 0; q < kPer / 2; ++q) x[e][q] = p[q];
+      }
+#pragma unroll
+      for (int e = 0; e < kU; ++e) {
+        const int32_t t = t0 + e;
+        if (t >= m1) break;
+#pragma unroll
+        for (int q = 0; q < kPer / 2; ++q) {
+          acc[2 * q + 0] += x[e][q].x;
+          acc[2 * q + 1] += x[e][q].y;
+        }
+        if ((t - m0) % G == lg) {  // this lane's share of the scalars
+          size += s.size[mm[e]];
+          mp = min(mp, s.minpt[mm[e]]);
+          cap += deg[mm[e]];
+        }
       }
     }
   }
@@ -3822,14 +3768,9 @@ void launch_round(const Bufs &b, const Adj &adj, int cur, int32_t n,
                   b.minpt[nxt], b.capn,    b.wl[nxt],
                   b.cbig,      chunk,     kBigComp,
                   b.tile_c,    b.tile_i};
-  if constexpr (DT > 0 && !FIRST) {
+  if constexpr (DT > 0) {
     constexpr int G = kStatsLanes;
-    hipLaunchKernelGGL((k_stats_s<DT, G>),
-                       xblocks_for((int64_t)nn * G + kXcd * G), dim3(256), 0,
-                       st, nn, b.mem, b.moff, s, b.deg, o, b.big, ctl);
-  } else if constexpr (DT > 0) {
-    constexpr int G = kStatsLanes;
-    hipLaunchKernelGGL((k_stats_g<FIRST, DT, G>),
+    hipLaunchKernelGGL((k_stats_s<FIRST, DT, G>),
                        xblocks_for((int64_t)nn * G + kXcd * G), dim3(256), 0,
                        st, nn, b.mem, b.moff, s, b.deg, o, b.big, ctl);
   } else {
