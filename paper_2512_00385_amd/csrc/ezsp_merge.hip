@@ -1327,6 +1327,13 @@ __device__ __forceinline__ void batch_find_n(const int32_t *pre,
 }
 
 
+// Start slot of key B in a window of cap slots: the multiplicative hash
+// scaled into [0, cap) by the high half of a 32x32 product (one
+// instruction, where a remainder by a variable takes a dozen).
+__device__ __forceinline__ uint32_t window_slot(int32_t B, int32_t cap) {
+  return __umulhi((uint32_t)B * 2654435761u, (uint32_t)cap);
+}
+
 template <bool FIRST>
 __global__ __launch_bounds__(256) void k_contract_chunk(
     int32_t nn, Adj a, const int32_t *__restrict__ L,
@@ -1419,7 +1426,7 @@ __global__ __launch_bounds__(256) void k_contract_chunk(
           const int32_t A = ok[e] ? bA[slot[e]] : -1;
           if (!ok[e] || A == B[e]) continue;  // edge inside a merged component
           const int32_t lb = blb[slot[e]], cp = bcp[slot[e]];
-          uint32_t h = ((uint32_t)B[e] * 2654435761u) % (uint32_t)cp;
+          uint32_t h = window_slot(B[e], cp);
           int32_t probe = 0;
           for (; probe < cp; ++probe) {
             const int32_t old = atomicCAS(&kb[lb + h], -1, B[e]);
@@ -1489,7 +1496,7 @@ __global__ __launch_bounds__(256) void k_clear_big(
 __device__ __forceinline__ bool table_add(uint64_t *tbl, int32_t base,
                                           int32_t cap, int32_t B, int32_t w,
                                           Ctl *ctl, int64_t base64 = 0) {
-  uint32_t h = ((uint32_t)B * 2654435761u) % (uint32_t)cap;
+  uint32_t h = window_slot(B, cap);
   const unsigned long long mine =
       ((unsigned long long)(uint32_t)B << 32) | (uint32_t)w;
   for (int32_t probe = 0; probe < cap; ++probe) {
@@ -2358,9 +2365,7 @@ __global__ __launch_bounds__(kTailNT) void k_tail(TailState t, Ctl *ctl) {
           W[j] = (int32_t)(uint32_t)e;
           pend[j] = A[j] != B[j];  // not inside a component
           np[j] = 0;
-          h[j] = pend[j] ? ((uint32_t)B[j] * 2654435761u) %
-                               (uint32_t)(spread * s_cap[A[j]])
-                         : 0u;
+          h[j] = pend[j] ? window_slot(B[j], spread * s_cap[A[j]]) : 0u;
         }
         for (bool any = true; any;) {
           uint64_t cur[kIU];
