@@ -2030,7 +2030,7 @@ __global__ __launch_bounds__(kTailNT) void k_tail(TailState t, Ctl *ctl) {
   __shared__ double s_lambda[kTailLevels];
   __shared__ long long s_smin[kTailLevels];
   const int lane = threadIdx.x & (kWave - 1);
-  const int32_t d = t.d;
+  const int32_t d = DT > 0 ? DT : t.d;  // a constant divisor when DT is given
   const int32_t N = t.nn0;
   const double sIF = ldexp(1.0, -ctl->F);
   // s_key doubles as the new entry counts once the choices are made
