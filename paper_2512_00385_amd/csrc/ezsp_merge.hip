@@ -1371,9 +1371,27 @@ __global__ __launch_bounds__(256) void k_contract_chunk(
     const int32_t m_hi =
         (c_hi > c_lo && cap[c_hi - 1] > chunk) ? moff[c_hi - 1] : moff[c_hi];
     constexpr int kUnroll = 4;  // entries per thread with their loads in flight
+    // entry (slot, u, w) of the batch into its component's LDS window
+    auto insert = [&](bool ok, int32_t sl, int32_t B, int32_t w) {
+      const int32_t A = ok ? bA[sl] : -1;
+      if (!ok || A == B) return;  // edge inside a merged component
+      const int32_t lb = blb[sl], cp = bcp[sl];
+      uint32_t h = window_slot(B, cp);
+      int32_t probe = 0;
+      for (; probe < cp; ++probe) {
+        const int32_t old = atomicCAS(&kb[lb + h], -1, B);
+        if (old == -1 || old == B) {
+          atomicAdd(&kw[lb + h], w);
+          break;
+        }
+        h = (h + 1 == (uint32_t)cp) ? 0u : h + 1;
+      }
+      if (probe == cp) raise_err(ctl, kErrInternal);
+    };
     for (int32_t b0 = m_lo; b0 < m_hi; b0 += kBatch) {
       const int32_t idx = b0 + (int32_t)threadIdx.x;
       int32_t span = 0;
+      bool take = false;
       if (idx < m_hi) {
         const int32_t m = mem[idx];
         // the row's span and base depend on m only: loaded with L[m]
@@ -1386,7 +1404,10 @@ __global__ __launch_bounds__(256) void k_contract_chunk(
           if (lb < 0 || lb + cp > 2 * chunk) {
             raise_err(ctl, kErrInternal);
           } else {
-            span = sp;
+            take = true;
+            // first round: the k forward entries go by position (slot =
+            // entry / k), only the reverse lists by search
+            span = FIRST ? sp - a.k : sp;
             bm[threadIdx.x] = m;
             bA[threadIdx.x] = A;
             blb[threadIdx.x] = lb;
@@ -1395,10 +1416,40 @@ __global__ __launch_bounds__(256) void k_contract_chunk(
           }
         }
       }
+      if (FIRST && !take) bA[threadIdx.x] = -1;  // no forward entries
       int32_t total;
       pre[threadIdx.x] = block_excl_scan<256>(span, wsum, &total);
       if (threadIdx.x == 0) pre[kBatch] = total;
       __syncthreads();
+      if constexpr (FIRST) {
+        const int32_t nsl = min(kBatch, m_hi - b0);
+        const int32_t kf = a.k, totf = nsl * kf;
+        // f / k as a multiply-high: ceil(2^32 / k) is exact for f * k < 2^32
+        const uint32_t kmag = 0xffffffffu / (uint32_t)kf + 1u;
+        for (int32_t f0 = threadIdx.x; f0 < totf; f0 += kUnroll * 256) {
+          int32_t sl[kUnroll], u[kUnroll], B[kUnroll];
+          bool ok[kUnroll];
+#pragma unroll
+          for (int e = 0; e < kUnroll; ++e) {
+            const int32_t f = min(f0 + e * 256, totf - 1);
+            sl[e] = kf == 1 ? f : (int32_t)__umulhi((uint32_t)f, kmag);
+            const int32_t j = f - sl[e] * kf;
+            ok[e] = f0 + e * 256 < totf && bA[sl[e]] >= 0;
+            u[e] = ok[e] ? a.nbr[(int64_t)bm[sl[e]] * a.kp + j] : -1;
+          }
+#pragma unroll
+          for (int e = 0; e < kUnroll; ++e) {
+            ok[e] = ok[e] && u[e] >= 0;
+            if (ok[e] && (uint32_t)u[e] >= (uint32_t)nn) {
+              raise_err(ctl, kErrInternal);
+              ok[e] = false;
+            }
+            B[e] = ok[e] ? L[u[e]] : -1;
+          }
+#pragma unroll
+          for (int e = 0; e < kUnroll; ++e) insert(ok[e], sl[e], B[e], 1);
+        }
+      }
       for (int32_t f0 = threadIdx.x; f0 < total; f0 += kUnroll * 256) {
         int32_t slot[kUnroll], u[kUnroll], w[kUnroll], B[kUnroll];
         int32_t fe[kUnroll], je[kUnroll];
@@ -1409,9 +1460,10 @@ __global__ __launch_bounds__(256) void k_contract_chunk(
   #pragma unroll
         for (int e = 0; e < kUnroll; ++e) {
           ok[e] = false;
-          if (f0 + e * 256 < total)
-            ok[e] = row_entry_at<FIRST>(a, bm[slot[e]], bbase[slot[e]], je[e],
-                                        u[e], w[e]);
+          if (f0 + e * 256 < total)  // (first round: reverse entry je)
+            ok[e] = row_entry_at<FIRST>(a, bm[slot[e]], bbase[slot[e]],
+                                        FIRST ? a.k + je[e] : je[e], u[e],
+                                        w[e]);
         }
   #pragma unroll
         for (int e = 0; e < kUnroll; ++e) {
@@ -1422,22 +1474,7 @@ __global__ __launch_bounds__(256) void k_contract_chunk(
           B[e] = ok[e] ? L[u[e]] : -1;
         }
   #pragma unroll
-        for (int e = 0; e < kUnroll; ++e) {
-          const int32_t A = ok[e] ? bA[slot[e]] : -1;
-          if (!ok[e] || A == B[e]) continue;  // edge inside a merged component
-          const int32_t lb = blb[slot[e]], cp = bcp[slot[e]];
-          uint32_t h = window_slot(B[e], cp);
-          int32_t probe = 0;
-          for (; probe < cp; ++probe) {
-            const int32_t old = atomicCAS(&kb[lb + h], -1, B[e]);
-            if (old == -1 || old == B[e]) {
-              atomicAdd(&kw[lb + h], w[e]);
-              break;
-            }
-            h = (h + 1 == (uint32_t)cp) ? 0u : h + 1;
-          }
-          if (probe == cp) raise_err(ctl, kErrInternal);
-        }
+        for (int e = 0; e < kUnroll; ++e) insert(ok[e], slot[e], B[e], w[e]);
       }
       __syncthreads();
     }
