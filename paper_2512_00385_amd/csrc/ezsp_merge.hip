@@ -2070,6 +2070,11 @@ __global__ __launch_bounds__(kTailNT) void k_tail(TailState t, Ctl *ctl) {
   const int32_t d = DT > 0 ? DT : t.d;  // a constant divisor when DT is given
   const int32_t N = t.nn0;
   const double sIF = ldexp(1.0, -ctl->F);
+  // the window area is free during selection: it holds the first kLE
+  // listed edges and their gains, the rest go to global memory
+  constexpr int32_t kLE = kTailWin / 2;
+  uint64_t *s_el = s_win;
+  double *s_gn = reinterpret_cast<double *>(s_win + kLE);
   // s_key doubles as the new entry counts once the choices are made
   int32_t *s_ndeg = reinterpret_cast<int32_t *>(s_key);
   if (N > kTailNodes || N < 1) {
@@ -2147,9 +2152,12 @@ __global__ __launch_bounds__(kTailNT) void k_tail(TailState t, Ctl *ctl) {
         }
         if (u < v && scanned(u)) return;
         const int32_t i = atomicAdd(&s_ne, 1);
-        if (i < t.gcap)
-          t.elist[i] = ((uint64_t)(uint32_t)(v | (u << 16)) << 32) |
-                       (uint32_t)e;
+        const uint64_t le =
+            ((uint64_t)(uint32_t)(v | (u << 16)) << 32) | (uint32_t)e;
+        if (i < kLE)
+          s_el[i] = le;
+        else if (i < t.gcap)
+          t.elist[i] = le;
         else
           raise_err(ctl, kErrInternal);
       });
@@ -2160,7 +2168,10 @@ __global__ __launch_bounds__(kTailNT) void k_tail(TailState t, Ctl *ctl) {
       for (int32_t i0 = threadIdx.x; i0 < ne; i0 += 2 * kTailNT) {
         uint64_t ev[2];
 #pragma unroll
-        for (int j = 0; j < 2; ++j) ev[j] = t.elist[min(i0 + j * kTailNT, ne - 1)];
+        for (int j = 0; j < 2; ++j) {
+          const int32_t i = min(i0 + j * kTailNT, ne - 1);
+          ev[j] = i < kLE ? s_el[i] : t.elist[i];
+        }
 #pragma unroll
         for (int j = 0; j < 2; ++j) {
           const int32_t i = i0 + j * kTailNT;
@@ -2170,7 +2181,10 @@ __global__ __launch_bounds__(kTailNT) void k_tail(TailState t, Ctl *ctl) {
           const int32_t w = (int32_t)(uint32_t)ev[j];
           const double g = tail_gain<DT>(t.mu, v, u, d, (double)s_size[v],
                                          (double)s_size[u], w, lambda);
-          t.gain[i] = g;
+          if (i < kLE)
+            s_gn[i] = g;
+          else
+            t.gain[i] = g;
           const unsigned long long kg = gain_key(g);
           if (g > 0.0 || (long long)s_size[v] < smin) atomicMax(&s_key[v], kg);
           if (g > 0.0 || (long long)s_size[u] < smin) atomicMax(&s_key[u], kg);
@@ -2186,8 +2200,8 @@ __global__ __launch_bounds__(kTailNT) void k_tail(TailState t, Ctl *ctl) {
 #pragma unroll
         for (int j = 0; j < kTU; ++j) {
           const int32_t i = min(i0 + j * kTailNT, ne - 1);  // no branch
-          ev[j] = t.elist[i];
-          gv[j] = t.gain[i];
+          ev[j] = i < kLE ? s_el[i] : t.elist[i];
+          gv[j] = i < kLE ? s_gn[i] : t.gain[i];
         }
 #pragma unroll
         for (int j = 0; j < kTU; ++j) {
@@ -2361,7 +2375,9 @@ __global__ __launch_bounds__(kTailNT) void k_tail(TailState t, Ctl *ctl) {
       const int32_t base = whole ? 0 : top;
       uint64_t *tn_tbl = t.tbl[tn];
       // the windows are built in LDS when they fit (their probes are then
-      // LDS atomics, not L2 round trips), else in place in the table
+      // LDS atomics, not L2 round trips), else in place in the table; LDS
+      // at load factor <= 1 beats the table at <= 1/2
+      if (spread == 2 && 2 * need > kTailWin && need <= kTailWin) spread = 1;
       const bool in_lds = spread * need <= kTailWin;
       for (int32_t q = threadIdx.x; q < spread * need; q += kTailNT) {
         if (in_lds)
