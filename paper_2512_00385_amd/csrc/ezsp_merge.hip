@@ -670,6 +670,145 @@ __global__ __launch_bounds__(256) void k_select(
     ctl->any_choice = 1;
 }
 
+// Steps 1-2 of the first round for D = DT (a multiple of 4): a block takes
+// kSelFirstBytes / (4 DT) consecutive nodes and stages their embedding rows
+// in LDS.  Internal order is Morton order, so most neighbours of a node lie
+// in its own block (on the driving tile, 86 % of the kNN entries for blocks
+// of 512 nodes) and are read from LDS, the others from global memory.
+// Every node is one point (|P| = 1), so the smallest point of a neighbour,
+// which only breaks ties of equal gains, is loaded only for a tie and for
+// each lane's final choice.  The same choice as k_select<true>.
+// The rows are staged as the fp32 integers a = rint(e * 2^F): e * 2^F is
+// exact in fp32 (16 <= F <= 40, |e| * 2^F < 2^62) and so is its rounding,
+// and mu = a * 2^-F.  Scaling by a power of two commutes with rounding in
+// the normal range, so the sum of the squared differences of the a's
+// times 2^-2F is, bit for bit, the sum over the mu's: the conversion is
+// done once per staged row, and a gain costs four operations a dimension.
+constexpr int kSelFirstBytes = 32768;
+template <int DT, int G>
+__global__ __launch_bounds__(256) void k_select_first(
+    int32_t nn, Adj a, NodeIn s, double lambda, int64_t smin,
+    int32_t *__restrict__ target, int32_t *__restrict__ deg, LongWork lw,
+    Ctl *ctl) {
+  static_assert(DT > 0 && DT % 4 == 0, "float4 rows");
+  constexpr int Q = DT / 4;                          // float4 per row
+  constexpr int32_t R = kSelFirstBytes / (16 * Q);   // nodes per block
+  __shared__ float4 sE[R * Q];
+  const int32_t lo = xcd_block() * R;
+  if (lo >= nn) return;  // the whole block
+  const int32_t nr = min(R, nn - lo);
+  const float4 *gE = reinterpret_cast<const float4 *>(s.emb);
+  const int F = ctl->F;
+  const float sFf = ldexpf(1.0f, F);
+  const double sIF2 = ldexp(1.0, -2 * F);
+  auto quant = [&](float4 x) {
+    return make_float4(rintf(x.x * sFf), rintf(x.y * sFf), rintf(x.z * sFf),
+                       rintf(x.w * sFf));
+  };
+  for (int32_t q = threadIdx.x; q < nr * Q; q += blockDim.x)
+    sE[q] = quant(gE[(int64_t)lo * Q + q]);
+  __syncthreads();
+  const bool small = (int64_t)1 < smin;
+  const int lg = threadIdx.x & (G - 1);
+  bool chose = false;
+  for (int32_t r0 = 0; r0 < nr; r0 += (int32_t)blockDim.x / G) {
+    const int32_t r = r0 + (int32_t)threadIdx.x / G;
+    const int32_t v = lo + r;
+    const bool in = r < nr;
+    const int32_t span = in ? row_span<true>(a, v) : 0;
+    const bool live = in && span <= kLongRow;
+    if (in && !live && lg == 0) {  // listed with its chunks
+      const int32_t nch = (span + kLongChunk - 1) / kLongChunk;
+      const int32_t slot = atomicAdd(&ctl->n_long, 1);
+      const int32_t base = atomicAdd(&ctl->n_lchunk, nch);
+      if (slot < nn && base + nch <= lw.cap) {
+        lw.rows[slot] = v;
+        lw.base[slot] = base;
+        lw.nch[slot] = nch;
+        for (int32_t c = 0; c < nch; ++c) lw.item[base + c] = slot;
+      } else {
+        raise_err(ctl, kErrInternal);
+      }
+    }
+    Best b{0.0, -1, -1};  // mp < 0: not loaded yet
+    int32_t cnt = 0;
+    if (live) {
+      double mv[DT];  // the a's of v's row
+#pragma unroll
+      for (int q = 0; q < Q; ++q) {
+        const float4 x = sE[r * Q + q];
+        mv[4 * q + 0] = (double)x.x;
+        mv[4 * q + 1] = (double)x.y;
+        mv[4 * q + 2] = (double)x.z;
+        mv[4 * q + 3] = (double)x.w;
+      }
+      for_row<true>(a, v, lg, G, [&](int32_t u, int32_t w) {
+        ++cnt;
+        if ((uint32_t)u >= (uint32_t)nn) {
+          raise_err(ctl, kErrInternal);
+          return;
+        }
+        float4 x[Q];
+        const uint32_t ru = (uint32_t)(u - lo);
+        if (ru < (uint32_t)nr) {
+#pragma unroll
+          for (int q = 0; q < Q; ++q) x[q] = sE[ru * Q + q];
+        } else {
+#pragma unroll
+          for (int q = 0; q < Q; ++q) x[q] = quant(gE[(int64_t)u * Q + q]);
+        }
+        // edge_gain_t's operations in its order, with |P| = |Q| = 1
+        const double dsv = 1.0, dsu = 1.0;
+        const double num = dsv * dsu;
+        const double den = dsv + dsu;
+        const double f = num / den;
+        double ss = 0.0;
+#pragma unroll
+        for (int q = 0; q < Q; ++q) {
+          const float e4[4] = {x[q].x, x[q].y, x[q].z, x[q].w};
+#pragma unroll
+          for (int c = 0; c < 4; ++c) {
+            const double diff = mv[4 * q + c] - (double)e4[c];
+            const double sq = diff * diff;
+            ss = ss + sq;
+          }
+        }
+        ss = ss * sIF2;  // exact: a power of two
+        const double cut = lambda * (double)w;
+        const double fit = f * ss;
+        const double g = cut - fit;
+        if (g > 0.0 || small) {
+          if (b.u < 0 || g > b.g) {
+            b = Best{g, -1, u};
+          } else if (g == b.g) {
+            if (b.mp < 0) b.mp = node_minpt<true>(s, b.u);
+            const int32_t mp = node_minpt<true>(s, u);
+            if (mp < b.mp) b = Best{g, mp, u};
+          }
+        }
+      });
+      if (b.u >= 0 && b.mp < 0) b.mp = node_minpt<true>(s, b.u);
+    }
+    if constexpr (G > 1) {
+#pragma unroll
+      for (int off = G / 2; off > 0; off >>= 1) {
+        Best o;
+        o.g = __shfl_xor(b.g, off, kWave);
+        o.mp = __shfl_xor(b.mp, off, kWave);
+        o.u = __shfl_xor(b.u, off, kWave);
+        if (best_before(o, b)) b = o;
+        cnt += __shfl_xor(cnt, off, kWave);
+      }
+    }
+    if (live && lg == 0) {
+      target[v] = b.u;
+      deg[v] = cnt;
+      chose |= b.u >= 0;
+    }
+  }
+  if (__ballot(chose) && (threadIdx.x & (kWave - 1)) == 0) ctl->any_choice = 1;
+}
+
 // Steps 1-2 over the chunks of the long rows, a wave per chunk.
 template <bool FIRST, int DT>
 __global__ __launch_bounds__(256) void k_select_long(
@@ -3792,9 +3931,18 @@ void launch_round(const Bufs &b, const Adj &adj, int cur, int32_t n,
     hipLaunchKernelGGL(k_round_init, dim3(1), dim3(64), 0, st, ctl);
     prof_begin("select", st);
     constexpr int G = FIRST ? kSelLanesFirst : kSelLanes;
-    hipLaunchKernelGGL((k_select<FIRST, DT, G>), xblocks_for((int64_t)nn * G),
-                       dim3(256), 0, st, nn, adj, s, d, lambda, smin,
-                       b.target, b.deg, lw, (const int32_t *)nullptr, 0, ctl);
+    if constexpr (FIRST && DT > 0) {
+      constexpr int32_t R = kSelFirstBytes / (4 * DT);
+      hipLaunchKernelGGL((k_select_first<DT, G>),
+                         dim3(xcd_grid(((int64_t)nn + R - 1) / R)), dim3(256),
+                         0, st, nn, adj, s, lambda, smin, b.target, b.deg, lw,
+                         ctl);
+    } else {
+      hipLaunchKernelGGL((k_select<FIRST, DT, G>),
+                         xblocks_for((int64_t)nn * G), dim3(256), 0, st, nn,
+                         adj, s, d, lambda, smin, b.target, b.deg, lw,
+                         (const int32_t *)nullptr, 0, ctl);
+    }
     hipLaunchKernelGGL((k_select_long<FIRST, DT>), long_grid, dim3(256), 0,
                        st, nn, adj, s, d, lambda, smin, lw, ctl);
     hipLaunchKernelGGL(k_select_combine, dim3(64), dim3(256), 0, st, lw,
