@@ -190,88 +190,12 @@ __global__ __launch_bounds__(256) void k_rev_count(const int32_t *nbr,
   if ((threadIdx.x & (kWave - 1)) == 0 && fwd) stripe_add(ctl->e_fwd_s, fwd);
 }
 
-// The same count when the table came from this library's kNN: u lists i
-// exactly when i's key as seen from u, (d2 bits, original index) with d2 in
-// the kNN's own operation order, does not exceed u's k-th key.  That needs
-// u's point and k-th key (24 bytes) instead of u's whole row.
-__global__ __launch_bounds__(256) void k_rev_count_kth(
-    const int32_t *nbr, int32_t n, int32_t k, const float4 *__restrict__ pts,
-    const uint64_t *__restrict__ kth, int32_t *rev, uint64_t *nmask,
-    Ctl *ctl) {
-  // Row chunks of four entries taken at once: the row, then every
-  // neighbour's point and k-th key, are loaded before any is used (empty
-  // entries load the point itself), so a row of up to 12 entries costs two
-  // memory round trips.
-  constexpr int kCh = 3;
-  const int32_t i = xcd_tid();
-  const int32_t kp = pad4(k);
-  int32_t fwd = 0;
-  if (i < n) {
-    const int4 *r4 = reinterpret_cast<const int4 *>(nbr + (int64_t)i * kp);
-    const float4 pi = pts[i];
-    const int32_t nch = kp / 4;
-    uint64_t mask = 0;
-    for (int32_t c0 = 0; c0 < nch; c0 += kCh) {
-      int32_t u[4 * kCh];
-#pragma unroll
-      for (int j = 0; j < kCh; ++j) {
-        const int4 c = r4[min(c0 + j, nch - 1)];
-        const bool in = c0 + j < nch;
-        u[4 * j + 0] = in ? c.x : -1;
-        u[4 * j + 1] = in ? c.y : -1;
-        u[4 * j + 2] = in ? c.z : -1;
-        u[4 * j + 3] = in ? c.w : -1;
-      }
-      float4 pu[4 * kCh];
-      uint64_t ku[4 * kCh];
-#pragma unroll
-      for (int t = 0; t < 4 * kCh; ++t) {
-        const int32_t uc = u[t] >= 0 ? u[t] : i;
-        pu[t] = pts[uc];
-        ku[t] = kth[uc];
-      }
-#pragma unroll
-      for (int t = 0; t < 4 * kCh; ++t) {
-        const int32_t slot = 4 * c0 + t;  // entries past k hold -1
-        if (u[t] < 0) continue;
-        ++fwd;
-        const float dx = pi.x - pu[t].x, dy = pi.y - pu[t].y,
-                    dz = pi.z - pu[t].z;
-        const float d2 = fmaf(dz, dz, fmaf(dy, dy, dx * dx));
-        const uint64_t key = ((uint64_t)__float_as_uint(d2) << 32) |
-                             (uint32_t)__float_as_int(pi.w);
-        if (key > ku[t]) mask |= 1ull << slot;
-      }
-    }
-    nmask[i] = mask;
-    // u gets i as a reverse entry: four neighbours reloaded at a time
-    const int32_t *r = nbr + (int64_t)i * kp;
-    for (uint64_t m = mask; m;) {
-      int32_t uu[4];
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        uu[q] = -1;
-        if (m) {
-          uu[q] = r[__builtin_ctzll(m)];
-          m &= m - 1;
-        }
-      }
-#pragma unroll
-      for (int q = 0; q < 4; ++q)
-        if (uu[q] >= 0) atomicAdd(&rev[uu[q]], 1);
-    }
-  }
-  fwd = wave_sum(fwd);
-  if ((threadIdx.x & (kWave - 1)) == 0 && fwd) stripe_add(ctl->e_fwd_s, fwd);
-}
-
 __global__ __launch_bounds__(256) void k_rev_fill(const int32_t *nbr,
                                                   int32_t n, int32_t k,
                                                   const uint64_t *nmask,
                                                   const int32_t *rrp,
                                                   int32_t *cursor,
-                                                  int32_t *rcol,
-                                                  int32_t *rown, Ctl *ctl) {
+                                                  int32_t *rcol, Ctl *ctl) {
   const int32_t i = xcd_tid();
   if (i >= n) return;
   const int32_t *r = nbr + (int64_t)i * pad4(k);
@@ -304,9 +228,167 @@ __global__ __launch_bounds__(256) void k_rev_fill(const int32_t *nbr,
       const int32_t p = lo[q] + pos[q];
       if (p < hi[q]) {
         rcol[p] = i;
-        rown[p] = u[q];
       } else {
         raise_err(ctl, kErrInternal);
+      }
+    }
+  }
+}
+
+// The reverse count and fill of a kNN graph from this library, a block per
+// kRevR consecutive points.  Internal order is Morton order, so most
+// neighbours of a point lie in its own block (89 % of the driving tile's
+// kNN entries for blocks of 1024): their points and k-th keys are read from
+// LDS, and the reverse entries they receive are counted with LDS atomics,
+// one global add per point at the end.  In the fill, the entries from
+// inside the block take the top of u's list (LDS cursors, counting down
+// from rrp[u+1]) and those from other blocks the bottom (global cursors
+// from rrp[u]); both kernels split the entries the same way, so the two
+// parts fill the list exactly.  u lists i exactly when i's key as seen from
+// u, (d2 bits, original index) with d2 in the kNN's own operation order,
+// does not exceed u's k-th key: the test needs u's point and k-th key
+// instead of u's whole row.  Same lists as k_rev_count and k_rev_fill, up
+// to the order inside a list.
+constexpr int kRevR = 1024;
+__global__ __launch_bounds__(256) void k_rev_count_blk(
+    const int32_t *nbr, int32_t n, int32_t k, const float4 *__restrict__ pts,
+    const uint64_t *__restrict__ kth, int32_t *rev, uint64_t *nmask,
+    Ctl *ctl) {
+  __shared__ float4 sp[kRevR];
+  __shared__ uint64_t sk[kRevR];
+  __shared__ int32_t sc[kRevR];
+  const int32_t lo = xcd_block() * kRevR;
+  if (lo >= n) return;  // the whole block
+  const int32_t nr = min(kRevR, n - lo);
+  for (int32_t q = threadIdx.x; q < nr; q += blockDim.x) {
+    sp[q] = pts[lo + q];
+    sk[q] = kth[lo + q];
+    sc[q] = 0;
+  }
+  __syncthreads();
+  constexpr int kCh = 3;  // row chunks of four entries taken at once
+  const int32_t kp = pad4(k);
+  const int32_t nch = kp / 4;
+  int32_t fwd = 0;
+  for (int32_t r = threadIdx.x; r < nr; r += blockDim.x) {
+    const int32_t i = lo + r;
+    const int4 *r4 = reinterpret_cast<const int4 *>(nbr + (int64_t)i * kp);
+    const float4 pi = sp[r];
+    uint64_t mask = 0;
+    for (int32_t c0 = 0; c0 < nch; c0 += kCh) {
+      int32_t u[4 * kCh];
+#pragma unroll
+      for (int j = 0; j < kCh; ++j) {
+        const int4 c = r4[min(c0 + j, nch - 1)];
+        const bool in = c0 + j < nch;
+        u[4 * j + 0] = in ? c.x : -1;
+        u[4 * j + 1] = in ? c.y : -1;
+        u[4 * j + 2] = in ? c.z : -1;
+        u[4 * j + 3] = in ? c.w : -1;
+      }
+      float4 pu[4 * kCh];
+      uint64_t ku[4 * kCh];
+#pragma unroll
+      for (int t = 0; t < 4 * kCh; ++t) {
+        // empty entries read the point itself; entries out of range are
+        // caught by the sanitizer or the kNN, never reach here
+        const int32_t uc = (uint32_t)u[t] < (uint32_t)n ? u[t] : i;
+        const uint32_t ru = (uint32_t)(uc - lo);
+        if (ru < (uint32_t)nr) {
+          pu[t] = sp[ru];
+          ku[t] = sk[ru];
+        } else {
+          pu[t] = pts[uc];
+          ku[t] = kth[uc];
+        }
+      }
+#pragma unroll
+      for (int t = 0; t < 4 * kCh; ++t) {
+        const int32_t slot = 4 * c0 + t;  // entries past k hold -1
+        if (u[t] < 0) continue;
+        ++fwd;
+        const float dx = pi.x - pu[t].x, dy = pi.y - pu[t].y,
+                    dz = pi.z - pu[t].z;
+        const float d2 = fmaf(dz, dz, fmaf(dy, dy, dx * dx));
+        const uint64_t key = ((uint64_t)__float_as_uint(d2) << 32) |
+                             (uint32_t)__float_as_int(pi.w);
+        if (key > ku[t]) mask |= 1ull << slot;
+      }
+    }
+    nmask[i] = mask;
+    const int32_t *row = nbr + (int64_t)i * kp;
+    for (uint64_t m = mask; m; m &= m - 1) {
+      const int32_t u = row[__builtin_ctzll(m)];
+      const uint32_t ru = (uint32_t)(u - lo);
+      if (ru < (uint32_t)nr)
+        atomicAdd(&sc[ru], 1);
+      else if ((uint32_t)u < (uint32_t)n)
+        atomicAdd(&rev[u], 1);
+      else
+        raise_err(ctl, kErrInternal);
+    }
+  }
+  __syncthreads();
+  for (int32_t q = threadIdx.x; q < nr; q += blockDim.x)
+    if (sc[q]) atomicAdd(&rev[lo + q], sc[q]);
+  fwd = wave_sum(fwd);
+  if ((threadIdx.x & (kWave - 1)) == 0 && fwd) stripe_add(ctl->e_fwd_s, fwd);
+}
+
+__global__ __launch_bounds__(256) void k_rev_fill_blk(
+    const int32_t *nbr, int32_t n, int32_t k, const uint64_t *nmask,
+    const int32_t *rrp, int32_t *cursor, int32_t *rcol, Ctl *ctl) {
+  __shared__ int32_t srp[kRevR + 1];
+  __shared__ int32_t sc[kRevR];
+  const int32_t lo = xcd_block() * kRevR;
+  if (lo >= n) return;  // the whole block
+  const int32_t nr = min(kRevR, n - lo);
+  for (int32_t q = threadIdx.x; q <= nr; q += blockDim.x) {
+    srp[q] = rrp[lo + q];
+    if (q < nr) sc[q] = 0;
+  }
+  __syncthreads();
+  const int32_t kp = pad4(k);
+  for (int32_t r = threadIdx.x; r < nr; r += blockDim.x) {
+    const int32_t i = lo + r;
+    const int32_t *row = nbr + (int64_t)i * kp;
+    // four entries at a time: their positions (atomics that return one)
+    // and list bounds are issued before any is used
+    constexpr int kQ = 4;
+    for (uint64_t m = nmask[i]; m;) {
+      int32_t u[kQ], p[kQ], lim[kQ];
+#pragma unroll
+      for (int q = 0; q < kQ; ++q) {
+        u[q] = -1;
+        if (m) {
+          u[q] = row[__builtin_ctzll(m)];
+          m &= m - 1;
+        }
+      }
+#pragma unroll
+      for (int q = 0; q < kQ; ++q) {
+        p[q] = -1;
+        lim[q] = 0;
+        const uint32_t ru = (uint32_t)(u[q] - lo);
+        if (u[q] < 0 || (uint32_t)u[q] >= (uint32_t)n) {
+          u[q] = -1;
+        } else if (ru < (uint32_t)nr) {  // top of the list, counting down
+          p[q] = srp[ru + 1] - 1 - atomicAdd(&sc[ru], 1);
+          lim[q] = srp[ru];
+        } else {  // bottom of the list
+          p[q] = rrp[u[q]] + atomicAdd(&cursor[u[q]], 1);
+          lim[q] = rrp[u[q] + 1];
+        }
+      }
+#pragma unroll
+      for (int q = 0; q < kQ; ++q) {
+        if (u[q] < 0) continue;
+        const uint32_t ru = (uint32_t)(u[q] - lo);
+        const bool ok = ru < (uint32_t)nr ? p[q] >= lim[q] : p[q] < lim[q];
+        if (ok)
+          rcol[p[q]] = i;
+        else
+          raise_err(ctl, kErrInternal);
       }
     }
   }
@@ -331,7 +413,7 @@ struct Adj {
   // first round
   const int32_t *nbr;  // n rows of stride kp, -1 = no entry
   int32_t k, kp;
-  const int32_t *rrp, *rcol, *rown;  // reverse list and the row it is in
+  const int32_t *rrp, *rcol;  // reverse lists
   int32_t n_rev;
   // later rounds
   const int32_t *ws, *wl;
@@ -3746,7 +3828,7 @@ __global__ __launch_bounds__(256) void k_compose_rep(
 struct Bufs {
   float *emb_int;
   int32_t *nbr_clean;                   // sanitised caller table
-  int32_t *rrp, *rcol, *rown, *rev, *cursor;  // first-round reverse list
+  int32_t *rrp, *rcol, *rev, *cursor;  // first-round reverse lists
   uint64_t *nmask;                      // non-mutual entries of each row
   int32_t *ws[2], *wl[2];               // row windows (= toff, cap)
   uint64_t *tbl[2];
@@ -3797,7 +3879,6 @@ void carve(Arena &a, int32_t n, int32_t d, int32_t k, bool link, Bufs *b) {
   b->nbr_clean = a.take<int32_t>((size_t)n * pad4(k));
   b->rrp = a.take<int32_t>(n1);
   b->rcol = a.take<int32_t>((size_t)n * k);
-  b->rown = a.take<int32_t>((size_t)n * k);
   b->rev = a.take<int32_t>(n1);
   b->cursor = a.take<int32_t>(n1);
   b->nmask = a.take<uint64_t>(n1);
@@ -4576,16 +4657,22 @@ int ladder_run(const LadderArgs &g, Ctl *ctl, Arena &a, hipStream_t st) {
                      (int64_t)n, 0);
   hipLaunchKernelGGL(k_fill_i32, blocks_for(n), dim3(256), 0, st, b.cursor,
                      (int64_t)n, 0);
-  if (g.kth && g.pts)
-    hipLaunchKernelGGL(k_rev_count_kth, xblocks_for(n), dim3(256), 0, st, nbr,
-                       n, k, g.pts, g.kth, b.rev, b.nmask, ctl);
+  const bool blk = g.kth && g.pts;  // block-local count and fill
+  const dim3 rev_grid(xcd_grid(((int64_t)n + kRevR - 1) / kRevR));
+  if (blk)
+    hipLaunchKernelGGL(k_rev_count_blk, rev_grid, dim3(256), 0, st, nbr, n, k,
+                       g.pts, g.kth, b.rev, b.nmask, ctl);
   else
     hipLaunchKernelGGL(k_rev_count, xblocks_for(n), dim3(256), 0, st, nbr, n,
                        k, b.rev, b.nmask, ctl);
   device_scan(ScanArray{b.rev, b.rrp, n, nullptr}, n + 1, b.bsum, &ctl->e_rev,
               st);
-  hipLaunchKernelGGL(k_rev_fill, xblocks_for(n), dim3(256), 0, st, nbr, n, k,
-                     b.nmask, b.rrp, b.cursor, b.rcol, b.rown, ctl);
+  if (blk)
+    hipLaunchKernelGGL(k_rev_fill_blk, rev_grid, dim3(256), 0, st, nbr, n, k,
+                       b.nmask, b.rrp, b.cursor, b.rcol, ctl);
+  else
+    hipLaunchKernelGGL(k_rev_fill, xblocks_for(n), dim3(256), 0, st, nbr, n, k,
+                       b.nmask, b.rrp, b.cursor, b.rcol, ctl);
   prof_end(st);
   if ((rc = read_ctl(ctl, h, st))) return rc;
   if (h->err) return status_from_err(h->err);
@@ -4604,7 +4691,6 @@ int ladder_run(const LadderArgs &g, Ctl *ctl, Arena &a, hipStream_t st) {
   adj.kp = pad4(k);
   adj.rrp = b.rrp;
   adj.rcol = b.rcol;
-  adj.rown = b.rown;
   adj.n_rev = h->e_rev;
   adj.ws = nullptr;
   adj.wl = nullptr;
