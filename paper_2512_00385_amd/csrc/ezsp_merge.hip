@@ -767,8 +767,12 @@ __global__ __launch_bounds__(256) void k_select(
 // times 2^-2F is, bit for bit, the sum over the mu's: the conversion is
 // done once per staged row, and a gain costs four operations a dimension.
 constexpr int kSelFirstBytes = 32768;
+// 512 threads take a block's nodes in two passes: measured faster than
+// four passes (256 threads), one (1024 threads, fewer blocks resident), and
+// blocks of 256 or 1024 nodes
+constexpr int kSelFirstNT = 512;
 template <int DT, int G>
-__global__ __launch_bounds__(256) void k_select_first(
+__global__ __launch_bounds__(kSelFirstNT) void k_select_first(
     int32_t nn, Adj a, NodeIn s, double lambda, int64_t smin,
     int32_t *__restrict__ target, int32_t *__restrict__ deg, LongWork lw,
     Ctl *ctl) {
@@ -4015,7 +4019,8 @@ void launch_round(const Bufs &b, const Adj &adj, int cur, int32_t n,
     if constexpr (FIRST && DT > 0) {
       constexpr int32_t R = kSelFirstBytes / (4 * DT);
       hipLaunchKernelGGL((k_select_first<DT, G>),
-                         dim3(xcd_grid(((int64_t)nn + R - 1) / R)), dim3(256),
+                         dim3(xcd_grid(((int64_t)nn + R - 1) / R)),
+                         dim3(kSelFirstNT),
                          0, st, nn, adj, s, lambda, smin, b.target, b.deg, lw,
                          ctl);
     } else {
