@@ -237,8 +237,8 @@ __global__ __launch_bounds__(256) void k_rev_fill(const int32_t *nbr,
 
 // The reverse count and fill of a kNN graph from this library, a block per
 // kRevR consecutive points.  Internal order is Morton order, so most
-// neighbours of a point lie in its own block (89 % of the driving tile's
-// kNN entries for blocks of 1024): their points and k-th keys are read from
+// neighbours of a point lie in its own block (86 % of the driving tile's
+// kNN entries for blocks of 512): their points and k-th keys are read from
 // LDS, and the reverse entries they receive are counted with LDS atomics,
 // one global add per point at the end.  In the fill, the entries from
 // inside the block take the top of u's list (LDS cursors, counting down
@@ -249,8 +249,10 @@ __global__ __launch_bounds__(256) void k_rev_fill(const int32_t *nbr,
 // does not exceed u's k-th key: the test needs u's point and k-th key
 // instead of u's whole row.  Same lists as k_rev_count and k_rev_fill, up
 // to the order inside a list.
-constexpr int kRevR = 1024;
-__global__ __launch_bounds__(256) void k_rev_count_blk(
+constexpr int kRevR = 512;
+constexpr int kRevNT = 256;  // threads per block: two passes over its points
+                             // (faster than four, or one of 1024 threads)
+__global__ __launch_bounds__(kRevNT) void k_rev_count_blk(
     const int32_t *nbr, int32_t n, int32_t k, const float4 *__restrict__ pts,
     const uint64_t *__restrict__ kth, int32_t *rev, uint64_t *nmask,
     Ctl *ctl) {
@@ -335,7 +337,7 @@ __global__ __launch_bounds__(256) void k_rev_count_blk(
   if ((threadIdx.x & (kWave - 1)) == 0 && fwd) stripe_add(ctl->e_fwd_s, fwd);
 }
 
-__global__ __launch_bounds__(256) void k_rev_fill_blk(
+__global__ __launch_bounds__(kRevNT) void k_rev_fill_blk(
     const int32_t *nbr, int32_t n, int32_t k, const uint64_t *nmask,
     const int32_t *rrp, int32_t *cursor, int32_t *rcol, Ctl *ctl) {
   __shared__ int32_t srp[kRevR + 1];
@@ -1011,24 +1013,43 @@ __global__ __launch_bounds__(256) void k_hook(int32_t nn, const int32_t *target,
 // reached and marks the round unfinished (any_choice = -1), so that the
 // round's later kernels wait; the host then completes the forest with
 // pointer-doubling passes (k_double) and launches them again.
+// A block stages the parents of its kJumpR consecutive nodes in LDS: a
+// node's choice is a neighbour, mostly in the same block of Morton order,
+// so most steps read LDS, and only a step out of the block reads global
+// memory.  The staged values and the block's own updates are ancestors
+// too, and a root's entry is itself in both copies.
+constexpr int kJumpR = 512;  // (two passes: faster than blocks of 1024)
 __global__ __launch_bounds__(256) void k_jump(int32_t nn, int32_t *parent,
                                               Ctl *ctl) {
-  const int32_t v = blockIdx.x * blockDim.x + threadIdx.x;
-  if (v >= nn) return;
-  int32_t p = parent[v];
-  int it = 0;
-  for (; it < kJumpWalk; ++it) {
-    if ((uint32_t)p >= (uint32_t)nn) {
-      raise_err(ctl, kErrInternal);
-      p = v;
-      break;
+  __shared__ int32_t sp[kJumpR];
+  const int32_t lo = xcd_block() * kJumpR;
+  if (lo >= nn) return;  // the whole block
+  const int32_t nr = min(kJumpR, nn - lo);
+  for (int32_t q = threadIdx.x; q < nr; q += blockDim.x) sp[q] = parent[lo + q];
+  __syncthreads();
+  bool deep = false;
+  for (int32_t r = threadIdx.x; r < nr; r += blockDim.x) {
+    const int32_t v = lo + r;
+    int32_t p = sp[r];
+    int it = 0;
+    for (; it < kJumpWalk; ++it) {
+      if ((uint32_t)p >= (uint32_t)nn) {
+        raise_err(ctl, kErrInternal);
+        p = v;
+        break;
+      }
+      const uint32_t rp = (uint32_t)(p - lo);
+      const int32_t pp = rp < (uint32_t)nr
+                             ? __atomic_load_n(&sp[rp], __ATOMIC_RELAXED)
+                             : __atomic_load_n(&parent[p], __ATOMIC_RELAXED);
+      if (pp == p) break;
+      p = pp;
     }
-    const int32_t pp = __atomic_load_n(&parent[p], __ATOMIC_RELAXED);
-    if (pp == p) break;
-    p = pp;
+    __atomic_store_n(&sp[r], p, __ATOMIC_RELAXED);
+    __atomic_store_n(&parent[v], p, __ATOMIC_RELAXED);
+    deep |= it == kJumpWalk;
   }
-  __atomic_store_n(&parent[v], p, __ATOMIC_RELAXED);
-  if (it == kJumpWalk) __atomic_store_n(&ctl->any_choice, -1, __ATOMIC_RELAXED);
+  if (deep) __atomic_store_n(&ctl->any_choice, -1, __ATOMIC_RELAXED);
 }
 
 // One pointer-doubling pass: parent[v] = parent[parent[v]].  Values read
@@ -4039,7 +4060,9 @@ void launch_round(const Bufs &b, const Adj &adj, int cur, int32_t n,
   if (!rest_only) {
     hipLaunchKernelGGL(k_hook, blocks_for(nn), dim3(256), 0, st, nn,
                        b.target, b.parent, ctl);
-    hipLaunchKernelGGL(k_jump, blocks_for(nn), dim3(256), 0, st, nn,
+    hipLaunchKernelGGL(k_jump,
+                       dim3(xcd_grid(((int64_t)nn + kJumpR - 1) / kJumpR)),
+                       dim3(256), 0, st, nn,
                        b.parent, ctl);
   }
   device_scan(ScanRoots{b.parent, b.newid, b.cnt, nn}, nn, b.bsum,
@@ -4665,7 +4688,7 @@ int ladder_run(const LadderArgs &g, Ctl *ctl, Arena &a, hipStream_t st) {
   const bool blk = g.kth && g.pts;  // block-local count and fill
   const dim3 rev_grid(xcd_grid(((int64_t)n + kRevR - 1) / kRevR));
   if (blk)
-    hipLaunchKernelGGL(k_rev_count_blk, rev_grid, dim3(256), 0, st, nbr, n, k,
+    hipLaunchKernelGGL(k_rev_count_blk, rev_grid, dim3(kRevNT), 0, st, nbr, n, k,
                        g.pts, g.kth, b.rev, b.nmask, ctl);
   else
     hipLaunchKernelGGL(k_rev_count, xblocks_for(n), dim3(256), 0, st, nbr, n,
@@ -4673,7 +4696,7 @@ int ladder_run(const LadderArgs &g, Ctl *ctl, Arena &a, hipStream_t st) {
   device_scan(ScanArray{b.rev, b.rrp, n, nullptr}, n + 1, b.bsum, &ctl->e_rev,
               st);
   if (blk)
-    hipLaunchKernelGGL(k_rev_fill_blk, rev_grid, dim3(256), 0, st, nbr, n, k,
+    hipLaunchKernelGGL(k_rev_fill_blk, rev_grid, dim3(kRevNT), 0, st, nbr, n, k,
                        b.nmask, b.rrp, b.cursor, b.rcol, ctl);
   else
     hipLaunchKernelGGL(k_rev_fill, xblocks_for(n), dim3(256), 0, st, nbr, n, k,
