@@ -296,13 +296,14 @@ __global__ __launch_bounds__(kRevNT) void k_rev_count_blk(
         // caught by the sanitizer or the kNN, never reach here
         const int32_t uc = (uint32_t)u[t] < (uint32_t)n ? u[t] : i;
         const uint32_t ru = (uint32_t)(uc - lo);
-        if (ru < (uint32_t)nr) {
-          pu[t] = sp[ru];
-          ku[t] = sk[ru];
-        } else {
-          pu[t] = pts[uc];
-          ku[t] = kth[uc];
-        }
+        // one generic pointer for LDS and global memory: a flat load each,
+        // with no branch (two branches writing the same registers make the
+        // LDS one wait for every global load in flight)
+        const bool inb = ru < (uint32_t)nr;
+        const float4 *ps = inb ? &sp[ru] : &pts[uc];
+        const uint64_t *ks = inb ? &sk[ru] : &kth[uc];
+        pu[t] = *ps;
+        ku[t] = *ks;
       }
 #pragma unroll
       for (int t = 0; t < 4 * kCh; ++t) {
@@ -367,26 +368,32 @@ __global__ __launch_bounds__(kRevNT) void k_rev_fill_blk(
           m &= m - 1;
         }
       }
+      // each entry's position and list bounds through one generic pointer
+      // (flat atomics and loads, no branch): the top of the list from the
+      // LDS cursors, counting down, or the bottom from the global ones
+      int32_t pos[kQ], b0[kQ], b1[kQ];
+      bool inb[kQ];
 #pragma unroll
       for (int q = 0; q < kQ; ++q) {
-        p[q] = -1;
-        lim[q] = 0;
-        const uint32_t ru = (uint32_t)(u[q] - lo);
-        if (u[q] < 0 || (uint32_t)u[q] >= (uint32_t)n) {
-          u[q] = -1;
-        } else if (ru < (uint32_t)nr) {  // top of the list, counting down
-          p[q] = srp[ru + 1] - 1 - atomicAdd(&sc[ru], 1);
-          lim[q] = srp[ru];
-        } else {  // bottom of the list
-          p[q] = rrp[u[q]] + atomicAdd(&cursor[u[q]], 1);
-          lim[q] = rrp[u[q] + 1];
-        }
+        if ((uint32_t)u[q] >= (uint32_t)n) u[q] = -1;
+        const int32_t uq = u[q] < 0 ? lo : u[q];
+        const uint32_t ru = (uint32_t)(uq - lo);
+        inb[q] = ru < (uint32_t)nr;
+        int32_t *cur = inb[q] ? &sc[ru] : &cursor[uq];
+        const int32_t *bnd = inb[q] ? &srp[ru] : &rrp[uq];
+        pos[q] = u[q] >= 0 ? atomicAdd(cur, 1) : 0;
+        b0[q] = bnd[0];
+        b1[q] = bnd[1];
+      }
+#pragma unroll
+      for (int q = 0; q < kQ; ++q) {
+        p[q] = inb[q] ? b1[q] - 1 - pos[q] : b0[q] + pos[q];
+        lim[q] = inb[q] ? b0[q] : b1[q];
       }
 #pragma unroll
       for (int q = 0; q < kQ; ++q) {
         if (u[q] < 0) continue;
-        const uint32_t ru = (uint32_t)(u[q] - lo);
-        const bool ok = ru < (uint32_t)nr ? p[q] >= lim[q] : p[q] < lim[q];
+        const bool ok = inb[q] ? p[q] >= lim[q] : p[q] < lim[q];
         if (ok)
           rcol[p[q]] = i;
         else
