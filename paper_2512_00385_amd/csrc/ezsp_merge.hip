@@ -695,7 +695,7 @@ __global__ __launch_bounds__(256) void k_select(
       raise_err(ctl, kErrInternal);
     }
   }
-  Best b{0.0, 0, -1};
+  Best b{0.0, -1, -1};  // mp < 0: not loaded yet
   int32_t cnt = 0;
   bool skip = false;
   if constexpr (!FIRST) {
@@ -736,11 +736,19 @@ __global__ __launch_bounds__(256) void k_select(
       }
       const double g =
           edge_gain_t<FIRST, DT>(s, mv, v, dsv, u, w, d, lambda, sF, sIF);
+      // the smallest point only breaks a tie of equal gains: loaded for a
+      // tie and for the lane's final choice, not for every candidate
       if (g > 0.0 || small) {
-        const Best c{g, node_minpt<FIRST>(s, u), u};
-        if (best_before(c, b)) b = c;
+        if (b.u < 0 || g > b.g) {
+          b = Best{g, -1, u};
+        } else if (g == b.g) {
+          if (b.mp < 0) b.mp = node_minpt<FIRST>(s, b.u);
+          const int32_t mp = node_minpt<FIRST>(s, u);
+          if (mp < b.mp) b = Best{g, mp, u};
+        }
       }
     });
+    if (b.u >= 0 && b.mp < 0) b.mp = node_minpt<FIRST>(s, b.u);
   }
   if constexpr (G > 1) {
 #pragma unroll
