@@ -975,24 +975,40 @@ __global__ __launch_bounds__(256) void k_select_long(
 }
 
 // The long rows' choices from their chunks (same order as best_before).
+// A wave per long row: the lanes take every 64th chunk, then the wave
+// reduces (a giant component's row has hundreds of chunks).
 __global__ __launch_bounds__(256) void k_select_combine(
     LongWork lw, int32_t *__restrict__ target, int32_t *__restrict__ deg,
     Ctl *ctl) {
   const int32_t n_long = ctl->n_long;
-  for (int32_t slot = blockIdx.x * blockDim.x + threadIdx.x; slot < n_long;
-       slot += gridDim.x * blockDim.x) {
+  const int lane = threadIdx.x & (kWave - 1);
+  const int32_t wave0 = (int32_t)(blockIdx.x * (blockDim.x / kWave) +
+                                  threadIdx.x / kWave);
+  const int32_t nwaves = (int32_t)(gridDim.x * (blockDim.x / kWave));
+  for (int32_t slot = wave0; slot < n_long; slot += nwaves) {
     const int32_t b0 = lw.base[slot], nch = lw.nch[slot];
     Best b{0.0, 0, -1};
     int32_t cnt = 0;
-    for (int32_t c = b0; c < b0 + nch; ++c) {
+    for (int32_t c = b0 + lane; c < b0 + nch; c += kWave) {
       const Best o{lw.g[c], lw.mp[c], lw.u[c]};
       if (best_before(o, b)) b = o;
       cnt += lw.cnt[c];
     }
-    const int32_t v = lw.rows[slot];
-    target[v] = b.u;
-    deg[v] = cnt;
-    if (b.u >= 0) ctl->any_choice = 1;
+#pragma unroll
+    for (int off = kWave / 2; off > 0; off >>= 1) {
+      Best o;
+      o.g = __shfl_xor(b.g, off, kWave);
+      o.mp = __shfl_xor(b.mp, off, kWave);
+      o.u = __shfl_xor(b.u, off, kWave);
+      if (best_before(o, b)) b = o;
+      cnt += __shfl_xor(cnt, off, kWave);
+    }
+    if (lane == 0) {
+      const int32_t v = lw.rows[slot];
+      target[v] = b.u;
+      deg[v] = cnt;
+      if (b.u >= 0) ctl->any_choice = 1;
+    }
   }
 }
 
@@ -1459,6 +1475,124 @@ __global__ __launch_bounds__(256) void k_stats_s(
     const double q0 = (double)acc[2 * q] / dsz;
     const double q1 = (double)acc[2 * q + 1] / dsz;
     Mo[q] = make_double2(q0 * sIF, q1 * sIF);
+  }
+}
+
+// k_stats_big for D = DT: one pass over the members, each thread summing
+// whole rows (16-byte loads, two members in flight), then a block
+// reduction (exact int64, so the order does not matter).
+template <bool FIRST, int DT>
+__global__ __launch_bounds__(256) void k_stats_big_t(
+    const int32_t *__restrict__ mem, const int32_t *__restrict__ moff,
+    NodeIn s, const int32_t *__restrict__ deg, NodeOut o,
+    const int32_t *__restrict__ big, Ctl *ctl) {
+  static_assert(DT > 0 && DT % 4 == 0, "vector rows");
+  constexpr int kU = 2;
+  constexpr int NW = 256 / kWave;
+  __shared__ long long sS[NW][DT];
+  __shared__ int32_t ssize[NW], smp[NW], scap[NW];
+  if (!round_live(ctl)) return;
+  const double sF = ldexp(1.0, ctl->F), sIF = ldexp(1.0, -ctl->F);
+  const int32_t n_big = ctl->n_big;
+  const int lane = threadIdx.x & (kWave - 1), wv = threadIdx.x / kWave;
+  for (int32_t bi = blockIdx.x; bi < n_big; bi += gridDim.x) {
+    const int32_t c = big[bi];
+    const int32_t m0 = moff[c], m1 = moff[c + 1];
+    int64_t acc[DT];
+#pragma unroll
+    for (int q = 0; q < DT; ++q) acc[q] = 0;
+    int32_t size = 0, mp = INT32_MAX, cap = 0;
+    for (int32_t j0 = m0 + (int32_t)threadIdx.x; j0 < m1; j0 += kU * 256) {
+      int32_t mm[kU];
+#pragma unroll
+      for (int e = 0; e < kU; ++e) mm[e] = mem[min(j0 + e * 256, m1 - 1)];
+      if constexpr (FIRST) {
+        float4 x[kU][DT / 4];
+#pragma unroll
+        for (int e = 0; e < kU; ++e) {
+          const float4 *p =
+              reinterpret_cast<const float4 *>(s.emb + (int64_t)mm[e] * DT);
+#pragma unroll
+          for (int q = 0; q < DT / 4; ++q) x[e][q] = p[q];
+        }
+#pragma unroll
+        for (int e = 0; e < kU; ++e) {
+          if (j0 + e * 256 >= m1) break;
+#pragma unroll
+          for (int q = 0; q < DT / 4; ++q) {
+            acc[4 * q + 0] += (int64_t)rint((double)x[e][q].x * sF);
+            acc[4 * q + 1] += (int64_t)rint((double)x[e][q].y * sF);
+            acc[4 * q + 2] += (int64_t)rint((double)x[e][q].z * sF);
+            acc[4 * q + 3] += (int64_t)rint((double)x[e][q].w * sF);
+          }
+          size += 1;
+          mp = min(mp, node_minpt<true>(s, mm[e]));
+          cap += deg[mm[e]];
+        }
+      } else {
+        longlong2 x[kU][DT / 2];
+#pragma unroll
+        for (int e = 0; e < kU; ++e) {
+          const longlong2 *p =
+              reinterpret_cast<const longlong2 *>(s.S + (int64_t)mm[e] * DT);
+#pragma unroll
+          for (int q = 0; q < DT / 2; ++q) x[e][q] = p[q];
+        }
+#pragma unroll
+        for (int e = 0; e < kU; ++e) {
+          if (j0 + e * 256 >= m1) break;
+#pragma unroll
+          for (int q = 0; q < DT / 2; ++q) {
+            acc[2 * q + 0] += x[e][q].x;
+            acc[2 * q + 1] += x[e][q].y;
+          }
+          size += s.size[mm[e]];
+          mp = min(mp, s.minpt[mm[e]]);
+          cap += deg[mm[e]];
+        }
+      }
+    }
+#pragma unroll
+    for (int off = kWave / 2; off > 0; off >>= 1) {
+#pragma unroll
+      for (int q = 0; q < DT; ++q)
+        acc[q] += (int64_t)__shfl_xor((long long)acc[q], off, kWave);
+      size += __shfl_xor(size, off, kWave);
+      cap += __shfl_xor(cap, off, kWave);
+      mp = min(mp, __shfl_xor(mp, off, kWave));
+    }
+    if (lane == 0) {
+#pragma unroll
+      for (int q = 0; q < DT; ++q) sS[wv][q] = (long long)acc[q];
+      ssize[wv] = size;
+      smp[wv] = mp;
+      scap[wv] = cap;
+    }
+    __syncthreads();
+    int32_t tsize = 0;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) tsize += ssize[w];
+    if (threadIdx.x == 0) {
+      int32_t tmp = INT32_MAX, tcap = 0;
+#pragma unroll
+      for (int w = 0; w < NW; ++w) {
+        tmp = min(tmp, smp[w]);
+        tcap += scap[w];
+      }
+      o.size[c] = tsize;
+      o.minpt[c] = tmp;
+      note_window(o, c, tcap, m1 - m0, ctl);
+    }
+    if (threadIdx.x < DT) {
+      long long v = 0;
+#pragma unroll
+      for (int w = 0; w < NW; ++w) v += sS[w][threadIdx.x];
+      const int64_t t = (int64_t)c * DT + threadIdx.x;
+      o.S[t] = v;
+      const double qv = (double)v / (double)tsize;
+      o.mu[t] = qv * sIF;
+    }
+    __syncthreads();  // the shared sums are reused by the next component
   }
 }
 
@@ -4107,7 +4241,11 @@ void launch_round(const Bufs &b, const Adj &adj, int cur, int32_t n,
     hipLaunchKernelGGL((k_stats<FIRST, DT>), xblocks_for(nn), dim3(256), 0,
                        st, nn, b.mem, b.moff, s, b.deg, d, o, b.big, ctl);
   }
-  hipLaunchKernelGGL(k_stats_big<FIRST>, big_grid, dim3(256), 0, st,
+  if constexpr (DT > 0)
+    hipLaunchKernelGGL((k_stats_big_t<FIRST, DT>), big_grid, dim3(256), 0, st,
+                       b.mem, b.moff, s, b.deg, o, b.big, ctl);
+  else
+    hipLaunchKernelGGL(k_stats_big<FIRST>, big_grid, dim3(256), 0, st,
                      b.mem, b.moff, s, b.deg, d, o, b.big, ctl);
   if (b.link) {  // position sums of the next round's nodes
     hipLaunchKernelGGL(k_link_accum<FIRST>, xblocks_for(nn), dim3(256), 0, st,
