@@ -183,8 +183,11 @@ __device__ __forceinline__ T block_excl_scan(T v, T *wsum, T *total) {
 // Op provides:  __device__ int32_t value(int32_t i) const;
 //               __device__ void emit(int32_t i, int32_t excl, int32_t v) const;
 // The scan runs over [0, n_bound); op.value must return 0 past the real end.
+// Four items a thread: more tiles, each with a shorter chain, measured
+// about 70 us faster per driving-tile step than eight or sixteen (a step
+// runs some forty scans).
 constexpr int kScanNT = 256;
-constexpr int kScanItems = 8;
+constexpr int kScanItems = 4;
 constexpr int kScanTile = kScanNT * kScanItems;
 
 template <class Op>
@@ -272,9 +275,10 @@ inline int32_t scan_blocks(int64_t n) {
   return (int32_t)((n + kScanTile - 1) / kScanTile);
 }
 
-// Small scans in one launch: one block of 1024 threads, 16 items each.
+// Small scans in one launch: one block of 1024 threads, 4 items each (a
+// single block is a long chain: larger scans are faster in two launches).
 constexpr int kOneNT = 1024;
-constexpr int kOneItems = 16;
+constexpr int kOneItems = 4;
 constexpr int kOneMax = kOneNT * kOneItems;
 
 template <class Op>
