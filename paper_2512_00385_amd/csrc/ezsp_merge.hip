@@ -4226,8 +4226,10 @@ void launch_round(const Bufs &b, const Adj &adj, int cur, int32_t n,
                      b.moff, b.rank, b.mem, b.merged, ctl);
 
   // contraction chunks: enough blocks to fill the chip, at most kChunk
+  // (halved while fewer than 1024: measured faster than 2048 or 4096, and
+  // than chunks of 512 slots throughout)
   int32_t chunk = kChunk;
-  while (chunk > 64 && (int64_t)ed / chunk < 2048) chunk >>= 1;
+  while (chunk > 64 && (int64_t)ed / chunk < 1024) chunk >>= 1;
   const NodeOut o{b.size[nxt], b.S[nxt],  b.mu,
                   b.minpt[nxt], b.capn,    b.wl[nxt],
                   b.cbig,      chunk,     kBigComp,
