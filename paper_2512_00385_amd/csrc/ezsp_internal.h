@@ -90,6 +90,12 @@ bool radix_sort_pairs(uint64_t *keys, uint32_t *vals, uint64_t *keys_alt,
                       int32_t *hist, int32_t *bsum, int32_t *total, Ctl *ctl,
                       hipStream_t st);
 size_t radix_hist_ints(int32_t n);
+// Radix sort of 64-bit keys alone on bits [shift0, shift0 + nbits) (stable,
+// so bits below shift0 keep their input order within equal digits).
+// Returns true when the sorted result ended in keys_alt.
+bool radix_sort_keys(uint64_t *keys, uint64_t *keys_alt, int32_t n,
+                     int shift0, int nbits, int32_t *hist, int32_t *bsum,
+                     int32_t *total, Ctl *ctl, hipStream_t st);
 
 // kNN: Morton sort, box tree, exact query.  Produces the internal
 // (Morton-order) neighbour table nbr_int (n rows of pad4(k), -1 padded) and

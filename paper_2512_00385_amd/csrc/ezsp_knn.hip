@@ -126,6 +126,10 @@ __device__ __forceinline__ uint64_t spread3(uint32_t v) {
   return x;
 }
 
+// The point's index either goes to vals, or (vals null, n <= 2^kPackBits)
+// into the key's low kPackBits bits below the code, so that a key-only sort
+// of the code bits carries it.
+constexpr int kPackBits = 25;
 __global__ __launch_bounds__(256) void k_morton(const float *xyz, int32_t n,
                                                 const Ctl *ctl, uint64_t *keys,
                                                 uint32_t *vals) {
@@ -145,8 +149,14 @@ __global__ __launch_bounds__(256) void k_morton(const float *xyz, int32_t n,
     t = fminf(fmaxf(t, 0.0f), kMortonMax);  // NaN maps to 0
     q[a] = (uint32_t)t;
   }
-  keys[i] = spread3(q[0]) | (spread3(q[1]) << 1) | (spread3(q[2]) << 2);
-  vals[i] = (uint32_t)i;
+  const uint64_t code =
+      spread3(q[0]) | (spread3(q[1]) << 1) | (spread3(q[2]) << 2);
+  if (vals) {
+    keys[i] = code;
+    vals[i] = (uint32_t)i;
+  } else {
+    keys[i] = (code << kPackBits) | (uint64_t)i;
+  }
 }
 
 // Min and max along each 16-lane DPP row (a bucket of points): after the
@@ -190,9 +200,9 @@ __device__ __forceinline__ void box_join(float4 &lo, float4 &hi,
 // tree's two lowest levels: each bucket's box (16 consecutive points, one
 // DPP row) and the box of every 8 buckets (16 buckets per block).
 __global__ __launch_bounds__(256) void k_gather_points(
-    const float *xyz, int32_t n, const uint32_t *order, float4 *pts,
-    int32_t *perm, int32_t *inv, float4 *blo, float4 *bhi, Tree tree,
-    Ctl *ctl) {
+    const float *xyz, int32_t n, const uint32_t *order,
+    const uint64_t *packed, float4 *pts, int32_t *perm, int32_t *inv,
+    float4 *blo, float4 *bhi, Tree tree, Ctl *ctl) {
   __shared__ float4 s_lo[256 / kBucket], s_hi[256 / kBucket];
   const int32_t i = blockIdx.x * blockDim.x + threadIdx.x;
   // points past the end (the last bucket's missing ones) are infinitely
@@ -202,7 +212,8 @@ __global__ __launch_bounds__(256) void k_gather_points(
                          __int_as_float(kPadIndex));
   bool real = false;
   if (i < n) {
-    const uint32_t o = order[i];
+    const uint32_t o =
+        packed ? (uint32_t)(packed[i] & ((1ull << kPackBits) - 1)) : order[i];
     if (o >= (uint32_t)n) {
       raise_err(ctl, kErrInternal);
     } else {
@@ -672,18 +683,26 @@ static hipError_t knn_impl(const float *xyz, int32_t n, int32_t k, Ctl *ctl,
   const int gb = (n + nt - 1) / nt;
   hipLaunchKernelGGL(k_bbox, dim3(min(gb, 256)), dim3(nt), 0, st, xyz, n,
                      ctl);
+  // the index packed under the code when it fits in 64 bits: the sort then
+  // moves 8 bytes a key instead of 12
+  const bool pack = n <= (1 << kPackBits);
+  static_assert(3 * kMortonBits + kPackBits <= 64, "code and index in a key");
   hipLaunchKernelGGL(k_morton, dim3(gb), dim3(nt), 0, st, xyz, n, ctl, s.keys,
-                     s.vals);
+                     pack ? (uint32_t *)nullptr : s.vals);
   prof_begin("morton_sort", st);
-  const bool alt = radix_sort_pairs(s.keys, s.vals, s.keys2, s.vals2, n,
-                                    3 * kMortonBits,
-                                    s.hist, s.bsum, s.total, ctl, st);
+  const bool alt =
+      pack ? radix_sort_keys(s.keys, s.keys2, n, kPackBits, 3 * kMortonBits,
+                             s.hist, s.bsum, s.total, ctl, st)
+           : radix_sort_pairs(s.keys, s.vals, s.keys2, s.vals2, n,
+                              3 * kMortonBits, s.hist, s.bsum, s.total, ctl,
+                              st);
   prof_end(st);
-  const uint32_t *order = alt ? s.vals2 : s.vals;
+  const uint32_t *order = pack ? nullptr : (alt ? s.vals2 : s.vals);
+  const uint64_t *packed = pack ? (alt ? s.keys2 : s.keys) : nullptr;
   // points in Morton order with the two lowest box levels, then a launch
   // per level while a level is large, the rest in one block
   hipLaunchKernelGGL(k_gather_points, dim3(gb), dim3(nt), 0, st, xyz, n, order,
-                     s.pts, w.perm, w.inv, s.blo, s.bhi, tree, ctl);
+                     packed, s.pts, w.perm, w.inv, s.blo, s.bhi, tree, ctl);
   int l = 2;
   for (; l <= tree.top && tree.cnt[l] > kTopBoxes; ++l)
     hipLaunchKernelGGL(k_up_boxes, dim3((tree.cnt[l] + nt - 1) / nt), dim3(nt),

@@ -72,6 +72,9 @@ __global__ __launch_bounds__(kSortNT) void k_rs_hist(const uint64_t *keys,
 constexpr int kScatNT = 2 * kSortNT;
 constexpr int kScatItems = kSortTile / kScatNT;
 
+// VALS: keys carry 32-bit values; otherwise the keys alone (a value packed
+// into bits the sort does not look at).
+template <bool VALS>
 __global__ __launch_bounds__(kScatNT) void k_rs_scatter(
     const uint64_t *__restrict__ kin, const uint32_t *__restrict__ vin,
     uint64_t *__restrict__ kout, uint32_t *__restrict__ vout, int32_t n,
@@ -101,7 +104,7 @@ __global__ __launch_bounds__(kScatNT) void k_rs_scatter(
   for (int j = 0; j < kScatItems; ++j) {
     const int32_t i = min(base + j * kScatNT + (int32_t)threadIdx.x, n - 1);
     kt[j] = kin[i];
-    vt[j] = vin[i];
+    vt[j] = VALS ? vin[i] : 0u;
   }
   __syncthreads();
 #pragma unroll
@@ -138,7 +141,7 @@ __global__ __launch_bounds__(kScatNT) void k_rs_scatter(
       const int32_t pos = pos0[wid][dig] + rank;
       if ((uint32_t)pos < (uint32_t)n) {
         kout[pos] = key;
-        vout[pos] = val;
+        if (VALS) vout[pos] = val;
       } else {
         raise_err(ctl, kErrInternal);
       }
@@ -164,8 +167,8 @@ bool radix_sort_pairs(uint64_t *keys, uint32_t *vals, uint64_t *keys_alt,
                        shift, hist, nb);
     const int32_t nh = kSortBins * nb;
     device_scan(ScanArray{hist, hist, nh, nullptr}, nh, bsum, total, st);
-    hipLaunchKernelGGL(k_rs_scatter, dim3(nb), dim3(kScatNT), 0, st, kin, vin,
-                       kout, vout, n, shift, hist, nb, ctl);
+    hipLaunchKernelGGL(k_rs_scatter<true>, dim3(nb), dim3(kScatNT), 0, st,
+                       kin, vin, kout, vout, n, shift, hist, nb, ctl);
     uint64_t *tk = kin;
     kin = kout;
     kout = tk;
@@ -264,6 +267,29 @@ __global__ void k_fixshift(Ctl *ctl, int32_t n) {
   const int F = fixshift_rule(__uint_as_float(bits), n);
   ctl->F = F;
   if (F < 16) raise_err(ctl, kErrRange);
+}
+
+bool radix_sort_keys(uint64_t *keys, uint64_t *keys_alt, int32_t n,
+                     int shift0, int nbits, int32_t *hist, int32_t *bsum,
+                     int32_t *total, Ctl *ctl, hipStream_t st) {
+  if (n <= 1) return false;
+  const int32_t nb = sort_blocks(n);
+  uint64_t *kin = keys, *kout = keys_alt;
+  bool flip = false;
+  for (int shift = shift0; shift < shift0 + nbits; shift += 8) {
+    hipLaunchKernelGGL(k_rs_hist, dim3(nb), dim3(kSortNT), 0, st, kin, n,
+                       shift, hist, nb);
+    const int32_t nh = kSortBins * nb;
+    device_scan(ScanArray{hist, hist, nh, nullptr}, nh, bsum, total, st);
+    hipLaunchKernelGGL(k_rs_scatter<false>, dim3(nb), dim3(kScatNT), 0, st,
+                       kin, (const uint32_t *)nullptr, kout, (uint32_t *)nullptr,
+                       n, shift, hist, nb, ctl);
+    uint64_t *tk = kin;
+    kin = kout;
+    kout = tk;
+    flip = !flip;
+  }
+  return flip;
 }
 
 // ---------------------------------------------------------------------------
