@@ -72,6 +72,8 @@ struct Ctl {
   Stripe e_next_s[kStripes];  // device side of e_next
   Stripe e_fwd_s[kStripes];   // device side of e_fwd
   Stripe maxabs_s[kStripes];  // max |e| bits from the fused gather
+  Stripe bbox_s[6][kStripes]; // bbox_enc's min xyz, max xyz per stripe
+                              // (folded into bbox_enc by k_bbox_fold)
   int32_t tail_nc[16];        // superpoints of every level the tail ended
   int64_t tail_cut2[16];      // ... and 2 x their cut weight
   // linking of isolated nodes

@@ -126,6 +126,7 @@ int grid_run(const float *xyz, int32_t n, float h, int32_t *keep,
   prof_begin("grid_subsample", st);
   hipLaunchKernelGGL(k_bbox, dim3((unsigned)(gb < 256 ? gb : 256)), dim3(nt),
                      0, st, xyz, n, ctl);
+  hipLaunchKernelGGL(k_bbox_fold, dim3(1), dim3(64), 0, st, ctl);
   const int64_t cb = (int64_t)((cap + nt - 1) / nt);
   hipLaunchKernelGGL(k_grid_clear, dim3((unsigned)(cb < 4096 ? cb : 4096)),
                      dim3(nt), 0, st, t, (int64_t)cap);

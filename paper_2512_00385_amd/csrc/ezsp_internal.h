@@ -224,6 +224,7 @@ int check_hip(hipError_t e, const char *what);
 Ctl *pinned_ctl();
 __global__ void k_ctl_init(Ctl *ctl);
 __global__ void k_bbox(const float *xyz, int32_t n, Ctl *ctl);
+__global__ void k_bbox_fold(Ctl *ctl);
 __global__ void k_maxabs(const float *v, int64_t count, Ctl *ctl);
 __global__ void k_fixshift(Ctl *ctl, int32_t n);
 

@@ -54,21 +54,34 @@ __global__ __launch_bounds__(256) void k_bbox(const float *xyz, int32_t n,
   if ((reinterpret_cast<uintptr_t>(xyz) & 15) == 0) {
     const float4 *v = reinterpret_cast<const float4 *>(xyz);
     const int32_t groups = n / 4;
-    for (int32_t g = tid; g < groups; g += stride) {
-      const float4 a = v[3 * (int64_t)g], b = v[3 * (int64_t)g + 1],
-                   c = v[3 * (int64_t)g + 2];
-      bbox_take(a.x, 0, mn, mx, bad);
-      bbox_take(a.y, 1, mn, mx, bad);
-      bbox_take(a.z, 2, mn, mx, bad);
-      bbox_take(a.w, 0, mn, mx, bad);
-      bbox_take(b.x, 1, mn, mx, bad);
-      bbox_take(b.y, 2, mn, mx, bad);
-      bbox_take(b.z, 0, mn, mx, bad);
-      bbox_take(b.w, 1, mn, mx, bad);
-      bbox_take(c.x, 2, mn, mx, bad);
-      bbox_take(c.y, 0, mn, mx, bad);
-      bbox_take(c.z, 1, mn, mx, bad);
-      bbox_take(c.w, 2, mn, mx, bad);
+    // four groups a thread in flight per step; indices past the end are
+    // clamped to the last group, whose second reading changes neither a
+    // minimum, a maximum nor the finiteness check
+    constexpr int kG = 4;
+    for (int32_t g0 = tid; g0 < groups; g0 += kG * stride) {
+      float4 a[kG], b[kG], c[kG];
+#pragma unroll
+      for (int e = 0; e < kG; ++e) {
+        const int64_t g = min(g0 + e * stride, groups - 1);
+        a[e] = v[3 * g];
+        b[e] = v[3 * g + 1];
+        c[e] = v[3 * g + 2];
+      }
+#pragma unroll
+      for (int e = 0; e < kG; ++e) {
+        bbox_take(a[e].x, 0, mn, mx, bad);
+        bbox_take(a[e].y, 1, mn, mx, bad);
+        bbox_take(a[e].z, 2, mn, mx, bad);
+        bbox_take(a[e].w, 0, mn, mx, bad);
+        bbox_take(b[e].x, 1, mn, mx, bad);
+        bbox_take(b[e].y, 2, mn, mx, bad);
+        bbox_take(b[e].z, 0, mn, mx, bad);
+        bbox_take(b[e].w, 1, mn, mx, bad);
+        bbox_take(c[e].x, 2, mn, mx, bad);
+        bbox_take(c[e].y, 0, mn, mx, bad);
+        bbox_take(c[e].z, 1, mn, mx, bad);
+        bbox_take(c[e].w, 2, mn, mx, bad);
+      }
     }
     done = groups * 4;
   }
@@ -106,10 +119,28 @@ __global__ __launch_bounds__(256) void k_bbox(const float *xyz, int32_t n,
         lo = fminf(lo, smn[a][q]);
         hi = fmaxf(hi, smx[a][q]);
       }
-      atomicMin(&ctl->bbox_enc[a], f2ord(lo));
-      atomicMax(&ctl->bbox_enc[3 + a], f2ord(hi));
+      // striped: device-scope atomics on one address are serialised at the
+      // memory side (256 blocks x 6 of them took most of this kernel)
+      atomicMin(&ctl->bbox_s[a][blockIdx.x % kStripes].v, f2ord(lo));
+      atomicMax(&ctl->bbox_s[3 + a][blockIdx.x % kStripes].v, f2ord(hi));
     }
     if (sbad) raise_err(ctl, kErrNonFinite);
+  }
+}
+
+// The box from its stripes, one wave: bbox_enc = min / max over them.
+__global__ __launch_bounds__(64) void k_bbox_fold(Ctl *ctl) {
+  const int lane = threadIdx.x;
+#pragma unroll
+  for (int a = 0; a < 6; ++a) {
+    int32_t v = lane < kStripes ? ctl->bbox_s[a][lane].v
+                                : f2ord(a < 3 ? INFINITY : -INFINITY);
+#pragma unroll
+    for (int off = kWave / 2; off > 0; off >>= 1) {
+      const int32_t o = __shfl_xor(v, off, kWave);
+      v = a < 3 ? min(v, o) : max(v, o);
+    }
+    if (lane == 0) ctl->bbox_enc[a] = v;
   }
 }
 
@@ -683,6 +714,7 @@ static hipError_t knn_impl(const float *xyz, int32_t n, int32_t k, Ctl *ctl,
   const int gb = (n + nt - 1) / nt;
   hipLaunchKernelGGL(k_bbox, dim3(min(gb, 256)), dim3(nt), 0, st, xyz, n,
                      ctl);
+  hipLaunchKernelGGL(k_bbox_fold, dim3(1), dim3(64), 0, st, ctl);
   // the index packed under the code when it fits in 64 bits: the sort then
   // moves 8 bytes a key instead of 12
   const bool pack = n <= (1 << kPackBits);

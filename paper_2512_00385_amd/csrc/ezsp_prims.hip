@@ -227,6 +227,9 @@ __global__ void k_ctl_init(Ctl *ctl) {
     stripe_zero(ctl->e_next_s);
     stripe_zero(ctl->e_fwd_s);
     stripe_zero(ctl->maxabs_s);
+    for (int i = threadIdx.x; i < 6 * kStripes; i += blockDim.x)
+      ctl->bbox_s[i / kStripes][i % kStripes].v =
+          f2ord(i < 3 * kStripes ? INFINITY : -INFINITY);
   }
 }
 
